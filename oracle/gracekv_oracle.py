@@ -1,0 +1,695 @@
+"""CPU oracle for GraceKV's one-shot KV-cache compression (segment -> build ->
+score -> select -> pack).
+
+TEST INFRASTRUCTURE ONLY.  This module is a plain, slow, fp64 restatement of
+the method as the paper defines it.  Only the tests, the smoke check and the
+``cpu_baseline`` leg of the benchmark may import it; the product path (the HIP
+library and its Python binding) never does, and it shares no code with it.
+
+Every function cites the passage it follows (section / equation of the paper,
+arXiv 2608.07001).  Quantities are computed from their literal definitions:
+interval sums are explicit sums over the interval's tokens, the budget auction
+is a literal max-priority queue.  Where the paper is silent or ambiguous the
+reading used is named in the docstring (the list of readings is in the design
+notes).  The hot-path settings are the paper's own ablation settings
+lambda_graph = 0 (no multi-hop relevance) and alpha = 0 (no singleton floor).
+
+Where a floating-point score decides a discrete outcome, the decision is taken
+on the score rounded to fp32 (the precision in which the GPU decides), except
+for the segmentation DP, which both sides run in fp64.
+
+Parity unpinned: the absolute values of D, of the gains and of the selected set
+on general inputs have no printed value to check against; they are pinned
+through the invariants and special cases in tests/test_oracle_*.py.
+"""
+from __future__ import annotations
+
+import dataclasses
+import heapq
+import math
+from typing import Dict, List, Optional, Tuple
+
+import numpy as np
+
+F64 = np.float64
+
+
+# ---------------------------------------------------------------------------
+# Hyperparameters (Appendix A and B; defaults as stated there)
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class Params:
+    r_default: int = 32            # recent window (App. A.1)
+    r_min: int = 4
+    seg_rhos: Tuple[float, ...] = (0.33, 0.50, 0.67)   # eq:app_seg_layers
+    windows: Tuple[int, ...] = (4, 8, 16)              # eq:app_curvature_windows
+    lam_stab: float = 0.25         # eq:app_stabilized_curvature
+    lam_s: float = 0.15            # eq:app_boundary_score
+    eps_seg: float = 1e-6          # eq:app_hidden_normalization, eq:app_mad
+    mad_factor: float = 1.4826     # eq:app_robust_z
+    n_min: int = 16                # eq:app_slot_length_defaults
+    n_max: int = 128
+    n0: int = 64
+    lam_d: float = 0.25            # eq:app_segmentation_defaults
+    lam_n: float = 0.10
+    c_cut: float = 1.0
+    lam_Z: float = 0.25            # eq:app_probe_distortion
+    lam_M: float = 0.75
+    k_curv: int = 16               # eq:app_tree_split_candidates
+    lam_kappa: float = 0.05        # eq:app_binary_split
+    beta_frac: float = 0.1         # eq:app_value_prototype
+    eps: float = 1e-6              # every unstated epsilon (reading A6)
+
+
+def f32(x) -> float:
+    """Round to the nearest fp32 value (decision precision of the GPU)."""
+    return float(np.float32(x))
+
+
+# ---------------------------------------------------------------------------
+# Budget and regions (Problem Formulation; App. A.1 eq:app_total_budget,
+# eq:app_compressible_context, eq:app_free_budget)
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class Budget:
+    B_total: int
+    r: int
+    N_c: int
+    B_free: int
+
+
+def budget(L: int, G: int, N_ctx: int, x: float, p: Params = Params()) -> Budget:
+    """B_total = floor(L G N_ctx / x); r = 32 unless the total budget cannot hold
+    the window (then shortened, minimum 4); C = [0, N_ctx - r); with the floor
+    disabled B_free = B_total - L G r."""
+    B_total = int(math.floor(L * G * N_ctx / x))
+    r = p.r_default
+    if L * G * r > B_total:
+        r = B_total // (L * G)
+    r = min(r, N_ctx)
+    if r < p.r_min:
+        raise ValueError("budget cannot hold the minimum recent window")
+    N_c = N_ctx - r
+    return Budget(B_total, r, N_c, B_total - L * G * r)
+
+
+# ---------------------------------------------------------------------------
+# Segmentation (App. B.2 - B.3)
+# ---------------------------------------------------------------------------
+def seg_layer_indices(L: int, rhos=(0.33, 0.50, 0.67)) -> List[int]:
+    """eq:app_seg_layers: Unique{min(floor(rho L), L-1)}."""
+    out: List[int] = []
+    for rho in rhos:
+        l = min(int(math.floor(rho * L)), L - 1)
+        if l not in out:
+            out.append(l)
+    return out
+
+
+def normalize_hidden(h: np.ndarray, eps: float = 1e-6) -> np.ndarray:
+    """eq:app_hidden_normalization: h / max(||h||_2, eps), row-wise."""
+    h = np.asarray(h, dtype=F64)
+    n = np.sqrt((h * h).sum(axis=-1, keepdims=True))
+    return h / np.maximum(n, eps)
+
+
+def curvature_single(hbar: np.ndarray, w: int, eps: float = 1e-6) -> np.ndarray:
+    """eq:app_local_means .. eq:app_local_curvature for one slab and one window.
+
+    mu_- averages hbar_{i-w+1..i} (the current position included), mu_+ averages
+    hbar_{i+1..i+w}; delta_- = hbar_i - mu_-, delta_+ = mu_+ - hbar_i; each is
+    divided by max(||.||, eps); kappa = 1 - <u_-, u_+>.  Defined only for
+    w <= i < T - w; zero elsewhere (and everywhere when T < 2w + 1)."""
+    T = hbar.shape[0]
+    kap = np.zeros(T, dtype=F64)
+    if T < 2 * w + 1:
+        return kap
+    win = np.lib.stride_tricks.sliding_window_view(hbar, w, axis=0)   # [T-w+1, D, w]: rows j..j+w-1
+    for i0 in range(w, T - w, 4096):
+        i1 = min(T - w, i0 + 4096)
+        idx = np.arange(i0, i1)
+        mu_m = win[idx - w + 1].mean(axis=-1)       # rows i-w+1 .. i
+        mu_p = win[idx + 1].mean(axis=-1)           # rows i+1 .. i+w
+        dm = hbar[idx] - mu_m
+        dp = mu_p - hbar[idx]
+        um = dm / np.maximum(np.sqrt((dm * dm).sum(-1, keepdims=True)), eps)
+        up = dp / np.maximum(np.sqrt((dp * dp).sum(-1, keepdims=True)), eps)
+        kap[idx] = 1.0 - (um * up).sum(-1)
+    return kap
+
+
+def stabilized_curvature(hbars: List[np.ndarray], p: Params = Params()) -> np.ndarray:
+    """eq:app_stabilized_curvature: Mean - lam_stab * (population) Std over the
+    |L_seg| x |W| values; positions without a full window contribute their zero
+    (reading S3)."""
+    vals = np.stack([curvature_single(hb, w, p.eps_seg) for hb in hbars for w in p.windows])
+    return vals.mean(axis=0) - p.lam_stab * vals.std(axis=0)
+
+
+def lower_median(a: np.ndarray) -> float:
+    """Median of an even-length sequence taken as the lower middle element
+    (reading S1)."""
+    s = np.sort(np.asarray(a, dtype=F64))
+    return float(s[(len(s) - 1) // 2])
+
+
+def robust_z(a: np.ndarray, p: Params = Params()) -> np.ndarray:
+    """eq:app_robust_z / eq:app_mad over the complete sequence, no clipping."""
+    a = np.asarray(a, dtype=F64)
+    med = lower_median(a)
+    mad = lower_median(np.abs(a - med))
+    return (a - med) / (p.mad_factor * mad + p.eps_seg)
+
+
+def boundary_score(kappa: np.ndarray, surprisal: np.ndarray, p: Params = Params()) -> np.ndarray:
+    """eq:app_boundary_score: b_i = z(kappa_i) + lam_s z(s_i)."""
+    return robust_z(kappa, p) + p.lam_s * robust_z(surprisal, p)
+
+
+def slot_dispersion_literal(hbars: List[np.ndarray], a: int, e: int) -> float:
+    """eq:app_adjacent_difference .. eq:app_slot_dispersion: mean over slabs of
+    the sample variance of the adjacent differences d_t, t = a..e-2 (context
+    starts at 0); zero when fewer than two differences."""
+    nS = e - a - 1
+    if nS < 2:
+        return 0.0
+    tot = 0.0
+    for hb in hbars:
+        d = hb[a + 1:e] - hb[a:e - 1]
+        dbar = d.mean(axis=0)
+        tot += float(((d - dbar) ** 2).sum()) / (nS - 1)
+    return tot / len(hbars)
+
+
+class PrefixDispersion:
+    """eq:app_prefix_dispersion: Disp_l([a,e)) = (sum ||d_t||^2 - ||sum d_t||^2 / n_S)
+    / max(n_S - 1, 1), from prefix statistics.  The prefix of d_t telescopes:
+    sum_{t=a}^{e-2} d_t = hbar_{e-1} - hbar_a, which is what is evaluated."""
+
+    def __init__(self, hbars: List[np.ndarray], N: int):
+        self.hbars = [hb[:N] for hb in hbars]
+        sq = np.zeros(max(N - 1, 0), dtype=F64)
+        for hb in self.hbars:
+            d = hb[1:N] - hb[:N - 1]
+            sq += (d * d).sum(axis=-1)
+        self.P2 = np.concatenate([[0.0], np.cumsum(sq)])   # P2[t] = sum_{tau<t} ||d_tau||^2 (summed over slabs)
+        self.nl = len(hbars)
+
+    def many(self, a: np.ndarray, e: int) -> np.ndarray:
+        """Disp([a, e)) for an array of starts a (all with the same end e)."""
+        a = np.asarray(a)
+        nS = e - a - 1
+        out = np.zeros(len(a), dtype=F64)
+        ok = nS >= 1
+        if not ok.any():
+            return out
+        aa = a[ok]
+        s2 = self.P2[e - 1] - self.P2[aa]
+        sd = np.zeros(len(aa), dtype=F64)
+        for hb in self.hbars:
+            diff = hb[e - 1][None, :] - hb[aa]
+            sd += (diff * diff).sum(axis=-1)
+        n = nS[ok].astype(F64)
+        out[ok] = (s2 - sd / n) / np.maximum(n - 1.0, 1.0) / self.nl
+        return out
+
+
+def segment_dp(b: np.ndarray, disp, N: int, p: Params = Params()) -> Tuple[List[int], np.ndarray]:
+    """eq:app_boundary_reward .. eq:app_terminal_predecessor.
+
+    F[0] = 0; F[i] = max over a in A(i) of F[a] + Gamma(a) - lam_d Disp([a,i))
+    - lam_n ((i-a-n0)/n0)^2 with A(i) = {a : n_min <= i-a <= n_max}; Gamma(0)=0,
+    Gamma(a) = b_{a-1} - c_cut.  Unreachable states are -inf; argmax ties go to
+    the smallest a (reading S2).  If no standard predecessor of N has a finite
+    F, the last slot's minimum length is relaxed.  ``disp(a_array, e)`` returns
+    Disp([a, e)).  Returns the slot starts [a_1 = 0, ..., a_J] and F."""
+    if N <= 0:
+        return [], np.zeros(1)
+    F = np.full(N + 1, -np.inf)
+    P = np.full(N + 1, -1, dtype=np.int64)
+    F[0] = 0.0
+    gam = np.empty(N + 1, dtype=F64)
+    gam[0] = 0.0
+    gam[1:] = np.asarray(b[:N], dtype=F64) - p.c_cut
+
+    def relax(i: int, lo_len: int) -> Tuple[float, int]:
+        a = np.arange(max(0, i - p.n_max), i - lo_len + 1)
+        if len(a) == 0:
+            return -np.inf, -1
+        a = a[np.isfinite(F[a])]
+        if len(a) == 0:
+            return -np.inf, -1
+        n = (i - a).astype(F64)
+        val = F[a] + gam[a] - p.lam_d * disp(a, i) - p.lam_n * ((n - p.n0) / p.n0) ** 2
+        k = int(np.argmax(val))                         # first maximum -> smallest a
+        return float(val[k]), int(a[k])
+
+    for i in range(1, N + 1):
+        F[i], P[i] = relax(i, p.n_min)
+    if P[N] < 0:
+        F[N], P[N] = relax(N, 1)
+    starts = []
+    i = N
+    while i > 0:
+        i = int(P[i])
+        starts.append(i)
+    return starts[::-1], F
+
+
+@dataclasses.dataclass
+class SegmentResult:
+    kappa: np.ndarray          # [T] stabilized curvature
+    b: np.ndarray              # [T] boundary score
+    slot_starts: List[int]     # [J] absolute starts; the slots tile [0, N_c)
+    N_c: int
+
+
+def segment(hidden: np.ndarray, surprisal: np.ndarray, N_c: int, p: Params = Params()) -> SegmentResult:
+    """Curvature-guided slot segmentation over C = [0, N_c) (App. B.2 - B.3).
+    ``hidden`` holds the |L_seg| slabs [n_seg, T, D]."""
+    hbars = [normalize_hidden(h, p.eps_seg) for h in hidden]
+    kappa = stabilized_curvature(hbars, p)
+    b = boundary_score(kappa, np.asarray(surprisal, dtype=F64), p)
+    pd = PrefixDispersion(hbars, N_c)
+    starts, _ = segment_dp(b, pd.many, N_c, p)
+    return SegmentResult(kappa, b, starts, N_c)
+
+
+# ---------------------------------------------------------------------------
+# RoPE (rotate-half convention, reading A7) from the caller's tables
+# ---------------------------------------------------------------------------
+def rope_inverse(k: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """k° = RoPE^{-1}(k, t) row-wise, cos/sin already gathered at t."""
+    h = k.shape[-1] // 2
+    k1, k2 = k[..., :h], k[..., h:]
+    return np.concatenate([k1 * cos + k2 * sin, k2 * cos - k1 * sin], axis=-1)
+
+
+def rope_apply(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    h = x.shape[-1] // 2
+    x1, x2 = x[..., :h], x[..., h:]
+    return np.concatenate([x1 * cos - x2 * sin, x2 * cos + x1 * sin], axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Relevance and probes for one (layer, KV head) (App. A.4 eq:app_attention_probability,
+# eq:app_direct_relevance; App. A.3 "Prototype distortion")
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class LGContext:
+    """Everything the trees of one (l, g) need, in fp64."""
+    K: np.ndarray          # [T, d] post-RoPE keys
+    V: np.ndarray          # [T, d]
+    kr: np.ndarray         # [T, d] k° = RoPE^{-1}(k, t)
+    cos: np.ndarray        # [T, d/2]
+    sin: np.ndarray
+    R: np.ndarray          # [N_c] token values R^tok (lambda_graph = 0: R = s-hat)
+    s: np.ndarray          # [N_c] un-normalised direct relevance
+    Qp: np.ndarray         # [W, d] distortion probes (round-robin heads, reading A2)
+    E: np.ndarray          # [W, N_c] e_{q,t} = exp(l_{q,t} - m_q), m_q = max over C (reading A5)
+    ZC: np.ndarray         # [W] Z_q(C)
+    m: np.ndarray          # [W] shifts
+    kappa: np.ndarray      # [T] curvature used for split candidates
+    d: int
+
+
+def relevance(K: np.ndarray, Qg: np.ndarray, N_ctx: int, N_c: int, p: Params = Params()) -> Tuple[np.ndarray, np.ndarray]:
+    """Direct relevance of context tokens for one (l, g).
+
+    ``Qg`` [H/G, W, d] holds the window queries of the query heads sharing KV
+    head g, at positions N_ctx + u.  For each row (u, h) the softmax runs over
+    the whole visible range V(u) = [0, N_ctx + u] (reading A3); the slice t in
+    C is taken afterwards.  s_t = sum over rows of pi; s-hat = s / (sum_C s + eps).
+    """
+    d = K.shape[1]
+    W = Qg.shape[1]
+    s = np.zeros(N_c, dtype=F64)
+    for h in range(Qg.shape[0]):
+        for u in range(W):
+            vis = N_ctx + u + 1
+            lg = K[:vis] @ Qg[h, u] / math.sqrt(d)
+            e = np.exp(lg - lg.max())
+            pi = e / e.sum()
+            s += pi[:N_c]
+    return s / (s.sum() + p.eps), s
+
+
+def lg_context(K: np.ndarray, V: np.ndarray, Qg: np.ndarray, cos: np.ndarray, sin: np.ndarray,
+               kappa: np.ndarray, N_ctx: int, N_c: int, p: Params = Params()) -> LGContext:
+    K = np.asarray(K, dtype=F64)
+    V = np.asarray(V, dtype=F64)
+    Qg = np.asarray(Qg, dtype=F64)
+    cos = np.asarray(cos, dtype=F64)
+    sin = np.asarray(sin, dtype=F64)
+    hpg, W, d = Qg.shape
+    R, s = relevance(K, Qg, N_ctx, N_c, p)
+    # distortion probes: probe i is window query i of head H(g)[i mod |H(g)|]
+    Qp = np.stack([Qg[i % hpg, i] for i in range(W)])
+    lg = Qp @ K[:N_c].T / math.sqrt(d)            # [W, N_c]
+    m = lg.max(axis=1)
+    E = np.exp(lg - m[:, None])
+    kr = rope_inverse(K, cos, sin)
+    return LGContext(K, V, kr, cos, sin, R, s, Qp, E, E.sum(axis=1), m,
+                     np.asarray(kappa, dtype=F64), d)
+
+
+# ---------------------------------------------------------------------------
+# Prototypes and distortion (App. A.3 eq:app_rope_prototype ..
+# eq:app_node_and_drop_distortion)
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class Proto:
+    k: np.ndarray
+    v: np.ndarray
+    pos: int
+    m_eff: float
+
+
+def prototype(c: LGContext, x: int, y: int, p: Params = Params()) -> Proto:
+    """Prototype of the interval [x, y).  A singleton is the original entry
+    with multiplicity 1 (App. C.5, reading A15)."""
+    n = y - x
+    if n == 1:
+        return Proto(c.K[x].copy(), c.V[x].copy(), x, 1.0)
+    kr = c.kr[x:y]
+    mean_k = kr.mean(axis=0)
+    pos = int(np.round(np.mean(np.arange(x, y, dtype=F64))))     # round half to even (reading A8)
+    h = c.d // 2
+    k_t = rope_apply(mean_k, c.cos[pos], c.sin[pos])
+    R = c.R[x:y]
+    beta = p.beta_frac * R.mean()
+    w = R + beta
+    v_t = (w[:, None] * c.V[x:y]).sum(axis=0) / (w.sum() + p.eps)
+    coh = np.sqrt((mean_k * mean_k).sum()) / (np.sqrt((kr * kr).sum(axis=1)).mean() + p.eps)
+    m_eff = float(np.clip(n * coh * coh, 1.0, n))
+    return Proto(k_t, v_t, pos, m_eff)
+
+
+def distortion(c: LGContext, x: int, y: int, p: Params = Params()) -> Tuple[float, float]:
+    """(D(I), D_drop(I)) for I = [x, y).  Z and M are explicit sums over the
+    interval; the attention-mass normaliser is Z_q(C) (reading A4); a singleton
+    has D = 0 (reading A15)."""
+    e = c.E[:, x:y]                      # [W, n]
+    Z = e.sum(axis=1)
+    frac = Z / c.ZC
+    Ddrop = float(frac.mean())
+    if y - x == 1:
+        return 0.0, Ddrop
+    pr = prototype(c, x, y, p)
+    M = e @ c.V[x:y]                     # [W, d]
+    zt = pr.m_eff * np.exp(c.Qp @ pr.k / math.sqrt(c.d) - c.m)
+    Mt = zt[:, None] * pr.v[None, :]
+    Dq = (p.lam_Z * (Z - zt) ** 2 / (Z * Z + p.eps)
+          + p.lam_M * ((M - Mt) ** 2).sum(axis=1) / ((M * M).sum(axis=1) + p.eps))
+    return float((frac * Dq).mean()), Ddrop
+
+
+# ---------------------------------------------------------------------------
+# Tree construction (App. A.3 "Recursive refinement rule", eq:app_binary_split ..
+# eq:app_split_choice; App. B.4 eq:app_tree_split_candidates)
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class Node:
+    a: int
+    b: int
+    D: float
+    Ddrop: float
+    R: float
+    children: List[int] = dataclasses.field(default_factory=list)   # node indices (BFS numbering)
+    kind: str = "leaf"        # "bin", "ext" or "leaf"
+    cut: int = -1             # xi for "bin", p for "ext"
+    # candidate table for the parity near-tie check: list of (children intervals, score)
+    cands: list = dataclasses.field(default_factory=list)
+    depth: int = 0
+
+
+def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache=None):
+    """Choose the preselected refinement of node [a, b) (n >= 2).
+
+    Binary candidates: the top-16 curvature positions t in [a, b-2] (ties to
+    the smaller t) each propose the cut xi = t + 1 (reading A10), plus the
+    midpoint a + floor(n/2); G_bin = D(I) - D(L) - D(R) + lam_kappa kappa-hat_{xi-1}
+    with kappa min-max normalised over I (reading A11); cost 1.  Extraction:
+    p = argmax_t mean_q e_{q,t}/Z_q(C) (reading A12); children are the
+    non-empty parts of [a,p), {p}, [p+1,b); rho_ext = G_ext / (#children - 1).
+    The binary form wins ties, and n = 2 is always binary (reading A13).
+    Scores are compared in fp32."""
+    if dcache is None:
+        dcache = {}
+
+    def D(x, y):
+        if (x, y) not in dcache:
+            dcache[(x, y)] = distortion(c, x, y, p)
+        return dcache[(x, y)][0]
+
+    n = b - a
+    cands = []
+    if n == 2:
+        kids = [(a, a + 1), (a + 1, b)]
+        score = Dv - D(a, a + 1) - D(a + 1, b)
+        return "bin", a + 1, kids, [("bin", a + 1, kids, f32(score))]
+    kap = c.kappa[a:b]
+    kmin, kmax = kap.min(), kap.max()
+    khat = (kap - kmin) / (kmax - kmin) if kmax > kmin else np.zeros_like(kap)
+    ts = list(range(a, b - 1))
+    # stable descending sort on fp32 curvature -> ties keep the smaller t first
+    ts.sort(key=lambda t: -np.float32(c.kappa[t]))
+    xis = sorted(set([t + 1 for t in ts[:p.k_curv]] + [a + n // 2]))
+    best_bin, best_xi = -np.inf, -1
+    for xi in xis:
+        g = f32(Dv - D(a, xi) - D(xi, b) + p.lam_kappa * khat[xi - 1 - a])
+        cands.append(("bin", xi, [(a, xi), (xi, b)], g))
+        if g > best_bin:                      # strict: smaller xi wins ties
+            best_bin, best_xi = g, xi
+    A = (c.E[:, a:b] / c.ZC[:, None]).mean(axis=0)
+    A32 = A.astype(np.float32)
+    pp = a + int(np.argmax(A32))              # first maximum -> smaller t
+    kids = [iv for iv in [(a, pp), (pp, pp + 1), (pp + 1, b)] if iv[1] > iv[0]]
+    g_ext = f32(f32(Dv - sum(D(x, y) for (x, y) in kids)) / (len(kids) - 1))
+    cands.append(("ext", pp, kids, g_ext))
+    if best_bin >= g_ext:
+        return "bin", best_xi, [(a, best_xi), (best_xi, b)], cands
+    return "ext", pp, kids, cands
+
+
+def build_tree(c: LGContext, a: int, b: int, p: Params = Params()) -> List[Node]:
+    """Full prototype tree of slot [a, b), recursing to singletons (reading A14).
+    Nodes are returned in BFS order (level by level, left to right)."""
+    dcache: Dict[Tuple[int, int], Tuple[float, float]] = {}
+
+    def dd(x, y):
+        if (x, y) not in dcache:
+            dcache[(x, y)] = distortion(c, x, y, p)
+        return dcache[(x, y)]
+
+    D0, Dd0 = dd(a, b)
+    nodes = [Node(a, b, D0, Dd0, float(c.R[a:b].sum()), depth=0)]
+    head = 0
+    while head < len(nodes):
+        v = nodes[head]
+        if v.b - v.a >= 2:
+            kind, cut, kids, cands = refine(c, v.a, v.b, v.D, p, dcache)
+            v.kind, v.cut, v.cands = kind, cut, cands
+            for (x, y) in kids:
+                Dk, Ddk = dd(x, y)
+                v.children.append(len(nodes))
+                nodes.append(Node(x, y, Dk, Ddk, float(c.R[x:y].sum()), depth=v.depth + 1))
+        head += 1
+    return nodes
+
+
+# ---------------------------------------------------------------------------
+# Gains, utility and keys (App. A.5 eq:app_operation_gains, eq:app_operation_costs,
+# eq:app_unit_utility; App. C.5 "lower-bounded by zero")
+# ---------------------------------------------------------------------------
+def normalize_omega(omega_raw: np.ndarray, p: Params = Params()) -> np.ndarray:
+    """eq:app_head_sensitivity: omega = omega_raw / (mean omega_raw + eps)."""
+    w = np.asarray(omega_raw, dtype=F64)
+    return w / (w.mean() + p.eps)
+
+
+@dataclasses.dataclass
+class Op:
+    oid: int                  # tie-break id: unit ordinal * 256 + local index
+    lg: int
+    unit: int                 # unit ordinal (l*G + g) * J + j
+    node: int                 # node index created/refined (-1 for Add = root 0 created)
+    kind: str                 # "add" or "split"
+    gain: float               # Delta+ (clamped)
+    cost: int
+    U: float                  # fp32-rounded utility
+    key: int                  # (U fp32 bits << 32) | (2^32 - 1 - oid)
+    children: List[int] = dataclasses.field(default_factory=list)   # op indices made available
+
+
+def composite_key(U32: float, oid: int) -> int:
+    """Unique priority: utility first, then the smaller id (reading Q1)."""
+    bits = int(np.float32(U32).view(np.uint32))
+    return (bits << 32) | (0xFFFFFFFF - oid)
+
+
+def make_ops(trees: Dict[Tuple[int, int, int], List[Node]], omega: np.ndarray, G: int, J: int) -> List[Op]:
+    """Add(l,g,j): Delta = omega R(root) (D_drop(root) - D(root)), cost 1;
+    Split(v): Delta = omega R(v) (D(v) - sum_children D), cost |child| - 1;
+    Delta+ = max(Delta, 0); U = Delta+ / c.  Op ids order units (l, g, j)
+    major, then Add, then Split(v) in BFS order of v (reading Q1)."""
+    ops: List[Op] = []
+    for (l, g, j), nodes in sorted(trees.items()):
+        lg = l * G + g
+        unit = lg * J + j
+        w = float(omega[l, g])
+        split_op: Dict[int, int] = {}
+        root = nodes[0]
+        gain = max(w * root.R * (root.Ddrop - root.D), 0.0)
+        add = Op(unit * 256, lg, unit, 0, "add", gain, 1, f32(gain), 0)
+        add.key = composite_key(add.U, add.oid)
+        ops.append(add)
+        add_idx = len(ops) - 1
+        for i, v in enumerate(nodes):
+            if not v.children:
+                continue
+            c = len(v.children) - 1
+            gain = max(w * v.R * (v.D - sum(nodes[k].D for k in v.children)), 0.0)
+            U = f32(gain / c)
+            op = Op(unit * 256 + 1 + i, lg, unit, i, "split", gain, c, U, 0)
+            op.key = composite_key(U, op.oid)
+            ops.append(op)
+            split_op[i] = len(ops) - 1
+        # availability links: Add exposes Split(root); Split(v) exposes Split(child)
+        if 0 in split_op:
+            ops[add_idx].children.append(split_op[0])
+        for i, v in enumerate(nodes):
+            if i in split_op:
+                ops[split_op[i]].children.extend(split_op[k] for k in v.children if k in split_op)
+    return ops
+
+
+# ---------------------------------------------------------------------------
+# Global greedy allocation (App. A.5 "Stage II", eq:app_allocation_problem;
+# App. C.3 procedure; App. C.5 non-elastic)
+# ---------------------------------------------------------------------------
+def select_heap(ops: List[Op], B_free: int) -> List[bool]:
+    """Literal max-priority queue: start from every Add; pop the highest key;
+    execute it if its cost fits the remaining budget (then push the Splits it
+    exposes), otherwise discard it for good (reading Q2); stop when the budget
+    is zero or the queue is empty (reading Q3)."""
+    executed = [False] * len(ops)
+    heap = [(-op.key, i) for i, op in enumerate(ops) if op.kind == "add"]
+    heapq.heapify(heap)
+    B = B_free
+    while heap and B > 0:
+        _, i = heapq.heappop(heap)
+        if ops[i].cost <= B:
+            executed[i] = True
+            B -= ops[i].cost
+            for k in ops[i].children:
+                heapq.heappush(heap, (-ops[k].key, k))
+    return executed
+
+
+# ---------------------------------------------------------------------------
+# Packing (App. A.5 "Frontier updates and physical packing", eq:app_frontier_update)
+# ---------------------------------------------------------------------------
+def frontier(nodes: List[Node], add_exec: bool, split_exec: Dict[int, bool]) -> List[int]:
+    """Frontier of one tree: empty unless Add executed; every executed Split
+    replaces its node by its children."""
+    if not add_exec:
+        return []
+    out, stack = [], [0]
+    while stack:
+        i = stack.pop()
+        if split_exec.get(i, False):
+            stack.extend(reversed(nodes[i].children))
+        else:
+            out.append(i)
+    return sorted(out, key=lambda i: nodes[i].a)
+
+
+def round_kv(x: np.ndarray, kv_dtype: str) -> np.ndarray:
+    """Storage rounding of a prototype to the cache dtype (RNE for bf16)."""
+    if kv_dtype == "f32":
+        return x.astype(np.float32)
+    x32 = np.asarray(x, dtype=np.float32)
+    bits = x32.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    bits = ((bits + 0x7FFF + lsb) >> 16) << 16
+    return bits.astype(np.uint32).view(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# The whole path for one case
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass
+class OracleResult:
+    budget: Budget
+    seg: Optional[SegmentResult]
+    slot_starts: List[int]
+    trees: Dict[Tuple[int, int, int], List[Node]]
+    ctx: Dict[Tuple[int, int], LGContext]
+    ops: List[Op]
+    executed: List[bool]
+    counts: np.ndarray                         # [L*G] entries per (l, g) including the recent window
+    packed: Dict[Tuple[int, int], dict]       # per (l, g): k, v, pos, logm arrays
+
+
+def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ctx, x,
+        kv_dtype="f32", p: Params = Params(), slot_starts: Optional[List[int]] = None,
+        kappa: Optional[np.ndarray] = None, lg_pairs=None, do_select=True) -> OracleResult:
+    """Segment -> build -> score -> select -> pack for one case.  Arrays are
+    numpy (any float dtype; converted to fp64).  ``slot_starts``/``kappa`` may be
+    given to test the later stages on their own; ``lg_pairs`` restricts the tree
+    build to some (l, g) pairs (then selection is skipped)."""
+    bud = budget(L, G, N_ctx, x, p)
+    seg = None
+    if slot_starts is None or kappa is None:
+        seg = segment(np.asarray(hidden), np.asarray(surprisal), bud.N_c, p)
+        slot_starts = seg.slot_starts if slot_starts is None else slot_starts
+        kappa = seg.kappa if kappa is None else kappa
+    J = len(slot_starts)
+    bounds = list(slot_starts) + [bud.N_c]
+    hpg = H // G
+    pairs = lg_pairs if lg_pairs is not None else [(l, g) for l in range(L) for g in range(G)]
+    trees: Dict[Tuple[int, int, int], List[Node]] = {}
+    ctxs: Dict[Tuple[int, int], LGContext] = {}
+    for (l, g) in pairs:
+        c = lg_context(K[l, g], V[l, g], Q[l, g * hpg:(g + 1) * hpg], rope_cos, rope_sin, kappa,
+                       N_ctx, bud.N_c, p)
+        ctxs[(l, g)] = c
+        for j in range(J):
+            trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p)
+    if not do_select or lg_pairs is not None:
+        return OracleResult(bud, seg, list(slot_starts), trees, ctxs, [], [], np.zeros(0), {})
+    omega = normalize_omega(omega_raw, p)
+    ops = make_ops(trees, omega, G, J)
+    ex = select_heap(ops, bud.B_free)
+    add_exec: Dict[Tuple[int, int, int], bool] = {}
+    split_exec: Dict[Tuple[int, int, int], Dict[int, bool]] = {}
+    for op, e in zip(ops, ex):
+        lg, j = divmod(op.unit, J)
+        key = (lg // G, lg % G, j)
+        if op.kind == "add":
+            add_exec[key] = e
+        else:
+            split_exec.setdefault(key, {})[op.node] = e
+    counts = np.zeros(L * G, dtype=np.int64)
+    packed = {}
+    for (l, g) in pairs:
+        c = ctxs[(l, g)]
+        ks, vs, ps, lm = [], [], [], []
+        for j in range(J):
+            nodes = trees[(l, g, j)]
+            for i in frontier(nodes, add_exec[(l, g, j)], split_exec.get((l, g, j), {})):
+                pr = prototype(c, nodes[i].a, nodes[i].b, p)
+                ks.append(round_kv(pr.k, kv_dtype))
+                vs.append(round_kv(pr.v, kv_dtype))
+                ps.append(pr.pos)
+                lm.append(math.log(pr.m_eff))
+        for t in range(bud.N_c, N_ctx):            # recent window, kept exactly
+            ks.append(round_kv(c.K[t], kv_dtype))
+            vs.append(round_kv(c.V[t], kv_dtype))
+            ps.append(t)
+            lm.append(0.0)
+        counts[l * G + g] = len(ps)
+        packed[(l, g)] = dict(k=np.array(ks), v=np.array(vs), pos=np.array(ps, dtype=np.int64),
+                              logm=np.array(lm))
+    return OracleResult(bud, seg, list(slot_starts), trees, ctxs, ops, ex, counts, packed)

@@ -1,0 +1,202 @@
+"""Pins for the oracle's budget auction (App. A.5 Stage II, App. C.3, C.5):
+a hand-worked trace, three independent implementations that must agree
+(literal queue, naive rescan, effective-key cut), exhaustive optimum on tiny
+forests, and the budget accounting.  CPU only."""
+import itertools
+import os
+import random
+
+import numpy as np
+import pytest
+
+from oracle import gracekv_oracle as O
+
+
+def _forest(rng, n_units, max_ops, p_zero=0.2):
+    """Random op forest: per unit an Add and a tree of Splits (cost 1 or 2)."""
+    ops = []
+    for u in range(n_units):
+        def mk(kind, local):
+            U = 0.0 if rng.random() < p_zero else float(np.float32(rng.uniform(0, 4)))
+            oid = u * 256 + local
+            op = O.Op(oid, 0, u, local, kind, U, 1 if kind == "add" else rng.choice([1, 2]), U, 0)
+            op.key = O.composite_key(U, oid)
+            return op
+        base = len(ops)
+        ops.append(mk("add", 0))
+        n = rng.randint(0, max_ops)
+        for i in range(n):
+            parent = base + (0 if i == 0 else rng.randrange(0, i + 1))
+            ops.append(mk("split", 1 + i))
+            ops[parent].children.append(len(ops) - 1)
+    return ops
+
+
+def _naive(ops, B):
+    """Rescan greedy: each step scans every available op for the largest key."""
+    avail = {i for i, o in enumerate(ops) if o.kind == "add"}
+    done = [False] * len(ops)
+    while avail and B > 0:
+        i = max(avail, key=lambda k: ops[k].key)
+        avail.remove(i)
+        if ops[i].cost <= B:
+            done[i] = True
+            B -= ops[i].cost
+            avail.update(ops[i].children)
+    return done
+
+
+def _effective_key_cut(ops, B):
+    """The parallel form used on the GPU: E(a) = min(k(a), E(parent)); every op
+    with E above the cut theta executes; the one group with E = theta is run
+    as a sub-greedy; with one unit left the best available cost-1 op fills it."""
+    parent = [-1] * len(ops)
+    for i, o in enumerate(ops):
+        for k in o.children:
+            parent[k] = i
+    E = [0] * len(ops)
+    for i, o in enumerate(ops):                 # parents precede children in this list
+        E[i] = o.key if parent[i] < 0 else min(o.key, E[parent[i]])
+    order = sorted(range(len(ops)), key=lambda i: -E[i])
+    total = sum(o.cost for o in ops)
+    done = [False] * len(ops)
+    if B <= 0:
+        return done
+    if total <= B - 1 or total == B:
+        return [True] * len(ops) if total <= B else done
+    # theta: first E-group (descending) where the inclusive cumulative cost reaches B - 1
+    cum, theta = 0, None
+    groups = {}
+    for i in order:
+        groups.setdefault(E[i], []).append(i)
+    for e in sorted(groups, reverse=True):
+        cum += sum(ops[i].cost for i in groups[e])
+        if cum >= B - 1:
+            theta = e
+            break
+    if theta is None:
+        return [True] * len(ops)
+    above = 0
+    for i in range(len(ops)):
+        if E[i] > theta:
+            done[i] = True
+            above += ops[i].cost
+    R = B - above
+    grp = set(groups[theta])
+    root = [i for i in grp if parent[i] < 0 or parent[i] not in grp][0]
+    avail = {root}
+    while avail and R >= 2:
+        i = max(avail, key=lambda k: ops[k].key)
+        avail.remove(i)
+        done[i] = True
+        R -= ops[i].cost
+        avail.update(k for k in ops[i].children if k in grp)
+    if R == 1:
+        best = None
+        for i, o in enumerate(ops):
+            if not done[i] and o.cost == 1 and (parent[i] < 0 or done[parent[i]]):
+                if best is None or o.key > ops[best].key:
+                    best = i
+        if best is not None:
+            done[best] = True
+    return done
+
+
+def test_worked_example():
+    lines = [l.split() for l in open(os.path.join(os.path.dirname(__file__), "golden",
+                                                  "select_worked_example.txt")) if l.strip() and not l.startswith("#")]
+    def op(oid, kind, U, cost):
+        o = O.Op(oid, 0, oid // 256, 0, kind, U, cost, U, 0)
+        o.key = O.composite_key(U, oid)
+        return o
+    ops = [op(0, "add", 5.0, 1), op(1, "split", 9.0, 2), op(2, "split", 1.0, 1),
+           op(256, "add", 7.0, 1), op(257, "split", 3.0, 2)]
+    ops[0].children = [1]
+    ops[1].children = [2]
+    ops[3].children = [4]
+    names = {"a0": 0, "s0": 1, "s1": 2, "a1": 3, "s2": 4}
+    for row in lines:
+        B = int(row[0][1:])
+        ex = O.select_heap(ops, B)
+        assert {i for i, e in enumerate(ex) if e} == {names[n] for n in row[1:]}
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_three_implementations_agree(seed):
+    rng = random.Random(seed)
+    ops = _forest(rng, rng.randint(1, 6), 9, p_zero=0.3 if seed % 2 else 0.0)
+    total = sum(o.cost for o in ops)
+    for B in sorted({0, 1, 2, 3, total // 3, total // 2, total - 1, total, total + 2}):
+        if B < 0:
+            continue
+        a = O.select_heap(ops, B)
+        b = _naive(ops, B)
+        c = _effective_key_cut(ops, B)
+        assert a == b == c, (seed, B)
+        spent = sum(o.cost for o, e in zip(ops, a) if e)
+        assert spent <= B
+        # non-elastic: budget left only if the queue ran dry or one unit had no cost-1 op
+        assert spent == min(B, total) or spent == B - 1 or spent == total
+
+
+def _ideals(ops):
+    parent = [-1] * len(ops)
+    for i, o in enumerate(ops):
+        for k in o.children:
+            parent[k] = i
+    n = len(ops)
+    for mask in range(1 << n):
+        ok = all(not (mask >> i) & 1 or parent[i] < 0 or (mask >> parent[i]) & 1 for i in range(n))
+        if ok:
+            yield mask
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_greedy_versus_exhaustive_optimum(seed):
+    rng = random.Random(100 + seed)
+    ops = _forest(rng, 3, 4, p_zero=0.0)
+    ops = ops[:14]
+    for o in ops:
+        o.children = [k for k in o.children if k < len(ops)]
+    gain = [o.U * o.cost for o in ops]
+    total = sum(o.cost for o in ops)
+    for B in range(0, total + 1):
+        ex = O.select_heap(ops, B)
+        val = sum(g for g, e in zip(gain, ex) if e)
+        opt = max(sum(gain[i] for i in range(len(ops)) if (m >> i) & 1)
+                  for m in _ideals(ops) if sum(ops[i].cost for i in range(len(ops)) if (m >> i) & 1) <= B)
+        assert val <= opt + 1e-9
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_greedy_is_optimal_for_unit_costs_and_monotone_utilities(seed):
+    rng = random.Random(200 + seed)
+    ops = _forest(rng, 3, 4, p_zero=0.0)[:13]
+    parent = [-1] * len(ops)
+    for i, o in enumerate(ops):
+        o.children = [k for k in o.children if k < len(ops)]
+        for k in o.children:
+            parent[k] = i
+    for i, o in enumerate(ops):                 # unit costs, utilities non-increasing down every path
+        o.cost = 1
+        if parent[i] >= 0:
+            o.U = o.gain = float(np.float32(min(o.U, ops[parent[i]].U)))
+        o.key = O.composite_key(o.U, o.oid)
+    gain = [o.U for o in ops]
+    for B in range(0, len(ops) + 1):
+        ex = O.select_heap(ops, B)
+        val = sum(g for g, e in zip(gain, ex) if e)
+        opt = max(sum(gain[i] for i in range(len(ops)) if (m >> i) & 1)
+                  for m in _ideals(ops) if bin(m).count("1") <= B)
+        assert val == pytest.approx(opt, abs=1e-9)
+
+
+def test_budget_formulas():
+    b = O.budget(2, 2, 1024, 16.0)
+    assert (b.B_total, b.r, b.N_c, b.B_free) == (256, 32, 992, 128)
+    b = O.budget(32, 8, 131072, 128.0)
+    assert (b.B_total, b.r, b.B_free) == (262144, 32, 253952)
+    b = O.budget(32, 8, 8192, 1000.0)          # window shrinks: 2097 // 256 = 8
+    assert (b.B_total, b.r) == (2097, 8)
+    with pytest.raises(ValueError):
+        O.budget(32, 8, 8192, 4000.0)          # cannot hold 4 entries per (l, g)
