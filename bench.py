@@ -1,0 +1,175 @@
+"""Throughput of one-shot KV-cache compression (segment -> build -> score ->
+select -> pack) on one MI355X, on a synthetic Llama-3-8B-shaped cache.
+
+One step = one pass of the whole path over one cache resident in HBM.  Prints
+one JSON line (metric: compressed context tokens/s = L * G * N_ctx / step
+time), with a roofline entry for the tree-build call and the CPU oracle timed
+on a bounded sample of the same workload as a baseline.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="8b-128k")
+    ap.add_argument("--x", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=12.0)
+    return ap.parse_args()
+
+
+def algorithmic_bytes(sh, plan, b):
+    """Bytes the method must move once: K + V + window queries + RoPE tables
+    (build), hidden slabs + surprisal (segment), packed cache (pack)."""
+    kv = 2 * sh.L * sh.G * sh.T * sh.d * b
+    q = sh.L * sh.H * sh.W * sh.d * b
+    rope = 2 * sh.T * (sh.d // 2) * 4
+    hidden = sh.n_seg * sh.T * sh.D * b + sh.T * 4
+    out = plan.B_total * (2 * sh.d * b + 8) + (sh.L * sh.G + 1) * 8
+    return dict(build=kv + q + rope, segment=hidden, pack=out, total=kv + q + rope + hidden + out)
+
+
+def cpu_baseline(case, sh, budget_s):
+    """The oracle as it stands, one thread, on bounded samples of this workload.
+    Per (layer, KV head, token) it costs: segmentation of a 4096-token window
+    (shared by all L*G heads), relevance of one (l, g) over the full sequence,
+    tree build + auction of the first slots of that (l, g) until the time
+    budget is spent.  value = 1 / (sum of the per-token costs)."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import gracekv_oracle as O
+    with threadpool_limits(limits=1):
+        np32 = lambda t: t.detach().float().cpu().numpy()
+        bud = O.budget(sh.L, sh.G, sh.N_ctx, sh.x)
+        nseg = min(4096, bud.N_c)
+        hid = np32(case["hidden"][:, :nseg + 32])
+        t0 = time.perf_counter()
+        seg = O.segment(hid, np32(case["surprisal"][:nseg + 32]), nseg)
+        t_seg = time.perf_counter() - t0
+        l, g = 0, 0
+        hpg = sh.H // sh.G
+        K = np32(case["K"][l, g])
+        V = np32(case["V"][l, g])
+        Qg = np32(case["Q"][l, g * hpg:(g + 1) * hpg])
+        cos, sin = np32(case["rope_cos"]), np32(case["rope_sin"])
+        kappa = np.zeros(sh.T)
+        kappa[:nseg + 32] = seg.kappa
+        t0 = time.perf_counter()
+        ctx = O.lg_context(K, V, Qg, cos, sin, kappa, sh.N_ctx, bud.N_c)
+        t_rel = time.perf_counter() - t0
+        bounds = seg.slot_starts + [nseg]
+        trees, toks = {}, 0
+        t0 = time.perf_counter()
+        for j in range(len(seg.slot_starts)):
+            trees[(0, 0, j)] = O.build_tree(ctx, bounds[j], bounds[j + 1])
+            toks += bounds[j + 1] - bounds[j]
+            if time.perf_counter() - t0 > budget_s:
+                break
+        t_tree = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        ops = O.make_ops(trees, np.ones((1, 1)), 1, len(seg.slot_starts))
+        O.select_heap(ops, max(1, toks // int(sh.x)))
+        t_sel = time.perf_counter() - t0
+    per_tok = t_seg / (nseg * sh.L * sh.G) + t_rel / sh.N_ctx + (t_tree + t_sel) / toks
+    return dict(value=1.0 / per_tok, unit="compressed context tokens/s", cores=1, kind="oracle",
+                sample=(f"1 thread; segmentation of a {nseg}-token window ({t_seg:.1f} s, shared by L*G heads); "
+                        f"relevance of (l,g)=(0,0) over {sh.T} positions ({t_rel:.1f} s); trees + auction of "
+                        f"{toks} tokens of that head ({t_tree + t_sel:.1f} s)"))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; the multi-GPU layout is described in DESIGN.md",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2608_07001_amd import gracekv as gk
+    from synth.workloads import CONFIGS, make_case
+    sh = CONFIGS[args.config]
+    if args.x is not None:
+        sh = sh.with_(x=args.x)
+    dev = "cuda"
+    case = make_case(sh, args.seed, device=dev)
+    cfg = gk.config_for(L=sh.L, G=sh.G, H=sh.H, d=sh.d, W=sh.W, N_ctx=sh.N_ctx, x=sh.x,
+                        dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D)
+    buf = gk.allocate(cfg, dev)
+    p = buf.plan
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record(stream)
+        mark(0)
+        gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
+                   buf.seg_ws, stream)
+        mark(1)
+        gk.build_trees(cfg, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
+                       buf.n_slots, buf.kappa, buf.trees, stream)
+        mark(2)
+        gk.score(cfg, case["omega_raw"], buf.trees, stream)
+        mark(3)
+        gk.select(cfg, buf.trees, buf.b_used, buf.sel_ws, stream)
+        mark(4)
+        gk.pack(cfg, case["K"], case["V"], case["rope_cos"], case["rope_sin"], buf.trees, buf.offsets,
+                buf.counts, buf.K_out, buf.V_out, buf.pos_out, buf.logm_out, buf.pack_ws, stream)
+        mark(5)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    gk.check(cfg, buf.trees, stream)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    names = ["segment", "build", "score", "select", "pack"]
+    stage_ms = {n: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)) / args.steps
+                for i, n in enumerate(names)}
+    ms = sum(evs[s][0].elapsed_time(evs[s][5]) for s in range(args.steps)) / args.steps
+    tokens = sh.L * sh.G * sh.N_ctx
+    b = 2 if sh.dtype == "bf16" else 4
+    ab = algorithmic_bytes(sh, p, b)
+    build_gbs = ab["build"] / (stage_ms["build"] * 1e-3) / 1e9
+    res = {
+        "metric": "compressed context tokens/sec (layers x KV-heads x tokens)",
+        "value": tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": sh.dtype, "data": "synthetic (seeded Llama-shaped cache, see DESIGN.md)",
+        "config": {"workload": f"{sh.name}: L={sh.L} G={sh.G} H={sh.H} d={sh.d} N_ctx={sh.N_ctx} W={sh.W} "
+                               f"x={sh.x:g} ({sh.dtype})",
+                   "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item())},
+        "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "stages_ms": stage_ms,
+        "wall_s": wall,
+        "roofline": {"kernel": "gracekv_build_trees (k_rowstats + k_build)", "bound": "hbm",
+                     "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": build_gbs / HBM_PEAK_GBS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,193 @@
+/*
+ * gracekv.h -- C ABI of the MI355X (gfx950) implementation of GraceKV's
+ * one-shot, post-prefill KV-cache compression (arXiv 2608.07001).
+ *
+ * The path has five calls, run in this order on one HIP stream:
+ *   gracekv_segment      curvature-guided slot partition      (App. B.2-B.3)
+ *   gracekv_build_trees  direct relevance + prototype trees    (App. A.3-A.4)
+ *   gracekv_score        Add / Split gains, utilities, keys    (App. A.5 eq:app_operation_gains..eq:app_unit_utility)
+ *   gracekv_select       global budgeted greedy auction        (App. A.5 Stage II, App. C.3)
+ *   gracekv_pack         ragged compressed cache               (App. A.5 "Frontier updates and physical packing")
+ *
+ * Conventions shared by every call
+ *   - Positions are absolute.  The sequence is the context [0, N_ctx) followed
+ *     by a question suffix of W tokens [N_ctx, T), T = N_ctx + W (no prompt
+ *     prefix, c_s = 0).  The W window queries sit at the suffix positions and
+ *     are both the direct-relevance probes and the distortion probes.
+ *   - The recent window r and the budgets follow eq:app_total_budget,
+ *     eq:app_compressible_context and eq:app_free_budget with the singleton
+ *     floor disabled (alpha = 0) and lambda_graph = 0 (the paper's "w/o SF"
+ *     and "w/o MH" settings).  Compressible context C = [0, N_c), N_c = N_ctx - r.
+ *   - Every pointer argument except `cfg`, `plan` and host-side outputs is a
+ *     DEVICE pointer owned by the caller; the library never allocates, frees or
+ *     synchronises device memory (gracekv_plan reports every size).  All device
+ *     buffers must be 16-byte aligned.
+ *   - `stream` is a hipStream_t passed as void*; kernels are only enqueued.
+ *   - Layouts are row-major:  K, V [L][G][T][d];  Q [L][H][W][d];
+ *     hidden [n_seg][T][D_hidden];  rope_cos/rope_sin [T][d/2] fp32 (rotate-half
+ *     RoPE: the pair (i, i + d/2) turns by the table's angle);  K/V/Q/hidden are
+ *     all of cfg->dtype.  Query head h belongs to KV head h / (H/G).
+ *   - Errors: argument errors are detected on the host before anything is
+ *     enqueued and return GRACEKV_ERR_INVALID_ARG / _UNSUPPORTED / _BUDGET /
+ *     _WORKSPACE.  A failed launch returns GRACEKV_ERR_HIP.  Numeric faults
+ *     found on the device (NaN gains, capacity overflow) are latched in the
+ *     status word inside the tree buffer and returned by gracekv_check.
+ */
+#ifndef GRACEKV_H
+#define GRACEKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GRACEKV_OK = 0,
+  GRACEKV_ERR_INVALID_ARG = -1,
+  GRACEKV_ERR_UNSUPPORTED = -2,
+  GRACEKV_ERR_BUDGET = -3,
+  GRACEKV_ERR_WORKSPACE = -4,
+  GRACEKV_ERR_HIP = -5,
+  GRACEKV_ERR_NUMERIC = -6
+} gracekv_status;
+
+typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
+
+/* Shapes and hyperparameters.  gracekv_default_config fills the paper's
+ * defaults (App. A and B); the caller then sets the shape fields. */
+typedef struct {
+  int32_t L, G, H, d;      /* layers, KV heads, query heads, head dim (d even, <= 128) */
+  int32_t n_seg;           /* hidden-state slabs (|L_seg|, eq:app_seg_layers), 1..8 */
+  int32_t D_hidden;        /* hidden size of each slab */
+  int32_t W;               /* window queries (1..64) */
+  int32_t dtype;           /* gracekv_dtype of K, V, Q and hidden */
+  int64_t N_ctx;           /* context length */
+  double x;                /* compression ratio x >= 1 (eq:app_total_budget) */
+  int32_t r_default, r_min;                  /* recent window 32, minimum 4 (App. A.1) */
+  float lam_stab, lam_s, eps_seg, mad_factor; /* 0.25, 0.15, 1e-6, 1.4826 (App. B.2) */
+  int32_t win[3];                            /* curvature windows {4, 8, 16} */
+  int32_t n_min, n_max, n0;                  /* 16, 128, 64 (eq:app_slot_length_defaults) */
+  float lam_d, lam_n, c_cut;                 /* 0.25, 0.10, 1.0 (eq:app_segmentation_defaults) */
+  float lam_Z, lam_M;                        /* 0.25, 0.75 (eq:app_probe_distortion) */
+  int32_t k_curv;                            /* 16 curvature split candidates */
+  float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
+  float lambda_graph, alpha_floor;           /* must be 0 on this path */
+} gracekv_config;
+
+/* Sizes derived from a config (host only). */
+typedef struct {
+  int64_t T, N_c, B_total, B_free;
+  int32_t r;
+  int32_t J_cap;           /* slot capacity floor(N_c / n_min) + 1 */
+  int64_t unit_cap;        /* L * G * J_cap */
+  int64_t node_cap;        /* L * G * 2 * N_c node-table entries */
+  size_t seg_ws_bytes;     /* workspace of gracekv_segment */
+  size_t tree_bytes;       /* the tree buffer shared by build/score/select/pack */
+  size_t sel_ws_bytes;     /* workspace of gracekv_select */
+  size_t pack_ws_bytes;    /* workspace of gracekv_pack */
+  /* byte offsets of the tree buffer's arrays (see gracekv_build_trees) */
+  size_t off_node_a, off_node_n, off_node_child, off_node_parent, off_node_nch,
+         off_node_kind, off_node_cut, off_node_D, off_node_R,
+         off_sp_U, off_sp_E, off_sp_cost, off_sp_exec,
+         off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
+         off_tok_R, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
+         off_omega, off_status, off_slots, off_nslots, off_partial;
+  int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
+} gracekv_plan;
+
+/* Paper defaults (App. A, App. B): see the field comments above. */
+gracekv_status gracekv_default_config(gracekv_config* cfg);
+
+/* Validates cfg and fills plan.  Returns GRACEKV_ERR_BUDGET when the budget
+ * cannot hold a recent window of r_min entries per (layer, KV head)
+ * (App. A.1), GRACEKV_ERR_UNSUPPORTED for lambda_graph != 0 or
+ * alpha_floor != 0 or shapes outside the documented limits. */
+gracekv_status gracekv_plan_sizes(const gracekv_config* cfg, gracekv_plan* plan);
+
+/* Human-readable name of a status. */
+const char* gracekv_status_string(gracekv_status s);
+
+/* Synchronises `stream` and returns the device status word latched in the
+ * tree buffer (GRACEKV_OK, GRACEKV_ERR_NUMERIC). */
+gracekv_status gracekv_check(const gracekv_config* cfg, void* trees, void* stream);
+
+/* Curvature-guided slot segmentation (App. B.2 eq:app_hidden_normalization ..
+ * eq:app_boundary_score; App. B.3 eq:app_adjacent_difference ..
+ * eq:app_terminal_predecessor).
+ *   hidden     [n_seg][T][D_hidden] (cfg->dtype), the slabs at the segmentation depths
+ *   surprisal  [T] fp32, surprisal of each token (position 0 holds 0)
+ *   kappa      [T] fp32 out: stabilized curvature (eq:app_stabilized_curvature)
+ *   bscore     [T] fp32 out: boundary score b_i (eq:app_boundary_score)
+ *   slot_starts [J_cap + 1] int32 out: slot starts a_1 = 0 < ... < a_J, then N_c
+ *   n_slots    [1] int32 out: J
+ *   ws         workspace of plan.seg_ws_bytes bytes */
+gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, const float* surprisal,
+                               float* kappa, float* bscore, int32_t* slot_starts, int32_t* n_slots,
+                               void* ws, size_t ws_bytes, void* stream);
+
+/* Direct relevance and one prototype tree per (layer, KV head, slot) unit
+ * (App. A.3 eq:app_rope_prototype .. eq:app_split_choice; App. A.4
+ * eq:app_attention_probability, eq:app_direct_relevance, eq:app_bottom_up_value;
+ * App. B.4 eq:app_tree_split_candidates).
+ *   K, V       [L][G][T][d], Q [L][H][W][d] (cfg->dtype)
+ *   rope_cos/rope_sin [T][d/2] fp32
+ *   slot_starts, n_slots, kappa: outputs of gracekv_segment (or caller-made)
+ *   trees      the tree buffer (plan.tree_bytes).  Unit u = (l*G + g)*J_cap + j
+ *              owns node slots [(l*G+g)*2*N_c + 2*a_j, ... + 2*n_j); nodes are in
+ *              BFS order (root first; children of a node are contiguous, left to
+ *              right).  Node arrays: start (int32, absolute), length (int32),
+ *              first child (int32 local index, -1 for a leaf), parent (int32 local,
+ *              -1 for the root), #children (uint8), kind (uint8: 0 leaf, 1 binary,
+ *              2 extraction), cut (int32: xi or the extracted token), D and R (fp32).
+ *              Per unit: node count (int32), D_drop of the root (fp32).  Token
+ *              values R^tok [L*G][N_c] fp32; per (l,g) row statistics of the
+ *              relevance softmax and the probe shifts m_q and Z_q(C); a copy of
+ *              the slot partition (read by score, select and pack).
+ *   ws         unused (pass NULL, 0); reserved. */
+gracekv_status gracekv_build_trees(const gracekv_config* cfg, const void* K, const void* V, const void* Q,
+                                   const float* rope_cos, const float* rope_sin,
+                                   const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
+                                   void* trees, void* ws, size_t ws_bytes, void* stream);
+
+/* Gains, utilities and priority keys (App. A.5 eq:app_operation_gains,
+ * eq:app_operation_costs, eq:app_unit_utility; eq:app_head_sensitivity).
+ *   omega_raw  [L][G] fp32 raw sensitivity, or NULL for all ones.
+ * For every op: Delta+ = max(Delta, 0), U = Delta+ / c, composite key
+ * k = (bits(U) << 32) | (2^32 - 1 - id) with id = unit ordinal * 256 + local
+ * index (Add 0, Split(node i) 1 + i) and unit ordinal (l*G + g)*J + j, and the
+ * effective key E = min(k, E(parent op)). */
+gracekv_status gracekv_score(const gracekv_config* cfg, const float* omega_raw, void* trees, void* stream);
+
+/* The budgeted greedy auction of App. A.5 / App. C.3, computed exactly: a
+ * cost-weighted radix select over E finds the cut; ops above it execute, the
+ * single group at the cut is resolved by the literal queue rule, and a
+ * remaining single budget unit buys the best available cost-1 op.
+ *   b_used     [1] int64 out: budget spent by the auction
+ *   ws         workspace of plan.sel_ws_bytes bytes */
+gracekv_status gracekv_select(const gracekv_config* cfg, void* trees, int64_t* b_used, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* Ragged compressed cache (App. A.5 "Frontier updates and physical packing").
+ * Per (l, g), in ascending position: every frontier node (singleton: original
+ * K/V, its position, log m = 0; other: prototype k~, v~ rounded to cfg->dtype,
+ * representative position p_v, log m_eff), then the r recent-window tokens.
+ *   offsets    [L*G + 1] int64 out (CSR), counts [L*G] int64 out
+ *   K_out, V_out [B_total][d] (cfg->dtype), pos_out [B_total] int32,
+ *   logm_out [B_total] fp32
+ *   ws         workspace of plan.pack_ws_bytes bytes */
+gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void* V,
+                            const float* rope_cos, const float* rope_sin, void* trees,
+                            int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
+                            int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Layout check of the matrix-core instructions used by the kernels: computes
+ * a 16x16 product with the bf16 (which = 1) or fp32 (which = 0) MFMA path
+ * from fixed inputs and copies it to host_out[256] (synchronous). */
+gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GRACEKV_H */

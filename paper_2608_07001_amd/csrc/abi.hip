@@ -1,0 +1,274 @@
+// Host side of the C ABI: defaults, size planning, argument validation and
+// the five entry points.  Every entry point validates on the host and only
+// enqueues kernels on the caller's stream.
+#include <math.h>
+#include <string.h>
+
+#include "common.h"
+
+using namespace gkv;
+
+namespace gkv {
+
+static size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
+  Dims d;
+  memset(&d, 0, sizeof(d));
+  d.L = c.L; d.G = c.G; d.H = c.H; d.d = c.d; d.hpg = c.H / c.G; d.W = c.W; d.n_seg = c.n_seg;
+  d.Dh = c.D_hidden; d.dtype = c.dtype; d.r = p.r; d.J_cap = p.J_cap;
+  d.T = p.T; d.N_ctx = c.N_ctx; d.N_c = p.N_c; d.B_total = p.B_total; d.B_free = p.B_free;
+  d.lam_stab = c.lam_stab; d.lam_s = c.lam_s; d.eps_seg = c.eps_seg; d.mad = c.mad_factor;
+  d.win[0] = c.win[0]; d.win[1] = c.win[1]; d.win[2] = c.win[2];
+  d.n_min = c.n_min; d.n_max = c.n_max; d.n0 = c.n0;
+  d.lam_d = c.lam_d; d.lam_n = c.lam_n; d.c_cut = c.c_cut;
+  d.lam_Z = c.lam_Z; d.lam_M = c.lam_M; d.lam_kappa = c.lam_kappa; d.beta_frac = c.beta_frac; d.eps = c.eps;
+  d.k_curv = c.k_curv;
+  d.rows = d.hpg * c.W;
+  return d;
+}
+
+TreeView make_view(void* base, const gracekv_plan& p) {
+  char* b = (char*)base;
+  TreeView v;
+  v.node_a = (int32_t*)(b + p.off_node_a);
+  v.node_n = (int32_t*)(b + p.off_node_n);
+  v.node_child = (int32_t*)(b + p.off_node_child);
+  v.node_parent = (int32_t*)(b + p.off_node_parent);
+  v.node_nch = (uint8_t*)(b + p.off_node_nch);
+  v.node_kind = (uint8_t*)(b + p.off_node_kind);
+  v.node_cut = (int32_t*)(b + p.off_node_cut);
+  v.node_D = (float*)(b + p.off_node_D);
+  v.node_R = (float*)(b + p.off_node_R);
+  v.sp_U = (float*)(b + p.off_sp_U);
+  v.sp_E = (uint64_t*)(b + p.off_sp_E);
+  v.sp_cost = (uint8_t*)(b + p.off_sp_cost);
+  v.sp_exec = (uint8_t*)(b + p.off_sp_exec);
+  v.unit_nn = (int32_t*)(b + p.off_unit_nn);
+  v.unit_Ddrop = (float*)(b + p.off_unit_Ddrop);
+  v.add_U = (float*)(b + p.off_add_U);
+  v.add_E = (uint64_t*)(b + p.off_add_E);
+  v.add_exec = (uint8_t*)(b + p.off_add_exec);
+  v.tok_R = (float*)(b + p.off_tok_R);
+  v.row_stats = (float4*)(b + p.off_row_stats);
+  v.probe_m = (float*)(b + p.off_probe_m);
+  v.probe_ZC = (float*)(b + p.off_probe_ZC);
+  v.lg_S = (float*)(b + p.off_lg_S);
+  v.omega = (float*)(b + p.off_omega);
+  v.status = (int32_t*)(b + p.off_status);
+  v.slots = (int32_t*)(b + p.off_slots);
+  v.nslots = (int32_t*)(b + p.off_nslots);
+  return v;
+}
+
+__global__ void k_copy_slots(const int32_t* __restrict__ slot_starts, const int32_t* __restrict__ n_slots, int J_cap,
+                             TreeView tv) {
+  for (int i = threadIdx.x; i <= J_cap; i += blockDim.x) tv.slots[i] = slot_starts[i];
+  if (threadIdx.x == 0) { *tv.nslots = *n_slots; *tv.status = 0; }
+}
+
+}  // namespace gkv
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+extern "C" {
+
+gracekv_status gracekv_default_config(gracekv_config* c) {
+  if (!c) return GRACEKV_ERR_INVALID_ARG;
+  memset(c, 0, sizeof(*c));
+  c->n_seg = 3;
+  c->dtype = GRACEKV_BF16;
+  c->x = 1.0;
+  c->r_default = 32; c->r_min = 4;
+  c->lam_stab = 0.25f; c->lam_s = 0.15f; c->eps_seg = 1e-6f; c->mad_factor = 1.4826f;
+  c->win[0] = 4; c->win[1] = 8; c->win[2] = 16;
+  c->n_min = 16; c->n_max = 128; c->n0 = 64;
+  c->lam_d = 0.25f; c->lam_n = 0.10f; c->c_cut = 1.0f;
+  c->lam_Z = 0.25f; c->lam_M = 0.75f;
+  c->k_curv = 16;
+  c->lam_kappa = 0.05f; c->beta_frac = 0.1f; c->eps = 1e-6f;
+  c->lambda_graph = 0.f; c->alpha_floor = 0.f;
+  return GRACEKV_OK;
+}
+
+const char* gracekv_status_string(gracekv_status s) {
+  switch (s) {
+    case GRACEKV_OK: return "ok";
+    case GRACEKV_ERR_INVALID_ARG: return "invalid argument";
+    case GRACEKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case GRACEKV_ERR_BUDGET: return "budget cannot hold the minimum recent window";
+    case GRACEKV_ERR_WORKSPACE: return "workspace too small";
+    case GRACEKV_ERR_HIP: return "HIP error";
+    case GRACEKV_ERR_NUMERIC: return "non-finite gain on the device";
+  }
+  return "unknown status";
+}
+
+gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
+  if (!c || !p) return GRACEKV_ERR_INVALID_ARG;
+  memset(p, 0, sizeof(*p));
+  if (c->L < 1 || c->G < 1 || c->H < 1 || c->d < 2 || c->W < 1 || c->N_ctx < 1 || c->n_seg < 1 || c->D_hidden < 1)
+    return GRACEKV_ERR_INVALID_ARG;
+  if (c->H % c->G != 0) return GRACEKV_ERR_INVALID_ARG;
+  if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
+  if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
+  if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->W > WMAX || c->n_seg > 8) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->n_min < 16 || c->n_max > NMAX || c->n_max < c->n_min || c->n0 < 1) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->win[0] != 4 || c->win[1] != 8 || c->win[2] != 16) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->k_curv < 1 || c->k_curv > CAND_MAX - 2) return GRACEKV_ERR_UNSUPPORTED;
+  const int64_t T = c->N_ctx + c->W;
+  if (T > (int64_t)0x7fffffff / 2) return GRACEKV_ERR_UNSUPPORTED;
+  const int64_t LG = (int64_t)c->L * c->G;
+  const int64_t B_total = (int64_t)floor((double)LG * (double)c->N_ctx / c->x);
+  int64_t r = c->r_default;
+  if (LG * r > B_total) r = B_total / LG;
+  if (r > c->N_ctx) r = c->N_ctx;
+  if (r < c->r_min) return GRACEKV_ERR_BUDGET;
+  p->T = T;
+  p->r = (int32_t)r;
+  p->N_c = c->N_ctx - r;
+  p->B_total = B_total;
+  p->B_free = B_total - LG * r;
+  p->J_cap = (int32_t)(p->N_c / c->n_min + 1);
+  p->unit_cap = LG * p->J_cap;
+  p->node_cap = LG * 2 * p->N_c;
+  gracekv_plan tmp = *p;
+  Dims dm = make_dims(*c, tmp);
+  p->build_lds_bytes = build_lds_bytes(dm);
+  if (p->build_lds_bytes > 160 * 1024) return GRACEKV_ERR_UNSUPPORTED;
+  const size_t NC = (size_t)p->node_cap, UC = (size_t)p->unit_cap;
+  size_t o = 0;
+  auto put = [&](size_t& off, size_t bytes) { off = o; o = al256(o + bytes); };
+  put(p->off_sp_E, NC * 8);
+  put(p->off_add_E, UC * 8);
+  put(p->off_node_a, NC * 4);
+  put(p->off_node_n, NC * 4);
+  put(p->off_node_child, NC * 4);
+  put(p->off_node_parent, NC * 4);
+  put(p->off_node_cut, NC * 4);
+  put(p->off_node_D, NC * 4);
+  put(p->off_node_R, NC * 4);
+  put(p->off_sp_U, NC * 4);
+  put(p->off_node_nch, NC);
+  put(p->off_node_kind, NC);
+  put(p->off_sp_cost, NC);
+  put(p->off_sp_exec, NC);
+  put(p->off_unit_nn, UC * 4);
+  put(p->off_unit_Ddrop, UC * 4);
+  put(p->off_add_U, UC * 4);
+  put(p->off_add_exec, UC);
+  put(p->off_tok_R, (size_t)LG * p->N_c * 4);
+  put(p->off_row_stats, (size_t)LG * dm.rows * 16);
+  put(p->off_probe_m, (size_t)LG * c->W * 4);
+  put(p->off_probe_ZC, (size_t)LG * c->W * 4);
+  put(p->off_lg_S, (size_t)LG * 4);
+  put(p->off_omega, (size_t)LG * 4);
+  put(p->off_status, 16);
+  put(p->off_slots, (size_t)(p->J_cap + 1) * 4);
+  put(p->off_nslots, 16);
+  put(p->off_partial, (size_t)LG * rowstats_chunks(dm) * dm.rows * 16);
+  p->tree_bytes = o;
+  p->seg_ws_bytes = segment_ws_bytes(dm);
+  p->sel_ws_bytes = select_ws_bytes(dm);
+  p->pack_ws_bytes = pack_ws_bytes(dm);
+  return GRACEKV_OK;
+}
+
+static gracekv_status prep(const gracekv_config* c, gracekv_plan* p) {
+  if (!c) return GRACEKV_ERR_INVALID_ARG;
+  return gracekv_plan_sizes(c, p);
+}
+
+static gracekv_status hip_status(hipError_t e) { return e == hipSuccess ? GRACEKV_OK : GRACEKV_ERR_HIP; }
+
+gracekv_status gracekv_check(const gracekv_config* c, void* trees, void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!trees) return GRACEKV_ERR_INVALID_ARG;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return GRACEKV_ERR_HIP;
+  int32_t st = 0;
+  if (hipMemcpy(&st, (char*)trees + p.off_status, 4, hipMemcpyDeviceToHost) != hipSuccess) return GRACEKV_ERR_HIP;
+  return st ? GRACEKV_ERR_NUMERIC : GRACEKV_OK;
+}
+
+gracekv_status gracekv_segment(const gracekv_config* c, const void* hidden, const float* surprisal, float* kappa,
+                               float* bscore, int32_t* slot_starts, int32_t* n_slots, void* ws, size_t ws_bytes,
+                               void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!hidden || !surprisal || !kappa || !bscore || !slot_starts || !n_slots || !ws) return GRACEKV_ERR_INVALID_ARG;
+  if (!aligned16(hidden) || !aligned16(ws)) return GRACEKV_ERR_INVALID_ARG;
+  if (ws_bytes < p.seg_ws_bytes) return GRACEKV_ERR_WORKSPACE;
+  Dims dm = make_dims(*c, p);
+  return hip_status(launch_segment(dm, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, (hipStream_t)stream));
+}
+
+gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const void* V, const void* Q,
+                                   const float* rope_cos, const float* rope_sin, const int32_t* slot_starts,
+                                   const int32_t* n_slots, const float* kappa, void* trees, void* ws, size_t ws_bytes,
+                                   void* stream) {
+  (void)ws; (void)ws_bytes;
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!K || !V || !Q || !rope_cos || !rope_sin || !slot_starts || !n_slots || !kappa || !trees)
+    return GRACEKV_ERR_INVALID_ARG;
+  if (!aligned16(K) || !aligned16(V) || !aligned16(Q) || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
+  Dims dm = make_dims(*c, p);
+  TreeView tv = make_view(trees, p);
+  hipStream_t st = (hipStream_t)stream;
+  hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  e = launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st);
+  if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  return hip_status(launch_build(dm, p.build_lds_bytes, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st));
+}
+
+gracekv_status gracekv_score(const gracekv_config* c, const float* omega_raw, void* trees, void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!trees || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
+  Dims dm = make_dims(*c, p);
+  return hip_status(launch_score(dm, omega_raw, make_view(trees, p), (hipStream_t)stream));
+}
+
+gracekv_status gracekv_select(const gracekv_config* c, void* trees, int64_t* b_used, void* ws, size_t ws_bytes,
+                              void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!trees || !b_used || !ws || !aligned16(trees) || !aligned16(ws)) return GRACEKV_ERR_INVALID_ARG;
+  if (ws_bytes < p.sel_ws_bytes) return GRACEKV_ERR_WORKSPACE;
+  Dims dm = make_dims(*c, p);
+  return hip_status(launch_select(dm, make_view(trees, p), b_used, ws, (hipStream_t)stream));
+}
+
+gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* V, const float* rope_cos,
+                            const float* rope_sin, void* trees, int64_t* offsets, int64_t* counts, void* K_out,
+                            void* V_out, int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!K || !V || !rope_cos || !rope_sin || !trees || !offsets || !counts || !K_out || !V_out || !pos_out ||
+      !logm_out || !ws)
+    return GRACEKV_ERR_INVALID_ARG;
+  if (!aligned16(K) || !aligned16(V) || !aligned16(trees) || !aligned16(ws) || !aligned16(K_out) || !aligned16(V_out))
+    return GRACEKV_ERR_INVALID_ARG;
+  if (ws_bytes < p.pack_ws_bytes) return GRACEKV_ERR_WORKSPACE;
+  Dims dm = make_dims(*c, p);
+  return hip_status(launch_pack(dm, K, V, rope_cos, rope_sin, make_view(trees, p), offsets, counts, K_out, V_out,
+                                pos_out, logm_out, ws, (hipStream_t)stream));
+}
+
+gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out) {
+  if (!host_out || (which != 0 && which != 1)) return GRACEKV_ERR_INVALID_ARG;
+  return hip_status(selftest_mfma(which, host_out));
+}
+
+}  // extern "C"

@@ -1,0 +1,611 @@
+// Prototype-tree construction, one workgroup per (layer, KV head, slot) unit.
+//
+// Implements App. A.3 (RoPE-consistent key prototype eq:app_rope_prototype,
+// value prototype eq:app_value_prototype, effective multiplicity
+// eq:app_effective_multiplicity, distortion eq:app_original_attention_stats ..
+// eq:app_node_and_drop_distortion, recursive refinement eq:app_binary_split ..
+// eq:app_split_choice) and pass 2 of the direct relevance (App. A.4
+// eq:app_attention_probability, eq:app_direct_relevance) with lambda_graph = 0,
+// so R^tok = s-hat (eq:app_bottom_up_value).
+//
+// Per unit (n <= 128 tokens):
+//   1. K and V tiles go to LDS; MFMA forms the logits of every relevance row
+//      (query head x window position) against the unit's keys.  With the row
+//      statistics of pass 1 they give pi, s_t and R^tok; probe rows also give
+//      e_{q,t} = exp(l_{q,t} - m_q) (kept in LDS, fp32).
+//   2. The tree is refined top-down in BFS order.  For node [a, b) the binary
+//      cuts (top-16 curvature positions t -> cut t+1, plus the midpoint) and the
+//      extraction token p define children that are all prefixes [a, x) or
+//      suffixes [x, b) of the node.  One left-to-right sweep evaluates every
+//      prefix child and one right-to-left sweep every suffix child: running
+//      sums of k°, R v, v, R, ||k||, and per probe of e and e v, are read off
+//      at each cut.  A probe's D_q needs only these sums and the child's
+//      prototype, so each child costs O(W d) once the sweep has passed it.
+//   3. Scores are compared in fp32 (binary form wins ties, smaller cut wins
+//      ties), children are appended, and the node table is written out.
+#include "common.h"
+
+namespace gkv {
+
+constexpr int BT = 256;          // threads per unit
+constexpr int TPQ = 4;           // threads per probe in the probe sweep
+
+template <typename T> struct BPad;
+template <> struct BPad<uint16_t> { static constexpr int v = 4; };
+template <> struct BPad<float> { static constexpr int v = 1; };
+
+template <typename T, int D>
+struct BuildLds {
+  static constexpr int LDK = D + BPad<T>::v;
+  // byte offsets inside dynamic LDS
+  static constexpr int oK = 0;
+  static constexpr int oV = oK + NMAX * LDK * (int)sizeof(T);
+  static constexpr int oE = ((oV + NMAX * D * (int)sizeof(T)) + 15) & ~15;
+  static constexpr int oR = oE + WMAX * NMAX * 4;
+  static constexpr int oKap = oR + NMAX * 4;
+  static constexpr int oA = oKap + NMAX * 4;
+  static constexpr int oKn = oA + NMAX * 4;
+  static constexpr int oS = oKn + NMAX * 4;                   // relevance partials [4][NMAX]
+  static constexpr int oNa = oS + 4 * NMAX * 4;
+  static constexpr int oNn = oNa + 256 * 4;
+  static constexpr int oNc = oNn + 256 * 4;
+  static constexpr int oNp = oNc + 256 * 4;
+  static constexpr int oNch = oNp + 256 * 4;
+  static constexpr int oNk = oNch + 256 * 4;
+  static constexpr int oNcut = oNk + 256 * 4;
+  static constexpr int oND = oNcut + 256 * 4;
+  static constexpr int oNR = oND + 256 * 4;
+  static constexpr int oCk = oNR + 256 * 4;                  // child mean k° / k~  [CAND_MAX][D]
+  static constexpr int oCv = oCk + CAND_MAX * D * 4;          // child v~           [CAND_MAX][D]
+  static constexpr int oCon = oCv + CAND_MAX * D * 4;         // contrib [CAND_MAX][WMAX]
+  static constexpr int oCs = oCon + CAND_MAX * WMAX * 4;      // child scalars [8][CAND_MAX]
+  static constexpr int oX = oCs + 8 * CAND_MAX * 4;           // cut lists and misc ints
+  static constexpr int oFlag = oX + 4 * 64 * 4;
+  static constexpr int bytes = oFlag + NMAX * 4;
+};
+
+int build_lds_bytes(const Dims& dm) {
+  if (dm.dtype == GRACEKV_BF16) return dm.d == 128 ? BuildLds<uint16_t, 128>::bytes : BuildLds<uint16_t, 64>::bytes;
+  return dm.d == 128 ? BuildLds<float, 128>::bytes : BuildLds<float, 64>::bytes;
+}
+
+__device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
+  // round((x0 + ... + x1-1) / n) = round((x0 + x1 - 1) / 2), ties to even
+  int s = x0 + x1 - 1;
+  if ((s & 1) == 0) return s >> 1;
+  int h = s >> 1;
+  return (h & 1) ? h + 1 : h;
+}
+
+// Child scalar slots (oCs): 0 n, 1 sumR, 2 mean||k°||, 3 m_eff, 4 p, 5 D, 6 x (cut)
+template <typename T, int D>
+struct Unit {
+  using Lay = BuildLds<T, D>;
+  char* s;
+  T* sK; T* sV; float* sE; float* sR; float* sKap; float* sA; float* sKn; float* sS;
+  int* na; int* nn; int* nc; int* np; int* nch; int* nk; int* ncut; float* nD; float* nR;
+  float* ck; float* cv; float* con; float* cs; int* xi; int* flag;
+  __device__ Unit(char* base) : s(base) {
+    sK = (T*)(s + Lay::oK); sV = (T*)(s + Lay::oV); sE = (float*)(s + Lay::oE); sR = (float*)(s + Lay::oR);
+    sKap = (float*)(s + Lay::oKap); sA = (float*)(s + Lay::oA); sKn = (float*)(s + Lay::oKn); sS = (float*)(s + Lay::oS);
+    na = (int*)(s + Lay::oNa); nn = (int*)(s + Lay::oNn); nc = (int*)(s + Lay::oNc); np = (int*)(s + Lay::oNp);
+    nch = (int*)(s + Lay::oNch); nk = (int*)(s + Lay::oNk); ncut = (int*)(s + Lay::oNcut);
+    nD = (float*)(s + Lay::oND); nR = (float*)(s + Lay::oNR);
+    ck = (float*)(s + Lay::oCk); cv = (float*)(s + Lay::oCv); con = (float*)(s + Lay::oCon);
+    cs = (float*)(s + Lay::oCs); xi = (int*)(s + Lay::oX); flag = (int*)(s + Lay::oFlag);
+  }
+};
+
+// Evaluate the children [a, xs[c]) (prefix) or [xs[c], b) (suffix) of a node
+// whose local token range is [a, b) (0-based inside the unit, absolute start a0).
+// Writes per child: n, sumR, D into cs[] rows 0, 1, 5.  `want_drop` is unused.
+template <typename T, int D>
+__device__ void sweep(Unit<T, D>& U, const Dims& dm, bool prefix, int a, int b, const int* xs, int nx, int64_t a0,
+                      const float* __restrict__ cosT, const float* __restrict__ sinT, const float* qv, float m_q,
+                      float zc_q, int q, float scale) {
+  using Lay = BuildLds<T, D>;
+  constexpr int H2 = D / 2;
+  constexpr int DPT = D / TPQ;
+  const int tid = threadIdx.x;
+  float* cn = U.cs + 0 * CAND_MAX;
+  float* cR = U.cs + 1 * CAND_MAX;
+  float* cKm = U.cs + 2 * CAND_MAX;
+  float* cMe = U.cs + 3 * CAND_MAX;
+  float* cP = U.cs + 4 * CAND_MAX;
+  float* cD = U.cs + 5 * CAND_MAX;
+  // ---- phase A: prototype sums (thread per dimension) ----
+  if (tid < D) {
+    const int i = tid;
+    const int ih = i < H2 ? i : i - H2;
+    const int ip = i < H2 ? i + H2 : i - H2;
+    float sk = 0.f, srv = 0.f, sv = 0.f, sr = 0.f, skn = 0.f;
+    int ci = prefix ? 0 : nx - 1;
+    const int t_first = prefix ? a : b - 1;
+    const int t_last = prefix ? xs[nx - 1] - 1 : xs[0];
+    const int step = prefix ? 1 : -1;
+    const int steps = prefix ? t_last - t_first + 1 : t_first - t_last + 1;
+    for (int it = 0, t = t_first; it < steps && it < NMAX; ++it, t += step) {
+      const int64_t ta = a0 + t;
+      const float c = cosT[ta * H2 + ih], sn = sinT[ta * H2 + ih];
+      const float x = ldf(U.sK, t * Lay::LDK + i), y = ldf(U.sK, t * Lay::LDK + ip);
+      const float kr = i < H2 ? x * c + y * sn : x * c - y * sn;
+      const float v = ldf(U.sV, t * D + i);
+      const float r = U.sR[t];
+      sk += kr;
+      srv += r * v;
+      sv += v;
+      sr += r;
+      skn += U.sKn[t];
+      const bool at = prefix ? (t + 1 == xs[ci]) : (t == xs[ci]);
+      if (at) {
+        const int nch_ = prefix ? xs[ci] - a : b - xs[ci];
+        if (nch_ >= 2) {
+          const float inv = 1.0f / (float)nch_;
+          U.ck[ci * D + i] = sk * inv;
+          const float beta = dm.beta_frac * sr * inv;
+          U.cv[ci * D + i] = (srv + beta * sv) / (sr + (float)nch_ * beta + dm.eps);
+        }
+        if (i == 0) {
+          cn[ci] = (float)nch_;
+          cR[ci] = sr;
+          cKm[ci] = skn / (float)nch_;
+        }
+        ci += prefix ? 1 : -1;
+        if (ci < 0 || ci >= nx) break;
+      }
+    }
+  }
+  __syncthreads();
+  // ---- phase A2: coherence, multiplicity, representative position, RoPE(k) ----
+  {
+    const int wave = tid >> 6, lane = tid & 63;
+    for (int c = wave; c < nx; c += BT / 64) {
+      const int nch_ = (int)cn[c];
+      if (nch_ < 2) continue;
+      float ss = 0.f;
+      for (int i = lane; i < D; i += 64) ss += U.ck[c * D + i] * U.ck[c * D + i];
+      ss = wave_sum(ss);
+      const int x0 = prefix ? a : xs[c];
+      const int x1 = prefix ? xs[c] : b;
+      const int p = round_half_even_mid((int)(a0 + x0), (int)(a0 + x1));
+      float coh = sqrtf(ss) / (cKm[c] + dm.eps);
+      float me = fminf(fmaxf((float)nch_ * coh * coh, 1.0f), (float)nch_);
+      if (lane == 0) { cMe[c] = me; cP[c] = (float)p; }
+      for (int i = lane; i < H2; i += 64) {
+        const float cc = cosT[(int64_t)p * H2 + i], sn = sinT[(int64_t)p * H2 + i];
+        const float m1 = U.ck[c * D + i], m2 = U.ck[c * D + i + H2];
+        U.ck[c * D + i] = m1 * cc - m2 * sn;
+        U.ck[c * D + i + H2] = m2 * cc + m1 * sn;
+      }
+    }
+  }
+  __syncthreads();
+  // ---- phase B: probe sweep (TPQ threads per probe, DPT dims each) ----
+  {
+    const int sub = tid % TPQ;
+    const int d0 = sub * DPT;
+    if (q < dm.W) {
+      float M[DPT];
+#pragma unroll
+      for (int k = 0; k < DPT; ++k) M[k] = 0.f;
+      float Z = 0.f;
+      int ci = prefix ? 0 : nx - 1;
+      const int t_first = prefix ? a : b - 1;
+      const int t_last = prefix ? xs[nx - 1] - 1 : xs[0];
+      const int step = prefix ? 1 : -1;
+      const int steps = prefix ? t_last - t_first + 1 : t_first - t_last + 1;
+      for (int it = 0, t = t_first; it < steps && it < NMAX; ++it, t += step) {
+        const float e = U.sE[q * NMAX + t];
+        Z += e;
+#pragma unroll
+        for (int k = 0; k < DPT; ++k) M[k] += e * ldf(U.sV, t * D + d0 + k);
+        const bool at = prefix ? (t + 1 == xs[ci]) : (t == xs[ci]);
+        if (at) {
+          const int nch_ = (int)cn[ci];
+          if (nch_ >= 2) {
+            float dot = 0.f;
+#pragma unroll
+            for (int k = 0; k < DPT; ++k) dot += qv[k] * U.ck[ci * D + d0 + k];
+            dot += __shfl_xor(dot, 1, 64);
+            dot += __shfl_xor(dot, 2, 64);
+            const float zt = cMe[ci] * expf(dot * scale - m_q);
+            float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+            for (int k = 0; k < DPT; ++k) {
+              const float df = M[k] - zt * U.cv[ci * D + d0 + k];
+              s1 += df * df;
+              s2 += M[k] * M[k];
+            }
+            s1 += __shfl_xor(s1, 1, 64);
+            s1 += __shfl_xor(s1, 2, 64);
+            s2 += __shfl_xor(s2, 1, 64);
+            s2 += __shfl_xor(s2, 2, 64);
+            const float dz = Z - zt;
+            const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
+            if (sub == 0) U.con[ci * WMAX + q] = (Z / zc_q) * Dq;
+          }
+          ci += prefix ? 1 : -1;
+          if (ci < 0 || ci >= nx) break;
+        }
+      }
+    } else {
+      // idle probe lanes still take part in the shuffles above only within
+      // their own TPQ group, so nothing to do here
+    }
+  }
+  __syncthreads();
+  // ---- phase C: D = mean over probes (fixed order) ----
+  if (tid < nx) {
+    const int c = tid;
+    float acc = 0.f;
+    if ((int)cn[c] >= 2) {
+      for (int qq = 0; qq < dm.W; ++qq) acc += U.con[c * WMAX + qq];
+      acc /= (float)dm.W;
+    }
+    cD[c] = acc;
+  }
+  __syncthreads();
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, const T* __restrict__ V,
+                                               const T* __restrict__ Q, const float* __restrict__ cosT,
+                                               const float* __restrict__ sinT, const int32_t* __restrict__ slot_starts,
+                                               const int32_t* __restrict__ n_slots, const float* __restrict__ kappa,
+                                               TreeView tv) {
+  using Lay = BuildLds<T, D>;
+  constexpr bool BF = sizeof(T) == 2;
+  constexpr int KS = BF ? D / 16 : D / 4;
+  constexpr int DPT = D / TPQ;
+  extern __shared__ __align__(16) char smem[];
+  Unit<T, D> U(smem);
+  const int J = *n_slots;
+  const int unit = blockIdx.x;
+  const int lg = unit / dm.J_cap, j = unit % dm.J_cap;
+  if (j >= J) return;
+  const int l = lg / dm.G, g = lg % dm.G;
+  const int64_t a0 = slot_starts[j];
+  const int n = slot_starts[j + 1] - (int)a0;
+  if (n < 1 || n > NMAX || a0 < 0 || a0 + n > dm.N_c) {   // malformed partition: refuse the unit
+    if (threadIdx.x == 0) { atomicOr(tv.status, 2); tv.unit_nn[unit] = 0; }
+    return;
+  }
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const float scale = 1.0f / sqrtf((float)D);
+  const T* Kp = K + ((int64_t)lg * dm.T + a0) * D;
+  const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
+  const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
+
+  // ---- stage K, V; token scalars ----
+  for (int e = tid; e < NMAX * D; e += BT) {
+    const int t = e / D, c = e % D;
+    U.sK[t * Lay::LDK + c] = t < n ? Kp[(int64_t)t * D + c] : (T)0;
+    U.sV[t * D + c] = t < n ? Vp[(int64_t)t * D + c] : (T)0;
+  }
+  for (int e = tid; e < 4 * NMAX; e += BT) U.sS[e] = 0.f;
+  __syncthreads();
+
+  // ---- relevance pass 2 and probe exponentials (MFMA logits) ----
+  {
+    const int rows = dm.rows;
+    const int n_rt = (rows + 15) / 16;
+    const int n_tt = (n + 15) / 16;
+    float sacc[NMAX / 16];
+#pragma unroll
+    for (int tt = 0; tt < NMAX / 16; ++tt) sacc[tt] = 0.f;
+    for (int rt = wave; rt < n_rt; rt += BT / 64) {
+      const int row_l = rt * 16 + (lane & 15);
+      const bool rok = row_l < rows;
+      const T* qr = Qp + (int64_t)(rok ? row_l : 0) * D;
+      s16x4 qb[BF ? KS : 1];
+      float qf[BF ? 1 : KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if constexpr (BF) {
+          const uint16_t* q16 = (const uint16_t*)qr + s * 16 + 4 * (lane >> 4);
+          s16x4 v;
+          v[0] = rok ? (short)q16[0] : 0; v[1] = rok ? (short)q16[1] : 0;
+          v[2] = rok ? (short)q16[2] : 0; v[3] = rok ? (short)q16[3] : 0;
+          qb[s] = v;
+        } else {
+          qf[s] = rok ? ((const float*)qr)[s * 4 + (lane >> 4)] : 0.f;
+        }
+      }
+      float4 st[4];
+      int rowi[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        rowi[i] = rt * 16 + 4 * (lane >> 4) + i;
+        st[i] = rowi[i] < rows ? tv.row_stats[(int64_t)lg * rows + rowi[i]] : make_float4(0.f, 1.f, 0.f, 1.f);
+      }
+#pragma unroll
+      for (int tt = 0; tt < NMAX / 16; ++tt) {
+        if (tt >= n_tt) break;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        const T* kr = U.sK + (tt * 16 + (lane & 15)) * Lay::LDK;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          if constexpr (BF) {
+            const uint16_t* k16 = (const uint16_t*)kr + s * 16 + 4 * (lane >> 4);
+            s16x4 bb;
+            bb[0] = (short)k16[0]; bb[1] = (short)k16[1]; bb[2] = (short)k16[2]; bb[3] = (short)k16[3];
+            acc = mfma_bf16_16x16x16(qb[s], bb, acc);
+          } else {
+            acc = mfma_f32_16x16x4(qf[s], ((const float*)kr)[s * 4 + (lane >> 4)], acc);
+          }
+        }
+        const int t = tt * 16 + (lane & 15);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (rowi[i] < rows && t < n) {
+            const float x = acc[i] * scale;
+            sacc[tt] += expf(x - st[i].x) / st[i].y;
+            const int u = rowi[i] % dm.W, hl = rowi[i] / dm.W;
+            if (u % dm.hpg == hl) {
+              const float mq = tv.probe_m[(int64_t)lg * dm.W + u];
+              U.sE[u * NMAX + t] = expf(x - mq);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int tt = 0; tt < NMAX / 16; ++tt) {
+      float v = sacc[tt];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      if (lane < 16) U.sS[wave * NMAX + tt * 16 + lane] = v;
+    }
+  }
+  __syncthreads();
+  const float S = tv.lg_S[lg];
+  if (tid < n) {
+    const int t = tid;
+    const float s = ((U.sS[t] + U.sS[NMAX + t]) + U.sS[2 * NMAX + t]) + U.sS[3 * NMAX + t];
+    const float R = s / (S + dm.eps);
+    U.sR[t] = R;
+    tv.tok_R[(int64_t)lg * dm.N_c + a0 + t] = R;
+    U.sKap[t] = kappa[a0 + t];
+    float kn = 0.f;
+    for (int c = 0; c < D; ++c) {
+      const float x = ldf(U.sK, t * Lay::LDK + c);
+      kn += x * x;
+    }
+    U.sKn[t] = sqrtf(kn);
+    float am = 0.f;
+    for (int qq = 0; qq < dm.W; ++qq) am += U.sE[qq * NMAX + t] / tv.probe_ZC[(int64_t)lg * dm.W + qq];
+    U.sA[t] = am / (float)dm.W;
+  }
+  __syncthreads();
+
+  // ---- probe registers for the sweeps ----
+  const int q = tid / TPQ;
+  float qv[DPT];
+  float m_q = 0.f, zc_q = 1.f;
+  if (q < dm.W) {
+    const int hl = q % dm.hpg;
+    const T* qr = Qp + ((int64_t)hl * dm.W + q) * D + (tid % TPQ) * DPT;
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) qv[k] = ldf(qr, k);
+    m_q = tv.probe_m[(int64_t)lg * dm.W + q];
+    zc_q = tv.probe_ZC[(int64_t)lg * dm.W + q];
+  } else {
+#pragma unroll
+    for (int k = 0; k < DPT; ++k) qv[k] = 0.f;
+  }
+
+  // ---- root ----
+  int* cnt = U.xi + 3 * 64;             // [0] node count, [1] head
+  float* cn = U.cs + 0 * CAND_MAX;
+  float* cR = U.cs + 1 * CAND_MAX;
+  float* cD = U.cs + 5 * CAND_MAX;
+  if (tid == 0) {
+    U.na[0] = 0; U.nn[0] = n; U.nc[0] = -1; U.np[0] = -1; U.nch[0] = 0; U.nk[0] = 0; U.ncut[0] = -1;
+    U.xi[0] = n;
+    cnt[0] = 1;
+  }
+  __syncthreads();
+  float Ddrop = 0.f;
+  if (n >= 2) {
+    sweep<T, D>(U, dm, true, 0, n, U.xi, 1, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
+    if (tid == 0) { U.nD[0] = cD[0]; U.nR[0] = cR[0]; }
+  } else if (tid == 0) {
+    U.nD[0] = 0.f;
+    U.nR[0] = U.sR[0];
+  }
+  if (tid == 0) {
+    float dd = 0.f;
+    for (int t = 0; t < n; ++t) dd += U.sA[t];
+    Ddrop = dd;
+  }
+  __syncthreads();
+
+  // ---- top-down refinement in BFS order ----
+  int* XL = U.xi;              // [0..31]
+  int* XR = U.xi + 32;         // [32..63]
+  int* XB = U.xi + 64;         // [64..95] binary cuts
+  int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits
+  for (int head = 0;; ++head) {
+    __syncthreads();
+    const int count = cnt[0];
+    if (head >= count) break;
+    const int a = U.na[head], nv = U.nn[head], b = a + nv;
+    if (nv < 2) continue;
+    const float Dv = U.nD[head];
+    if (nv == 2) {
+      if (tid == 0) {
+        const int c0 = count;
+        U.nc[head] = c0; U.nch[head] = 2; U.nk[head] = 1; U.ncut[head] = (int)a0 + a + 1;
+        for (int k = 0; k < 2; ++k) {
+          U.na[c0 + k] = a + k; U.nn[c0 + k] = 1; U.nc[c0 + k] = -1; U.np[c0 + k] = head;
+          U.nch[c0 + k] = 0; U.nk[c0 + k] = 0; U.ncut[c0 + k] = -1;
+          U.nD[c0 + k] = 0.f; U.nR[c0 + k] = U.sR[a + k];
+        }
+        cnt[0] = count + 2;
+      }
+      continue;
+    }
+    // candidate flags over cut positions xi in (a, b)
+    for (int t = tid; t < NMAX; t += BT) U.flag[t] = 0;
+    __syncthreads();
+    if (tid < nv - 1) {
+      const int t = a + tid;                     // curvature position t -> cut t + 1
+      const float kt = U.sKap[t];
+      int rank = 0;
+      for (int t2 = a; t2 <= b - 2; ++t2) {
+        const float k2 = U.sKap[t2];
+        rank += (k2 > kt) || (k2 == kt && t2 < t);
+      }
+      if (rank < dm.k_curv) U.flag[t + 1 - a] = 1;
+    }
+    if (tid == 0) U.flag[nv / 2] = 1;            // midpoint a + floor(n/2)
+    // curvature range and extraction token (wave 0)
+    if (wave == 0) {
+      float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY;
+      int bi = 0x7fffffff;
+      for (int t = a + lane; t < b; t += 64) {
+        const float k = U.sKap[t];
+        kmn = fminf(kmn, k);
+        kmx = fmaxf(kmx, k);
+        const float am = U.sA[t];
+        if (am > best || (am == best && t < bi)) { best = am; bi = t; }
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        kmn = fminf(kmn, __shfl_xor(kmn, o, 64));
+        kmx = fmaxf(kmx, __shfl_xor(kmx, o, 64));
+        const float b2 = __shfl_xor(best, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        if (b2 > best || (b2 == best && i2 < bi)) { best = b2; bi = i2; }
+      }
+      if (lane == 0) {
+        meta[3] = bi;
+        meta[4] = __float_as_int(kmn);
+        meta[5] = __float_as_int(kmx);
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      const int p = meta[3];
+      int nb = 0, nl = 0, nr = 0;
+      for (int x = 1; x < nv; ++x)
+        if (U.flag[x]) XB[nb++] = a + x;
+      // prefix children [a, x): binary cuts plus [a, p) when p > a
+      int i1 = 0;
+      bool addp = p > a;
+      for (int k = 0; k <= nb; ++k) {
+        const int xv = k < nb ? XB[k] : 0x7fffffff;
+        if (addp && p < xv) { XL[nl++] = p; addp = false; }
+        if (addp && p == xv) addp = false;
+        if (k < nb) XL[nl++] = xv;
+      }
+      (void)i1;
+      // suffix children [x, b): binary cuts plus [p+1, b) when p + 1 < b
+      bool addq = p + 1 < b;
+      for (int k = 0; k <= nb; ++k) {
+        const int xv = k < nb ? XB[k] : 0x7fffffff;
+        if (addq && p + 1 < xv) { XR[nr++] = p + 1; addq = false; }
+        if (addq && p + 1 == xv) addq = false;
+        if (k < nb) XR[nr++] = xv;
+      }
+      meta[0] = nl; meta[1] = nr; meta[2] = nb;
+    }
+    __syncthreads();
+    const int nl = meta[0], nr = meta[1], nb = meta[2], p = meta[3];
+    // prefix sweep; keep (x, n, R, D) of prefix children in slots 32..
+    sweep<T, D>(U, dm, true, a, b, XL, nl, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
+    float* keepL = U.sS;                       // reuse relevance partials: [0..CAND) D, [32..) R
+    if (tid < nl) { keepL[tid] = cD[tid]; keepL[32 + tid] = cR[tid]; }
+    __syncthreads();
+    sweep<T, D>(U, dm, false, a, b, XR, nr, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
+    float* keepR = U.sS + 64;
+    if (tid < nr) { keepR[tid] = cD[tid]; keepR[32 + tid] = cR[tid]; }
+    __syncthreads();
+    if (tid == 0) {
+      const float kmn = __int_as_float(meta[4]), kmx = __int_as_float(meta[5]);
+      const float kr = kmx - kmn;
+      auto findL = [&](int x) { for (int k = 0; k < nl; ++k) if (XL[k] == x) return k; return -1; };
+      auto findR = [&](int x) { for (int k = 0; k < nr; ++k) if (XR[k] == x) return k; return -1; };
+      float best = -INFINITY;
+      int bx = -1;
+      for (int k = 0; k < nb; ++k) {
+        const int x = XB[k];
+        const float kh = kr > 0.f ? (U.sKap[x - 1] - kmn) / kr : 0.f;
+        const float gsc = ((Dv - keepL[findL(x)]) - keepR[findR(x)]) + dm.lam_kappa * kh;
+        if (gsc > best) { best = gsc; bx = x; }
+      }
+      float dsum = 0.f;
+      int nkid = 1;
+      if (p > a) { dsum += keepL[findL(p)]; ++nkid; }
+      if (p + 1 < b) { dsum += keepR[findR(p + 1)]; ++nkid; }
+      const float gext = (Dv - dsum) / (float)(nkid - 1);
+      const int c0 = count;
+      U.nc[head] = c0;
+      if (best >= gext) {
+        U.nch[head] = 2; U.nk[head] = 1; U.ncut[head] = (int)a0 + bx;
+        const int kl = findL(bx), kr2 = findR(bx);
+        U.na[c0] = a; U.nn[c0] = bx - a; U.nD[c0] = keepL[kl]; U.nR[c0] = keepL[32 + kl];
+        U.na[c0 + 1] = bx; U.nn[c0 + 1] = b - bx; U.nD[c0 + 1] = keepR[kr2]; U.nR[c0 + 1] = keepR[32 + kr2];
+        cnt[0] = count + 2;
+      } else {
+        U.nch[head] = nkid; U.nk[head] = 2; U.ncut[head] = (int)a0 + p;
+        int c = c0;
+        if (p > a) { const int k = findL(p); U.na[c] = a; U.nn[c] = p - a; U.nD[c] = keepL[k]; U.nR[c] = keepL[32 + k]; ++c; }
+        U.na[c] = p; U.nn[c] = 1; U.nD[c] = 0.f; U.nR[c] = U.sR[p]; ++c;
+        if (p + 1 < b) { const int k = findR(p + 1); U.na[c] = p + 1; U.nn[c] = b - p - 1; U.nD[c] = keepR[k]; U.nR[c] = keepR[32 + k]; ++c; }
+        cnt[0] = c;
+      }
+      for (int c = c0; c < cnt[0]; ++c) { U.nc[c] = -1; U.np[c] = head; U.nch[c] = 0; U.nk[c] = 0; U.ncut[c] = -1; }
+    }
+  }
+  __syncthreads();
+  // ---- write the node table ----
+  const int count = cnt[0];
+  const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
+  for (int i = tid; i < 2 * n; i += BT) {
+    const int64_t s = base + i;
+    if (i < count) {
+      tv.node_a[s] = (int32_t)a0 + U.na[i];
+      tv.node_n[s] = U.nn[i];
+      tv.node_child[s] = U.nc[i];
+      tv.node_parent[s] = U.np[i];
+      tv.node_nch[s] = (uint8_t)U.nch[i];
+      tv.node_kind[s] = (uint8_t)U.nk[i];
+      tv.node_cut[s] = U.ncut[i];
+      tv.node_D[s] = U.nD[i];
+      tv.node_R[s] = U.nR[i];
+    } else {
+      tv.sp_cost[s] = 0;
+      tv.sp_E[s] = 0;
+      tv.sp_exec[s] = 0;
+    }
+  }
+  if (tid == 0) {
+    tv.unit_nn[unit] = count;
+    tv.unit_Ddrop[unit] = Ddrop;
+  }
+  (void)cn;
+}
+
+hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void* V, const void* Q,
+                        const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
+                        const float* kappa, const TreeView& tv, hipStream_t st) {
+  const dim3 grid((unsigned)((int64_t)dm.L * dm.G * dm.J_cap));
+#define GKV_LAUNCH_BUILD(TT, DD)                                                                           \
+  do {                                                                                                     \
+    auto fn = k_build<TT, DD>;                                                                             \
+    hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes); \
+    if (e0 != hipSuccess) return e0;                                                                       \
+    hipLaunchKernelGGL(fn, grid, dim3(BT), lds_bytes, st, dm, (const TT*)K, (const TT*)V, (const TT*)Q, cosT, \
+                       sinT, slot_starts, n_slots, kappa, tv);                                             \
+  } while (0)
+  if (dm.dtype == GRACEKV_BF16) {
+    if (dm.d == 128) GKV_LAUNCH_BUILD(uint16_t, 128); else GKV_LAUNCH_BUILD(uint16_t, 64);
+  } else {
+    if (dm.d == 128) GKV_LAUNCH_BUILD(float, 128); else GKV_LAUNCH_BUILD(float, 64);
+  }
+#undef GKV_LAUNCH_BUILD
+  return hipGetLastError();
+}
+
+}  // namespace gkv

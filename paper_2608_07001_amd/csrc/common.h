@@ -1,0 +1,138 @@
+// Internal declarations shared by the HIP translation units of libgracekv.
+// Target: gfx950 (CDNA4), wave64.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "gracekv.h"
+
+namespace gkv {
+
+constexpr int NMAX = 128;        // longest slot (n_max); units hold at most 2*NMAX-1 nodes
+constexpr int NODE_MAX = 2 * NMAX - 1;
+constexpr int WMAX = 64;         // window queries
+constexpr int DMAX = 128;        // head dim
+constexpr int CAND_MAX = 20;     // prefix (or suffix) children per refinement: 17 cuts + extraction side
+
+// Every size and hyperparameter a kernel needs, passed by value.
+struct Dims {
+  int L, G, H, d, hpg, W, n_seg, Dh, dtype;
+  int r, J_cap;
+  int64_t T, N_ctx, N_c, B_total, B_free;
+  float lam_stab, lam_s, eps_seg, mad;
+  int win[3];
+  int n_min, n_max, n0;
+  float lam_d, lam_n, c_cut;
+  float lam_Z, lam_M, lam_kappa, beta_frac, eps;
+  int k_curv;
+  int rows;                      // relevance rows per (l, g): hpg * W
+};
+
+// Typed views into the tree buffer (offsets come from gracekv_plan).
+struct TreeView {
+  int32_t* node_a;      // absolute start
+  int32_t* node_n;      // length
+  int32_t* node_child;  // first child (local index) or -1
+  int32_t* node_parent; // parent (local index) or -1
+  uint8_t* node_nch;
+  uint8_t* node_kind;   // 0 leaf, 1 binary split, 2 extraction
+  int32_t* node_cut;
+  float* node_D;
+  float* node_R;
+  float* sp_U;          // Split op of node slot i
+  uint64_t* sp_E;
+  uint8_t* sp_cost;
+  uint8_t* sp_exec;
+  int32_t* unit_nn;     // nodes per unit
+  float* unit_Ddrop;
+  float* add_U;
+  uint64_t* add_E;
+  uint8_t* add_exec;
+  float* tok_R;         // [LG][N_c] token values
+  float4* row_stats;    // [LG][rows] (m_V, Z_V, m_C, Z_C)
+  float* probe_m;       // [LG][W]
+  float* probe_ZC;      // [LG][W]
+  float* lg_S;          // [LG]
+  float* omega;         // [LG] normalised sensitivity
+  int32_t* status;      // device status word
+  int32_t* slots;       // [J_cap + 1] copy of the slot starts (then N_c)
+  int32_t* nslots;      // [1] J
+};
+
+Dims make_dims(const gracekv_config& c, const gracekv_plan& p);
+TreeView make_view(void* base, const gracekv_plan& p);
+
+// ---- device helpers -------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffff) ? 0x40 : 0));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// element load as fp32 for the two storage types
+__device__ __forceinline__ float ldf(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ldf(const uint16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+__device__ __forceinline__ void stf(float* p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16_rne(v); }
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Merge two (max, sum-of-exp) pairs: the sum is relative to its max.
+__device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2) {
+  float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) { m = mn; z = 0.f; return; }
+  z = z * expf(m - mn) + z2 * expf(m2 - mn);
+  m = mn;
+}
+
+// ---- matrix cores ---------------------------------------------------------
+// 16x16 output tile, C[i][j] += sum_k A[i][k] B[j][k].  Lane l holds
+// C[4*(l/16) + r][l % 16] in acc[r].  For bf16 each step consumes 16 k: lane
+// l supplies A[l%16][4*(l/16) .. +3] (same for B).  For fp32 each step
+// consumes 4 k: lane l supplies A[l%16][l/16].
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma_bf16_16x16x16(s16x4 a, s16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// ---- launchers (each defined in its own translation unit) -----------------
+hipError_t launch_rowstats(const Dims& dm, const void* K, const void* Q, const TreeView& tv, float4* partial,
+                           hipStream_t st);
+hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void* V, const void* Q,
+                        const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
+                        const float* kappa, const TreeView& tv, hipStream_t st);
+hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
+hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st);
+hipError_t launch_pack(const Dims& dm, const void* K, const void* V, const float* cosT, const float* sinT,
+                       const TreeView& tv, int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
+                       int32_t* pos_out, float* logm_out, void* ws, hipStream_t st);
+hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surprisal, float* kappa, float* bscore,
+                          int32_t* slot_starts, int32_t* n_slots, void* ws, hipStream_t st);
+size_t segment_ws_bytes(const Dims& dm);
+size_t select_ws_bytes(const Dims& dm);
+size_t pack_ws_bytes(const Dims& dm);
+int rowstats_chunks(const Dims& dm);
+int build_lds_bytes(const Dims& dm);
+hipError_t selftest_mfma(int which, float* host_out);
+
+}  // namespace gkv

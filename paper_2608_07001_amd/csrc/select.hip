@@ -1,0 +1,338 @@
+// Gains, keys and the global budgeted auction.
+//
+// Score (App. A.5 eq:app_operation_gains, eq:app_operation_costs,
+// eq:app_unit_utility; eq:app_head_sensitivity; gains clamped at zero as in
+// App. C.5):  Add(l,g,j): Delta = w R(root) (D_drop(root) - D(root)), cost 1;
+// Split(v): Delta = w R(v) (D(v) - sum_children D), cost |child| - 1;
+// U = max(Delta, 0) / c.  Every op gets the unique key
+//   k = (bits(U) << 32) | (2^32 - 1 - id),  id = unit_ordinal * 256 + local,
+// (larger U first, then the smaller id) and the effective key
+//   E(a) = min(k(a), E(parent op)).
+//
+// Select (App. A.5 Stage II and App. C.3: pop the best available op, execute
+// it if it fits, discard it otherwise, expose its children).  While at least
+// two budget units remain every pop executes, and the queue pops ops in
+// descending E (an op can only be popped after every ancestor, and once the
+// queue top drops below v every op with E > v has been popped).  Hence, with
+// theta the E value at which the cumulative cost in descending-E order first
+// reaches B_free - 1:
+//   * every op with E > theta executes;
+//   * the ops with E == theta share one minimising ancestor, so they lie in
+//     one unit; the queue rule is replayed there while >= 2 units remain;
+//   * if exactly one unit remains, the queue discards cost-2 ops until it pops
+//     a cost-1 op, i.e. it executes the best-keyed available cost-1 op.
+// theta is found with an 8-pass, 8-bit, cost-weighted radix select.
+#include <algorithm>
+
+#include "common.h"
+
+namespace gkv {
+
+enum { SEL_SELECT = 0, SEL_ALL = 1, SEL_NONE = 2, SEL_RESID = 3 };
+
+struct SelState {
+  uint64_t prefix;
+  int64_t target;
+  int64_t above;
+  int64_t total;
+  int64_t R;
+  uint64_t resid_key;
+  int32_t mode;
+  int32_t pad;
+  unsigned long long hist[256];
+};
+
+size_t select_ws_bytes(const Dims&) { return sizeof(SelState); }
+
+__device__ __forceinline__ uint64_t make_key(float U, uint32_t id) {
+  return ((uint64_t)__float_as_uint(U) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+
+__global__ void k_omega(Dims dm, const float* __restrict__ omega_raw, TreeView tv) {
+  __shared__ float red[256];
+  const int LG = dm.L * dm.G;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < LG; i += 256) s += omega_raw ? omega_raw[i] : 1.0f;
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+    __syncthreads();
+  }
+  const float mean = red[0] / (float)LG;
+  for (int i = threadIdx.x; i < LG; i += 256) tv.omega[i] = (omega_raw ? omega_raw[i] : 1.0f) / (mean + dm.eps);
+}
+
+__global__ void k_score(Dims dm, TreeView tv) {
+  const int32_t* n_slots = tv.nslots;
+  const int32_t* slot_starts = tv.slots;
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= (int64_t)dm.L * dm.G * dm.J_cap) return;
+  const int lg = (int)(u / dm.J_cap), j = (int)(u % dm.J_cap);
+  const int J = *n_slots;
+  if (j >= J) return;
+  const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+  const float w = tv.omega[lg];
+  const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[j];
+  const int nn = tv.unit_nn[u];
+  if (nn < 1) { tv.add_U[u] = 0.f; tv.add_E[u] = 0; tv.add_exec[u] = 0; return; }
+  bool bad = false;
+  float gain = w * tv.node_R[base] * (tv.unit_Ddrop[u] - tv.node_D[base]);
+  bad |= gain != gain;
+  gain = gain > 0.f ? gain : 0.f;
+  const uint64_t kadd = make_key(gain, ord * 256u);
+  tv.add_U[u] = gain;
+  tv.add_E[u] = kadd;
+  tv.add_exec[u] = 0;
+  for (int i = 0; i < nn; ++i) {
+    const int64_t s = base + i;
+    const int nch = tv.node_nch[s];
+    tv.sp_exec[s] = 0;
+    if (nch == 0) {
+      tv.sp_cost[s] = 0;
+      tv.sp_E[s] = 0;
+      tv.sp_U[s] = 0.f;
+      continue;
+    }
+    const int c0 = tv.node_child[s];
+    float sd = 0.f;
+    for (int k = 0; k < nch; ++k) sd += tv.node_D[base + c0 + k];
+    float g = w * tv.node_R[s] * (tv.node_D[s] - sd);
+    bad |= g != g;
+    g = g > 0.f ? g : 0.f;
+    const float Uv = g / (float)(nch - 1);
+    const uint64_t k = make_key(Uv, ord * 256u + 1u + (uint32_t)i);
+    const int par = tv.node_parent[s];
+    const uint64_t Ep = par < 0 ? kadd : tv.sp_E[base + par];
+    tv.sp_E[s] = k < Ep ? k : Ep;
+    tv.sp_U[s] = Uv;
+    tv.sp_cost[s] = (uint8_t)(nch - 1);
+  }
+  if (bad) atomicOr(tv.status, 1);
+}
+
+hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st) {
+  hipLaunchKernelGGL(k_omega, dim3(1), dim3(256), 0, st, dm, omega_raw, tv);
+  const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
+  hipLaunchKernelGGL(k_score, dim3((unsigned)((units + 127) / 128)), dim3(128), 0, st, dm, tv);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_sel_init(Dims dm, SelState* S) {
+  const int t = threadIdx.x;
+  S->hist[t] = 0;
+  if (t == 0) {
+    S->prefix = 0; S->target = dm.B_free - 1; S->above = 0; S->total = 0; S->R = 0;
+    S->resid_key = 0; S->mode = SEL_SELECT;
+  }
+}
+
+// cost-weighted histogram of digit `pass` among ops matching the prefix
+__global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState* S, int pass) {
+  const int32_t* n_slots = tv.nslots;
+  __shared__ unsigned int h[256];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int mode = S->mode;
+  if (mode == SEL_SELECT) {
+    const int shift = 56 - 8 * pass;
+    const uint64_t pre = S->prefix;
+    const int J = *n_slots;
+    const int64_t node_cap = (int64_t)dm.L * dm.G * 2 * dm.N_c;
+    const int64_t unit_cap = (int64_t)dm.L * dm.G * dm.J_cap;
+    const int64_t tot = node_cap + unit_cap;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < tot; i += (int64_t)gridDim.x * 256) {
+      uint64_t E;
+      int c;
+      if (i < node_cap) {
+        c = tv.sp_cost[i];
+        E = tv.sp_E[i];
+      } else {
+        const int64_t u = i - node_cap;
+        if ((int)(u % dm.J_cap) >= J) continue;
+        c = 1;
+        E = tv.add_E[u];
+      }
+      if (c == 0) continue;
+      if (pass > 0 && (E >> (shift + 8)) != (pre >> (shift + 8))) continue;
+      atomicAdd(&h[(E >> shift) & 255u], (unsigned)c);
+    }
+  }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd(&S->hist[threadIdx.x], (unsigned long long)h[threadIdx.x]);
+}
+
+__global__ void k_sel_scan(Dims dm, SelState* S, int pass) {
+  if (threadIdx.x != 0) return;
+  if (S->mode != SEL_SELECT) return;
+  if (pass == 0) {
+    int64_t tot = 0;
+    for (int k = 0; k < 256; ++k) tot += (int64_t)S->hist[k];
+    S->total = tot;
+    if (dm.B_free <= 0) { S->mode = SEL_NONE; return; }
+    if (tot <= dm.B_free) { S->mode = SEL_ALL; return; }
+    if (dm.B_free == 1) { S->mode = SEL_RESID; S->R = 1; return; }
+  }
+  const int shift = 56 - 8 * pass;
+  const int64_t need = S->target - S->above;
+  int64_t cum = 0;
+  for (int k = 255; k >= 0; --k) {
+    const int64_t hk = (int64_t)S->hist[k];
+    if (cum + hk >= need) {
+      S->prefix |= (uint64_t)k << shift;
+      S->above += cum;
+      break;
+    }
+    cum += hk;
+  }
+  for (int k = 0; k < 256; ++k) S->hist[k] = 0;
+}
+
+__global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const SelState* S) {
+  const int32_t* n_slots = tv.nslots;
+  const int mode = S->mode;
+  const uint64_t theta = S->prefix;
+  const int J = *n_slots;
+  const int64_t node_cap = (int64_t)dm.L * dm.G * 2 * dm.N_c;
+  const int64_t unit_cap = (int64_t)dm.L * dm.G * dm.J_cap;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < node_cap + unit_cap; i += (int64_t)gridDim.x * 256) {
+    if (i < node_cap) {
+      const int c = tv.sp_cost[i];
+      const uint64_t E = tv.sp_E[i];
+      uint8_t x = 0;
+      if (c > 0) x = (mode == SEL_ALL) || (mode == SEL_SELECT && E > theta);
+      tv.sp_exec[i] = x;
+    } else {
+      const int64_t u = i - node_cap;
+      if ((int)(u % dm.J_cap) >= J) continue;
+      tv.add_exec[u] = (mode == SEL_ALL) || (mode == SEL_SELECT && tv.add_E[u] > theta);
+    }
+  }
+}
+
+// Replays the queue rule inside the one group with E == theta.
+__global__ void k_sel_group(Dims dm, TreeView tv, SelState* S) {
+  const int32_t* n_slots = tv.nslots;
+  const int32_t* slot_starts = tv.slots;
+  if (threadIdx.x != 0 || S->mode != SEL_SELECT) return;
+  const uint64_t theta = S->prefix;
+  int64_t R = dm.B_free - S->above;
+  const int J = *n_slots;
+  const uint32_t id = 0xFFFFFFFFu - (uint32_t)(theta & 0xFFFFFFFFu);
+  const uint32_t ord = id >> 8;
+  const int lg = (int)(ord / (uint32_t)J), j = (int)(ord % (uint32_t)J);
+  const int64_t u = (int64_t)lg * dm.J_cap + j;
+  const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[j];
+  // available ops as local indices: 0 = Add, 1 + i = Split(node i)
+  int avail[NODE_MAX + 1];
+  int na = 0;
+  avail[na++] = (int)(id & 255u);
+  while (R >= 2 && na > 0) {
+    int bi = 0;
+    uint64_t bk = 0;
+    for (int k = 0; k < na; ++k) {
+      const int loc = avail[k];
+      const uint64_t key = loc == 0 ? make_key(tv.add_U[u], ord * 256u)
+                                    : make_key(tv.sp_U[base + loc - 1], ord * 256u + (uint32_t)loc);
+      if (key > bk) { bk = key; bi = k; }
+    }
+    const int loc = avail[bi];
+    avail[bi] = avail[--na];
+    int node;
+    if (loc == 0) {
+      tv.add_exec[u] = 1;
+      R -= 1;
+      node = 0;                              // Add exposes Split(root)
+      if (tv.node_nch[base] > 0 && tv.sp_E[base] == theta) avail[na++] = 1;
+    } else {
+      node = loc - 1;
+      tv.sp_exec[base + node] = 1;
+      R -= tv.sp_cost[base + node];
+      const int c0 = tv.node_child[base + node], nc = tv.node_nch[base + node];
+      for (int k = 0; k < nc; ++k) {
+        const int64_t s = base + c0 + k;
+        if (tv.node_nch[s] > 0 && tv.sp_E[s] == theta) avail[na++] = 1 + c0 + k;
+      }
+    }
+  }
+  S->R = R;
+}
+
+// Best available cost-1 op when exactly one unit remains.
+__global__ __launch_bounds__(256) void k_sel_resid_find(Dims dm, TreeView tv, SelState* S) {
+  const int32_t* n_slots = tv.nslots;
+  const int32_t* slot_starts = tv.slots;
+  if (!((S->mode == SEL_SELECT || S->mode == SEL_RESID) && S->R == 1)) return;
+  const int J = *n_slots;
+  const int64_t node_cap = (int64_t)dm.L * dm.G * 2 * dm.N_c;
+  const int64_t unit_cap = (int64_t)dm.L * dm.G * dm.J_cap;
+  uint64_t best = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < node_cap + unit_cap; i += (int64_t)gridDim.x * 256) {
+    if (i < node_cap) {
+      if (tv.sp_cost[i] != 1 || tv.sp_exec[i]) continue;
+      const int lg = (int)(i / (2 * dm.N_c));
+      const int o = (int)(i % (2 * dm.N_c));
+      // unit j with 2 a_j <= o < 2 a_{j+1}
+      int lo = 0, hi = J - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (2 * slot_starts[mid] <= o) lo = mid; else hi = mid - 1;
+      }
+      const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[lo];
+      const int loc = (int)(i - base);
+      const int par = tv.node_parent[i];
+      const bool pe = par < 0 ? tv.add_exec[(int64_t)lg * dm.J_cap + lo] : tv.sp_exec[base + par];
+      if (!pe) continue;
+      const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)lo;
+      const uint64_t k = make_key(tv.sp_U[i], ord * 256u + 1u + (uint32_t)loc);
+      best = k > best ? k : best;
+    } else {
+      const int64_t u = i - node_cap;
+      const int j = (int)(u % dm.J_cap);
+      if (j >= J || tv.add_exec[u]) continue;
+      const uint32_t ord = (uint32_t)(u / dm.J_cap) * (uint32_t)J + (uint32_t)j;
+      const uint64_t k = make_key(tv.add_U[u], ord * 256u);
+      best = k > best ? k : best;
+    }
+  }
+  if (best) atomicMax((unsigned long long*)&S->resid_key, (unsigned long long)best);
+}
+
+__global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used) {
+  const int32_t* n_slots = tv.nslots;
+  const int32_t* slot_starts = tv.slots;
+  if (threadIdx.x != 0) return;
+  const int mode = S->mode;
+  int64_t R = S->R;
+  if (mode == SEL_ALL) { *b_used = S->total; return; }
+  if (mode == SEL_NONE) { *b_used = 0; return; }
+  if (R == 1 && S->resid_key) {
+    const int J = *n_slots;
+    const uint32_t id = 0xFFFFFFFFu - (uint32_t)(S->resid_key & 0xFFFFFFFFu);
+    const uint32_t ord = id >> 8, loc = id & 255u;
+    const int lg = (int)(ord / (uint32_t)J), j = (int)(ord % (uint32_t)J);
+    if (loc == 0) tv.add_exec[(int64_t)lg * dm.J_cap + j] = 1;
+    else tv.sp_exec[(int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[j] + loc - 1] = 1;
+    R = 0;
+  }
+  *b_used = dm.B_free - R;
+}
+
+hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st) {
+  SelState* S = (SelState*)ws;
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S);
+  const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
+  const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
+  for (int pass = 0; pass < 8; ++pass) {
+    hipLaunchKernelGGL(k_sel_hist, dim3(blocks), dim3(256), 0, st, dm, tv, S, pass);
+    hipLaunchKernelGGL(k_sel_scan, dim3(1), dim3(64), 0, st, dm, S, pass);
+  }
+  hipLaunchKernelGGL(k_sel_flag, dim3(blocks), dim3(256), 0, st, dm, tv, (const SelState*)S);
+  hipLaunchKernelGGL(k_sel_group, dim3(1), dim3(64), 0, st, dm, tv, S);
+  hipLaunchKernelGGL(k_sel_resid_find, dim3(blocks), dim3(256), 0, st, dm, tv, S);
+  hipLaunchKernelGGL(k_sel_finish, dim3(1), dim3(64), 0, st, dm, tv, S, b_used);
+  return hipGetLastError();
+}
+
+}  // namespace gkv

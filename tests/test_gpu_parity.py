@@ -1,0 +1,173 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle on the same
+seeded inputs.  Marked gpu: needs an MI355X.
+
+Tolerances (fp32 arithmetic on both sides of a comparison, inputs exact):
+  * token values R^tok and node values R: rtol 1e-4 (sums of <= 10^4
+    exponentials in fp32 against fp64);
+  * distortions D: |dD| <= 2e-3 |D| + 1e-7 -- D is a mean of squared relative
+    errors, so an fp32 error e in Z~ or M~ moves D_q by about 2 e sqrt(D_q);
+  * topology, partition and selection: exact except near ties, where the
+    GPU's choice scores within tau = 2e-4 (relative) of the oracle's best; those
+    are counted and their subtrees are only checked for validity.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import gracekv_oracle as O
+from synth.workloads import CONFIGS, make_case, make_kappa, small_shape
+
+pytestmark = pytest.mark.gpu
+
+import gpu_harness as H  # noqa: E402
+
+RTOL_R = 1e-4
+RTOL_D, ATOL_D = 2e-3, 1e-7
+TAU = 2e-4
+
+
+def _partition(N, lens=(16, 40, 64, 100, 128, 23, 77)):
+    starts, a, k = [], 0, 0
+    while a < N:
+        starts.append(a)
+        a += lens[k % len(lens)]
+        k += 1
+    return starts
+
+
+def test_mfma_layout_bf16_and_fp32():
+    from paper_2608_07001_amd import gracekv as gk
+    i = np.arange(16)[:, None]
+    k = np.arange(16)[None, :]
+    A = (i - 3 * k) / 8.0
+    B = (2 * i + k) / 16.0
+    want = A @ B.T
+    for which in (0, 1):
+        got = gk.selftest_mfma(which).numpy()
+        assert np.array_equal(got, want.astype(np.float32)), which
+
+
+@pytest.fixture(scope="module")
+def tiny_staged():
+    sh = CONFIGS["tiny"]
+    case = make_case(sh, 0, with_hidden=False)
+    kappa = make_kappa(sh, 0)
+    N_c = O.budget(sh.L, sh.G, sh.N_ctx, sh.x).N_c
+    slots = _partition(N_c)
+    g = H.gpu_run(H.to_dev(case), slots=slots, kappa=kappa)
+    o = H.oracle_run(case, slots=slots, kappa=kappa)
+    return sh, case, g, o
+
+
+def test_tiny_token_values(tiny_staged):
+    sh, case, g, o = tiny_staged
+    N_c = g["plan"].N_c
+    tokR = g["tok_R"].numpy().reshape(sh.L * sh.G, N_c)
+    worst = 0.0
+    for (l, gg), c in o.ctx.items():
+        err = np.abs(tokR[l * sh.G + gg] - c.R) / np.maximum(np.abs(c.R), 1e-30)
+        worst = max(worst, float(err.max()))
+    print(f"tiny R^tok max rel err {worst:.3e}")
+    assert worst < RTOL_R
+
+
+def test_tiny_trees(tiny_staged):
+    sh, case, g, o = tiny_staged
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    print(f"tiny trees: nodes {st.nodes} near-ties {st.near_ties} maxrelD {st.max_rel_D:.3e} "
+          f"maxabsD {st.max_abs_D:.3e} maxrelR {st.max_rel_R:.3e} maxrelDdrop {st.max_rel_Ddrop:.3e}")
+    assert not st.mismatches, st.mismatches[:10]
+    assert st.max_rel_Ddrop < RTOL_R
+
+
+def test_tiny_selection_and_pack(tiny_staged):
+    sh, case, g, o = tiny_staged
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    ga, gs = H.gpu_selected(g)
+    oa, os_ = H.oracle_selected(o, sh.G)
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    print(f"tiny select: oracle adds {len(oa)} splits {len(os_)} spent {spent}; gpu adds {len(ga)} splits {len(gs)} "
+          f"b_used {g['b_used']}; diff adds {len(ga ^ oa)} splits {len(gs ^ os_)}")
+    assert g["b_used"] == spent
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
+    # packed cache
+    offs = g["offsets"].numpy()
+    assert offs[-1] == o.counts.sum() == g["plan"].B_total - (g["plan"].B_free - spent)
+    K_out, V_out = g["K_out"].float().numpy(), g["V_out"].float().numpy()
+    pos, logm = g["pos_out"].numpy(), g["logm_out"].numpy()
+    worst_k = worst_v = worst_l = 0.0
+    for (l, gg), pk in o.packed.items():
+        lg = l * sh.G + gg
+        s, e = offs[lg], offs[lg + 1]
+        assert np.array_equal(pos[s:e], pk["pos"]), (l, gg)
+        scale_k = np.abs(pk["k"]).max()
+        worst_k = max(worst_k, float(np.abs(K_out[s:e] - pk["k"]).max() / scale_k))
+        worst_v = max(worst_v, float(np.abs(V_out[s:e] - pk["v"]).max() / np.abs(pk["v"]).max()))
+        worst_l = max(worst_l, float(np.abs(logm[s:e] - pk["logm"]).max()))
+    print(f"tiny pack: max rel err k {worst_k:.3e} v {worst_v:.3e} logm abs {worst_l:.3e}")
+    assert worst_k < 1e-5 and worst_v < 1e-5 and worst_l < 1e-4
+
+
+def test_tiny_full_pipeline_with_segmentation():
+    sh = CONFIGS["tiny"]
+    case = make_case(sh, 1, with_hidden=True)
+    g = H.gpu_run(H.to_dev(case))
+    o = H.oracle_run(case)
+    kap_err = float(np.abs(g["kappa"].numpy() - o.seg.kappa).max())
+    b_err = float(np.abs(g["bscore"].numpy() - o.seg.b).max() / np.abs(o.seg.b).max())
+    print(f"tiny segment: kappa max abs err {kap_err:.3e}, b max rel err {b_err:.3e}; "
+          f"J gpu {len(g['slots'])} oracle {len(o.slot_starts)}")
+    print("gpu slots", g["slots"])
+    print("orc slots", o.slot_starts)
+    assert kap_err < 1e-4
+    assert g["slots"] == o.slot_starts
+
+
+def test_fullkv_recovery_on_gpu():
+    # x = 1: the packed cache is the original context cache, entry by entry
+    sh = small_shape(L=2, G=2, H=4, d=64, N_ctx=600, W=16, x=1.0, n_segments=5)
+    case = make_case(sh, 3, with_hidden=True)
+    g = H.gpu_run(H.to_dev(case))
+    offs = g["offsets"].numpy()
+    for lg in range(sh.L * sh.G):
+        s, e = offs[lg], offs[lg + 1]
+        assert np.array_equal(g["pos_out"].numpy()[s:e], np.arange(sh.N_ctx))
+        K = case["K"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx].numpy()
+        V = case["V"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx].numpy()
+        assert np.array_equal(g["K_out"].numpy()[s:e], K)
+        assert np.array_equal(g["V_out"].numpy()[s:e], V)
+        assert np.all(g["logm_out"].numpy()[s:e] == 0.0)
+
+
+@pytest.fixture(scope="module")
+def bf16_staged():
+    sh = small_shape("bf16-small", L=2, G=2, H=8, d=128, N_ctx=1500, W=64, dtype="bf16", x=8.0, n_segments=12,
+                     rope_base=5.0e5, channel_scale="outlier")
+    case = make_case(sh, 7, with_hidden=False)
+    kappa = make_kappa(sh, 7)
+    N_c = O.budget(sh.L, sh.G, sh.N_ctx, sh.x).N_c
+    slots = _partition(N_c, lens=(128, 16, 64, 97, 33, 128, 50))
+    g = H.gpu_run(H.to_dev(case), slots=slots, kappa=kappa)
+    o = H.oracle_run(case, slots=slots, kappa=kappa)
+    return sh, case, g, o
+
+
+def test_bf16_trees_and_selection(bf16_staged):
+    sh, case, g, o = bf16_staged
+    N_c = g["plan"].N_c
+    tokR = g["tok_R"].numpy().reshape(sh.L * sh.G, N_c)
+    worstR = max(float((np.abs(tokR[l * sh.G + gg] - c.R) / np.maximum(c.R, 1e-30)).max())
+                 for (l, gg), c in o.ctx.items())
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    ga, gs = H.gpu_selected(g)
+    oa, os_ = H.oracle_selected(o, sh.G)
+    print(f"bf16 R^tok maxrel {worstR:.3e}; trees nodes {st.nodes} near-ties {st.near_ties} "
+          f"maxrelD {st.max_rel_D:.3e} maxabsD {st.max_abs_D:.3e}; select diff adds {len(ga ^ oa)} "
+          f"splits {len(gs ^ os_)}")
+    assert worstR < RTOL_R
+    assert not st.mismatches, st.mismatches[:10]
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
