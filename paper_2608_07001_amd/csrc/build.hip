@@ -8,7 +8,7 @@
 // eq:app_attention_probability, eq:app_direct_relevance) with lambda_graph = 0,
 // so R^tok = s-hat (eq:app_bottom_up_value).
 //
-// Per unit (n <= 128 tokens):
+// Per unit (n <= 128 tokens), 512 threads:
 //   1. K and V tiles go to LDS; MFMA forms the logits of every relevance row
 //      (query head x window position) against the unit's keys.  With the row
 //      statistics of pass 1 they give pi, s_t and R^tok; probe rows also give
@@ -16,19 +16,23 @@
 //   2. The tree is refined top-down in BFS order.  For node [a, b) the binary
 //      cuts (top-16 curvature positions t -> cut t+1, plus the midpoint) and the
 //      extraction token p define children that are all prefixes [a, x) or
-//      suffixes [x, b) of the node.  One left-to-right sweep evaluates every
-//      prefix child and one right-to-left sweep every suffix child: running
-//      sums of k°, R v, v, R, ||k||, and per probe of e and e v, are read off
-//      at each cut.  A probe's D_q needs only these sums and the child's
-//      prototype, so each child costs O(W d) once the sweep has passed it.
+//      suffixes [x, b) of the node.  The two halves of the workgroup sweep the
+//      node at the same time, one left to right (prefix children) and one right
+//      to left (suffix children): running sums of k°, R v, v, R and ||k||, and per
+//      probe of e and e v, are read off at each cut, so a child costs O(W d)
+//      once its sweep has passed it.  Loads are issued 8 (prototype sums) or 4
+//      (probe sums) tokens ahead.
 //   3. Scores are compared in fp32 (binary form wins ties, smaller cut wins
 //      ties), children are appended, and the node table is written out.
 #include "common.h"
 
 namespace gkv {
 
-constexpr int BT = 256;          // threads per unit
+constexpr int BT = 512;          // threads per unit
+constexpr int GT = 256;          // threads per sweep group
 constexpr int TPQ = 4;           // threads per probe in the probe sweep
+constexpr int CM = 18;           // children per sweep: up to 17 cuts + one extraction side
+constexpr int ES = NMAX + 1;     // row stride of the probe exponentials (odd: no bank conflicts across probes)
 
 template <typename T> struct BPad;
 template <> struct BPad<uint16_t> { static constexpr int v = 4; };
@@ -37,16 +41,14 @@ template <> struct BPad<float> { static constexpr int v = 1; };
 template <typename T, int D>
 struct BuildLds {
   static constexpr int LDK = D + BPad<T>::v;
-  // byte offsets inside dynamic LDS
   static constexpr int oK = 0;
   static constexpr int oV = oK + NMAX * LDK * (int)sizeof(T);
   static constexpr int oE = ((oV + NMAX * D * (int)sizeof(T)) + 15) & ~15;
-  static constexpr int oR = oE + WMAX * NMAX * 4;
+  static constexpr int oR = oE + WMAX * ES * 4;
   static constexpr int oKap = oR + NMAX * 4;
   static constexpr int oA = oKap + NMAX * 4;
   static constexpr int oKn = oA + NMAX * 4;
-  static constexpr int oS = oKn + NMAX * 4;                   // relevance partials [4][NMAX]
-  static constexpr int oNa = oS + 4 * NMAX * 4;
+  static constexpr int oNa = oKn + NMAX * 4;
   static constexpr int oNn = oNa + 256 * 4;
   static constexpr int oNc = oNn + 256 * 4;
   static constexpr int oNp = oNc + 256 * 4;
@@ -55,13 +57,16 @@ struct BuildLds {
   static constexpr int oNcut = oNk + 256 * 4;
   static constexpr int oND = oNcut + 256 * 4;
   static constexpr int oNR = oND + 256 * 4;
-  static constexpr int oCk = oNR + 256 * 4;                  // child mean k° / k~  [CAND_MAX][D]
-  static constexpr int oCv = oCk + CAND_MAX * D * 4;          // child v~           [CAND_MAX][D]
-  static constexpr int oCon = oCv + CAND_MAX * D * 4;         // contrib [CAND_MAX][WMAX]
-  static constexpr int oCs = oCon + CAND_MAX * WMAX * 4;      // child scalars [8][CAND_MAX]
-  static constexpr int oX = oCs + 8 * CAND_MAX * 4;           // cut lists and misc ints
+  // per sweep group g: child mean k° / k~ [CM][D], child v~ [CM][D], contributions [CM][WMAX]
+  static constexpr int oCk = oNR + 256 * 4;
+  static constexpr int oCv = oCk + 2 * CM * D * 4;
+  static constexpr int oCon = oCv + 2 * CM * D * 4;
+  static constexpr int oCs = oCon + 2 * CM * WMAX * 4;       // child scalars [2][8][CM]
+  static constexpr int oX = oCs + 2 * 8 * CM * 4;            // cut lists and misc ints
   static constexpr int oFlag = oX + 4 * 64 * 4;
   static constexpr int bytes = oFlag + NMAX * 4;
+  // relevance partial sums [8 waves][NMAX] alias the child buffers (used before any sweep)
+  static constexpr int oS = oCk;
 };
 
 int build_lds_bytes(const Dims& dm) {
@@ -77,7 +82,7 @@ __device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
   return (h & 1) ? h + 1 : h;
 }
 
-// Child scalar slots (oCs): 0 n, 1 sumR, 2 mean||k°||, 3 m_eff, 4 p, 5 D, 6 x (cut)
+// child scalar rows in cs: 0 n, 1 sumR, 2 mean||k||, 3 m_eff, 4 p, 5 D
 template <typename T, int D>
 struct Unit {
   using Lay = BuildLds<T, D>;
@@ -94,152 +99,220 @@ struct Unit {
     ck = (float*)(s + Lay::oCk); cv = (float*)(s + Lay::oCv); con = (float*)(s + Lay::oCon);
     cs = (float*)(s + Lay::oCs); xi = (int*)(s + Lay::oX); flag = (int*)(s + Lay::oFlag);
   }
+  __device__ float* gck(int g) { return ck + g * CM * D; }
+  __device__ float* gcv(int g) { return cv + g * CM * D; }
+  __device__ float* gcon(int g) { return con + g * CM * WMAX; }
+  __device__ float* gcs(int g, int row) { return cs + (g * 8 + row) * CM; }
 };
 
-// Evaluate the children [a, xs[c]) (prefix) or [xs[c], b) (suffix) of a node
-// whose local token range is [a, b) (0-based inside the unit, absolute start a0).
-// Writes per child: n, sumR, D into cs[] rows 0, 1, 5.  `want_drop` is unused.
+// DPT consecutive elements of an LDS row as fp32 (16-byte aligned chunks)
+template <int DPT>
+__device__ __forceinline__ void lds_row(const uint16_t* p, float* out) {
+  const uint4* q = (const uint4*)p;
+#pragma unroll
+  for (int k = 0; k < DPT / 8; ++k) {
+    const uint4 w = q[k];
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      out[8 * k + 2 * h] = __uint_as_float(ws[h] << 16);
+      out[8 * k + 2 * h + 1] = __uint_as_float(ws[h] & 0xffff0000u);
+    }
+  }
+}
+template <int DPT>
+__device__ __forceinline__ void lds_row(const float* p, float* out) {
+  const float4* q = (const float4*)p;
+#pragma unroll
+  for (int k = 0; k < DPT / 4; ++k) {
+    const float4 w = q[k];
+    out[4 * k] = w.x; out[4 * k + 1] = w.y; out[4 * k + 2] = w.z; out[4 * k + 3] = w.w;
+  }
+}
+
+// Both sweeps of one node at once.  Group 0 evaluates the prefix children
+// [a, XL[c]), group 1 the suffix children [XR[c], b) (0-based inside the unit,
+// absolute start a0).  Per child: rows 0 n, 1 sum R, 5 D of the group's cs.
 template <typename T, int D>
-__device__ void sweep(Unit<T, D>& U, const Dims& dm, bool prefix, int a, int b, const int* xs, int nx, int64_t a0,
-                      const float* __restrict__ cosT, const float* __restrict__ sinT, const float* qv, float m_q,
-                      float zc_q, int q, float scale) {
+__device__ void sweep2(Unit<T, D>& U, const Dims& dm, int a, int b, const int* XL, int nl, const int* XR, int nr,
+                       int64_t a0, const float* __restrict__ cosT, const float* __restrict__ sinT, const float* qv,
+                       float m_q, float zc_q, float scale) {
   using Lay = BuildLds<T, D>;
   constexpr int H2 = D / 2;
   constexpr int DPT = D / TPQ;
   const int tid = threadIdx.x;
-  float* cn = U.cs + 0 * CAND_MAX;
-  float* cR = U.cs + 1 * CAND_MAX;
-  float* cKm = U.cs + 2 * CAND_MAX;
-  float* cMe = U.cs + 3 * CAND_MAX;
-  float* cP = U.cs + 4 * CAND_MAX;
-  float* cD = U.cs + 5 * CAND_MAX;
-  // ---- phase A: prototype sums (thread per dimension) ----
-  if (tid < D) {
-    const int i = tid;
+  const int g = tid / GT, lt = tid % GT;
+  const bool prefix = g == 0;
+  const int* xs = prefix ? XL : XR;
+  const int nx = prefix ? nl : nr;
+  float* ck = U.gck(g);
+  float* cv = U.gcv(g);
+  float* con = U.gcon(g);
+  float* cn = U.gcs(g, 0);
+  float* cR = U.gcs(g, 1);
+  float* cKm = U.gcs(g, 2);
+  float* cMe = U.gcs(g, 3);
+  float* cD = U.gcs(g, 5);
+  const int t_first = prefix ? a : b - 1;
+  const int step = prefix ? 1 : -1;
+  const int t_last = nx > 0 ? (prefix ? xs[nx - 1] - 1 : xs[0]) : t_first;
+  const int steps = nx > 0 ? (prefix ? t_last - t_first + 1 : t_first - t_last + 1) : 0;
+  // ---- phase A: prototype sums, loads 8 tokens ahead.  Threads lt < D sum
+  // k° of dimension lt (and the scalars); threads D <= lt < 2D sum R v and v of
+  // dimension lt - D. ----
+  if (lt < 2 * D && steps > 0) {
+    const bool kside = lt < D;
+    const int i = kside ? lt : lt - D;
     const int ih = i < H2 ? i : i - H2;
     const int ip = i < H2 ? i + H2 : i - H2;
-    float sk = 0.f, srv = 0.f, sv = 0.f, sr = 0.f, skn = 0.f;
+    float s0 = 0.f, s1 = 0.f, sr = 0.f, skn = 0.f;
     int ci = prefix ? 0 : nx - 1;
-    const int t_first = prefix ? a : b - 1;
-    const int t_last = prefix ? xs[nx - 1] - 1 : xs[0];
-    const int step = prefix ? 1 : -1;
-    const int steps = prefix ? t_last - t_first + 1 : t_first - t_last + 1;
-    for (int it = 0, t = t_first; it < steps && it < NMAX; ++it, t += step) {
-      const int64_t ta = a0 + t;
-      const float c = cosT[ta * H2 + ih], sn = sinT[ta * H2 + ih];
-      const float x = ldf(U.sK, t * Lay::LDK + i), y = ldf(U.sK, t * Lay::LDK + ip);
-      const float kr = i < H2 ? x * c + y * sn : x * c - y * sn;
-      const float v = ldf(U.sV, t * D + i);
-      const float r = U.sR[t];
-      sk += kr;
-      srv += r * v;
-      sv += v;
-      sr += r;
-      skn += U.sKn[t];
-      const bool at = prefix ? (t + 1 == xs[ci]) : (t == xs[ci]);
-      if (at) {
-        const int nch_ = prefix ? xs[ci] - a : b - xs[ci];
-        if (nch_ >= 2) {
-          const float inv = 1.0f / (float)nch_;
-          U.ck[ci * D + i] = sk * inv;
-          const float beta = dm.beta_frac * sr * inv;
-          U.cv[ci * D + i] = (srv + beta * sv) / (sr + (float)nch_ * beta + dm.eps);
+    int xnext = xs[ci];
+    bool done = false;
+    for (int it0 = 0; it0 < steps && !done; it0 += 8) {
+      float f0[8], f1[8], f2[8], f3[8], r8[8], k8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int it = min(it0 + u, steps - 1);
+        const int t = t_first + step * it;
+        if (kside) {
+          const int64_t ta = a0 + t;
+          f0[u] = cosT[ta * H2 + ih];
+          f1[u] = sinT[ta * H2 + ih];
+          f2[u] = ldf(U.sK, t * Lay::LDK + i);
+          f3[u] = ldf(U.sK, t * Lay::LDK + ip);
+          k8[u] = U.sKn[t];
+        } else {
+          f0[u] = ldf(U.sV, t * D + i);
         }
-        if (i == 0) {
-          cn[ci] = (float)nch_;
-          cR[ci] = sr;
-          cKm[ci] = skn / (float)nch_;
+        r8[u] = U.sR[t];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (done || it0 + u >= steps) break;
+        const int t = t_first + step * (it0 + u);
+        if (kside) {
+          s0 += i < H2 ? f2[u] * f0[u] + f3[u] * f1[u] : f2[u] * f0[u] - f3[u] * f1[u];
+          skn += k8[u];
+        } else {
+          s0 += r8[u] * f0[u];
+          s1 += f0[u];
         }
-        ci += prefix ? 1 : -1;
-        if (ci < 0 || ci >= nx) break;
+        sr += r8[u];
+        if (prefix ? (t + 1 == xnext) : (t == xnext)) {
+          const int nch_ = prefix ? xnext - a : b - xnext;
+          if (nch_ >= 2) {
+            const float inv = 1.0f / (float)nch_;
+            if (kside) {
+              ck[ci * D + i] = s0 * inv;
+            } else {
+              const float beta = dm.beta_frac * sr * inv;
+              cv[ci * D + i] = (s0 + beta * s1) / (sr + (float)nch_ * beta + dm.eps);
+            }
+          }
+          if (lt == 0) {
+            cn[ci] = (float)nch_;
+            cR[ci] = sr;
+            cKm[ci] = skn / (float)nch_;
+          }
+          ci += prefix ? 1 : -1;
+          if (ci < 0 || ci >= nx) done = true;
+          else xnext = xs[ci];
+        }
       }
     }
   }
   __syncthreads();
   // ---- phase A2: coherence, multiplicity, representative position, RoPE(k) ----
   {
-    const int wave = tid >> 6, lane = tid & 63;
-    for (int c = wave; c < nx; c += BT / 64) {
+    const int wave = lt >> 6, lane = lt & 63;
+    for (int c = wave; c < nx; c += GT / 64) {
       const int nch_ = (int)cn[c];
       if (nch_ < 2) continue;
       float ss = 0.f;
-      for (int i = lane; i < D; i += 64) ss += U.ck[c * D + i] * U.ck[c * D + i];
+      for (int i = lane; i < D; i += 64) ss += ck[c * D + i] * ck[c * D + i];
       ss = wave_sum(ss);
       const int x0 = prefix ? a : xs[c];
       const int x1 = prefix ? xs[c] : b;
       const int p = round_half_even_mid((int)(a0 + x0), (int)(a0 + x1));
-      float coh = sqrtf(ss) / (cKm[c] + dm.eps);
-      float me = fminf(fmaxf((float)nch_ * coh * coh, 1.0f), (float)nch_);
-      if (lane == 0) { cMe[c] = me; cP[c] = (float)p; }
+      const float coh = sqrtf(ss) / (cKm[c] + dm.eps);
+      const float me = fminf(fmaxf((float)nch_ * coh * coh, 1.0f), (float)nch_);
+      if (lane == 0) cMe[c] = me;
       for (int i = lane; i < H2; i += 64) {
         const float cc = cosT[(int64_t)p * H2 + i], sn = sinT[(int64_t)p * H2 + i];
-        const float m1 = U.ck[c * D + i], m2 = U.ck[c * D + i + H2];
-        U.ck[c * D + i] = m1 * cc - m2 * sn;
-        U.ck[c * D + i + H2] = m2 * cc + m1 * sn;
+        const float m1 = ck[c * D + i], m2 = ck[c * D + i + H2];
+        ck[c * D + i] = m1 * cc - m2 * sn;
+        ck[c * D + i + H2] = m2 * cc + m1 * sn;
       }
     }
   }
   __syncthreads();
-  // ---- phase B: probe sweep (TPQ threads per probe, DPT dims each) ----
+  // ---- phase B: probe sweep (TPQ threads per probe, DPT dims each), loads 4 tokens ahead ----
   {
-    const int sub = tid % TPQ;
+    const int q = lt / TPQ, sub = lt % TPQ;
     const int d0 = sub * DPT;
-    if (q < dm.W) {
+    if (q < dm.W && steps > 0) {
       float M[DPT];
 #pragma unroll
       for (int k = 0; k < DPT; ++k) M[k] = 0.f;
       float Z = 0.f;
       int ci = prefix ? 0 : nx - 1;
-      const int t_first = prefix ? a : b - 1;
-      const int t_last = prefix ? xs[nx - 1] - 1 : xs[0];
-      const int step = prefix ? 1 : -1;
-      const int steps = prefix ? t_last - t_first + 1 : t_first - t_last + 1;
-      for (int it = 0, t = t_first; it < steps && it < NMAX; ++it, t += step) {
-        const float e = U.sE[q * NMAX + t];
-        Z += e;
+      int xnext = xs[ci];
+      bool done = false;
+      for (int it0 = 0; it0 < steps && !done; it0 += 4) {
+        float e4[4];
+        float v4[4][DPT];
 #pragma unroll
-        for (int k = 0; k < DPT; ++k) M[k] += e * ldf(U.sV, t * D + d0 + k);
-        const bool at = prefix ? (t + 1 == xs[ci]) : (t == xs[ci]);
-        if (at) {
-          const int nch_ = (int)cn[ci];
-          if (nch_ >= 2) {
-            float dot = 0.f;
+        for (int u = 0; u < 4; ++u) {
+          const int t = t_first + step * min(it0 + u, steps - 1);
+          e4[u] = U.sE[q * ES + t];
+          lds_row<DPT>(U.sV + t * D + d0, v4[u]);
+        }
 #pragma unroll
-            for (int k = 0; k < DPT; ++k) dot += qv[k] * U.ck[ci * D + d0 + k];
-            dot += __shfl_xor(dot, 1, 64);
-            dot += __shfl_xor(dot, 2, 64);
-            const float zt = cMe[ci] * expf(dot * scale - m_q);
-            float s1 = 0.f, s2 = 0.f;
+        for (int u = 0; u < 4; ++u) {
+          if (done || it0 + u >= steps) break;
+          const int t = t_first + step * (it0 + u);
+          Z += e4[u];
 #pragma unroll
-            for (int k = 0; k < DPT; ++k) {
-              const float df = M[k] - zt * U.cv[ci * D + d0 + k];
-              s1 += df * df;
-              s2 += M[k] * M[k];
+          for (int k = 0; k < DPT; ++k) M[k] += e4[u] * v4[u][k];
+          if (prefix ? (t + 1 == xnext) : (t == xnext)) {
+            if ((int)cn[ci] >= 2) {
+              float dot = 0.f;
+#pragma unroll
+              for (int k = 0; k < DPT; ++k) dot += qv[k] * ck[ci * D + d0 + k];
+              dot += __shfl_xor(dot, 1, 64);
+              dot += __shfl_xor(dot, 2, 64);
+              const float zt = cMe[ci] * expf(dot * scale - m_q);
+              float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+              for (int k = 0; k < DPT; ++k) {
+                const float df = M[k] - zt * cv[ci * D + d0 + k];
+                s1 += df * df;
+                s2 += M[k] * M[k];
+              }
+              s1 += __shfl_xor(s1, 1, 64);
+              s1 += __shfl_xor(s1, 2, 64);
+              s2 += __shfl_xor(s2, 1, 64);
+              s2 += __shfl_xor(s2, 2, 64);
+              const float dz = Z - zt;
+              const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
+              if (sub == 0) con[ci * WMAX + q] = (Z / zc_q) * Dq;
             }
-            s1 += __shfl_xor(s1, 1, 64);
-            s1 += __shfl_xor(s1, 2, 64);
-            s2 += __shfl_xor(s2, 1, 64);
-            s2 += __shfl_xor(s2, 2, 64);
-            const float dz = Z - zt;
-            const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
-            if (sub == 0) U.con[ci * WMAX + q] = (Z / zc_q) * Dq;
+            ci += prefix ? 1 : -1;
+            if (ci < 0 || ci >= nx) done = true;
+            else xnext = xs[ci];
           }
-          ci += prefix ? 1 : -1;
-          if (ci < 0 || ci >= nx) break;
         }
       }
-    } else {
-      // idle probe lanes still take part in the shuffles above only within
-      // their own TPQ group, so nothing to do here
     }
   }
   __syncthreads();
   // ---- phase C: D = mean over probes (fixed order) ----
-  if (tid < nx) {
-    const int c = tid;
+  if (lt < nx) {
+    const int c = lt;
     float acc = 0.f;
     if ((int)cn[c] >= 2) {
-      for (int qq = 0; qq < dm.W; ++qq) acc += U.con[c * WMAX + qq];
+      for (int qq = 0; qq < dm.W; ++qq) acc += con[c * WMAX + qq];
       acc /= (float)dm.W;
     }
     cD[c] = acc;
@@ -257,6 +330,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   constexpr bool BF = sizeof(T) == 2;
   constexpr int KS = BF ? D / 16 : D / 4;
   constexpr int DPT = D / TPQ;
+  constexpr int NW = BT / 64;
   extern __shared__ __align__(16) char smem[];
   Unit<T, D> U(smem);
   const int J = *n_slots;
@@ -276,13 +350,13 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
   const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
 
-  // ---- stage K, V; token scalars ----
+  // ---- stage K, V ----
   for (int e = tid; e < NMAX * D; e += BT) {
     const int t = e / D, c = e % D;
     U.sK[t * Lay::LDK + c] = t < n ? Kp[(int64_t)t * D + c] : (T)0;
     U.sV[t * D + c] = t < n ? Vp[(int64_t)t * D + c] : (T)0;
   }
-  for (int e = tid; e < 4 * NMAX; e += BT) U.sS[e] = 0.f;
+  for (int e = tid; e < NW * NMAX; e += BT) U.sS[e] = 0.f;
   __syncthreads();
 
   // ---- relevance pass 2 and probe exponentials (MFMA logits) ----
@@ -293,7 +367,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
     float sacc[NMAX / 16];
 #pragma unroll
     for (int tt = 0; tt < NMAX / 16; ++tt) sacc[tt] = 0.f;
-    for (int rt = wave; rt < n_rt; rt += BT / 64) {
+    for (int rt = wave; rt < n_rt; rt += NW) {
       const int row_l = rt * 16 + (lane & 15);
       const bool rok = row_l < rows;
       const T* qr = Qp + (int64_t)(rok ? row_l : 0) * D;
@@ -343,7 +417,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
             const int u = rowi[i] % dm.W, hl = rowi[i] / dm.W;
             if (u % dm.hpg == hl) {
               const float mq = tv.probe_m[(int64_t)lg * dm.W + u];
-              U.sE[u * NMAX + t] = expf(x - mq);
+              U.sE[u * ES + t] = expf(x - mq);
             }
           }
         }
@@ -361,7 +435,8 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   const float S = tv.lg_S[lg];
   if (tid < n) {
     const int t = tid;
-    const float s = ((U.sS[t] + U.sS[NMAX + t]) + U.sS[2 * NMAX + t]) + U.sS[3 * NMAX + t];
+    float s = 0.f;
+    for (int w = 0; w < NW; ++w) s += U.sS[w * NMAX + t];
     const float R = s / (S + dm.eps);
     U.sR[t] = R;
     tv.tok_R[(int64_t)lg * dm.N_c + a0 + t] = R;
@@ -373,18 +448,19 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
     }
     U.sKn[t] = sqrtf(kn);
     float am = 0.f;
-    for (int qq = 0; qq < dm.W; ++qq) am += U.sE[qq * NMAX + t] / tv.probe_ZC[(int64_t)lg * dm.W + qq];
+    for (int qq = 0; qq < dm.W; ++qq) am += U.sE[qq * ES + t] / tv.probe_ZC[(int64_t)lg * dm.W + qq];
     U.sA[t] = am / (float)dm.W;
   }
   __syncthreads();
 
-  // ---- probe registers for the sweeps ----
-  const int q = tid / TPQ;
+  // ---- probe registers for the sweeps (same probe in both groups) ----
+  const int lt = tid % GT;
+  const int q = lt / TPQ;
   float qv[DPT];
   float m_q = 0.f, zc_q = 1.f;
   if (q < dm.W) {
     const int hl = q % dm.hpg;
-    const T* qr = Qp + ((int64_t)hl * dm.W + q) * D + (tid % TPQ) * DPT;
+    const T* qr = Qp + ((int64_t)hl * dm.W + q) * D + (lt % TPQ) * DPT;
 #pragma unroll
     for (int k = 0; k < DPT; ++k) qv[k] = ldf(qr, k);
     m_q = tv.probe_m[(int64_t)lg * dm.W + q];
@@ -395,20 +471,26 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   }
 
   // ---- root ----
-  int* cnt = U.xi + 3 * 64;             // [0] node count, [1] head
-  float* cn = U.cs + 0 * CAND_MAX;
-  float* cR = U.cs + 1 * CAND_MAX;
-  float* cD = U.cs + 5 * CAND_MAX;
+  int* XL = U.xi;              // [0..31]
+  int* XR = U.xi + 32;         // [32..63]
+  int* XB = U.xi + 64;         // [64..95] binary cuts
+  int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits, index of p in XL, of p+1 in XR
+  int* cnt = U.xi + 192;       // node count
+  float* cnL = U.gcs(0, 0);
+  float* cRL = U.gcs(0, 1);
+  float* cDL = U.gcs(0, 5);
+  float* cRR = U.gcs(1, 1);
+  float* cDR = U.gcs(1, 5);
   if (tid == 0) {
     U.na[0] = 0; U.nn[0] = n; U.nc[0] = -1; U.np[0] = -1; U.nch[0] = 0; U.nk[0] = 0; U.ncut[0] = -1;
-    U.xi[0] = n;
+    XL[0] = n;
     cnt[0] = 1;
   }
   __syncthreads();
   float Ddrop = 0.f;
   if (n >= 2) {
-    sweep<T, D>(U, dm, true, 0, n, U.xi, 1, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
-    if (tid == 0) { U.nD[0] = cD[0]; U.nR[0] = cR[0]; }
+    sweep2<T, D>(U, dm, 0, n, XL, 1, XR, 0, a0, cosT, sinT, qv, m_q, zc_q, scale);
+    if (tid == 0) { U.nD[0] = cDL[0]; U.nR[0] = cRL[0]; }
   } else if (tid == 0) {
     U.nD[0] = 0.f;
     U.nR[0] = U.sR[0];
@@ -421,10 +503,6 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   __syncthreads();
 
   // ---- top-down refinement in BFS order ----
-  int* XL = U.xi;              // [0..31]
-  int* XR = U.xi + 32;         // [32..63]
-  int* XB = U.xi + 64;         // [64..95] binary cuts
-  int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits
   for (int head = 0;; ++head) {
     __syncthreads();
     const int count = cnt[0];
@@ -458,7 +536,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
       }
       if (rank < dm.k_curv) U.flag[t + 1 - a] = 1;
     }
-    if (tid == 0) U.flag[nv / 2] = 1;            // midpoint a + floor(n/2)
+    if (tid == BT - 1) U.flag[nv / 2] = 1;      // midpoint a + floor(n/2)
     // curvature range and extraction token (wave 0)
     if (wave == 0) {
       float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY;
@@ -485,77 +563,91 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
       }
     }
     __syncthreads();
-    if (tid == 0) {
-      const int p = meta[3];
-      int nb = 0, nl = 0, nr = 0;
-      for (int x = 1; x < nv; ++x)
-        if (U.flag[x]) XB[nb++] = a + x;
-      // prefix children [a, x): binary cuts plus [a, p) when p > a
-      int i1 = 0;
-      bool addp = p > a;
-      for (int k = 0; k <= nb; ++k) {
-        const int xv = k < nb ? XB[k] : 0x7fffffff;
-        if (addp && p < xv) { XL[nl++] = p; addp = false; }
-        if (addp && p == xv) addp = false;
-        if (k < nb) XL[nl++] = xv;
+    // binary cuts XB (ascending) by ballot over the flags, then the prefix list
+    // XL = XB + {p} (if p > a) and suffix list XR = XB + {p+1} (if p+1 < b)
+    int* posL = U.xi + 128;      // index of XB[k] in XL
+    int* posR = U.xi + 160;      // index of XB[k] in XR
+    if (wave == 0) {
+      const bool f0 = lane >= 1 && lane < nv && U.flag[lane];
+      const bool f1 = 64 + lane < nv && U.flag[64 + lane];
+      const uint64_t m0 = __ballot(f0), m1 = __ballot(f1);
+      const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+      const int n0 = __popcll(m0);
+      if (f0) XB[__popcll(m0 & below)] = a + lane;
+      if (f1) XB[n0 + __popcll(m1 & below)] = a + 64 + lane;
+      if (lane == 0) meta[2] = n0 + __popcll(m1);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const int nb = meta[2], p = meta[3];
+      const bool on = lane < nb;
+      const int xk = on ? XB[lane] : 0x7fffffff;
+      const bool useP = p > a, useQ = p + 1 < b;
+      const uint64_t lessP = __ballot(on && xk < p), eqP = __ballot(on && xk == p);
+      const uint64_t lessQ = __ballot(on && xk < p + 1), eqQ = __ballot(on && xk == p + 1);
+      const bool insL = useP && eqP == 0ull, insR = useQ && eqQ == 0ull;
+      if (on) {
+        const int pl = lane + ((insL && xk > p) ? 1 : 0);
+        const int pr = lane + ((insR && xk > p + 1) ? 1 : 0);
+        XL[pl] = xk; posL[lane] = pl;
+        XR[pr] = xk; posR[lane] = pr;
       }
-      (void)i1;
-      // suffix children [x, b): binary cuts plus [p+1, b) when p + 1 < b
-      bool addq = p + 1 < b;
-      for (int k = 0; k <= nb; ++k) {
-        const int xv = k < nb ? XB[k] : 0x7fffffff;
-        if (addq && p + 1 < xv) { XR[nr++] = p + 1; addq = false; }
-        if (addq && p + 1 == xv) addq = false;
-        if (k < nb) XR[nr++] = xv;
+      if (lane == 0) {
+        const int cp = __popcll(lessP), cq = __popcll(lessQ);
+        if (insL) XL[cp] = p;
+        if (insR) XR[cq] = p + 1;
+        meta[0] = nb + (insL ? 1 : 0);
+        meta[1] = nb + (insR ? 1 : 0);
+        meta[6] = useP ? cp : -1;         // index of p in XL ([a, p))
+        meta[7] = useQ ? cq : -1;         // index of p + 1 in XR ([p+1, b))
       }
-      meta[0] = nl; meta[1] = nr; meta[2] = nb;
     }
     __syncthreads();
     const int nl = meta[0], nr = meta[1], nb = meta[2], p = meta[3];
-    // prefix sweep; keep (x, n, R, D) of prefix children in slots 32..
-    sweep<T, D>(U, dm, true, a, b, XL, nl, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
-    float* keepL = U.sS;                       // reuse relevance partials: [0..CAND) D, [32..) R
-    if (tid < nl) { keepL[tid] = cD[tid]; keepL[32 + tid] = cR[tid]; }
-    __syncthreads();
-    sweep<T, D>(U, dm, false, a, b, XR, nr, a0, cosT, sinT, qv, m_q, zc_q, q, scale);
-    float* keepR = U.sS + 64;
-    if (tid < nr) { keepR[tid] = cD[tid]; keepR[32 + tid] = cR[tid]; }
-    __syncthreads();
-    if (tid == 0) {
+    sweep2<T, D>(U, dm, a, b, XL, nl, XR, nr, a0, cosT, sinT, qv, m_q, zc_q, scale);
+    // scores (fp32): best binary cut by a wave-0 argmax (smaller cut wins ties),
+    // then the extraction score and the append by lane 0
+    if (wave == 0) {
       const float kmn = __int_as_float(meta[4]), kmx = __int_as_float(meta[5]);
       const float kr = kmx - kmn;
-      auto findL = [&](int x) { for (int k = 0; k < nl; ++k) if (XL[k] == x) return k; return -1; };
-      auto findR = [&](int x) { for (int k = 0; k < nr; ++k) if (XR[k] == x) return k; return -1; };
       float best = -INFINITY;
-      int bx = -1;
-      for (int k = 0; k < nb; ++k) {
-        const int x = XB[k];
+      int bk = 0x7fffffff;
+      if (lane < nb) {
+        const int x = XB[lane];
         const float kh = kr > 0.f ? (U.sKap[x - 1] - kmn) / kr : 0.f;
-        const float gsc = ((Dv - keepL[findL(x)]) - keepR[findR(x)]) + dm.lam_kappa * kh;
-        if (gsc > best) { best = gsc; bx = x; }
+        best = ((Dv - cDL[posL[lane]]) - cDR[posR[lane]]) + dm.lam_kappa * kh;
+        bk = lane;
       }
-      float dsum = 0.f;
-      int nkid = 1;
-      if (p > a) { dsum += keepL[findL(p)]; ++nkid; }
-      if (p + 1 < b) { dsum += keepR[findR(p + 1)]; ++nkid; }
-      const float gext = (Dv - dsum) / (float)(nkid - 1);
-      const int c0 = count;
-      U.nc[head] = c0;
-      if (best >= gext) {
-        U.nch[head] = 2; U.nk[head] = 1; U.ncut[head] = (int)a0 + bx;
-        const int kl = findL(bx), kr2 = findR(bx);
-        U.na[c0] = a; U.nn[c0] = bx - a; U.nD[c0] = keepL[kl]; U.nR[c0] = keepL[32 + kl];
-        U.na[c0 + 1] = bx; U.nn[c0 + 1] = b - bx; U.nD[c0 + 1] = keepR[kr2]; U.nR[c0 + 1] = keepR[32 + kr2];
-        cnt[0] = count + 2;
-      } else {
-        U.nch[head] = nkid; U.nk[head] = 2; U.ncut[head] = (int)a0 + p;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float b2 = __shfl_xor(best, o, 64);
+        const int k2 = __shfl_xor(bk, o, 64);
+        if (b2 > best || (b2 == best && k2 < bk)) { best = b2; bk = k2; }
+      }
+      if (lane == 0) {
+        const int iL = meta[6], iR = meta[7];
+        float dsum = 0.f;
+        int nkid = 1;
+        if (p > a) { dsum += cDL[iL]; ++nkid; }
+        if (p + 1 < b) { dsum += cDR[iR]; ++nkid; }
+        const float gext = (Dv - dsum) / (float)(nkid - 1);
+        const int c0 = count;
+        U.nc[head] = c0;
         int c = c0;
-        if (p > a) { const int k = findL(p); U.na[c] = a; U.nn[c] = p - a; U.nD[c] = keepL[k]; U.nR[c] = keepL[32 + k]; ++c; }
-        U.na[c] = p; U.nn[c] = 1; U.nD[c] = 0.f; U.nR[c] = U.sR[p]; ++c;
-        if (p + 1 < b) { const int k = findR(p + 1); U.na[c] = p + 1; U.nn[c] = b - p - 1; U.nD[c] = keepR[k]; U.nR[c] = keepR[32 + k]; ++c; }
+        if (best >= gext) {
+          const int bx = XB[bk];
+          U.nch[head] = 2; U.nk[head] = 1; U.ncut[head] = (int)a0 + bx;
+          U.na[c] = a; U.nn[c] = bx - a; U.nD[c] = cDL[posL[bk]]; U.nR[c] = cRL[posL[bk]]; ++c;
+          U.na[c] = bx; U.nn[c] = b - bx; U.nD[c] = cDR[posR[bk]]; U.nR[c] = cRR[posR[bk]]; ++c;
+        } else {
+          U.nch[head] = nkid; U.nk[head] = 2; U.ncut[head] = (int)a0 + p;
+          if (p > a) { U.na[c] = a; U.nn[c] = p - a; U.nD[c] = cDL[iL]; U.nR[c] = cRL[iL]; ++c; }
+          U.na[c] = p; U.nn[c] = 1; U.nD[c] = 0.f; U.nR[c] = U.sR[p]; ++c;
+          if (p + 1 < b) { U.na[c] = p + 1; U.nn[c] = b - p - 1; U.nD[c] = cDR[iR]; U.nR[c] = cRR[iR]; ++c; }
+        }
+        for (int k = c0; k < c; ++k) { U.nc[k] = -1; U.np[k] = head; U.nch[k] = 0; U.nk[k] = 0; U.ncut[k] = -1; }
         cnt[0] = c;
       }
-      for (int c = c0; c < cnt[0]; ++c) { U.nc[c] = -1; U.np[c] = head; U.nch[c] = 0; U.nk[c] = 0; U.ncut[c] = -1; }
     }
   }
   __syncthreads();
@@ -584,7 +676,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
     tv.unit_nn[unit] = count;
     tv.unit_Ddrop[unit] = Ddrop;
   }
-  (void)cn;
+  (void)cnL;
 }
 
 hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void* V, const void* Q,

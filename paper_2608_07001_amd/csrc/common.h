@@ -13,7 +13,7 @@ constexpr int NMAX = 128;        // longest slot (n_max); units hold at most 2*N
 constexpr int NODE_MAX = 2 * NMAX - 1;
 constexpr int WMAX = 64;         // window queries
 constexpr int DMAX = 128;        // head dim
-constexpr int CAND_MAX = 20;     // prefix (or suffix) children per refinement: 17 cuts + extraction side
+constexpr int CAND_MAX = 18;     // prefix (or suffix) children per refinement: 17 cuts + extraction side
 
 // Every size and hyperparameter a kernel needs, passed by value.
 struct Dims {
