@@ -28,6 +28,7 @@ def parse():
     ap.add_argument("--x", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prune", action="store_true", help="build every tree completely")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
     return ap.parse_args()
 
@@ -106,7 +107,8 @@ def main():
     dev = "cuda"
     case = make_case(sh, args.seed, device=dev)
     cfg = gk.config_for(L=sh.L, G=sh.G, H=sh.H, d=sh.d, W=sh.W, N_ctx=sh.N_ctx, x=sh.x,
-                        dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D)
+                        dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D,
+                        flags=0 if args.no_prune else gk.FLAG_PRUNE)
     buf = gk.allocate(cfg, dev)
     p = buf.plan
     stream = torch.cuda.current_stream()
@@ -120,7 +122,7 @@ def main():
                    buf.seg_ws, stream)
         mark(1)
         gk.build_trees(cfg, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
-                       buf.n_slots, buf.kappa, buf.trees, stream)
+                       buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"])
         mark(2)
         gk.score(cfg, case["omega_raw"], buf.trees, stream)
         mark(3)
@@ -158,7 +160,9 @@ def main():
         "dtype": sh.dtype, "data": "synthetic (seeded Llama-shaped cache, see DESIGN.md)",
         "config": {"workload": f"{sh.name}: L={sh.L} G={sh.G} H={sh.H} d={sh.d} N_ctx={sh.N_ctx} W={sh.W} "
                                f"x={sh.x:g} ({sh.dtype})",
-                   "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item())},
+                   "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),
+                   "pruned_build": not args.no_prune,
+                   "tree_nodes": int(gk.tree_arrays(p, buf.trees)["unit_nn"].sum().item())},
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": stage_ms,
         "wall_s": wall,

@@ -74,7 +74,11 @@ typedef struct {
   int32_t k_curv;                            /* 16 curvature split candidates */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph, alpha_floor;           /* must be 0 on this path */
+  int32_t flags;                             /* GRACEKV_FLAG_PRUNE: budget-aware pruning of the tree build */
 } gracekv_config;
+
+/* Budget-aware pruning of the tree build (output unchanged; see gracekv_build_trees). */
+#define GRACEKV_FLAG_PRUNE 1
 
 /* Sizes derived from a config (host only). */
 typedef struct {
@@ -93,7 +97,7 @@ typedef struct {
          off_sp_U, off_sp_E, off_sp_cost, off_sp_exec,
          off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
          off_tok_R, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
-         off_omega, off_status, off_slots, off_nslots, off_partial;
+         off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
 } gracekv_plan;
 
@@ -134,6 +138,8 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  *   K, V       [L][G][T][d], Q [L][H][W][d] (cfg->dtype)
  *   rope_cos/rope_sin [T][d/2] fp32
  *   slot_starts, n_slots, kappa: outputs of gracekv_segment (or caller-made)
+ *   omega_raw  [L][G] fp32 raw sensitivity (or NULL for ones); read only with
+ *              GRACEKV_FLAG_PRUNE, which needs the gains to bound the auction
  *   trees      the tree buffer (plan.tree_bytes).  Unit u = (l*G + g)*J_cap + j
  *              owns node slots [(l*G+g)*2*N_c + 2*a_j, ... + 2*n_j); nodes are in
  *              BFS order (root first; children of a node are contiguous, left to
@@ -145,11 +151,19 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  *              values R^tok [L*G][N_c] fp32; per (l,g) row statistics of the
  *              relevance softmax and the probe shifts m_q and Z_q(C); a copy of
  *              the slot partition (read by score, select and pack).
- *   ws         unused (pass NULL, 0); reserved. */
+ *   ws         unused (pass NULL, 0); reserved.
+ * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
+ * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops
+ * known so far gives theta_lb, the (B_free-1)-th largest effective key among
+ * them, which bounds the final cut from below (more ops only raise it and
+ * known effective keys never change); a node is refined only if the op that
+ * creates it has E >= theta_lb.  A node that is not refined could be neither
+ * split nor on the final frontier, so score, select and pack give the same
+ * result as the full build. */
 gracekv_status gracekv_build_trees(const gracekv_config* cfg, const void* K, const void* V, const void* Q,
                                    const float* rope_cos, const float* rope_sin,
                                    const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
-                                   void* trees, void* ws, size_t ws_bytes, void* stream);
+                                   const float* omega_raw, void* trees, void* ws, size_t ws_bytes, void* stream);
 
 /* Gains, utilities and priority keys (App. A.5 eq:app_operation_gains,
  * eq:app_operation_costs, eq:app_unit_utility; eq:app_head_sensitivity).

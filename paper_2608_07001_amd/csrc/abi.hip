@@ -58,6 +58,8 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.status = (int32_t*)(b + p.off_status);
   v.slots = (int32_t*)(b + p.off_slots);
   v.nslots = (int32_t*)(b + p.off_nslots);
+  v.theta = (uint64_t*)(b + p.off_theta);
+  v.selstate = (void*)(b + p.off_selstate);
   return v;
 }
 
@@ -113,6 +115,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->flags & ~GRACEKV_FLAG_PRUNE) return GRACEKV_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
   if (c->W > WMAX || c->n_seg > 8) return GRACEKV_ERR_UNSUPPORTED;
   if (c->n_min < 16 || c->n_max > NMAX || c->n_max < c->n_min || c->n0 < 1) return GRACEKV_ERR_UNSUPPORTED;
@@ -169,6 +172,8 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_slots, (size_t)(p->J_cap + 1) * 4);
   put(p->off_nslots, 16);
   put(p->off_partial, (size_t)LG * rowstats_chunks(dm) * dm.rows * 16);
+  put(p->off_theta, 16);
+  put(p->off_selstate, selstate_bytes());
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
   p->sel_ws_bytes = select_ws_bytes(dm);
@@ -209,8 +214,8 @@ gracekv_status gracekv_segment(const gracekv_config* c, const void* hidden, cons
 
 gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const void* V, const void* Q,
                                    const float* rope_cos, const float* rope_sin, const int32_t* slot_starts,
-                                   const int32_t* n_slots, const float* kappa, void* trees, void* ws, size_t ws_bytes,
-                                   void* stream) {
+                                   const int32_t* n_slots, const float* kappa, const float* omega_raw, void* trees,
+                                   void* ws, size_t ws_bytes, void* stream) {
   (void)ws; (void)ws_bytes;
   gracekv_plan p;
   gracekv_status s = prep(c, &p);
@@ -222,11 +227,19 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   TreeView tv = make_view(trees, p);
   hipStream_t st = (hipStream_t)stream;
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return GRACEKV_ERR_HIP;
-  e = launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st);
-  if (e != hipSuccess) return GRACEKV_ERR_HIP;
-  return hip_status(launch_build(dm, p.build_lds_bytes, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st));
+  if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess) return GRACEKV_ERR_HIP;
+  auto build = [&](int mode) {
+    return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
+  };
+  if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
+  // pruned: roots -> bound -> root splits -> tighter bound -> the rest
+  if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (build(BUILD_ROOT) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (build(BUILD_ROOT_SPLIT) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  return hip_status(build(BUILD_CONTINUE));
 }
 
 gracekv_status gracekv_score(const gracekv_config* c, const float* omega_raw, void* trees, void* stream) {

@@ -64,7 +64,9 @@ struct BuildLds {
   static constexpr int oCs = oCon + 2 * CM * WMAX * 4;       // child scalars [2][8][CM]
   static constexpr int oX = oCs + 2 * 8 * CM * 4;            // cut lists and misc ints
   static constexpr int oFlag = oX + 4 * 64 * 4;
-  static constexpr int bytes = oFlag + NMAX * 4;
+  static constexpr int oNE = oFlag + NMAX * 4;                // effective key of each node's creating op
+  static constexpr int oNU = oNE + 256 * 8;                   // utility of each node's Split
+  static constexpr int bytes = oNU + 256 * 4;
   // relevance partial sums [8 waves][NMAX] alias the child buffers (used before any sweep)
   static constexpr int oS = oCk;
 };
@@ -90,6 +92,7 @@ struct Unit {
   T* sK; T* sV; float* sE; float* sR; float* sKap; float* sA; float* sKn; float* sS;
   int* na; int* nn; int* nc; int* np; int* nch; int* nk; int* ncut; float* nD; float* nR;
   float* ck; float* cv; float* con; float* cs; int* xi; int* flag;
+  uint64_t* nE; float* nU;
   __device__ Unit(char* base) : s(base) {
     sK = (T*)(s + Lay::oK); sV = (T*)(s + Lay::oV); sE = (float*)(s + Lay::oE); sR = (float*)(s + Lay::oR);
     sKap = (float*)(s + Lay::oKap); sA = (float*)(s + Lay::oA); sKn = (float*)(s + Lay::oKn); sS = (float*)(s + Lay::oS);
@@ -98,6 +101,7 @@ struct Unit {
     nD = (float*)(s + Lay::oND); nR = (float*)(s + Lay::oNR);
     ck = (float*)(s + Lay::oCk); cv = (float*)(s + Lay::oCv); con = (float*)(s + Lay::oCon);
     cs = (float*)(s + Lay::oCs); xi = (int*)(s + Lay::oX); flag = (int*)(s + Lay::oFlag);
+    nE = (uint64_t*)(s + Lay::oNE); nU = (float*)(s + Lay::oNU);
   }
   __device__ float* gck(int g) { return ck + g * CM * D; }
   __device__ float* gcv(int g) { return cv + g * CM * D; }
@@ -321,7 +325,7 @@ __device__ void sweep2(Unit<T, D>& U, const Dims& dm, int a, int b, const int* X
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, const T* __restrict__ V,
+__global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __restrict__ K, const T* __restrict__ V,
                                                const T* __restrict__ Q, const float* __restrict__ cosT,
                                                const float* __restrict__ sinT, const int32_t* __restrict__ slot_starts,
                                                const int32_t* __restrict__ n_slots, const float* __restrict__ kappa,
@@ -346,6 +350,28 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   }
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const float scale = 1.0f / sqrtf((float)D);
+  const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
+  const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+  const bool cont = mode == BUILD_ROOT_SPLIT || mode == BUILD_CONTINUE;
+  const uint64_t theta = mode == BUILD_FULL || mode == BUILD_ROOT ? 0ull : *tv.theta;
+  int* cnt = U.xi + 192;       // node count
+  if (cont) {
+    // resume from the node table: refine only nodes whose creating op reaches theta
+    const int nn0 = tv.unit_nn[unit];
+    const uint64_t Eadd = tv.add_E[unit];
+    bool any = false;
+    for (int i = tid; i < nn0; i += BT) {
+      const int64_t sl = base + i;
+      U.na[i] = tv.node_a[sl] - (int)a0; U.nn[i] = tv.node_n[sl]; U.nc[i] = tv.node_child[sl];
+      U.np[i] = tv.node_parent[sl]; U.nch[i] = tv.node_nch[sl]; U.nk[i] = tv.node_kind[sl];
+      U.ncut[i] = tv.node_cut[sl]; U.nD[i] = tv.node_D[sl]; U.nR[i] = tv.node_R[sl]; U.nU[i] = tv.sp_U[sl];
+      const uint64_t ec = U.np[i] < 0 ? Eadd : tv.sp_E[base + U.np[i]];
+      U.nE[i] = ec;
+      any |= U.nch[i] == 0 && U.nn[i] >= 2 && ec >= theta && (mode == BUILD_CONTINUE || i == 0);
+    }
+    if (tid == 0) cnt[0] = nn0;
+    if (!__syncthreads_or(any)) return;
+  }
   const T* Kp = K + ((int64_t)lg * dm.T + a0) * D;
   const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
   const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
@@ -475,40 +501,48 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
   int* XR = U.xi + 32;         // [32..63]
   int* XB = U.xi + 64;         // [64..95] binary cuts
   int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits, index of p in XL, of p+1 in XR
-  int* cnt = U.xi + 192;       // node count
-  float* cnL = U.gcs(0, 0);
   float* cRL = U.gcs(0, 1);
   float* cDL = U.gcs(0, 5);
   float* cRR = U.gcs(1, 1);
   float* cDR = U.gcs(1, 5);
-  if (tid == 0) {
-    U.na[0] = 0; U.nn[0] = n; U.nc[0] = -1; U.np[0] = -1; U.nch[0] = 0; U.nk[0] = 0; U.ncut[0] = -1;
-    XL[0] = n;
-    cnt[0] = 1;
-  }
-  __syncthreads();
+  const float w = tv.omega[lg];
   float Ddrop = 0.f;
-  if (n >= 2) {
-    sweep2<T, D>(U, dm, 0, n, XL, 1, XR, 0, a0, cosT, sinT, qv, m_q, zc_q, scale);
-    if (tid == 0) { U.nD[0] = cDL[0]; U.nR[0] = cRL[0]; }
-  } else if (tid == 0) {
-    U.nD[0] = 0.f;
-    U.nR[0] = U.sR[0];
+  if (!cont) {
+    if (tid == 0) {
+      U.na[0] = 0; U.nn[0] = n; U.nc[0] = -1; U.np[0] = -1; U.nch[0] = 0; U.nk[0] = 0; U.ncut[0] = -1;
+      XL[0] = n;
+      cnt[0] = 1;
+    }
+    __syncthreads();
+    if (n >= 2) {
+      sweep2<T, D>(U, dm, 0, n, XL, 1, XR, 0, a0, cosT, sinT, qv, m_q, zc_q, scale);
+      if (tid == 0) { U.nD[0] = cDL[0]; U.nR[0] = cRL[0]; }
+    } else if (tid == 0) {
+      U.nD[0] = 0.f;
+      U.nR[0] = U.sR[0];
+    }
+    if (tid == 0) {
+      float dd = 0.f;
+      for (int t = 0; t < n; ++t) dd += U.sA[t];
+      Ddrop = dd;
+      if (mode != BUILD_FULL) {          // the Add key (the root's creating op)
+        const float Ua = utility(add_gain(w, U.nR[0], Ddrop, U.nD[0]), 1);
+        U.nE[0] = op_key(Ua, ord * 256u);
+        tv.add_U[unit] = Ua;
+        tv.add_E[unit] = U.nE[0];
+      }
+    }
+    __syncthreads();
   }
-  if (tid == 0) {
-    float dd = 0.f;
-    for (int t = 0; t < n; ++t) dd += U.sA[t];
-    Ddrop = dd;
-  }
-  __syncthreads();
 
   // ---- top-down refinement in BFS order ----
   for (int head = 0;; ++head) {
     __syncthreads();
     const int count = cnt[0];
-    if (head >= count) break;
+    if (head >= count || mode == BUILD_ROOT || (mode == BUILD_ROOT_SPLIT && head > 0)) break;
     const int a = U.na[head], nv = U.nn[head], b = a + nv;
-    if (nv < 2) continue;
+    if (nv < 2 || U.nch[head] > 0) continue;                  // leaf, or refined by an earlier pass
+    if (mode != BUILD_FULL && U.nE[head] < theta) continue;    // cannot reach the auction's cut
     const float Dv = U.nD[head];
     if (nv == 2) {
       if (tid == 0) {
@@ -520,6 +554,13 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
           U.nD[c0 + k] = 0.f; U.nR[c0 + k] = U.sR[a + k];
         }
         cnt[0] = count + 2;
+        if (mode != BUILD_FULL) {
+          const float Us = utility(split_gain(w, U.nR[head], Dv, U.nD[c0] + U.nD[c0 + 1]), 1);
+          const uint64_t k = op_key(Us, ord * 256u + 1u + (uint32_t)head);
+          const uint64_t E = k < U.nE[head] ? k : U.nE[head];
+          U.nU[head] = Us;
+          U.nE[c0] = E; U.nE[c0 + 1] = E;
+        }
       }
       continue;
     }
@@ -647,39 +688,60 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, const T* __restrict__ K, 
         }
         for (int k = c0; k < c; ++k) { U.nc[k] = -1; U.np[k] = head; U.nch[k] = 0; U.nk[k] = 0; U.ncut[k] = -1; }
         cnt[0] = c;
+        if (mode != BUILD_FULL) {
+          float sd = 0.f;
+          for (int k = c0; k < c; ++k) sd += U.nD[k];
+          const float Us = utility(split_gain(w, U.nR[head], Dv, sd), c - c0 - 1);
+          const uint64_t kk = op_key(Us, ord * 256u + 1u + (uint32_t)head);
+          const uint64_t E = kk < U.nE[head] ? kk : U.nE[head];
+          U.nU[head] = Us;
+          for (int k = c0; k < c; ++k) U.nE[k] = E;
+        }
       }
     }
   }
   __syncthreads();
   // ---- write the node table ----
   const int count = cnt[0];
-  const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
   for (int i = tid; i < 2 * n; i += BT) {
-    const int64_t s = base + i;
+    const int64_t sl = base + i;
     if (i < count) {
-      tv.node_a[s] = (int32_t)a0 + U.na[i];
-      tv.node_n[s] = U.nn[i];
-      tv.node_child[s] = U.nc[i];
-      tv.node_parent[s] = U.np[i];
-      tv.node_nch[s] = (uint8_t)U.nch[i];
-      tv.node_kind[s] = (uint8_t)U.nk[i];
-      tv.node_cut[s] = U.ncut[i];
-      tv.node_D[s] = U.nD[i];
-      tv.node_R[s] = U.nR[i];
+      tv.node_a[sl] = (int32_t)a0 + U.na[i];
+      tv.node_n[sl] = U.nn[i];
+      tv.node_child[sl] = U.nc[i];
+      tv.node_parent[sl] = U.np[i];
+      tv.node_nch[sl] = (uint8_t)U.nch[i];
+      tv.node_kind[sl] = (uint8_t)U.nk[i];
+      tv.node_cut[sl] = U.ncut[i];
+      tv.node_D[sl] = U.nD[i];
+      tv.node_R[sl] = U.nR[i];
+      if (mode != BUILD_FULL) {          // keys of the Splits known so far (refined nodes)
+        const int c = U.nch[i];
+        if (c > 0) {
+          const uint64_t k = op_key(U.nU[i], ord * 256u + 1u + (uint32_t)i);
+          tv.sp_U[sl] = U.nU[i];
+          tv.sp_E[sl] = k < U.nE[i] ? k : U.nE[i];
+          tv.sp_cost[sl] = (uint8_t)(c - 1);
+        } else {
+          tv.sp_U[sl] = 0.f;
+          tv.sp_E[sl] = 0;
+          tv.sp_cost[sl] = 0;
+        }
+        tv.sp_exec[sl] = 0;
+      }
     } else {
-      tv.sp_cost[s] = 0;
-      tv.sp_E[s] = 0;
-      tv.sp_exec[s] = 0;
+      tv.sp_cost[sl] = 0;
+      tv.sp_E[sl] = 0;
+      tv.sp_exec[sl] = 0;
     }
   }
   if (tid == 0) {
     tv.unit_nn[unit] = count;
-    tv.unit_Ddrop[unit] = Ddrop;
+    if (!cont) tv.unit_Ddrop[unit] = Ddrop;
   }
-  (void)cnL;
 }
 
-hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void* V, const void* Q,
+hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
                         const float* kappa, const TreeView& tv, hipStream_t st) {
   const dim3 grid((unsigned)((int64_t)dm.L * dm.G * dm.J_cap));
@@ -688,7 +750,7 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void
     auto fn = k_build<TT, DD>;                                                                             \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes); \
     if (e0 != hipSuccess) return e0;                                                                       \
-    hipLaunchKernelGGL(fn, grid, dim3(BT), lds_bytes, st, dm, (const TT*)K, (const TT*)V, (const TT*)Q, cosT, \
+    hipLaunchKernelGGL(fn, grid, dim3(BT), lds_bytes, st, dm, mode, (const TT*)K, (const TT*)V, (const TT*)Q, cosT, \
                        sinT, slot_starts, n_slots, kappa, tv);                                             \
   } while (0)
   if (dm.dtype == GRACEKV_BF16) {

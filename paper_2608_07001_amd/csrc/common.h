@@ -58,7 +58,30 @@ struct TreeView {
   int32_t* status;      // device status word
   int32_t* slots;       // [J_cap + 1] copy of the slot starts (then N_c)
   int32_t* nslots;      // [1] J
+  uint64_t* theta;      // [1] lower bound of the auction cut used by the pruned build
+  void* selstate;       // radix-select state of that bound
 };
+
+// Build modes: FULL refines every node; ROOT evaluates only the root (and its
+// Add key); ROOT_SPLIT refines the root of units whose Add key reaches theta;
+// CONTINUE refines every unrefined node whose creating op reaches theta.
+enum { BUILD_FULL = 0, BUILD_ROOT = 1, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3 };
+
+// ---- gains, utilities and keys (shared by the build and score kernels so that
+// both produce bit-identical keys) -------------------------------------------
+// Add: Delta = w R(root) (D_drop - D); Split: Delta = w R(v) (D(v) - sum D(children)),
+// cost |child| - 1; U = max(Delta, 0) / cost (App. A.5 eq:app_operation_gains,
+// eq:app_operation_costs, eq:app_unit_utility; App. C.5 clamp at zero).
+__device__ __forceinline__ float add_gain(float w, float R, float Ddrop, float D) { return w * R * (Ddrop - D); }
+__device__ __forceinline__ float split_gain(float w, float R, float D, float sumD) { return w * R * (D - sumD); }
+__device__ __forceinline__ float utility(float gain, int cost) {
+  const float g = gain > 0.f ? gain : 0.f;
+  return cost == 1 ? g : g / (float)cost;
+}
+// unique priority: larger U first, then the smaller id
+__device__ __forceinline__ uint64_t op_key(float U, uint32_t id) {
+  return ((uint64_t)__float_as_uint(U) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
 
 Dims make_dims(const gracekv_config& c, const gracekv_plan& p);
 TreeView make_view(void* base, const gracekv_plan& p);
@@ -118,9 +141,12 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
 // ---- launchers (each defined in its own translation unit) -----------------
 hipError_t launch_rowstats(const Dims& dm, const void* K, const void* Q, const TreeView& tv, float4* partial,
                            hipStream_t st);
-hipError_t launch_build(const Dims& dm, int lds_bytes, const void* K, const void* V, const void* Q,
+hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
                         const float* kappa, const TreeView& tv, hipStream_t st);
+hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
+hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st);
+size_t selstate_bytes();
 hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st);
 hipError_t launch_pack(const Dims& dm, const void* K, const void* V, const float* cosT, const float* sinT,

@@ -43,10 +43,9 @@ struct SelState {
 };
 
 size_t select_ws_bytes(const Dims&) { return sizeof(SelState); }
+size_t selstate_bytes() { return sizeof(SelState); }
 
-__device__ __forceinline__ uint64_t make_key(float U, uint32_t id) {
-  return ((uint64_t)__float_as_uint(U) << 32) | (uint64_t)(0xFFFFFFFFu - id);
-}
+__device__ __forceinline__ uint64_t make_key(float U, uint32_t id) { return op_key(U, id); }
 
 __global__ void k_omega(Dims dm, const float* __restrict__ omega_raw, TreeView tv) {
   __shared__ float red[256];
@@ -77,11 +76,11 @@ __global__ void k_score(Dims dm, TreeView tv) {
   const int nn = tv.unit_nn[u];
   if (nn < 1) { tv.add_U[u] = 0.f; tv.add_E[u] = 0; tv.add_exec[u] = 0; return; }
   bool bad = false;
-  float gain = w * tv.node_R[base] * (tv.unit_Ddrop[u] - tv.node_D[base]);
+  const float gain = add_gain(w, tv.node_R[base], tv.unit_Ddrop[u], tv.node_D[base]);
   bad |= gain != gain;
-  gain = gain > 0.f ? gain : 0.f;
-  const uint64_t kadd = make_key(gain, ord * 256u);
-  tv.add_U[u] = gain;
+  const float Ua = utility(gain, 1);
+  const uint64_t kadd = make_key(Ua, ord * 256u);
+  tv.add_U[u] = Ua;
   tv.add_E[u] = kadd;
   tv.add_exec[u] = 0;
   for (int i = 0; i < nn; ++i) {
@@ -97,10 +96,9 @@ __global__ void k_score(Dims dm, TreeView tv) {
     const int c0 = tv.node_child[s];
     float sd = 0.f;
     for (int k = 0; k < nch; ++k) sd += tv.node_D[base + c0 + k];
-    float g = w * tv.node_R[s] * (tv.node_D[s] - sd);
+    const float g = split_gain(w, tv.node_R[s], tv.node_D[s], sd);
     bad |= g != g;
-    g = g > 0.f ? g : 0.f;
-    const float Uv = g / (float)(nch - 1);
+    const float Uv = utility(g, nch - 1);
     const uint64_t k = make_key(Uv, ord * 256u + 1u + (uint32_t)i);
     const int par = tv.node_parent[s];
     const uint64_t Ep = par < 0 ? kadd : tv.sp_E[base + par];
@@ -109,6 +107,11 @@ __global__ void k_score(Dims dm, TreeView tv) {
     tv.sp_cost[s] = (uint8_t)(nch - 1);
   }
   if (bad) atomicOr(tv.status, 1);
+}
+
+hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st) {
+  hipLaunchKernelGGL(k_omega, dim3(1), dim3(256), 0, st, dm, omega_raw, tv);
+  return hipGetLastError();
 }
 
 hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st) {
@@ -332,6 +335,28 @@ hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, vo
   hipLaunchKernelGGL(k_sel_group, dim3(1), dim3(64), 0, st, dm, tv, S);
   hipLaunchKernelGGL(k_sel_resid_find, dim3(blocks), dim3(256), 0, st, dm, tv, S);
   hipLaunchKernelGGL(k_sel_finish, dim3(1), dim3(64), 0, st, dm, tv, S, b_used);
+  return hipGetLastError();
+}
+
+// Lower bound of the cut over the ops known so far (the pruned build): the
+// same cost-weighted radix select; with every known op affordable nothing can
+// be pruned (bound 0); with B_free <= 1 no Split can execute (bound max).
+__global__ void k_theta_store(Dims dm, const SelState* S, uint64_t* theta) {
+  if (threadIdx.x != 0) return;
+  const int mode = S->mode;
+  *theta = mode == SEL_SELECT ? S->prefix : (mode == SEL_ALL ? 0ull : ~0ull);
+}
+
+hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st) {
+  SelState* S = (SelState*)tv.selstate;
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S);
+  const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
+  const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
+  for (int pass = 0; pass < 8; ++pass) {
+    hipLaunchKernelGGL(k_sel_hist, dim3(blocks), dim3(256), 0, st, dm, tv, S, pass);
+    hipLaunchKernelGGL(k_sel_scan, dim3(1), dim3(64), 0, st, dm, S, pass);
+  }
+  hipLaunchKernelGGL(k_theta_store, dim3(1), dim3(64), 0, st, dm, (const SelState*)S, tv.theta);
   return hipGetLastError();
 }
 

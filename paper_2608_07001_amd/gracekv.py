@@ -37,14 +37,16 @@ class Config(ctypes.Structure):
                 ("lam_d", ctypes.c_float), ("lam_n", ctypes.c_float), ("c_cut", ctypes.c_float),
                 ("lam_Z", ctypes.c_float), ("lam_M", ctypes.c_float), ("k_curv", ctypes.c_int32),
                 ("lam_kappa", ctypes.c_float), ("beta_frac", ctypes.c_float), ("eps", ctypes.c_float),
-                ("lambda_graph", ctypes.c_float), ("alpha_floor", ctypes.c_float)]
+                ("lambda_graph", ctypes.c_float), ("alpha_floor", ctypes.c_float), ("flags", ctypes.c_int32)]
+
+FLAG_PRUNE = 1
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",
          "off_node_cut", "off_node_D", "off_node_R", "off_sp_U", "off_sp_E", "off_sp_cost", "off_sp_exec",
          "off_unit_nn", "off_unit_Ddrop", "off_add_U", "off_add_E", "off_add_exec", "off_tok_R",
          "off_row_stats", "off_probe_m", "off_probe_ZC", "off_lg_S", "off_omega", "off_status", "off_slots",
-         "off_nslots", "off_partial"]
+         "off_nslots", "off_partial", "off_theta", "off_selstate"]
 
 
 class Plan(ctypes.Structure):
@@ -78,7 +80,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_plan_sizes": [ctypes.POINTER(Config), ctypes.POINTER(Plan)],
         "gracekv_check": [ctypes.POINTER(Config), P, P],
         "gracekv_segment": [ctypes.POINTER(Config), P, P, P, P, P, P, P, S, P],
-        "gracekv_build_trees": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, S, P],
+        "gracekv_build_trees": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, S, P],
         "gracekv_score": [ctypes.POINTER(Config), P, P, P],
         "gracekv_select": [ctypes.POINTER(Config), P, P, P, S, P],
         "gracekv_pack": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
@@ -137,10 +139,10 @@ def segment(cfg, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, str
                               _stream(stream)), "segment")
 
 
-def build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, trees, stream=None):
+def build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, trees, stream=None, omega_raw=None):
     _ok(lib().gracekv_build_trees(ctypes.byref(cfg), _ptr(K), _ptr(V), _ptr(Q), _ptr(rope_cos), _ptr(rope_sin),
-                                  _ptr(slot_starts), _ptr(n_slots), _ptr(kappa), _ptr(trees), None, 0,
-                                  _stream(stream)), "build_trees")
+                                  _ptr(slot_starts), _ptr(n_slots), _ptr(kappa), _ptr(omega_raw), _ptr(trees), None,
+                                  0, _stream(stream)), "build_trees")
 
 
 def score(cfg, omega_raw, trees, stream=None):
@@ -247,7 +249,7 @@ def compress(buf: Buffers, K, V, Q, rope_cos, rope_sin, hidden, surprisal, omega
     if slot_starts is None:
         segment(cfg, hidden, surprisal, buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots, buf.seg_ws, stream)
         kappa, slot_starts, n_slots = buf.kappa, buf.slot_starts, buf.n_slots
-    build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, buf.trees, stream)
+    build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, buf.trees, stream, omega_raw=omega_raw)
     score(cfg, omega_raw, buf.trees, stream)
     select(cfg, buf.trees, buf.b_used, buf.sel_ws, stream)
     pack(cfg, K, V, rope_cos, rope_sin, buf.trees, buf.offsets, buf.counts, buf.K_out, buf.V_out, buf.pos_out,

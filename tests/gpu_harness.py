@@ -25,10 +25,10 @@ def np32(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy()
 
 
-def make_cfg(shape, x=None):
+def make_cfg(shape, x=None, flags=0):
     return gk.config_for(L=shape.L, G=shape.G, H=shape.H, d=shape.d, W=shape.W, N_ctx=shape.N_ctx,
                          x=float(shape.x if x is None else x), dtype=gk.BF16 if shape.dtype == "bf16" else gk.F32,
-                         n_seg=shape.n_seg, D_hidden=shape.D)
+                         n_seg=shape.n_seg, D_hidden=shape.D, flags=flags)
 
 
 def to_dev(case: dict, device="cuda") -> dict:
@@ -36,10 +36,10 @@ def to_dev(case: dict, device="cuda") -> dict:
 
 
 def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Optional[torch.Tensor] = None,
-            omega=True) -> dict:
+            omega=True, prune=False) -> dict:
     """All five calls through the C ABI; returns host copies of every output."""
     sh = case_dev["shape"]
-    cfg = make_cfg(sh, x)
+    cfg = make_cfg(sh, x, gk.FLAG_PRUNE if prune else 0)
     buf = gk.allocate(cfg)
     ss = ns = kp = None
     if slots is not None:

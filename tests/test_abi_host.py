@@ -80,7 +80,7 @@ def test_plan_rejections():
     assert e.value.status == -3
     for bad, code in [(dict(lambda_graph=0.3), -2), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
                       (dict(W=65), -2), (dict(H=30), -1), (dict(x=0.5), -1), (dict(n_min=8), -2),
-                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1)]:
+                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=2), -1)]:
         with pytest.raises(gk.GraceKVError) as e:
             gk.plan_sizes(_cfg(**bad))
         assert e.value.status == code, bad
@@ -90,7 +90,7 @@ def test_null_pointers_are_refused_before_any_launch():
     c = _cfg(N_ctx=8192, x=8.0)
     lib = gk.lib()
     assert lib.gracekv_segment(ctypes.byref(c), None, None, None, None, None, None, None, 0, None) == -1
-    assert lib.gracekv_build_trees(ctypes.byref(c), *([None] * 9), None, 0, None) == -1
+    assert lib.gracekv_build_trees(ctypes.byref(c), *([None] * 10), None, 0, None) == -1
     assert lib.gracekv_score(ctypes.byref(c), None, None, None) == -1
     assert lib.gracekv_select(ctypes.byref(c), None, None, None, 0, None) == -1
     assert lib.gracekv_pack(ctypes.byref(c), *([None] * 12), 0, None) == -1

@@ -171,3 +171,47 @@ def test_bf16_trees_and_selection(bf16_staged):
     assert not st.mismatches, st.mismatches[:10]
     if st.near_ties == 0:
         assert ga == oa and gs == os_
+
+
+def _same_cache(g1, g2):
+    assert g1["b_used"] == g2["b_used"]
+    assert torch.equal(g1["offsets"], g2["offsets"])
+    n = int(g1["offsets"][-1])
+    for k in ("pos_out", "logm_out", "K_out", "V_out"):
+        assert torch.equal(g1[k][:n], g2[k][:n]), k
+
+
+def _nodes(g):
+    return int(g["trees"]["unit_nn"].sum())
+
+
+@pytest.mark.parametrize("x", [2.0, 16.0, 64.0, 200.0])
+def test_pruned_build_gives_the_same_result_tiny(x):
+    # budget-aware pruning must not change the selection or the packed cache
+    sh = CONFIGS["tiny"]
+    case = make_case(sh, 0, with_hidden=False)
+    kappa = make_kappa(sh, 0)
+    N_c = O.budget(sh.L, sh.G, sh.N_ctx, x).N_c
+    slots = _partition(N_c)
+    cd = H.to_dev(case)
+    full = H.gpu_run(cd, x=x, slots=slots, kappa=kappa)
+    pr = H.gpu_run(cd, x=x, slots=slots, kappa=kappa, prune=True)
+    print(f"tiny x={x}: nodes full {_nodes(full)} pruned {_nodes(pr)}; b_used {pr['b_used']}")
+    assert H.gpu_selected(full) == H.gpu_selected(pr)
+    _same_cache(full, pr)
+    o = H.oracle_run(case, x=x, slots=slots, kappa=kappa)
+    assert H.gpu_selected(pr) == H.oracle_selected(o, sh.G)
+
+
+@pytest.mark.parametrize("x", [4.0, 32.0, 120.0])
+def test_pruned_build_gives_the_same_result_bf16(x):
+    sh = small_shape("bf16-small", L=2, G=2, H=8, d=128, N_ctx=1500, W=64, dtype="bf16", x=x, n_segments=12,
+                     rope_base=5.0e5, channel_scale="outlier", heavy_tail=0.01)
+    case = make_case(sh, 9, with_hidden=True)
+    cd = H.to_dev(case)
+    full = H.gpu_run(cd)
+    pr = H.gpu_run(cd, prune=True)
+    print(f"bf16 x={x}: J {len(full['slots'])} nodes full {_nodes(full)} pruned {_nodes(pr)}; b_used {pr['b_used']}")
+    assert full["slots"] == pr["slots"]
+    assert H.gpu_selected(full) == H.gpu_selected(pr)
+    _same_cache(full, pr)
