@@ -55,6 +55,11 @@ typedef enum {
 
 typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 
+/* Version of this interface (structures and signatures).  A binding must
+ * refuse a library whose gracekv_abi_version() differs from the value it was
+ * written for: argument lists shift silently across versions. */
+#define GRACEKV_ABI_VERSION 2
+
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
 typedef struct {
@@ -100,6 +105,9 @@ typedef struct {
          off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
 } gracekv_plan;
+
+/* GRACEKV_ABI_VERSION of the compiled library. */
+int32_t gracekv_abi_version(void);
 
 /* Paper defaults (App. A, App. B): see the field comments above. */
 gracekv_status gracekv_default_config(gracekv_config* cfg);

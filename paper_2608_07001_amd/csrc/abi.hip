@@ -75,6 +75,8 @@ static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 extern "C" {
 
+int32_t gracekv_abi_version(void) { return GRACEKV_ABI_VERSION; }
+
 gracekv_status gracekv_default_config(gracekv_config* c) {
   if (!c) return GRACEKV_ERR_INVALID_ARG;
   memset(c, 0, sizeof(*c));

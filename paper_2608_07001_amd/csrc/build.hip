@@ -376,11 +376,29 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
   const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
   const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
 
-  // ---- stage K, V ----
-  for (int e = tid; e < NMAX * D; e += BT) {
-    const int t = e / D, c = e % D;
-    U.sK[t * Lay::LDK + c] = t < n ? Kp[(int64_t)t * D + c] : (T)0;
-    U.sV[t * D + c] = t < n ? Vp[(int64_t)t * D + c] : (T)0;
+  // ---- stage K, V (16-byte chunks; rows up to the last 16-token tile, zero past n) ----
+  {
+    constexpr int CH = 16 / (int)sizeof(T);          // elements per chunk
+    constexpr int CPR = D / CH;                       // chunks per row
+    const int rows = ((n + 15) / 16) * 16;
+    for (int e = tid; e < rows * CPR; e += BT) {
+      const int t = e / CPR, c = (e % CPR) * CH;
+      uint4 kk = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+      if (t < n) {
+        kk = *(const uint4*)(Kp + (int64_t)t * D + c);
+        vv = *(const uint4*)(Vp + (int64_t)t * D + c);
+      }
+      T* dk = U.sK + t * Lay::LDK + c;
+      if constexpr (sizeof(T) == 2) {                 // LDK rows are 8-byte aligned for bf16
+        uint2* d2 = (uint2*)dk;
+        d2[0] = make_uint2(kk.x, kk.y);
+        d2[1] = make_uint2(kk.z, kk.w);
+      } else {
+        const float* kf = (const float*)&kk;
+        for (int h = 0; h < 4; ++h) dk[h] = kf[h];
+      }
+      *(uint4*)(U.sV + t * D + c) = vv;
+    }
   }
   for (int e = tid; e < NW * NMAX; e += BT) U.sS[e] = 0.f;
   __syncthreads();
@@ -413,10 +431,15 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
       }
       float4 st[4];
       int rowi[4];
+      float mqi[4];                 // probe shift of the row (if it is a probe row)
+      bool isp[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         rowi[i] = rt * 16 + 4 * (lane >> 4) + i;
         st[i] = rowi[i] < rows ? tv.row_stats[(int64_t)lg * rows + rowi[i]] : make_float4(0.f, 1.f, 0.f, 1.f);
+        const int u = rowi[i] % dm.W, hl = rowi[i] / dm.W;
+        isp[i] = rowi[i] < rows && u % dm.hpg == hl;
+        mqi[i] = isp[i] ? tv.probe_m[(int64_t)lg * dm.W + u] : 0.f;
       }
 #pragma unroll
       for (int tt = 0; tt < NMAX / 16; ++tt) {
@@ -440,11 +463,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
           if (rowi[i] < rows && t < n) {
             const float x = acc[i] * scale;
             sacc[tt] += expf(x - st[i].x) / st[i].y;
-            const int u = rowi[i] % dm.W, hl = rowi[i] / dm.W;
-            if (u % dm.hpg == hl) {
-              const float mq = tv.probe_m[(int64_t)lg * dm.W + u];
-              U.sE[u * ES + t] = expf(x - mq);
-            }
+            if (isp[i]) U.sE[(rowi[i] % dm.W) * ES + t] = expf(x - mqi[i]);
           }
         }
       }

@@ -16,6 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
+ABI_VERSION = 2          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
 
@@ -58,7 +59,7 @@ class Plan(ctypes.Structure):
                 + [(n, ctypes.c_size_t) for n in _OFFS] + [("build_lds_bytes", ctypes.c_int32)])
 
 
-SYMBOLS = ["gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
+SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
            "gracekv_segment", "gracekv_build_trees", "gracekv_score", "gracekv_select", "gracekv_pack",
            "gracekv_selftest_mfma"]
 
@@ -73,6 +74,14 @@ def lib() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
     L = ctypes.CDLL(LIB_PATH)
+    # argument lists and structures differ across interface versions: refuse a stale library
+    if not hasattr(L, "gracekv_abi_version"):
+        raise RuntimeError(f"{LIB_PATH} predates the versioned interface; rebuild it")
+    L.gracekv_abi_version.argtypes = []
+    L.gracekv_abi_version.restype = ctypes.c_int32
+    if L.gracekv_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{LIB_PATH} has interface version {L.gracekv_abi_version()}, "
+                           f"this binding needs {ABI_VERSION}; rebuild it")
     P = ctypes.c_void_p
     S = ctypes.c_size_t
     sig = {

@@ -22,6 +22,12 @@ def test_every_declared_symbol_is_exported():
         assert getattr(lib, name) is not None
 
 
+def test_interface_version_matches_the_header():
+    hdr = open(os.path.join(ROOT, "include", "gracekv.h")).read()
+    ver = int(re.search(r"#define GRACEKV_ABI_VERSION (\d+)", hdr).group(1))
+    assert gk.lib().gracekv_abi_version() == ver == gk.ABI_VERSION
+
+
 def test_struct_layouts_match_the_header(tmp_path):
     # compile the header with the host C compiler and compare sizes and field offsets
     fields_c = [f for f, _ in gk.Config._fields_]
