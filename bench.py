@@ -162,11 +162,12 @@ def main():
                                f"x={sh.x:g} ({sh.dtype})",
                    "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),
                    "pruned_build": not args.no_prune,
-                   "tree_nodes": int(gk.tree_arrays(p, buf.trees)["unit_nn"].sum().item())},
+                   "tree_nodes": int(gk.tree_arrays(p, buf.trees)["unit_nn"].view(sh.L * sh.G, p.J_cap)
+                                     [:, :int(buf.n_slots.item())].sum().item())},
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": stage_ms,
         "wall_s": wall,
-        "roofline": {"kernel": "gracekv_build_trees (k_rowstats + k_build)", "bound": "hbm",
+        "roofline": {"kernel": "gracekv_build_trees (k_rowstats + k_root + k_build)", "bound": "hbm",
                      "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": build_gbs / HBM_PEAK_GBS, "traffic": None},
     }

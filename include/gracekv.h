@@ -58,7 +58,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 2
+#define GRACEKV_ABI_VERSION 3
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -101,7 +101,7 @@ typedef struct {
          off_node_kind, off_node_cut, off_node_D, off_node_R,
          off_sp_U, off_sp_E, off_sp_cost, off_sp_exec,
          off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
-         off_tok_R, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
+         off_tok_R, off_tok_A, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
          off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
 } gracekv_plan;

@@ -50,6 +50,7 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.add_E = (uint64_t*)(b + p.off_add_E);
   v.add_exec = (uint8_t*)(b + p.off_add_exec);
   v.tok_R = (float*)(b + p.off_tok_R);
+  v.tok_A = (float*)(b + p.off_tok_A);
   v.row_stats = (float4*)(b + p.off_row_stats);
   v.probe_m = (float*)(b + p.off_probe_m);
   v.probe_ZC = (float*)(b + p.off_probe_ZC);
@@ -142,7 +143,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   gracekv_plan tmp = *p;
   Dims dm = make_dims(*c, tmp);
   p->build_lds_bytes = build_lds_bytes(dm);
-  if (p->build_lds_bytes > 160 * 1024) return GRACEKV_ERR_UNSUPPORTED;
+  if (p->build_lds_bytes > 160 * 1024 || root_lds_bytes(dm) > 160 * 1024) return GRACEKV_ERR_UNSUPPORTED;
   const size_t NC = (size_t)p->node_cap, UC = (size_t)p->unit_cap;
   size_t o = 0;
   auto put = [&](size_t& off, size_t bytes) { off = o; o = al256(o + bytes); };
@@ -165,6 +166,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_add_U, UC * 4);
   put(p->off_add_exec, UC);
   put(p->off_tok_R, (size_t)LG * p->N_c * 4);
+  put(p->off_tok_A, (size_t)LG * p->N_c * 4);
   put(p->off_row_stats, (size_t)LG * dm.rows * 16);
   put(p->off_probe_m, (size_t)LG * c->W * 4);
   put(p->off_probe_ZC, (size_t)LG * c->W * 4);
@@ -234,10 +236,10 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   auto build = [&](int mode) {
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
   };
-  if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
-  // pruned: roots -> bound -> root splits -> tighter bound -> the rest
   if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (build(BUILD_ROOT) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
+  // pruned: bound from the roots -> root splits -> tighter bound -> the rest
   if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (build(BUILD_ROOT_SPLIT) != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;

@@ -1,17 +1,16 @@
-// Prototype-tree construction, one workgroup per (layer, KV head, slot) unit.
+// Prototype-tree refinement, one workgroup per (layer, KV head, slot) unit.
 //
 // Implements App. A.3 (RoPE-consistent key prototype eq:app_rope_prototype,
 // value prototype eq:app_value_prototype, effective multiplicity
 // eq:app_effective_multiplicity, distortion eq:app_original_attention_stats ..
 // eq:app_node_and_drop_distortion, recursive refinement eq:app_binary_split ..
-// eq:app_split_choice) and pass 2 of the direct relevance (App. A.4
-// eq:app_attention_probability, eq:app_direct_relevance) with lambda_graph = 0,
-// so R^tok = s-hat (eq:app_bottom_up_value).
+// eq:app_split_choice).  The root of every unit, the token values R_t and the
+// probe masses A_t come from the root kernel; this kernel resumes from the node
+// table.
 //
 // Per unit (n <= 128 tokens), 512 threads:
-//   1. K and V tiles go to LDS; MFMA forms the logits of every relevance row
-//      (query head x window position) against the unit's keys.  With the row
-//      statistics of pass 1 they give pi, s_t and R^tok; probe rows also give
+//   1. K and V tiles go to LDS; the matrix cores form the logits of the W
+//      distortion probes against the unit's keys, giving
 //      e_{q,t} = exp(l_{q,t} - m_q) (kept in LDS, fp32).
 //   2. The tree is refined top-down in BFS order.  For node [a, b) the binary
 //      cuts (top-16 curvature positions t -> cut t+1, plus the midpoint) and the
@@ -67,8 +66,6 @@ struct BuildLds {
   static constexpr int oNE = oFlag + NMAX * 4;                // effective key of each node's creating op
   static constexpr int oNU = oNE + 256 * 8;                   // utility of each node's Split
   static constexpr int bytes = oNU + 256 * 4;
-  // relevance partial sums [8 waves][NMAX] alias the child buffers (used before any sweep)
-  static constexpr int oS = oCk;
 };
 
 int build_lds_bytes(const Dims& dm) {
@@ -76,26 +73,18 @@ int build_lds_bytes(const Dims& dm) {
   return dm.d == 128 ? BuildLds<float, 128>::bytes : BuildLds<float, 64>::bytes;
 }
 
-__device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
-  // round((x0 + ... + x1-1) / n) = round((x0 + x1 - 1) / 2), ties to even
-  int s = x0 + x1 - 1;
-  if ((s & 1) == 0) return s >> 1;
-  int h = s >> 1;
-  return (h & 1) ? h + 1 : h;
-}
-
 // child scalar rows in cs: 0 n, 1 sumR, 2 mean||k||, 3 m_eff, 4 p, 5 D
 template <typename T, int D>
 struct Unit {
   using Lay = BuildLds<T, D>;
   char* s;
-  T* sK; T* sV; float* sE; float* sR; float* sKap; float* sA; float* sKn; float* sS;
+  T* sK; T* sV; float* sE; float* sR; float* sKap; float* sA; float* sKn;
   int* na; int* nn; int* nc; int* np; int* nch; int* nk; int* ncut; float* nD; float* nR;
   float* ck; float* cv; float* con; float* cs; int* xi; int* flag;
   uint64_t* nE; float* nU;
   __device__ Unit(char* base) : s(base) {
     sK = (T*)(s + Lay::oK); sV = (T*)(s + Lay::oV); sE = (float*)(s + Lay::oE); sR = (float*)(s + Lay::oR);
-    sKap = (float*)(s + Lay::oKap); sA = (float*)(s + Lay::oA); sKn = (float*)(s + Lay::oKn); sS = (float*)(s + Lay::oS);
+    sKap = (float*)(s + Lay::oKap); sA = (float*)(s + Lay::oA); sKn = (float*)(s + Lay::oKn);
     na = (int*)(s + Lay::oNa); nn = (int*)(s + Lay::oNn); nc = (int*)(s + Lay::oNc); np = (int*)(s + Lay::oNp);
     nch = (int*)(s + Lay::oNch); nk = (int*)(s + Lay::oNk); ncut = (int*)(s + Lay::oNcut);
     nD = (float*)(s + Lay::oND); nR = (float*)(s + Lay::oNR);
@@ -332,7 +321,6 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
                                                TreeView tv) {
   using Lay = BuildLds<T, D>;
   constexpr bool BF = sizeof(T) == 2;
-  constexpr int KS = BF ? D / 16 : D / 4;
   constexpr int DPT = D / TPQ;
   constexpr int NW = BT / 64;
   extern __shared__ __align__(16) char smem[];
@@ -352,10 +340,9 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
   const float scale = 1.0f / sqrtf((float)D);
   const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
   const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
-  const bool cont = mode == BUILD_ROOT_SPLIT || mode == BUILD_CONTINUE;
-  const uint64_t theta = mode == BUILD_FULL || mode == BUILD_ROOT ? 0ull : *tv.theta;
+  const uint64_t theta = mode == BUILD_FULL ? 0ull : *tv.theta;
   int* cnt = U.xi + 192;       // node count
-  if (cont) {
+  {
     // resume from the node table: refine only nodes whose creating op reaches theta
     const int nn0 = tv.unit_nn[unit];
     const uint64_t Eadd = tv.add_E[unit];
@@ -367,7 +354,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
       U.ncut[i] = tv.node_cut[sl]; U.nD[i] = tv.node_D[sl]; U.nR[i] = tv.node_R[sl]; U.nU[i] = tv.sp_U[sl];
       const uint64_t ec = U.np[i] < 0 ? Eadd : tv.sp_E[base + U.np[i]];
       U.nE[i] = ec;
-      any |= U.nch[i] == 0 && U.nn[i] >= 2 && ec >= theta && (mode == BUILD_CONTINUE || i == 0);
+      any |= U.nch[i] == 0 && U.nn[i] >= 2 && ec >= theta && (mode != BUILD_ROOT_SPLIT || i == 0);
     }
     if (tid == 0) cnt[0] = nn0;
     if (!__syncthreads_or(any)) return;
@@ -400,91 +387,55 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
       *(uint4*)(U.sV + t * D + c) = vv;
     }
   }
-  for (int e = tid; e < NW * NMAX; e += BT) U.sS[e] = 0.f;
   __syncthreads();
 
-  // ---- relevance pass 2 and probe exponentials (MFMA logits) ----
+  // ---- probe exponentials e_{q,t} (matrix cores; probe q = window query q of
+  // head q mod |H(g)|).  A = probe rows, B = keys; each lane supplies a quarter
+  // row (D/4 consecutive dims) per operand. ----
   {
-    const int rows = dm.rows;
-    const int n_rt = (rows + 15) / 16;
-    const int n_tt = (n + 15) / 16;
-    float sacc[NMAX / 16];
+    constexpr int QE = D / 4;
+    const int i16 = lane & 15, g4 = lane >> 4;
+    const int n_pt = (dm.W + 15) / 16, n_tt = (n + 15) / 16;
+    for (int pi = wave; pi < n_pt * n_tt; pi += NW) {
+      const int pt = pi % n_pt, tt = pi / n_pt;
+      const int up = 16 * pt + i16;
+      const int uq = up < dm.W ? up : 0;
+      const T* qr = Qp + ((int64_t)(uq % dm.hpg) * dm.W + uq) * D + QE * g4;
+      const T* kr = U.sK + (16 * tt + i16) * Lay::LDK + QE * g4;
+      float mqr[4];
 #pragma unroll
-    for (int tt = 0; tt < NMAX / 16; ++tt) sacc[tt] = 0.f;
-    for (int rt = wave; rt < n_rt; rt += NW) {
-      const int row_l = rt * 16 + (lane & 15);
-      const bool rok = row_l < rows;
-      const T* qr = Qp + (int64_t)(rok ? row_l : 0) * D;
-      s16x4 qb[BF ? KS : 1];
-      float qf[BF ? 1 : KS];
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        if constexpr (BF) {
-          const uint16_t* q16 = (const uint16_t*)qr + s * 16 + 4 * (lane >> 4);
-          s16x4 v;
-          v[0] = rok ? (short)q16[0] : 0; v[1] = rok ? (short)q16[1] : 0;
-          v[2] = rok ? (short)q16[2] : 0; v[3] = rok ? (short)q16[3] : 0;
-          qb[s] = v;
-        } else {
-          qf[s] = rok ? ((const float*)qr)[s * 4 + (lane >> 4)] : 0.f;
-        }
+      for (int r = 0; r < 4; ++r) {
+        const int u2 = 16 * pt + 4 * g4 + r;
+        mqr[r] = u2 < dm.W ? tv.probe_m[(int64_t)lg * dm.W + u2] : 0.f;
       }
-      float4 st[4];
-      int rowi[4];
-      float mqi[4];                 // probe shift of the row (if it is a probe row)
-      bool isp[4];
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (BF) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        rowi[i] = rt * 16 + 4 * (lane >> 4) + i;
-        st[i] = rowi[i] < rows ? tv.row_stats[(int64_t)lg * rows + rowi[i]] : make_float4(0.f, 1.f, 0.f, 1.f);
-        const int u = rowi[i] % dm.W, hl = rowi[i] / dm.W;
-        isp[i] = rowi[i] < rows && u % dm.hpg == hl;
-        mqi[i] = isp[i] ? tv.probe_m[(int64_t)lg * dm.W + u] : 0.f;
-      }
-#pragma unroll
-      for (int tt = 0; tt < NMAX / 16; ++tt) {
-        if (tt >= n_tt) break;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        const T* kr = U.sK + (tt * 16 + (lane & 15)) * Lay::LDK;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          if constexpr (BF) {
-            const uint16_t* k16 = (const uint16_t*)kr + s * 16 + 4 * (lane >> 4);
-            s16x4 bb;
-            bb[0] = (short)k16[0]; bb[1] = (short)k16[1]; bb[2] = (short)k16[2]; bb[3] = (short)k16[3];
-            acc = mfma_bf16_16x16x16(qb[s], bb, acc);
-          } else {
-            acc = mfma_f32_16x16x4(qf[s], ((const float*)kr)[s * 4 + (lane >> 4)], acc);
-          }
+        for (int s2 = 0; s2 < QE / 4; ++s2) {
+          const uint2 qa = *(const uint2*)(qr + 4 * s2);
+          const uint2 kb = *(const uint2*)(kr + 4 * s2);
+          s16x4 av, bv;
+          av[0] = (short)(qa.x & 0xffffu); av[1] = (short)(qa.x >> 16); av[2] = (short)(qa.y & 0xffffu); av[3] = (short)(qa.y >> 16);
+          bv[0] = (short)(kb.x & 0xffffu); bv[1] = (short)(kb.x >> 16); bv[2] = (short)(kb.y & 0xffffu); bv[3] = (short)(kb.y >> 16);
+          acc = mfma_bf16_16x16x16(av, bv, acc);
         }
-        const int t = tt * 16 + (lane & 15);
+      } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (rowi[i] < rows && t < n) {
-            const float x = acc[i] * scale;
-            sacc[tt] += expf(x - st[i].x) / st[i].y;
-            if (isp[i]) U.sE[(rowi[i] % dm.W) * ES + t] = expf(x - mqi[i]);
-          }
-        }
+        for (int s2 = 0; s2 < QE; ++s2) acc = mfma_f32_16x16x4(((const float*)qr)[s2], ((const float*)kr)[s2], acc);
       }
-    }
+      const int t = 16 * tt + i16;
 #pragma unroll
-    for (int tt = 0; tt < NMAX / 16; ++tt) {
-      float v = sacc[tt];
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      if (lane < 16) U.sS[wave * NMAX + tt * 16 + lane] = v;
+      for (int r = 0; r < 4; ++r) {
+        const int u2 = 16 * pt + 4 * g4 + r;
+        if (u2 < dm.W && t < n) U.sE[u2 * ES + t] = expf(acc[r] * scale - mqr[r]);
+      }
     }
   }
-  __syncthreads();
-  const float S = tv.lg_S[lg];
+  // ---- token values, probe masses, curvature, key norms ----
   if (tid < n) {
     const int t = tid;
-    float s = 0.f;
-    for (int w = 0; w < NW; ++w) s += U.sS[w * NMAX + t];
-    const float R = s / (S + dm.eps);
-    U.sR[t] = R;
-    tv.tok_R[(int64_t)lg * dm.N_c + a0 + t] = R;
+    U.sR[t] = tv.tok_R[(int64_t)lg * dm.N_c + a0 + t];
+    U.sA[t] = tv.tok_A[(int64_t)lg * dm.N_c + a0 + t];
     U.sKap[t] = kappa[a0 + t];
     float kn = 0.f;
     for (int c = 0; c < D; ++c) {
@@ -492,9 +443,6 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
       kn += x * x;
     }
     U.sKn[t] = sqrtf(kn);
-    float am = 0.f;
-    for (int qq = 0; qq < dm.W; ++qq) am += U.sE[qq * ES + t] / tv.probe_ZC[(int64_t)lg * dm.W + qq];
-    U.sA[t] = am / (float)dm.W;
   }
   __syncthreads();
 
@@ -525,40 +473,12 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
   float* cRR = U.gcs(1, 1);
   float* cDR = U.gcs(1, 5);
   const float w = tv.omega[lg];
-  float Ddrop = 0.f;
-  if (!cont) {
-    if (tid == 0) {
-      U.na[0] = 0; U.nn[0] = n; U.nc[0] = -1; U.np[0] = -1; U.nch[0] = 0; U.nk[0] = 0; U.ncut[0] = -1;
-      XL[0] = n;
-      cnt[0] = 1;
-    }
-    __syncthreads();
-    if (n >= 2) {
-      sweep2<T, D>(U, dm, 0, n, XL, 1, XR, 0, a0, cosT, sinT, qv, m_q, zc_q, scale);
-      if (tid == 0) { U.nD[0] = cDL[0]; U.nR[0] = cRL[0]; }
-    } else if (tid == 0) {
-      U.nD[0] = 0.f;
-      U.nR[0] = U.sR[0];
-    }
-    if (tid == 0) {
-      float dd = 0.f;
-      for (int t = 0; t < n; ++t) dd += U.sA[t];
-      Ddrop = dd;
-      if (mode != BUILD_FULL) {          // the Add key (the root's creating op)
-        const float Ua = utility(add_gain(w, U.nR[0], Ddrop, U.nD[0]), 1);
-        U.nE[0] = op_key(Ua, ord * 256u);
-        tv.add_U[unit] = Ua;
-        tv.add_E[unit] = U.nE[0];
-      }
-    }
-    __syncthreads();
-  }
 
   // ---- top-down refinement in BFS order ----
   for (int head = 0;; ++head) {
     __syncthreads();
     const int count = cnt[0];
-    if (head >= count || mode == BUILD_ROOT || (mode == BUILD_ROOT_SPLIT && head > 0)) break;
+    if (head >= count || (mode == BUILD_ROOT_SPLIT && head > 0)) break;
     const int a = U.na[head], nv = U.nn[head], b = a + nv;
     if (nv < 2 || U.nch[head] > 0) continue;                  // leaf, or refined by an earlier pass
     if (mode != BUILD_FULL && U.nE[head] < theta) continue;    // cannot reach the auction's cut
@@ -754,10 +674,7 @@ __global__ __launch_bounds__(BT) void k_build(Dims dm, int mode, const T* __rest
       tv.sp_exec[sl] = 0;
     }
   }
-  if (tid == 0) {
-    tv.unit_nn[unit] = count;
-    if (!cont) tv.unit_Ddrop[unit] = Ddrop;
-  }
+  if (tid == 0) tv.unit_nn[unit] = count;
 }
 
 hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,

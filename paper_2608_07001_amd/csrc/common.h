@@ -50,6 +50,7 @@ struct TreeView {
   uint64_t* add_E;
   uint8_t* add_exec;
   float* tok_R;         // [LG][N_c] token values
+  float* tok_A;         // [LG][N_c] mean normalised probe attention of each token
   float4* row_stats;    // [LG][rows] (m_V, Z_V, m_C, Z_C)
   float* probe_m;       // [LG][W]
   float* probe_ZC;      // [LG][W]
@@ -62,10 +63,10 @@ struct TreeView {
   void* selstate;       // radix-select state of that bound
 };
 
-// Build modes: FULL refines every node; ROOT evaluates only the root (and its
-// Add key); ROOT_SPLIT refines the root of units whose Add key reaches theta;
+// Refinement modes (the roots come from the root kernel): FULL refines every
+// node; ROOT_SPLIT refines the root of units whose Add key reaches theta;
 // CONTINUE refines every unrefined node whose creating op reaches theta.
-enum { BUILD_FULL = 0, BUILD_ROOT = 1, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3 };
+enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3 };
 
 // ---- gains, utilities and keys (shared by the build and score kernels so that
 // both produce bit-identical keys) -------------------------------------------
@@ -81,6 +82,14 @@ __device__ __forceinline__ float utility(float gain, int cost) {
 // unique priority: larger U first, then the smaller id
 __device__ __forceinline__ uint64_t op_key(float U, uint32_t id) {
   return ((uint64_t)__float_as_uint(U) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+
+// representative position of [x0, x1): round((x0 + x1 - 1) / 2), ties to even
+__device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
+  const int s = x0 + x1 - 1;
+  if ((s & 1) == 0) return s >> 1;
+  const int h = s >> 1;
+  return (h & 1) ? h + 1 : h;
 }
 
 Dims make_dims(const gracekv_config& c, const gracekv_plan& p);
@@ -141,6 +150,10 @@ __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
 // ---- launchers (each defined in its own translation unit) -----------------
 hipError_t launch_rowstats(const Dims& dm, const void* K, const void* Q, const TreeView& tv, float4* partial,
                            hipStream_t st);
+hipError_t launch_root(const Dims& dm, const void* K, const void* V, const void* Q, const float* cosT,
+                       const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const TreeView& tv,
+                       hipStream_t st);
+int root_lds_bytes(const Dims& dm);
 hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
                         const float* kappa, const TreeView& tv, hipStream_t st);

@@ -57,6 +57,7 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
     LG = sh.L * sh.G
     out = dict(cfg=cfg, plan=buf.plan, trees=arr,
                tok_R=buf.trees[buf.plan.off_tok_R:buf.plan.off_tok_R + LG * buf.plan.N_c * 4].view(torch.float32).cpu(),
+               tok_A=buf.trees[buf.plan.off_tok_A:buf.plan.off_tok_A + LG * buf.plan.N_c * 4].view(torch.float32).cpu(),
                b_used=int(buf.b_used.item()), offsets=buf.offsets.cpu(), counts=buf.counts.cpu(),
                K_out=buf.K_out.cpu(), V_out=buf.V_out.cpu(), pos_out=buf.pos_out.cpu(), logm_out=buf.logm_out.cpu())
     if slots is None:

@@ -61,16 +61,25 @@ def tiny_staged():
     return sh, case, g, o
 
 
+def _probe_mass(c):
+    # A_t: probe mean of e_{q,t} / Z_q(C), the attention mass a dropped token takes away
+    return (c.E / c.ZC[:, None]).mean(axis=0)
+
+
 def test_tiny_token_values(tiny_staged):
     sh, case, g, o = tiny_staged
     N_c = g["plan"].N_c
     tokR = g["tok_R"].numpy().reshape(sh.L * sh.G, N_c)
-    worst = 0.0
+    tokA = g["tok_A"].numpy().reshape(sh.L * sh.G, N_c)
+    worst = worstA = 0.0
     for (l, gg), c in o.ctx.items():
         err = np.abs(tokR[l * sh.G + gg] - c.R) / np.maximum(np.abs(c.R), 1e-30)
         worst = max(worst, float(err.max()))
-    print(f"tiny R^tok max rel err {worst:.3e}")
+        A = _probe_mass(c)
+        worstA = max(worstA, float((np.abs(tokA[l * sh.G + gg] - A) / np.maximum(A, 1e-30)).max()))
+    print(f"tiny R^tok max rel err {worst:.3e}, A max rel err {worstA:.3e}")
     assert worst < RTOL_R
+    assert worstA < RTOL_R
 
 
 def test_tiny_trees(tiny_staged):
@@ -167,7 +176,12 @@ def test_bf16_trees_and_selection(bf16_staged):
     print(f"bf16 R^tok maxrel {worstR:.3e}; trees nodes {st.nodes} near-ties {st.near_ties} "
           f"maxrelD {st.max_rel_D:.3e} maxabsD {st.max_abs_D:.3e}; select diff adds {len(ga ^ oa)} "
           f"splits {len(gs ^ os_)}")
+    tokA = g["tok_A"].numpy().reshape(sh.L * sh.G, N_c)
+    worstA = max(float((np.abs(tokA[l * sh.G + gg] - _probe_mass(c)) / np.maximum(_probe_mass(c), 1e-30)).max())
+                 for (l, gg), c in o.ctx.items())
+    print(f"bf16 A maxrel {worstA:.3e}")
     assert worstR < RTOL_R
+    assert worstA < RTOL_R
     assert not st.mismatches, st.mismatches[:10]
     if st.near_ties == 0:
         assert ga == oa and gs == os_
@@ -182,7 +196,9 @@ def _same_cache(g1, g2):
 
 
 def _nodes(g):
-    return int(g["trees"]["unit_nn"].sum())
+    # units j >= J of each (l, g) are not written
+    J, J_cap = len(g["slots"]), g["plan"].J_cap
+    return int(g["trees"]["unit_nn"].view(-1, J_cap)[:, :J].sum())
 
 
 @pytest.mark.parametrize("x", [2.0, 16.0, 64.0, 200.0])
