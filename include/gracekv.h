@@ -58,12 +58,12 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 3
+#define GRACEKV_ABI_VERSION 4
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
 typedef struct {
-  int32_t L, G, H, d;      /* layers, KV heads, query heads, head dim (d even, <= 128) */
+  int32_t L, G, H, d;      /* layers, KV heads, query heads, head dim: 64 or 128 (fp32 data: 64) */
   int32_t n_seg;           /* hidden-state slabs (|L_seg|, eq:app_seg_layers), 1..8 */
   int32_t D_hidden;        /* hidden size of each slab */
   int32_t W;               /* window queries (1..64) */
@@ -102,7 +102,8 @@ typedef struct {
          off_sp_U, off_sp_E, off_sp_cost, off_sp_exec,
          off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
          off_tok_R, off_tok_A, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
-         off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate;
+         off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate,
+         off_work, off_wctr;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
 } gracekv_plan;
 

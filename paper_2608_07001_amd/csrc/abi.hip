@@ -61,6 +61,8 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.nslots = (int32_t*)(b + p.off_nslots);
   v.theta = (uint64_t*)(b + p.off_theta);
   v.selstate = (void*)(b + p.off_selstate);
+  v.work = (int32_t*)(b + p.off_work);
+  v.wctr = (int32_t*)(b + p.off_wctr);
   return v;
 }
 
@@ -120,6 +122,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
   if (c->flags & ~GRACEKV_FLAG_PRUNE) return GRACEKV_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->dtype == GRACEKV_F32 && c->d != 64) return GRACEKV_ERR_UNSUPPORTED;   // refinement LDS
   if (c->W > WMAX || c->n_seg > 8) return GRACEKV_ERR_UNSUPPORTED;
   if (c->n_min < 16 || c->n_max > NMAX || c->n_max < c->n_min || c->n0 < 1) return GRACEKV_ERR_UNSUPPORTED;
   if (c->win[0] != 4 || c->win[1] != 8 || c->win[2] != 16) return GRACEKV_ERR_UNSUPPORTED;
@@ -178,6 +181,8 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_partial, (size_t)LG * rowstats_chunks(dm) * dm.rows * 16);
   put(p->off_theta, 16);
   put(p->off_selstate, selstate_bytes());
+  put(p->off_work, UC * 4);
+  put(p->off_wctr, 16);
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
   p->sel_ws_bytes = select_ws_bytes(dm);

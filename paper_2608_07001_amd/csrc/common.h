@@ -61,6 +61,8 @@ struct TreeView {
   int32_t* nslots;      // [1] J
   uint64_t* theta;      // [1] lower bound of the auction cut used by the pruned build
   void* selstate;       // radix-select state of that bound
+  int32_t* work;        // [L*G*J_cap] units to refine
+  int32_t* wctr;        // [4] list length, next item
 };
 
 // Refinement modes (the roots come from the root kernel): FULL refines every
