@@ -101,29 +101,35 @@ struct Ref {
   __device__ float* crow(int row) { return cs + row * CC; }
 };
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 __device__ __forceinline__ s16x4 pk4(uint32_t lo, uint32_t hi) {
-  s16x4 v;
-  v[0] = (short)(lo & 0xffffu); v[1] = (short)(lo >> 16);
-  v[2] = (short)(hi & 0xffffu); v[3] = (short)(hi >> 16);
-  return v;
+  u32x2 v;
+  v.x = lo;
+  v.y = hi;
+  return __builtin_bit_cast(s16x4, v);
 }
 __device__ __forceinline__ uint32_t bf16_bits_fin(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
-// x = hi + mid + lo, each a bf16 (the remainders are exact in fp32)
-__device__ __forceinline__ void split3x4(const float* x, s16x4& hi, s16x4& mid, s16x4& lo) {
+// x = hi + mid + lo, each a bf16 (the remainders are exact in fp32), packed
+// two per 32-bit word as the matrix-core operands want them
+__device__ __forceinline__ void split3x4(const float* x, u32x2& hi, u32x2& mid, u32x2& lo) {
+  uint32_t h[4], m[4], l[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const uint32_t h = bf16_bits_fin(x[r]);
-    const float r1 = x[r] - __uint_as_float(h << 16);
-    const uint32_t m = bf16_bits_fin(r1);
-    const float r2 = r1 - __uint_as_float(m << 16);
-    hi[r] = (short)h;
-    mid[r] = (short)m;
-    lo[r] = (short)bf16_bits_fin(r2);
+    h[r] = bf16_bits_fin(x[r]);
+    const float r1 = x[r] - __uint_as_float(h[r] << 16);
+    m[r] = bf16_bits_fin(r1);
+    const float r2 = r1 - __uint_as_float(m[r] << 16);
+    l[r] = bf16_bits_fin(r2);
   }
+  hi.x = h[0] | (h[1] << 16); hi.y = h[2] | (h[3] << 16);
+  mid.x = m[0] | (m[1] << 16); mid.y = m[2] | (m[3] << 16);
+  lo.x = l[0] | (l[1] << 16); lo.y = l[2] | (l[3] << 16);
 }
+__device__ __forceinline__ s16x4 as_op(u32x2 v) { return __builtin_bit_cast(s16x4, v); }
 
 // ---------------------------------------------------------------------------
 // Prototype sums of both directions at once.  Group 0 reads the prefix
@@ -140,59 +146,66 @@ __device__ void proto_sums(Ref<T, D>& U, const Dims& dm, int a, int b, const int
   const int* xs = prefix ? XL : XR;
   const int nx = prefix ? nl : nr;
   if (lt >= 2 * D || nx == 0) return;
-  const int t_first = prefix ? a : b - 1;
-  const int step = prefix ? 1 : -1;
-  const int t_last = prefix ? xs[nx - 1] - 1 : xs[0];
-  const int steps = prefix ? t_last - t_first + 1 : t_first - t_last + 1;
   const bool kside = lt < D;
   const int i = kside ? lt : lt - D;
   float s0 = 0.f, s1 = 0.f, sr = 0.f, skn = 0.f;
-  int ci = prefix ? 0 : nx - 1;
-  int xnext = xs[ci];
-  bool done = false;
-  for (int it0 = 0; it0 < steps && !done; it0 += 8) {
-    float f8[8], r8[8], k8[8];
+  int t = prefix ? a : b - 1;                 // next token of the sweep
+  for (int k = 0; k < nx; ++k) {
+    const int c = prefix ? k : nx - 1 - k;
+    const int x = xs[c];
+    // tokens up to the read-off: prefix [t, x), suffix down to x (inclusive)
+    const int cntk = prefix ? x - t : t - x + 1;
+    const int step = prefix ? 1 : -1;
+    if (kside) {
+      int u = 0;
+      for (; u + 4 <= cntk; u += 4) {
+        float f[4], kk[4], rr[4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int it = min(it0 + u, steps - 1);
-      const int t = t_first + step * it;
-      f8[u] = kside ? U.Ko[t * D + i] : ldf(U.Vt, i * Lay::LDV + t);
-      r8[u] = U.R[t];
-      k8[u] = U.Kn[t];
+        for (int v = 0; v < 4; ++v) {
+          const int tt = t + step * (u + v);
+          f[v] = U.Ko[tt * D + i]; kk[v] = U.Kn[tt]; rr[v] = U.R[tt];
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) { s0 += f[v]; skn += kk[v]; sr += rr[v]; }
+      }
+      for (; u < cntk; ++u) {
+        const int tt = t + step * u;
+        s0 += U.Ko[tt * D + i]; skn += U.Kn[tt]; sr += U.R[tt];
+      }
+    } else {
+      int u = 0;
+      for (; u + 4 <= cntk; u += 4) {
+        float f[4], rr[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int tt = t + step * (u + v);
+          f[v] = ldf(U.Vt, i * Lay::LDV + tt); rr[v] = U.R[tt];
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) { s0 += rr[v] * f[v]; s1 += f[v]; sr += rr[v]; }
+      }
+      for (; u < cntk; ++u) {
+        const int tt = t + step * u;
+        const float f = ldf(U.Vt, i * Lay::LDV + tt), rr = U.R[tt];
+        s0 += rr * f; s1 += f; sr += rr;
+      }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (done || it0 + u >= steps) break;
-      const int t = t_first + step * (it0 + u);
+    t += step * cntk;
+    const int nch = prefix ? x - a : b - x;
+    const int gc = g * CM + c;
+    if (nch >= 2) {
+      const float inv = 1.0f / (float)nch;
       if (kside) {
-        s0 += f8[u];
-        skn += k8[u];
+        U.Kt[gc * Lay::KTS + i] = s0 * inv;
       } else {
-        s0 += r8[u] * f8[u];
-        s1 += f8[u];
+        const float beta = dm.beta_frac * sr * inv;
+        U.Vv[gc * D + i] = (s0 + beta * s1) / (sr + (float)nch * beta + dm.eps);
       }
-      sr += r8[u];
-      if (prefix ? (t + 1 == xnext) : (t == xnext)) {
-        const int nch = prefix ? xnext - a : b - xnext;
-        const int gc = g * CM + ci;
-        if (nch >= 2) {
-          const float inv = 1.0f / (float)nch;
-          if (kside) {
-            U.Kt[gc * Lay::KTS + i] = s0 * inv;
-          } else {
-            const float beta = dm.beta_frac * sr * inv;
-            U.Vv[gc * D + i] = (s0 + beta * s1) / (sr + (float)nch * beta + dm.eps);
-          }
-        }
-        if (lt == 0) {
-          U.crow(0)[gc] = (float)nch;
-          U.crow(1)[gc] = sr;
-          U.crow(2)[gc] = skn / (float)nch;
-        }
-        ci += prefix ? 1 : -1;
-        if (ci < 0 || ci >= nx) done = true;
-        else xnext = xs[ci];
-      }
+    }
+    if (lt == 0) {
+      U.crow(0)[gc] = (float)nch;
+      U.crow(1)[gc] = sr;
+      U.crow(2)[gc] = skn / (float)nch;
     }
   }
 }
@@ -255,12 +268,12 @@ __device__ void proto_attention(Ref<T, D>& U, const Dims& dm, int nl, int nr, co
         float x[4];
         const float4 v = *(const float4*)(kt + 4 * s);
         x[0] = cok ? v.x : 0.f; x[1] = cok ? v.y : 0.f; x[2] = cok ? v.z : 0.f; x[3] = cok ? v.w : 0.f;
-        s16x4 h, m, l;
+        u32x2 h, m, l;
         split3x4(x, h, m, l);
         const s16x4 qa = pk4(qreg[2 * s], qreg[2 * s + 1]);
-        acc = mfma_bf16_16x16x16(qa, l, acc);
-        acc = mfma_bf16_16x16x16(qa, m, acc);
-        acc = mfma_bf16_16x16x16(qa, h, acc);
+        acc = mfma_bf16_16x16x16(qa, as_op(l), acc);
+        acc = mfma_bf16_16x16x16(qa, as_op(m), acc);
+        acc = mfma_bf16_16x16x16(qa, as_op(h), acc);
       }
     } else {
 #pragma unroll
@@ -331,6 +344,9 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
   for (int dt = 0; dt < DT; ++dt) M[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   float Z = 0.f;
   float ev[4] = {0.f, 0.f, 0.f, 0.f};
+  u32x2 eh = {0u, 0u}, em = {0u, 0u}, el = {0u, 0u};   // bf16 parts of the block's e
+  u32x2 vop[BF ? DT : 1];                             // V^T operands of the block (bf16)
+  float4 vf[BF ? 1 : DT];                             // ... (fp32)
   int eblk = -1;
   int cur = prefix ? a : b;
   for (int k = 0; k < nx; ++k) {
@@ -343,34 +359,50 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
       const int hi = prefix ? min(x, (blk + 1) << 4) : cur;
       if (blk != eblk) {
         block_e<T, D, QW>(Kp, n, blk, qreg, mq, pok, scale, ev);
+        if constexpr (BF) {
+          split3x4(ev, eh, em, el);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const uint2 vv = *(const uint2*)(U.Vt + (16 * dt + i16) * Lay::LDV + 16 * blk + 4 * g4);
+            vop[dt].x = vv.x;
+            vop[dt].y = vv.y;
+          }
+        } else {
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            vf[dt] = *(const float4*)(U.Vt + (16 * dt + i16) * Lay::LDV + 16 * blk + 4 * g4);
+        }
         eblk = blk;
       }
-      float em[4];
+      const int t0 = 16 * blk + 4 * g4;
+      bool in[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int t = 16 * blk + 4 * g4 + r;
-        em[r] = (t >= lo && t < hi) ? ev[r] : 0.f;
-        Z += em[r];
+        in[r] = t0 + r >= lo && t0 + r < hi;
+        Z += in[r] ? ev[r] : 0.f;
       }
       if constexpr (BF) {
-        s16x4 h, m, l;
-        split3x4(em, h, m, l);
+        u32x2 mk;
+        mk.x = (in[0] ? 0xffffu : 0u) | (in[1] ? 0xffff0000u : 0u);
+        mk.y = (in[2] ? 0xffffu : 0u) | (in[3] ? 0xffff0000u : 0u);
+        const s16x4 ph = as_op(eh & mk), pm = as_op(em & mk), pl = as_op(el & mk);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const uint2 vv = *(const uint2*)(U.Vt + (16 * dt + i16) * Lay::LDV + 16 * blk + 4 * g4);
-          const s16x4 va = pk4(vv.x, vv.y);
-          M[dt] = mfma_bf16_16x16x16(va, l, M[dt]);
-          M[dt] = mfma_bf16_16x16x16(va, m, M[dt]);
-          M[dt] = mfma_bf16_16x16x16(va, h, M[dt]);
+          const s16x4 va = as_op(vop[dt]);
+          M[dt] = mfma_bf16_16x16x16(va, pl, M[dt]);
+          M[dt] = mfma_bf16_16x16x16(va, pm, M[dt]);
+          M[dt] = mfma_bf16_16x16x16(va, ph, M[dt]);
         }
       } else {
+        float emk[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) emk[r] = in[r] ? ev[r] : 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const float4 vv = *(const float4*)(U.Vt + (16 * dt + i16) * Lay::LDV + 16 * blk + 4 * g4);
-          M[dt] = mfma_f32_16x16x4(vv.x, em[0], M[dt]);
-          M[dt] = mfma_f32_16x16x4(vv.y, em[1], M[dt]);
-          M[dt] = mfma_f32_16x16x4(vv.z, em[2], M[dt]);
-          M[dt] = mfma_f32_16x16x4(vv.w, em[3], M[dt]);
+          M[dt] = mfma_f32_16x16x4(vf[dt].x, emk[0], M[dt]);
+          M[dt] = mfma_f32_16x16x4(vf[dt].y, emk[1], M[dt]);
+          M[dt] = mfma_f32_16x16x4(vf[dt].z, emk[2], M[dt]);
+          M[dt] = mfma_f32_16x16x4(vf[dt].w, emk[3], M[dt]);
         }
       }
       if (prefix) cur = hi; else cur = lo;
@@ -511,6 +543,13 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
         float4* d2 = (float4*)(U.Ko + t * D + c + H2);
         d1[0] = make_float4(o1[0], o1[1], o1[2], o1[3]); d1[1] = make_float4(o1[4], o1[5], o1[6], o1[7]);
         d2[0] = make_float4(o2[0], o2[1], o2[2], o2[3]); d2[1] = make_float4(o2[4], o2[5], o2[6], o2[7]);
+        // ||k°_t||^2: the CH items of token t sit in CH consecutive lanes
+        float ss = 0.f;
+#pragma unroll
+        for (int h = 0; h < 8; ++h) ss += o1[h] * o1[h] + o2[h] * o2[h];
+#pragma unroll
+        for (int o = 1; o < CH; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        if (e % CH == 0) U.Kn[t] = sqrtf(ss);
       }
       // V^T, zero past n
       const int rows16 = (n + 15) & ~15;
@@ -567,14 +606,6 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
     __syncthreads();
     float mq = 0.f, zc = 1.f;
     if (16 * pt + i16 < dm.W) { mq = U.Mq[16 * pt + i16]; zc = U.Zc[16 * pt + i16]; }
-    if (tid < n) {                 // ||k_t|| = ||k°_t|| (dims visited from a rotated start: no bank conflicts)
-      float s = 0.f;
-      for (int c = 0; c < D; ++c) {
-        const float x = U.Ko[tid * D + ((c + tid) & (D - 1))];
-        s += x * x;
-      }
-      U.Kn[tid] = sqrtf(s);
-    }
     const float w = tv.omega[lg];
 
     // ---- top-down refinement in BFS order ----
