@@ -101,14 +101,6 @@ struct Ref {
   __device__ float* crow(int row) { return cs + row * CC; }
 };
 
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ s16x4 pk4(uint32_t lo, uint32_t hi) {
-  u32x2 v;
-  v.x = lo;
-  v.y = hi;
-  return __builtin_bit_cast(s16x4, v);
-}
 __device__ __forceinline__ uint32_t bf16_bits_fin(float f) {
   const uint32_t u = __float_as_uint(f);
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;

@@ -142,6 +142,16 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// four bf16 packed two per 32-bit word (low half first) as an MFMA operand
+__device__ __forceinline__ s16x4 pk4(uint32_t lo, uint32_t hi) {
+  u32x2 v;
+  v.x = lo;
+  v.y = hi;
+  return __builtin_bit_cast(s16x4, v);
+}
+
 __device__ __forceinline__ f32x4 mfma_bf16_16x16x16(s16x4 a, s16x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }

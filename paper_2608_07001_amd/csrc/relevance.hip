@@ -10,11 +10,14 @@
 // eq:app_direct_relevance follows exactly:
 //   sum_{t in C} s_t = sum_r exp(m_C - m_V) Z_C / Z_V.
 //
-// K5a: grid (chunks of T, L*G, row groups of 256).  Each workgroup stages
-// 64-token sub-chunks of K in LDS and forms 16x16 logit tiles with MFMA
-// (bf16 inputs: exact products, fp32 accumulation); each lane keeps online
-// (max, sum-exp) pairs for its 4 rows, merged across lanes at the end.
-// K5b: per (l, g), merge the chunk partials in order and reduce S.
+// Pass 1: grid (chunks of T, L*G, row groups of 256).  Each workgroup stages
+// 64-token sub-chunks of K in LDS (16-byte loads) and forms transposed 16x16
+// logit tiles on the matrix cores (tokens x rows; bf16 inputs give exact
+// products, fp32 accumulation), so each lane holds 4 tokens of one row.  A
+// token t < N_c is in both C and V(u); the lane keeps one online (max,
+// sum-exp) pair over C and one over the visible tail [N_c, N_ctx + u], merged
+// into V afterwards.  Pass 2 (combine): per (l, g), merge the chunk partials
+// in order and reduce S.
 #include "common.h"
 
 namespace gkv {
@@ -24,129 +27,125 @@ constexpr int RS_CHUNK = 2048;  // tokens per workgroup
 
 int rowstats_chunks(const Dims& dm) { return (int)((dm.T + RS_CHUNK - 1) / RS_CHUNK); }
 
-template <typename T> struct KPad;
-template <> struct KPad<uint16_t> { static constexpr int v = 4; };
-template <> struct KPad<float> { static constexpr int v = 1; };
-
-template <typename T, int D>
-__device__ __forceinline__ f32x4 logit_tile(const T* qrow_unused, const T* sK, int ldk, int tok0, int lane,
-                                            const void* qf, f32x4 acc);
+// online (max, sum-exp) update with four values (-inf = absent)
+__device__ __forceinline__ void lse_add4(float& m, float& z, float x0, float x1, float x2, float x3) {
+  const float mn = fmaxf(m, fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
+  if (mn == -INFINITY) return;
+  if (mn > m) z *= expf(m - mn);
+  z += expf(x0 - mn) + expf(x1 - mn) + expf(x2 - mn) + expf(x3 - mn);
+  m = mn;
+}
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_rowstats(Dims dm, const T* __restrict__ K, const T* __restrict__ Q,
                                                   float4* __restrict__ partial, int nchunk) {
   constexpr bool BF = sizeof(T) == 2;
-  constexpr int KS = BF ? D / 16 : D / 4;         // MFMA k-steps
-  constexpr int LDK = D + KPad<T>::v;
-  __shared__ T sK[RS_SUB * LDK];
+  constexpr int QE = D / 4;                       // elements of a lane's quarter row
+  constexpr int QW = BF ? QE / 2 : QE;            // ... in 32-bit words
+  constexpr int LDK = BF ? D + 8 : D + 4;
+  constexpr int CH = 16 / (int)sizeof(T);         // elements per 16-byte chunk
+  __shared__ __align__(16) T sK[RS_SUB * LDK];
 
   const int ck = blockIdx.x, lg = blockIdx.y, rg = blockIdx.z;
   const int l = lg / dm.G, g = lg % dm.G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
   const int64_t t_begin = (int64_t)ck * RS_CHUNK;
   const int64_t t_end = min(dm.T, t_begin + RS_CHUNK);
   const T* Kp = K + (int64_t)lg * dm.T * D;
   const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
   const float scale = 1.0f / sqrtf((float)D);
 
-  // this wave's 4 row tiles
-  int rt0 = rg * 16 + wave * 4;
-  bool tile_ok[4];
-  // Q fragments in registers
-  s16x4 qb[4][BF ? KS : 1];
-  float qf[4][BF ? 1 : KS];
+  // the wave's 4 row tiles: Q quarter rows in registers
+  uint32_t qreg[4][QW];
+  int vlim[4];                    // last visible position N_ctx + u of the lane's row
+  bool tile_ok[4], rok[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    int rt = rt0 + k;
+    const int rt = rg * 16 + wave * 4 + k;
     tile_ok[k] = rt * 16 < dm.rows;
-    int row = rt * 16 + (lane & 15);
-    bool rok = row < dm.rows;
-    const T* qr = Qp + (int64_t)(rok ? row : 0) * D;
+    const int row = rt * 16 + i16;
+    rok[k] = row < dm.rows;
+    vlim[k] = (int)dm.N_ctx + (rok[k] ? row % dm.W : 0);
+    const uint4* q4 = (const uint4*)(Qp + (int64_t)(rok[k] ? row : 0) * D + QE * g4);
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if constexpr (BF) {
-        s16x4 v;
-        const uint16_t* q16 = (const uint16_t*)qr + s * 16 + 4 * (lane >> 4);
-        v[0] = rok ? (short)q16[0] : 0;
-        v[1] = rok ? (short)q16[1] : 0;
-        v[2] = rok ? (short)q16[2] : 0;
-        v[3] = rok ? (short)q16[3] : 0;
-        qb[k][s] = v;
-      } else {
-        qf[k][s] = rok ? ((const float*)qr)[s * 4 + (lane >> 4)] : 0.f;
-      }
+    for (int h = 0; h < QW / 4; ++h) {
+      const uint4 v = q4[h];
+      qreg[k][4 * h] = v.x; qreg[k][4 * h + 1] = v.y; qreg[k][4 * h + 2] = v.z; qreg[k][4 * h + 3] = v.w;
     }
   }
-  float mV[4][4], zV[4][4], mC[4][4], zC[4][4];
+  float mC[4], zC[4], mT[4], zT[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { mV[k][i] = -INFINITY; zV[k][i] = 0.f; mC[k][i] = -INFINITY; zC[k][i] = 0.f; }
+  for (int k = 0; k < 4; ++k) { mC[k] = -INFINITY; zC[k] = 0.f; mT[k] = -INFINITY; zT[k] = 0.f; }
 
   for (int64_t s0 = t_begin; s0 < t_end; s0 += RS_SUB) {
     __syncthreads();
-    // stage K[s0 .. s0+SUB) (zero beyond the chunk)
-    for (int e = threadIdx.x; e < RS_SUB * D; e += 256) {
-      int tr = e / D, c = e % D;
-      int64_t t = s0 + tr;
-      sK[tr * LDK + c] = (t < t_end) ? Kp[t * D + c] : (T)0;
+    for (int e = tid; e < RS_SUB * (D / CH); e += 256) {      // stage K[s0 .. s0+SUB), zero past the chunk
+      const int tr = e / (D / CH), c = (e % (D / CH)) * CH;
+      const int64_t t = s0 + tr;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (t < t_end) v = *(const uint4*)(Kp + t * D + c);
+      *(uint4*)(sK + tr * LDK + c) = v;
     }
     __syncthreads();
+    const bool allC = s0 + RS_SUB <= dm.N_c && s0 + RS_SUB <= t_end;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (!tile_ok[k]) continue;
+    for (int tt = 0; tt < RS_SUB / 16; ++tt) {
+      uint32_t kreg[QW];
+      const uint4* k4 = (const uint4*)(sK + (tt * 16 + i16) * LDK + QE * g4);
 #pragma unroll
-      for (int tt = 0; tt < RS_SUB / 16; ++tt) {
+      for (int h = 0; h < QW / 4; ++h) {
+        const uint4 v = k4[h];
+        kreg[4 * h] = v.x; kreg[4 * h + 1] = v.y; kreg[4 * h + 2] = v.z; kreg[4 * h + 3] = v.w;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!tile_ok[k]) continue;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        const T* kr = sK + (tt * 16 + (lane & 15)) * LDK;
+        if constexpr (BF) {
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-          if constexpr (BF) {
-            const uint16_t* k16 = (const uint16_t*)kr + s * 16 + 4 * (lane >> 4);
-            s16x4 b;
-            b[0] = (short)k16[0]; b[1] = (short)k16[1]; b[2] = (short)k16[2]; b[3] = (short)k16[3];
-            acc = mfma_bf16_16x16x16(qb[k][s], b, acc);
-          } else {
-            acc = mfma_f32_16x16x4(qf[k][s], ((const float*)kr)[s * 4 + (lane >> 4)], acc);
+          for (int s = 0; s < QE / 4; ++s) {
+            acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qreg[k][2 * s], qreg[k][2 * s + 1]), acc);
           }
+        } else {
+#pragma unroll
+          for (int s = 0; s < QE; ++s) acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qreg[k][s]), acc);
         }
-        const int64_t t = s0 + tt * 16 + (lane & 15);
+        // lane holds tokens s0 + 16 tt + 4 g4 + r of its row
+        float x[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = (rt0 + k) * 16 + 4 * (lane >> 4) + i;
-          const int u = row % dm.W;
-          const float x = acc[i] * scale;
-          const bool vis = (t < t_end) && (t <= dm.N_ctx + u) && (row < dm.rows);
-          const bool inC = vis && (t < dm.N_c);
-          if (vis) {
-            if (x > mV[k][i]) { zV[k][i] = zV[k][i] * expf(mV[k][i] - x) + 1.f; mV[k][i] = x; }
-            else zV[k][i] += expf(x - mV[k][i]);
+        for (int r = 0; r < 4; ++r) x[r] = acc[r] * scale;
+        if (allC) {
+          if (rok[k]) lse_add4(mC[k], zC[k], x[0], x[1], x[2], x[3]);
+        } else {
+          float xc[4], xt[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t t = s0 + 16 * tt + 4 * g4 + r;
+            const bool vis = rok[k] && t < t_end && t <= vlim[k];
+            const bool inC = vis && t < dm.N_c;
+            xc[r] = inC ? x[r] : -INFINITY;
+            xt[r] = (vis && !inC) ? x[r] : -INFINITY;
           }
-          if (inC) {
-            if (x > mC[k][i]) { zC[k][i] = zC[k][i] * expf(mC[k][i] - x) + 1.f; mC[k][i] = x; }
-            else zC[k][i] += expf(x - mC[k][i]);
-          }
+          lse_add4(mC[k], zC[k], xc[0], xc[1], xc[2], xc[3]);
+          lse_add4(mT[k], zT[k], xt[0], xt[1], xt[2], xt[3]);
         }
       }
     }
   }
-  // merge across the 16 lanes holding the same rows
+  // merge the 4 lanes holding the same row (disjoint token subsets)
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) {
-        float m2 = __shfl_xor(mV[k][i], o, 64), z2 = __shfl_xor(zV[k][i], o, 64);
-        lse_merge(mV[k][i], zV[k][i], m2, z2);
-        m2 = __shfl_xor(mC[k][i], o, 64);
-        z2 = __shfl_xor(zC[k][i], o, 64);
-        lse_merge(mC[k][i], zC[k][i], m2, z2);
-      }
-      const int row = (rt0 + k) * 16 + 4 * (lane >> 4) + i;
-      if ((lane & 15) == 0 && tile_ok[k] && row < dm.rows)
-        partial[((int64_t)lg * nchunk + ck) * dm.rows + row] = make_float4(mV[k][i], zV[k][i], mC[k][i], zC[k][i]);
+    for (int o = 16; o < 64; o <<= 1) {
+      float m2 = __shfl_xor(mC[k], o, 64), z2 = __shfl_xor(zC[k], o, 64);
+      lse_merge(mC[k], zC[k], m2, z2);
+      m2 = __shfl_xor(mT[k], o, 64);
+      z2 = __shfl_xor(zT[k], o, 64);
+      lse_merge(mT[k], zT[k], m2, z2);
     }
+    const int row = (rg * 16 + wave * 4 + k) * 16 + i16;
+    if (g4 == 0 && tile_ok[k] && rok[k])
+      partial[((int64_t)lg * nchunk + ck) * dm.rows + row] = make_float4(mC[k], zC[k], mT[k], zT[k]);
   }
 }
 
@@ -157,12 +156,14 @@ __global__ __launch_bounds__(256) void k_rowstats_combine(Dims dm, const float4*
   __shared__ float red[256];
   float acc = 0.f;
   for (int r = threadIdx.x; r < dm.rows; r += 256) {
-    float mv = -INFINITY, zv = 0.f, mc = -INFINITY, zc = 0.f;
+    float mc = -INFINITY, zc = 0.f, mt = -INFINITY, zt = 0.f;
     for (int c = 0; c < nchunk; ++c) {
-      float4 p = partial[((int64_t)lg * nchunk + c) * dm.rows + r];
-      lse_merge(mv, zv, p.x, p.y);
-      lse_merge(mc, zc, p.z, p.w);
+      const float4 p = partial[((int64_t)lg * nchunk + c) * dm.rows + r];
+      lse_merge(mc, zc, p.x, p.y);
+      lse_merge(mt, zt, p.z, p.w);
     }
+    float mv = mc, zv = zc;                    // V(u) = C + the visible tail
+    lse_merge(mv, zv, mt, zt);
     tv.row_stats[(int64_t)lg * dm.rows + r] = make_float4(mv, zv, mc, zc);
     if (zc > 0.f) acc += expf(mc - mv) * zc / zv;
     const int u = r % dm.W, hl = r / dm.W;

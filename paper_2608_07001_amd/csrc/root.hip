@@ -59,12 +59,6 @@ int root_lds_bytes(const Dims& dm) {
   return dm.d == 128 ? RootLds<float, 128>::bytes : RootLds<float, 64>::bytes;
 }
 
-__device__ __forceinline__ s16x4 pack_s16x4(uint32_t lo, uint32_t hi) {
-  s16x4 v;
-  v[0] = (short)(lo & 0xffffu); v[1] = (short)(lo >> 16);
-  v[2] = (short)(hi & 0xffffu); v[3] = (short)(hi >> 16);
-  return v;
-}
 __device__ __forceinline__ float pick4(const float* v, int i) {
   return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
@@ -240,8 +234,8 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
               if constexpr (BF) {
 #pragma unroll
                 for (int s = 0; s < QE / 4; ++s)
-                  acc = mfma_bf16_16x16x16(pack_s16x4(kreg[2 * s], kreg[2 * s + 1]),
-                                           pack_s16x4(qreg[kk][2 * s], qreg[kk][2 * s + 1]), acc);
+                  acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]),
+                                           pk4(qreg[kk][2 * s], qreg[kk][2 * s + 1]), acc);
               } else {
 #pragma unroll
                 for (int s = 0; s < QE; ++s)
@@ -268,7 +262,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
 #pragma unroll
               for (int dt = 0; dt < DT; ++dt) {
                 const uint2 vv = *(const uint2*)(sVt + (16 * dt + i16) * Lay::LDV + t0 + 4 * g4);
-                const s16x4 va = pack_s16x4(vv.x, vv.y);
+                const s16x4 va = pk4(vv.x, vv.y);
                 Macc[dt] = mfma_bf16_16x16x16(va, el, Macc[dt]);
                 Macc[dt] = mfma_bf16_16x16x16(va, em, Macc[dt]);
                 Macc[dt] = mfma_bf16_16x16x16(va, eh, Macc[dt]);
