@@ -65,7 +65,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 typedef struct {
   int32_t L, G, H, d;      /* layers, KV heads, query heads, head dim: 64 or 128 (fp32 data: 64) */
   int32_t n_seg;           /* hidden-state slabs (|L_seg|, eq:app_seg_layers), 1..8 */
-  int32_t D_hidden;        /* hidden size of each slab */
+  int32_t D_hidden;        /* hidden size of each slab (a multiple of 8) */
   int32_t W;               /* window queries (1..64) */
   int32_t dtype;           /* gracekv_dtype of K, V, Q and hidden */
   int64_t N_ctx;           /* context length */

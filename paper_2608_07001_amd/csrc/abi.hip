@@ -123,6 +123,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->flags & ~GRACEKV_FLAG_PRUNE) return GRACEKV_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
   if (c->dtype == GRACEKV_F32 && c->d != 64) return GRACEKV_ERR_UNSUPPORTED;   // refinement LDS
+  if (c->D_hidden % 8 != 0) return GRACEKV_ERR_UNSUPPORTED;                   // 16-byte hidden rows
   if (c->W > WMAX || c->n_seg > 8) return GRACEKV_ERR_UNSUPPORTED;
   if (c->n_min < 16 || c->n_max > NMAX || c->n_max < c->n_min || c->n0 < 1) return GRACEKV_ERR_UNSUPPORTED;
   if (c->win[0] != 4 || c->win[1] != 8 || c->win[2] != 16) return GRACEKV_ERR_UNSUPPORTED;

@@ -14,14 +14,14 @@
 //     b_i = z(kappa_i) + lam_s z(s_i) (eq:app_robust_z, eq:app_mad,
 //     eq:app_boundary_score).
 // K3  seg_gram: banded Gram <h_i, h_j>, 0 <= i - j < 128, of the raw hidden
-//     rows with MFMA (bf16 products are exact).  Since the prefix sums of d_t
+//     rows with MFMA (bf16 products are exact), LDS-tiled for bf16.  Since the prefix sums of d_t
 //     telescope, sum_{t=a}^{e-2} d_t = hbar_{e-1} - hbar_a, and
 //     ||hbar_i - hbar_j||^2 follows from the Gram and the row norms; with the
 //     fp64 prefix of ||d_t||^2 this gives the dispersion in O(1) per slot
 //     (eq:app_prefix_dispersion, eq:app_slot_dispersion).
-// K4  seg_dp: the DP of eq:app_dp_recurrence in fp64 by one workgroup.  With
-//     n_min = 16, F[i .. i+15] depend only on F[< i], so 16 states advance per
-//     step, one wave each, lanes over predecessor lengths; ties go to the
+// K4  seg_dp: slot scores tabulated in parallel (fp64), then the DP of
+//     eq:app_dp_recurrence by one workgroup.  With n_min >= 16, F[i .. i+15]
+//     depend only on F[< i], so 16 ends advance per step; ties go to the
 //     smallest predecessor; terminal relaxation eq:app_terminal_predecessor;
 //     backtrack from LDS.
 #include "common.h"
@@ -44,6 +44,7 @@ struct SegWs {
   uint8_t* Poff;    // [N_c + 1]
   float* scratch;   // [T] for the robust z
   double* Fdbg;     // [1]
+  double* S;        // [N_c][128] slot scores by (i, length), candidate-major per lane
 };
 
 static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -51,7 +52,7 @@ static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t segment_ws_bytes(const Dims& dm) {
   const size_t T = (size_t)dm.T, N = (size_t)dm.N_c;
   return al(dm.n_seg * 3 * T * 4) + al(dm.n_seg * T * 4) + al(T * 4) + al((size_t)dm.n_seg * T * BAND * 4) +
-         al(N * BAND * 4) + al((N + 1) * 8) + al(N + 1) + al(T * 4) + al(8);
+         al(N * BAND * 4) + al((N + 1) * 8) + al(N + 1) + al(T * 4) + al(8) + al(N * BAND * 8);
 }
 
 static SegWs seg_view(void* ws, const Dims& dm) {
@@ -66,7 +67,8 @@ static SegWs seg_view(void* ws, const Dims& dm) {
   s.P2 = (double*)p; p += al((N + 1) * 8);
   s.Poff = (uint8_t*)p; p += al(N + 1);
   s.scratch = (float*)p; p += al(T * 4);
-  s.Fdbg = (double*)p;
+  s.Fdbg = (double*)p; p += al(8);
+  s.S = (double*)p;
   return s;
 }
 
@@ -219,14 +221,95 @@ __global__ __launch_bounds__(1024) void k_robust_z(Dims dm, const float* __restr
 }
 
 // ---- K3: banded Gram --------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(192) void k_gram(Dims dm, const T* __restrict__ hidden, SegWs ws) {
-  constexpr bool BF = sizeof(T) == 2;
+// bf16: a workgroup owns 64 rows i0 .. i0+63 of one slab and the 192 rows
+// j in [i0 - 128, i0 + 64) they pair with; 64-dim chunks of those rows are
+// staged in LDS (double-buffered, 16-byte loads) and wave w accumulates the
+// 16 x 16 tiles (i-tile w, j-tile w .. w + 8) that touch the band.  A lane
+// supplies 16 consecutive dims of a chunk per operand (4 k-steps), so each
+// operand is two 16-byte LDS reads.
+constexpr int GB_I = 64;                 // rows i per workgroup
+constexpr int GB_J = GB_I + BAND;        // rows j staged
+constexpr int GB_C = 64;                 // dims per chunk
+constexpr int GB_LD = GB_C + 8;          // LDS row stride (bf16)
+
+__global__ __launch_bounds__(256) void k_gram_bf16(Dims dm, const uint16_t* __restrict__ hidden, SegWs ws) {
+  __shared__ __align__(16) uint16_t sh[2][GB_J * GB_LD];
+  const int slab = blockIdx.y;
+  const int64_t i0 = (int64_t)blockIdx.x * GB_I;
+  const int64_t j0 = i0 - BAND;
+  const int64_t T_ = dm.T;
+  const int Dh = dm.Dh;
+  const uint16_t* H = hidden + (int64_t)slab * T_ * Dh;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+  f32x4 acc[9];
+#pragma unroll
+  for (int k = 0; k < 9; ++k) acc[k] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int CPR = GB_C / 8;          // 16-byte chunks per staged row
+  auto stage = [&](int buf, int c0, uint4* reg) {
+#pragma unroll
+    for (int k = 0; k < (GB_J * CPR) / 256; ++k) {
+      const int e = tid + 256 * k;
+      const int r = e / CPR, c = (e % CPR) * 8;
+      const int64_t row = j0 + r;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (row >= 0 && row < T_ && c0 + c < Dh) v = *(const uint4*)(H + row * Dh + c0 + c);
+      reg[k] = v;
+    }
+  };
+  auto store = [&](int buf, const uint4* reg) {
+#pragma unroll
+    for (int k = 0; k < (GB_J * CPR) / 256; ++k) {
+      const int e = tid + 256 * k;
+      const int r = e / CPR, c = (e % CPR) * 8;
+      *(uint4*)(sh[buf] + r * GB_LD + c) = reg[k];
+    }
+  };
+  uint4 reg[(GB_J * CPR) / 256];
+  stage(0, 0, reg);
+  store(0, reg);
+  int buf = 0;
+  for (int c0 = 0; c0 < Dh; c0 += GB_C) {
+    __syncthreads();
+    const bool more = c0 + GB_C < Dh;
+    if (more) stage(buf ^ 1, c0 + GB_C, reg);              // next chunk in flight
+    const uint16_t* base = sh[buf];
+    // A: rows i0 + 16 w + i16 = staged row 128 + 16 w + i16
+    const uint4* pa = (const uint4*)(base + (BAND + 16 * wave + i16) * GB_LD + 16 * g4);
+    const uint4 a0 = pa[0], a1 = pa[1];
+    const uint32_t aw[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+      const uint4* pb = (const uint4*)(base + (16 * (wave + k) + i16) * GB_LD + 16 * g4);
+      const uint4 b0 = pb[0], b1 = pb[1];
+      const uint32_t bw[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        acc[k] = mfma_bf16_16x16x16(pk4(aw[2 * s], aw[2 * s + 1]), pk4(bw[2 * s], bw[2 * s + 1]), acc[k]);
+    }
+    if (more) store(buf ^ 1, reg);
+    buf ^= 1;
+  }
+  // C[i][j]: lane holds i = 4 g4 + r of the i-tile, j = i16 of the j-tile
+#pragma unroll
+  for (int k = 0; k < 9; ++k) {
+    const int64_t j = j0 + 16 * (wave + k) + i16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t i = i0 + 16 * wave + 4 * g4 + r;
+      const int64_t dlt = i - j;
+      if (i < T_ && j >= 0 && dlt >= 0 && dlt < BAND)
+        ws.gram[((int64_t)slab * T_ + i) * BAND + dlt] = acc[k][r];
+    }
+  }
+}
+
+// fp32: one 16-row tile per workgroup, operands straight from memory
+__global__ __launch_bounds__(192) void k_gram_f32(Dims dm, const float* __restrict__ hidden, SegWs ws) {
   const int slab = blockIdx.y;
   const int64_t i0 = (int64_t)blockIdx.x * 16;
   const int64_t T_ = dm.T;
   const int Dh = dm.Dh;
-  const T* H = hidden + (int64_t)slab * T_ * Dh;
+  const float* H = hidden + (int64_t)slab * T_ * Dh;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t ri = i0 + (lane & 15);
   const bool iok = ri < T_;
@@ -239,33 +322,13 @@ __global__ __launch_bounds__(192) void k_gram(Dims dm, const T* __restrict__ hid
     rj[k] = i0 - BAND + 16 * (wave * 3 + k) + (lane & 15);
     jok[k] = rj[k] >= 0 && rj[k] < T_;
   }
-  if constexpr (BF) {
-    const uint16_t* Hb = (const uint16_t*)H;
-    for (int s = 0; s < Dh; s += 16) {
-      const int kc = s + 4 * (lane >> 4);
-      s16x4 a;
-      const uint16_t* pa = Hb + (iok ? ri : 0) * Dh + kc;
-      a[0] = iok ? (short)pa[0] : 0; a[1] = iok ? (short)pa[1] : 0;
-      a[2] = iok ? (short)pa[2] : 0; a[3] = iok ? (short)pa[3] : 0;
+  for (int s = 0; s < Dh; s += 4) {
+    const int kc = s + (lane >> 4);
+    const float a = iok ? H[ri * Dh + kc] : 0.f;
 #pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        s16x4 b;
-        const uint16_t* pb = Hb + (jok[k] ? rj[k] : 0) * Dh + kc;
-        b[0] = jok[k] ? (short)pb[0] : 0; b[1] = jok[k] ? (short)pb[1] : 0;
-        b[2] = jok[k] ? (short)pb[2] : 0; b[3] = jok[k] ? (short)pb[3] : 0;
-        acc[k] = mfma_bf16_16x16x16(a, b, acc[k]);
-      }
-    }
-  } else {
-    const float* Hf = (const float*)H;
-    for (int s = 0; s < Dh; s += 4) {
-      const int kc = s + (lane >> 4);
-      const float a = iok ? Hf[ri * Dh + kc] : 0.f;
-#pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        const float b = jok[k] ? Hf[rj[k] * Dh + kc] : 0.f;
-        acc[k] = mfma_f32_16x16x4(a, b, acc[k]);
-      }
+    for (int k = 0; k < 3; ++k) {
+      const float b = jok[k] ? H[rj[k] * Dh + kc] : 0.f;
+      acc[k] = mfma_f32_16x16x4(a, b, acc[k]);
     }
   }
 #pragma unroll
@@ -325,69 +388,109 @@ __global__ __launch_bounds__(1024) void k_prefix_sq(Dims dm, SegWs ws) {
 }
 
 // ---- K4: DP -----------------------------------------------------------------
+// The slot score Gamma(a) - lam_d Disp([a, i)) - lam_n ((i - a - n0) / n0)^2 of
+// eq:app_dp_recurrence does not depend on F: it is tabulated for every end i
+// and length in parallel (fp64), then the recurrence only adds F[a] and takes
+// the maximum.  Candidate c = len - n_min of end i is stored at
+// S[(i - 1) * 128 + (c % 16) * 8 + c / 16], so the lane that owns candidates
+// c = sub, sub + 16, ... reads 8 consecutive doubles.
 __device__ __forceinline__ void dp_better(double& bv, int64_t& ba, double v, int64_t a) {
   if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
 }
 
-__global__ __launch_bounds__(1024) void k_dp(Dims dm, const float* __restrict__ b, SegWs ws, int32_t* slots,
-                                             int32_t* nslots, int use_lds) {
+__device__ __forceinline__ double slot_score(const Dims& dm, const float* __restrict__ b, const SegWs& ws, int64_t i,
+                                             int len) {
+  const int64_t a = i - len;
+  const double gam = a == 0 ? 0.0 : (double)b[a - 1] - (double)dm.c_cut;
+  const int nS = len - 1;
+  double disp = 0.0;
+  if (nS >= 1) {
+    const double s2 = ws.P2[i - 1] - ws.P2[a];
+    const double dd = (double)ws.dist2[(i - 1) * BAND + (len - 1)];
+    disp = (s2 - dd / nS) / (double)(nS - 1 > 1 ? nS - 1 : 1);
+  }
+  const double x = (len - (double)dm.n0) / (double)dm.n0;
+  return gam - (double)dm.lam_d * disp - (double)dm.lam_n * x * x;
+}
+
+__global__ __launch_bounds__(128) void k_slot_scores(Dims dm, const float* __restrict__ b, SegWs ws) {
+  const int64_t i = (int64_t)blockIdx.x + 1;
+  const int c = threadIdx.x;
+  const int len = dm.n_min + c;
+  double v = -INFINITY;
+  if (len <= dm.n_max && i - len >= 0) v = slot_score(dm, b, ws, i, len);
+  ws.S[(i - 1) * BAND + (c % 16) * 8 + c / 16] = v;
+}
+
+// F over [1, N] in steps of 16 ends (an end depends only on ends >= 16
+// positions earlier): wave w owns ends i0 + 4 w .. i0 + 4 w + 3, 16 lanes per
+// end, each lane 8 candidate lengths; ties go to the smallest start.  Terminal
+// relaxation eq:app_terminal_predecessor, then the backtrack.
+__global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b, SegWs ws, int32_t* slots,
+                                            int32_t* nslots, int use_lds) {
   extern __shared__ __align__(16) char dsm[];
-  __shared__ double Fr[256];
-  __shared__ double Fn[16];
-  __shared__ int Pn[16];
+  __shared__ double Fr[256];                 // F ring indexed by end & 255
   uint8_t* Poff = use_lds ? (uint8_t*)dsm : ws.Poff;
   const int64_t N = dm.N_c;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int st = lane >> 4, sub = lane & 15;
   if (N <= 0) {
-    if (threadIdx.x == 0) { slots[0] = 0; *nslots = 0; }
+    if (tid == 0) { slots[0] = 0; *nslots = 0; }
     return;
   }
-  if (threadIdx.x < 256) Fr[threadIdx.x] = -INFINITY;
+  Fr[tid] = -INFINITY;
   __syncthreads();
-  if (threadIdx.x == 0) { Fr[0] = 0.0; Poff[0] = 0; }
+  if (tid == 0) { Fr[0] = 0.0; Poff[0] = 0; }
   __syncthreads();
-  const double lam_d = dm.lam_d, lam_n = dm.lam_n, c_cut = dm.c_cut, n0 = dm.n0;
-  auto cand = [&](int64_t i, int len, double& bv, int64_t& ba) {
-    const int64_t a = i - len;
-    if (a < 0) return;
-    const double Fa = Fr[a & 255];
-    if (Fa == -INFINITY) return;
-    const double gam = a == 0 ? 0.0 : (double)b[a - 1] - c_cut;
-    const int nS = len - 1;
-    double disp = 0.0;
-    if (nS >= 1) {
-      const double s2 = ws.P2[i - 1] - ws.P2[a];
-      const double dd = (double)ws.dist2[(i - 1) * BAND + (len - 1)];
-      disp = (s2 - dd / nS) / (double)(nS - 1 > 1 ? nS - 1 : 1);
+  auto load = [&](int64_t i, double* sv) {
+    if (i <= N) {
+      const double2* p = (const double2*)(ws.S + (i - 1) * BAND + sub * 8);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) { const double2 v = p[k]; sv[2 * k] = v.x; sv[2 * k + 1] = v.y; }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) sv[k] = -INFINITY;
     }
-    const double x = (len - n0) / n0;
-    dp_better(bv, ba, Fa + gam - lam_d * disp - lam_n * x * x, a);
   };
+  double cur[8], nxt[8];
+  load(1 + 4 * wave + st, cur);
   for (int64_t i0 = 1; i0 <= N; i0 += 16) {
-    const int64_t i = i0 + wave;
+    const int64_t i = i0 + 4 * wave + st;
+    load(i + 16, nxt);                       // next step's scores in flight
     double bv = -INFINITY;
     int64_t ba = -1;
-    if (i <= N)
-      for (int len = dm.n_min + lane; len <= dm.n_max; len += 64) cand(i, len, bv, ba);
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
+    for (int k = 0; k < 8; ++k) {
+      const int len = dm.n_min + sub + 16 * k;
+      const int64_t a = i - len;
+      if (i <= N && len <= dm.n_max && a >= 0) {
+        const double Fa = Fr[a & 255];
+        if (Fa != -INFINITY) dp_better(bv, ba, Fa + cur[k], a);
+      }
+    }
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) {
       const double v2 = __shfl_xor(bv, o, 64);
       const int64_t a2 = __shfl_xor(ba, o, 64);
       if (a2 >= 0) dp_better(bv, ba, v2, a2);
     }
-    if (lane == 0) { Fn[wave] = bv; Pn[wave] = ba >= 0 ? (int)(i - ba) : 0; }
+    __syncthreads();                         // every end of this step has read its F
+    if (sub == 0 && i <= N) { Fr[i & 255] = bv; Poff[i] = ba >= 0 ? (uint8_t)(i - ba) : 0; }
     __syncthreads();
-    if (threadIdx.x < 16) {
-      const int64_t ii = i0 + threadIdx.x;
-      if (ii <= N) { Fr[ii & 255] = Fn[threadIdx.x]; Poff[ii] = (uint8_t)Pn[threadIdx.x]; }
-    }
-    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 8; ++k) cur[k] = nxt[k];
   }
   // terminal relaxation of the last slot's minimum length
   if (Poff[N] == 0 && wave == 0) {
     double bv = -INFINITY;
     int64_t ba = -1;
-    for (int len = 1 + lane; len <= dm.n_max; len += 64) cand(N, len, bv, ba);
+    for (int len = 1 + lane; len <= dm.n_max; len += 64) {
+      const int64_t a = N - len;
+      if (a < 0) continue;
+      const double Fa = Fr[a & 255];
+      if (Fa == -INFINITY) continue;
+      dp_better(bv, ba, Fa + slot_score(dm, b, ws, N, len), a);
+    }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
       const double v2 = __shfl_xor(bv, o, 64);
@@ -395,11 +498,11 @@ __global__ __launch_bounds__(1024) void k_dp(Dims dm, const float* __restrict__ 
       if (a2 >= 0) dp_better(bv, ba, v2, a2);
     }
     if (lane == 0) { Poff[N] = ba >= 0 ? (uint8_t)(N - ba) : 0; ws.Fdbg[0] = bv; }
-  } else if (threadIdx.x == 0) {
+  } else if (tid == 0) {
     ws.Fdbg[0] = Fr[N & 255];
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     int J = 0;
     for (int64_t i = N; i > 0; i -= Poff[i]) {
       if (Poff[i] == 0) break;
@@ -416,13 +519,14 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
                           int32_t* slot_starts, int32_t* n_slots, void* wsp, hipStream_t st) {
   SegWs ws = seg_view(wsp, dm);
   const dim3 g1((unsigned)((dm.T + CT - 1) / CT), dm.n_seg);
-  const dim3 g3((unsigned)((dm.T + 15) / 16), dm.n_seg);
   if (dm.dtype == GRACEKV_BF16) {
     hipLaunchKernelGGL(k_curvature<uint16_t>, g1, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
-    hipLaunchKernelGGL(k_gram<uint16_t>, g3, dim3(192), 0, st, dm, (const uint16_t*)hidden, ws);
+    const dim3 g3((unsigned)((dm.T + GB_I - 1) / GB_I), dm.n_seg);
+    hipLaunchKernelGGL(k_gram_bf16, g3, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
   } else {
     hipLaunchKernelGGL(k_curvature<float>, g1, dim3(256), 0, st, dm, (const float*)hidden, ws);
-    hipLaunchKernelGGL(k_gram<float>, g3, dim3(192), 0, st, dm, (const float*)hidden, ws);
+    const dim3 g3((unsigned)((dm.T + 15) / 16), dm.n_seg);
+    hipLaunchKernelGGL(k_gram_f32, g3, dim3(192), 0, st, dm, (const float*)hidden, ws);
   }
   hipLaunchKernelGGL(k_stabilize, dim3((unsigned)((dm.T + 255) / 256)), dim3(256), 0, st, dm, ws, kappa);
   hipLaunchKernelGGL(k_robust_z, dim3(1), dim3(1024), 0, st, dm, (const float*)kappa, surprisal, bscore);
@@ -437,7 +541,9 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
     hipError_t e = hipFuncSetAttribute((const void*)k_dp, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k_dp, dim3(1), dim3(1024), dyn, st, dm, (const float*)bscore, ws, slot_starts, n_slots, use_lds);
+  if (dm.N_c > 0)
+    hipLaunchKernelGGL(k_slot_scores, dim3((unsigned)dm.N_c), dim3(BAND), 0, st, dm, (const float*)bscore, ws);
+  hipLaunchKernelGGL(k_dp, dim3(1), dim3(256), dyn, st, dm, (const float*)bscore, ws, slot_starts, n_slots, use_lds);
   return hipGetLastError();
 }
 
