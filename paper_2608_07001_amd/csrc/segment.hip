@@ -1,8 +1,8 @@
 // Curvature-guided slot segmentation (App. B.2 - B.3).
 //
 // K1  seg_curvature: per slab and 64-position tile, L2-normalised hidden rows
-//     (eq:app_hidden_normalization) are staged in LDS column-chunk by
-//     column-chunk; each position accumulates, for w in {4, 8, 16}, the three
+//     (eq:app_hidden_normalization; norms from the Gram diagonal of K3) are
+//     staged in LDS column-chunk by column-chunk; each position accumulates, for w in {4, 8, 16}, the three
 //     dot products of delta_- = hbar_i - mean(hbar_{i-w+1..i}) and
 //     delta_+ = mean(hbar_{i+1..i+w}) - hbar_i (eq:app_local_means,
 //     eq:app_local_directions), giving kappa^{(l,w)} (eq:app_local_curvature;
@@ -28,10 +28,11 @@
 
 namespace gkv {
 
-constexpr int CT = 64;                  // positions per curvature tile
+constexpr int CT = 64;                  // positions per curvature tile (one per lane)
 constexpr int CHALO = 16;               // max window
 constexpr int CROWS = CT + 2 * CHALO;   // rows staged (i0 - 16 .. i0 + 80)
 constexpr int CCOL = 64;                // columns per LDS chunk
+constexpr int CLD = CCOL + 4;           // LDS row stride: 16-byte reads of 16 consecutive rows hit distinct banks
 constexpr int BAND = 128;
 
 struct SegWs {
@@ -72,82 +73,117 @@ static SegWs seg_view(void* ws, const Dims& dm) {
   return s;
 }
 
+// Lane p owns position i0 + p; wave w owns the column quads w, w + 4, ... of
+// each 64-column chunk and keeps partial dot products, summed over the waves
+// at the end.  Rows are scaled by 1 / max(||h||, eps) while staged, the norm
+// taken from the diagonal of the banded Gram (computed first).
 template <typename T>
 __global__ __launch_bounds__(256) void k_curvature(Dims dm, const T* __restrict__ hidden, SegWs ws) {
-  __shared__ float nrm[CROWS];
-  __shared__ float hb[CROWS][CCOL + 1];
+  __shared__ float inv[CROWS];
+  __shared__ __align__(16) float hb[CROWS * CLD];
+  __shared__ float red[4][10][CT];
   const int slab = blockIdx.y;
   const int64_t i0 = (int64_t)blockIdx.x * CT;
   const int64_t T_ = dm.T;
   const int Dh = dm.Dh;
   const T* H = hidden + (int64_t)slab * T_ * Dh;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  for (int rr = wave; rr < CROWS; rr += 4) {
-    const int64_t i = i0 - CHALO + rr;
-    float s = 0.f;
-    if (i >= 0 && i < T_)
-      for (int c = lane; c < Dh; c += 64) { const float x = ldf(H, i * Dh + c); s += x * x; }
-    s = wave_sum(s);
-    if (lane == 0) nrm[rr] = fmaxf(sqrtf(s), dm.eps_seg);
+  if (tid < CROWS) {
+    const int64_t i = i0 - CHALO + tid;
+    float v = 0.f;
+    if (i >= 0 && i < T_) v = 1.0f / fmaxf(sqrtf(ws.gram[((int64_t)slab * T_ + i) * BAND]), dm.eps_seg);
+    inv[tid] = v;
   }
-  const int p = tid >> 2, qq = tid & 3;
-  const int rr_i = p + CHALO;
+  const int rr = lane + CHALO;
   float acc[3][3], accD = 0.f;
 #pragma unroll
   for (int w = 0; w < 3; ++w) acc[w][0] = acc[w][1] = acc[w][2] = 0.f;
+  constexpr int EPL = 16 / (int)sizeof(T);          // elements per 16-byte load
+  constexpr int LPR = CCOL / EPL;                   // loads per staged row
   for (int c0 = 0; c0 < Dh; c0 += CCOL) {
     __syncthreads();
-    for (int e = tid; e < CROWS * CCOL; e += 256) {
-      const int rr = e / CCOL, c = e % CCOL;
-      const int64_t i = i0 - CHALO + rr;
-      float x = 0.f;
-      if (i >= 0 && i < T_ && c0 + c < Dh) x = ldf(H, i * Dh + c0 + c) / nrm[rr];
-      hb[rr][c] = x;
+    for (int e = tid; e < CROWS * LPR; e += 256) {
+      const int r = e / LPR, c = (e % LPR) * EPL;
+      const int64_t i = i0 - CHALO + r;
+      float x[EPL];
+#pragma unroll
+      for (int k = 0; k < EPL; ++k) x[k] = 0.f;
+      if (i >= 0 && i < T_ && c0 + c < Dh) {
+        const float sc = inv[r];
+        if constexpr (sizeof(T) == 2) {
+          const uint4 u = *(const uint4*)(H + i * Dh + c0 + c);
+          const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            x[2 * h] = __uint_as_float(w4[h] << 16) * sc;
+            x[2 * h + 1] = __uint_as_float(w4[h] & 0xffff0000u) * sc;
+          }
+        } else {
+          const float4 u = *(const float4*)((const float*)H + i * Dh + c0 + c);
+          x[0] = u.x * sc; x[1] = u.y * sc; x[2] = u.z * sc; x[3] = u.w * sc;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < EPL; k += 4) *(float4*)(hb + r * CLD + c + k) = make_float4(x[k], x[k + 1], x[k + 2], x[k + 3]);
     }
     __syncthreads();
-    for (int c = qq; c < CCOL; c += 4) {
-      const float x = hb[rr_i][c];
-      float sm = 0.f, sp = 0.f;
+#pragma unroll 1
+    for (int qd = wave; qd < CCOL / 4; qd += 4) {
+      const int c = 4 * qd;
+      const float4 x4 = *(const float4*)(hb + rr * CLD + c);
+      const float xv[4] = {x4.x, x4.y, x4.z, x4.w};
+      float sm[4] = {0.f, 0.f, 0.f, 0.f}, sp[4] = {0.f, 0.f, 0.f, 0.f};
       int tau = 0;
 #pragma unroll
       for (int w = 0; w < 3; ++w) {
         const int ww = w == 0 ? 4 : (w == 1 ? 8 : 16);
+#pragma unroll
         for (; tau < ww; ++tau) {
-          sm += hb[rr_i - tau][c];
-          sp += hb[rr_i + 1 + tau][c];
+          const float4 a = *(const float4*)(hb + (rr - tau) * CLD + c);
+          const float4 b = *(const float4*)(hb + (rr + 1 + tau) * CLD + c);
+          sm[0] += a.x; sm[1] += a.y; sm[2] += a.z; sm[3] += a.w;
+          sp[0] += b.x; sp[1] += b.y; sp[2] += b.z; sp[3] += b.w;
         }
-        const float dmn = x - sm / (float)ww;
-        const float dpl = sp / (float)ww - x;
-        acc[w][0] += dmn * dpl;
-        acc[w][1] += dmn * dmn;
-        acc[w][2] += dpl * dpl;
+        const float iw = 1.0f / (float)ww;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float dmn = xv[k] - sm[k] * iw;
+          const float dpl = sp[k] * iw - xv[k];
+          acc[w][0] += dmn * dpl;
+          acc[w][1] += dmn * dmn;
+          acc[w][2] += dpl * dpl;
+        }
       }
-      const float dd = hb[rr_i + 1][c] - x;
-      accD += dd * dd;
+      const float4 n4 = *(const float4*)(hb + (rr + 1) * CLD + c);
+      const float nv[4] = {n4.x, n4.y, n4.z, n4.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) { const float dd = nv[k] - xv[k]; accD += dd * dd; }
     }
   }
 #pragma unroll
   for (int w = 0; w < 3; ++w)
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-      acc[w][k] += __shfl_xor(acc[w][k], 1, 64);
-      acc[w][k] += __shfl_xor(acc[w][k], 2, 64);
-    }
-  accD += __shfl_xor(accD, 1, 64);
-  accD += __shfl_xor(accD, 2, 64);
-  const int64_t i = i0 + p;
-  if (qq == 0 && i < T_) {
+    for (int k = 0; k < 3; ++k) red[wave][3 * w + k][lane] = acc[w][k];
+  red[wave][9][lane] = accD;
+  __syncthreads();
+  if (wave == 0) {
+    float v[10];
 #pragma unroll
-    for (int w = 0; w < 3; ++w) {
-      const int ww = dm.win[w];
-      float kap = 0.f;
-      if (i >= ww && i < T_ - ww) {
-        const float nm = fmaxf(sqrtf(acc[w][1]), dm.eps_seg), np = fmaxf(sqrtf(acc[w][2]), dm.eps_seg);
-        kap = 1.f - acc[w][0] / (nm * np);
+    for (int k = 0; k < 10; ++k) v[k] = red[0][k][lane] + red[1][k][lane] + red[2][k][lane] + red[3][k][lane];
+    const int64_t i = i0 + lane;
+    if (i < T_) {
+#pragma unroll
+      for (int w = 0; w < 3; ++w) {
+        const int ww = dm.win[w];
+        float kap = 0.f;
+        if (i >= ww && i < T_ - ww) {
+          const float nm = fmaxf(sqrtf(v[3 * w + 1]), dm.eps_seg), np = fmaxf(sqrtf(v[3 * w + 2]), dm.eps_seg);
+          kap = 1.f - v[3 * w] / (nm * np);
+        }
+        ws.kap9[((int64_t)slab * 3 + w) * T_ + i] = kap;
       }
-      ws.kap9[((int64_t)slab * 3 + w) * T_ + i] = kap;
+      ws.sqd[(int64_t)slab * T_ + i] = (i + 1 < T_) ? v[9] : 0.f;
     }
-    ws.sqd[(int64_t)slab * T_ + i] = (i + 1 < T_) ? accD : 0.f;
   }
 }
 
@@ -398,6 +434,28 @@ __device__ __forceinline__ void dp_better(double& bv, int64_t& ba, double v, int
   if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
 }
 
+__device__ __forceinline__ void dp_better32(double& bv, int& ba, double v, int a) {
+  if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
+}
+// one DPP step of the (value, smallest start) maximum within 16-lane rows
+template <int CTRL>
+__device__ __forceinline__ void dp_step(double& bv, int& ba) {
+  const long long b = __double_as_longlong(bv);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffll), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xf, 0xf, false);
+  const int a2 = __builtin_amdgcn_update_dpp(0, ba, CTRL, 0xf, 0xf, false);
+  const double v2 = __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
+  if (a2 >= 0) dp_better32(bv, ba, v2, a2);
+}
+// every lane of a 16-lane row ends with the row's best: lanes ^1, ^2 (quad
+// permutes), then rotations by 4 and 8 within the row
+__device__ __forceinline__ void dp_reduce16(double& bv, int& ba) {
+  dp_step<0xB1>(bv, ba);     // quad_perm(1, 0, 3, 2)
+  dp_step<0x4E>(bv, ba);     // quad_perm(2, 3, 0, 1)
+  dp_step<0x124>(bv, ba);    // row_ror:4
+  dp_step<0x128>(bv, ba);    // row_ror:8
+}
+
 __device__ __forceinline__ double slot_score(const Dims& dm, const float* __restrict__ b, const SegWs& ws, int64_t i,
                                              int len) {
   const int64_t a = i - len;
@@ -452,33 +510,33 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
       for (int k = 0; k < 8; ++k) sv[k] = -INFINITY;
     }
   };
-  double cur[8], nxt[8];
-  load(1 + 4 * wave + st, cur);
-  for (int64_t i0 = 1; i0 <= N; i0 += 16) {
-    const int64_t i = i0 + 4 * wave + st;
-    load(i + 16, nxt);                       // next step's scores in flight
-    double bv = -INFINITY;
-    int64_t ba = -1;
+  // scores of 4 steps in flight (static register indices: the step loop is unrolled by 4)
+  double sv[4][8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int len = dm.n_min + sub + 16 * k;
-      const int64_t a = i - len;
-      if (i <= N && len <= dm.n_max && a >= 0) {
-        const double Fa = Fr[a & 255];
-        if (Fa != -INFINITY) dp_better(bv, ba, Fa + cur[k], a);
+  for (int q = 0; q < 4; ++q) load(1 + 16 * q + 4 * wave + st, sv[q]);
+  for (int64_t i00 = 1; i00 <= N; i00 += 64) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t i0 = i00 + 16 * q;
+      if (i0 > N) break;
+      const int64_t i = i0 + 4 * wave + st;
+      double bv = -INFINITY;
+      int ba = -1;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int len = dm.n_min + sub + 16 * k;
+        const int64_t a = i - len;
+        if (i <= N && len <= dm.n_max && a >= 0) {
+          const double Fa = Fr[a & 255];
+          if (Fa != -INFINITY) dp_better32(bv, ba, Fa + sv[q][k], (int)a);
+        }
       }
+      load(i + 64, sv[q]);                   // the same lane's end four steps later
+      dp_reduce16(bv, ba);
+      __syncthreads();                       // every end of this step has read its F
+      if (sub == 0 && i <= N) { Fr[i & 255] = bv; Poff[i] = ba >= 0 ? (uint8_t)(i - ba) : 0; }
+      __syncthreads();
     }
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) {
-      const double v2 = __shfl_xor(bv, o, 64);
-      const int64_t a2 = __shfl_xor(ba, o, 64);
-      if (a2 >= 0) dp_better(bv, ba, v2, a2);
-    }
-    __syncthreads();                         // every end of this step has read its F
-    if (sub == 0 && i <= N) { Fr[i & 255] = bv; Poff[i] = ba >= 0 ? (uint8_t)(i - ba) : 0; }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 8; ++k) cur[k] = nxt[k];
   }
   // terminal relaxation of the last slot's minimum length
   if (Poff[N] == 0 && wave == 0) {
@@ -519,14 +577,15 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
                           int32_t* slot_starts, int32_t* n_slots, void* wsp, hipStream_t st) {
   SegWs ws = seg_view(wsp, dm);
   const dim3 g1((unsigned)((dm.T + CT - 1) / CT), dm.n_seg);
+  // the Gram first: its diagonal gives the row norms of the curvature pass
   if (dm.dtype == GRACEKV_BF16) {
-    hipLaunchKernelGGL(k_curvature<uint16_t>, g1, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
     const dim3 g3((unsigned)((dm.T + GB_I - 1) / GB_I), dm.n_seg);
     hipLaunchKernelGGL(k_gram_bf16, g3, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
+    hipLaunchKernelGGL(k_curvature<uint16_t>, g1, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
   } else {
-    hipLaunchKernelGGL(k_curvature<float>, g1, dim3(256), 0, st, dm, (const float*)hidden, ws);
     const dim3 g3((unsigned)((dm.T + 15) / 16), dm.n_seg);
     hipLaunchKernelGGL(k_gram_f32, g3, dim3(192), 0, st, dm, (const float*)hidden, ws);
+    hipLaunchKernelGGL(k_curvature<float>, g1, dim3(256), 0, st, dm, (const float*)hidden, ws);
   }
   hipLaunchKernelGGL(k_stabilize, dim3((unsigned)((dm.T + 255) / 256)), dim3(256), 0, st, dm, ws, kappa);
   hipLaunchKernelGGL(k_robust_z, dim3(1), dim3(1024), 0, st, dm, (const float*)kappa, surprisal, bscore);
