@@ -277,7 +277,7 @@ __device__ void proto_attention(Ref<T, D>& U, const Dims& dm, int nl, int nr, co
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int q = 16 * pt + 4 * g4 + r;
-        if (q < dm.W) U.Zt[gc * WMAX + q] = me * expf(acc[r] * scale - U.Mq[q]);
+        if (q < dm.W) U.Zt[gc * WMAX + q] = me * fexp(acc[r] * scale - U.Mq[q]);
       }
     }
   }
@@ -312,7 +312,7 @@ __device__ __forceinline__ void block_e(const T* __restrict__ Kp, int n, int blk
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int t = 16 * blk + 4 * g4 + r;
-    ev[r] = (pok && t < n) ? expf(acc[r] * scale - mq) : 0.f;
+    ev[r] = (pok && t < n) ? fexp(acc[r] * scale - mq) : 0.f;
   }
 }
 

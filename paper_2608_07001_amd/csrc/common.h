@@ -114,6 +114,24 @@ __device__ __forceinline__ float ldf(const uint16_t* p, int64_t i) { return bf16
 __device__ __forceinline__ void stf(float* p, int64_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16_rne(v); }
 
+// Workgroup barrier that orders LDS accesses only: unlike __syncthreads() it
+// does not wait for the wave's global loads in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Sum over the 16 lanes of each row (every lane gets it): lanes ^1, ^2 by
+// quad permutes, then rotations by 4 and 8 within the row.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+  return v;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll
@@ -125,6 +143,11 @@ __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
 }
+
+// e^x as the hardware base-2 exponential (v_exp_f32, about 1 ulp) of
+// x log2(e); the rounding of that product adds a relative error of about
+// |x| 2^-24, the same order as the rounding already carried by x.
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
 
 // Merge two (max, sum-of-exp) pairs: the sum is relative to its max.
 __device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2) {

@@ -31,8 +31,8 @@ int rowstats_chunks(const Dims& dm) { return (int)((dm.T + RS_CHUNK - 1) / RS_CH
 __device__ __forceinline__ void lse_add4(float& m, float& z, float x0, float x1, float x2, float x3) {
   const float mn = fmaxf(m, fmaxf(fmaxf(x0, x1), fmaxf(x2, x3)));
   if (mn == -INFINITY) return;
-  if (mn > m) z *= expf(m - mn);
-  z += expf(x0 - mn) + expf(x1 - mn) + expf(x2 - mn) + expf(x3 - mn);
+  if (mn > m) z *= fexp(m - mn);
+  z += fexp(x0 - mn) + fexp(x1 - mn) + fexp(x2 - mn) + fexp(x3 - mn);
   m = mn;
 }
 

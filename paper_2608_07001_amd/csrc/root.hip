@@ -22,7 +22,7 @@
 // product M^T = V^T E^T (values x probes), which the matrix cores accumulate
 // over the unit; e is split into three bf16 parts so the products are exact
 // (fp32 data uses the fp32 matrix instruction directly).  The Q quarter rows of
-// up to 2 heads are held in registers at a time.
+// one head at a time is held in registers, the next one in flight.
 #include "common.h"
 
 namespace gkv {
@@ -36,7 +36,7 @@ struct RootLds {
   static constexpr bool BF = sizeof(T) == 2;
   static constexpr int LDK = BF ? D + 8 : D + 4;        // K rows [NMAX][LDK]
   static constexpr int LDV = BF ? NMAX + 8 : NMAX + 4;  // V^T rows [D][LDV]
-  static constexpr int NPK = RT / (D / 2);              // token phases of the k° sums
+  static constexpr int NPK = RWV;                       // per-wave partial sums of k°
   static constexpr int NPV = RT / D;                    // token phases of the v sums
   static constexpr int oK = 0;
   static constexpr int oVt = oK + NMAX * LDK * (int)sizeof(T);
@@ -92,7 +92,6 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   constexpr int DT = D / 16;                 // 16-wide value tiles of M^T
   constexpr int QE = D / 4;                  // elements of a lane's quarter row
   constexpr int QW = BF ? QE / 2 : QE;       // ... in 32-bit words
-  constexpr int HG = BF ? 2 : 1;             // heads per register group
   extern __shared__ __align__(16) char smem[];
   T* sK = (T*)(smem + Lay::oK);
   T* sVt = (T*)(smem + Lay::oVt);
@@ -124,11 +123,11 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   const int uq = uok ? u : 0;
   const int hp = uq % dm.hpg;                 // query head of probe u
   const bool wave_on = 16 * w < dm.W;
-  const int ngr = (dm.hpg + HG - 1) / HG;
 
-  uint32_t qreg[HG][QW];                      // Q quarter rows (head slots k0 .. k0+HG-1)
-  float2 rs[HG];                              // (m_V, Z_V) of the lane's rows
-  float mq = 0.f, zcq = 1.f;                  // probe shift and Z_q(C)
+  constexpr int CHP = H2 / 8;                // 8-dim pair chunks per token in the k° staging
+  uint32_t qa[QW], qb[QW];                    // Q quarter rows: current head, next head
+  float2 rsa = make_float2(0.f, 1.f), rsb = rsa;   // (m_V, 1 / Z_V) of the lane's rows
+  float mq = 0.f, zcq = 1.f;                  // probe shift and 1 / Z_q(C)
 
   for (int64_t uu = ub; uu < ue; ++uu) {
     const int lg = (int)(uu / J), j = (int)(uu % J);
@@ -144,43 +143,103 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
     const int n_tt = rows16 / 16;
     const T* Kp = K + ((int64_t)lg * dm.T + a0) * D;
     const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
-    // Q quarter rows and row statistics of head group gr (issued early for the last group)
-    auto load_q = [&](int gr) {
-      const int k0 = gr * HG;
+    // Q quarter row and row statistics of head slot k (head (hp + k) mod |H(g)|)
+    auto load_q = [&](int k, uint32_t* q, float2& rsv) {
+      const int hl = (hp + k) % dm.hpg;
+      const uint4* q4 = (const uint4*)(Q + (((int64_t)l * dm.H + (int64_t)g * dm.hpg + hl) * dm.W + uq) * D + QE * g4);
 #pragma unroll
-      for (int kk = 0; kk < HG; ++kk) {
-        if (k0 + kk < dm.hpg) {
-          const int hl = (hp + k0 + kk) % dm.hpg;
-          const uint4* q4 = (const uint4*)(Q + (((int64_t)l * dm.H + (int64_t)g * dm.hpg + hl) * dm.W + uq) * D + QE * g4);
-#pragma unroll
-          for (int h = 0; h < QW / 4; ++h) {
-            const uint4 v = q4[h];
-            qreg[kk][4 * h] = v.x; qreg[kk][4 * h + 1] = v.y; qreg[kk][4 * h + 2] = v.z; qreg[kk][4 * h + 3] = v.w;
-          }
-          const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
-          rs[kk] = make_float2(st.x, st.y);
-        }
+      for (int h = 0; h < QW / 4; ++h) {
+        const uint4 v = q4[h];
+        q[4 * h] = v.x; q[4 * h + 1] = v.y; q[4 * h + 2] = v.z; q[4 * h + 3] = v.w;
       }
+      const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
+      rsv = make_float2(st.x, 1.0f / st.y);      // (m_V, 1 / Z_V)
     };
     if (wave_on) {
-      load_q(ngr - 1);
+      load_q(dm.hpg - 1, qa, rsa);
       mq = tv.probe_m[(int64_t)lg * dm.W + uq];
-      zcq = tv.probe_ZC[(int64_t)lg * dm.W + uq];
+      zcq = 1.0f / tv.probe_ZC[(int64_t)lg * dm.W + uq];
     }
+    // representative position of the root and its RoPE row (wave 0, used at the end)
+    const int64_t pmid = round_half_even_mid((int)a0, (int)a0 + n);
+    float pcos = 0.f, psin = 0.f;
+    if (w == 0) { pcos = cosT[pmid * H2 + (lane % H2)]; psin = sinT[pmid * H2 + (lane % H2)]; }
     __syncthreads();                          // the previous unit is done with LDS
 
-    // ---- stage K (row-major) and V (transposed), zero past n ----
+    // ---- stage K (row-major) and undo RoPE on the way: per-thread sums of k°
+    // for the thread's 8-dim pair chunk, ||k°_t|| reduced across the CHP lanes
+    // of token t; V transposed; zero past n ----
+    {
+      float kacc[16];
+#pragma unroll
+      for (int h = 0; h < 16; ++h) kacc[h] = 0.f;
+      const int c = 8 * (tid % CHP);
+      for (int e = tid; e < rows16 * CHP; e += RT) {
+        const int t = e / CHP;
+        float k1[8], k2[8], o1[8], o2[8];
+        if constexpr (BF) {
+          uint4 u1 = make_uint4(0, 0, 0, 0), u2 = u1;
+          if (t < n) { u1 = *(const uint4*)(Kp + (int64_t)t * D + c); u2 = *(const uint4*)(Kp + (int64_t)t * D + c + H2); }
+          *(uint4*)(sK + t * Lay::LDK + c) = u1;
+          *(uint4*)(sK + t * Lay::LDK + c + H2) = u2;
+          const uint32_t w1[4] = {u1.x, u1.y, u1.z, u1.w}, w2[4] = {u2.x, u2.y, u2.z, u2.w};
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            k1[2 * h] = __uint_as_float(w1[h] << 16); k1[2 * h + 1] = __uint_as_float(w1[h] & 0xffff0000u);
+            k2[2 * h] = __uint_as_float(w2[h] << 16); k2[2 * h + 1] = __uint_as_float(w2[h] & 0xffff0000u);
+          }
+        } else {
+          float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a, cq = a, dq = a;
+          if (t < n) {
+            const float4* p1 = (const float4*)((const float*)Kp + (int64_t)t * D + c);
+            const float4* p2 = (const float4*)((const float*)Kp + (int64_t)t * D + c + H2);
+            a = p1[0]; b = p1[1]; cq = p2[0]; dq = p2[1];
+          }
+          float4* d1 = (float4*)((float*)sK + t * Lay::LDK + c);
+          float4* d2 = (float4*)((float*)sK + t * Lay::LDK + c + H2);
+          d1[0] = a; d1[1] = b; d2[0] = cq; d2[1] = dq;
+          k1[0] = a.x; k1[1] = a.y; k1[2] = a.z; k1[3] = a.w; k1[4] = b.x; k1[5] = b.y; k1[6] = b.z; k1[7] = b.w;
+          k2[0] = cq.x; k2[1] = cq.y; k2[2] = cq.z; k2[3] = cq.w; k2[4] = dq.x; k2[5] = dq.y; k2[6] = dq.z; k2[7] = dq.w;
+        }
+        float ss = 0.f;
+        if (t < n) {
+          const int64_t ta = a0 + t;
+          const float4 c0 = *(const float4*)(cosT + ta * H2 + c), c1 = *(const float4*)(cosT + ta * H2 + c + 4);
+          const float4 s0 = *(const float4*)(sinT + ta * H2 + c), s1 = *(const float4*)(sinT + ta * H2 + c + 4);
+          const float cs8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+          const float sn8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+          for (int h = 0; h < 8; ++h) {
+            o1[h] = k1[h] * cs8[h] + k2[h] * sn8[h];
+            o2[h] = k2[h] * cs8[h] - k1[h] * sn8[h];
+            kacc[h] += o1[h];
+            kacc[8 + h] += o2[h];
+            ss += o1[h] * o1[h] + o2[h] * o2[h];
+          }
+        }
+#pragma unroll
+        for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        if (t < n && c == 0) sKn[t] = sqrtf(ss);
+      }
+      // lanes l, l + CHP, ... of the wave hold the same chunk
+#pragma unroll
+      for (int o = CHP; o < 64; o <<= 1)
+#pragma unroll
+        for (int h = 0; h < 16; ++h) kacc[h] += __shfl_xor(kacc[h], o, 64);
+      if (lane < CHP) {
+#pragma unroll
+        for (int h = 0; h < 8; ++h) { sPk[w * D + c + h] = kacc[h]; sPk[w * D + c + H2 + h] = kacc[8 + h]; }
+      }
+    }
     if constexpr (BF) {
       constexpr int CPR = D / 8;              // 16-byte chunks per row
       // lane -> (token pair, chunk): 8 pairs x CPR chunks per group
       for (int e = tid; e < (rows16 / 2) * CPR; e += RT) {
         const int grp = e / (8 * CPR), rem = e % (8 * CPR);
         const int c = rem / 8, t = 2 * (8 * grp + rem % 8);
-        uint4 k0 = make_uint4(0, 0, 0, 0), k1 = k0, v0 = k0, v1 = k0;
-        if (t < n) { k0 = *(const uint4*)(Kp + (int64_t)t * D + 8 * c); v0 = *(const uint4*)(Vp + (int64_t)t * D + 8 * c); }
-        if (t + 1 < n) { k1 = *(const uint4*)(Kp + (int64_t)(t + 1) * D + 8 * c); v1 = *(const uint4*)(Vp + (int64_t)(t + 1) * D + 8 * c); }
-        *(uint4*)(sK + t * Lay::LDK + 8 * c) = k0;
-        *(uint4*)(sK + (t + 1) * Lay::LDK + 8 * c) = k1;
+        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = v0;
+        if (t < n) v0 = *(const uint4*)(Vp + (int64_t)t * D + 8 * c);
+        if (t + 1 < n) v1 = *(const uint4*)(Vp + (int64_t)(t + 1) * D + 8 * c);
         const uint32_t a[4] = {v0.x, v0.y, v0.z, v0.w}, b[4] = {v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
         for (int h = 0; h < 4; ++h) {
@@ -193,9 +252,8 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       for (int e = tid; e < rows16 * CPR; e += RT) {
         const int grp = e / (16 * CPR), rem = e % (16 * CPR);
         const int c = rem / 16, t = 16 * grp + rem % 16;
-        float4 kk = make_float4(0.f, 0.f, 0.f, 0.f), vv = kk;
-        if (t < n) { kk = *(const float4*)(Kp + (int64_t)t * D + 4 * c); vv = *(const float4*)(Vp + (int64_t)t * D + 4 * c); }
-        *(float4*)(sK + t * Lay::LDK + 4 * c) = kk;
+        float4 vv = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (t < n) vv = *(const float4*)(Vp + (int64_t)t * D + 4 * c);
         sVt[(4 * c + 0) * Lay::LDV + t] = vv.x;
         sVt[(4 * c + 1) * Lay::LDV + t] = vv.y;
         sVt[(4 * c + 2) * Lay::LDV + t] = vv.z;
@@ -205,16 +263,15 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
     for (int e = tid; e < RWV * NMAX; e += RT) { sRp[e] = 0.f; sAp[e] = 0.f; }
     __syncthreads();
 
-    // ---- logits, relevance, probe exponentials and M^T = V^T E^T ----
+    // ---- logits, relevance, probe exponentials and M^T = V^T E^T: heads one
+    // at a time with the next head's Q in flight, the probe head (slot 0) last ----
     f32x4 Macc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) Macc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float Zl = 0.f;
     if (wave_on) {
-      // head groups in reverse so that the probe head (slot 0) is in registers at the end
-      for (int gr = ngr - 1; gr >= 0; --gr) {
-        const int k0 = gr * HG;
-        if (gr != ngr - 1) load_q(gr);
+      for (int k = dm.hpg - 1; k >= 0; --k) {
+        if (k > 0) load_q(k - 1, qb, rsb);
         for (int tb = 0; tb < n_tt; ++tb) {
           const int t0 = 16 * tb;
           uint32_t kreg[QW];
@@ -226,36 +283,31 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
               kreg[4 * h] = v.x; kreg[4 * h + 1] = v.y; kreg[4 * h + 2] = v.z; kreg[4 * h + 3] = v.w;
             }
           }
-          float Rp[4] = {0.f, 0.f, 0.f, 0.f}, ev[4] = {0.f, 0.f, 0.f, 0.f};
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          if constexpr (BF) {
 #pragma unroll
-          for (int kk = 0; kk < HG; ++kk) {
-            if (k0 + kk < dm.hpg) {
-              f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-              if constexpr (BF) {
+            for (int s = 0; s < QE / 4; ++s)
+              acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qa[2 * s], qa[2 * s + 1]), acc);
+          } else {
 #pragma unroll
-                for (int s = 0; s < QE / 4; ++s)
-                  acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]),
-                                           pk4(qreg[kk][2 * s], qreg[kk][2 * s + 1]), acc);
-              } else {
+            for (int s = 0; s < QE; ++s)
+              acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qa[s]), acc);
+          }
+          // lane holds tokens t0 + 4 g4 + r of the lane's query row
+          float Rp[4], ev[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int s = 0; s < QE; ++s)
-                  acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qreg[kk][s]), acc);
-              }
-              // lane holds tokens t0 + 4 g4 + r of the lane's query row
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                if (uok && t0 + 4 * g4 + r < n) {
-                  const float x = acc[r] * scale;
-                  Rp[r] += expf(x - rs[kk].x) / rs[kk].y;
-                  if (gr == 0 && kk == 0) ev[r] = expf(x - mq);
-                }
-              }
+          for (int r = 0; r < 4; ++r) {
+            Rp[r] = 0.f;
+            if (uok && t0 + 4 * g4 + r < n) {
+              const float x = acc[r] * scale;
+              Rp[r] = fexp(x - rsa.x) * rsa.y;
+              if (k == 0) ev[r] = fexp(x - mq);
             }
           }
-          if (gr == 0) {
+          if (k == 0) {
             float ap[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) { ap[r] = ev[r] / zcq; Zl += ev[r]; }
+            for (int r = 0; r < 4; ++r) { ap[r] = ev[r] * zcq; Zl += ev[r]; }
             if constexpr (BF) {
               s16x4 eh, em, el;
               split3(ev, eh, em, el);
@@ -278,16 +330,17 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
               }
             }
 #pragma unroll
-            for (int o = 1; o < 16; o <<= 1)
-#pragma unroll
-              for (int r = 0; r < 4; ++r) ap[r] += __shfl_xor(ap[r], o, 64);
+            for (int r = 0; r < 4; ++r) ap[r] = row_sum16(ap[r]);
             if (i16 < 4) sAp[w * NMAX + t0 + 4 * g4 + i16] = pick4(ap, i16);
           }
 #pragma unroll
-          for (int o = 1; o < 16; o <<= 1)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) Rp[r] += __shfl_xor(Rp[r], o, 64);
+          for (int r = 0; r < 4; ++r) Rp[r] = row_sum16(Rp[r]);
           if (i16 < 4) sRp[w * NMAX + t0 + 4 * g4 + i16] += pick4(Rp, i16);
+        }
+        if (k > 0) {
+#pragma unroll
+          for (int h = 0; h < QW; ++h) qa[h] = qb[h];
+          rsa = rsb;
         }
       }
     }
@@ -305,41 +358,11 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       sA[t] = A;
       tv.tok_R[(int64_t)lg * dm.N_c + a0 + t] = R;
       tv.tok_A[(int64_t)lg * dm.N_c + a0 + t] = A;
-      float kn = 0.f;
-      for (int c = 0; c < D; ++c) {
-        const float x = ldf(sK, t * Lay::LDK + c);
-        kn += x * x;
-      }
-      sKn[t] = sqrtf(kn);
     }
     __syncthreads();
 
-    // ---- per-dimension sums over the unit: k° (RoPE undone at t), R v and v ----
+    // ---- per-dimension sums of R v and v over the unit ----
     {
-      const int i = tid % H2, q = tid / H2;
-      float s0 = 0.f, s1 = 0.f;
-      for (int tb = q; tb < n; tb += 4 * Lay::NPK) {
-        float c8[4], s8[4], a8[4], b8[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int t = tb + v * Lay::NPK;
-          const int tt = t < n ? t : n - 1;
-          const int64_t ta = a0 + tt;
-          c8[v] = cosT[ta * H2 + i];
-          s8[v] = sinT[ta * H2 + i];
-          a8[v] = ldf(sK, tt * Lay::LDK + i);
-          b8[v] = ldf(sK, tt * Lay::LDK + i + H2);
-        }
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          if (tb + v * Lay::NPK < n) {
-            s0 += a8[v] * c8[v] + b8[v] * s8[v];
-            s1 += b8[v] * c8[v] - a8[v] * s8[v];
-          }
-        }
-      }
-      sPk[q * D + i] = s0;
-      sPk[q * D + i + H2] = s1;
       const int d = tid % D, q2 = tid / D;
       float sv = 0.f, srv = 0.f;
       for (int t = q2; t < n; t += Lay::NPV) {
@@ -375,16 +398,12 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       ss = wave_sum(ss);
       const float coh = sqrtf(ss) / (skn * inv + dm.eps);
       const float me = fminf(fmaxf((float)n * coh * coh, 1.0f), (float)n);
-      const int64_t p = round_half_even_mid((int)a0, (int)a0 + n);
       if constexpr (D == 128) {               // lane holds the pair (lane, lane + 64)
-        const float c = cosT[p * H2 + lane], sn = sinT[p * H2 + lane];
-        sKt[lane] = kb[0] * c - kb[1] * sn;
-        sKt[lane + H2] = kb[1] * c + kb[0] * sn;
+        sKt[lane] = kb[0] * pcos - kb[1] * psin;
+        sKt[lane + H2] = kb[1] * pcos + kb[0] * psin;
       } else {                                // D == 64: partner dim lane ^ 32
         const float other = __shfl_xor(kb[0], 32, 64);
-        const int i = lane & 31;
-        const float c = cosT[p * H2 + i], sn = sinT[p * H2 + i];
-        sKt[lane] = lane < 32 ? kb[0] * c - other * sn : kb[0] * c + other * sn;
+        sKt[lane] = lane < 32 ? kb[0] * pcos - other * psin : kb[0] * pcos + other * psin;
       }
       const float beta = dm.beta_frac * sr * inv;
       const float den = sr + (float)n * beta + dm.eps;
@@ -409,13 +428,13 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
 #pragma unroll
         for (int e = 0; e < QE; ++e) {
           float qv;
-          if constexpr (BF) qv = __uint_as_float(e & 1 ? (qreg[0][e >> 1] & 0xffff0000u) : (qreg[0][e >> 1] << 16));
-          else qv = __uint_as_float(qreg[0][e]);
+          if constexpr (BF) qv = __uint_as_float(e & 1 ? (qa[e >> 1] & 0xffff0000u) : (qa[e >> 1] << 16));
+          else qv = __uint_as_float(qa[e]);
           qk += qv * sKt[QE * g4 + e];
         }
         qk += __shfl_xor(qk, 16, 64);
         qk += __shfl_xor(qk, 32, 64);
-        const float z = me * expf(qk * scale - mq);
+        const float z = me * fexp(qk * scale - mq);
         float Z = Zl;
         Z += __shfl_xor(Z, 16, 64);
         Z += __shfl_xor(Z, 32, 64);
@@ -438,7 +457,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
         s2 += __shfl_xor(s2, 32, 64);
         const float dz = Z - z;
         const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
-        con = (uok && g4 == 0) ? (Z / zcq) * Dq : 0.f;
+        con = (uok && g4 == 0) ? (Z * zcq) * Dq : 0.f;
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) con += __shfl_xor(con, o, 64);
       }

@@ -533,9 +533,9 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
       }
       load(i + 64, sv[q]);                   // the same lane's end four steps later
       dp_reduce16(bv, ba);
-      __syncthreads();                       // every end of this step has read its F
+      lds_barrier();                         // every end of this step has read its F
       if (sub == 0 && i <= N) { Fr[i & 255] = bv; Poff[i] = ba >= 0 ? (uint8_t)(i - ba) : 0; }
-      __syncthreads();
+      lds_barrier();                         // (Poff is only read after the loop's final full barrier)
     }
   }
   // terminal relaxation of the last slot's minimum length
