@@ -438,6 +438,7 @@ __device__ __forceinline__ void dp_better32(double& bv, int& ba, double v, int a
   if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
 }
 // one DPP step of the (value, smallest start) maximum within 16-lane rows
+// (an absent candidate is (-inf, INT_MAX) and never wins)
 template <int CTRL>
 __device__ __forceinline__ void dp_step(double& bv, int& ba) {
   const long long b = __double_as_longlong(bv);
@@ -445,7 +446,9 @@ __device__ __forceinline__ void dp_step(double& bv, int& ba) {
   const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xf, 0xf, false);
   const int a2 = __builtin_amdgcn_update_dpp(0, ba, CTRL, 0xf, 0xf, false);
   const double v2 = __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
-  if (a2 >= 0) dp_better32(bv, ba, v2, a2);
+  const bool better = v2 > bv || (v2 == bv && a2 < ba);
+  bv = better ? v2 : bv;
+  ba = better ? a2 : ba;
 }
 // every lane of a 16-lane row ends with the row's best: lanes ^1, ^2 (quad
 // permutes), then rotations by 4 and 8 within the row
@@ -500,15 +503,12 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
   __syncthreads();
   if (tid == 0) { Fr[0] = 0.0; Poff[0] = 0; }
   __syncthreads();
+  // unconditional loads (row clamped to N) keep the load counter exact
   auto load = [&](int64_t i, double* sv) {
-    if (i <= N) {
-      const double2* p = (const double2*)(ws.S + (i - 1) * BAND + sub * 8);
+    const int64_t ic = i <= N ? i : N;
+    const double2* p = (const double2*)(ws.S + (ic - 1) * BAND + sub * 8);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) { const double2 v = p[k]; sv[2 * k] = v.x; sv[2 * k + 1] = v.y; }
-    } else {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) sv[k] = -INFINITY;
-    }
+    for (int k = 0; k < 4; ++k) { const double2 v = p[k]; sv[2 * k] = v.x; sv[2 * k + 1] = v.y; }
   };
   // scores of 4 steps in flight (static register indices: the step loop is unrolled by 4)
   double sv[4][8];
@@ -520,21 +520,35 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
       const int64_t i0 = i00 + 16 * q;
       if (i0 > N) break;
       const int64_t i = i0 + 4 * wave + st;
-      double bv = -INFINITY;
-      int ba = -1;
+      // all F reads first, then a branch-free (value, smallest start) maximum
+      double Fa[8];
+      int av[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int len = dm.n_min + sub + 16 * k;
         const int64_t a = i - len;
-        if (i <= N && len <= dm.n_max && a >= 0) {
-          const double Fa = Fr[a & 255];
-          if (Fa != -INFINITY) dp_better32(bv, ba, Fa + sv[q][k], (int)a);
-        }
+        const bool ok = i <= N && len <= dm.n_max && a >= 0;
+        av[k] = ok ? (int)a : 0x7fffffff;
+        Fa[k] = Fr[ok ? (int)(a & 255) : 0];
+      }
+      double bv = -INFINITY;
+      int ba = 0x7fffffff;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const bool ok = av[k] != 0x7fffffff && Fa[k] != -INFINITY;
+        const double v = ok ? Fa[k] + sv[q][k] : -INFINITY;
+        const int a = ok ? av[k] : 0x7fffffff;
+        const bool better = v > bv || (v == bv && a < ba);
+        bv = better ? v : bv;
+        ba = better ? a : ba;
       }
       load(i + 64, sv[q]);                   // the same lane's end four steps later
       dp_reduce16(bv, ba);
       lds_barrier();                         // every end of this step has read its F
-      if (sub == 0 && i <= N) { Fr[i & 255] = bv; Poff[i] = ba >= 0 ? (uint8_t)(i - ba) : 0; }
+      if (sub == 0 && i <= N) {
+        Fr[i & 255] = bv;
+        Poff[i] = ba != 0x7fffffff ? (uint8_t)(i - ba) : 0;
+      }
       lds_barrier();                         // (Poff is only read after the loop's final full barrier)
     }
   }
