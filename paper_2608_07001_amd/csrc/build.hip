@@ -283,23 +283,30 @@ __device__ void proto_attention(Ref<T, D>& U, const Dims& dm, int nl, int nr, co
   }
 }
 
-// e_{q,t} for the 16 tokens of block blk (unit-local) and the lane's probe:
-// transposed logits, lane holds tokens 16 blk + 4 g4 + r.
+// the lane's key quarter row of block blk (unit-local token 16 blk + i16,
+// clamped to the unit)
 template <typename T, int D, int QW>
-__device__ __forceinline__ void block_e(const T* __restrict__ Kp, int n, int blk, const uint32_t* qreg, float mq,
-                                        bool pok, float scale, float* ev) {
-  constexpr bool BF = sizeof(T) == 2;
+__device__ __forceinline__ void block_k(const T* __restrict__ Kp, int n, int blk, uint32_t* kreg) {
   constexpr int QE = D / 4;
   const int lane = threadIdx.x & 63, i16 = lane & 15, g4 = lane >> 4;
   int tr = 16 * blk + i16;
   tr = tr < n ? tr : n - 1;
   const uint4* k4 = (const uint4*)(Kp + (int64_t)tr * D + QE * g4);
-  uint32_t kreg[QW];
 #pragma unroll
   for (int h = 0; h < QW / 4; ++h) {
     const uint4 v = k4[h];
     kreg[4 * h] = v.x; kreg[4 * h + 1] = v.y; kreg[4 * h + 2] = v.z; kreg[4 * h + 3] = v.w;
   }
+}
+
+// e_{q,t} for the 16 tokens of block blk and the lane's probe: transposed
+// logits, lane holds tokens 16 blk + 4 g4 + r.
+template <typename T, int D, int QW>
+__device__ __forceinline__ void block_e(const uint32_t* kreg, int n, int blk, const uint32_t* qreg, float mq,
+                                        bool pok, float scale, float* ev) {
+  constexpr bool BF = sizeof(T) == 2;
+  constexpr int QE = D / 4;
+  const int lane = threadIdx.x & 63, g4 = lane >> 4;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   if constexpr (BF) {
 #pragma unroll
@@ -339,7 +346,10 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
   u32x2 eh = {0u, 0u}, em = {0u, 0u}, el = {0u, 0u};   // bf16 parts of the block's e
   u32x2 vop[BF ? DT : 1];                             // V^T operands of the block (bf16)
   float4 vf[BF ? 1 : DT];                             // ... (fp32)
+  uint32_t kpre[QW];                                  // key quarter rows of the next block of the sweep
   int eblk = -1;
+  const int lastblk = (n - 1) >> 4;
+  block_k<T, D, QW>(Kp, n, prefix ? (a >> 4) : ((b - 1) >> 4), kpre);   // the sweep's first block
   int cur = prefix ? a : b;
   for (int k = 0; k < nx; ++k) {
     const int c = prefix ? k : nx - 1 - k;
@@ -350,7 +360,15 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
       const int lo = prefix ? cur : max(x, blk << 4);
       const int hi = prefix ? min(x, (blk + 1) << 4) : cur;
       if (blk != eblk) {
-        block_e<T, D, QW>(Kp, n, blk, qreg, mq, pok, scale, ev);
+        // sweeps visit consecutive blocks: this one was prefetched, the next one
+        // goes in flight now (straight-line, so only the older loads are waited for)
+        uint32_t kreg[QW];
+#pragma unroll
+        for (int h = 0; h < QW; ++h) kreg[h] = kpre[h];
+        int nb = prefix ? blk + 1 : blk - 1;
+        nb = nb < 0 ? 0 : (nb > lastblk ? lastblk : nb);
+        block_k<T, D, QW>(Kp, n, nb, kpre);
+        block_e<T, D, QW>(kreg, n, blk, qreg, mq, pok, scale, ev);
         if constexpr (BF) {
           split3x4(ev, eh, em, el);
 #pragma unroll
@@ -477,6 +495,7 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
     const T* Kp = K + ((int64_t)lg * dm.T + a0) * D;
     const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
     const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
+    const float w = tv.omega[lg];
 
     // ---- node table; refine only nodes whose creating op reaches theta ----
     {
@@ -598,8 +617,6 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
     __syncthreads();
     float mq = 0.f, zc = 1.f;
     if (16 * pt + i16 < dm.W) { mq = U.Mq[16 * pt + i16]; zc = U.Zc[16 * pt + i16]; }
-    const float w = tv.omega[lg];
-
     // ---- top-down refinement in BFS order ----
     for (int head = 0;; ++head) {
       __syncthreads();
