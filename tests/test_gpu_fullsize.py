@@ -1,0 +1,147 @@
+"""Parity at the benchmarked size: the 8B-shaped 128K-token cache at 128x
+(L=32, G=8, H=32, d=128, W=64, bf16), run exactly as bench.py runs it
+(segmentation, budget-pruned tree build, score, select, pack).
+
+The oracle cannot run the whole case, so:
+  * sampled outputs are recomputed one by one: the token values R^tok and
+    probe masses of two (layer, KV head) pairs over the full context, the
+    trees of sampled slots of those pairs (from the GPU slots and curvature),
+    and the stabilised curvature on a sampled window of positions;
+  * the rest is checked through properties that hold at any size: the pruned
+    build selects and packs exactly what the complete build does, the budget
+    is spent exactly, and every (layer, KV head) row of the packed cache is a
+    valid frontier (positions strictly increasing, recent window kept).
+Tolerances are those of the small parity cases."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import gracekv_oracle as O
+from paper_2608_07001_amd import gracekv as gk
+from synth.workloads import CONFIGS, make_case
+
+import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+SH = CONFIGS["8b-128k"]
+RTOL_R = 1e-4
+RTOL_D, ATOL_D = 2e-3, 1e-7
+TAU = 2e-4
+LG_SAMPLES = [(0, 0), (17, 5)]
+
+
+def _run(case, cfg, slots=None, n_slots=None, kappa=None):
+    buf = gk.allocate(cfg)
+    gk.compress(buf, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], case["hidden"],
+                case["surprisal"], case["omega_raw"], kappa=kappa, slot_starts=slots, n_slots=n_slots)
+    torch.cuda.synchronize()
+    gk.check(cfg, buf.trees)
+    return buf
+
+
+@pytest.fixture(scope="module")
+def runs():
+    case = make_case(SH, 0, device="cuda")
+    pruned = _run(case, H.make_cfg(SH, flags=gk.FLAG_PRUNE))
+    full = _run(case, H.make_cfg(SH), slots=pruned.slot_starts, n_slots=pruned.n_slots, kappa=pruned.kappa)
+    return case, pruned, full
+
+
+def _unit_view(arr, p, lg, j, a0, n):
+    """Host copies of one unit's node slots and unit fields, re-based to 0."""
+    base = lg * 2 * p.N_c + 2 * a0
+    u = lg * p.J_cap + j
+    out = {k: arr[k][base:base + 2 * n].cpu() for k in
+           ("node_a", "node_n", "node_child", "node_parent", "node_nch", "node_kind", "node_cut", "node_D",
+            "node_R", "sp_exec")}
+    out["unit_nn"] = arr["unit_nn"][u:u + 1].cpu()
+    out["unit_Ddrop"] = arr["unit_Ddrop"][u:u + 1].cpu()
+    return out
+
+
+def test_pruned_equals_complete_build_at_full_size(runs):
+    case, pr, fu = runs
+    assert int(pr.b_used.item()) == int(fu.b_used.item())
+    assert torch.equal(pr.offsets, fu.offsets)
+    n = int(pr.offsets[-1].item())
+    for k in ("pos_out", "logm_out", "K_out", "V_out"):
+        assert torch.equal(getattr(pr, k)[:n], getattr(fu, k)[:n]), k
+    J = int(pr.n_slots.item())
+    ta, tb = gk.tree_arrays(pr.plan, pr.trees), gk.tree_arrays(fu.plan, fu.trees)
+    adds_p = ta["add_exec"].view(-1, pr.plan.J_cap)[:, :J]
+    adds_f = tb["add_exec"].view(-1, fu.plan.J_cap)[:, :J]
+    assert torch.equal(adds_p, adds_f)
+    nodes_p = int(ta["unit_nn"].view(-1, pr.plan.J_cap)[:, :J].sum())
+    nodes_f = int(tb["unit_nn"].view(-1, fu.plan.J_cap)[:, :J].sum())
+    print(f"full size: J {J} nodes pruned {nodes_p} complete {nodes_f} b_used {int(pr.b_used)}")
+
+
+def test_budget_and_frontier_properties_at_full_size(runs):
+    case, pr, fu = runs
+    p = pr.plan
+    LG = SH.L * SH.G
+    b_used = int(pr.b_used.item())
+    offs = pr.offsets.cpu().numpy()
+    assert b_used <= p.B_free and p.B_free - b_used <= 1     # the auction leaves at most one unit unspent
+    assert offs[0] == 0 and offs[-1] == p.B_total - (p.B_free - b_used)
+    pos = pr.pos_out[:offs[-1]].cpu().numpy()
+    logm = pr.logm_out[:offs[-1]].cpu().numpy()
+    r = p.r
+    for lg in range(LG):
+        row = pos[offs[lg]:offs[lg + 1]]
+        assert np.all(np.diff(row) > 0), lg                  # strictly increasing representative positions
+        assert np.array_equal(row[-r:], np.arange(p.N_c, SH.N_ctx)), lg
+        assert row[0] >= 0 and row[-r - 1] < p.N_c
+    assert np.all(logm >= 0.0) and np.all(np.isfinite(logm))
+
+
+def test_sampled_token_values_and_trees_at_full_size(runs):
+    case, pr, fu = runs
+    p = fu.plan
+    hpg = SH.H // SH.G
+    # the complete build reused the pruned run's segmentation (its own buffers are not filled)
+    J = int(pr.n_slots.item())
+    slots = pr.slot_starts[:J + 1].cpu().numpy().astype(np.int64)
+    slots[J] = p.N_c
+    kappa = pr.kappa.cpu().numpy().astype(np.float64)
+    arr = gk.tree_arrays(p, fu.trees)
+    tokR = fu.trees[p.off_tok_R:p.off_tok_R + SH.L * SH.G * p.N_c * 4].view(torch.float32)
+    tokA = fu.trees[p.off_tok_A:p.off_tok_A + SH.L * SH.G * p.N_c * 4].view(torch.float32)
+    cos, sin = H.np32(case["rope_cos"]), H.np32(case["rope_sin"])
+    rng = np.random.default_rng(5)
+    st = H.TreeStats()
+    worstR = worstA = 0.0
+    for (l, g) in LG_SAMPLES:
+        lg = l * SH.G + g
+        ctx = O.lg_context(H.np32(case["K"][l, g]), H.np32(case["V"][l, g]),
+                           H.np32(case["Q"][l, g * hpg:(g + 1) * hpg]), cos, sin, kappa, SH.N_ctx, p.N_c)
+        gR = tokR[lg * p.N_c:(lg + 1) * p.N_c].cpu().numpy()
+        gA = tokA[lg * p.N_c:(lg + 1) * p.N_c].cpu().numpy()
+        A = (ctx.E / ctx.ZC[:, None]).mean(axis=0)
+        worstR = max(worstR, float((np.abs(gR - ctx.R) / np.maximum(ctx.R, 1e-30)).max()))
+        worstA = max(worstA, float((np.abs(gA - A) / np.maximum(A, 1e-30)).max()))
+        # sampled slots: short, long, first, last and random ones
+        lens = np.diff(slots)
+        pick = {0, J - 1, int(np.argmax(lens)), int(np.argmin(lens))} | set(rng.choice(J, 8, replace=False).tolist())
+        for j in sorted(pick):
+            a0, b0 = int(slots[j]), int(slots[j + 1])
+            nodes = O.build_tree(ctx, a0, b0)
+            H.compare_unit(nodes, _unit_view(arr, p, lg, j, a0, b0 - a0), 0, 0, st, RTOL_D, ATOL_D, RTOL_R, TAU)
+    print(f"full size sampled: R^tok maxrel {worstR:.3e} A maxrel {worstA:.3e}; nodes {st.nodes} "
+          f"near-ties {st.near_ties} maxrelD {st.max_rel_D:.3e} maxabsD {st.max_abs_D:.3e}")
+    assert worstR < RTOL_R and worstA < RTOL_R
+    assert not st.mismatches, st.mismatches[:10]
+    assert st.max_rel_Ddrop < RTOL_R
+
+
+def test_sampled_curvature_window_at_full_size(runs):
+    case, pr, fu = runs
+    s, e = 70000, 72048                         # positions compared; 16 rows of context on each side
+    hid = case["hidden"][:, s - 16:e + 16].float().cpu().numpy()
+    hbars = [O.normalize_hidden(hid[k]) for k in range(hid.shape[0])]
+    kap = O.stabilized_curvature(hbars)[16:-16]
+    got = pr.kappa[s:e].cpu().numpy()
+    err = float(np.abs(got - kap).max())
+    print(f"full size curvature window [{s}, {e}): max abs err {err:.3e}")
+    assert err < 1e-4

@@ -231,3 +231,60 @@ def test_pruned_build_gives_the_same_result_bf16(x):
     assert full["slots"] == pr["slots"]
     assert H.gpu_selected(full) == H.gpu_selected(pr)
     _same_cache(full, pr)
+
+
+# ---- edge cases: masked probe tiles, one or eight query heads per KV head,
+# slots of 1, 2 and 3 tokens next to the longest, an empty free budget ----
+EDGE = [
+    ("w8-hpg1", dict(L=2, G=2, H=2, d=64, N_ctx=700, W=8, dtype="f32", x=6.0, n_segments=5)),
+    ("w24-hpg8", dict(L=1, G=2, H=16, d=128, N_ctx=900, W=24, dtype="bf16", x=5.0, n_segments=6)),
+    ("w64-hpg4-d64", dict(L=2, G=1, H=4, d=64, N_ctx=800, W=64, dtype="bf16", x=3.0, n_segments=6)),
+]
+
+
+@pytest.mark.parametrize("name,kw", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_shapes_trees_and_selection(name, kw):
+    sh = small_shape(name, **kw)
+    case = make_case(sh, 11, with_hidden=False)
+    kappa = make_kappa(sh, 11)
+    N_c = O.budget(sh.L, sh.G, sh.N_ctx, sh.x).N_c
+    slots = _partition(N_c, lens=(1, 2, 3, 128, 17, 31, 64, 2, 90))
+    g = H.gpu_run(H.to_dev(case), slots=slots, kappa=kappa)
+    o = H.oracle_run(case, slots=slots, kappa=kappa)
+    tokR = g["tok_R"].numpy().reshape(sh.L * sh.G, N_c)
+    tokA = g["tok_A"].numpy().reshape(sh.L * sh.G, N_c)
+    worstR = max(float((np.abs(tokR[l * sh.G + gg] - c.R) / np.maximum(c.R, 1e-30)).max())
+                 for (l, gg), c in o.ctx.items())
+    worstA = max(float((np.abs(tokA[l * sh.G + gg] - _probe_mass(c)) / np.maximum(_probe_mass(c), 1e-30)).max())
+                 for (l, gg), c in o.ctx.items())
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    ga, gs = H.gpu_selected(g)
+    oa, os_ = H.oracle_selected(o, sh.G)
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    print(f"{name}: R^tok maxrel {worstR:.3e} A maxrel {worstA:.3e}; nodes {st.nodes} near-ties {st.near_ties} "
+          f"maxrelD {st.max_rel_D:.3e}; b_used {g['b_used']} oracle {spent}")
+    assert worstR < RTOL_R and worstA < RTOL_R
+    assert not st.mismatches, st.mismatches[:10]
+    assert g["b_used"] == spent
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
+    offs = g["offsets"].numpy()
+    assert offs[-1] == o.counts.sum()
+    for (l, gg), pk in o.packed.items():
+        lg = l * sh.G + gg
+        assert np.array_equal(g["pos_out"].numpy()[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+
+
+def test_budget_with_nothing_free():
+    # x so large that the budget holds only the recent windows: nothing is selected,
+    # the cache is the recent windows alone
+    sh = small_shape("nofree", L=1, G=2, H=4, d=64, N_ctx=600, W=16, x=18.75, n_segments=4)
+    bud = O.budget(sh.L, sh.G, sh.N_ctx, sh.x)
+    assert bud.B_free == 0
+    case = make_case(sh, 4, with_hidden=True)
+    g = H.gpu_run(H.to_dev(case))
+    assert g["b_used"] == 0
+    offs = g["offsets"].numpy()
+    assert offs[-1] == bud.B_total
+    for lg in range(sh.L * sh.G):
+        assert np.array_equal(g["pos_out"].numpy()[offs[lg]:offs[lg + 1]], np.arange(bud.N_c, sh.N_ctx))
