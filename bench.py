@@ -30,7 +30,39 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prune", action="store_true", help="build every tree completely")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed steps, one device-to-device copy of this size (counter calibration)")
     return ap.parse_args()
+
+
+def source_digest():
+    """sha256 over the kernel sources and the C header: a recorded traffic
+    figure is reported only while the kernels it was measured on are unchanged."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_07001_amd", "csrc")
+    files = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    for f in files + ["../../include/gracekv.h"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """HBM bytes per gracekv_build_trees call from the committed counter summary
+    of this workload, if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None, None
+    text = open(path).read()
+    try:
+        blob = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (IndexError, ValueError):
+        return None, None
+    if blob.get("source_digest") != source_digest():
+        return None, blob
+    return blob.get("build_trees_bytes_per_call"), blob
 
 
 def algorithmic_bytes(sh, plan, b):
@@ -147,6 +179,14 @@ def main():
     stage_ms = {n: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)) / args.steps
                 for i, n in enumerate(names)}
     ms = sum(evs[s][0].elapsed_time(evs[s][5]) for s in range(args.steps)) / args.steps
+    if args.copy_probe_mib > 0:                    # untimed: a plain copy of known size for the counters
+        a = torch.ones(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+        b2 = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b2.copy_(a)
+        torch.cuda.synchronize()
+        del a, b2
+    traffic, _ = recorded_traffic(sh.name)
     tokens = sh.L * sh.G * sh.N_ctx
     b = 2 if sh.dtype == "bf16" else 4
     ab = algorithmic_bytes(sh, p, b)
@@ -167,9 +207,9 @@ def main():
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": stage_ms,
         "wall_s": wall,
-        "roofline": {"kernel": "gracekv_build_trees (k_rowstats + k_root + k_build)", "bound": "hbm",
+        "roofline": {"kernel": "gracekv_build_trees (k_rowstats, k_root, k_work_mark, k_refine)", "bound": "hbm",
                      "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": build_gbs / HBM_PEAK_GBS, "traffic": None},
+                     "frac": build_gbs / HBM_PEAK_GBS, "traffic": traffic},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)

@@ -150,6 +150,7 @@ __global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState
       int c;
       if (i < node_cap) {
         c = tv.sp_cost[i];
+        if (c == 0) continue;                 // empty slot or leaf: its key is never read
         E = tv.sp_E[i];
       } else {
         const int64_t u = i - node_cap;
@@ -157,7 +158,6 @@ __global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState
         c = 1;
         E = tv.add_E[u];
       }
-      if (c == 0) continue;
       if (pass > 0 && (E >> (shift + 8)) != (pre >> (shift + 8))) continue;
       atomicAdd(&h[(E >> shift) & 255u], (unsigned)c);
     }
@@ -202,9 +202,8 @@ __global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const Se
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < node_cap + unit_cap; i += (int64_t)gridDim.x * 256) {
     if (i < node_cap) {
       const int c = tv.sp_cost[i];
-      const uint64_t E = tv.sp_E[i];
       uint8_t x = 0;
-      if (c > 0) x = (mode == SEL_ALL) || (mode == SEL_SELECT && E > theta);
+      if (c > 0) x = (mode == SEL_ALL) || (mode == SEL_SELECT && tv.sp_E[i] > theta);
       tv.sp_exec[i] = x;
     } else {
       const int64_t u = i - node_cap;
