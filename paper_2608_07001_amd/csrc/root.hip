@@ -38,8 +38,9 @@ struct RootLds {
   static constexpr int LDV = BF ? NMAX + 8 : NMAX + 4;  // V^T rows [D][LDV]
   static constexpr int NPK = RWV;                       // per-wave partial sums of k°
   static constexpr int NPV = RT / D;                    // token phases of the v sums
-  static constexpr int oK = 0;
-  static constexpr int oVt = oK + NMAX * LDK * (int)sizeof(T);
+  // V^T first and the small arrays next keep every fixed offset within the 16-bit
+  // immediate of the LDS instructions; K rows are addressed per tile anyway
+  static constexpr int oVt = 0;
   static constexpr int oRp = oVt + D * LDV * (int)sizeof(T);   // [RWV][NMAX] relevance partials
   static constexpr int oAp = oRp + RWV * NMAX * 4;              // [RWV][NMAX] probe-mass partials
   static constexpr int oR = oAp + RWV * NMAX * 4;               // [NMAX] R_t
@@ -51,7 +52,8 @@ struct RootLds {
   static constexpr int oKt = oPs + NPV * D * 4;                 // [D] prototype key k~
   static constexpr int oVv = oKt + D * 4;                       // [D] prototype value v~
   static constexpr int oRed = oVv + D * 4;                      // [16] unit scalars
-  static constexpr int bytes = oRed + 16 * 4;
+  static constexpr int oK = oRed + 16 * 4;                      // K rows [NMAX][LDK]
+  static constexpr int bytes = oK + NMAX * LDK * (int)sizeof(T);
 };
 
 int root_lds_bytes(const Dims& dm) {
@@ -81,7 +83,15 @@ __device__ __forceinline__ void split3(const float* e, s16x4& hi, s16x4& mid, s1
   }
 }
 
-template <typename T, int D>
+// One 16-byte chunk of the staging of a unit: a K pair chunk (dims c .. c + 7
+// and c + H2 .. c + H2 + 7 of token t) with its RoPE rows, and two V chunks
+// (dims 8 cv .. 8 cv + 7 of tokens tv and tv + 1).  bf16 only.
+struct StageChunk {
+  uint4 k1, k2, v0, v1;
+  float4 c0, c1, s0, s1;
+};
+
+template <typename T, int D, bool MP>
 __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K, const T* __restrict__ V,
                                                 const T* __restrict__ Q, const float* __restrict__ cosT,
                                                 const float* __restrict__ sinT, const int32_t* __restrict__ slot_starts,
@@ -92,6 +102,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   constexpr int DT = D / 16;                 // 16-wide value tiles of M^T
   constexpr int QE = D / 4;                  // elements of a lane's quarter row
   constexpr int QW = BF ? QE / 2 : QE;       // ... in 32-bit words
+  constexpr int HG = 4;                      // head slots whose Q rows are held at once
   extern __shared__ __align__(16) char smem[];
   T* sK = (T*)(smem + Lay::oK);
   T* sVt = (T*)(smem + Lay::oVt);
@@ -107,7 +118,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   float* sVv = (float*)(smem + Lay::oVv);
   float* sRed = (float*)(smem + Lay::oRed);
 
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+  const int tid0 = threadIdx.x, w = tid0 >> 6, g4o = (tid0 >> 4) & 3;
   const int J = *n_slots;
   if (J < 1 || J > dm.J_cap) {                // malformed partition: nothing to build
     if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(tv.status, 2);
@@ -118,18 +129,46 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   const int64_t ub = (int64_t)blockIdx.x * per;
   const int64_t ue = ub + per < total ? ub + per : total;
   const float scale = 1.0f / sqrtf((float)D);
-  const int u = 16 * w + i16;                 // the lane's window query
+  const int u = 16 * w + (tid0 & 15);         // the lane's window query
   const bool uok = u < dm.W;
   const int uq = uok ? u : 0;
   const int hp = uq % dm.hpg;                 // query head of probe u
   const bool wave_on = 16 * w < dm.W;
+  // passes over the unit, HG head slots each (MP: more than one, so Q is reloaded per pass)
+  const int npass = MP ? (dm.hpg + HG - 1) / HG : 1;
+  const int klast = HG * (npass - 1);         // first slot of the last pass (run first)
 
   constexpr int CHP = H2 / 8;                // 8-dim pair chunks per token in the k° staging
-  uint32_t qa[QW], qb[QW];                    // Q quarter rows: current head, next head
-  float2 rsa = make_float2(0.f, 1.f), rsb = rsa;   // (m_V, 1 / Z_V) of the lane's rows
+  // Q quarter rows of head slots k0 .. k0 + HG - 1 (slot k = head (hp + k) mod |H(g)|) and
+  // their row statistics (m_V, 1 / Z_V); a slot past |H(g)| gets weight 0.  With one pass
+  // they stay valid for every unit of the same (l, g).
+  uint32_t qr[HG][QW];
+  float2 rs[HG];
   float mq = 0.f, zcq = 1.f;                  // probe shift and 1 / Z_q(C)
+  float Sg = 1.f, om = 0.f;                   // S_{l,g} and the head weight of the current (l, g)
+  int cur_lg = -1;
+  auto load_pass = [&](int l, int g, int lg, int k0) {
+#pragma unroll
+    for (int h = 0; h < HG; ++h) {
+      const int k = k0 + h;
+      const int hl = (hp + k) % dm.hpg;
+      const uint4* q4 = (const uint4*)(Q + (((int64_t)l * dm.H + (int64_t)g * dm.hpg + hl) * dm.W + uq) * D + QE * g4o);
+#pragma unroll
+      for (int x = 0; x < QW / 4; ++x) {
+        const uint4 v = q4[x];
+        qr[h][4 * x] = v.x; qr[h][4 * x + 1] = v.y; qr[h][4 * x + 2] = v.z; qr[h][4 * x + 3] = v.w;
+      }
+      const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
+      rs[h] = make_float2(st.x, k < dm.hpg ? 1.0f / st.y : 0.f);
+    }
+  };
 
   for (int64_t uu = ub; uu < ue; ++uu) {
+    // the thread index passes through an empty asm per unit, so that per-thread
+    // addresses are formed inside the loop instead of being held in registers across it
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
     const int lg = (int)(uu / J), j = (int)(uu % J);
     const int l = lg / dm.G, g = lg % dm.G;
     const int64_t unit = (int64_t)lg * dm.J_cap + j;
@@ -143,22 +182,17 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
     const int n_tt = rows16 / 16;
     const T* Kp = K + ((int64_t)lg * dm.T + a0) * D;
     const T* Vp = V + ((int64_t)lg * dm.T + a0) * D;
-    // Q quarter row and row statistics of head slot k (head (hp + k) mod |H(g)|)
-    auto load_q = [&](int k, uint32_t* q, float2& rsv) {
-      const int hl = (hp + k) % dm.hpg;
-      const uint4* q4 = (const uint4*)(Q + (((int64_t)l * dm.H + (int64_t)g * dm.hpg + hl) * dm.W + uq) * D + QE * g4);
-#pragma unroll
-      for (int h = 0; h < QW / 4; ++h) {
-        const uint4 v = q4[h];
-        q[4 * h] = v.x; q[4 * h + 1] = v.y; q[4 * h + 2] = v.z; q[4 * h + 3] = v.w;
+    if (lg != cur_lg || MP) {
+      if (wave_on) load_pass(l, g, lg, klast);
+      if (lg != cur_lg) {
+        if (wave_on) {
+          mq = tv.probe_m[(int64_t)lg * dm.W + uq];
+          zcq = 1.0f / tv.probe_ZC[(int64_t)lg * dm.W + uq];
+        }
+        Sg = tv.lg_S[lg] + dm.eps;
+        om = tv.omega[lg];
+        cur_lg = lg;
       }
-      const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
-      rsv = make_float2(st.x, 1.0f / st.y);      // (m_V, 1 / Z_V)
-    };
-    if (wave_on) {
-      load_q(dm.hpg - 1, qa, rsa);
-      mq = tv.probe_m[(int64_t)lg * dm.W + uq];
-      zcq = 1.0f / tv.probe_ZC[(int64_t)lg * dm.W + uq];
     }
     // representative position of the root and its RoPE row (wave 0, used at the end)
     const int64_t pmid = round_half_even_mid((int)a0, (int)a0 + n);
@@ -174,21 +208,74 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
 #pragma unroll
       for (int h = 0; h < 16; ++h) kacc[h] = 0.f;
       const int c = 8 * (tid % CHP);
-      for (int e = tid; e < rows16 * CHP; e += RT) {
-        const int t = e / CHP;
-        float k1[8], k2[8], o1[8], o2[8];
-        if constexpr (BF) {
-          uint4 u1 = make_uint4(0, 0, 0, 0), u2 = u1;
-          if (t < n) { u1 = *(const uint4*)(Kp + (int64_t)t * D + c); u2 = *(const uint4*)(Kp + (int64_t)t * D + c + H2); }
-          *(uint4*)(sK + t * Lay::LDK + c) = u1;
-          *(uint4*)(sK + t * Lay::LDK + c + H2) = u2;
-          const uint32_t w1[4] = {u1.x, u1.y, u1.z, u1.w}, w2[4] = {u2.x, u2.y, u2.z, u2.w};
+      // k°, ||k°|| and the partial sums of one token chunk (k1 holds dims c.., k2 dims c + H2..)
+      auto rope_undo = [&](int t, const float* k1, const float* k2, const float* cs8, const float* sn8) {
+        float ss = 0.f;
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const float o1 = k1[h] * cs8[h] + k2[h] * sn8[h];
+          const float o2 = k2[h] * cs8[h] - k1[h] * sn8[h];
+          kacc[h] += o1;
+          kacc[8 + h] += o2;
+          ss += o1 * o1 + o2 * o2;
+        }
+#pragma unroll
+        for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        if (t < n && c == 0) sKn[t] = sqrtf(ss);
+      };
+      if constexpr (BF) {
+        constexpr int CPR = D / 8;            // 16-byte chunks per row of V
+        const int cnt = rows16 * CHP;         // = (rows16 / 2) * CPR
+        // every load is unconditional (rows clamped to the unit) so that the loads of two
+        // chunks are in flight together; rows past n are zeroed after the load
+        auto load = [&](int e) {
+          StageChunk s;
+          const int t = e / CHP;
+          const int tk = t < n ? t : n - 1;
+          const uint4* kp = (const uint4*)(Kp + (int64_t)tk * D + c);
+          s.k1 = kp[0];
+          s.k2 = *(const uint4*)(Kp + (int64_t)tk * D + c + H2);
+          const int64_t ta = a0 + tk;
+          s.c0 = *(const float4*)(cosT + ta * H2 + c); s.c1 = *(const float4*)(cosT + ta * H2 + c + 4);
+          s.s0 = *(const float4*)(sinT + ta * H2 + c); s.s1 = *(const float4*)(sinT + ta * H2 + c + 4);
+          const int grp = e / (8 * CPR), rem = e % (8 * CPR);
+          const int cv = rem / 8, tv0 = 2 * (8 * grp + rem % 8);
+          const int t0c = tv0 < n ? tv0 : n - 1, t1c = tv0 + 1 < n ? tv0 + 1 : n - 1;
+          s.v0 = *(const uint4*)(Vp + (int64_t)t0c * D + 8 * cv);
+          s.v1 = *(const uint4*)(Vp + (int64_t)t1c * D + 8 * cv);
+          return s;
+        };
+        auto store = [&](int e, StageChunk s) {
+          const int t = e / CHP;
+          if (t >= n) { s.k1 = make_uint4(0, 0, 0, 0); s.k2 = s.k1; }
+          *(uint4*)(sK + t * Lay::LDK + c) = s.k1;
+          *(uint4*)(sK + t * Lay::LDK + c + H2) = s.k2;
+          const uint32_t w1[4] = {s.k1.x, s.k1.y, s.k1.z, s.k1.w}, w2[4] = {s.k2.x, s.k2.y, s.k2.z, s.k2.w};
+          float k1[8], k2[8];
 #pragma unroll
           for (int h = 0; h < 4; ++h) {
             k1[2 * h] = __uint_as_float(w1[h] << 16); k1[2 * h + 1] = __uint_as_float(w1[h] & 0xffff0000u);
             k2[2 * h] = __uint_as_float(w2[h] << 16); k2[2 * h + 1] = __uint_as_float(w2[h] & 0xffff0000u);
           }
-        } else {
+          const float cs8[8] = {s.c0.x, s.c0.y, s.c0.z, s.c0.w, s.c1.x, s.c1.y, s.c1.z, s.c1.w};
+          const float sn8[8] = {s.s0.x, s.s0.y, s.s0.z, s.s0.w, s.s1.x, s.s1.y, s.s1.z, s.s1.w};
+          rope_undo(t, k1, k2, cs8, sn8);
+          const int grp = e / (8 * CPR), rem = e % (8 * CPR);
+          const int cv = rem / 8, tv0 = 2 * (8 * grp + rem % 8);
+          if (tv0 >= n) s.v0 = make_uint4(0, 0, 0, 0);
+          if (tv0 + 1 >= n) s.v1 = make_uint4(0, 0, 0, 0);
+          const uint32_t a[4] = {s.v0.x, s.v0.y, s.v0.z, s.v0.w}, b[4] = {s.v1.x, s.v1.y, s.v1.z, s.v1.w};
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            *(uint32_t*)(sVt + (8 * cv + 2 * h) * Lay::LDV + tv0) = (a[h] & 0xffffu) | (b[h] << 16);
+            *(uint32_t*)(sVt + (8 * cv + 2 * h + 1) * Lay::LDV + tv0) = (a[h] >> 16) | (b[h] & 0xffff0000u);
+          }
+        };
+        for (int e = tid; e < cnt; e += RT) store(e, load(e));
+      } else {
+        for (int e = tid; e < rows16 * CHP; e += RT) {
+          const int t = e / CHP;
+          float k1[8], k2[8];
           float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a, cq = a, dq = a;
           if (t < n) {
             const float4* p1 = (const float4*)((const float*)Kp + (int64_t)t * D + c);
@@ -200,26 +287,24 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
           d1[0] = a; d1[1] = b; d2[0] = cq; d2[1] = dq;
           k1[0] = a.x; k1[1] = a.y; k1[2] = a.z; k1[3] = a.w; k1[4] = b.x; k1[5] = b.y; k1[6] = b.z; k1[7] = b.w;
           k2[0] = cq.x; k2[1] = cq.y; k2[2] = cq.z; k2[3] = cq.w; k2[4] = dq.x; k2[5] = dq.y; k2[6] = dq.z; k2[7] = dq.w;
-        }
-        float ss = 0.f;
-        if (t < n) {
-          const int64_t ta = a0 + t;
+          const int64_t ta = a0 + (t < n ? t : n - 1);
           const float4 c0 = *(const float4*)(cosT + ta * H2 + c), c1 = *(const float4*)(cosT + ta * H2 + c + 4);
           const float4 s0 = *(const float4*)(sinT + ta * H2 + c), s1 = *(const float4*)(sinT + ta * H2 + c + 4);
           const float cs8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
           const float sn8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-#pragma unroll
-          for (int h = 0; h < 8; ++h) {
-            o1[h] = k1[h] * cs8[h] + k2[h] * sn8[h];
-            o2[h] = k2[h] * cs8[h] - k1[h] * sn8[h];
-            kacc[h] += o1[h];
-            kacc[8 + h] += o2[h];
-            ss += o1[h] * o1[h] + o2[h] * o2[h];
-          }
+          rope_undo(t, k1, k2, cs8, sn8);
         }
-#pragma unroll
-        for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
-        if (t < n && c == 0) sKn[t] = sqrtf(ss);
+        constexpr int CPR = D / 4;
+        for (int e = tid; e < rows16 * CPR; e += RT) {
+          const int grp = e / (16 * CPR), rem = e % (16 * CPR);
+          const int cv = rem / 16, t = 16 * grp + rem % 16;
+          float4 vv = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (t < n) vv = *(const float4*)(Vp + (int64_t)t * D + 4 * cv);
+          sVt[(4 * cv + 0) * Lay::LDV + t] = vv.x;
+          sVt[(4 * cv + 1) * Lay::LDV + t] = vv.y;
+          sVt[(4 * cv + 2) * Lay::LDV + t] = vv.z;
+          sVt[(4 * cv + 3) * Lay::LDV + t] = vv.w;
+        }
       }
       // lanes l, l + CHP, ... of the wave hold the same chunk
 #pragma unroll
@@ -231,83 +316,62 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
         for (int h = 0; h < 8; ++h) { sPk[w * D + c + h] = kacc[h]; sPk[w * D + c + H2 + h] = kacc[8 + h]; }
       }
     }
-    if constexpr (BF) {
-      constexpr int CPR = D / 8;              // 16-byte chunks per row
-      // lane -> (token pair, chunk): 8 pairs x CPR chunks per group
-      for (int e = tid; e < (rows16 / 2) * CPR; e += RT) {
-        const int grp = e / (8 * CPR), rem = e % (8 * CPR);
-        const int c = rem / 8, t = 2 * (8 * grp + rem % 8);
-        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = v0;
-        if (t < n) v0 = *(const uint4*)(Vp + (int64_t)t * D + 8 * c);
-        if (t + 1 < n) v1 = *(const uint4*)(Vp + (int64_t)(t + 1) * D + 8 * c);
-        const uint32_t a[4] = {v0.x, v0.y, v0.z, v0.w}, b[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          *(uint32_t*)(sVt + (8 * c + 2 * h) * Lay::LDV + t) = (a[h] & 0xffffu) | (b[h] << 16);
-          *(uint32_t*)(sVt + (8 * c + 2 * h + 1) * Lay::LDV + t) = (a[h] >> 16) | (b[h] & 0xffff0000u);
-        }
-      }
-    } else {
-      constexpr int CPR = D / 4;
-      for (int e = tid; e < rows16 * CPR; e += RT) {
-        const int grp = e / (16 * CPR), rem = e % (16 * CPR);
-        const int c = rem / 16, t = 16 * grp + rem % 16;
-        float4 vv = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (t < n) vv = *(const float4*)(Vp + (int64_t)t * D + 4 * c);
-        sVt[(4 * c + 0) * Lay::LDV + t] = vv.x;
-        sVt[(4 * c + 1) * Lay::LDV + t] = vv.y;
-        sVt[(4 * c + 2) * Lay::LDV + t] = vv.z;
-        sVt[(4 * c + 3) * Lay::LDV + t] = vv.w;
-      }
-    }
-    for (int e = tid; e < RWV * NMAX; e += RT) { sRp[e] = 0.f; sAp[e] = 0.f; }
     __syncthreads();
 
-    // ---- logits, relevance, probe exponentials and M^T = V^T E^T: heads one
-    // at a time with the next head's Q in flight, the probe head (slot 0) last ----
+    // ---- logits, relevance, probe exponentials and M^T = V^T E^T: per 16-token
+    // tile the HG held head slots together; the pass holding the probe head
+    // (slot 0) runs last ----
     f32x4 Macc[DT];
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) Macc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     float Zl = 0.f;
     if (wave_on) {
-      for (int k = dm.hpg - 1; k >= 0; --k) {
-        if (k > 0) load_q(k - 1, qb, rsb);
+      for (int k0 = klast; k0 >= 0; k0 -= HG) {
+        if (MP && k0 != klast) load_pass(l, g, lg, k0);
         for (int tb = 0; tb < n_tt; ++tb) {
           const int t0 = 16 * tb;
           uint32_t kreg[QW];
           {
             const uint4* k4 = (const uint4*)(sK + (t0 + i16) * Lay::LDK + QE * g4);
 #pragma unroll
-            for (int h = 0; h < QW / 4; ++h) {
-              const uint4 v = k4[h];
-              kreg[4 * h] = v.x; kreg[4 * h + 1] = v.y; kreg[4 * h + 2] = v.z; kreg[4 * h + 3] = v.w;
+            for (int x = 0; x < QW / 4; ++x) {
+              const uint4 v = k4[x];
+              kreg[4 * x] = v.x; kreg[4 * x + 1] = v.y; kreg[4 * x + 2] = v.z; kreg[4 * x + 3] = v.w;
             }
           }
-          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          f32x4 acc[HG];
+#pragma unroll
+          for (int h = 0; h < HG; ++h) acc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
           if constexpr (BF) {
 #pragma unroll
             for (int s = 0; s < QE / 4; ++s)
-              acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qa[2 * s], qa[2 * s + 1]), acc);
+#pragma unroll
+              for (int h = 0; h < HG; ++h)
+                acc[h] = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qr[h][2 * s], qr[h][2 * s + 1]), acc[h]);
           } else {
 #pragma unroll
             for (int s = 0; s < QE; ++s)
-              acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qa[s]), acc);
+#pragma unroll
+              for (int h = 0; h < HG; ++h)
+                acc[h] = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qr[h][s]), acc[h]);
           }
-          // lane holds tokens t0 + 4 g4 + r of the lane's query row
-          float Rp[4], ev[4] = {0.f, 0.f, 0.f, 0.f};
+          // lane holds tokens t0 + 4 g4 + r of the lane's query row in every slot
+          float Rp[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            Rp[r] = 0.f;
-            if (uok && t0 + 4 * g4 + r < n) {
-              const float x = acc[r] * scale;
-              Rp[r] = fexp(x - rsa.x) * rsa.y;
-              if (k == 0) ev[r] = fexp(x - mq);
-            }
-          }
-          if (k == 0) {
-            float ap[4];
+            float s = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) { ap[r] = ev[r] * zcq; Zl += ev[r]; }
+            for (int h = 0; h < HG; ++h) s += fexp(acc[h][r] * scale - rs[h].x) * rs[h].y;
+            Rp[r] = (uok && t0 + 4 * g4 + r < n) ? s : 0.f;
+          }
+          if (k0 == 0) {
+            float ev[4], ap[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              ev[r] = (uok && t0 + 4 * g4 + r < n) ? fexp(acc[0][r] * scale - mq) : 0.f;
+              ap[r] = ev[r] * zcq;
+              Zl += ev[r];
+            }
             if constexpr (BF) {
               s16x4 eh, em, el;
               split3(ev, eh, em, el);
@@ -335,12 +399,10 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
           }
 #pragma unroll
           for (int r = 0; r < 4; ++r) Rp[r] = row_sum16(Rp[r]);
-          if (i16 < 4) sRp[w * NMAX + t0 + 4 * g4 + i16] += pick4(Rp, i16);
-        }
-        if (k > 0) {
-#pragma unroll
-          for (int h = 0; h < QW; ++h) qa[h] = qb[h];
-          rsa = rsb;
+          if (i16 < 4) {
+            float* dst = sRp + w * NMAX + t0 + 4 * g4 + i16;
+            *dst = (k0 == klast ? 0.f : *dst) + pick4(Rp, i16);
+          }
         }
       }
     }
@@ -351,8 +413,9 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       const int t = tid;
       float s = 0.f, am = 0.f;
 #pragma unroll
-      for (int w2 = 0; w2 < RWV; ++w2) { s += sRp[w2 * NMAX + t]; am += sAp[w2 * NMAX + t]; }
-      const float R = s / (tv.lg_S[lg] + dm.eps);
+      for (int w2 = 0; w2 < RWV; ++w2)
+        if (16 * w2 < dm.W) { s += sRp[w2 * NMAX + t]; am += sAp[w2 * NMAX + t]; }
+      const float R = s / Sg;
       const float A = am / (float)dm.W;
       sR[t] = R;
       sA[t] = A;
@@ -419,7 +482,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
     }
     __syncthreads();
 
-    // ---- distortion of the root: probes of wave w ----
+    // ---- distortion of the root: probes of wave w (head slot 0 is in qr[0]) ----
     {
       float con = 0.f;
       if (wave_on) {
@@ -428,8 +491,8 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
 #pragma unroll
         for (int e = 0; e < QE; ++e) {
           float qv;
-          if constexpr (BF) qv = __uint_as_float(e & 1 ? (qa[e >> 1] & 0xffff0000u) : (qa[e >> 1] << 16));
-          else qv = __uint_as_float(qa[e]);
+          if constexpr (BF) qv = __uint_as_float(e & 1 ? (qr[0][e >> 1] & 0xffff0000u) : (qr[0][e >> 1] << 16));
+          else qv = __uint_as_float(qr[0][e]);
           qk += qv * sKt[QE * g4 + e];
         }
         qk += __shfl_xor(qk, 16, 64);
@@ -484,7 +547,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       tv.unit_nn[unit] = 1;
       tv.unit_Ddrop[unit] = dd;
       const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
-      const float Ua = utility(add_gain(tv.omega[lg], sr, dd, Dv), 1);
+      const float Ua = utility(add_gain(om, sr, dd, Dv), 1);
       tv.add_U[unit] = Ua;
       tv.add_E[unit] = op_key(Ua, ord * 256u);
       tv.add_exec[unit] = 0;
@@ -507,7 +570,7 @@ hipError_t launch_root(const Dims& dm, const void* K, const void* V, const void*
   const int lds = root_lds_bytes(dm);
 #define GKV_LAUNCH_ROOT(TT, DD)                                                                            \
   do {                                                                                                     \
-    auto fn = k_root<TT, DD>;                                                                              \
+    auto fn = dm.hpg > 4 ? k_root<TT, DD, true> : k_root<TT, DD, false>;                                   \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds); \
     if (e0 != hipSuccess) return e0;                                                                       \
     hipLaunchKernelGGL(fn, grid, dim3(RT), lds, st, dm, (const TT*)K, (const TT*)V, (const TT*)Q, cosT, sinT, \
@@ -516,7 +579,8 @@ hipError_t launch_root(const Dims& dm, const void* K, const void* V, const void*
   if (dm.dtype == GRACEKV_BF16) {
     if (dm.d == 128) GKV_LAUNCH_ROOT(uint16_t, 128); else GKV_LAUNCH_ROOT(uint16_t, 64);
   } else {
-    if (dm.d == 128) GKV_LAUNCH_ROOT(float, 128); else GKV_LAUNCH_ROOT(float, 64);
+    if (dm.d != 64) return hipErrorInvalidValue;   // fp32 caches take d = 64 only
+    GKV_LAUNCH_ROOT(float, 64);
   }
 #undef GKV_LAUNCH_ROOT
   return hipGetLastError();
