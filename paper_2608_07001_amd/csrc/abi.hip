@@ -245,10 +245,14 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
-  // pruned: bound from the roots -> root splits -> tighter bound -> the rest
-  if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  // pruned: bound from the roots -> root splits -> tighter bound -> the rest.  The
+  // first bound is taken at rank B_free (one below the cut's rank B_free - 1): it
+  // is still a lower bound of the cut, and at least one Add keyed at or above it
+  // is left unexecuted and affordable when a single unit remains, so a root whose
+  // Split key bound lies below it can neither reach the cut nor be the last fill.
+  if (launch_theta(dm, tv, st, true) != hipSuccess) return GRACEKV_ERR_HIP;
   if (build(BUILD_ROOT_SPLIT) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (launch_theta(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_theta(dm, tv, st, false) != hipSuccess) return GRACEKV_ERR_HIP;
   return hip_status(build(BUILD_CONTINUE));
 }
 

@@ -465,7 +465,8 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
   const int J = *n_slots;
   const int nwork = tv.wctr[0];
-  const uint64_t theta = mode == BUILD_FULL ? 0ull : *tv.theta;
+  const uint64_t theta = mode == BUILD_FULL ? 0ull : tv.theta[0];
+  const uint64_t theta_skip = mode == BUILD_FULL ? 0ull : tv.theta[1];
   const float scale = 1.0f / sqrtf((float)D);
   const int pt = wave & 3;                    // probe tile of this wave
   int* XL = U.xi;              // [0..31]  prefix cut list
@@ -497,6 +498,9 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
     const T* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
     const float w = tv.omega[lg];
 
+    // the root's Split cannot be selected (its key bound is below the skip bound)
+    const bool rskip = mode != BUILD_FULL &&
+                       root_split_key_bound(w, tv.node_R[base], tv.node_D[base], ord) < theta_skip;
     // ---- node table; refine only nodes whose creating op reaches theta ----
     {
       const int nn0 = tv.unit_nn[unit];
@@ -509,7 +513,8 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
         U.ncut[i] = tv.node_cut[sl]; U.nD[i] = tv.node_D[sl]; U.nR[i] = tv.node_R[sl]; U.nU[i] = tv.sp_U[sl];
         const uint64_t ec = U.np[i] < 0 ? Eadd : tv.sp_E[base + U.np[i]];
         U.nE[i] = ec;
-        any |= U.nch[i] == 0 && U.nn[i] >= 2 && ec >= theta && (mode != BUILD_ROOT_SPLIT || i == 0);
+        any |= U.nch[i] == 0 && U.nn[i] >= 2 && ec >= theta && (mode != BUILD_ROOT_SPLIT || i == 0) &&
+               !(i == 0 && rskip);
       }
       if (tid == 0) cnt[0] = nn0;
       if (!__syncthreads_or(any)) continue;
@@ -624,7 +629,7 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
       if (head >= count || (mode == BUILD_ROOT_SPLIT && head > 0)) break;
       const int a = U.na[head], nv = U.nn[head], b = a + nv;
       if (nv < 2 || U.nch[head] > 0) continue;                  // leaf, or refined by an earlier pass
-      if (mode != BUILD_FULL && U.nE[head] < theta) continue;    // cannot reach the auction's cut
+      if (mode != BUILD_FULL && (U.nE[head] < theta || (head == 0 && rskip))) continue;  // cannot reach the cut
       const float Dv = U.nD[head];
       if (nv == 2) {
         if (tid == 0) {
@@ -853,7 +858,7 @@ __global__ void k_work_mark(Dims dm, int mode, TreeView tv) {
   const int64_t a0 = tv.slots[j];
   const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
   const int nn = tv.unit_nn[unit];
-  const uint64_t theta = mode == BUILD_FULL ? 0ull : *tv.theta;
+  const uint64_t theta = mode == BUILD_FULL ? 0ull : tv.theta[0];
   bool need = false;
   for (int i = 0; i < nn && !need; ++i) {
     if (mode == BUILD_ROOT_SPLIT && i > 0) break;
@@ -861,8 +866,13 @@ __global__ void k_work_mark(Dims dm, int mode, TreeView tv) {
     if (tv.node_nch[s] != 0 || tv.node_n[s] < 2) continue;
     if (mode == BUILD_FULL) { need = true; break; }
     const int par = tv.node_parent[s];
-    const uint64_t E = par < 0 ? tv.add_E[unit] : tv.sp_E[base + par];
-    need = E >= theta;
+    if (par < 0) {                          // the root: its Add reaches theta and its Split may
+      const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+      need = tv.add_E[unit] >= theta &&
+             root_split_key_bound(tv.omega[lg], tv.node_R[s], tv.node_D[s], ord) >= tv.theta[1];
+    } else {
+      need = tv.sp_E[base + par] >= theta;
+    }
   }
   if (need) {
     const int pos = atomicAdd(&tv.wctr[0], 1);

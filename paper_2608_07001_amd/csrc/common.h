@@ -59,7 +59,7 @@ struct TreeView {
   int32_t* status;      // device status word
   int32_t* slots;       // [J_cap + 1] copy of the slot starts (then N_c)
   int32_t* nslots;      // [1] J
-  uint64_t* theta;      // [1] lower bound of the auction cut used by the pruned build
+  uint64_t* theta;      // [2] pruned build: [0] lower bound of the auction cut, [1] root-split skip bound
   void* selstate;       // radix-select state of that bound
   int32_t* work;        // [L*G*J_cap] units to refine
   int32_t* wctr;        // [4] list length, next item
@@ -84,6 +84,13 @@ __device__ __forceinline__ float utility(float gain, int cost) {
 // unique priority: larger U first, then the smaller id
 __device__ __forceinline__ uint64_t op_key(float U, uint32_t id) {
   return ((uint64_t)__float_as_uint(U) << 32) | (uint64_t)(0xFFFFFFFFu - id);
+}
+// Upper bound of the key of a root's Split before the root is refined: the
+// children's distortions are >= 0 and the cost is >= 1, and every rounding step
+// of split_gain / utility is monotone, so the key the Split gets once its
+// children are known (and its effective key) is <= this value, bit for bit.
+__device__ __forceinline__ uint64_t root_split_key_bound(float w, float R, float D, uint32_t ord) {
+  return op_key(utility(split_gain(w, R, D, 0.f), 1), ord * 256u + 1u);
 }
 
 // representative position of [x0, x1): round((x0 + x1 - 1) / 2), ties to even
@@ -193,7 +200,8 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
                         const float* kappa, const TreeView& tv, hipStream_t st);
 hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
-hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st);
+// rank: B_free - 1 (the cut) or B_free (the skip bound, also stored in theta[1])
+hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound);
 size_t selstate_bytes();
 hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st);

@@ -122,11 +122,11 @@ hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& 
 }
 
 // ---------------------------------------------------------------------------
-__global__ void k_sel_init(Dims dm, SelState* S) {
+__global__ void k_sel_init(Dims dm, SelState* S, int rank_extra) {
   const int t = threadIdx.x;
   S->hist[t] = 0;
   if (t == 0) {
-    S->prefix = 0; S->target = dm.B_free - 1; S->above = 0; S->total = 0; S->R = 0;
+    S->prefix = 0; S->target = dm.B_free - 1 + rank_extra; S->above = 0; S->total = 0; S->R = 0;
     S->resid_key = 0; S->mode = SEL_SELECT;
   }
 }
@@ -323,7 +323,7 @@ __global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used)
 
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st) {
   SelState* S = (SelState*)ws;
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, 0);
   const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
   const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
   for (int pass = 0; pass < 8; ++pass) {
@@ -340,22 +340,24 @@ hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, vo
 // Lower bound of the cut over the ops known so far (the pruned build): the
 // same cost-weighted radix select; with every known op affordable nothing can
 // be pruned (bound 0); with B_free <= 1 no Split can execute (bound max).
-__global__ void k_theta_store(Dims dm, const SelState* S, uint64_t* theta) {
+__global__ void k_theta_store(Dims dm, const SelState* S, uint64_t* theta, bool skip_bound) {
   if (threadIdx.x != 0) return;
   const int mode = S->mode;
-  *theta = mode == SEL_SELECT ? S->prefix : (mode == SEL_ALL ? 0ull : ~0ull);
+  const uint64_t v = mode == SEL_SELECT ? S->prefix : (mode == SEL_ALL ? 0ull : ~0ull);
+  theta[0] = v;
+  if (skip_bound) theta[1] = v;
 }
 
-hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st) {
+hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound) {
   SelState* S = (SelState*)tv.selstate;
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, skip_bound ? 1 : 0);
   const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
   const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
   for (int pass = 0; pass < 8; ++pass) {
     hipLaunchKernelGGL(k_sel_hist, dim3(blocks), dim3(256), 0, st, dm, tv, S, pass);
     hipLaunchKernelGGL(k_sel_scan, dim3(1), dim3(64), 0, st, dm, S, pass);
   }
-  hipLaunchKernelGGL(k_theta_store, dim3(1), dim3(64), 0, st, dm, (const SelState*)S, tv.theta);
+  hipLaunchKernelGGL(k_theta_store, dim3(1), dim3(64), 0, st, dm, (const SelState*)S, tv.theta, skip_bound);
   return hipGetLastError();
 }
 

@@ -139,6 +139,81 @@ def test_three_implementations_agree(seed):
         assert spent == min(B, total) or spent == B - 1 or spent == total
 
 
+def _unit_forest(rng, n_units, max_ops, p_zero):
+    """Forest shaped like the trees' ops: per unit an Add whose only child is the
+    root's Split, under which the Splits of the descendants hang."""
+    ops, root_split = [], {}
+    for u in range(n_units):
+        def mk(kind, local):
+            U = 0.0 if rng.random() < p_zero else float(np.float32(rng.uniform(0, 4)))
+            oid = u * 256 + local
+            op = O.Op(oid, 0, u, local, kind, U, 1 if kind == "add" else rng.choice([1, 2]), U, 0)
+            op.key = O.composite_key(U, oid)
+            return op
+        base = len(ops)
+        ops.append(mk("add", 0))
+        n = rng.randint(0, max_ops)
+        for i in range(n):
+            parent = base if i == 0 else base + 1 + rng.randrange(0, i)
+            ops.append(mk("split", 1 + i))
+            ops[parent].children.append(len(ops) - 1)
+        if n:
+            root_split[u] = base + 1
+    return ops, root_split
+
+
+def _subtree(ops, i):
+    out, st = [], [i]
+    while st:
+        k = st.pop()
+        out.append(k)
+        st.extend(ops[k].children)
+    return out
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_root_split_skip_bound_keeps_the_selection(seed):
+    """The pruned build leaves a root unrefined when an upper bound of its
+    Split's key lies below the B-th largest Add key (the first bound pass runs
+    at rank B).  Dropping those Splits with their whole subtrees must leave the
+    literal queue's executed set unchanged, for every budget, including the
+    single-unit fill at the end."""
+    rng = random.Random(1000 + seed)
+    ops, root_split = _unit_forest(rng, rng.randint(2, 9), 7, p_zero=0.3 if seed % 3 == 0 else 0.05)
+    n_units = sum(1 for o in ops if o.kind == "add")
+    total = sum(o.cost for o in ops)
+    add_keys = sorted((o.key for o in ops if o.kind == "add"), reverse=True)
+    for B in sorted({0, 1, 2, 3, n_units - 1, n_units, n_units + 1, total // 2, total - 1, total}):
+        if B < 0:
+            continue
+        # the first bound pass over the Adds alone (cost 1 each), with its special cases
+        if B <= 0 or B == 1:
+            skip = None                                   # nothing is refined at all
+        elif n_units <= B:
+            skip = 0                                      # every op fits: nothing skipped
+        else:
+            skip = add_keys[B - 1]
+        full = O.select_heap(ops, B)
+        drop = set()
+        for u, i in root_split.items():
+            slack = 0.0 if rng.random() < 0.5 else float(np.float32(rng.uniform(0, 0.5)))
+            bound = O.composite_key(float(np.float32(ops[i].U + slack)), ops[i].oid)
+            assert bound >= ops[i].key
+            if skip is None or bound < skip:
+                drop.update(_subtree(ops, i))
+        keep = [i for i in range(len(ops)) if i not in drop]
+        remap = {old: new for new, old in enumerate(keep)}
+        pruned = []
+        for i in keep:
+            o = ops[i]
+            c = O.Op(o.oid, o.lg, o.unit, o.node, o.kind, o.gain, o.cost, o.U, o.key)
+            c.children = [remap[k] for k in o.children if k in remap]
+            pruned.append(c)
+        got = O.select_heap(pruned, B)
+        assert not any(full[i] for i in drop), (seed, B)
+        assert [full[i] for i in keep] == got, (seed, B)
+
+
 def _ideals(ops):
     parent = [-1] * len(ops)
     for i, o in enumerate(ops):
