@@ -79,11 +79,15 @@ typedef struct {
   int32_t k_curv;                            /* 16 curvature split candidates */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph, alpha_floor;           /* must be 0 on this path */
-  int32_t flags;                             /* GRACEKV_FLAG_PRUNE: budget-aware pruning of the tree build */
+  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL */
 } gracekv_config;
 
 /* Budget-aware pruning of the tree build (output unchanged; see gracekv_build_trees). */
 #define GRACEKV_FLAG_PRUNE 1
+/* Segmentation DP without the chunk-parallel guess: every chunk of the
+ * recurrence is run from the true state, one after the other (output
+ * unchanged, slower; see gracekv_segment). */
+#define GRACEKV_FLAG_DP_SERIAL 2
 
 /* Sizes derived from a config (host only). */
 typedef struct {
@@ -135,7 +139,13 @@ gracekv_status gracekv_check(const gracekv_config* cfg, void* trees, void* strea
  *   bscore     [T] fp32 out: boundary score b_i (eq:app_boundary_score)
  *   slot_starts [J_cap + 1] int32 out: slot starts a_1 = 0 < ... < a_J, then N_c
  *   n_slots    [1] int32 out: J
- *   ws         workspace of plan.seg_ws_bytes bytes */
+ *   ws         workspace of plan.seg_ws_bytes bytes
+ * The recurrence runs on slot scores rounded once to a common fixed-point grid
+ * (a power-of-two step chosen from the largest |score|, finer than 1e-12 for
+ * scores of order one), so its additions are exact; chunks of 1024 ends are
+ * solved in parallel from a guessed state and accepted only where that is
+ * provably exact, the rest is recomputed (GRACEKV_FLAG_DP_SERIAL recomputes
+ * all of them).  Ties go to the smallest slot start. */
 gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, const float* surprisal,
                                float* kappa, float* bscore, int32_t* slot_starts, int32_t* n_slots,
                                void* ws, size_t ws_bytes, void* stream);

@@ -25,6 +25,7 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.lam_Z = c.lam_Z; d.lam_M = c.lam_M; d.lam_kappa = c.lam_kappa; d.beta_frac = c.beta_frac; d.eps = c.eps;
   d.k_curv = c.k_curv;
   d.rows = d.hpg * c.W;
+  d.dp_serial = (c.flags & GRACEKV_FLAG_DP_SERIAL) ? 1 : 0;
   return d;
 }
 
@@ -120,7 +121,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
-  if (c->flags & ~GRACEKV_FLAG_PRUNE) return GRACEKV_ERR_INVALID_ARG;
+  if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL)) return GRACEKV_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
   if (c->dtype == GRACEKV_F32 && c->d != 64) return GRACEKV_ERR_UNSUPPORTED;   // refinement LDS
   if (c->D_hidden % 8 != 0) return GRACEKV_ERR_UNSUPPORTED;                   // 16-byte hidden rows

@@ -27,6 +27,7 @@ struct Dims {
   float lam_Z, lam_M, lam_kappa, beta_frac, eps;
   int k_curv;
   int rows;                      // relevance rows per (l, g): hpg * W
+  int dp_serial;                 // segmentation DP: no warm-up guess, every chunk from the true state
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).

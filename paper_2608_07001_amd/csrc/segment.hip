@@ -24,6 +24,8 @@
 //     depend only on F[< i], so 16 ends advance per step; ties go to the
 //     smallest predecessor; terminal relaxation eq:app_terminal_predecessor;
 //     backtrack from LDS.
+#include <climits>
+
 #include "common.h"
 
 namespace gkv {
@@ -42,22 +44,34 @@ struct SegWs {
   float* gram;      // [n_seg][T][BAND]
   float* dist2;     // [N_c][BAND]
   double* P2;       // [N_c + 1]
-  uint8_t* Poff;    // [N_c + 1]
-  float* scratch;   // [T] for the robust z
-  double* Fdbg;     // [1]
+  uint8_t* Poff;    // [N_c + 1] backpointer offsets i - P(i) (0: none)
+  double* Fdbg;     // [4] F(N), chunks recomputed by the fix-up
   double* S;        // [N_c][128] slot scores by (i, length), candidate-major per lane
+  long long* Fg;    // [C][DPC + 128] fixed-point F of positions c DPC - 127 .. (c + 1) DPC
+  long long* dlt;   // [C] offset that turns Fg[c] into the true F
+  long long* cdiff; // [C] constant difference Fg[c-1] - Fg[c] over chunk c's window
+  int32_t* cok;     // [C] that difference is constant
+  double* smax_part; // [N_c / SLE + 1] largest finite |S| per slot-score workgroup
+  int2* bt_tab;     // [C][128] backtrack: (exit, starts emitted) per chunk entry
+  int2* bt_ent;     // [C] (entry, output offset) of each chunk on the path
 };
+
+// Chunk-parallel DP: ends per chunk and the warm-up margin of a chunk's guessed run.
+constexpr int DPC = 1024;
+constexpr int DPM = 1024;
+__host__ __device__ inline int64_t dp_chunks(int64_t N) { return (N + DPC - 1) / DPC; }
 
 static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t segment_ws_bytes(const Dims& dm) {
-  const size_t T = (size_t)dm.T, N = (size_t)dm.N_c;
+  const size_t T = (size_t)dm.T, N = (size_t)dm.N_c, C = (size_t)dp_chunks(dm.N_c) + 1;
   return al(dm.n_seg * 3 * T * 4) + al(dm.n_seg * T * 4) + al(T * 4) + al((size_t)dm.n_seg * T * BAND * 4) +
-         al(N * BAND * 4) + al((N + 1) * 8) + al(N + 1) + al(T * 4) + al(8) + al(N * BAND * 8);
+         al(N * BAND * 4) + al((N + 1) * 8) + al(N + 1) + al(4 * 8) + al(N * BAND * 8) + al(C * (DPC + 128) * 8) +
+         3 * al(C * 8) + al((N / 16 + 2) * 8) + al(C * 128 * 8) + al(C * 8);
 }
 
 static SegWs seg_view(void* ws, const Dims& dm) {
-  const size_t T = (size_t)dm.T, N = (size_t)dm.N_c;
+  const size_t T = (size_t)dm.T, N = (size_t)dm.N_c, C = (size_t)dp_chunks(dm.N_c) + 1;
   char* p = (char*)ws;
   SegWs s;
   s.kap9 = (float*)p; p += al(dm.n_seg * 3 * T * 4);
@@ -67,9 +81,15 @@ static SegWs seg_view(void* ws, const Dims& dm) {
   s.dist2 = (float*)p; p += al(N * BAND * 4);
   s.P2 = (double*)p; p += al((N + 1) * 8);
   s.Poff = (uint8_t*)p; p += al(N + 1);
-  s.scratch = (float*)p; p += al(T * 4);
-  s.Fdbg = (double*)p; p += al(8);
-  s.S = (double*)p;
+  s.Fdbg = (double*)p; p += al(4 * 8);
+  s.S = (double*)p; p += al(N * BAND * 8);
+  s.Fg = (long long*)p; p += al(C * (DPC + 128) * 8);
+  s.dlt = (long long*)p; p += al(C * 8);
+  s.cdiff = (long long*)p; p += al(C * 8);
+  s.cok = (int32_t*)p; p += al(C * 8);
+  s.smax_part = (double*)p; p += al((N / 16 + 2) * 8);
+  s.bt_tab = (int2*)p; p += al(C * 128 * 8);
+  s.bt_ent = (int2*)p;
   return s;
 }
 
@@ -430,34 +450,26 @@ __global__ __launch_bounds__(1024) void k_prefix_sq(Dims dm, SegWs ws) {
 // the maximum.  Candidate c = len - n_min of end i is stored at
 // S[(i - 1) * 128 + (c % 16) * 8 + c / 16], so the lane that owns candidates
 // c = sub, sub + 16, ... reads 8 consecutive doubles.
-__device__ __forceinline__ void dp_better(double& bv, int64_t& ba, double v, int64_t a) {
-  if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
-}
-
-__device__ __forceinline__ void dp_better32(double& bv, int& ba, double v, int a) {
-  if (v > bv || (v == bv && a < ba)) { bv = v; ba = a; }
-}
-// one DPP step of the (value, smallest start) maximum within 16-lane rows
-// (an absent candidate is (-inf, INT_MAX) and never wins)
-template <int CTRL>
-__device__ __forceinline__ void dp_step(double& bv, int& ba) {
-  const long long b = __double_as_longlong(bv);
-  const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffll), CTRL, 0xf, 0xf, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xf, 0xf, false);
-  const int a2 = __builtin_amdgcn_update_dpp(0, ba, CTRL, 0xf, 0xf, false);
-  const double v2 = __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
-  const bool better = v2 > bv || (v2 == bv && a2 < ba);
-  bv = better ? v2 : bv;
-  ba = better ? a2 : ba;
-}
-// every lane of a 16-lane row ends with the row's best: lanes ^1, ^2 (quad
-// permutes), then rotations by 4 and 8 within the row
-__device__ __forceinline__ void dp_reduce16(double& bv, int& ba) {
-  dp_step<0xB1>(bv, ba);     // quad_perm(1, 0, 3, 2)
-  dp_step<0x4E>(bv, ba);     // quad_perm(2, 3, 0, 1)
-  dp_step<0x124>(bv, ba);    // row_ror:4
-  dp_step<0x128>(bv, ba);    // row_ror:8
-}
+//
+// The recurrence runs in fixed point: every score is rounded once to an
+// integer multiple of 2^-e (e chosen from the largest |S| so that no F can
+// overflow 2^60), after which additions are exact and associative.  That makes
+// the chunk-parallel form below give bit for bit the result of the serial
+// recurrence on the same integers, ties included:
+//   * the ends are cut into chunks of DPC; every chunk runs the recurrence from
+//     a guessed state DPM positions before it (all F there = 0), all chunks at
+//     once;
+//   * if the guessed F over the 128 positions a chunk's ends can reach back to
+//     differ from the true F there by one constant, every F of the chunk
+//     differs by that constant and every backpointer is the true one (adding a
+//     constant to all predecessors changes neither the maximum's position nor
+//     its ties);
+//   * a check kernel tests that condition for all chunks in parallel against
+//     the previous chunk's guess, and a one-workgroup pass chains the
+//     constants and recomputes, from the true state, any chunk that fails.
+// Ties go to the smallest predecessor; terminal relaxation
+// eq:app_terminal_predecessor; backtrack from LDS.
+constexpr long long DP_NEG = LLONG_MIN / 2;    // unreachable
 
 __device__ __forceinline__ double slot_score(const Dims& dm, const float* __restrict__ b, const SegWs& ws, int64_t i,
                                              int len) {
@@ -474,38 +486,94 @@ __device__ __forceinline__ double slot_score(const Dims& dm, const float* __rest
   return gam - (double)dm.lam_d * disp - (double)dm.lam_n * x * x;
 }
 
+// SLE ends per workgroup, one candidate length per thread; the workgroup's
+// largest finite |S| goes to smax_part (reduced by the DP kernels).
+constexpr int SLE = 16;
 __global__ __launch_bounds__(128) void k_slot_scores(Dims dm, const float* __restrict__ b, SegWs ws) {
-  const int64_t i = (int64_t)blockIdx.x + 1;
+  __shared__ double red[2];
   const int c = threadIdx.x;
   const int len = dm.n_min + c;
-  double v = -INFINITY;
-  if (len <= dm.n_max && i - len >= 0) v = slot_score(dm, b, ws, i, len);
-  ws.S[(i - 1) * BAND + (c % 16) * 8 + c / 16] = v;
+  double m = 0.0;
+  for (int k = 0; k < SLE; ++k) {
+    const int64_t i = (int64_t)blockIdx.x * SLE + k + 1;
+    if (i > dm.N_c) break;
+    double v = -INFINITY;
+    if (len <= dm.n_max && i - len >= 0) v = slot_score(dm, b, ws, i, len);
+    ws.S[(i - 1) * BAND + (c % 16) * 8 + c / 16] = v;
+    if (isfinite(v)) m = fmax(m, fabs(v));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o, 64));
+  if ((c & 63) == 0) red[c >> 6] = m;
+  __syncthreads();
+  if (c == 0) ws.smax_part[blockIdx.x] = fmax(red[0], red[1]);
 }
 
-// F over [1, N] in steps of 16 ends (an end depends only on ends >= 16
-// positions earlier): wave w owns ends i0 + 4 w .. i0 + 4 w + 3, 16 lanes per
-// end, each lane 8 candidate lengths; ties go to the smallest start.  Terminal
-// relaxation eq:app_terminal_predecessor, then the backtrack.
-__global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b, SegWs ws, int32_t* slots,
-                                            int32_t* nslots, int use_lds) {
-  extern __shared__ __align__(16) char dsm[];
-  __shared__ double Fr[256];                 // F ring indexed by end & 255
-  uint8_t* Poff = use_lds ? (uint8_t*)dsm : ws.Poff;
-  const int64_t N = dm.N_c;
+// largest finite |S| over the slot-score workgroups (every thread gets it)
+__device__ double dp_smax(const Dims& dm, const SegWs& ws) {
+  __shared__ double red[16];
+  const int64_t nb = (dm.N_c + SLE - 1) / SLE;
+  double m = 0.0;
+  for (int64_t k = threadIdx.x; k < nb; k += blockDim.x) m = fmax(m, ws.smax_part[k]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o, 64));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  double r = 0.0;
+  for (int w = 0; w < (int)(blockDim.x + 63) / 64; ++w) r = fmax(r, red[w]);
+  __syncthreads();
+  return r;
+}
+
+// 2^e with (max |S| + 1) (N / n_min + 2) 2^e < 2^60 (every thread of the workgroup calls it)
+__device__ __forceinline__ double dp_scale(const Dims& dm, const SegWs& ws) {
+  const double mx = dp_smax(dm, ws);
+  const double bound = (mx + 1.0) * (double)(dm.N_c / dm.n_min + 2);
+  int e = 0;
+  frexp(bound, &e);                            // bound < 2^e
+  int sh = 60 - e;
+  if (sh > 48) sh = 48;
+  return ldexp(1.0, sh);
+}
+__device__ __forceinline__ long long dp_fix(double s, double sc) {
+  return isfinite(s) ? (long long)__double2ll_rn(s * sc) : DP_NEG;
+}
+
+// one DPP step of the (value, smallest start) maximum within 16-lane rows
+// (an absent candidate is (DP_NEG, INT_MAX) and never wins)
+template <int CTRL>
+__device__ __forceinline__ void dp_step(long long& bv, int& ba) {
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(bv & 0xffffffffll), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(bv >> 32), CTRL, 0xf, 0xf, false);
+  const int a2 = __builtin_amdgcn_update_dpp(0, ba, CTRL, 0xf, 0xf, false);
+  const long long v2 = ((long long)hi << 32) | (long long)(unsigned)lo;
+  const bool better = v2 > bv || (v2 == bv && a2 < ba);
+  bv = better ? v2 : bv;
+  ba = better ? a2 : ba;
+}
+// every lane of a 16-lane row ends with the row's best: lanes ^1, ^2 (quad
+// permutes), then rotations by 4 and 8 within the row
+__device__ __forceinline__ void dp_reduce16(long long& bv, int& ba) {
+  dp_step<0xB1>(bv, ba);     // quad_perm(1, 0, 3, 2)
+  dp_step<0x4E>(bv, ba);     // quad_perm(2, 3, 0, 1)
+  dp_step<0x124>(bv, ba);    // row_ror:4
+  dp_step<0x128>(bv, ba);    // row_ror:8
+}
+
+// F of the ends lo .. hi (inclusive), 256 threads: with n_min >= 16,
+// F[i .. i+15] depend only on F[< i], so wave w owns ends i0 + 4 w .. i0 + 4 w + 3
+// of a step, 16 lanes per end, each lane 8 candidate lengths.  Fr (LDS ring,
+// index position & 255) holds F of positions lo - 128 .. lo - 1 on entry.
+// Backpointer offsets go to Poff for ends >= own_lo; F of positions >= fg_lo
+// to Fg[position - fg_lo].
+__device__ void dp_run(const Dims& dm, const SegWs& ws, double sc, long long* Fr, int64_t lo, int64_t hi,
+                       int64_t own_lo, long long* Fg, int64_t fg_lo) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int st = lane >> 4, sub = lane & 15;
-  if (N <= 0) {
-    if (tid == 0) { slots[0] = 0; *nslots = 0; }
-    return;
-  }
-  Fr[tid] = -INFINITY;
-  __syncthreads();
-  if (tid == 0) { Fr[0] = 0.0; Poff[0] = 0; }
-  __syncthreads();
-  // unconditional loads (row clamped to N) keep the load counter exact
+  // unconditional loads (row clamped to hi) keep the load counter exact
   auto load = [&](int64_t i, double* sv) {
-    const int64_t ic = i <= N ? i : N;
+    const int64_t ic = i <= hi ? i : hi;
     const double2* p = (const double2*)(ws.S + (ic - 1) * BAND + sub * 8);
 #pragma unroll
     for (int k = 0; k < 4; ++k) { const double2 v = p[k]; sv[2 * k] = v.x; sv[2 * k + 1] = v.y; }
@@ -513,30 +581,31 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
   // scores of 4 steps in flight (static register indices: the step loop is unrolled by 4)
   double sv[4][8];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) load(1 + 16 * q + 4 * wave + st, sv[q]);
-  for (int64_t i00 = 1; i00 <= N; i00 += 64) {
+  for (int q = 0; q < 4; ++q) load(lo + 16 * q + 4 * wave + st, sv[q]);
+  for (int64_t i00 = lo; i00 <= hi; i00 += 64) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int64_t i0 = i00 + 16 * q;
-      if (i0 > N) break;
+      if (i0 > hi) break;
       const int64_t i = i0 + 4 * wave + st;
       // all F reads first, then a branch-free (value, smallest start) maximum
-      double Fa[8];
+      long long Fa[8];
       int av[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int len = dm.n_min + sub + 16 * k;
         const int64_t a = i - len;
-        const bool ok = i <= N && len <= dm.n_max && a >= 0;
+        const bool ok = i <= hi && len <= dm.n_max && a >= 0;
         av[k] = ok ? (int)a : 0x7fffffff;
         Fa[k] = Fr[ok ? (int)(a & 255) : 0];
       }
-      double bv = -INFINITY;
+      long long bv = DP_NEG;
       int ba = 0x7fffffff;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const bool ok = av[k] != 0x7fffffff && Fa[k] != -INFINITY;
-        const double v = ok ? Fa[k] + sv[q][k] : -INFINITY;
+        const long long s = dp_fix(sv[q][k], sc);
+        const bool ok = av[k] != 0x7fffffff && Fa[k] != DP_NEG && s != DP_NEG;
+        const long long v = ok ? Fa[k] + s : DP_NEG;
         const int a = ok ? av[k] : 0x7fffffff;
         const bool better = v > bv || (v == bv && a < ba);
         bv = better ? v : bv;
@@ -545,45 +614,277 @@ __global__ __launch_bounds__(256) void k_dp(Dims dm, const float* __restrict__ b
       load(i + 64, sv[q]);                   // the same lane's end four steps later
       dp_reduce16(bv, ba);
       lds_barrier();                         // every end of this step has read its F
-      if (sub == 0 && i <= N) {
+      if (sub == 0 && i <= hi) {
         Fr[i & 255] = bv;
-        Poff[i] = ba != 0x7fffffff ? (uint8_t)(i - ba) : 0;
+        if (i >= own_lo) ws.Poff[i] = ba != 0x7fffffff ? (uint8_t)(i - ba) : 0;
+        if (Fg != nullptr && i >= fg_lo) Fg[i - fg_lo] = bv;
       }
-      lds_barrier();                         // (Poff is only read after the loop's final full barrier)
+      lds_barrier();
     }
   }
-  // terminal relaxation of the last slot's minimum length
-  if (Poff[N] == 0 && wave == 0) {
-    double bv = -INFINITY;
-    int64_t ba = -1;
-    for (int len = 1 + lane; len <= dm.n_max; len += 64) {
-      const int64_t a = N - len;
-      if (a < 0) continue;
-      const double Fa = Fr[a & 255];
-      if (Fa == -INFINITY) continue;
-      dp_better(bv, ba, Fa + slot_score(dm, b, ws, N, len), a);
+}
+
+// Guessed run of chunk c = blockIdx.x: ends c DPC + 1 .. min((c + 1) DPC, N),
+// warmed up from F = 0 at the 128 positions before max(c DPC - DPM, 0) (from
+// the true start F[0] = 0 when that is position 0).
+__global__ __launch_bounds__(256) void k_dp_chunk(Dims dm, SegWs ws) {
+  __shared__ long long Fr[256];
+  const int64_t N = dm.N_c;
+  const int64_t c = blockIdx.x;
+  const int64_t lo = c * DPC + 1, hi = (c + 1) * DPC < N ? (c + 1) * DPC : N;
+  const int64_t margin = dm.dp_serial ? 0 : DPM;
+  const int64_t s = c * DPC - margin > 0 ? c * DPC - margin : 0;
+  const double sc = dp_scale(dm, ws);
+  long long* Fg = ws.Fg + c * (DPC + 128);
+  const int64_t fg_lo = c * DPC - 127;
+  // ring: positions s - 127 .. s (guess 0, or the true start)
+  Fr[threadIdx.x] = s == 0 ? DP_NEG : 0;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (s == 0) Fr[0] = 0;
+    if (c == 0) ws.Poff[0] = 0;
+  }
+  if (threadIdx.x < 128) {                   // window positions the run does not reach
+    const int64_t pos = fg_lo + threadIdx.x;
+    if (pos <= s) Fg[threadIdx.x] = pos < 0 ? DP_NEG : (s == 0 ? (pos == 0 ? 0 : DP_NEG) : 0);
+  }
+  __syncthreads();
+  dp_run(dm, ws, sc, Fr, s + 1, hi, lo, Fg, fg_lo);
+}
+
+// For chunks c >= 1: is Fg[c-1] - Fg[c] one constant over positions
+// c DPC - 127 .. c DPC (all ends of chunk c-1, since DPC >= 128)?
+__global__ __launch_bounds__(128) void k_dp_check(Dims dm, SegWs ws) {
+  __shared__ long long mn[2], mx[2];
+  __shared__ int bad[2];
+  const int64_t c = (int64_t)blockIdx.x + 1;
+  const int t = threadIdx.x, w = t >> 6;
+  const long long a = ws.Fg[(c - 1) * (DPC + 128) + DPC + t];   // position c DPC - 127 + t
+  const long long b = ws.Fg[c * (DPC + 128) + t];
+  const bool ng = a == DP_NEG || b == DP_NEG;
+  long long d = a - b, dn = d, dx = d;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    dn = min(dn, (long long)__shfl_xor(dn, o, 64));
+    dx = max(dx, (long long)__shfl_xor(dx, o, 64));
+  }
+  const bool anyng = __any(ng);
+  if ((t & 63) == 0) { mn[w] = dn; mx[w] = dx; bad[w] = anyng; }
+  __syncthreads();
+  if (t == 0) {
+    const long long n0 = min(mn[0], mn[1]), x0 = max(mx[0], mx[1]);
+    ws.cok[c] = (n0 == x0 && !bad[0] && !bad[1]) ? 1 : 0;
+    ws.cdiff[c] = n0;
+  }
+}
+
+// Chains the chunk offsets, recomputes failing chunks from the true state,
+// then the terminal relaxation (one workgroup).
+__global__ __launch_bounds__(256) void k_dp_fix(Dims dm, const float* __restrict__ b, SegWs ws) {
+  __shared__ long long Fr[256];
+  __shared__ long long red[4];
+  __shared__ int flags[4];
+  __shared__ long long cur;
+  const int64_t N = dm.N_c;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const double sc = dp_scale(dm, ws);
+  const int64_t C = dp_chunks(N);
+  auto Fg = [&](int64_t c) { return ws.Fg + c * (DPC + 128); };
+  long long Dprev = 0;                         // chunk 0 starts at the true F[0] = 0
+  bool dirty = false;                          // chunk c-1 was recomputed: recheck c here
+  int nfix = 0;
+  if (tid == 0) ws.dlt[0] = 0;
+  __shared__ long long tdiff[256];
+  __shared__ int tok[256];
+  for (int64_t c = 1; c < C; ++c) {
+    if ((c - 1) % 256 == 0) {                  // stage the check results of the next 256 chunks
+      __syncthreads();
+      if (c + tid < C) { tok[tid] = ws.cok[c + tid]; tdiff[tid] = ws.cdiff[c + tid]; }
+      __syncthreads();
+    }
+    const int tc = (int)((c - 1) % 256);
+    if (!dirty && tok[tc]) {
+      Dprev += tdiff[tc];
+      if (tid == 0) ws.dlt[c] = Dprev;
+      continue;
+    }
+    // check against the true F of chunk c-1 (Fg + Dprev)
+    long long dlo = LLONG_MAX, dhi = LLONG_MIN;
+    int ng = 0;
+    if (tid < 128) {
+      const long long a = Fg(c - 1)[DPC + tid], g = Fg(c)[tid];
+      ng = a == DP_NEG || g == DP_NEG;
+      const long long d = a + Dprev - g;
+      dlo = d; dhi = d;
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-      const double v2 = __shfl_xor(bv, o, 64);
-      const int64_t a2 = __shfl_xor(ba, o, 64);
-      if (a2 >= 0) dp_better(bv, ba, v2, a2);
+      dlo = min(dlo, (long long)__shfl_xor(dlo, o, 64));
+      dhi = max(dhi, (long long)__shfl_xor(dhi, o, 64));
     }
-    if (lane == 0) { Poff[N] = ba >= 0 ? (uint8_t)(N - ba) : 0; ws.Fdbg[0] = bv; }
-  } else if (tid == 0) {
-    ws.Fdbg[0] = Fr[N & 255];
+    const bool ngw = __any(ng);
+    __syncthreads();
+    if (lane == 0 && wave < 2) { red[wave] = dlo; red[2 + wave] = dhi; flags[wave] = ngw; }
+    __syncthreads();
+    const long long lo2 = min(red[0], red[1]), hi2 = max(red[2], red[3]);
+    if (lo2 == hi2 && !flags[0] && !flags[1]) {
+      Dprev = lo2;
+      dirty = false;
+      if (tid == 0) ws.dlt[c] = Dprev;
+      continue;
+    }
+    // recompute chunk c from the true state; its Fg then holds true values
+    if (tid < 128) {
+      const int64_t pos = c * DPC - 127 + tid;
+      const long long a = Fg(c - 1)[DPC + tid];
+      Fr[pos & 255] = a == DP_NEG ? DP_NEG : a + Dprev;
+    }
+    __syncthreads();
+    const int64_t lo = c * DPC + 1, hi = (c + 1) * DPC < N ? (c + 1) * DPC : N;
+    dp_run(dm, ws, sc, Fr, lo, hi, lo, Fg(c), c * DPC - 127);
+    __threadfence();
+    __syncthreads();
+    Dprev = 0;
+    dirty = true;
+    ++nfix;
+    if (tid == 0) ws.dlt[c] = 0;
   }
+  __threadfence();
+  __syncthreads();
+  // true F at position p (p >= 0)
+  auto Ftrue = [&](int64_t p) -> long long {
+    if (p == 0) return 0;
+    const int64_t c = (p - 1) / DPC;
+    const long long v = Fg(c)[p - (c * DPC - 127)];
+    return v == DP_NEG ? DP_NEG : v + ws.dlt[c];
+  };
+  // terminal relaxation of the last slot's minimum length
+  if (ws.Poff[N] == 0 && wave == 0) {
+    long long bv = DP_NEG;
+    int ba = 0x7fffffff;
+    for (int len = 1 + lane; len <= dm.n_max; len += 64) {
+      const int64_t a = N - len;
+      if (a < 0) continue;
+      const long long Fa = Ftrue(a);
+      if (Fa == DP_NEG) continue;
+      const long long s = dp_fix(slot_score(dm, b, ws, N, len), sc);
+      if (s == DP_NEG) continue;
+      const long long v = Fa + s;
+      if (v > bv || (v == bv && (int)a < ba)) { bv = v; ba = (int)a; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const long long v2 = __shfl_xor(bv, o, 64);
+      const int a2 = __shfl_xor(ba, o, 64);
+      if (v2 > bv || (v2 == bv && a2 < ba)) { bv = v2; ba = a2; }
+    }
+    if (lane == 0) {
+      ws.Poff[N] = ba != 0x7fffffff ? (uint8_t)(N - ba) : 0;
+      cur = bv;
+    }
+  } else if (tid == 0) {
+    cur = Ftrue(N);
+  }
+  __threadfence();
   __syncthreads();
   if (tid == 0) {
-    int J = 0;
-    for (int64_t i = N; i > 0; i -= Poff[i]) {
-      if (Poff[i] == 0) break;
-      ++J;
+    ws.Fdbg[0] = (double)cur / sc;
+    ws.Fdbg[1] = (double)nfix;
+  }
+}
+
+__global__ void k_seg_empty(int32_t* slots, int32_t* nslots) {
+  if (threadIdx.x == 0) { slots[0] = 0; *nslots = 0; }
+}
+
+// ---- backtrack, chunk-parallel ---------------------------------------------
+// The path N = x_0 > x_1 > ... > x_J = 0 follows x_{m+1} = x_m - Poff[x_m]; the
+// slot starts are x_1 .. x_J.  A path node of chunk c (ends c DPC + 1 ..
+// (c + 1) DPC) is entered from the chunk above at one of its 128 top positions
+// (a slot is at most 128 long), so: every chunk walks from each of its 128
+// possible entries down to its exit (the first start <= c DPC, the entry of
+// chunk c - 1), counting the starts it emits; one thread chains the entries
+// from N down; every chunk then re-walks from its true entry and writes its
+// starts at the offset the chain gives.
+__device__ __forceinline__ int bt_stage(const SegWs& ws, int64_t c, int64_t N, uint8_t* P) {
+  // P[k] = Poff[c DPC + 1 + k], k < DPC
+  const int64_t lo = c * DPC + 1;
+  const int n = (int)((c + 1) * DPC < N ? DPC : N - c * DPC);
+  for (int k = threadIdx.x; k < n; k += blockDim.x) P[k] = ws.Poff[lo + k];
+  __syncthreads();
+  return n;
+}
+
+// walk of chunk c from entry position e: (exit position or -1 if the path
+// breaks, starts emitted)
+__device__ __forceinline__ int2 bt_walk(int64_t c, const uint8_t* P, int64_t e) {
+  int64_t p = e;
+  int cnt = 0;
+  while (p > c * DPC) {
+    const int o = P[p - c * DPC - 1];
+    if (o == 0) return make_int2(-1, cnt);
+    p -= o;
+    ++cnt;
+  }
+  return make_int2((int)p, cnt);
+}
+
+// bt_tab[c * 128 + k] = (exit, count) of chunk c from entry (c + 1) DPC - 127 + k
+// (the last chunk: entry N, k = 0)
+__global__ __launch_bounds__(128) void k_bt_walk(Dims dm, SegWs ws) {
+  __shared__ uint8_t P[DPC];
+  const int64_t N = dm.N_c, C = dp_chunks(N);
+  const int64_t c = blockIdx.x;
+  bt_stage(ws, c, N, P);
+  const int k = threadIdx.x;
+  int64_t e = (c + 1) * DPC - 127 + k;
+  if (c == C - 1) {
+    if (k != 0) return;
+    e = N;
+  }
+  ws.bt_tab[c * 128 + k] = e > c * DPC ? bt_walk(c, P, e) : make_int2(-1, 0);
+}
+
+// entries and output offsets of every chunk, J, slots[J] = N (one thread)
+__global__ void k_bt_chain(Dims dm, SegWs ws, int32_t* slots, int32_t* nslots) {
+  if (threadIdx.x != 0) return;
+  const int64_t N = dm.N_c, C = dp_chunks(N);
+  int64_t e = N;
+  int total = 0;
+  for (int64_t c = C - 1; c >= 0; --c) {
+    int k = c == C - 1 ? 0 : (int)(e - ((c + 1) * DPC - 127));
+    if (e <= 0 || k < 0 || k >= 128) {       // the path ended (or broke) above this chunk
+      ws.bt_ent[c] = make_int2(-1, 0);
+      e = -1;
+      continue;
     }
-    int idx = J - 1;
-    for (int64_t i = N; i > 0 && idx >= 0; i -= Poff[i]) slots[idx--] = (int32_t)(i - Poff[i]);
-    slots[J] = (int32_t)N;
-    *nslots = J;
+    const int2 t = ws.bt_tab[c * 128 + k];
+    ws.bt_ent[c] = make_int2((int)e, total);
+    total += t.y;
+    e = t.x;
+  }
+  slots[total] = (int32_t)N;
+  *nslots = total;
+}
+
+// chunk c re-walks from its entry; the m-th start it emits is slots[J - 1 - (offset + m)]
+__global__ __launch_bounds__(64) void k_bt_emit(Dims dm, SegWs ws, int32_t* slots, const int32_t* nslots) {
+  __shared__ uint8_t P[DPC];
+  const int64_t N = dm.N_c;
+  const int64_t c = blockIdx.x;
+  const int2 ent = ws.bt_ent[c];
+  if (ent.x < 0) return;
+  bt_stage(ws, c, N, P);
+  if (threadIdx.x != 0) return;
+  const int J = *nslots;
+  int64_t p = ent.x;
+  int m = ent.y;
+  while (p > c * DPC) {
+    const int o = P[p - c * DPC - 1];
+    if (o == 0) break;
+    p -= o;
+    slots[J - 1 - m] = (int32_t)p;
+    ++m;
   }
 }
 
@@ -607,16 +908,19 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
     hipLaunchKernelGGL(k_dist2, dim3((unsigned)dm.N_c), dim3(BAND), 0, st, dm, ws);
     hipLaunchKernelGGL(k_prefix_sq, dim3(1), dim3(1024), 0, st, dm, ws);
   }
-  const size_t lds = (size_t)dm.N_c + 1;
-  const int use_lds = lds <= 150 * 1024 ? 1 : 0;
-  const size_t dyn = use_lds ? ((lds + 15) & ~(size_t)15) : 0;
-  if (dyn > 0) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_dp, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-    if (e != hipSuccess) return e;
+  if (dm.N_c > 0) {
+    const int64_t C = dp_chunks(dm.N_c);
+    hipLaunchKernelGGL(k_slot_scores, dim3((unsigned)((dm.N_c + SLE - 1) / SLE)), dim3(BAND), 0, st, dm,
+                       (const float*)bscore, ws);
+    hipLaunchKernelGGL(k_dp_chunk, dim3((unsigned)C), dim3(256), 0, st, dm, ws);
+    if (C > 1) hipLaunchKernelGGL(k_dp_check, dim3((unsigned)(C - 1)), dim3(128), 0, st, dm, ws);
+    hipLaunchKernelGGL(k_dp_fix, dim3(1), dim3(256), 0, st, dm, (const float*)bscore, ws);
+    hipLaunchKernelGGL(k_bt_walk, dim3((unsigned)C), dim3(128), 0, st, dm, ws);
+    hipLaunchKernelGGL(k_bt_chain, dim3(1), dim3(64), 0, st, dm, ws, slot_starts, n_slots);
+    hipLaunchKernelGGL(k_bt_emit, dim3((unsigned)C), dim3(64), 0, st, dm, ws, slot_starts, (const int32_t*)n_slots);
+  } else {
+    hipLaunchKernelGGL(k_seg_empty, dim3(1), dim3(64), 0, st, slot_starts, n_slots);
   }
-  if (dm.N_c > 0)
-    hipLaunchKernelGGL(k_slot_scores, dim3((unsigned)dm.N_c), dim3(BAND), 0, st, dm, (const float*)bscore, ws);
-  hipLaunchKernelGGL(k_dp, dim3(1), dim3(256), dyn, st, dm, (const float*)bscore, ws, slot_starts, n_slots, use_lds);
   return hipGetLastError();
 }
 

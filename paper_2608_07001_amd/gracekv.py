@@ -41,6 +41,7 @@ class Config(ctypes.Structure):
                 ("lambda_graph", ctypes.c_float), ("alpha_floor", ctypes.c_float), ("flags", ctypes.c_int32)]
 
 FLAG_PRUNE = 1
+FLAG_DP_SERIAL = 2
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",

@@ -145,3 +145,17 @@ def test_sampled_curvature_window_at_full_size(runs):
     err = float(np.abs(got - kap).max())
     print(f"full size curvature window [{s}, {e}): max abs err {err:.3e}")
     assert err < 1e-4
+
+
+def test_parallel_dp_equals_serial_dp_at_full_size(runs):
+    # the chunk-parallel recurrence against the one that runs every chunk from
+    # the true state: the same partition, slot for slot
+    case, pr, fu = runs
+    cfg = H.make_cfg(SH, flags=gk.FLAG_PRUNE | gk.FLAG_DP_SERIAL)
+    buf = gk.allocate(cfg)
+    gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
+               buf.seg_ws)
+    torch.cuda.synchronize()
+    J = int(pr.n_slots.item())
+    assert int(buf.n_slots.item()) == J
+    assert torch.equal(buf.slot_starts[:J + 1].cpu(), pr.slot_starts[:J + 1].cpu())

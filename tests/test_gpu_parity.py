@@ -135,6 +135,28 @@ def test_tiny_full_pipeline_with_segmentation():
     assert g["slots"] == o.slot_starts
 
 
+@pytest.mark.parametrize("serial", [False, True])
+def test_segmentation_across_dp_chunks(serial):
+    # 4968 compressible positions: four full chunks of the parallel recurrence
+    # and a ragged fifth, against the oracle's literal DP
+    from paper_2608_07001_amd import gracekv as gk
+    sh = small_shape("seg-chunks", L=1, G=1, H=4, d=64, N_ctx=5000, W=16, x=8.0, n_segments=40)
+    case = make_case(sh, 5, with_hidden=True)
+    cfg = H.make_cfg(sh, flags=gk.FLAG_DP_SERIAL if serial else 0)
+    buf = gk.allocate(cfg)
+    dev = H.to_dev(case)
+    gk.segment(cfg, dev["hidden"], dev["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
+               buf.seg_ws)
+    torch.cuda.synchronize()
+    J = int(buf.n_slots.item())
+    got = buf.slot_starts[:J].cpu().tolist()
+    N_c = buf.plan.N_c
+    seg = O.segment(H.np32(case["hidden"]).astype(np.float64), H.np32(case["surprisal"]), N_c)
+    print(f"{N_c} positions: J gpu {J} oracle {len(seg.slot_starts)}")
+    assert got == seg.slot_starts
+    assert int(buf.slot_starts[J].item()) == N_c
+
+
 def test_fullkv_recovery_on_gpu():
     # x = 1: the packed cache is the original context cache, entry by entry
     sh = small_shape(L=2, G=2, H=4, d=64, N_ctx=600, W=16, x=1.0, n_segments=5)
