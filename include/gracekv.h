@@ -58,7 +58,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 4
+#define GRACEKV_ABI_VERSION 5
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -107,7 +107,7 @@ typedef struct {
          off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
          off_tok_R, off_tok_A, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
          off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate,
-         off_work, off_wctr;
+         off_work, off_wctr, off_proto, off_proto_logm;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
 } gracekv_plan;
 
@@ -169,7 +169,10 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  *              Per unit: node count (int32), D_drop of the root (fp32).  Token
  *              values R^tok [L*G][N_c] fp32; per (l,g) row statistics of the
  *              relevance softmax and the probe shifts m_q and Z_q(C); a copy of
- *              the slot partition (read by score, select and pack).
+ *              the slot partition (read by score, select and pack); per unit the
+ *              root prototype (k~ then v~, d values each, rounded to cfg->dtype)
+ *              and its log m_eff (fp32), which pack copies for a root on the
+ *              frontier.
  *   ws         unused (pass NULL, 0); reserved.
  * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
  * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops
@@ -216,8 +219,9 @@ gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void
                             int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
 
 /* Layout check of the matrix-core instructions used by the kernels: computes
- * a 16x16 product with the bf16 (which = 1) or fp32 (which = 0) MFMA path
- * from fixed inputs and copies it to host_out[256] (synchronous). */
+ * a 16x16 product from fixed inputs with the fp32 16x16x4 (which = 0), the
+ * bf16 16x16x16 (which = 1) or the bf16 16x16x32 (which = 2) instruction and
+ * copies it to host_out[256] (synchronous). */
 gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out);
 
 #ifdef __cplusplus

@@ -59,6 +59,8 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.omega = (float*)(b + p.off_omega);
   v.status = (int32_t*)(b + p.off_status);
   v.slots = (int32_t*)(b + p.off_slots);
+  v.proto = (void*)(b + p.off_proto);
+  v.proto_logm = (float*)(b + p.off_proto_logm);
   v.nslots = (int32_t*)(b + p.off_nslots);
   v.theta = (uint64_t*)(b + p.off_theta);
   v.selstate = (void*)(b + p.off_selstate);
@@ -185,6 +187,8 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_selstate, selstate_bytes());
   put(p->off_work, UC * 4);
   put(p->off_wctr, 16);
+  put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));
+  put(p->off_proto_logm, UC * 4);
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
   p->sel_ws_bytes = select_ws_bytes(dm);
@@ -295,7 +299,7 @@ gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* 
 }
 
 gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out) {
-  if (!host_out || (which != 0 && which != 1)) return GRACEKV_ERR_INVALID_ARG;
+  if (!host_out || which < 0 || which > 2) return GRACEKV_ERR_INVALID_ARG;
   return hip_status(selftest_mfma(which, host_out));
 }
 

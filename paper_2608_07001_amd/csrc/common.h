@@ -64,6 +64,8 @@ struct TreeView {
   void* selstate;       // radix-select state of that bound
   int32_t* work;        // [L*G*J_cap] units to refine
   int32_t* wctr;        // [4] list length, next item
+  void* proto;          // [unit_cap][2][d] root prototype (k~, v~) of each unit, cache dtype
+  float* proto_logm;    // [unit_cap] log m_eff of the root
 };
 
 // Refinement modes (the roots come from the root kernel): FULL refines every
@@ -189,6 +191,16 @@ __device__ __forceinline__ f32x4 mfma_bf16_16x16x16(s16x4 a, s16x4 b, f32x4 c) {
 __device__ __forceinline__ f32x4 mfma_f32_16x16x4(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
+// gfx950 16x16x32 bf16: lane l supplies A[l%16][8*(l/16) .. +7] and
+// B[l%16][8*(l/16) .. +7] (eight bf16, low half of each 32-bit word first);
+// output layout as above.  Twice the k of the 16x16x16 form per instruction.
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ s16x8 pk8(uint4 v) { return __builtin_bit_cast(s16x8, v); }
+__device__ __forceinline__ f32x4 mfma_bf16_16x16x32(s16x8 a, s16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
 
 // ---- launchers (each defined in its own translation unit) -----------------
 hipError_t launch_rowstats(const Dims& dm, const void* K, const void* Q, const TreeView& tv, float4* partial,
@@ -197,6 +209,10 @@ hipError_t launch_root(const Dims& dm, const void* K, const void* V, const void*
                        const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const TreeView& tv,
                        hipStream_t st);
 int root_lds_bytes(const Dims& dm);
+hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const void* Q, const float* cosT,
+                            const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const TreeView& tv,
+                            hipStream_t st);
+int root_bf16_lds_bytes(int d);
 hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
                         const float* kappa, const TreeView& tv, hipStream_t st);

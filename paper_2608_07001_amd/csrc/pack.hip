@@ -5,7 +5,8 @@
 // frontier node -- a singleton as its original K/V with its position and
 // log-multiplicity 0, any other node as its prototype (k~, v~ rounded to the
 // cache dtype, p_v, log m_eff; App. A.3) -- followed by the r recent-window
-// tokens.  Offsets are a CSR over (l, g).
+// tokens.  A root's prototype is the one the tree build stored; deeper nodes
+// are recomputed from K and V.  Offsets are a CSR over (l, g).
 #include "common.h"
 
 namespace gkv {
@@ -133,6 +134,15 @@ __global__ __launch_bounds__(64) void k_pack_emit(Dims dm, const T* __restrict__
         Vo[o * D + c] = Vp[(int64_t)a * D + c];
       }
       if (lane == 0) { po[o] = a; lo[o] = 0.f; }
+      continue;
+    }
+    if (i == 0) {                             // the root: the prototype the build stored
+      const T* pr = (const T*)tv.proto + u * 2 * D;
+      for (int c = lane; c < D; c += 64) {
+        Ko[o * D + c] = pr[c];
+        Vo[o * D + c] = pr[D + c];
+      }
+      if (lane == 0) { po[o] = round_half_even_mid(a, a + n); lo[o] = tv.proto_logm[u]; }
       continue;
     }
     float sk[DL], srv[DL], sv[DL];

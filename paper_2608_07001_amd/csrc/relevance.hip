@@ -207,7 +207,15 @@ __global__ void k_selftest_mfma(int which, float* out) {
   const int lane = threadIdx.x;
   // A[i][k] = (i - 3k) / 8, B[j][k] = (2j + k) / 16 -- exact in bf16 for 0 <= i, j, k < 16
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (which == 1) {
+  if (which == 2) {                     // 16x16x32: k < 32
+    s16x8 a, b;
+    for (int q = 0; q < 8; ++q) {
+      int k = 8 * (lane >> 4) + q;
+      a[q] = (short)f32_to_bf16_rne((float)((lane & 15) - 3 * k) / 8.f);
+      b[q] = (short)f32_to_bf16_rne((float)(2 * (lane & 15) + k) / 16.f);
+    }
+    acc = mfma_bf16_16x16x32(a, b, acc);
+  } else if (which == 1) {
     s16x4 a, b;
     for (int q = 0; q < 4; ++q) {
       int k = 4 * (lane >> 4) + q;

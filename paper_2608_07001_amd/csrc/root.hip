@@ -57,7 +57,7 @@ struct RootLds {
 };
 
 int root_lds_bytes(const Dims& dm) {
-  if (dm.dtype == GRACEKV_BF16) return dm.d == 128 ? RootLds<uint16_t, 128>::bytes : RootLds<uint16_t, 64>::bytes;
+  if (dm.dtype == GRACEKV_BF16) return root_bf16_lds_bytes(dm.d);
   return dm.d == 128 ? RootLds<float, 128>::bytes : RootLds<float, 64>::bytes;
 }
 
@@ -481,6 +481,11 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
       if (lane == 0) { sRed[0] = sr; sRed[1] = sa; sRed[2] = me; }
     }
     __syncthreads();
+    if (tid < 2 * D) {                        // the unit's root prototype, as pack writes it
+      T* pr = (T*)tv.proto + unit * 2 * D;
+      stf(pr, tid, tid < D ? sKt[tid] : sVv[tid - D]);
+    }
+    if (tid == 0) tv.proto_logm[unit] = logf(sRed[2]);
 
     // ---- distortion of the root: probes of wave w (head slot 0 is in qr[0]) ----
     {
@@ -577,7 +582,7 @@ hipError_t launch_root(const Dims& dm, const void* K, const void* V, const void*
                        slot_starts, n_slots, tv);                                                          \
   } while (0)
   if (dm.dtype == GRACEKV_BF16) {
-    if (dm.d == 128) GKV_LAUNCH_ROOT(uint16_t, 128); else GKV_LAUNCH_ROOT(uint16_t, 64);
+    return launch_root_bf16(dm, K, V, Q, cosT, sinT, slot_starts, n_slots, tv, st);
   } else {
     if (dm.d != 64) return hipErrorInvalidValue;   // fp32 caches take d = 64 only
     GKV_LAUNCH_ROOT(float, 64);

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 4          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 5          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
 
@@ -48,7 +48,8 @@ _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_n
          "off_node_cut", "off_node_D", "off_node_R", "off_sp_U", "off_sp_E", "off_sp_cost", "off_sp_exec",
          "off_unit_nn", "off_unit_Ddrop", "off_add_U", "off_add_E", "off_add_exec", "off_tok_R",
          "off_tok_A", "off_row_stats", "off_probe_m", "off_probe_ZC", "off_lg_S", "off_omega", "off_status", "off_slots",
-         "off_nslots", "off_partial", "off_theta", "off_selstate", "off_work", "off_wctr"]
+         "off_nslots", "off_partial", "off_theta", "off_selstate", "off_work", "off_wctr", "off_proto",
+         "off_proto_logm"]
 
 
 class Plan(ctypes.Structure):

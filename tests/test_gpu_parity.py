@@ -40,11 +40,11 @@ def _partition(N, lens=(16, 40, 64, 100, 128, 23, 77)):
 def test_mfma_layout_bf16_and_fp32():
     from paper_2608_07001_amd import gracekv as gk
     i = np.arange(16)[:, None]
-    k = np.arange(16)[None, :]
-    A = (i - 3 * k) / 8.0
-    B = (2 * i + k) / 16.0
-    want = A @ B.T
-    for which in (0, 1):
+    for which, nk in ((0, 16), (1, 16), (2, 32)):
+        k = np.arange(nk)[None, :]
+        A = (i - 3 * k) / 8.0
+        B = (2 * i + k) / 16.0
+        want = A @ B.T
         got = gk.selftest_mfma(which).numpy()
         assert np.array_equal(got, want.astype(np.float32)), which
 
