@@ -65,7 +65,7 @@ struct RefLds {
   static constexpr int oNE = oNU + 256 * 4;               // uint64
   static constexpr int oNch = oNE + 256 * 8;              // uint8
   static constexpr int oNk = oNch + 256;
-  static constexpr int oKt = oNk + 256;                   // [CC][KTS] mean k° -> k~; then D_q contributions [CC][WMAX]
+  static constexpr int oKt = oNk + 256;                   // [CC][KTS] mean k° -> k~; then per-wave D sums [CC][4]
   static constexpr int oVv = oKt + CC * KTS * 4;          // [CC][D] v~
   static constexpr int oZt = oVv + CC * D * 4;            // [CC][WMAX] z_{q,c}
   static constexpr int oCs = oZt + CC * WMAX * 4;         // [5][CC] n, sum R, mean ||k||, m_eff, D
@@ -101,25 +101,23 @@ struct Ref {
   __device__ float* crow(int row) { return cs + row * CC; }
 };
 
-__device__ __forceinline__ uint32_t bf16_bits_fin(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-// x = hi + mid + lo, each a bf16 (the remainders are exact in fp32), packed
-// two per 32-bit word as the matrix-core operands want them
+// x = hi + mid + lo exactly, each a bf16 (hi: top 8 significant bits by
+// truncation, mid: the next 8, lo: the rest), packed two per 32-bit word as
+// the matrix-core operands want them
 __device__ __forceinline__ void split3x4(const float* x, u32x2& hi, u32x2& mid, u32x2& lo) {
   uint32_t h[4], m[4], l[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    h[r] = bf16_bits_fin(x[r]);
-    const float r1 = x[r] - __uint_as_float(h[r] << 16);
-    m[r] = bf16_bits_fin(r1);
-    const float r2 = r1 - __uint_as_float(m[r] << 16);
-    l[r] = bf16_bits_fin(r2);
+    h[r] = __float_as_uint(x[r]) & 0xffff0000u;
+    const float r1 = x[r] - __uint_as_float(h[r]);
+    m[r] = __float_as_uint(r1) & 0xffff0000u;
+    l[r] = __float_as_uint(r1 - __uint_as_float(m[r]));
   }
-  hi.x = h[0] | (h[1] << 16); hi.y = h[2] | (h[3] << 16);
-  mid.x = m[0] | (m[1] << 16); mid.y = m[2] | (m[3] << 16);
-  lo.x = l[0] | (l[1] << 16); lo.y = l[2] | (l[3] << 16);
+#define GKV_HI2(a, b) __builtin_amdgcn_perm((b), (a), 0x07060302u)
+  hi.x = GKV_HI2(h[0], h[1]); hi.y = GKV_HI2(h[2], h[3]);
+  mid.x = GKV_HI2(m[0], m[1]); mid.y = GKV_HI2(m[2], m[3]);
+  lo.x = GKV_HI2(l[0], l[1]); lo.y = GKV_HI2(l[2], l[3]);
+#undef GKV_HI2
 }
 __device__ __forceinline__ s16x4 as_op(u32x2 v) { return __builtin_bit_cast(s16x4, v); }
 
@@ -209,8 +207,30 @@ __device__ void proto_keys(Ref<T, D>& U, const Dims& dm, int64_t a0, int a, int 
                            const int* XR, int nr, const float* __restrict__ cosT, const float* __restrict__ sinT) {
   using Lay = RefLds<T, D>;
   constexpr int H2 = D / 2;
+  constexpr int KPW = (CC + NWV - 1) / NWV;   // children per wave
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int k = wave; k < nl + nr; k += NWV) {
+  const int i = lane < H2 ? lane : 0;         // the lane's rotation pair (i, i + H2)
+  // rotation rows of the wave's children, all loads in flight together
+  float cc[KPW], sn[KPW];
+#pragma unroll
+  for (int m = 0; m < KPW; ++m) {
+    const int k = wave + NWV * m;
+    cc[m] = 1.f;
+    sn[m] = 0.f;
+    if (k < nl + nr) {
+      const bool pre = k < nl;
+      const int c = pre ? k : k - nl;
+      const int x0 = pre ? a : XR[c];
+      const int x1 = pre ? XL[c] : b;
+      const int64_t p = round_half_even_mid((int)(a0 + x0), (int)(a0 + x1));
+      cc[m] = cosT[p * H2 + i];
+      sn[m] = sinT[p * H2 + i];
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < KPW; ++m) {
+    const int k = wave + NWV * m;
+    if (k >= nl + nr) break;
     const bool pre = k < nl;
     const int c = pre ? k : k - nl;
     const int gc = pre ? c : CM + c;
@@ -218,19 +238,15 @@ __device__ void proto_keys(Ref<T, D>& U, const Dims& dm, int64_t a0, int a, int 
     if (nch < 2) continue;
     float* kt = U.Kt + gc * Lay::KTS;
     float ss = 0.f;
-    for (int i = lane; i < D; i += 64) ss += kt[i] * kt[i];
-    ss = wave_sum(ss);
-    const int x0 = pre ? a : XR[c];
-    const int x1 = pre ? XL[c] : b;
-    const int64_t p = round_half_even_mid((int)(a0 + x0), (int)(a0 + x1));
+    for (int d = lane; d < D; d += 64) ss += kt[d] * kt[d];
+    ss = wave_sum_dpp(ss);
     const float coh = sqrtf(ss) / (U.crow(2)[gc] + dm.eps);
     const float me = fminf(fmaxf((float)nch * coh * coh, 1.0f), (float)nch);
     if (lane == 0) U.crow(3)[gc] = me;
-    for (int i = lane; i < H2; i += 64) {
-      const float cc = cosT[p * H2 + i], sn = sinT[p * H2 + i];
+    if (lane < H2) {
       const float m1 = kt[i], m2 = kt[i + H2];
-      kt[i] = m1 * cc - m2 * sn;
-      kt[i + H2] = m2 * cc + m1 * sn;
+      kt[i] = m1 * cc[m] - m2 * sn[m];
+      kt[i + H2] = m2 * cc[m] + m1 * sn[m];
     }
   }
 }
@@ -300,18 +316,21 @@ __device__ __forceinline__ void block_k(const T* __restrict__ Kp, int n, int blk
 }
 
 // e_{q,t} for the 16 tokens of block blk and the lane's probe: transposed
-// logits, lane holds tokens 16 blk + 4 g4 + r.
+// logits, lane holds tokens 16 blk + 4 g4 + r; e = 2^(l sc2 - mq2) with the
+// logit scale and the probe shift in base-2 units.  The lane's key and probe
+// registers cover dims QE g4 .. QE g4 + QE - 1, eight per 16x16x32 step.
 template <typename T, int D, int QW>
-__device__ __forceinline__ void block_e(const uint32_t* kreg, int n, int blk, const uint32_t* qreg, float mq,
-                                        bool pok, float scale, float* ev) {
+__device__ __forceinline__ void block_e(const uint32_t* kreg, int n, int blk, const uint32_t* qreg, float mq2,
+                                        bool pok, float sc2, float* ev) {
   constexpr bool BF = sizeof(T) == 2;
   constexpr int QE = D / 4;
   const int lane = threadIdx.x & 63, g4 = lane >> 4;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   if constexpr (BF) {
 #pragma unroll
-    for (int s = 0; s < QE / 4; ++s)
-      acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qreg[2 * s], qreg[2 * s + 1]), acc);
+    for (int s = 0; s < QE / 8; ++s)
+      acc = mfma_bf16_16x16x32(pk8(make_uint4(kreg[4 * s], kreg[4 * s + 1], kreg[4 * s + 2], kreg[4 * s + 3])),
+                               pk8(make_uint4(qreg[4 * s], qreg[4 * s + 1], qreg[4 * s + 2], qreg[4 * s + 3])), acc);
   } else {
 #pragma unroll
     for (int s = 0; s < QE; ++s) acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qreg[s]), acc);
@@ -319,16 +338,17 @@ __device__ __forceinline__ void block_e(const uint32_t* kreg, int n, int blk, co
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int t = 16 * blk + 4 * g4 + r;
-    ev[r] = (pok && t < n) ? fexp(acc[r] * scale - mq) : 0.f;
+    ev[r] = (pok && t < n) ? __builtin_amdgcn_exp2f(acc[r] * sc2 - mq2) : 0.f;
   }
 }
 
 // Distortion sweeps: wave (pt, dir) accumulates M^T (values x its 16 probes)
-// over the direction's children and writes (Z / Z_q(C)) D_q per child.
+// over the direction's children and sums (Z / Z_q(C)) D_q over its probes per
+// child, scoring each child when the sweep reaches its cut.
 template <typename T, int D, int QW>
 __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__ Kp, int n, int a, int b,
-                             const int* XL, int nl, const int* XR, int nr, const uint32_t* qreg, int pt, float mq,
-                             float zc, float scale) {
+                             const int* XL, int nl, const int* XR, int nr, const uint32_t* qreg, int pt, float mq2,
+                             float zc, float sc2) {
   using Lay = RefLds<T, D>;
   constexpr bool BF = Lay::BF;
   constexpr int DT = D / 16;
@@ -351,6 +371,36 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
   const int lastblk = (n - 1) >> 4;
   block_k<T, D, QW>(Kp, n, prefix ? (a >> 4) : ((b - 1) >> 4), kpre);   // the sweep's first block
   int cur = prefix ? a : b;
+  // scores child gc (prefix or suffix) from M and Z: (Z / Z_q(C)) D_q summed over the wave's probes
+  auto score_child = [&](int gc) {
+    float Zs = Z;
+    Zs += __shfl_xor(Zs, 16, 64);
+    Zs += __shfl_xor(Zs, 32, 64);
+    const float z = pok ? U.Zt[gc * WMAX + q] : 0.f;
+    const float* vt = U.Vv + gc * D + 4 * g4;
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const float4 v4 = *(const float4*)(vt + 16 * dt);
+      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float Mv = M[dt][r];
+        const float df = Mv - z * vv[r];
+        s1 += df * df;
+        s2 += Mv * Mv;
+      }
+    }
+    s1 += __shfl_xor(s1, 16, 64);
+    s1 += __shfl_xor(s1, 32, 64);
+    s2 += __shfl_xor(s2, 16, 64);
+    s2 += __shfl_xor(s2, 32, 64);
+    const float dz = Zs - z;
+    const float Dq = dm.lam_Z * dz * dz / (Zs * Zs + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
+    // sum over the wave's 16 probes (row 0 of the wave)
+    const float con = row_sum16((g4 == 0 && pok) ? (Zs / zc) * Dq : 0.f);
+    if (lane == 0) U.Con[gc * 4 + pt] = con;
+  };
   for (int k = 0; k < nx; ++k) {
     const int c = prefix ? k : nx - 1 - k;
     const int x = prefix ? XL[c] : XR[c];
@@ -368,7 +418,7 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
         int nb = prefix ? blk + 1 : blk - 1;
         nb = nb < 0 ? 0 : (nb > lastblk ? lastblk : nb);
         block_k<T, D, QW>(Kp, n, nb, kpre);
-        block_e<T, D, QW>(kreg, n, blk, qreg, mq, pok, scale, ev);
+        block_e<T, D, QW>(kreg, n, blk, qreg, mq2, pok, sc2, ev);
         if constexpr (BF) {
           split3x4(ev, eh, em, el);
 #pragma unroll
@@ -417,35 +467,8 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
       }
       if (prefix) cur = hi; else cur = lo;
     }
-    // child [a, x) or [x, b): D_q of the wave's probes
     const int gc = prefix ? c : CM + c;
-    if ((int)U.crow(0)[gc] >= 2) {
-      float Zs = Z;
-      Zs += __shfl_xor(Zs, 16, 64);
-      Zs += __shfl_xor(Zs, 32, 64);
-      const float z = pok ? U.Zt[gc * WMAX + q] : 0.f;
-      const float* vt = U.Vv + gc * D + 4 * g4;
-      float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const float4 v4 = *(const float4*)(vt + 16 * dt);
-        const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float Mv = M[dt][r];
-          const float df = Mv - z * vv[r];
-          s1 += df * df;
-          s2 += Mv * Mv;
-        }
-      }
-      s1 += __shfl_xor(s1, 16, 64);
-      s1 += __shfl_xor(s1, 32, 64);
-      s2 += __shfl_xor(s2, 16, 64);
-      s2 += __shfl_xor(s2, 32, 64);
-      const float dz = Zs - z;
-      const float Dq = dm.lam_Z * dz * dz / (Zs * Zs + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
-      if (g4 == 0 && pok) U.Con[gc * WMAX + q] = (Zs / zc) * Dq;
-    }
+    if ((int)U.crow(0)[gc] >= 2) score_child(gc);
   }
 }
 
@@ -520,6 +543,18 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
       if (!__syncthreads_or(any)) continue;
     }
 
+    // probe quarter rows of the wave's tile (probe q: window query q of head q mod |H(g)|)
+    uint32_t qreg[QW];
+    {
+      const int q = 16 * pt + i16;
+      const int uq = q < dm.W ? q : 0;
+      const uint4* q4 = (const uint4*)(Qp + ((int64_t)(uq % dm.hpg) * dm.W + uq) * D + QE * g4);
+#pragma unroll
+      for (int h = 0; h < QW / 4; ++h) {
+        const uint4 v = q4[h];
+        qreg[4 * h] = v.x; qreg[4 * h + 1] = v.y; qreg[4 * h + 2] = v.z; qreg[4 * h + 3] = v.w;
+      }
+    }
     // ---- staging ----
     {
       // k° = RoPE^{-1}(k): item (token, 8-dim chunk of the first half) also
@@ -607,18 +642,6 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
         U.Zc[tid] = tv.probe_ZC[(int64_t)lg * dm.W + tid];
       }
     }
-    // probe quarter rows of the wave's tile (probe q: window query q of head q mod |H(g)|)
-    uint32_t qreg[QW];
-    {
-      const int q = 16 * pt + i16;
-      const int uq = q < dm.W ? q : 0;
-      const uint4* q4 = (const uint4*)(Qp + ((int64_t)(uq % dm.hpg) * dm.W + uq) * D + QE * g4);
-#pragma unroll
-      for (int h = 0; h < QW / 4; ++h) {
-        const uint4 v = q4[h];
-        qreg[4 * h] = v.x; qreg[4 * h + 1] = v.y; qreg[4 * h + 2] = v.z; qreg[4 * h + 3] = v.w;
-      }
-    }
     __syncthreads();
     float mq = 0.f, zc = 1.f;
     if (16 * pt + i16 < dm.W) { mq = U.Mq[16 * pt + i16]; zc = U.Zc[16 * pt + i16]; }
@@ -658,9 +681,15 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
         const int t = a + tid;                     // curvature position t -> cut t + 1
         const float kt = U.Kap[t];
         int rank = 0;
-        for (int t2 = a; t2 <= b - 2; ++t2) {
-          const float k2 = U.Kap[t2];
-          rank += (k2 > kt) || (k2 == kt && t2 < t);
+        // positions a .. b - 2, read four at a time (all lanes read the same words)
+        for (int t4 = a & ~3; t4 <= b - 2; t4 += 4) {
+          const float4 k4 = *(const float4*)(U.Kap + t4);
+          const float kk[4] = {k4.x, k4.y, k4.z, k4.w};
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const int t2 = t4 + jj;
+            rank += (t2 >= a && t2 <= b - 2) && ((kk[jj] > kt) || (kk[jj] == kt && t2 < t));
+          }
         }
         if (rank < dm.k_curv) U.flag[t + 1 - a] = 1;
       }
@@ -736,14 +765,15 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
       __syncthreads();
       proto_attention<T, D, QW>(U, dm, nl, nr, qreg, pt, scale);
       __syncthreads();
-      probe_sweeps<T, D, QW>(U, dm, Kp, n, a, b, XL, nl, XR, nr, qreg, pt, mq, zc, scale);
+      probe_sweeps<T, D, QW>(U, dm, Kp, n, a, b, XL, nl, XR, nr, qreg, pt, mq * 1.44269504088896341f, zc,
+                             scale * 1.44269504088896341f);
       __syncthreads();
       // D of each child: mean over probes (fixed order)
       if (tid < nl + nr) {
         const int gc = tid < nl ? tid : CM + (tid - nl);
         float acc = 0.f;
         if ((int)U.crow(0)[gc] >= 2) {
-          for (int qq = 0; qq < dm.W; ++qq) acc += U.Con[gc * WMAX + qq];
+          for (int p4 = 0; p4 < 4 && 16 * p4 < dm.W; ++p4) acc += U.Con[gc * 4 + p4];
           acc /= (float)dm.W;
         }
         U.crow(4)[gc] = acc;

@@ -142,6 +142,17 @@ __device__ __forceinline__ float row_sum16(float v) {
   return v;
 }
 
+// Sum over the wave, returned to every lane: 16-lane row sums by DPP, then the
+// four row results read as scalars.
+__device__ __forceinline__ float wave_sum_dpp(float v) {
+  v = row_sum16(v);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (r0 + r1) + (r2 + r3);
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll

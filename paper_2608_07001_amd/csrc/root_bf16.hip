@@ -401,9 +401,9 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
         tv.tok_A[(int64_t)lg * dm.N_c + a0 + tid] = A;
       }
       if (tid < 32 * nb) { sR[tid] = R; sA[tid] = A; }
-      R = wave_sum(R);
-      A = wave_sum(A);
-      kn = wave_sum(kn);
+      R = wave_sum_dpp(R);
+      A = wave_sum_dpp(A);
+      kn = wave_sum_dpp(kn);
       if (lane == 0) { sSum[4 * w] = R; sSum[4 * w + 1] = A; sSum[4 * w + 2] = kn; }
     }
     __syncthreads();                          // B: token values and their sums in LDS
@@ -455,7 +455,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
         m *= inv;
         ss += m * m;
       }
-      ss = wave_sum(ss);
+      ss = wave_sum_dpp(ss);
       const float coh = sqrtf(ss) / (skn * inv + dm.eps);
       const float me = fminf(fmaxf((float)n * coh * coh, 1.0f), (float)n);
       if (tid == 0) tv.proto_logm[unit] = logf(me);
