@@ -11,9 +11,10 @@
 //   sum_{t in C} s_t = sum_r exp(m_C - m_V) Z_C / Z_V.
 //
 // Pass 1: grid (chunks of T, L*G, row groups of 256).  Each workgroup stages
-// 64-token sub-chunks of K in LDS (16-byte loads) and forms transposed 16x16
-// logit tiles on the matrix cores (tokens x rows; bf16 inputs give exact
-// products, fp32 accumulation), so each lane holds 4 tokens of one row.  A
+// 64-token sub-chunks of K in LDS (16-byte loads, the next sub-chunk in flight
+// while the current one is used) and forms transposed 16x16 logit tiles on the
+// matrix cores (tokens x rows, 16x16x32 steps for bf16; exact products, fp32
+// accumulation), so each lane holds 4 tokens of one row.  A
 // token t < N_c is in both C and V(u); the lane keeps one online (max,
 // sum-exp) pair over C and one over the visible tail [N_c, N_ctx + u], merged
 // into V afterwards.  Pass 2 (combine): per (l, g), merge the chunk partials
@@ -77,15 +78,28 @@ __global__ __launch_bounds__(256) void k_rowstats(Dims dm, const T* __restrict__
 #pragma unroll
   for (int k = 0; k < 4; ++k) { mC[k] = -INFINITY; zC[k] = 0.f; mT[k] = -INFINITY; zT[k] = 0.f; }
 
-  for (int64_t s0 = t_begin; s0 < t_end; s0 += RS_SUB) {
-    __syncthreads();
-    for (int e = tid; e < RS_SUB * (D / CH); e += 256) {      // stage K[s0 .. s0+SUB), zero past the chunk
+  // the next sub-chunk is loaded into registers while the current one is used
+  constexpr int NLD = RS_SUB * (D / CH) / 256;    // 16-byte loads per thread per sub-chunk
+  uint4 pre[NLD];
+  auto load_sub = [&](int64_t s0) {
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {
+      const int e = tid + 256 * q;
       const int tr = e / (D / CH), c = (e % (D / CH)) * CH;
       const int64_t t = s0 + tr;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (t < t_end) v = *(const uint4*)(Kp + t * D + c);
-      *(uint4*)(sK + tr * LDK + c) = v;
+      pre[q] = t < t_end ? *(const uint4*)(Kp + t * D + c) : make_uint4(0, 0, 0, 0);
     }
+  };
+  load_sub(t_begin);
+  for (int64_t s0 = t_begin; s0 < t_end; s0 += RS_SUB) {
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {              // stage K[s0 .. s0+SUB), zero past the chunk
+      const int e = tid + 256 * q;
+      const int tr = e / (D / CH), c = (e % (D / CH)) * CH;
+      *(uint4*)(sK + tr * LDK + c) = pre[q];
+    }
+    if (s0 + RS_SUB < t_end) load_sub(s0 + RS_SUB);
     __syncthreads();
     const bool allC = s0 + RS_SUB <= dm.N_c && s0 + RS_SUB <= t_end;
 #pragma unroll
@@ -102,10 +116,12 @@ __global__ __launch_bounds__(256) void k_rowstats(Dims dm, const T* __restrict__
         if (!tile_ok[k]) continue;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
         if constexpr (BF) {
+          // dims QE g4 + 8 s .. + 7 of the lane's token and row per 16x16x32 step
 #pragma unroll
-          for (int s = 0; s < QE / 4; ++s) {
-            acc = mfma_bf16_16x16x16(pk4(kreg[2 * s], kreg[2 * s + 1]), pk4(qreg[k][2 * s], qreg[k][2 * s + 1]), acc);
-          }
+          for (int s = 0; s < QE / 8; ++s)
+            acc = mfma_bf16_16x16x32(
+                pk8(make_uint4(kreg[4 * s], kreg[4 * s + 1], kreg[4 * s + 2], kreg[4 * s + 3])),
+                pk8(make_uint4(qreg[k][4 * s], qreg[k][4 * s + 1], qreg[k][4 * s + 2], qreg[k][4 * s + 3])), acc);
         } else {
 #pragma unroll
           for (int s = 0; s < QE; ++s) acc = mfma_f32_16x16x4(__uint_as_float(kreg[s]), __uint_as_float(qreg[k][s]), acc);
