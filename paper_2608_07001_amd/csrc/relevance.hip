@@ -165,6 +165,145 @@ __global__ __launch_bounds__(256) void k_rowstats(Dims dm, const T* __restrict__
   }
 }
 
+// bf16 keys: 16x16x32 steps with the operands held as 16-byte register
+// tuples (no repacking), two token tiles per statistics update, and the C
+// statistics kept in base-2 units (logit * scale * log2 e) with a branch-free
+// running maximum; converted to natural units at the end.
+// Running (max, sum 2^(y - max)) update with eight values; -inf values are absent.
+__device__ __forceinline__ void lse2_add8(float& m, float& z, const float* y) {
+  const float mx = fmaxf(fmaxf(fmaxf(y[0], y[1]), fmaxf(y[2], y[3])), fmaxf(fmaxf(y[4], y[5]), fmaxf(y[6], y[7])));
+  const float mn = fmaxf(m, mx);
+  const float ms = mn == -INFINITY ? 0.f : mn;    // all absent so far: keep (−inf, 0)
+  float acc = z * __builtin_amdgcn_exp2f(m - ms);
+#pragma unroll
+  for (int r = 0; r < 8; ++r) acc += __builtin_amdgcn_exp2f(y[r] - ms);
+  z = acc;
+  m = mn;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __restrict__ K,
+                                                     const uint16_t* __restrict__ Q, float4* __restrict__ partial,
+                                                     int nchunk) {
+  constexpr int QE = D / 4;                       // elements of a lane's quarter row
+  constexpr int KS = QE / 8;                      // 16x16x32 steps per tile
+  constexpr int LDK = D + 8;
+  constexpr int CH = 8;                           // elements per 16-byte chunk
+  __shared__ __align__(16) uint16_t sK[RS_SUB * LDK];
+
+  const int ck = blockIdx.x, lg = blockIdx.y, rg = blockIdx.z;
+  const int l = lg / dm.G, g = lg % dm.G;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+  const int64_t t_begin = (int64_t)ck * RS_CHUNK;
+  const int64_t t_end = min(dm.T, t_begin + RS_CHUNK);
+  const uint16_t* Kp = K + (int64_t)lg * dm.T * D;
+  const uint16_t* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
+  const float scale = 1.0f / sqrtf((float)D);
+  const float sc2 = scale * 1.44269504088896341f;
+
+  // the wave's 4 row tiles: lane (row i16, group g4) holds dims QE g4 .. QE g4 + QE - 1
+  uint4 qv[4][KS];
+  int vlim[4];                    // last visible position N_ctx + u of the lane's row
+  bool tile_ok[4], rok[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int rt = rg * 16 + wave * 4 + k;
+    tile_ok[k] = rt * 16 < dm.rows;
+    const int row = rt * 16 + i16;
+    rok[k] = row < dm.rows;
+    vlim[k] = (int)dm.N_ctx + (rok[k] ? row % dm.W : 0);
+    const uint4* q4 = (const uint4*)(Qp + (int64_t)(rok[k] ? row : 0) * D + QE * g4);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qv[k][s] = q4[s];
+  }
+  float mC[4], zC[4], mT[4], zT[4];               // C in base-2 units, the tail in natural units
+#pragma unroll
+  for (int k = 0; k < 4; ++k) { mC[k] = -INFINITY; zC[k] = 0.f; mT[k] = -INFINITY; zT[k] = 0.f; }
+
+  constexpr int NLD = RS_SUB * (D / CH) / 256;    // 16-byte loads per thread per sub-chunk
+  uint4 pre[NLD];
+  auto load_sub = [&](int64_t s0) {
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {
+      const int e = tid + 256 * q;
+      const int tr = e / (D / CH), c = (e % (D / CH)) * CH;
+      const int64_t t = s0 + tr;
+      pre[q] = t < t_end ? *(const uint4*)(Kp + t * D + c) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  load_sub(t_begin);
+  for (int64_t s0 = t_begin; s0 < t_end; s0 += RS_SUB) {
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {
+      const int e = tid + 256 * q;
+      const int tr = e / (D / CH), c = (e % (D / CH)) * CH;
+      *(uint4*)(sK + tr * LDK + c) = pre[q];
+    }
+    if (s0 + RS_SUB < t_end) load_sub(s0 + RS_SUB);
+    __syncthreads();
+    const bool allC = s0 + RS_SUB <= dm.N_c && s0 + RS_SUB <= t_end;
+#pragma unroll
+    for (int tp = 0; tp < RS_SUB / 32; ++tp) {
+      uint4 kv[2][KS];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint4* k4 = (const uint4*)(sK + (32 * tp + 16 * h + i16) * LDK + QE * g4);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) kv[h][s] = k4[s];
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (!tile_ok[k]) continue;
+        f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) acc[h] = mfma_bf16_16x16x32(pk8(kv[h][s]), pk8(qv[k][s]), acc[h]);
+        // lane holds tokens s0 + 32 tp + 16 h + 4 g4 + r of its row
+        float y[8];
+        if (allC) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[4 * h + r] = rok[k] ? acc[h][r] * sc2 : -INFINITY;
+        } else {
+          float xt[8];
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int64_t t = s0 + 32 * tp + 16 * h + 4 * g4 + r;
+              const bool vis = rok[k] && t < t_end && t <= vlim[k];
+              const bool inC = vis && t < dm.N_c;
+              y[4 * h + r] = inC ? acc[h][r] * sc2 : -INFINITY;
+              xt[4 * h + r] = (vis && !inC) ? acc[h][r] * scale : -INFINITY;
+            }
+          lse_add4(mT[k], zT[k], xt[0], xt[1], xt[2], xt[3]);
+          lse_add4(mT[k], zT[k], xt[4], xt[5], xt[6], xt[7]);
+        }
+        lse2_add8(mC[k], zC[k], y);
+      }
+    }
+  }
+  // C statistics back to natural units; merge the 4 lanes holding the same row
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    mC[k] = mC[k] * 0.69314718055994531f;
+#pragma unroll
+    for (int o = 16; o < 64; o <<= 1) {
+      float m2 = __shfl_xor(mC[k], o, 64), z2 = __shfl_xor(zC[k], o, 64);
+      lse_merge(mC[k], zC[k], m2, z2);
+      m2 = __shfl_xor(mT[k], o, 64);
+      z2 = __shfl_xor(zT[k], o, 64);
+      lse_merge(mT[k], zT[k], m2, z2);
+    }
+    const int row = (rg * 16 + wave * 4 + k) * 16 + i16;
+    if (g4 == 0 && tile_ok[k] && rok[k])
+      partial[((int64_t)lg * nchunk + ck) * dm.rows + row] = make_float4(mC[k], zC[k], mT[k], zT[k]);
+  }
+}
+
 // K5b: merge chunk partials in order; S = sum_r exp(m_C - m_V) Z_C / Z_V.
 __global__ __launch_bounds__(256) void k_rowstats_combine(Dims dm, const float4* __restrict__ partial, int nchunk,
                                                           TreeView tv) {
@@ -203,9 +342,11 @@ hipError_t launch_rowstats(const Dims& dm, const void* K, const void* Q, const T
   dim3 grid(nchunk, dm.L * dm.G, (dm.rows + 255) / 256);
   if (dm.dtype == GRACEKV_BF16) {
     if (dm.d == 128)
-      hipLaunchKernelGGL((k_rowstats<uint16_t, 128>), grid, dim3(256), 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, partial, nchunk);
+      hipLaunchKernelGGL((k_rowstats_bf<128>), grid, dim3(256), 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, partial,
+                         nchunk);
     else
-      hipLaunchKernelGGL((k_rowstats<uint16_t, 64>), grid, dim3(256), 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, partial, nchunk);
+      hipLaunchKernelGGL((k_rowstats_bf<64>), grid, dim3(256), 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, partial,
+                         nchunk);
   } else {
     if (dm.d == 128)
       hipLaunchKernelGGL((k_rowstats<float, 128>), grid, dim3(256), 0, st, dm, (const float*)K, (const float*)Q, partial, nchunk);
