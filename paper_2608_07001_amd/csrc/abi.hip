@@ -184,7 +184,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_nslots, 16);
   put(p->off_partial, (size_t)LG * rowstats_chunks(dm) * dm.rows * 16);
   put(p->off_theta, 16);
-  put(p->off_selstate, selstate_bytes());
+  put(p->off_selstate, selstate_bytes(dm));
   put(p->off_work, UC * 4);
   put(p->off_wctr, 16);
   put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));

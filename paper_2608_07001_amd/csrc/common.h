@@ -230,7 +230,7 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
 hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
 // rank: B_free - 1 (the cut) or B_free (the skip bound, also stored in theta[1])
 hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound);
-size_t selstate_bytes();
+size_t selstate_bytes(const Dims& dm);
 hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st);
 hipError_t launch_pack(const Dims& dm, const void* K, const void* V, const float* cosT, const float* sinT,

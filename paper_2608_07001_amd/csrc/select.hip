@@ -21,7 +21,8 @@
 //     one unit; the queue rule is replayed there while >= 2 units remain;
 //   * if exactly one unit remains, the queue discards cost-2 ops until it pops
 //     a cost-1 op, i.e. it executes the best-keyed available cost-1 op.
-// theta is found with an 8-pass, 8-bit, cost-weighted radix select.
+// theta is found with an 8-pass, 8-bit, cost-weighted radix select (the last
+// seven passes over a compact list of the ops that have a cost).
 #include <algorithm>
 
 #include "common.h"
@@ -38,12 +39,36 @@ struct SelState {
   int64_t R;
   uint64_t resid_key;
   int32_t mode;
-  int32_t pad;
+  uint32_t done;        // workgroups finished with the current pass (the last one scans)
+  uint64_t ncand;       // ops in the candidate list (> cap: the list is not used)
   unsigned long long hist[256];
 };
 
-size_t select_ws_bytes(const Dims&) { return sizeof(SelState); }
-size_t selstate_bytes() { return sizeof(SelState); }
+// After the first pass over the whole op table the remaining passes read a
+// compact list of the ops with nonzero cost: (E, cost) pairs.
+constexpr int SEL_GRID = 4096;
+__host__ __device__ inline int64_t sel_ops(const Dims& dm) { return (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap; }
+static int64_t sel_cap(const Dims& dm) { return std::min<int64_t>(sel_ops(dm), (int64_t)1 << 23); }
+static size_t al256s(size_t x) { return (x + 255) & ~(size_t)255; }
+size_t selstate_bytes(const Dims& dm) {
+  const size_t cap = (size_t)sel_cap(dm);
+  return al256s(sizeof(SelState)) + al256s(cap * 8) + al256s(cap);
+}
+size_t select_ws_bytes(const Dims& dm) { return selstate_bytes(dm); }
+struct SelList {
+  uint64_t* E;
+  uint8_t* c;
+  int64_t cap;
+};
+static SelList sel_list(void* state, const Dims& dm) {
+  const size_t cap = (size_t)sel_cap(dm);
+  char* p = (char*)state + al256s(sizeof(SelState));
+  SelList L;
+  L.E = (uint64_t*)p; p += al256s(cap * 8);
+  L.c = (uint8_t*)p;
+  L.cap = (int64_t)cap;
+  return L;
+}
 
 __device__ __forceinline__ uint64_t make_key(float U, uint32_t id) { return op_key(U, id); }
 
@@ -127,69 +152,135 @@ __global__ void k_sel_init(Dims dm, SelState* S, int rank_extra) {
   S->hist[t] = 0;
   if (t == 0) {
     S->prefix = 0; S->target = dm.B_free - 1 + rank_extra; S->above = 0; S->total = 0; S->R = 0;
-    S->resid_key = 0; S->mode = SEL_SELECT;
+    S->resid_key = 0; S->mode = SEL_SELECT; S->done = 0; S->ncand = 0;
   }
 }
 
-// cost-weighted histogram of digit `pass` among ops matching the prefix
-__global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState* S, int pass) {
+// Chooses the digit of pass `pass` from the complete histogram (one thread),
+// then clears the histogram for the next pass.
+__device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
+  do {
+    if (S->mode != SEL_SELECT) break;
+    if (pass == 0) {
+      int64_t tot = 0;
+      for (int k = 0; k < 256; ++k) tot += (int64_t)S->hist[k];
+      S->total = tot;
+      if (dm.B_free <= 0) { S->mode = SEL_NONE; break; }
+      if (tot <= dm.B_free) { S->mode = SEL_ALL; break; }
+      if (dm.B_free == 1) { S->mode = SEL_RESID; S->R = 1; break; }
+    }
+    const int shift = 56 - 8 * pass;
+    const int64_t need = S->target - S->above;
+    int64_t cum = 0;
+    for (int k = 255; k >= 0; --k) {
+      const int64_t hk = (int64_t)S->hist[k];
+      if (cum + hk >= need) {
+        S->prefix |= (uint64_t)k << shift;
+        S->above += cum;
+        break;
+      }
+      cum += hk;
+    }
+  } while (0);
+  for (int k = 0; k < 256; ++k) S->hist[k] = 0;
+  S->done = 0;
+}
+
+// cost-weighted histogram of digit `pass` among ops matching the prefix.
+// Pass 0 reads the whole op table and also collects the ops that have a cost
+// into a compact list (each workgroup buffers its share in LDS and appends it
+// with one atomic; a workgroup whose share overflows the buffer invalidates the
+// list, and the later passes then read the whole table again).  The last
+// workgroup to finish a pass chooses its digit.
+constexpr int SEL_BUF = 4096;
+__global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState* S, int pass, SelList Lc) {
   const int32_t* n_slots = tv.nslots;
-  __shared__ unsigned int h[256];
-  h[threadIdx.x] = 0;
+  __shared__ unsigned int h[4][256];          // one histogram per wave (less atomic contention)
+  __shared__ uint64_t bufE[SEL_BUF];
+  __shared__ uint8_t bufC[SEL_BUF];
+  __shared__ unsigned int nbuf;
+  __shared__ unsigned long long lbase;
+  __shared__ bool last;
+  const int tid = threadIdx.x, wave = tid >> 6;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) h[w][tid] = 0;
+  if (tid == 0) nbuf = 0;
   __syncthreads();
   const int mode = S->mode;
-  if (mode == SEL_SELECT) {
-    const int shift = 56 - 8 * pass;
-    const uint64_t pre = S->prefix;
+  const int shift = 56 - 8 * pass;
+  const uint64_t pre = S->prefix;
+  const int64_t ncand = (int64_t)S->ncand;
+  auto take = [&](uint64_t E, int c) {
+    if (pass == 0) {
+      const unsigned pos = atomicAdd(&nbuf, 1u);
+      if (pos < SEL_BUF) { bufE[pos] = E; bufC[pos] = (uint8_t)c; }
+    }
+    if (pass > 0 && (E >> (shift + 8)) != (pre >> (shift + 8))) return;
+    atomicAdd(&h[wave][(E >> shift) & 255u], (unsigned)c);
+  };
+  if (mode == SEL_SELECT && pass > 0 && ncand <= Lc.cap) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + tid; i < ncand; i += (int64_t)gridDim.x * 256) {
+      const uint64_t E = Lc.E[i];
+      if ((E >> (shift + 8)) != (pre >> (shift + 8))) continue;
+      atomicAdd(&h[wave][(E >> shift) & 255u], (unsigned)Lc.c[i]);
+    }
+  } else if (mode == SEL_SELECT) {
     const int J = *n_slots;
     const int64_t node_cap = (int64_t)dm.L * dm.G * 2 * dm.N_c;
-    const int64_t unit_cap = (int64_t)dm.L * dm.G * dm.J_cap;
-    const int64_t tot = node_cap + unit_cap;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < tot; i += (int64_t)gridDim.x * 256) {
-      uint64_t E;
-      int c;
-      if (i < node_cap) {
-        c = tv.sp_cost[i];
-        if (c == 0) continue;                 // empty slot or leaf: its key is never read
-        E = tv.sp_E[i];
-      } else {
-        const int64_t u = i - node_cap;
-        if ((int)(u % dm.J_cap) >= J) continue;
-        c = 1;
-        E = tv.add_E[u];
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    // Splits: sixteen cost bytes per load (an empty slot or a leaf has cost 0 and
+    // its key is never read)
+    const int64_t n16 = node_cap / 16;
+    for (int64_t v = (int64_t)blockIdx.x * 256 + tid; v < n16; v += stride) {
+      const uint4 cw = ((const uint4*)tv.sp_cost)[v];
+      if ((cw.x | cw.y | cw.z | cw.w) == 0u) continue;
+      const uint32_t wds[4] = {cw.x, cw.y, cw.z, cw.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (wds[q] == 0u) continue;
+#pragma unroll
+        for (int bt = 0; bt < 4; ++bt) {
+          const int c = (wds[q] >> (8 * bt)) & 255u;
+          if (c) take(tv.sp_E[16 * v + 4 * q + bt], c);
+        }
       }
-      if (pass > 0 && (E >> (shift + 8)) != (pre >> (shift + 8))) continue;
-      atomicAdd(&h[(E >> shift) & 255u], (unsigned)c);
+    }
+    for (int64_t i = 16 * n16 + (int64_t)blockIdx.x * 256 + tid; i < node_cap; i += stride) {
+      const int c = tv.sp_cost[i];
+      if (c) take(tv.sp_E[i], c);
+    }
+    // Adds: cost 1 for every unit (l, g, j < J) of the partition
+    const int64_t nadd = (int64_t)dm.L * dm.G * J;
+    for (int64_t x = (int64_t)blockIdx.x * 256 + tid; x < nadd; x += stride) {
+      const int lg = (int)(x / J), j = (int)(x - (int64_t)lg * J);
+      take(tv.add_E[(int64_t)lg * dm.J_cap + j], 1);
+    }
+    if (pass == 0) {                          // append the workgroup's share to the list
+      __syncthreads();
+      const unsigned nb = nbuf;
+      if (tid == 0)
+        lbase = atomicAdd((unsigned long long*)&S->ncand,
+                          nb <= SEL_BUF ? (unsigned long long)nb : (unsigned long long)Lc.cap + 1ull);
+      __syncthreads();
+      if (nb <= SEL_BUF) {
+        const uint64_t base = lbase;
+        for (unsigned k = tid; k < nb; k += 256) {
+          if (base + k < (uint64_t)Lc.cap) { Lc.E[base + k] = bufE[k]; Lc.c[base + k] = bufC[k]; }
+        }
+      }
     }
   }
   __syncthreads();
-  if (h[threadIdx.x]) atomicAdd(&S->hist[threadIdx.x], (unsigned long long)h[threadIdx.x]);
-}
-
-__global__ void k_sel_scan(Dims dm, SelState* S, int pass) {
-  if (threadIdx.x != 0) return;
-  if (S->mode != SEL_SELECT) return;
-  if (pass == 0) {
-    int64_t tot = 0;
-    for (int k = 0; k < 256; ++k) tot += (int64_t)S->hist[k];
-    S->total = tot;
-    if (dm.B_free <= 0) { S->mode = SEL_NONE; return; }
-    if (tot <= dm.B_free) { S->mode = SEL_ALL; return; }
-    if (dm.B_free == 1) { S->mode = SEL_RESID; S->R = 1; return; }
+  const unsigned hs = h[0][tid] + h[1][tid] + h[2][tid] + h[3][tid];
+  if (hs) atomicAdd(&S->hist[tid], (unsigned long long)hs);
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) last = atomicAdd(&S->done, 1u) == gridDim.x - 1;
+  __syncthreads();
+  if (last && tid == 0) {
+    __threadfence();
+    sel_scan(dm, S, pass);
   }
-  const int shift = 56 - 8 * pass;
-  const int64_t need = S->target - S->above;
-  int64_t cum = 0;
-  for (int k = 255; k >= 0; --k) {
-    const int64_t hk = (int64_t)S->hist[k];
-    if (cum + hk >= need) {
-      S->prefix |= (uint64_t)k << shift;
-      S->above += cum;
-      break;
-    }
-    cum += hk;
-  }
-  for (int k = 0; k < 256; ++k) S->hist[k] = 0;
 }
 
 __global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const SelState* S) {
@@ -321,15 +412,25 @@ __global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used)
   *b_used = dm.B_free - R;
 }
 
+// the eight radix passes of one cost-weighted select
+static void sel_passes(const Dims& dm, const TreeView& tv, SelState* S, hipStream_t st) {
+  const int64_t tot = sel_ops(dm);
+  const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, SEL_GRID);
+  const SelList Lc = sel_list(S, dm);
+  for (int pass = 0; pass < 8; ++pass) {
+    // few workgroups: their per-pass global atomics (list base, histogram, completion) meet at single
+    // addresses
+    const unsigned g = std::min<unsigned>(blocks, pass == 0 ? 512u : 256u);
+    hipLaunchKernelGGL(k_sel_hist, dim3(g), dim3(256), 0, st, dm, tv, S, pass, Lc);
+  }
+}
+
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st) {
   SelState* S = (SelState*)ws;
   hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, 0);
   const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
   const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
-  for (int pass = 0; pass < 8; ++pass) {
-    hipLaunchKernelGGL(k_sel_hist, dim3(blocks), dim3(256), 0, st, dm, tv, S, pass);
-    hipLaunchKernelGGL(k_sel_scan, dim3(1), dim3(64), 0, st, dm, S, pass);
-  }
+  sel_passes(dm, tv, S, st);
   hipLaunchKernelGGL(k_sel_flag, dim3(blocks), dim3(256), 0, st, dm, tv, (const SelState*)S);
   hipLaunchKernelGGL(k_sel_group, dim3(1), dim3(64), 0, st, dm, tv, S);
   hipLaunchKernelGGL(k_sel_resid_find, dim3(blocks), dim3(256), 0, st, dm, tv, S);
@@ -351,12 +452,7 @@ __global__ void k_theta_store(Dims dm, const SelState* S, uint64_t* theta, bool 
 hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound) {
   SelState* S = (SelState*)tv.selstate;
   hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, skip_bound ? 1 : 0);
-  const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
-  const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
-  for (int pass = 0; pass < 8; ++pass) {
-    hipLaunchKernelGGL(k_sel_hist, dim3(blocks), dim3(256), 0, st, dm, tv, S, pass);
-    hipLaunchKernelGGL(k_sel_scan, dim3(1), dim3(64), 0, st, dm, S, pass);
-  }
+  sel_passes(dm, tv, S, st);
   hipLaunchKernelGGL(k_theta_store, dim3(1), dim3(64), 0, st, dm, (const SelState*)S, tv.theta, skip_bound);
   return hipGetLastError();
 }
