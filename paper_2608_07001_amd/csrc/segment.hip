@@ -44,6 +44,9 @@ struct SegWs {
   float* gram;      // [n_seg][T][BAND]
   float* dist2;     // [N_c][BAND]
   double* P2;       // [N_c + 1]
+  double* bsum;     // [N_c / PS_BLK + 1] prefix block totals, then offsets
+  double* boff;
+  void* rz;         // robust-z select state
   uint8_t* Poff;    // [N_c + 1] backpointer offsets i - P(i) (0: none)
   double* Fdbg;     // [4] F(N), chunks recomputed by the fix-up
   double* S;        // [N_c][128] slot scores by (i, length), candidate-major per lane
@@ -66,7 +69,7 @@ static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t segment_ws_bytes(const Dims& dm) {
   const size_t T = (size_t)dm.T, N = (size_t)dm.N_c, C = (size_t)dp_chunks(dm.N_c) + 1;
   return al(dm.n_seg * 3 * T * 4) + al(dm.n_seg * T * 4) + al(T * 4) + al((size_t)dm.n_seg * T * BAND * 4) +
-         al(N * BAND * 4) + al((N + 1) * 8) + al(N + 1) + al(4 * 8) + al(N * BAND * 8) + al(C * (DPC + 128) * 8) +
+         al(N * BAND * 4) + 2 * al((N / 2048 + 2) * 8) + al(4096) + al((N + 1) * 8) + al(N + 1) + al(4 * 8) + al(N * BAND * 8) + al(C * (DPC + 128) * 8) +
          3 * al(C * 8) + al((N / 16 + 2) * 8) + al(C * 128 * 8) + al(C * 8);
 }
 
@@ -79,6 +82,9 @@ static SegWs seg_view(void* ws, const Dims& dm) {
   s.sq = (float*)p; p += al(T * 4);
   s.gram = (float*)p; p += al((size_t)dm.n_seg * T * BAND * 4);
   s.dist2 = (float*)p; p += al(N * BAND * 4);
+  s.bsum = (double*)p; p += al((N / 2048 + 2) * 8);
+  s.boff = (double*)p; p += al((N / 2048 + 2) * 8);
+  s.rz = (void*)p; p += al(4096);
   s.P2 = (double*)p; p += al((N + 1) * 8);
   s.Poff = (uint8_t*)p; p += al(N + 1);
   s.Fdbg = (double*)p; p += al(4 * 8);
@@ -231,49 +237,81 @@ __device__ __forceinline__ float okey_inv(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
-// value of rank `rank` (ascending, 0-based) of f(src[i]) = |src[i] - center| or src[i]
-__device__ float block_select(const float* src, int64_t n, int64_t rank, bool absdev, float center, uint32_t* hist) {
-  uint32_t prefix = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int k = threadIdx.x; k < 256; k += blockDim.x) hist[k] = 0;
-    __syncthreads();
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
-      const float v = absdev ? fabsf(src[i] - center) : src[i];
-      const uint32_t k = okey(v);
-      if (pass > 0 && (k >> (shift + 8)) != (prefix >> (shift + 8))) continue;
-      atomicAdd(&hist[(k >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    __shared__ uint32_t pick;
-    __shared__ int64_t below;
-    if (threadIdx.x == 0) {
-      int64_t cum = 0;
-      for (int k = 0; k < 256; ++k) {
-        if (cum + hist[k] > rank) { pick = (uint32_t)k; below = cum; break; }
-        cum += hist[k];
-      }
-    }
-    __syncthreads();
-    prefix |= pick << shift;
-    rank -= below;
-    __syncthreads();
+// Lower medians by a multi-workgroup radix select on order-preserving keys:
+// selects 0 and 1 run together (kappa and s, then |kappa - med| and |s - med|);
+// per pass every workgroup adds its 256-bin histogram of the keys matching the
+// prefix, and the last one to finish picks the digit.
+struct RzState {
+  uint32_t prefix[2];
+  int64_t rank[2];
+  float center[2];
+  float med[4];                 // med kappa, med s, MAD kappa, MAD s
+  uint32_t done[2];
+  uint32_t hist[2][256];
+};
+constexpr int RZ_WG = 128;      // workgroups per select and pass
+
+__global__ void k_rz_init(Dims dm, RzState* R, int stage) {
+  const int t = threadIdx.x;
+  R->hist[0][t] = 0;
+  R->hist[1][t] = 0;
+  if (t < 2) {
+    R->prefix[t] = 0;
+    R->rank[t] = (dm.T - 1) / 2;
+    R->done[t] = 0;
+    R->center[t] = stage == 0 ? 0.f : R->med[t];
   }
-  return okey_inv(prefix);
 }
 
-__global__ __launch_bounds__(1024) void k_robust_z(Dims dm, const float* __restrict__ kappa,
-                                                   const float* __restrict__ surp, float* bscore) {
-  __shared__ uint32_t hist[256];
-  const int64_t n = dm.T;
-  const int64_t rk = (n - 1) / 2;
-  const float mk = block_select(kappa, n, rk, false, 0.f, hist);
-  const float madk = block_select(kappa, n, rk, true, mk, hist);
-  const float ms = block_select(surp, n, rk, false, 0.f, hist);
-  const float mads = block_select(surp, n, rk, true, ms, hist);
-  const float dk = dm.mad * madk + dm.eps_seg, ds = dm.mad * mads + dm.eps_seg;
-  for (int64_t i = threadIdx.x; i < n; i += blockDim.x)
-    bscore[i] = (kappa[i] - mk) / dk + dm.lam_s * ((surp[i] - ms) / ds);
+__global__ __launch_bounds__(256) void k_rz_hist(Dims dm, const float* __restrict__ kappa,
+                                                 const float* __restrict__ surp, RzState* R, int stage, int pass) {
+  __shared__ uint32_t h[256];
+  __shared__ bool last;
+  const int which = blockIdx.y;
+  const float* src = which == 0 ? kappa : surp;
+  const bool absdev = stage == 1;
+  const float center = R->center[which];
+  const uint32_t prefix = R->prefix[which];
+  const int shift = 24 - 8 * pass;
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < dm.T; i += (int64_t)gridDim.x * 256) {
+    const float v = absdev ? fabsf(src[i] - center) : src[i];
+    const uint32_t k = okey(v);
+    if (pass > 0 && (k >> (shift + 8)) != (prefix >> (shift + 8))) continue;
+    atomicAdd(&h[(k >> shift) & 255u], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd(&R->hist[which][threadIdx.x], h[threadIdx.x]);
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(&R->done[which], 1u) == gridDim.x - 1;
+  __syncthreads();
+  if (last && threadIdx.x == 0) {
+    __threadfence();
+    int64_t cum = 0, rank = R->rank[which];
+    for (int k = 0; k < 256; ++k) {
+      const int64_t hk = R->hist[which][k];
+      if (cum + hk > rank) {
+        R->prefix[which] = prefix | ((uint32_t)k << shift);
+        R->rank[which] = rank - cum;
+        break;
+      }
+      cum += hk;
+    }
+    for (int k = 0; k < 256; ++k) R->hist[which][k] = 0;
+    R->done[which] = 0;
+    if (pass == 3) R->med[2 * stage + which] = okey_inv(R->prefix[which]);
+  }
+}
+
+__global__ void k_rz_score(Dims dm, const float* __restrict__ kappa, const float* __restrict__ surp,
+                           const RzState* __restrict__ R, float* bscore) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= dm.T) return;
+  const float mk = R->med[0], ms = R->med[1];
+  const float dk = dm.mad * R->med[2] + dm.eps_seg, ds = dm.mad * R->med[3] + dm.eps_seg;
+  bscore[i] = (kappa[i] - mk) / dk + dm.lam_s * ((surp[i] - ms) / ds);
 }
 
 // ---- K3: banded Gram --------------------------------------------------------
@@ -400,7 +438,8 @@ __global__ __launch_bounds__(192) void k_gram_f32(Dims dm, const float* __restri
   }
 }
 
-// dist2[e][delta] = mean over slabs of ||hbar_e - hbar_{e-delta}||^2, e < N_c
+// dist2[e][delta] = mean over slabs of ||hbar_e - hbar_{e-delta}||^2, e < N_c, from the
+// banded Gram of the raw rows and their norms
 __global__ void k_dist2(Dims dm, SegWs ws) {
   const int64_t e = blockIdx.x;
   const int dlt = threadIdx.x;
@@ -418,16 +457,32 @@ __global__ void k_dist2(Dims dm, SegWs ws) {
   ws.dist2[e * BAND + dlt] = acc;
 }
 
-// P2[t] = sum_{tau < t} sq[tau] (fp64), t = 0..N_c
-__global__ __launch_bounds__(1024) void k_prefix_sq(Dims dm, SegWs ws) {
+// P2[t] = sum_{tau < t} sq[tau] (fp64), t = 0..N_c (d_t exists for t <= N_c - 2):
+// block totals of PS_BLK terms, an exclusive scan of the totals, then each
+// block's own scan plus its offset.
+constexpr int PS_BLK = 2048;    // terms per workgroup (8 per thread)
+__device__ __forceinline__ double sq_term(const Dims& dm, const SegWs& ws, int64_t t) {
+  return t < dm.N_c - 1 ? (double)ws.sq[t] : 0.0;
+}
+__global__ __launch_bounds__(256) void k_psum_blocks(Dims dm, SegWs ws) {
+  __shared__ double red[4];
+  const int64_t t0 = (int64_t)blockIdx.x * PS_BLK + 8 * threadIdx.x;
+  double s8 = 0.0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s8 += sq_term(dm, ws, t0 + k);
+  s8 = wave_sum(s8);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s8;
+  __syncthreads();
+  if (threadIdx.x == 0) ws.bsum[blockIdx.x] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+__global__ __launch_bounds__(1024) void k_psum_top(Dims dm, SegWs ws, int nblk) {
   __shared__ double part[1024];
   __shared__ double carry;
-  const int64_t N = dm.N_c;
-  if (threadIdx.x == 0) { carry = 0.0; ws.P2[0] = 0.0; }
+  if (threadIdx.x == 0) carry = 0.0;
   __syncthreads();
-  for (int64_t t0 = 0; t0 < N; t0 += 1024) {
-    const int64_t t = t0 + threadIdx.x;
-    const double v = (t < N - 1) ? (double)ws.sq[t] : 0.0;     // d_t exists for t <= N - 2
+  for (int b0 = 0; b0 < nblk; b0 += 1024) {
+    const int b = b0 + threadIdx.x;
+    const double v = b < nblk ? ws.bsum[b] : 0.0;
     part[threadIdx.x] = v;
     __syncthreads();
     for (int o = 1; o < 1024; o <<= 1) {
@@ -436,11 +491,33 @@ __global__ __launch_bounds__(1024) void k_prefix_sq(Dims dm, SegWs ws) {
       part[threadIdx.x] += x;
       __syncthreads();
     }
-    if (t < N) ws.P2[t + 1] = carry + part[threadIdx.x];
+    if (b < nblk) ws.boff[b] = carry + part[threadIdx.x] - v;
     __syncthreads();
     if (threadIdx.x == 0) carry += part[1023];
     __syncthreads();
   }
+}
+__global__ __launch_bounds__(256) void k_psum_apply(Dims dm, SegWs ws) {
+  __shared__ double part[256];
+  const int64_t t0 = (int64_t)blockIdx.x * PS_BLK + 8 * threadIdx.x;
+  double v[8], s8 = 0.0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) { v[k] = sq_term(dm, ws, t0 + k); s8 += v[k]; }
+  part[threadIdx.x] = s8;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {
+    const double x = threadIdx.x >= o ? part[threadIdx.x - o] : 0.0;
+    __syncthreads();
+    part[threadIdx.x] += x;
+    __syncthreads();
+  }
+  double run = ws.boff[blockIdx.x] + part[threadIdx.x] - s8;   // sum of the terms before t0
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    run += v[k];
+    if (t0 + k < dm.N_c) ws.P2[t0 + k + 1] = run;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) ws.P2[0] = 0.0;
 }
 
 // ---- K4: DP -----------------------------------------------------------------
@@ -903,10 +980,23 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
     hipLaunchKernelGGL(k_curvature<float>, g1, dim3(256), 0, st, dm, (const float*)hidden, ws);
   }
   hipLaunchKernelGGL(k_stabilize, dim3((unsigned)((dm.T + 255) / 256)), dim3(256), 0, st, dm, ws, kappa);
-  hipLaunchKernelGGL(k_robust_z, dim3(1), dim3(1024), 0, st, dm, (const float*)kappa, surprisal, bscore);
+  {
+    RzState* R = (RzState*)ws.rz;
+    for (int stage = 0; stage < 2; ++stage) {
+      hipLaunchKernelGGL(k_rz_init, dim3(1), dim3(256), 0, st, dm, R, stage);
+      for (int pass = 0; pass < 4; ++pass)
+        hipLaunchKernelGGL(k_rz_hist, dim3(RZ_WG, 2), dim3(256), 0, st, dm, (const float*)kappa, surprisal, R, stage,
+                           pass);
+    }
+    hipLaunchKernelGGL(k_rz_score, dim3((unsigned)((dm.T + 255) / 256)), dim3(256), 0, st, dm, (const float*)kappa,
+                       surprisal, (const RzState*)R, bscore);
+  }
   if (dm.N_c > 0) {
     hipLaunchKernelGGL(k_dist2, dim3((unsigned)dm.N_c), dim3(BAND), 0, st, dm, ws);
-    hipLaunchKernelGGL(k_prefix_sq, dim3(1), dim3(1024), 0, st, dm, ws);
+    const int nblk = (int)((dm.N_c + PS_BLK - 1) / PS_BLK);
+    hipLaunchKernelGGL(k_psum_blocks, dim3(nblk), dim3(256), 0, st, dm, ws);
+    hipLaunchKernelGGL(k_psum_top, dim3(1), dim3(1024), 0, st, dm, ws, nblk);
+    hipLaunchKernelGGL(k_psum_apply, dim3(nblk), dim3(256), 0, st, dm, ws);
   }
   if (dm.N_c > 0) {
     const int64_t C = dp_chunks(dm.N_c);
