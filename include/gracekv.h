@@ -218,10 +218,12 @@ gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void
                             int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
                             int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
 
-/* Layout check of the matrix-core instructions used by the kernels: computes
+/* Layout check of the cross-lane instructions used by the kernels: computes
  * a 16x16 product from fixed inputs with the fp32 16x16x4 (which = 0), the
- * bf16 16x16x16 (which = 1) or the bf16 16x16x32 (which = 2) instruction and
- * copies it to host_out[256] (synchronous). */
+ * bf16 16x16x16 (which = 1) or the bf16 16x16x32 (which = 2) matrix
+ * instruction, or (which = 3) the sum of lane + 1 over the four lanes
+ * l % 16 + 16 k of a wave (host_out[0..63], the rest 0), and copies it to
+ * host_out[256] (synchronous). */
 gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out);
 
 #ifdef __cplusplus

@@ -299,7 +299,7 @@ gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* 
 }
 
 gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out) {
-  if (!host_out || which < 0 || which > 2) return GRACEKV_ERR_INVALID_ARG;
+  if (!host_out || which < 0 || which > 3) return GRACEKV_ERR_INVALID_ARG;
   return hip_status(selftest_mfma(which, host_out));
 }
 

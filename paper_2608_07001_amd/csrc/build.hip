@@ -371,18 +371,15 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
   const int lastblk = (n - 1) >> 4;
   block_k<T, D, QW>(Kp, n, prefix ? (a >> 4) : ((b - 1) >> 4), kpre);   // the sweep's first block
   int cur = prefix ? a : b;
-  // scores child gc (prefix or suffix) from M and Z: (Z / Z_q(C)) D_q summed over the wave's probes
-  auto score_child = [&](int gc) {
-    float Zs = Z;
-    Zs += __shfl_xor(Zs, 16, 64);
-    Zs += __shfl_xor(Zs, 32, 64);
-    const float z = pok ? U.Zt[gc * WMAX + q] : 0.f;
-    const float* vt = U.Vv + gc * D + 4 * g4;
+  const float izc = 1.0f / zc;
+  // scores child gc (prefix or suffix) from M and Z: (Z / Z_q(C)) D_q summed over
+  // the wave's probes; z and v~ of the child were loaded before the sweep reached it
+  auto score_child = [&](int gc, float z, const float4* vt) {
+    const float Zs = col_sum4(Z);
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const float4 v4 = *(const float4*)(vt + 16 * dt);
-      const float vv[4] = {v4.x, v4.y, v4.z, v4.w};
+      const float vv[4] = {vt[dt].x, vt[dt].y, vt[dt].z, vt[dt].w};
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float Mv = M[dt][r];
@@ -391,19 +388,19 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
         s2 += Mv * Mv;
       }
     }
-    s1 += __shfl_xor(s1, 16, 64);
-    s1 += __shfl_xor(s1, 32, 64);
-    s2 += __shfl_xor(s2, 16, 64);
-    s2 += __shfl_xor(s2, 32, 64);
+    s1 = col_sum4(s1);
+    s2 = col_sum4(s2);
     const float dz = Zs - z;
-    const float Dq = dm.lam_Z * dz * dz / (Zs * Zs + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
+    const float Dq = dm.lam_Z * dz * dz * __builtin_amdgcn_rcpf(Zs * Zs + dm.eps) +
+                     dm.lam_M * s1 * __builtin_amdgcn_rcpf(s2 + dm.eps);
     // sum over the wave's 16 probes (row 0 of the wave)
-    const float con = row_sum16((g4 == 0 && pok) ? (Zs / zc) * Dq : 0.f);
+    const float con = row_sum16((g4 == 0 && pok) ? (Zs * izc) * Dq : 0.f);
     if (lane == 0) U.Con[gc * 4 + pt] = con;
   };
   for (int k = 0; k < nx; ++k) {
     const int c = prefix ? k : nx - 1 - k;
     const int x = prefix ? XL[c] : XR[c];
+    const int gc = prefix ? c : CM + c;
     // accumulate the pieces between cur and x (each within one 16-token block)
     while (prefix ? cur < x : cur > x) {
       const int blk = prefix ? (cur >> 4) : ((cur - 1) >> 4);
@@ -467,8 +464,13 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
       }
       if (prefix) cur = hi; else cur = lo;
     }
-    const int gc = prefix ? c : CM + c;
-    if ((int)U.crow(0)[gc] >= 2) score_child(gc);
+    if ((int)U.crow(0)[gc] >= 2) {
+      const float zk = pok ? U.Zt[gc * WMAX + q] : 0.f;
+      float4 vk[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vk[dt] = *(const float4*)(U.Vv + gc * D + 4 * g4 + 16 * dt);
+      score_child(gc, zk, vk);
+    }
   }
 }
 

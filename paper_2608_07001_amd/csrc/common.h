@@ -142,6 +142,16 @@ __device__ __forceinline__ float row_sum16(float v) {
   return v;
 }
 
+// Sum over the four lanes l % 16 + 16 k (one column of the four 16-lane rows),
+// returned to all four: two row-swap permutations, no LDS traffic.  Every
+// lane gets (r0 + r1) + (r2 + r3) in the same order.
+__device__ __forceinline__ float col_sum4(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
 // Sum over the wave, returned to every lane: 16-lane row sums by DPP, then the
 // four row results read as scalars.
 __device__ __forceinline__ float wave_sum_dpp(float v) {

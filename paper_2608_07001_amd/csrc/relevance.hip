@@ -364,6 +364,11 @@ __global__ void k_selftest_mfma(int which, float* out) {
   const int lane = threadIdx.x;
   // A[i][k] = (i - 3k) / 8, B[j][k] = (2j + k) / 16 -- exact in bf16 for 0 <= i, j, k < 16
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (which == 3) {                     // column sums over the four 16-lane rows
+    out[lane] = col_sum4((float)(lane + 1));
+    for (int i = 64 + lane; i < 256; i += 64) out[i] = 0.f;
+    return;
+  }
   if (which == 2) {                     // 16x16x32: k < 32
     s16x8 a, b;
     for (int q = 0; q < 8; ++q) {

@@ -473,12 +473,9 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
           for (int x = 0; x < 8; ++x)
             qk += __uint_as_float((x & 1) ? (qw[x >> 1] & 0xffff0000u) : (qw[x >> 1] << 16)) * kx[x];
         }
-        qk += __shfl_xor(qk, 16, 64);
-        qk += __shfl_xor(qk, 32, 64);
+        qk = col_sum4(qk);
         const float z = me * __builtin_amdgcn_exp2f(qk * sc2 - mq2);
-        float Z = Zl;
-        Z += __shfl_xor(Z, 16, 64);
-        Z += __shfl_xor(Z, 32, 64);
+        const float Z = col_sum4(Zl);
         float s1 = 0.f, s2 = 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
@@ -492,10 +489,8 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
             s2 += M * M;
           }
         }
-        s1 += __shfl_xor(s1, 16, 64);
-        s1 += __shfl_xor(s1, 32, 64);
-        s2 += __shfl_xor(s2, 16, 64);
-        s2 += __shfl_xor(s2, 32, 64);
+        s1 = col_sum4(s1);
+        s2 = col_sum4(s2);
         const float dz = Z - z;
         const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
         con = (uok && g4 == 0) ? (Z * zcq) * Dq : 0.f;

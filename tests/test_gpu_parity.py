@@ -47,6 +47,11 @@ def test_mfma_layout_bf16_and_fp32():
         want = A @ B.T
         got = gk.selftest_mfma(which).numpy()
         assert np.array_equal(got, want.astype(np.float32)), which
+    # column sums over the four 16-lane rows of a wave
+    lane = np.arange(64)
+    want = np.zeros(256, np.float32)
+    want[:64] = 4 * (lane % 16) + 100
+    assert np.array_equal(gk.selftest_mfma(3).numpy().reshape(-1), want)
 
 
 @pytest.fixture(scope="module")
