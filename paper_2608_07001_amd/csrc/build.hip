@@ -683,14 +683,18 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
         const int t = a + tid;                     // curvature position t -> cut t + 1
         const float kt = U.Kap[t];
         int rank = 0;
-        // positions a .. b - 2, read four at a time (all lanes read the same words)
-        for (int t4 = a & ~3; t4 <= b - 2; t4 += 4) {
+        // positions a .. b - 2, read eight at a time (all lanes read the same
+        // words; the last read may run past b - 2 into the next LDS array, which
+        // the position test masks), branch-free comparisons
+        const int hi = b - 2;
+        for (int t4 = a & ~3; t4 <= hi; t4 += 8) {
           const float4 k4 = *(const float4*)(U.Kap + t4);
-          const float kk[4] = {k4.x, k4.y, k4.z, k4.w};
+          const float4 k5 = *(const float4*)(U.Kap + t4 + 4);
+          const float kk[8] = {k4.x, k4.y, k4.z, k4.w, k5.x, k5.y, k5.z, k5.w};
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
+          for (int jj = 0; jj < 8; ++jj) {
             const int t2 = t4 + jj;
-            rank += (t2 >= a && t2 <= b - 2) && ((kk[jj] > kt) || (kk[jj] == kt && t2 < t));
+            rank += (int)((t2 >= a) & (t2 <= hi) & ((kk[jj] > kt) | ((kk[jj] == kt) & (t2 < t))));
           }
         }
         if (rank < dm.k_curv) U.flag[t + 1 - a] = 1;
