@@ -172,7 +172,8 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  *              the slot partition (read by score, select and pack); per unit the
  *              root prototype (k~ then v~, d values each, rounded to cfg->dtype)
  *              and its log m_eff (fp32), which pack copies for a root on the
- *              frontier.
+ *              frontier; the last 1024 bytes hold a device copy of the kernel
+ *              arguments, rewritten in stream order by every call.
  *   ws         unused (pass NULL, 0); reserved.
  * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
  * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops

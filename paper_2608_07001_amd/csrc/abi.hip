@@ -61,6 +61,7 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.slots = (int32_t*)(b + p.off_slots);
   v.proto = (void*)(b + p.off_proto);
   v.proto_logm = (float*)(b + p.off_proto_logm);
+  v.kargs = (void*)(b + p.tree_bytes - KARGS_BYTES);
   v.nslots = (int32_t*)(b + p.off_nslots);
   v.theta = (uint64_t*)(b + p.off_theta);
   v.selstate = (void*)(b + p.off_selstate);
@@ -73,6 +74,22 @@ __global__ void k_copy_slots(const int32_t* __restrict__ slot_starts, const int3
                              TreeView tv) {
   for (int i = threadIdx.x; i <= J_cap; i += blockDim.x) tv.slots[i] = slot_starts[i];
   if (threadIdx.x == 0) { *tv.nslots = *n_slots; *tv.status = 0; }
+}
+
+// Copies the kernel arguments into the tree buffer, in stream order, for the
+// kernels that read them through pointers (their argument structures would not
+// fit in scalar registers).
+__global__ void k_store_args(Dims dm, TreeView tv) {
+  if (threadIdx.x == 0) {
+    *(Dims*)tv.kargs = dm;
+    *(TreeView*)((char*)tv.kargs + 512) = tv;
+  }
+}
+
+hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st) {
+  static_assert(sizeof(Dims) <= 512 && sizeof(TreeView) <= KARGS_BYTES - 512, "kernel argument copy too small");
+  hipLaunchKernelGGL(k_store_args, dim3(1), dim3(64), 0, st, dm, tv);
+  return hipGetLastError();
 }
 
 }  // namespace gkv
@@ -189,6 +206,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_wctr, 16);
   put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));
   put(p->off_proto_logm, UC * 4);
+  o += KARGS_BYTES;                          // device copy of the kernel arguments
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
   p->sel_ws_bytes = select_ws_bytes(dm);
@@ -243,6 +261,7 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   hipStream_t st = (hipStream_t)stream;
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
   if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
+  if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess) return GRACEKV_ERR_HIP;
   auto build = [&](int mode) {
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);

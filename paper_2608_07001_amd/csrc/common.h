@@ -66,6 +66,8 @@ struct TreeView {
   int32_t* wctr;        // [4] list length, next item
   void* proto;          // [unit_cap][2][d] root prototype (k~, v~) of each unit, cache dtype
   float* proto_logm;    // [unit_cap] log m_eff of the root
+  void* kargs;          // device copy of the kernel arguments (Dims, then this view) for the
+                        // kernels that read them through pointers
 };
 
 // Refinement modes (the roots come from the root kernel): FULL refines every
@@ -105,6 +107,8 @@ __device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
 }
 
 Dims make_dims(const gracekv_config& c, const gracekv_plan& p);
+constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0, TreeView at 512
+hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
 TreeView make_view(void* base, const gracekv_plan& p);
 
 // ---- device helpers -------------------------------------------------------

@@ -50,7 +50,8 @@ struct RbLds {
   static constexpr int oVv = oKt + D * 4;                   // [D] prototype value v~
   static constexpr int oSum = oVv + D * 4;                  // [RB_W][4] per-wave sums of R, A, ||k°||
   static constexpr int oRed = oSum + RB_W * 4 * 4;          // [2][RB_W] distortion sums (unit parity)
-  static constexpr int oK = oRed + 2 * RB_W * 4;            // K rows [NMAX][LDK]
+  static constexpr int oPend = oRed + 2 * RB_W * 4;         // deferred outputs of the previous unit
+  static constexpr int oK = oPend + 64;                     // K rows [NMAX][LDK]
   static constexpr int bytes = oK + NMAX * LDK * 2;
 };
 
@@ -87,11 +88,15 @@ __device__ __forceinline__ float pick4f(const float* v, int i) {
 }
 
 template <int D, bool MP>
-__global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __restrict__ K,
+__global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ V, const uint16_t* __restrict__ Q,
                                                      const float* __restrict__ cosT, const float* __restrict__ sinT,
                                                      const int32_t* __restrict__ slot_starts,
-                                                     const int32_t* __restrict__ n_slots, TreeView tv) {
+                                                     const int32_t* __restrict__ n_slots, const TreeView* __restrict__ tvp) {
+  // the argument structures are read from device memory where used (held in
+  // scalar registers they would not fit)
+  const Dims& dm = *dmp;
+  const TreeView& tv = *tvp;
   using Lay = RbLds<D>;
   constexpr int H2 = D / 2;
   constexpr int DT = D / 16;                 // 16-wide value tiles of M^T
@@ -156,13 +161,18 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
     }
   };
 
-  // deferred outputs of the previous unit (thread 0)
+  // deferred outputs of the previous unit: written and read by thread 0 only,
+  // kept in LDS (not registers) across the next unit's staging
+  struct Pend { int64_t unit, sl; int n, a0; uint32_t ord; float sr, dd, om; };
+  static_assert(sizeof(Pend) <= 64, "deferred-output record");
+  Pend* sP = (Pend*)(smem + Lay::oPend);
   bool pend = false;
-  int64_t p_unit = 0, p_sl = 0;
-  int p_n = 0, p_a0 = 0;
-  uint32_t p_ord = 0;
-  float p_sr = 0.f, p_dd = 0.f, p_om = 0.f;
   auto flush = [&](int buf) {
+    const Pend P = *sP;
+    const int64_t p_unit = P.unit, p_sl = P.sl;
+    const int p_n = P.n, p_a0 = P.a0;
+    const uint32_t p_ord = P.ord;
+    const float p_sr = P.sr, p_dd = P.dd, p_om = P.om;
     float Dv = 0.f;
 #pragma unroll
     for (int w2 = 0; w2 < RB_W; ++w2) Dv += sRed[buf * RB_W + w2];
@@ -215,7 +225,6 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
       }
     }
     const int64_t pmid = round_half_even_mid((int)a0, (int)a0 + n);
-    const float pcos = cosT[pmid * H2 + (tid % H2)], psin = sinT[pmid * H2 + (tid % H2)];
     float* Kn = sKn + buf * NMAX;
 
     // ---- staging: K rows (zero past n) with RoPE undone on the way for the k°
@@ -227,67 +236,56 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
       for (int h = 0; h < 16; ++h) kacc[h] = 0.f;
       // K item e: token e / CHP, pair chunk c (rows up to 32 nb, zero past n);
       // V item e: token pair 16 (e / (16 CPR)) + e % 16 (pairs fastest within a
-      // 32-token block), 8-dim chunk (e / 16) % CPR.  Two rounds of every
-      // thread's items are loaded before any is processed.
+      // 32-token block), 8-dim chunk (e / 16) % CPR.  One item of each kind per
+      // thread and round, all its loads issued before any is used (a second
+      // round in flight would not fit the register budget).
       const int nk = 32 * nb * CHP, nv = 16 * nb * CPR;
       const int nmax = nk > nv ? nk : nv;
-      for (int e0 = tid; e0 < nmax; e0 += 2 * RB_T) {
-        uint4 k1[2], k2[2], v0[2], v1[2];
-        float4 c0[2], c1[2], s0[2], s1[2];
+      for (int e = tid; e < nmax; e += RB_T) {
+        const int t = e / CHP;
+        const int tk = t < n ? t : n - 1;
+        const uint4 k1 = *(const uint4*)(Kp + (int64_t)tk * D + c);
+        const uint4 k2 = *(const uint4*)(Kp + (int64_t)tk * D + c + H2);
+        const int64_t ta = a0 + tk;
+        const float4 c0 = *(const float4*)(cosT + ta * H2 + c), c1 = *(const float4*)(cosT + ta * H2 + c + 4);
+        const float4 s0 = *(const float4*)(sinT + ta * H2 + c), s1 = *(const float4*)(sinT + ta * H2 + c + 4);
+        const int cv = (e / 16) % CPR, t0 = 2 * (16 * (e / (16 * CPR)) + e % 16);
+        const int ta0 = t0 < n ? t0 : n - 1, ta1 = t0 + 1 < n ? t0 + 1 : n - 1;
+        const uint4 v0 = *(const uint4*)(Vp + (int64_t)ta0 * D + 8 * cv);
+        const uint4 v1 = *(const uint4*)(Vp + (int64_t)ta1 * D + 8 * cv);
+        if (e < nk) {
+          uint4 ka = k1, kc = k2;
+          if (t >= n) { ka = make_uint4(0, 0, 0, 0); kc = ka; }
+          *(uint4*)(sK + t * Lay::LDK + c) = ka;
+          *(uint4*)(sK + t * Lay::LDK + c + H2) = kc;
+          const uint32_t w1[4] = {ka.x, ka.y, ka.z, ka.w}, w2[4] = {kc.x, kc.y, kc.z, kc.w};
+          const float cs8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+          const float sn8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+          float ss = 0.f;
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int e = e0 + q * RB_T;
-          const int t = e / CHP;
-          const int tk = t < n ? t : n - 1;
-          k1[q] = *(const uint4*)(Kp + (int64_t)tk * D + c);
-          k2[q] = *(const uint4*)(Kp + (int64_t)tk * D + c + H2);
-          const int64_t ta = a0 + tk;
-          c0[q] = *(const float4*)(cosT + ta * H2 + c); c1[q] = *(const float4*)(cosT + ta * H2 + c + 4);
-          s0[q] = *(const float4*)(sinT + ta * H2 + c); s1[q] = *(const float4*)(sinT + ta * H2 + c + 4);
-          const int cv = (e / 16) % CPR, t0 = 2 * (16 * (e / (16 * CPR)) + e % 16);
-          const int ta0 = t0 < n ? t0 : n - 1, ta1 = t0 + 1 < n ? t0 + 1 : n - 1;
-          v0[q] = *(const uint4*)(Vp + (int64_t)ta0 * D + 8 * cv);
-          v1[q] = *(const uint4*)(Vp + (int64_t)ta1 * D + 8 * cv);
-        }
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const int e = e0 + q * RB_T;
-          if (e < nk) {
-            const int t = e / CHP;
-            uint4 ka = k1[q], kc = k2[q];
-            if (t >= n) { ka = make_uint4(0, 0, 0, 0); kc = ka; }
-            *(uint4*)(sK + t * Lay::LDK + c) = ka;
-            *(uint4*)(sK + t * Lay::LDK + c + H2) = kc;
-            const uint32_t w1[4] = {ka.x, ka.y, ka.z, ka.w}, w2[4] = {kc.x, kc.y, kc.z, kc.w};
-            const float cs8[8] = {c0[q].x, c0[q].y, c0[q].z, c0[q].w, c1[q].x, c1[q].y, c1[q].z, c1[q].w};
-            const float sn8[8] = {s0[q].x, s0[q].y, s0[q].z, s0[q].w, s1[q].x, s1[q].y, s1[q].z, s1[q].w};
-            float ss = 0.f;
-#pragma unroll
-            for (int h = 0; h < 8; ++h) {
-              const float a1 = __uint_as_float((h & 1) ? (w1[h >> 1] & 0xffff0000u) : (w1[h >> 1] << 16));
-              const float a2 = __uint_as_float((h & 1) ? (w2[h >> 1] & 0xffff0000u) : (w2[h >> 1] << 16));
-              const float o1 = a1 * cs8[h] + a2 * sn8[h];
-              const float o2 = a2 * cs8[h] - a1 * sn8[h];
-              kacc[h] += o1;
-              kacc[8 + h] += o2;
-              ss += o1 * o1 + o2 * o2;
-            }
-#pragma unroll
-            for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
-            if (t < n && c == 0) Kn[t] = sqrtf(ss);
+          for (int h = 0; h < 8; ++h) {
+            const float a1 = __uint_as_float((h & 1) ? (w1[h >> 1] & 0xffff0000u) : (w1[h >> 1] << 16));
+            const float a2 = __uint_as_float((h & 1) ? (w2[h >> 1] & 0xffff0000u) : (w2[h >> 1] << 16));
+            const float o1 = a1 * cs8[h] + a2 * sn8[h];
+            const float o2 = a2 * cs8[h] - a1 * sn8[h];
+            kacc[h] += o1;
+            kacc[8 + h] += o2;
+            ss += o1 * o1 + o2 * o2;
           }
-          if (e < nv) {
-            const int cv = (e / 16) % CPR, t0 = 2 * (16 * (e / (16 * CPR)) + e % 16);
-            uint4 va = v0[q], vb = v1[q];
-            if (t0 >= n) va = make_uint4(0, 0, 0, 0);
-            if (t0 + 1 >= n) vb = make_uint4(0, 0, 0, 0);
-            const uint32_t pa[4] = {va.x, va.y, va.z, va.w}, pb[4] = {vb.x, vb.y, vb.z, vb.w};
-            const int col = perm32(t0);        // t0 even: t0 + 1 sits at col + 1
 #pragma unroll
-            for (int h = 0; h < 4; ++h) {
-              *(uint32_t*)(sVt + (8 * cv + 2 * h) * Lay::LDV + col) = (pa[h] & 0xffffu) | (pb[h] << 16);
-              *(uint32_t*)(sVt + (8 * cv + 2 * h + 1) * Lay::LDV + col) = (pa[h] >> 16) | (pb[h] & 0xffff0000u);
-            }
+          for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
+          if (t < n && c == 0) Kn[t] = sqrtf(ss);
+        }
+        if (e < nv) {
+          uint4 va = v0, vb = v1;
+          if (t0 >= n) va = make_uint4(0, 0, 0, 0);
+          if (t0 + 1 >= n) vb = make_uint4(0, 0, 0, 0);
+          const uint32_t pa[4] = {va.x, va.y, va.z, va.w}, pb[4] = {vb.x, vb.y, vb.z, vb.w};
+          const int col = perm32(t0);          // t0 even: t0 + 1 sits at col + 1
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            *(uint32_t*)(sVt + (8 * cv + 2 * h) * Lay::LDV + col) = (pa[h] & 0xffffu) | (pb[h] << 16);
+            *(uint32_t*)(sVt + (8 * cv + 2 * h + 1) * Lay::LDV + col) = (pa[h] >> 16) | (pb[h] & 0xffff0000u);
           }
         }
       }
@@ -384,6 +382,8 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
         }
       }
     }
+    // rotation of the representative position (used by the k~ threads after barrier B)
+    const float pcos = cosT[pmid * H2 + (tid % H2)], psin = sinT[pmid * H2 + (tid % H2)];
     __syncthreads();                          // A: token loop done
 
     // ---- token values R_t, A_t (LDS and out, zero up to 32 nb) and their sums ----
@@ -500,14 +500,16 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(Dims dm, const uint16_t* __
       if (lane == 0) sRed[buf * RB_W + w] = con;
       if (tid == 0) {
         pend = true;
-        p_unit = unit;
-        p_sl = (int64_t)lg * 2 * dm.N_c + 2 * a0;
-        p_n = n;
-        p_a0 = (int)a0;
-        p_ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
-        p_sr = sr;
-        p_dd = sa;
-        p_om = om;
+        Pend P;
+        P.unit = unit;
+        P.sl = (int64_t)lg * 2 * dm.N_c + 2 * a0;
+        P.n = n;
+        P.a0 = (int)a0;
+        P.ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+        P.sr = sr;
+        P.dd = sa;
+        P.om = om;
+        *sP = P;
       }
     }
     buf ^= 1;
@@ -527,8 +529,9 @@ hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const 
     auto fn = dm.hpg > 4 ? k_root_bf<DD, true> : k_root_bf<DD, false>;                                      \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);  \
     if (e0 != hipSuccess) return e0;                                                                        \
-    hipLaunchKernelGGL(fn, grid, dim3(RB_T), lds, st, dm, (const uint16_t*)K, (const uint16_t*)V,          \
-                       (const uint16_t*)Q, cosT, sinT, slot_starts, n_slots, tv);                           \
+    hipLaunchKernelGGL(fn, grid, dim3(RB_T), lds, st, (const Dims*)tv.kargs, (const uint16_t*)K,            \
+                       (const uint16_t*)V, (const uint16_t*)Q, cosT, sinT, slot_starts, n_slots,               \
+                       (const TreeView*)((const char*)tv.kargs + 512));                           \
   } while (0)
   if (dm.d == 128) GKV_LAUNCH_ROOT_BF(128); else if (dm.d == 64) GKV_LAUNCH_ROOT_BF(64);
   else return hipErrorInvalidValue;
