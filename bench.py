@@ -30,6 +30,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prune", action="store_true", help="build every tree completely")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention measurement")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, one device-to-device copy of this size (counter calibration)")
     return ap.parse_args()
@@ -74,6 +75,56 @@ def algorithmic_bytes(sh, plan, b):
     hidden = sh.n_seg * sh.T * sh.D * b + sh.T * 4
     out = plan.B_total * (2 * sh.d * b + 8) + (sh.L * sh.G + 1) * 8
     return dict(build=kv + q + rope, segment=hidden, pack=out, total=kv + q + rope + hidden + out)
+
+
+def decode_measure(cfg, sh, case, buf, stream, reps=20, fullkv=True):
+    """Decode attention (eq:app_decode_logit) over the packed cache the step just
+    produced: one query per layer and query head (the last window query), the
+    packed rows plus the window rows, timed with HIP events over ``reps`` calls on
+    the stream the kernels run on.  With ``fullkv`` the same call also runs over
+    the uncompressed context laid out as a packed cache (x = 1, log m_eff = 0)."""
+    import torch
+    from paper_2608_07001_amd import gracekv as gk
+    dev = case["K"].device
+    q = case["Q"][:, :, -1, :].contiguous()
+    out = torch.empty(sh.L, sh.H, sh.d, dtype=torch.float32, device=dev)
+    b = 2 if sh.dtype == "bf16" else 4
+
+    def timed(c, offs, Ko, Vo, lm):
+        ws = torch.zeros(gk.decode_ws_bytes(c), dtype=torch.uint8, device=dev)
+        fn = lambda: gk.decode_attention(c, q, offs, Ko, Vo, lm, case["K"], case["V"], out, ws, stream)
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    def nbytes(entries):
+        return (entries * (2 * sh.d * b + 4) + sh.L * sh.G * sh.W * 2 * sh.d * b + sh.L * sh.H * sh.d * (b + 4)
+                + (sh.L * sh.G + 1) * 8)
+
+    entries = int(buf.offsets[-1].item())
+    ms = timed(cfg, buf.offsets, buf.K_out, buf.V_out, buf.logm_out)
+    gbs = nbytes(entries) / (ms * 1e-3) / 1e9
+    res = {"kernel": "k_decode + k_decode_combine", "ms": ms, "entries": entries, "bytes": nbytes(entries),
+           "achieved_gbs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS, "reps": reps}
+    if fullkv:
+        LG = sh.L * sh.G
+        cfg1 = gk.config_for(L=sh.L, G=sh.G, H=sh.H, d=sh.d, W=sh.W, N_ctx=sh.N_ctx, x=1.0,
+                             dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D)
+        Ko = case["K"][:, :, :sh.N_ctx].reshape(-1, sh.d).contiguous()
+        Vo = case["V"][:, :, :sh.N_ctx].reshape(-1, sh.d).contiguous()
+        lm = torch.zeros(LG * sh.N_ctx, dtype=torch.float32, device=dev)
+        offs = torch.arange(LG + 1, dtype=torch.int64, device=dev) * sh.N_ctx
+        ms1 = timed(cfg1, offs, Ko, Vo, lm)
+        del Ko, Vo, lm
+        gbs1 = nbytes(LG * sh.N_ctx) / (ms1 * 1e-3) / 1e9
+        res.update({"fullkv_ms": ms1, "fullkv_achieved_gbs": gbs1, "speedup_vs_fullkv": ms1 / ms})
+    return res
 
 
 def cpu_baseline(case, sh, budget_s):
@@ -211,6 +262,8 @@ def main():
                      "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": build_gbs / HBM_PEAK_GBS, "traffic": traffic},
     }
+    if not args.no_decode:
+        res["decode_attention"] = decode_measure(cfg, sh, case, buf, stream)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)
     print(json.dumps(res), flush=True)

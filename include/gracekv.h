@@ -58,7 +58,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 5
+#define GRACEKV_ABI_VERSION 6
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -218,6 +218,35 @@ gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void
                             const float* rope_cos, const float* rope_sin, void* trees,
                             int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
                             int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace of gracekv_decode_attention for this configuration (bytes). */
+gracekv_status gracekv_decode_ws_bytes(const gracekv_config* cfg, size_t* ws_bytes);
+
+/* Decode-time attention over the packed cache (App. A.3 eq:app_decode_logit;
+ * App. A.5 "Frontier updates and physical packing": every entry stores k~, v~
+ * and log m_eff, and attention at decode time adds log m_eff to the logit).
+ * For every layer l and query head h, with KV head g = h / (H / G), the query
+ * q[l][h] attends to the packed entries offsets[l*G+g] .. offsets[l*G+g+1] - 1
+ * with logits q.k_i / sqrt(d) + logm_out[i], and to the window rows
+ * N_ctx .. T-1 of K[l][g], V[l][g] (kept exactly, log m_eff = 0); out[l][h]
+ * is the softmax-weighted mean of the values (fp32).
+ *   q          [L][H][d] (cfg->dtype), already rotated to its position
+ *   offsets    [L*G + 1] int64, K_out / V_out [B_total][d] (cfg->dtype),
+ *              logm_out [B_total] fp32: the outputs of gracekv_pack (device);
+ *              offsets outside [0, B_total] are clamped into it, a decreasing
+ *              pair gives an empty row
+ *   K, V       [L][G][T][d] (cfg->dtype): only the window rows are read
+ *   out        [L][H][d] fp32 (device), written
+ *   ws         workspace of gracekv_decode_ws_bytes bytes (partial softmax
+ *              states of the split over entries), 16-byte aligned; calls that
+ *              overlap on one workspace race
+ * Returns GRACEKV_ERR_INVALID_ARG for null or misaligned pointers and
+ * GRACEKV_ERR_WORKSPACE for a short workspace; enqueued on stream, nothing is
+ * allocated or synchronised. */
+gracekv_status gracekv_decode_attention(const gracekv_config* cfg, const void* q, const int64_t* offsets,
+                                        const void* K_out, const void* V_out, const float* logm_out,
+                                        const void* K, const void* V, float* out, void* ws, size_t ws_bytes,
+                                        void* stream);
 
 /* Layout check of the cross-lane instructions used by the kernels: computes
  * a 16x16 product from fixed inputs with the fp32 16x16x4 (which = 0), the

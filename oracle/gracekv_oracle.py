@@ -693,3 +693,50 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
         packed[(l, g)] = dict(k=np.array(ks), v=np.array(vs), pos=np.array(ps, dtype=np.int64),
                               logm=np.array(lm))
     return OracleResult(bud, seg, list(slot_starts), trees, ctxs, ops, ex, counts, packed)
+
+
+# ---------------------------------------------------------------------------
+# Decode over the packed cache (App. A.3 eq:app_decode_logit; App. A.5
+# "Frontier updates and physical packing")
+# ---------------------------------------------------------------------------
+def decode_attention_row(q: np.ndarray, k: np.ndarray, v: np.ndarray, logm: np.ndarray,
+                         k_tail: Optional[np.ndarray] = None, v_tail: Optional[np.ndarray] = None) -> np.ndarray:
+    """One decode query against one (l, g) row of the packed cache: every
+    packed entry i gets the logit q.k_i / sqrt(d) + log m_eff_i
+    (eq:app_decode_logit); the tokens that follow the context (the window, kept
+    exactly: log m_eff = 0) are appended after the packed entries; the output
+    is the softmax-weighted mean of the values.  fp64, literal."""
+    q = np.asarray(q, dtype=F64)
+    d = q.shape[0]
+    keys = [np.asarray(k, dtype=F64).reshape(-1, d)]
+    vals = [np.asarray(v, dtype=F64).reshape(-1, d)]
+    bias = [np.asarray(logm, dtype=F64).reshape(-1)]
+    if k_tail is not None and len(k_tail):
+        keys.append(np.asarray(k_tail, dtype=F64).reshape(-1, d))
+        vals.append(np.asarray(v_tail, dtype=F64).reshape(-1, d))
+        bias.append(np.zeros(len(k_tail), dtype=F64))
+    Kall, Vall, ball = np.concatenate(keys), np.concatenate(vals), np.concatenate(bias)
+    if len(ball) == 0:
+        return np.zeros(d, dtype=F64)
+    logits = np.array([float(np.dot(q, Kall[i])) / math.sqrt(d) + ball[i] for i in range(len(ball))])
+    m = logits.max()
+    w = np.exp(logits - m)
+    return (w[:, None] * Vall).sum(axis=0) / w.sum()
+
+
+def decode_attention(qdec: np.ndarray, offsets: np.ndarray, K_out: np.ndarray, V_out: np.ndarray,
+                     logm_out: np.ndarray, K: np.ndarray, V: np.ndarray, N_ctx: int, G: int,
+                     pairs=None) -> Dict[Tuple[int, int], np.ndarray]:
+    """Decode attention for every (layer l, query head h) in ``pairs`` (all by
+    default): query qdec[l, h] against the packed row of (l, g = h // (H / G))
+    and the window rows N_ctx .. T-1 of K[l, g], V[l, g]."""
+    L, H = qdec.shape[0], qdec.shape[1]
+    hpg = H // G
+    out = {}
+    for (l, h) in (pairs if pairs is not None else [(l, h) for l in range(L) for h in range(H)]):
+        g = h // hpg
+        lg = l * G + g
+        a, b = int(offsets[lg]), int(offsets[lg + 1])
+        out[(l, h)] = decode_attention_row(qdec[l, h], K_out[a:b], V_out[a:b], logm_out[a:b],
+                                           K[l, g, N_ctx:], V[l, g, N_ctx:])
+    return out

@@ -317,6 +317,30 @@ gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* 
                                 pos_out, logm_out, ws, (hipStream_t)stream));
 }
 
+gracekv_status gracekv_decode_ws_bytes(const gracekv_config* c, size_t* ws_bytes) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!ws_bytes) return GRACEKV_ERR_INVALID_ARG;
+  const Dims dm = make_dims(*c, p);
+  *ws_bytes = decode_ws_bytes(dm, decode_parts(dm));
+  return GRACEKV_OK;
+}
+
+gracekv_status gracekv_decode_attention(const gracekv_config* c, const void* q, const int64_t* offsets,
+                                        const void* K_out, const void* V_out, const float* logm_out, const void* K,
+                                        const void* V, float* out, void* ws, size_t ws_bytes, void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!q || !offsets || !K_out || !V_out || !logm_out || !K || !V || !out || !ws) return GRACEKV_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(K_out) || !aligned16(V_out) || !aligned16(K) || !aligned16(V) || !aligned16(ws))
+    return GRACEKV_ERR_INVALID_ARG;
+  const Dims dm = make_dims(*c, p);
+  if (ws_bytes < decode_ws_bytes(dm, decode_parts(dm))) return GRACEKV_ERR_WORKSPACE;
+  return hip_status(launch_decode(dm, q, offsets, K_out, V_out, logm_out, K, V, out, ws, (hipStream_t)stream));
+}
+
 gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out) {
   if (!host_out || which < 0 || which > 3) return GRACEKV_ERR_INVALID_ARG;
   return hip_status(selftest_mfma(which, host_out));

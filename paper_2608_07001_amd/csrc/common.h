@@ -107,6 +107,10 @@ __device__ __forceinline__ int round_half_even_mid(int x0, int x1) {
 }
 
 Dims make_dims(const gracekv_config& c, const gracekv_plan& p);
+size_t decode_ws_bytes(const Dims& dm, int P);
+int decode_parts(const Dims& dm);
+hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out, const void* V_out,
+                         const float* logm_out, const void* K, const void* V, float* out, void* ws, hipStream_t st);
 constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0, TreeView at 512
 hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
 TreeView make_view(void* base, const gracekv_plan& p);

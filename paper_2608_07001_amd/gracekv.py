@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 5          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 6          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
 
@@ -63,7 +63,7 @@ class Plan(ctypes.Structure):
 
 SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
            "gracekv_segment", "gracekv_build_trees", "gracekv_score", "gracekv_select", "gracekv_pack",
-           "gracekv_selftest_mfma"]
+           "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention"]
 
 _lib = None
 
@@ -96,6 +96,8 @@ def lib() -> ctypes.CDLL:
         "gracekv_select": [ctypes.POINTER(Config), P, P, P, S, P],
         "gracekv_pack": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
         "gracekv_selftest_mfma": [ctypes.c_int32, P],
+        "gracekv_decode_ws_bytes": [ctypes.POINTER(Config), ctypes.POINTER(S)],
+        "gracekv_decode_attention": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, S, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -169,6 +171,21 @@ def pack(cfg, K, V, rope_cos, rope_sin, trees, offsets, counts, K_out, V_out, po
     _ok(lib().gracekv_pack(ctypes.byref(cfg), _ptr(K), _ptr(V), _ptr(rope_cos), _ptr(rope_sin), _ptr(trees),
                            _ptr(offsets), _ptr(counts), _ptr(K_out), _ptr(V_out), _ptr(pos_out), _ptr(logm_out),
                            _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)), "pack")
+
+
+def decode_ws_bytes(cfg: Config) -> int:
+    n = ctypes.c_size_t(0)
+    _ok(lib().gracekv_decode_ws_bytes(ctypes.byref(cfg), ctypes.byref(n)), "decode_ws_bytes")
+    return int(n.value)
+
+
+def decode_attention(cfg, q, offsets, K_out, V_out, logm_out, K, V, out, ws, stream=None):
+    """Attention of q [L][H][d] over the packed cache plus the window rows of K, V
+    (eq:app_decode_logit); out [L][H][d] fp32; ``ws``: decode_ws_bytes(cfg) bytes."""
+    _ok(lib().gracekv_decode_attention(ctypes.byref(cfg), _ptr(q), _ptr(offsets), _ptr(K_out), _ptr(V_out),
+                                       _ptr(logm_out), _ptr(K), _ptr(V), _ptr(out), _ptr(ws),
+                                       ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)),
+        "decode_attention")
 
 
 def selftest_mfma(which: int) -> torch.Tensor:

@@ -323,3 +323,46 @@ def small_shape(name="small", L=2, G=2, H=4, d=64, N_ctx=512, W=16, dtype="f32",
     return Shape(name, L=L, G=G, H=H, d=d, N_ctx=N_ctx, W=W, dtype=dtype, x=x,
                  n_segments=n_segments, rope_base=kw.pop("rope_base", 1.0e4),
                  min_gap=kw.pop("min_gap", 8), **kw)
+
+
+def make_packed_cache(shape: Shape, seed: int, B_total: int, r: int, device="cpu",
+                      empty_rows: Sequence[int] = ()) -> dict:
+    """A ragged packed cache of the shape the compression emits, for the decode
+    step: B_total entries split over the L*G rows (r recent tokens each plus a
+    lognormal share, sigma 0.8, of the rest; rows in ``empty_rows`` get none),
+    keys N(0, 1) with the 2 % outlier channels at 10x, values N(0, 1), and
+    log m_eff = 0 for 40 % of the entries (singletons) and log m with m uniform
+    in [2, 128] for the others.  Offsets are int64 [L*G + 1]."""
+    LG = shape.L * shape.G
+    g = _gen("cpu", seed, "packed", shape.name)
+    w = torch.exp(0.8 * torch.randn(LG, generator=g, dtype=torch.float64))
+    for i in empty_rows:
+        w[i] = 0.0
+    base = torch.full((LG,), r, dtype=torch.int64)
+    for i in empty_rows:
+        base[i] = 0
+    rest = B_total - int(base.sum())
+    share = w / w.sum() * rest
+    cnt = base + torch.floor(share).to(torch.int64)
+    left = B_total - int(cnt.sum())
+    order = torch.argsort(share - torch.floor(share), descending=True)
+    cnt[order[:left]] += 1
+    offsets = torch.zeros(LG + 1, dtype=torch.int64)
+    offsets[1:] = torch.cumsum(cnt, 0)
+    dt = torch_dtype(shape.dtype)
+    K = torch.randn(B_total, shape.d, generator=g)
+    n_out = max(1, math.ceil(0.02 * shape.d))
+    K[:, torch.randperm(shape.d, generator=g)[:n_out]] *= 10.0
+    V = torch.randn(B_total, shape.d, generator=g)
+    m = torch.randint(2, 129, (B_total,), generator=g).to(torch.float32)
+    logm = torch.where(torch.rand(B_total, generator=g) < 0.4, torch.zeros(B_total), torch.log(m))
+    return dict(offsets=offsets.to(device), K_out=K.to(dt).to(device), V_out=V.to(dt).to(device),
+                logm_out=logm.to(device))
+
+
+def make_decode_queries(shape: Shape, seed: int, device="cpu", scale: float = 0.125) -> torch.Tensor:
+    """One decode query per (layer, query head), [L][H][d]: N(0, scale^2) per dim
+    (logit std about 2 against the packed keys above for d = 128)."""
+    g = _gen("cpu", seed, "decode_q", shape.name)
+    q = torch.randn(shape.L, shape.H, shape.d, generator=g) * scale
+    return q.to(torch_dtype(shape.dtype)).to(device)

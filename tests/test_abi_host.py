@@ -100,4 +100,8 @@ def test_null_pointers_are_refused_before_any_launch():
     assert lib.gracekv_score(ctypes.byref(c), None, None, None) == -1
     assert lib.gracekv_select(ctypes.byref(c), None, None, None, 0, None) == -1
     assert lib.gracekv_pack(ctypes.byref(c), *([None] * 12), 0, None) == -1
+    assert lib.gracekv_decode_attention(ctypes.byref(c), *([None] * 9), 0, None) == -1
+    n = ctypes.c_size_t(0)
+    assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), None) == -1
+    assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0
     assert lib.gracekv_status_string(-3) == b"budget cannot hold the minimum recent window"

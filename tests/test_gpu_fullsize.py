@@ -18,7 +18,7 @@ import torch
 
 from oracle import gracekv_oracle as O
 from paper_2608_07001_amd import gracekv as gk
-from synth.workloads import CONFIGS, make_case
+from synth.workloads import CONFIGS, make_case, make_decode_queries, make_packed_cache
 
 import gpu_harness as H
 
@@ -159,3 +159,35 @@ def test_parallel_dp_equals_serial_dp_at_full_size(runs):
     J = int(pr.n_slots.item())
     assert int(buf.n_slots.item()) == J
     assert torch.equal(buf.slot_starts[:J + 1].cpu(), pr.slot_starts[:J + 1].cpu())
+
+
+def test_decode_attention_at_full_size(runs):
+    # a packed cache of the benchmarked size (262144 entries over the 256 rows,
+    # seeded), the window rows of the 128K case and one query per head; sampled
+    # (layer, query head) pairs against the oracle
+    case, pr, fu = runs
+    cfg = H.make_cfg(SH, flags=gk.FLAG_PRUNE)
+    p = gk.plan_sizes(cfg)
+    pc = make_packed_cache(SH, 1, p.B_total, p.r, device="cuda", empty_rows=(7,))
+    q = make_decode_queries(SH, 1, device="cuda")
+    out = torch.empty(SH.L, SH.H, SH.d, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(gk.decode_ws_bytes(cfg), dtype=torch.uint8, device="cuda")
+    gk.decode_attention(cfg, q, pc["offsets"], pc["K_out"], pc["V_out"], pc["logm_out"], case["K"], case["V"], out, ws)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    rng = np.random.default_rng(9)
+    pairs = [(0, 0), (1, 28), (SH.L - 1, SH.H - 1)] + [(int(rng.integers(SH.L)), int(rng.integers(SH.H))) for _ in range(13)]
+    offs = pc["offsets"].cpu().numpy()
+    Ko, Vo, lm = H.np32(pc["K_out"]), H.np32(pc["V_out"]), pc["logm_out"].cpu().numpy()
+    worst = 0.0
+    for (l, h) in pairs:
+        g = h // (SH.H // SH.G)
+        lg = l * SH.G + g
+        a, b = int(offs[lg]), int(offs[lg + 1])
+        want = O.decode_attention_row(H.np32(q[l, h]), Ko[a:b], Vo[a:b], lm[a:b],
+                                      H.np32(case["K"][l, g, SH.N_ctx:]), H.np32(case["V"][l, g, SH.N_ctx:]))
+        err = float(np.abs(got[l, h] - want).max())
+        tol = 1e-4 * float(np.abs(want).max()) + 1e-6
+        assert err <= tol, (l, h, err, tol)
+        worst = max(worst, err / float(np.abs(want).max()))
+    print(f"full size decode: {len(pairs)} (l, h) pairs, max rel err {worst:.2e}")
