@@ -150,6 +150,18 @@ __device__ __forceinline__ float row_sum16(float v) {
   return v;
 }
 
+// Last-workgroup hand-off without a device fence.  On this chip a device-scope
+// fence writes back and invalidates the XCD's L2; where the only data the last
+// workgroup reads are counters every workgroup updated with device-scope
+// atomics, it suffices that each thread's atomics are performed before its
+// workgroup takes a ticket (a wait on the vector-memory counter) and that the
+// last workgroup reads the counters with device-coherent loads.
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // s_waitcnt vmcnt(0)
+template <typename T>
+__device__ __forceinline__ T ld_agent(const T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Sum over the four lanes l % 16 + 16 k (one column of the four 16-lane rows),
 // returned to all four: two row-swap permutations, no LDS traffic.  Every
 // lane gets (r0 + r1) + (r2 + r3) in the same order.

@@ -283,15 +283,14 @@ __global__ __launch_bounds__(256) void k_rz_hist(Dims dm, const float* __restric
   }
   __syncthreads();
   if (h[threadIdx.x]) atomicAdd(&R->hist[which][threadIdx.x], h[threadIdx.x]);
-  __threadfence();
+  wait_vm();                                  // this thread's histogram atomics are performed
   __syncthreads();
   if (threadIdx.x == 0) last = atomicAdd(&R->done[which], 1u) == gridDim.x - 1;
   __syncthreads();
   if (last && threadIdx.x == 0) {
-    __threadfence();
     int64_t cum = 0, rank = R->rank[which];
     for (int k = 0; k < 256; ++k) {
-      const int64_t hk = R->hist[which][k];
+      const int64_t hk = ld_agent(&R->hist[which][k]);
       if (cum + hk > rank) {
         R->prefix[which] = prefix | ((uint32_t)k << shift);
         R->rank[which] = rank - cum;
@@ -819,14 +818,14 @@ __global__ __launch_bounds__(256) void k_dp_fix(Dims dm, const float* __restrict
     __syncthreads();
     const int64_t lo = c * DPC + 1, hi = (c + 1) * DPC < N ? (c + 1) * DPC : N;
     dp_run(dm, ws, sc, Fr, lo, hi, lo, Fg(c), c * DPC - 127);
-    __threadfence();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");   // one workgroup: its global writes, visible to itself
     __syncthreads();
     Dprev = 0;
     dirty = true;
     ++nfix;
     if (tid == 0) ws.dlt[c] = 0;
   }
-  __threadfence();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");   // one workgroup: its global writes, visible to itself
   __syncthreads();
   // true F at position p (p >= 0)
   auto Ftrue = [&](int64_t p) -> long long {
@@ -862,7 +861,7 @@ __global__ __launch_bounds__(256) void k_dp_fix(Dims dm, const float* __restrict
   } else if (tid == 0) {
     cur = Ftrue(N);
   }
-  __threadfence();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");   // one workgroup: its global writes, visible to itself
   __syncthreads();
   if (tid == 0) {
     ws.Fdbg[0] = (double)cur / sc;

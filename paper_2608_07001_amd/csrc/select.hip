@@ -163,7 +163,7 @@ __device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
     if (S->mode != SEL_SELECT) break;
     if (pass == 0) {
       int64_t tot = 0;
-      for (int k = 0; k < 256; ++k) tot += (int64_t)S->hist[k];
+      for (int k = 0; k < 256; ++k) tot += (int64_t)ld_agent(&S->hist[k]);
       S->total = tot;
       if (dm.B_free <= 0) { S->mode = SEL_NONE; break; }
       if (tot <= dm.B_free) { S->mode = SEL_ALL; break; }
@@ -173,7 +173,7 @@ __device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
     const int64_t need = S->target - S->above;
     int64_t cum = 0;
     for (int k = 255; k >= 0; --k) {
-      const int64_t hk = (int64_t)S->hist[k];
+      const int64_t hk = (int64_t)ld_agent(&S->hist[k]);
       if (cum + hk >= need) {
         S->prefix |= (uint64_t)k << shift;
         S->above += cum;
@@ -273,14 +273,11 @@ __global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState
   __syncthreads();
   const unsigned hs = h[0][tid] + h[1][tid] + h[2][tid] + h[3][tid];
   if (hs) atomicAdd(&S->hist[tid], (unsigned long long)hs);
-  __threadfence();
+  wait_vm();                                  // this thread's histogram atomics are performed
   __syncthreads();
   if (tid == 0) last = atomicAdd(&S->done, 1u) == gridDim.x - 1;
   __syncthreads();
-  if (last && tid == 0) {
-    __threadfence();
-    sel_scan(dm, S, pass);
-  }
+  if (last && tid == 0) sel_scan(dm, S, pass);   // reads the histogram with device-coherent loads
 }
 
 __global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const SelState* S) {
