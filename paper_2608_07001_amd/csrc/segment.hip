@@ -287,10 +287,16 @@ __global__ __launch_bounds__(256) void k_rz_hist(Dims dm, const float* __restric
   __syncthreads();
   if (threadIdx.x == 0) last = atomicAdd(&R->done[which], 1u) == gridDim.x - 1;
   __syncthreads();
-  if (last && threadIdx.x == 0) {
+  if (!last) return;
+  // the last workgroup: the histogram in one coalesced device-coherent read,
+  // cleared for the next pass, then scanned by one thread
+  h[threadIdx.x] = ld_agent(&R->hist[which][threadIdx.x]);
+  R->hist[which][threadIdx.x] = 0;
+  __syncthreads();
+  if (threadIdx.x == 0) {
     int64_t cum = 0, rank = R->rank[which];
     for (int k = 0; k < 256; ++k) {
-      const int64_t hk = ld_agent(&R->hist[which][k]);
+      const int64_t hk = h[k];
       if (cum + hk > rank) {
         R->prefix[which] = prefix | ((uint32_t)k << shift);
         R->rank[which] = rank - cum;
@@ -298,7 +304,6 @@ __global__ __launch_bounds__(256) void k_rz_hist(Dims dm, const float* __restric
       }
       cum += hk;
     }
-    for (int k = 0; k < 256; ++k) R->hist[which][k] = 0;
     R->done[which] = 0;
     if (pass == 3) R->med[2 * stage + which] = okey_inv(R->prefix[which]);
   }

@@ -156,14 +156,14 @@ __global__ void k_sel_init(Dims dm, SelState* S, int rank_extra) {
   }
 }
 
-// Chooses the digit of pass `pass` from the complete histogram (one thread),
-// then clears the histogram for the next pass.
-__device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
+// Chooses the digit of pass `pass` from the complete histogram hist (a copy in
+// LDS; one thread).
+__device__ void sel_scan(const Dims& dm, SelState* S, int pass, const unsigned long long* hist) {
   do {
     if (S->mode != SEL_SELECT) break;
     if (pass == 0) {
       int64_t tot = 0;
-      for (int k = 0; k < 256; ++k) tot += (int64_t)ld_agent(&S->hist[k]);
+      for (int k = 0; k < 256; ++k) tot += (int64_t)hist[k];
       S->total = tot;
       if (dm.B_free <= 0) { S->mode = SEL_NONE; break; }
       if (tot <= dm.B_free) { S->mode = SEL_ALL; break; }
@@ -173,7 +173,7 @@ __device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
     const int64_t need = S->target - S->above;
     int64_t cum = 0;
     for (int k = 255; k >= 0; --k) {
-      const int64_t hk = (int64_t)ld_agent(&S->hist[k]);
+      const int64_t hk = (int64_t)hist[k];
       if (cum + hk >= need) {
         S->prefix |= (uint64_t)k << shift;
         S->above += cum;
@@ -182,7 +182,6 @@ __device__ void sel_scan(const Dims& dm, SelState* S, int pass) {
       cum += hk;
     }
   } while (0);
-  for (int k = 0; k < 256; ++k) S->hist[k] = 0;
   S->done = 0;
 }
 
@@ -277,7 +276,14 @@ __global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState
   __syncthreads();
   if (tid == 0) last = atomicAdd(&S->done, 1u) == gridDim.x - 1;
   __syncthreads();
-  if (last && tid == 0) sel_scan(dm, S, pass);   // reads the histogram with device-coherent loads
+  if (!last) return;
+  // the last workgroup: the histogram in one coalesced device-coherent read,
+  // cleared for the next pass, then scanned by one thread
+  __shared__ unsigned long long hfull[256];
+  hfull[tid] = ld_agent(&S->hist[tid]);
+  S->hist[tid] = 0;
+  __syncthreads();
+  if (tid == 0) sel_scan(dm, S, pass, hfull);
 }
 
 __global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const SelState* S) {
