@@ -76,10 +76,10 @@ typedef struct {
   int32_t n_min, n_max, n0;                  /* 16, 128, 64 (eq:app_slot_length_defaults) */
   float lam_d, lam_n, c_cut;                 /* 0.25, 0.10, 1.0 (eq:app_segmentation_defaults) */
   float lam_Z, lam_M;                        /* 0.25, 0.75 (eq:app_probe_distortion) */
-  int32_t k_curv;                            /* 16 curvature split candidates */
+  int32_t k_curv;                            /* 16 curvature split candidates (0: midpoint only) */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph, alpha_floor;           /* must be 0 on this path */
-  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL */
+  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | _DP_SERIAL | _UNIFORM_SLOTS */
 } gracekv_config;
 
 /* Budget-aware pruning of the tree build (output unchanged; see gracekv_build_trees). */
@@ -88,6 +88,13 @@ typedef struct {
  * recurrence is run from the true state, one after the other (output
  * unchanged, slower; see gracekv_segment). */
 #define GRACEKV_FLAG_DP_SERIAL 2
+/* Uniform slots of n0 tokens (the last one shorter) instead of the curvature-
+ * guided partition: the segmentation half of the paper's "w/o Curv.
+ * Segmentation" ablation (App. C.4); kappa and b are still computed.  With
+ * k_curv = 0 and lam_kappa = 0 the tree refinement is that ablation's too
+ * (the interval midpoint as the only binary candidate, no curvature reward).
+ * Needs n_min <= n0 <= n_max. */
+#define GRACEKV_FLAG_UNIFORM_SLOTS 4
 
 /* Sizes derived from a config (host only). */
 typedef struct {

@@ -740,3 +740,21 @@ def decode_attention(qdec: np.ndarray, offsets: np.ndarray, K_out: np.ndarray, V
         out[(l, h)] = decode_attention_row(qdec[l, h], K_out[a:b], V_out[a:b], logm_out[a:b],
                                            K[l, g, N_ctx:], V[l, g, N_ctx:])
     return out
+
+
+# ---------------------------------------------------------------------------
+# Ablation without curvature-guided segmentation (App. C.4, "w/o Curv.
+# Segmentation"): uniform slots of the target length, and trees refined with the
+# interval midpoint as the only binary candidate and no curvature reward
+# (Params(k_curv=0, lam_kappa=0))
+# ---------------------------------------------------------------------------
+def uniform_slots(N_c: int, n0: int) -> List[int]:
+    """Slot starts 0, n0, 2 n0, ... over C = [0, N_c); the last slot is shorter
+    when n0 does not divide N_c."""
+    return list(range(0, N_c, n0))
+
+
+def ablation_params(p: Params = Params()) -> Params:
+    """The tree-refinement settings of the ablation: no curvature candidates,
+    no curvature reward."""
+    return dataclasses.replace(p, k_curv=0, lam_kappa=0.0)

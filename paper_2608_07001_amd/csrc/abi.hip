@@ -26,6 +26,7 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.k_curv = c.k_curv;
   d.rows = d.hpg * c.W;
   d.dp_serial = (c.flags & GRACEKV_FLAG_DP_SERIAL) ? 1 : 0;
+  d.uniform_slots = (c.flags & GRACEKV_FLAG_UNIFORM_SLOTS) ? 1 : 0;
   return d;
 }
 
@@ -140,14 +141,18 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
-  if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL)) return GRACEKV_ERR_INVALID_ARG;
+  if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS))
+    return GRACEKV_ERR_INVALID_ARG;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
   if (c->dtype == GRACEKV_F32 && c->d != 64) return GRACEKV_ERR_UNSUPPORTED;   // refinement LDS
   if (c->D_hidden % 8 != 0) return GRACEKV_ERR_UNSUPPORTED;                   // 16-byte hidden rows
   if (c->W > WMAX || c->n_seg > 8) return GRACEKV_ERR_UNSUPPORTED;
   if (c->n_min < 16 || c->n_max > NMAX || c->n_max < c->n_min || c->n0 < 1) return GRACEKV_ERR_UNSUPPORTED;
   if (c->win[0] != 4 || c->win[1] != 8 || c->win[2] != 16) return GRACEKV_ERR_UNSUPPORTED;
-  if (c->k_curv < 1 || c->k_curv > CAND_MAX - 2) return GRACEKV_ERR_UNSUPPORTED;
+  if (c->k_curv < 0 || c->k_curv > CAND_MAX - 2) return GRACEKV_ERR_UNSUPPORTED;
+  // uniform slots: J = ceil(N_c / n0) stays within the slot capacity floor(N_c / n_min) + 1
+  if ((c->flags & GRACEKV_FLAG_UNIFORM_SLOTS) && (c->n0 > c->n_max || c->n0 < c->n_min))
+    return GRACEKV_ERR_UNSUPPORTED;
   const int64_t T = c->N_ctx + c->W;
   if (T > (int64_t)0x7fffffff / 2) return GRACEKV_ERR_UNSUPPORTED;
   const int64_t LG = (int64_t)c->L * c->G;

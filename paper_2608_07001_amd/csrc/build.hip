@@ -679,7 +679,7 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
       // candidate flags over cut positions xi in (a, b)
       for (int t = tid; t < NMAX; t += BT) U.flag[t] = 0;
       __syncthreads();
-      if (tid < nv - 1) {
+      if (dm.k_curv > 0 && tid < nv - 1) {
         const int t = a + tid;                     // curvature position t -> cut t + 1
         const float kt = U.Kap[t];
         int rank = 0;

@@ -28,6 +28,7 @@ struct Dims {
   int k_curv;
   int rows;                      // relevance rows per (l, g): hpg * W
   int dp_serial;                 // segmentation DP: no warm-up guess, every chunk from the true state
+  int uniform_slots;             // slots of n0 tokens instead of the DP partition (ablation)
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).

@@ -874,6 +874,15 @@ __global__ __launch_bounds__(256) void k_dp_fix(Dims dm, const float* __restrict
   }
 }
 
+// Uniform slots of n0 tokens, the last one shorter (ablation without the
+// curvature-guided partition): starts 0, n0, 2 n0, ..., then N_c.
+__global__ void k_uniform_slots(Dims dm, int32_t* slots, int32_t* nslots) {
+  const int64_t J = (dm.N_c + dm.n0 - 1) / dm.n0;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j <= J; j += (int64_t)gridDim.x * blockDim.x)
+    slots[j] = (int32_t)(j < J ? j * dm.n0 : dm.N_c);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *nslots = (int32_t)J;
+}
+
 __global__ void k_seg_empty(int32_t* slots, int32_t* nslots) {
   if (threadIdx.x == 0) { slots[0] = 0; *nslots = 0; }
 }
@@ -994,6 +1003,11 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
     }
     hipLaunchKernelGGL(k_rz_score, dim3((unsigned)((dm.T + 255) / 256)), dim3(256), 0, st, dm, (const float*)kappa,
                        surprisal, (const RzState*)R, bscore);
+  }
+  if (dm.N_c > 0 && dm.uniform_slots) {
+    const int64_t J = (dm.N_c + dm.n0 - 1) / dm.n0;
+    hipLaunchKernelGGL(k_uniform_slots, dim3((unsigned)((J + 256) / 256)), dim3(256), 0, st, dm, slot_starts, n_slots);
+    return hipGetLastError();
   }
   if (dm.N_c > 0) {
     hipLaunchKernelGGL(k_dist2, dim3((unsigned)dm.N_c), dim3(BAND), 0, st, dm, ws);

@@ -25,10 +25,10 @@ def np32(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy()
 
 
-def make_cfg(shape, x=None, flags=0):
+def make_cfg(shape, x=None, flags=0, **hyper):
     return gk.config_for(L=shape.L, G=shape.G, H=shape.H, d=shape.d, W=shape.W, N_ctx=shape.N_ctx,
                          x=float(shape.x if x is None else x), dtype=gk.BF16 if shape.dtype == "bf16" else gk.F32,
-                         n_seg=shape.n_seg, D_hidden=shape.D, flags=flags)
+                         n_seg=shape.n_seg, D_hidden=shape.D, flags=flags, **hyper)
 
 
 def to_dev(case: dict, device="cuda") -> dict:
@@ -36,10 +36,10 @@ def to_dev(case: dict, device="cuda") -> dict:
 
 
 def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Optional[torch.Tensor] = None,
-            omega=True, prune=False) -> dict:
+            omega=True, prune=False, flags=0, **hyper) -> dict:
     """All five calls through the C ABI; returns host copies of every output."""
     sh = case_dev["shape"]
-    cfg = make_cfg(sh, x, gk.FLAG_PRUNE if prune else 0)
+    cfg = make_cfg(sh, x, (gk.FLAG_PRUNE if prune else 0) | flags, **hyper)
     buf = gk.allocate(cfg)
     ss = ns = kp = None
     if slots is not None:
@@ -68,13 +68,13 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
     return out
 
 
-def oracle_run(case: dict, x=None, slots=None, kappa=None, lg_pairs=None) -> O.OracleResult:
+def oracle_run(case: dict, x=None, slots=None, kappa=None, lg_pairs=None, p: O.Params = O.Params()) -> O.OracleResult:
     sh = case["shape"]
     return O.run(np32(case["K"]), np32(case["V"]), np32(case["Q"]), np32(case["rope_cos"]), np32(case["rope_sin"]),
                  np32(case["surprisal"]), np32(case["omega_raw"]),
                  np32(case["hidden"]) if "hidden" in case else None, sh.L, sh.G, sh.H, sh.N_ctx,
                  float(sh.x if x is None else x), kv_dtype=sh.dtype, slot_starts=slots,
-                 kappa=None if kappa is None else np32(kappa).astype(np.float64), lg_pairs=lg_pairs)
+                 kappa=None if kappa is None else np32(kappa).astype(np.float64), lg_pairs=lg_pairs, p=p)
 
 
 # ---------------------------------------------------------------------------

@@ -1,0 +1,44 @@
+"""The ablation without curvature-guided segmentation (App. C.4 "w/o Curv.
+Segmentation": uniform slots of n0 = 64 tokens, the interval midpoint as the
+only binary candidate, no curvature reward) on the GPU against the oracle:
+slots, trees, selected set and packed cache, as in the main parity tests."""
+import numpy as np
+import torch
+import pytest
+
+from oracle import gracekv_oracle as O
+from paper_2608_07001_amd import gracekv as gk
+from synth.workloads import CONFIGS, make_case, small_shape
+
+import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+RTOL_R, RTOL_D, ATOL_D, TAU = 1e-4, 2e-3, 1e-7, 2e-4
+
+
+@pytest.mark.parametrize("shape", [
+    CONFIGS["tiny"],
+    small_shape("abl-bf16", L=2, G=2, H=8, d=128, N_ctx=2000, W=32, dtype="bf16", x=16.0, n_segments=12),
+], ids=["tiny-f32", "bf16-d128"])
+def test_uniform_slots_and_midpoint_trees(shape):
+    case = make_case(shape, 2, with_hidden=True)
+    g = H.gpu_run(H.to_dev(case), flags=gk.FLAG_UNIFORM_SLOTS, k_curv=0, lam_kappa=0.0)
+    N_c = g["plan"].N_c
+    slots = O.uniform_slots(N_c, 64)
+    assert g["slots"] == slots
+    o = H.oracle_run(case, slots=slots, kappa=torch.zeros(shape.T), p=O.ablation_params())
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    assert not st.mismatches, st.mismatches[:10]
+    ga, gs = H.gpu_selected(g)
+    oa, os_ = H.oracle_selected(o, shape.G)
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    print(f"{shape.name} ablation: J {len(slots)} nodes {st.nodes} near-ties {st.near_ties} "
+          f"maxrelD {st.max_rel_D:.2e}; adds {len(oa)} splits {len(os_)} spent {spent} b_used {g['b_used']}")
+    assert g["b_used"] == spent
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
+        offs = g["offsets"].numpy()
+        pos = g["pos_out"].numpy()
+        for (l, gg), pk in o.packed.items():
+            lg = l * shape.G + gg
+            assert np.array_equal(pos[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
