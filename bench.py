@@ -29,6 +29,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prune", action="store_true", help="build every tree completely")
+    ap.add_argument("--ablation-pair-quotas", action="store_true",
+                    help="the paper's w/o-global-allocation ablation: fixed per-(l, g) capacities (complete build)")
     ap.add_argument("--ablation-uniform-slots", action="store_true",
                     help="the paper's w/o-curvature-segmentation ablation: uniform 64-token slots, midpoint-only "
                          "binary candidates, no curvature reward")
@@ -194,8 +196,9 @@ def main():
     case = make_case(sh, args.seed, device=dev)
     cfg = gk.config_for(L=sh.L, G=sh.G, H=sh.H, d=sh.d, W=sh.W, N_ctx=sh.N_ctx, x=sh.x,
                         dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D,
-                        flags=(0 if args.no_prune else gk.FLAG_PRUNE) |
-                              (gk.FLAG_UNIFORM_SLOTS if args.ablation_uniform_slots else 0),
+                        flags=(0 if args.no_prune or args.ablation_pair_quotas else gk.FLAG_PRUNE) |
+                              (gk.FLAG_UNIFORM_SLOTS if args.ablation_uniform_slots else 0) |
+                              (gk.FLAG_PAIR_QUOTAS if args.ablation_pair_quotas else 0),
                         **(dict(k_curv=0, lam_kappa=0.0, n0=64) if args.ablation_uniform_slots else {}))
     buf = gk.allocate(cfg, dev)
     p = buf.plan
@@ -257,8 +260,11 @@ def main():
         "config": {"workload": f"{sh.name}: L={sh.L} G={sh.G} H={sh.H} d={sh.d} N_ctx={sh.N_ctx} W={sh.W} "
                                f"x={sh.x:g} ({sh.dtype})",
                    "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),
-                   "pruned_build": not args.no_prune,
-                   "ablation": "uniform 64-token slots, midpoint-only trees" if args.ablation_uniform_slots else None,
+                   "pruned_build": not (args.no_prune or args.ablation_pair_quotas),
+                   "ablation": ", ".join(x for x, on in (("uniform 64-token slots, midpoint-only trees",
+                                                          args.ablation_uniform_slots),
+                                                         ("fixed per-(l, g) capacities", args.ablation_pair_quotas))
+                                         if on) or None,
                    "tree_nodes": int(gk.tree_arrays(p, buf.trees)["unit_nn"].view(sh.L * sh.G, p.J_cap)
                                      [:, :int(buf.n_slots.item())].sum().item())},
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,

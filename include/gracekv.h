@@ -79,7 +79,7 @@ typedef struct {
   int32_t k_curv;                            /* 16 curvature split candidates (0: midpoint only) */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph, alpha_floor;           /* must be 0 on this path */
-  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | _DP_SERIAL | _UNIFORM_SLOTS */
+  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | _DP_SERIAL | _UNIFORM_SLOTS | _PAIR_QUOTAS */
 } gracekv_config;
 
 /* Budget-aware pruning of the tree build (output unchanged; see gracekv_build_trees). */
@@ -95,6 +95,12 @@ typedef struct {
  * (the interval midpoint as the only binary candidate, no curvature reward).
  * Needs n_min <= n0 <= n_max. */
 #define GRACEKV_FLAG_UNIFORM_SLOTS 4
+/* Fixed per-(l, g) capacities instead of the shared budget: the paper's "w/o
+ * Global Allocation" ablation (App. C.3).  Pair i = l*G + g gets
+ * floor(B_free / (L G)) entries, plus one for i < B_free mod (L G), and runs
+ * the auction on its own ops; budget it leaves unused is not used elsewhere.
+ * Not with GRACEKV_FLAG_PRUNE (whose bounds belong to the shared auction). */
+#define GRACEKV_FLAG_PAIR_QUOTAS 8
 
 /* Sizes derived from a config (host only). */
 typedef struct {

@@ -587,6 +587,33 @@ def select_heap(ops: List[Op], B_free: int) -> List[bool]:
     return executed
 
 
+def pair_quotas(B_free: int, LG: int) -> List[int]:
+    """Fixed per-(l, g) capacities of the "w/o Global Allocation" ablation
+    (App. C.3): B_free split evenly over the L*G pairs, the remainder one entry
+    each to the first pairs in (l, g) order (reading of "fixed layer-KV-head-
+    level capacity limits")."""
+    q, r = divmod(max(B_free, 0), LG)
+    return [q + (1 if i < r else 0) for i in range(LG)]
+
+
+def select_heap_pairs(ops: List[Op], quotas: List[int]) -> List[bool]:
+    """The queue of select_heap run inside every (l, g) pair on the pair's own
+    ops with the pair's own capacity; budget a pair leaves unused is not
+    available to another pair (App. C.3, the ablation's local limits)."""
+    executed = [False] * len(ops)
+    for lg, B in enumerate(quotas):
+        heap = [(-op.key, i) for i, op in enumerate(ops) if op.kind == "add" and op.lg == lg]
+        heapq.heapify(heap)
+        while heap and B > 0:
+            _, i = heapq.heappop(heap)
+            if ops[i].cost <= B:
+                executed[i] = True
+                B -= ops[i].cost
+                for k in ops[i].children:
+                    heapq.heappush(heap, (-ops[k].key, k))
+    return executed
+
+
 # ---------------------------------------------------------------------------
 # Packing (App. A.5 "Frontier updates and physical packing", eq:app_frontier_update)
 # ---------------------------------------------------------------------------
@@ -634,11 +661,13 @@ class OracleResult:
 
 def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ctx, x,
         kv_dtype="f32", p: Params = Params(), slot_starts: Optional[List[int]] = None,
-        kappa: Optional[np.ndarray] = None, lg_pairs=None, do_select=True) -> OracleResult:
+        kappa: Optional[np.ndarray] = None, lg_pairs=None, do_select=True,
+        pair_capacities: bool = False) -> OracleResult:
     """Segment -> build -> score -> select -> pack for one case.  Arrays are
     numpy (any float dtype; converted to fp64).  ``slot_starts``/``kappa`` may be
     given to test the later stages on their own; ``lg_pairs`` restricts the tree
-    build to some (l, g) pairs (then selection is skipped)."""
+    build to some (l, g) pairs (then selection is skipped); ``pair_capacities``
+    runs the auction with fixed per-(l, g) capacities (select_heap_pairs)."""
     bud = budget(L, G, N_ctx, x, p)
     seg = None
     if slot_starts is None or kappa is None:
@@ -661,7 +690,8 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
         return OracleResult(bud, seg, list(slot_starts), trees, ctxs, [], [], np.zeros(0), {})
     omega = normalize_omega(omega_raw, p)
     ops = make_ops(trees, omega, G, J)
-    ex = select_heap(ops, bud.B_free)
+    ex = (select_heap_pairs(ops, pair_quotas(bud.B_free, L * G)) if pair_capacities
+          else select_heap(ops, bud.B_free))
     add_exec: Dict[Tuple[int, int, int], bool] = {}
     split_exec: Dict[Tuple[int, int, int], Dict[int, bool]] = {}
     for op, e in zip(ops, ex):

@@ -27,6 +27,7 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.rows = d.hpg * c.W;
   d.dp_serial = (c.flags & GRACEKV_FLAG_DP_SERIAL) ? 1 : 0;
   d.uniform_slots = (c.flags & GRACEKV_FLAG_UNIFORM_SLOTS) ? 1 : 0;
+  d.pair_quotas = (c.flags & GRACEKV_FLAG_PAIR_QUOTAS) ? 1 : 0;
   return d;
 }
 
@@ -141,8 +142,11 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
-  if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS))
+  if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
+                   GRACEKV_FLAG_PAIR_QUOTAS))
     return GRACEKV_ERR_INVALID_ARG;
+  // the pruning bounds are those of the shared auction
+  if ((c->flags & GRACEKV_FLAG_PAIR_QUOTAS) && (c->flags & GRACEKV_FLAG_PRUNE)) return GRACEKV_ERR_UNSUPPORTED;
   if (c->d != 64 && c->d != 128) return GRACEKV_ERR_UNSUPPORTED;
   if (c->dtype == GRACEKV_F32 && c->d != 64) return GRACEKV_ERR_UNSUPPORTED;   // refinement LDS
   if (c->D_hidden % 8 != 0) return GRACEKV_ERR_UNSUPPORTED;                   // 16-byte hidden rows

@@ -29,6 +29,7 @@ struct Dims {
   int rows;                      // relevance rows per (l, g): hpg * W
   int dp_serial;                 // segmentation DP: no warm-up guess, every chunk from the true state
   int uniform_slots;             // slots of n0 tokens instead of the DP partition (ablation)
+  int pair_quotas;               // the auction with fixed per-(l, g) capacities (ablation)
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).

@@ -415,6 +415,191 @@ __global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used)
   *b_used = dm.B_free - R;
 }
 
+// ---- the auction with fixed per-(l, g) capacities ---------------------------
+// The "w/o Global Allocation" ablation (App. C.3): every (l, g) pair runs the
+// queue of the global auction on its own ops with its own capacity
+// q_lg = floor(B_free / (L G)) (+1 for the first B_free mod (L G) pairs), and
+// budget a pair leaves unused is lost.  One workgroup per pair takes the same
+// exact parallel form as the global select: the cost-weighted radix select of
+// the cut (the pair's ops read from the tree buffer in each of the eight
+// passes), every op above the cut, the group at the cut replayed by one
+// thread, and the best available cost-1 op when one unit is left.
+__global__ __launch_bounds__(256) void k_sel_pairs(Dims dm, TreeView tv, int64_t* __restrict__ spent) {
+  const int lg = blockIdx.x, tid = threadIdx.x, wave = tid >> 6;
+  const int J = *tv.nslots;
+  const int32_t* slot_starts = tv.slots;
+  const int64_t LG = (int64_t)dm.L * dm.G;
+  const int64_t Bf = dm.B_free > 0 ? dm.B_free : 0;
+  const int64_t q = Bf / LG + (lg < Bf % LG ? 1 : 0);
+  const int64_t n0 = (int64_t)lg * 2 * dm.N_c, nn = 2 * dm.N_c;      // the pair's node slots
+  const int64_t u0 = (int64_t)lg * dm.J_cap;                         // ... and units j < J
+  __shared__ unsigned int h[4][256];
+  __shared__ unsigned long long sPrefix;
+  __shared__ long long sAbove, sR;
+  __shared__ int sMode;
+  __shared__ unsigned long long sBest[4];
+  if (tid == 0) { sPrefix = 0; sAbove = 0; sMode = SEL_SELECT; sR = 0; }
+  // op x of the pair: x < nn a Split slot, else the Add of unit x - nn
+  auto op_at = [&](int64_t x, uint64_t& E, int& c) {
+    if (x < nn) {
+      c = tv.sp_cost[n0 + x];
+      E = c ? tv.sp_E[n0 + x] : 0;
+    } else {
+      c = 1;
+      E = tv.add_E[u0 + (x - nn)];
+    }
+  };
+  const int64_t nops = nn + J;
+  for (int pass = 0; pass < 8; ++pass) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w) h[w][tid] = 0;
+    __syncthreads();
+    const int shift = 56 - 8 * pass;
+    const uint64_t pre = sPrefix;
+    for (int64_t x = tid; x < nops; x += 256) {
+      uint64_t E;
+      int c;
+      op_at(x, E, c);
+      if (!c) continue;
+      if (pass > 0 && (E >> (shift + 8)) != (pre >> (shift + 8))) continue;
+      atomicAdd(&h[wave][(E >> shift) & 255u], (unsigned)c);
+    }
+    __syncthreads();
+    h[0][tid] += h[1][tid] + h[2][tid] + h[3][tid];
+    __syncthreads();
+    if (tid == 0) {
+      if (pass == 0) {
+        int64_t tot = 0;
+        for (int k = 0; k < 256; ++k) tot += h[0][k];
+        if (q <= 0) sMode = SEL_NONE;
+        else if (tot <= q) { sMode = SEL_ALL; sR = q - tot; }
+        else if (q == 1) { sMode = SEL_RESID; sR = 1; }
+      }
+      if (sMode == SEL_SELECT) {
+        const int64_t need = (q - 1) - sAbove;     // the cut's rank q - 1 within the pair
+        int64_t cum = 0;
+        for (int k = 255; k >= 0; --k) {
+          const int64_t hk = h[0][k];
+          if (cum + hk >= need) { sPrefix |= (uint64_t)k << shift; sAbove += cum; break; }
+          cum += hk;
+        }
+      }
+    }
+    __syncthreads();
+    if (sMode != SEL_SELECT) break;
+  }
+  const int mode = sMode;
+  const uint64_t theta = sPrefix;
+  // every op above the cut (all of them when the pair's ops fit its capacity)
+  for (int64_t x = tid; x < nops; x += 256) {
+    uint64_t E;
+    int c;
+    op_at(x, E, c);
+    const uint8_t ex = c > 0 && (mode == SEL_ALL || (mode == SEL_SELECT && E > theta));
+    if (x < nn) tv.sp_exec[n0 + x] = ex; else tv.add_exec[u0 + (x - nn)] = ex;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");   // the flags, visible to the workgroup
+  __syncthreads();
+  if (tid == 0 && mode == SEL_SELECT) {
+    // the group at the cut lies in one unit of this pair: the queue rule replayed there
+    int64_t R = q - sAbove;
+    const uint32_t id = 0xFFFFFFFFu - (uint32_t)(theta & 0xFFFFFFFFu);
+    const uint32_t ord = id >> 8;
+    const int j = (int)(ord % (uint32_t)J);
+    const int64_t u = u0 + j;
+    const int64_t base = n0 + 2 * (int64_t)slot_starts[j];
+    int avail[NODE_MAX + 1];
+    int na = 0;
+    avail[na++] = (int)(id & 255u);
+    while (R >= 2 && na > 0) {
+      int bi = 0;
+      uint64_t bk = 0;
+      for (int k = 0; k < na; ++k) {
+        const int loc = avail[k];
+        const uint64_t key = loc == 0 ? make_key(tv.add_U[u], ord * 256u)
+                                      : make_key(tv.sp_U[base + loc - 1], ord * 256u + (uint32_t)loc);
+        if (key > bk) { bk = key; bi = k; }
+      }
+      const int loc = avail[bi];
+      avail[bi] = avail[--na];
+      if (loc == 0) {
+        tv.add_exec[u] = 1;
+        R -= 1;
+        if (tv.node_nch[base] > 0 && tv.sp_E[base] == theta) avail[na++] = 1;
+      } else {
+        const int node = loc - 1;
+        tv.sp_exec[base + node] = 1;
+        R -= tv.sp_cost[base + node];
+        const int c0 = tv.node_child[base + node], nc = tv.node_nch[base + node];
+        for (int k = 0; k < nc; ++k) {
+          const int64_t sl = base + c0 + k;
+          if (tv.node_nch[sl] > 0 && tv.sp_E[sl] == theta) avail[na++] = 1 + c0 + k;
+        }
+      }
+    }
+    sR = R;
+  }
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __syncthreads();
+  if (sR == 1 && mode != SEL_ALL && mode != SEL_NONE) {
+    // one unit left: the best available cost-1 op of the pair (its creating op executed, itself not)
+    uint64_t best = 0;
+    for (int64_t x = tid; x < nops; x += 256) {
+      if (x < nn) {
+        const int64_t i = n0 + x;
+        if (tv.sp_cost[i] != 1 || tv.sp_exec[i]) continue;
+        const int o = (int)x;
+        int lo = 0, hi = J - 1;                  // unit j with 2 a_j <= o < 2 a_{j+1}
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (2 * slot_starts[mid] <= o) lo = mid; else hi = mid - 1;
+        }
+        const int64_t base = n0 + 2 * (int64_t)slot_starts[lo];
+        const int par = tv.node_parent[i];
+        const bool pe = par < 0 ? tv.add_exec[u0 + lo] : tv.sp_exec[base + par];
+        if (!pe) continue;
+        const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)lo;
+        const uint64_t k = make_key(tv.sp_U[i], ord * 256u + 1u + (uint32_t)(i - base));
+        best = k > best ? k : best;
+      } else {
+        const int j = (int)(x - nn);
+        if (tv.add_exec[u0 + j]) continue;
+        const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+        const uint64_t k = make_key(tv.add_U[u0 + j], ord * 256u);
+        best = k > best ? k : best;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint64_t b2 = __shfl_xor(best, o, 64);
+      best = b2 > best ? b2 : best;
+    }
+    if ((tid & 63) == 0) sBest[wave] = best;
+    __syncthreads();
+    if (tid == 0) {
+      uint64_t b = sBest[0];
+      for (int w = 1; w < 4; ++w) b = sBest[w] > b ? sBest[w] : b;
+      if (b) {
+        const uint32_t id = 0xFFFFFFFFu - (uint32_t)(b & 0xFFFFFFFFu);
+        const uint32_t ord = id >> 8, loc = id & 255u;
+        const int j = (int)(ord % (uint32_t)J);
+        if (loc == 0) tv.add_exec[u0 + j] = 1;
+        else tv.sp_exec[n0 + 2 * (int64_t)slot_starts[j] + loc - 1] = 1;
+        sR = 0;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid == 0) spent[lg] = mode == SEL_NONE ? 0 : q - sR;
+}
+
+__global__ void k_sel_pairs_sum(Dims dm, const int64_t* __restrict__ spent, int64_t* b_used) {
+  if (threadIdx.x != 0) return;
+  int64_t s = 0;
+  for (int64_t i = 0; i < (int64_t)dm.L * dm.G; ++i) s += spent[i];
+  *b_used = s;
+}
+
 // the eight radix passes of one cost-weighted select
 static void sel_passes(const Dims& dm, const TreeView& tv, SelState* S, hipStream_t st) {
   const int64_t tot = sel_ops(dm);
@@ -429,6 +614,12 @@ static void sel_passes(const Dims& dm, const TreeView& tv, SelState* S, hipStrea
 }
 
 hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, void* ws, hipStream_t st) {
+  if (dm.pair_quotas) {
+    int64_t* spent = (int64_t*)ws;            // [L*G] spent per pair
+    hipLaunchKernelGGL(k_sel_pairs, dim3((unsigned)(dm.L * dm.G)), dim3(256), 0, st, dm, tv, spent);
+    hipLaunchKernelGGL(k_sel_pairs_sum, dim3(1), dim3(64), 0, st, dm, (const int64_t*)spent, b_used);
+    return hipGetLastError();
+  }
   SelState* S = (SelState*)ws;
   hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, 0);
   const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;

@@ -43,6 +43,7 @@ class Config(ctypes.Structure):
 FLAG_PRUNE = 1
 FLAG_DP_SERIAL = 2
 FLAG_UNIFORM_SLOTS = 4
+FLAG_PAIR_QUOTAS = 8
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",

@@ -68,13 +68,15 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
     return out
 
 
-def oracle_run(case: dict, x=None, slots=None, kappa=None, lg_pairs=None, p: O.Params = O.Params()) -> O.OracleResult:
+def oracle_run(case: dict, x=None, slots=None, kappa=None, lg_pairs=None, p: O.Params = O.Params(),
+               pair_capacities=False) -> O.OracleResult:
     sh = case["shape"]
     return O.run(np32(case["K"]), np32(case["V"]), np32(case["Q"]), np32(case["rope_cos"]), np32(case["rope_sin"]),
                  np32(case["surprisal"]), np32(case["omega_raw"]),
                  np32(case["hidden"]) if "hidden" in case else None, sh.L, sh.G, sh.H, sh.N_ctx,
                  float(sh.x if x is None else x), kv_dtype=sh.dtype, slot_starts=slots,
-                 kappa=None if kappa is None else np32(kappa).astype(np.float64), lg_pairs=lg_pairs, p=p)
+                 kappa=None if kappa is None else np32(kappa).astype(np.float64), lg_pairs=lg_pairs, p=p,
+                 pair_capacities=pair_capacities)
 
 
 # ---------------------------------------------------------------------------

@@ -42,3 +42,35 @@ def test_uniform_slots_and_midpoint_trees(shape):
         for (l, gg), pk in o.packed.items():
             lg = l * shape.G + gg
             assert np.array_equal(pos[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+
+
+@pytest.mark.parametrize("shape,x", [
+    (CONFIGS["tiny"], None),
+    (CONFIGS["tiny"], 20.0),
+    (CONFIGS["tiny"], 28.0),
+    (small_shape("pairs-bf16", L=2, G=2, H=8, d=128, N_ctx=1500, W=32, dtype="bf16", x=16.0, n_segments=10), None),
+    (small_shape("pairs-odd", L=1, G=3, H=3, d=64, N_ctx=700, W=8, x=7.0, n_segments=6), None),
+], ids=["tiny-f32", "tiny-x20", "tiny-x28", "bf16-d128", "f32-3pairs"])
+def test_fixed_pair_capacities(shape, x):
+    # the "w/o Global Allocation" ablation: every (l, g) pair spends its own share
+    case = make_case(shape, 3, with_hidden=True)
+    g = H.gpu_run(H.to_dev(case), x=x, flags=gk.FLAG_PAIR_QUOTAS)
+    o = H.oracle_run(case, x=x, pair_capacities=True)
+    assert g["slots"] == o.slot_starts
+    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
+    assert not st.mismatches, st.mismatches[:10]
+    ga, gs = H.gpu_selected(g)
+    oa, os_ = H.oracle_selected(o, shape.G)
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    quotas = O.pair_quotas(g["plan"].B_free, shape.L * shape.G)
+    per = np.zeros(shape.L * shape.G, dtype=np.int64)
+    for op, e in zip(o.ops, o.executed):
+        per[op.lg] += op.cost if e else 0
+    print(f"{shape.name} pair capacities {quotas[:4]}...: spent {spent} (per pair {per.tolist()[:4]}...), "
+          f"gpu b_used {g['b_used']}, near-ties {st.near_ties}")
+    assert np.all(per <= np.array(quotas))
+    assert g["b_used"] == spent
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
+        offs = g["offsets"].numpy()
+        assert np.array_equal(np.diff(offs), o.counts)

@@ -275,3 +275,56 @@ def test_budget_formulas():
     assert (b.B_total, b.r) == (2097, 8)
     with pytest.raises(ValueError):
         O.budget(32, 8, 8192, 4000.0)          # cannot hold 4 entries per (l, g)
+
+
+# ---- fixed per-(l, g) capacities (the "w/o Global Allocation" ablation) ----
+def _pairs_forest(rng, n_pairs, units_per_pair, max_ops):
+    ops = []
+    for lg in range(n_pairs):
+        sub = _forest(rng, units_per_pair, max_ops)
+        off = len(ops)
+        for o in sub:
+            o.lg = lg
+            o.unit += lg * units_per_pair
+            o.oid += lg * units_per_pair * 256
+            o.key = O.composite_key(o.U, o.oid)
+            o.children = [k + off for k in o.children]
+        ops.extend(sub)
+    return ops
+
+
+def test_pair_quotas_split_the_budget():
+    assert O.pair_quotas(10, 4) == [3, 3, 2, 2]
+    assert O.pair_quotas(8, 4) == [2, 2, 2, 2]
+    assert sum(O.pair_quotas(1001, 7)) == 1001 and O.pair_quotas(-3, 2) == [0, 0]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_pair_auction_is_the_queue_inside_each_pair(seed):
+    # per pair: the literal queue on the pair's ops alone, the naive rescan and
+    # the effective-key cut agree; pairs do not see each other's ops or budget
+    rng = random.Random(100 + seed)
+    n_pairs = 4
+    ops = _pairs_forest(rng, n_pairs, 3, 6)
+    B = rng.randint(0, 40)
+    quotas = O.pair_quotas(B, n_pairs)
+    ex = O.select_heap_pairs(ops, quotas)
+    for lg in range(n_pairs):
+        idx = [i for i, o in enumerate(ops) if o.lg == lg]
+        remap = {i: k for k, i in enumerate(idx)}
+        sub = []
+        for i in idx:
+            o = ops[i]
+            c = O.Op(o.oid, 0, o.unit, o.node, o.kind, o.gain, o.cost, o.U, o.key, [remap[k] for k in o.children])
+            sub.append(c)
+        want = O.select_heap(sub, quotas[lg])
+        assert [ex[i] for i in idx] == want
+        assert want == _naive(sub, quotas[lg]) == _effective_key_cut(sub, quotas[lg])
+        assert sum(o.cost for o, e in zip(sub, want) if e) <= quotas[lg]
+    # a pair's utilities do not change another pair's selection
+    for o in ops:
+        if o.lg == 0:
+            o.U = float(np.float32(o.U * 3.0 + 1.0))
+            o.key = O.composite_key(o.U, o.oid)
+    ex2 = O.select_heap_pairs(ops, quotas)
+    assert [e for e, o in zip(ex, ops) if o.lg > 0] == [e for e, o in zip(ex2, ops) if o.lg > 0]
