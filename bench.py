@@ -36,6 +36,9 @@ def parse():
                          "binary candidates, no curvature reward")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention measurement")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="relevance statistics inside gracekv_build_trees instead of on a second stream during "
+                         "segmentation")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, one device-to-device copy of this size (counter calibration)")
     return ap.parse_args()
@@ -203,16 +206,32 @@ def main():
     buf = gk.allocate(cfg, dev)
     p = buf.plan
     stream = torch.cuda.current_stream()
+    # the relevance row statistics need neither the hidden states nor the slots:
+    # they run on a second stream (default priority) while segmentation runs
+    overlap = not args.no_overlap
+    side = torch.cuda.Stream(device=dev)
+    cfg_b = gk.Config.from_buffer_copy(cfg)
+    if overlap:
+        cfg_b.flags |= gk.FLAG_STATS_READY
 
     def step(ev=None):
         def mark(i):
             if ev is not None:
                 ev[i].record(stream)
         mark(0)
+        if overlap:
+            fork = torch.cuda.Event()
+            fork.record(stream)
+            side.wait_event(fork)
+            gk.relevance_stats(cfg, case["K"], case["Q"], buf.trees, side)
+            join = torch.cuda.Event()
+            join.record(side)
         gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
                    buf.seg_ws, stream)
         mark(1)
-        gk.build_trees(cfg, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
+        if overlap:
+            stream.wait_event(join)
+        gk.build_trees(cfg_b, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
                        buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"])
         mark(2)
         gk.score(cfg, case["omega_raw"], buf.trees, stream)
@@ -261,6 +280,7 @@ def main():
                                f"x={sh.x:g} ({sh.dtype})",
                    "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),
                    "pruned_build": not (args.no_prune or args.ablation_pair_quotas),
+                   "stats_on_second_stream": overlap,
                    "ablation": ", ".join(x for x, on in (("uniform 64-token slots, midpoint-only trees",
                                                           args.ablation_uniform_slots),
                                                          ("fixed per-(l, g) capacities", args.ablation_pair_quotas))

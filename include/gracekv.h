@@ -58,7 +58,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 6
+#define GRACEKV_ABI_VERSION 7
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -79,7 +79,7 @@ typedef struct {
   int32_t k_curv;                            /* 16 curvature split candidates (0: midpoint only) */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph, alpha_floor;           /* must be 0 on this path */
-  int32_t flags;                             /* GRACEKV_FLAG_PRUNE | _DP_SERIAL | _UNIFORM_SLOTS | _PAIR_QUOTAS */
+  int32_t flags;                             /* GRACEKV_FLAG_* below */
 } gracekv_config;
 
 /* Budget-aware pruning of the tree build (output unchanged; see gracekv_build_trees). */
@@ -101,6 +101,10 @@ typedef struct {
  * the auction on its own ops; budget it leaves unused is not used elsewhere.
  * Not with GRACEKV_FLAG_PRUNE (whose bounds belong to the shared auction). */
 #define GRACEKV_FLAG_PAIR_QUOTAS 8
+/* gracekv_build_trees skips the relevance row statistics: the caller has run
+ * gracekv_relevance_stats on the same tree buffer, completed before this call
+ * starts (same stream, or joined with an event). */
+#define GRACEKV_FLAG_STATS_READY 16
 
 /* Sizes derived from a config (host only). */
 typedef struct {
@@ -231,6 +235,18 @@ gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void
                             const float* rope_cos, const float* rope_sin, void* trees,
                             int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
                             int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Pass 1 of the direct relevance (App. A.4 eq:app_attention_probability,
+ * eq:app_direct_relevance) on its own: per (l, g) and probe row the maximum
+ * and partition sum of the logits over the visible range and over C, the
+ * normaliser S_{l,g} and the probe shifts m_q, Z_q(C), written into the tree
+ * buffer (plan.tree_bytes).  It needs neither the hidden states nor the slot
+ * partition, so it can run on a second stream while gracekv_segment runs;
+ * gracekv_build_trees then takes GRACEKV_FLAG_STATS_READY.
+ *   K [L][G][T][d], Q [L][H][W][d] (cfg->dtype), 16-byte aligned; trees as in
+ *   gracekv_build_trees.  Enqueued on stream, nothing allocated. */
+gracekv_status gracekv_relevance_stats(const gracekv_config* cfg, const void* K, const void* Q, void* trees,
+                                       void* stream);
 
 /* Workspace of gracekv_decode_attention for this configuration (bytes). */
 gracekv_status gracekv_decode_ws_bytes(const gracekv_config* cfg, size_t* ws_bytes);

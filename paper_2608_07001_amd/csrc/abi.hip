@@ -143,7 +143,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
   if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
-                   GRACEKV_FLAG_PAIR_QUOTAS))
+                   GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY))
     return GRACEKV_ERR_INVALID_ARG;
   // the pruning bounds are those of the shared auction
   if ((c->flags & GRACEKV_FLAG_PAIR_QUOTAS) && (c->flags & GRACEKV_FLAG_PRUNE)) return GRACEKV_ERR_UNSUPPORTED;
@@ -271,7 +271,9 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
   if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (!(c->flags & GRACEKV_FLAG_STATS_READY) &&
+      launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess)
+    return GRACEKV_ERR_HIP;
   auto build = [&](int mode) {
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
   };
@@ -324,6 +326,17 @@ gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* 
   Dims dm = make_dims(*c, p);
   return hip_status(launch_pack(dm, K, V, rope_cos, rope_sin, make_view(trees, p), offsets, counts, K_out, V_out,
                                 pos_out, logm_out, ws, (hipStream_t)stream));
+}
+
+gracekv_status gracekv_relevance_stats(const gracekv_config* c, const void* K, const void* Q, void* trees,
+                                       void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!K || !Q || !trees || !aligned16(K) || !aligned16(Q) || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
+  const Dims dm = make_dims(*c, p);
+  return hip_status(launch_rowstats(dm, K, Q, make_view(trees, p), (float4*)((char*)trees + p.off_partial),
+                                    (hipStream_t)stream));
 }
 
 gracekv_status gracekv_decode_ws_bytes(const gracekv_config* c, size_t* ws_bytes) {

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 6          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 7          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
 
@@ -44,6 +44,7 @@ FLAG_PRUNE = 1
 FLAG_DP_SERIAL = 2
 FLAG_UNIFORM_SLOTS = 4
 FLAG_PAIR_QUOTAS = 8
+FLAG_STATS_READY = 16
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",
@@ -65,7 +66,7 @@ class Plan(ctypes.Structure):
 
 SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
            "gracekv_segment", "gracekv_build_trees", "gracekv_score", "gracekv_select", "gracekv_pack",
-           "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention"]
+           "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention", "gracekv_relevance_stats"]
 
 _lib = None
 
@@ -99,6 +100,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_pack": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
         "gracekv_selftest_mfma": [ctypes.c_int32, P],
         "gracekv_decode_ws_bytes": [ctypes.POINTER(Config), ctypes.POINTER(S)],
+        "gracekv_relevance_stats": [ctypes.POINTER(Config), P, P, P, P],
         "gracekv_decode_attention": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, S, P],
     }
     for name, args in sig.items():
@@ -158,6 +160,12 @@ def build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, t
     _ok(lib().gracekv_build_trees(ctypes.byref(cfg), _ptr(K), _ptr(V), _ptr(Q), _ptr(rope_cos), _ptr(rope_sin),
                                   _ptr(slot_starts), _ptr(n_slots), _ptr(kappa), _ptr(omega_raw), _ptr(trees), None,
                                   0, _stream(stream)), "build_trees")
+
+
+def relevance_stats(cfg, K, Q, trees, stream=None):
+    """Relevance row statistics into the tree buffer (see GRACEKV_FLAG_STATS_READY)."""
+    _ok(lib().gracekv_relevance_stats(ctypes.byref(cfg), _ptr(K), _ptr(Q), _ptr(trees), _stream(stream)),
+        "relevance_stats")
 
 
 def score(cfg, omega_raw, trees, stream=None):

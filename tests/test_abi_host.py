@@ -86,7 +86,7 @@ def test_plan_rejections():
     assert e.value.status == -3
     for bad, code in [(dict(lambda_graph=0.3), -2), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
                       (dict(W=65), -2), (dict(H=30), -1), (dict(x=0.5), -1), (dict(n_min=8), -2),
-                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=16), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
+                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=32), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
         with pytest.raises(gk.GraceKVError) as e:
             gk.plan_sizes(_cfg(**bad))
         assert e.value.status == code, bad
@@ -101,6 +101,7 @@ def test_null_pointers_are_refused_before_any_launch():
     assert lib.gracekv_select(ctypes.byref(c), None, None, None, 0, None) == -1
     assert lib.gracekv_pack(ctypes.byref(c), *([None] * 12), 0, None) == -1
     assert lib.gracekv_decode_attention(ctypes.byref(c), *([None] * 9), 0, None) == -1
+    assert lib.gracekv_relevance_stats(ctypes.byref(c), None, None, None, None) == -1
     n = ctypes.c_size_t(0)
     assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), None) == -1
     assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0

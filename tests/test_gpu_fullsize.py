@@ -1,6 +1,8 @@
-"""Parity at the benchmarked size: the 8B-shaped 128K-token cache at 128x
-(L=32, G=8, H=32, d=128, W=64, bf16), run exactly as bench.py runs it
-(segmentation, budget-pruned tree build, score, select, pack).
+"""Parity at full size: the 8B-shaped 128K-token cache at 128x (L=32, G=8,
+H=32, d=128, W=64, bf16), run exactly as bench.py runs it (segmentation,
+budget-pruned tree build, score, select, pack), and the 70B-shaped single-GPU
+share at 32K and 32x (L=80, G=8, H=64: eight query heads per KV head, 512
+lognormal segments, the widest auction).
 
 The oracle cannot run the whole case, so:
   * sampled outputs are recomputed one by one: the token values R^tok and
@@ -24,11 +26,9 @@ import gpu_harness as H
 
 pytestmark = pytest.mark.gpu
 
-SH = CONFIGS["8b-128k"]
 RTOL_R = 1e-4
 RTOL_D, ATOL_D = 2e-3, 1e-7
 TAU = 2e-4
-LG_SAMPLES = [(0, 0), (17, 5)]
 
 
 def _run(case, cfg, slots=None, n_slots=None, kappa=None):
@@ -40,12 +40,20 @@ def _run(case, cfg, slots=None, n_slots=None, kappa=None):
     return buf
 
 
-@pytest.fixture(scope="module")
-def runs():
+@pytest.fixture(scope="module", params=["8b-128k", "70b-32k"])
+def runs(request):
+    global SH
+    SH = CONFIGS[request.param]
     case = make_case(SH, 0, device="cuda")
     pruned = _run(case, H.make_cfg(SH, flags=gk.FLAG_PRUNE))
     full = _run(case, H.make_cfg(SH), slots=pruned.slot_starts, n_slots=pruned.n_slots, kappa=pruned.kappa)
-    return case, pruned, full
+    yield case, pruned, full
+    del case, pruned, full
+    torch.cuda.empty_cache()
+
+
+def _lg_samples():
+    return [(0, 0), ((SH.L * 17) // 32, 5)]
 
 
 def _unit_view(arr, p, lg, j, a0, n):
@@ -112,7 +120,7 @@ def test_sampled_token_values_and_trees_at_full_size(runs):
     rng = np.random.default_rng(5)
     st = H.TreeStats()
     worstR = worstA = 0.0
-    for (l, g) in LG_SAMPLES:
+    for (l, g) in _lg_samples():
         lg = l * SH.G + g
         ctx = O.lg_context(H.np32(case["K"][l, g]), H.np32(case["V"][l, g]),
                            H.np32(case["Q"][l, g * hpg:(g + 1) * hpg]), cos, sin, kappa, SH.N_ctx, p.N_c)
@@ -137,7 +145,8 @@ def test_sampled_token_values_and_trees_at_full_size(runs):
 
 def test_sampled_curvature_window_at_full_size(runs):
     case, pr, fu = runs
-    s, e = 70000, 72048                         # positions compared; 16 rows of context on each side
+    s = SH.N_ctx // 2 + 4464                    # positions compared; 16 rows of context on each side
+    e = s + 2048
     hid = case["hidden"][:, s - 16:e + 16].float().cpu().numpy()
     hbars = [O.normalize_hidden(hid[k]) for k in range(hid.shape[0])]
     kap = O.stabilized_curvature(hbars)[16:-16]

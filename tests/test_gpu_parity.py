@@ -315,3 +315,52 @@ def test_budget_with_nothing_free():
     assert offs[-1] == bud.B_total
     for lg in range(sh.L * sh.G):
         assert np.array_equal(g["pos_out"].numpy()[offs[lg]:offs[lg + 1]], np.arange(bud.N_c, sh.N_ctx))
+
+
+def test_relevance_stats_on_a_second_stream_give_the_same_result():
+    # gracekv_relevance_stats on a side stream during segmentation, then
+    # gracekv_build_trees with GRACEKV_FLAG_STATS_READY: every output equal to
+    # the one-stream pipeline bit for bit
+    from paper_2608_07001_amd import gracekv as gk
+    sh = small_shape("overlap", L=2, G=2, H=8, d=128, N_ctx=1800, W=32, dtype="bf16", x=8.0, n_segments=10)
+    case = H.to_dev(make_case(sh, 6, with_hidden=True))
+    cfg = H.make_cfg(sh, flags=gk.FLAG_PRUNE)
+    outs = []
+    for overlap in (False, True):
+        buf = gk.allocate(cfg)
+        main = torch.cuda.current_stream()
+        cfg_b = gk.Config.from_buffer_copy(cfg)
+        if overlap:
+            side = torch.cuda.Stream()
+            fork = torch.cuda.Event()
+            fork.record(main)
+            side.wait_event(fork)
+            gk.relevance_stats(cfg, case["K"], case["Q"], buf.trees, side)
+            join = torch.cuda.Event()
+            join.record(side)
+            cfg_b.flags |= gk.FLAG_STATS_READY
+        gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
+                   buf.seg_ws, main)
+        if overlap:
+            main.wait_event(join)
+        gk.build_trees(cfg_b, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
+                       buf.n_slots, buf.kappa, buf.trees, main, omega_raw=case["omega_raw"])
+        gk.score(cfg, case["omega_raw"], buf.trees, main)
+        gk.select(cfg, buf.trees, buf.b_used, buf.sel_ws, main)
+        gk.pack(cfg, case["K"], case["V"], case["rope_cos"], case["rope_sin"], buf.trees, buf.offsets, buf.counts,
+                buf.K_out, buf.V_out, buf.pos_out, buf.logm_out, buf.pack_ws, main)
+        torch.cuda.synchronize()
+        n = int(buf.offsets[-1].item())
+        J = int(buf.n_slots.item())
+        p = buf.plan
+        arr = gk.tree_arrays(p, buf.trees)
+        LG = sh.L * sh.G
+        # what every run writes: the Add keys and flags of the units, the token
+        # values, the packed cache (node slots past a unit's tree are not written)
+        tokR = buf.trees[p.off_tok_R:p.off_tok_R + LG * p.N_c * 4].view(torch.float32)
+        outs.append({"add_E": arr["add_E"].view(LG, p.J_cap)[:, :J].cpu(),
+                     "add_exec": arr["add_exec"].view(LG, p.J_cap)[:, :J].cpu(), "tok_R": tokR.cpu(),
+                     "K_out": buf.K_out[:n].cpu(), "V_out": buf.V_out[:n].cpu(), "pos": buf.pos_out[:n].cpu(),
+                     "logm": buf.logm_out[:n].cpu(), "offsets": buf.offsets.cpu(), "b_used": buf.b_used.cpu()})
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
