@@ -59,6 +59,14 @@ class Params:
     lam_kappa: float = 0.05        # eq:app_binary_split
     beta_frac: float = 0.1         # eq:app_value_prototype
     eps: float = 1e-6              # every unstated epsilon (reading A6)
+    # multi-hop relevance (App. A.4): off on the hot path (the paper's "w/o MH"
+    # setting); the paper's default weight is 0.3
+    lam_graph: float = 0.0         # eq:app_bottom_up_value
+    eta_seed: float = 0.9          # cumulative seed mass
+    m_seed: int = 64               # at most this many seeds per hop
+    r_hop: int = 2                 # propagation steps
+    rho_hop: float = 0.5           # inter-hop decay, eq:app_diffused_relevance
+    graph_rhos: Tuple[float, ...] = (0.50, 0.75)   # relative depths of the propagation layers
 
 
 def f32(x) -> float:
@@ -332,6 +340,80 @@ def relevance(K: np.ndarray, Qg: np.ndarray, N_ctx: int, N_c: int, p: Params = P
             pi = e / e.sum()
             s += pi[:N_c]
     return s / (s.sum() + p.eps), s
+
+
+# ---------------------------------------------------------------------------
+# Multi-hop relevance (App. A.4 eq:app_global_seed_score, eq:app_hop_propagation,
+# eq:app_diffused_relevance, eq:app_bottom_up_value)
+# ---------------------------------------------------------------------------
+def graph_layer_indices(L: int, p: Params = Params()) -> List[int]:
+    """The propagation layers: relative depths 0.50 and 0.75, the same
+    rounding as the segmentation layers (eq:app_seg_layers)."""
+    return seg_layer_indices(L, p.graph_rhos)
+
+
+def select_seeds(score: np.ndarray, p: Params = Params()) -> Tuple[List[int], np.ndarray]:
+    """Positions in descending score (ties to the smaller position), taken until
+    their cumulative share of the total score reaches eta_seed (the position
+    that reaches it is included), at most m_seed of them, zero scores never;
+    weights proportional to the score, normalised over the seeds."""
+    score = np.asarray(score, dtype=F64)
+    tot = score.sum()
+    if tot <= 0:
+        return [], np.zeros(0)
+    order = sorted(range(len(score)), key=lambda t: (-score[t], t))
+    seeds, cum = [], 0.0
+    for t in order:
+        if len(seeds) >= p.m_seed or score[t] <= 0 or cum >= p.eta_seed:
+            break
+        seeds.append(t)
+        cum += score[t] / tot
+    w = score[seeds]
+    return seeds, w / w.sum()
+
+
+def hop_scores(Kl: Dict[Tuple[int, int], np.ndarray], Qgraph: Dict[Tuple[int, int], np.ndarray], G: int, hpg: int,
+               seeds: List[int], w: np.ndarray, N_c: int) -> np.ndarray:
+    """eq:app_hop_propagation: d_t = sum over the propagation layers l, KV
+    heads g, query heads h of g and seeds u of w_u pi_{u,t}, with pi the
+    softmax of the query at position u (layer l, head h) over its causal range
+    [0, u]; t in C.  ``Kl[(l, g)]`` [T, d] keys, ``Qgraph[(l, h)]`` [T, d]
+    queries of every position."""
+    d = np.zeros(N_c, dtype=F64)
+    layers = sorted({l for (l, _) in Kl})
+    for l in layers:
+        for g in range(G):
+            K = Kl[(l, g)]
+            dim = K.shape[1]
+            for h in range(g * hpg, (g + 1) * hpg):
+                for u, wu in zip(seeds, w):
+                    lg = K[:u + 1] @ Qgraph[(l, h)][u] / math.sqrt(dim)
+                    e = np.exp(lg - lg.max())
+                    pi = e / e.sum()
+                    n = min(u + 1, N_c)
+                    d[:n] += wu * pi[:n]
+    return d
+
+
+def multi_hop(shat: Dict[Tuple[int, int], np.ndarray], Kl, Qgraph, G: int, hpg: int, N_c: int,
+              p: Params = Params()) -> np.ndarray:
+    """d-hat of eq:app_diffused_relevance.  Hop 1 seeds from the global seed
+    score S-hat (eq:app_global_seed_score: mean of s-hat over every (l, g),
+    normalised over C); after each hop the scores at the current and earlier
+    seeds are set to zero and the next seeds are taken from that hop's scores,
+    weighted by them; d = sum_k rho^(k-1) d^(k), d-hat = d / (sum_C d + eps)."""
+    S = np.mean(np.stack([shat[k] for k in sorted(shat)]), axis=0)
+    S = S / (S.sum() + p.eps)
+    seeds, w = select_seeds(S, p)
+    used: List[int] = []
+    dsum = np.zeros(N_c, dtype=F64)
+    for k in range(p.r_hop):
+        dk = hop_scores(Kl, Qgraph, G, hpg, seeds, w, N_c) if seeds else np.zeros(N_c)
+        used += seeds
+        dk[used] = 0.0
+        dsum += p.rho_hop ** k * dk
+        seeds, w = select_seeds(dk, p)
+    return dsum / (dsum.sum() + p.eps)
 
 
 def lg_context(K: np.ndarray, V: np.ndarray, Qg: np.ndarray, cos: np.ndarray, sin: np.ndarray,
@@ -662,12 +744,15 @@ class OracleResult:
 def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ctx, x,
         kv_dtype="f32", p: Params = Params(), slot_starts: Optional[List[int]] = None,
         kappa: Optional[np.ndarray] = None, lg_pairs=None, do_select=True,
-        pair_capacities: bool = False) -> OracleResult:
+        pair_capacities: bool = False, Qgraph: Optional[np.ndarray] = None) -> OracleResult:
     """Segment -> build -> score -> select -> pack for one case.  Arrays are
     numpy (any float dtype; converted to fp64).  ``slot_starts``/``kappa`` may be
     given to test the later stages on their own; ``lg_pairs`` restricts the tree
     build to some (l, g) pairs (then selection is skipped); ``pair_capacities``
-    runs the auction with fixed per-(l, g) capacities (select_heap_pairs)."""
+    runs the auction with fixed per-(l, g) capacities (select_heap_pairs).
+    With p.lam_graph > 0, ``Qgraph`` [len(graph layers)][H][T][d] holds the
+    queries of every position at the propagation layers and the token values
+    mix in the multi-hop relevance (eq:app_bottom_up_value)."""
     bud = budget(L, G, N_ctx, x, p)
     seg = None
     if slot_starts is None or kappa is None:
@@ -681,9 +766,18 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
     trees: Dict[Tuple[int, int, int], List[Node]] = {}
     ctxs: Dict[Tuple[int, int], LGContext] = {}
     for (l, g) in pairs:
-        c = lg_context(K[l, g], V[l, g], Q[l, g * hpg:(g + 1) * hpg], rope_cos, rope_sin, kappa,
-                       N_ctx, bud.N_c, p)
-        ctxs[(l, g)] = c
+        ctxs[(l, g)] = lg_context(K[l, g], V[l, g], Q[l, g * hpg:(g + 1) * hpg], rope_cos, rope_sin, kappa,
+                                  N_ctx, bud.N_c, p)
+    if p.lam_graph > 0:
+        assert Qgraph is not None and lg_pairs is None, "multi-hop relevance needs every (l, g) and the queries"
+        gl = graph_layer_indices(L, p)
+        Kl = {(l, g): np.asarray(K[l, g], dtype=F64) for l in gl for g in range(G)}
+        Qd = {(l, h): np.asarray(Qgraph[i, h], dtype=F64) for i, l in enumerate(gl) for h in range(H)}
+        dhat = multi_hop({k: c.R for k, c in ctxs.items()}, Kl, Qd, G, hpg, bud.N_c, p)
+        for c in ctxs.values():
+            c.R = (1.0 - p.lam_graph) * c.R + p.lam_graph * dhat
+    for (l, g) in pairs:
+        c = ctxs[(l, g)]
         for j in range(J):
             trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p)
     if not do_select or lg_pairs is not None:

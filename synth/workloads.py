@@ -366,3 +366,42 @@ def make_decode_queries(shape: Shape, seed: int, device="cpu", scale: float = 0.
     g = _gen("cpu", seed, "decode_q", shape.name)
     q = torch.randn(shape.L, shape.H, shape.d, generator=g) * scale
     return q.to(torch_dtype(shape.dtype)).to(device)
+
+
+def graph_layers(shape: Shape) -> List[int]:
+    """Layers whose queries of every position the multi-hop relevance reads:
+    relative depths 0.50 and 0.75 (rounded like the segmentation depths)."""
+    out: List[int] = []
+    for rho in (0.50, 0.75):
+        l = min(int(math.floor(rho * shape.L)), shape.L - 1)
+        if l not in out:
+            out.append(l)
+    return out
+
+
+def make_graph_queries(shape: Shape, seed: int, K: torch.Tensor, cos: torch.Tensor, sin: torch.Tensor,
+                       device="cpu") -> torch.Tensor:
+    """Post-RoPE queries of every position [len(graph_layers)][H][T][d] at the
+    propagation layers: the query of position t (head h) is
+    q°_t = 0.5 z + 0.5 k°_{tau(t)} with tau(t) uniform in [0, t] (a long-range
+    reference) and z ~ N(0, I) scaled like the keys, rotated at t, then scaled
+    per (layer, head) so that the logits against a sample of context keys have
+    standard deviation 2."""
+    L, G, H, T, d, N = shape.L, shape.G, shape.H, shape.T, shape.d, shape.N_ctx
+    hpg = H // G
+    gl = graph_layers(shape)
+    out = torch.empty(len(gl), H, T, d, dtype=torch_dtype(shape.dtype), device=device)
+    pos = torch.arange(T, device=device)
+    for i, l in enumerate(gl):
+        for g in range(G):
+            k = K[l, g].to(device).float()
+            kr = _rotate(k, cos, -sin)                 # the keys before rotation
+            samp = k[:N][:: max(1, N // 512)]
+            for hh in range(hpg):
+                gen = _gen(device, seed, shape.name, "graph_q", l, g * hpg + hh)
+                tau = (torch.rand(T, generator=gen, device=device) * (pos + 1).float()).long().clamp_max(T - 1)
+                qr = 0.5 * torch.randn(T, d, generator=gen, device=device) * kr.std() + 0.5 * kr[tau]
+                q = _rotate(qr, cos, sin)
+                lgt = (q[:: max(1, T // 512)] @ samp.t().contiguous()) / math.sqrt(d)
+                out[i, g * hpg + hh] = (q * (2.0 / lgt.std().clamp_min(1e-12))).to(out.dtype)
+    return out
