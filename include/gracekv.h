@@ -16,8 +16,10 @@
  *     are both the direct-relevance probes and the distortion probes.
  *   - The recent window r and the budgets follow eq:app_total_budget,
  *     eq:app_compressible_context and eq:app_free_budget with the singleton
- *     floor disabled (alpha = 0) and lambda_graph = 0 (the paper's "w/o SF"
- *     and "w/o MH" settings).  Compressible context C = [0, N_c), N_c = N_ctx - r.
+ *     floor disabled (alpha = 0, the paper's "w/o SF" setting).  The token
+ *     values are the direct relevance alone when lambda_graph = 0 (the "w/o MH"
+ *     setting) and mix in the multi-hop relevance when lambda_graph > 0
+ *     (gracekv_build_trees).  Compressible context C = [0, N_c), N_c = N_ctx - r.
  *   - Every pointer argument except `cfg`, `plan` and host-side outputs is a
  *     DEVICE pointer owned by the caller; the library never allocates, frees or
  *     synchronises device memory (gracekv_plan reports every size).  All device
@@ -58,7 +60,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 7
+#define GRACEKV_ABI_VERSION 8
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -78,7 +80,9 @@ typedef struct {
   float lam_Z, lam_M;                        /* 0.25, 0.75 (eq:app_probe_distortion) */
   int32_t k_curv;                            /* 16 curvature split candidates (0: midpoint only) */
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
-  float lambda_graph, alpha_floor;           /* must be 0 on this path */
+  float lambda_graph;                        /* multi-hop weight in [0, 1]: 0 (direct relevance
+                                                only) or e.g. 0.3 (App. A.4 eq:app_bottom_up_value) */
+  float alpha_floor;                         /* must be 0 (no singleton floor) */
   int32_t flags;                             /* GRACEKV_FLAG_* below */
 } gracekv_config;
 
@@ -126,6 +130,7 @@ typedef struct {
          off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate,
          off_work, off_wctr, off_proto, off_proto_logm;
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
+  size_t build_ws_bytes;   /* workspace of gracekv_build_trees: 0 unless lambda_graph > 0 */
 } gracekv_plan;
 
 /* GRACEKV_ABI_VERSION of the compiled library. */
@@ -136,8 +141,9 @@ gracekv_status gracekv_default_config(gracekv_config* cfg);
 
 /* Validates cfg and fills plan.  Returns GRACEKV_ERR_BUDGET when the budget
  * cannot hold a recent window of r_min entries per (layer, KV head)
- * (App. A.1), GRACEKV_ERR_UNSUPPORTED for lambda_graph != 0 or
- * alpha_floor != 0 or shapes outside the documented limits. */
+ * (App. A.1), GRACEKV_ERR_INVALID_ARG for lambda_graph outside [0, 1],
+ * GRACEKV_ERR_UNSUPPORTED for alpha_floor != 0 or shapes outside the
+ * documented limits. */
 gracekv_status gracekv_plan_sizes(const gracekv_config* cfg, gracekv_plan* plan);
 
 /* Human-readable name of a status. */
@@ -191,7 +197,24 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  *              and its log m_eff (fp32), which pack copies for a root on the
  *              frontier; the last 1024 bytes hold a device copy of the kernel
  *              arguments, rewritten in stream order by every call.
- *   ws         unused (pass NULL, 0); reserved.
+ *   Q_graph    [n_graph][H][T][d] (cfg->dtype) post-RoPE queries of every
+ *              position at the propagation layers floor(0.50 L) and
+ *              floor(0.75 L) (each capped at L - 1, a repeat dropped, so n_graph
+ *              is 1 or 2); read only when lambda_graph > 0 (else pass NULL)
+ *   ws         plan.build_ws_bytes of workspace when lambda_graph > 0 (NULL, 0
+ *              otherwise); its contents need no initialisation
+ * Multi-hop relevance (lambda_graph > 0; App. A.4 eq:app_global_seed_score,
+ * eq:app_hop_propagation, eq:app_diffused_relevance, eq:app_bottom_up_value):
+ * the seed score is the mean of s-hat over every (l, g); seeds are taken in
+ * descending score (ties to the smaller position) until their cumulative share
+ * of the total reaches 0.9 (the one reaching it included), at most 64, weighted
+ * by their normalised scores; hop k sums, over the propagation layers, KV
+ * heads, their query heads and the seeds u, w_u times the causal attention
+ * probability of the query at u (range [0, u]) on each token of C; the scores
+ * at the current and earlier seeds are then zeroed and the next hop seeds from
+ * them; d = d^(1) + 0.5 d^(2), d-hat = d / (sum_C d + eps), and every token
+ * value becomes (1 - lambda_graph) s-hat + lambda_graph d-hat.  The relevance
+ * and roots are evaluated twice (once for s-hat, once with the mix).
  * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
  * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops
  * known so far gives theta_lb, the (B_free-1)-th largest effective key among
@@ -201,7 +224,7 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  * split nor on the final frontier, so score, select and pack give the same
  * result as the full build. */
 gracekv_status gracekv_build_trees(const gracekv_config* cfg, const void* K, const void* V, const void* Q,
-                                   const float* rope_cos, const float* rope_sin,
+                                   const void* Q_graph, const float* rope_cos, const float* rope_sin,
                                    const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
                                    const float* omega_raw, void* trees, void* ws, size_t ws_bytes, void* stream);
 

@@ -28,6 +28,15 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.dp_serial = (c.flags & GRACEKV_FLAG_DP_SERIAL) ? 1 : 0;
   d.uniform_slots = (c.flags & GRACEKV_FLAG_UNIFORM_SLOTS) ? 1 : 0;
   d.pair_quotas = (c.flags & GRACEKV_FLAG_PAIR_QUOTAS) ? 1 : 0;
+  d.lam_graph = c.lambda_graph;
+  // propagation layers at relative depths 0.50 and 0.75, rounded like the
+  // segmentation layers (eq:app_seg_layers)
+  d.n_gl = 0;
+  const int cand[2] = {c.L / 2, (3 * c.L) / 4};
+  for (int i = 0; i < 2; ++i) {
+    const int l = cand[i] < c.L - 1 ? cand[i] : c.L - 1;
+    if (d.n_gl == 0 || d.gl[0] != l) d.gl[d.n_gl++] = l;
+  }
   return d;
 }
 
@@ -69,6 +78,7 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.selstate = (void*)(b + p.off_selstate);
   v.work = (int32_t*)(b + p.off_work);
   v.wctr = (int32_t*)(b + p.off_wctr);
+  v.dhat = nullptr;
   return v;
 }
 
@@ -141,7 +151,8 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->H % c->G != 0) return GRACEKV_ERR_INVALID_ARG;
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
-  if (c->lambda_graph != 0.f || c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
+  if (!(c->lambda_graph >= 0.f && c->lambda_graph <= 1.f)) return GRACEKV_ERR_INVALID_ARG;
+  if (c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
   if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
                    GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY))
     return GRACEKV_ERR_INVALID_ARG;
@@ -220,6 +231,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   p->seg_ws_bytes = segment_ws_bytes(dm);
   p->sel_ws_bytes = select_ws_bytes(dm);
   p->pack_ws_bytes = pack_ws_bytes(dm);
+  p->build_ws_bytes = mh_bytes(dm);
   return GRACEKV_OK;
 }
 
@@ -255,16 +267,20 @@ gracekv_status gracekv_segment(const gracekv_config* c, const void* hidden, cons
 }
 
 gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const void* V, const void* Q,
-                                   const float* rope_cos, const float* rope_sin, const int32_t* slot_starts,
-                                   const int32_t* n_slots, const float* kappa, const float* omega_raw, void* trees,
-                                   void* ws, size_t ws_bytes, void* stream) {
-  (void)ws; (void)ws_bytes;
+                                   const void* Q_graph, const float* rope_cos, const float* rope_sin,
+                                   const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
+                                   const float* omega_raw, void* trees, void* ws, size_t ws_bytes, void* stream) {
   gracekv_plan p;
   gracekv_status s = prep(c, &p);
   if (s != GRACEKV_OK) return s;
   if (!K || !V || !Q || !rope_cos || !rope_sin || !slot_starts || !n_slots || !kappa || !trees)
     return GRACEKV_ERR_INVALID_ARG;
   if (!aligned16(K) || !aligned16(V) || !aligned16(Q) || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
+  const bool graph = c->lambda_graph > 0.f;
+  if (graph) {
+    if (!Q_graph || !ws || !aligned16(Q_graph) || !aligned16(ws)) return GRACEKV_ERR_INVALID_ARG;
+    if (ws_bytes < p.build_ws_bytes) return GRACEKV_ERR_WORKSPACE;
+  }
   Dims dm = make_dims(*c, p);
   TreeView tv = make_view(trees, p);
   hipStream_t st = (hipStream_t)stream;
@@ -279,6 +295,15 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   };
   if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (graph) {
+    // the first root pass left s-hat in the token values: seeds and hops from
+    // it, then the roots again with R^tok = (1 - lambda) s-hat + lambda d-hat
+    if (launch_multihop(dm, K, Q_graph, tv, ws, st) != hipSuccess) return GRACEKV_ERR_HIP;
+    tv.dhat = mh_view(ws, dm).dhat;
+    if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+    if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess)
+      return GRACEKV_ERR_HIP;
+  }
   if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
   // pruned: bound from the roots -> root splits -> tighter bound -> the rest.  The
   // first bound is taken at rank B_free (one below the cut's rank B_free - 1): it

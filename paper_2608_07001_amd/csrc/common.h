@@ -30,6 +30,8 @@ struct Dims {
   int dp_serial;                 // segmentation DP: no warm-up guess, every chunk from the true state
   int uniform_slots;             // slots of n0 tokens instead of the DP partition (ablation)
   int pair_quotas;               // the auction with fixed per-(l, g) capacities (ablation)
+  float lam_graph;               // weight of the multi-hop relevance in the token values
+  int n_gl, gl[2];               // propagation layers of the multi-hop relevance
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).
@@ -70,6 +72,23 @@ struct TreeView {
   float* proto_logm;    // [unit_cap] log m_eff of the root
   void* kargs;          // device copy of the kernel arguments (Dims, then this view) for the
                         // kernels that read them through pointers
+  const float* dhat;    // [N_c] multi-hop relevance to mix into the token values, or null
+};
+
+// Multi-hop relevance scratch (the build workspace when lambda_graph > 0).
+struct MhView {
+  float* dk;            // [N_c] seed score, then the current hop's scores
+  float* dacc;          // [N_c] decayed sum of the hop scores
+  float* dhat;          // [N_c] normalised sum
+  int32_t* seeds;       // [64] current seeds
+  float* wts;           // [64] their weights
+  int32_t* ns;          // number of current seeds
+  int32_t* used;        // [hops * 64] every seed so far
+  int32_t* nused;
+  float2* rstat;        // [groups][rows] (max, log2 partition sum) of each seed row
+  float2* rpart;        // [chunks][groups][rows] their chunk partials
+  float* dpart;         // [groups][row blocks][N_c] per-token partial sums
+  size_t bytes;
 };
 
 // Refinement modes (the roots come from the root kernel): FULL refines every
@@ -115,6 +134,10 @@ hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, 
                          const float* logm_out, const void* K, const void* V, float* out, void* ws, hipStream_t st);
 constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0, TreeView at 512
 hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
+size_t mh_bytes(const Dims& dm);
+MhView mh_view(void* base, const Dims& dm);
+hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q_graph, const TreeView& tv, void* mh_base,
+                           hipStream_t st);
 TreeView make_view(void* base, const gracekv_plan& p);
 
 // ---- device helpers -------------------------------------------------------

@@ -3,8 +3,9 @@
 // For each unit [a0, a0 + n) of one (l, g) this computes, in one pass over the
 // unit's keys and values:
 //   * pass 2 of the direct relevance (App. A.4 eq:app_attention_probability,
-//     eq:app_direct_relevance, lambda_graph = 0 so R^tok = s-hat): R_t for each
-//     token, from the row statistics of pass 1;
+//     eq:app_direct_relevance): R_t = s-hat_t for each token, from the row
+//     statistics of pass 1, or (1 - lambda_graph) s-hat_t + lambda_graph d-hat_t
+//     when a multi-hop relevance is given (eq:app_bottom_up_value);
 //   * the probe exponentials e_{q,t} = exp(l_{q,t} - m_q) of the distortion
 //     probes (App. A.3 "Prototype distortion") and A_t, the probe-mean of
 //     e_{q,t} / Z_q(C) (the attention mass a dropped token takes away);
@@ -415,7 +416,8 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
 #pragma unroll
       for (int w2 = 0; w2 < RWV; ++w2)
         if (16 * w2 < dm.W) { s += sRp[w2 * NMAX + t]; am += sAp[w2 * NMAX + t]; }
-      const float R = s / Sg;
+      float R = s / Sg;
+      if (tv.dhat) R = (1.f - dm.lam_graph) * R + dm.lam_graph * tv.dhat[a0 + t];   // eq:app_bottom_up_value
       const float A = am / (float)dm.W;
       sR[t] = R;
       sA[t] = A;

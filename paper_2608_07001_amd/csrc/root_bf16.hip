@@ -395,6 +395,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
         for (int w2 = 0; w2 < RB_W; ++w2)
           if (16 * w2 < dm.W) { s += sRp[w2 * NMAX + tid]; am += sAp[w2 * NMAX + tid]; }
         R = s / Sg;
+        if (tv.dhat) R = (1.f - dm.lam_graph) * R + dm.lam_graph * tv.dhat[a0 + tid];   // eq:app_bottom_up_value
         A = am / (float)dm.W;
         kn = Kn[tid];
         tv.tok_R[(int64_t)lg * dm.N_c + a0 + tid] = R;

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 7          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 8          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
 
@@ -61,7 +61,8 @@ class Plan(ctypes.Structure):
                  ("unit_cap", ctypes.c_int64), ("node_cap", ctypes.c_int64),
                  ("seg_ws_bytes", ctypes.c_size_t), ("tree_bytes", ctypes.c_size_t),
                  ("sel_ws_bytes", ctypes.c_size_t), ("pack_ws_bytes", ctypes.c_size_t)]
-                + [(n, ctypes.c_size_t) for n in _OFFS] + [("build_lds_bytes", ctypes.c_int32)])
+                + [(n, ctypes.c_size_t) for n in _OFFS] + [("build_lds_bytes", ctypes.c_int32),
+                                                            ("build_ws_bytes", ctypes.c_size_t)])
 
 
 SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
@@ -94,7 +95,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_plan_sizes": [ctypes.POINTER(Config), ctypes.POINTER(Plan)],
         "gracekv_check": [ctypes.POINTER(Config), P, P],
         "gracekv_segment": [ctypes.POINTER(Config), P, P, P, P, P, P, P, S, P],
-        "gracekv_build_trees": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, S, P],
+        "gracekv_build_trees": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
         "gracekv_score": [ctypes.POINTER(Config), P, P, P],
         "gracekv_select": [ctypes.POINTER(Config), P, P, P, S, P],
         "gracekv_pack": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
@@ -156,10 +157,13 @@ def segment(cfg, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, str
                               _stream(stream)), "segment")
 
 
-def build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, trees, stream=None, omega_raw=None):
-    _ok(lib().gracekv_build_trees(ctypes.byref(cfg), _ptr(K), _ptr(V), _ptr(Q), _ptr(rope_cos), _ptr(rope_sin),
-                                  _ptr(slot_starts), _ptr(n_slots), _ptr(kappa), _ptr(omega_raw), _ptr(trees), None,
-                                  0, _stream(stream)), "build_trees")
+def build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, trees, stream=None, omega_raw=None,
+                Q_graph=None, ws=None):
+    """``Q_graph`` and ``ws`` (plan.build_ws_bytes) are read when cfg.lambda_graph > 0."""
+    _ok(lib().gracekv_build_trees(ctypes.byref(cfg), _ptr(K), _ptr(V), _ptr(Q), _ptr(Q_graph), _ptr(rope_cos),
+                                  _ptr(rope_sin), _ptr(slot_starts), _ptr(n_slots), _ptr(kappa), _ptr(omega_raw),
+                                  _ptr(trees), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                  _stream(stream)), "build_trees")
 
 
 def relevance_stats(cfg, K, Q, trees, stream=None):
@@ -246,6 +250,7 @@ class Buffers:
     V_out: torch.Tensor
     pos_out: torch.Tensor
     logm_out: torch.Tensor
+    build_ws: Optional[torch.Tensor] = None   # multi-hop scratch (lambda_graph > 0)
 
 
 def config_for(L, G, H, d, W, N_ctx, x, dtype, n_seg, D_hidden, **hyper) -> Config:
@@ -275,19 +280,22 @@ def allocate(cfg: Config, device="cuda") -> Buffers:
         V_out=torch.empty(max(p.B_total, 1), cfg.d, dtype=kvdt, device=device),
         pos_out=torch.empty(max(p.B_total, 1), dtype=torch.int32, device=device),
         logm_out=torch.empty(max(p.B_total, 1), dtype=torch.float32, device=device),
+        build_ws=torch.empty(p.build_ws_bytes, **u8) if p.build_ws_bytes else None,
     )
 
 
 def compress(buf: Buffers, K, V, Q, rope_cos, rope_sin, hidden, surprisal, omega_raw, stream=None,
              kappa: Optional[torch.Tensor] = None, slot_starts: Optional[torch.Tensor] = None,
-             n_slots: Optional[torch.Tensor] = None):
+             n_slots: Optional[torch.Tensor] = None, Q_graph: Optional[torch.Tensor] = None):
     """The five calls in order.  ``kappa``/``slot_starts``/``n_slots`` may be
-    given to skip segmentation (then ``hidden`` may be None)."""
+    given to skip segmentation (then ``hidden`` may be None); ``Q_graph`` is
+    read when cfg.lambda_graph > 0."""
     cfg = buf.cfg
     if slot_starts is None:
         segment(cfg, hidden, surprisal, buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots, buf.seg_ws, stream)
         kappa, slot_starts, n_slots = buf.kappa, buf.slot_starts, buf.n_slots
-    build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, buf.trees, stream, omega_raw=omega_raw)
+    build_trees(cfg, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, buf.trees, stream, omega_raw=omega_raw,
+                Q_graph=Q_graph, ws=buf.build_ws)
     score(cfg, omega_raw, buf.trees, stream)
     select(cfg, buf.trees, buf.b_used, buf.sel_ws, stream)
     pack(cfg, K, V, rope_cos, rope_sin, buf.trees, buf.offsets, buf.counts, buf.K_out, buf.V_out, buf.pos_out,

@@ -36,7 +36,7 @@ def to_dev(case: dict, device="cuda") -> dict:
 
 
 def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Optional[torch.Tensor] = None,
-            omega=True, prune=False, flags=0, **hyper) -> dict:
+            omega=True, prune=False, flags=0, Q_graph: Optional[torch.Tensor] = None, **hyper) -> dict:
     """All five calls through the C ABI; returns host copies of every output."""
     sh = case_dev["shape"]
     cfg = make_cfg(sh, x, (gk.FLAG_PRUNE if prune else 0) | flags, **hyper)
@@ -50,7 +50,7 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
         kp = kappa.to("cuda").float().contiguous()
     gk.compress(buf, case_dev["K"], case_dev["V"], case_dev["Q"], case_dev["rope_cos"], case_dev["rope_sin"],
                 case_dev.get("hidden"), case_dev["surprisal"], case_dev["omega_raw"] if omega else None,
-                kappa=kp, slot_starts=ss, n_slots=ns)
+                kappa=kp, slot_starts=ss, n_slots=ns, Q_graph=Q_graph)
     torch.cuda.synchronize()
     gk.check(cfg, buf.trees)
     arr = {k: v.cpu() for k, v in gk.tree_arrays(buf.plan, buf.trees).items()}
@@ -69,14 +69,14 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
 
 
 def oracle_run(case: dict, x=None, slots=None, kappa=None, lg_pairs=None, p: O.Params = O.Params(),
-               pair_capacities=False) -> O.OracleResult:
+               pair_capacities=False, Qgraph=None) -> O.OracleResult:
     sh = case["shape"]
     return O.run(np32(case["K"]), np32(case["V"]), np32(case["Q"]), np32(case["rope_cos"]), np32(case["rope_sin"]),
                  np32(case["surprisal"]), np32(case["omega_raw"]),
                  np32(case["hidden"]) if "hidden" in case else None, sh.L, sh.G, sh.H, sh.N_ctx,
                  float(sh.x if x is None else x), kv_dtype=sh.dtype, slot_starts=slots,
                  kappa=None if kappa is None else np32(kappa).astype(np.float64), lg_pairs=lg_pairs, p=p,
-                 pair_capacities=pair_capacities)
+                 pair_capacities=pair_capacities, Qgraph=None if Qgraph is None else np32(Qgraph))
 
 
 # ---------------------------------------------------------------------------

@@ -84,7 +84,7 @@ def test_plan_rejections():
     with pytest.raises(gk.GraceKVError) as e:
         gk.plan_sizes(_cfg(N_ctx=8192, x=4000.0))        # < 4 entries per (l, g)
     assert e.value.status == -3
-    for bad, code in [(dict(lambda_graph=0.3), -2), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
+    for bad, code in [(dict(lambda_graph=1.5), -1), (dict(lambda_graph=-0.1), -1), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
                       (dict(W=65), -2), (dict(H=30), -1), (dict(x=0.5), -1), (dict(n_min=8), -2),
                       (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=32), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
         with pytest.raises(gk.GraceKVError) as e:
@@ -92,11 +92,29 @@ def test_plan_rejections():
         assert e.value.status == code, bad
 
 
+def test_multi_hop_workspace_and_arguments():
+    # the build workspace exists only with lambda_graph > 0, and then Q_graph
+    # and the workspace are checked on the host before anything is enqueued
+    assert gk.plan_sizes(_cfg(N_ctx=8192, x=8.0)).build_ws_bytes == 0
+    c = _cfg(N_ctx=8192, x=8.0, lambda_graph=0.3)
+    p = gk.plan_sizes(c)
+    assert p.build_ws_bytes >= 3 * p.N_c * 4
+    lib = gk.lib()
+    fake = ctypes.c_void_p(1 << 20)                # aligned, never dereferenced on these paths
+    args = [fake] * 3 + [None] + [fake] * 7       # K V Q | Q_graph | cos sin slots n kappa omega trees
+    assert lib.gracekv_build_trees(ctypes.byref(c), *args, fake, p.build_ws_bytes, None) == -1
+    args[3] = fake
+    assert lib.gracekv_build_trees(ctypes.byref(c), *args, None, 0, None) == -1
+    assert lib.gracekv_build_trees(ctypes.byref(c), *args, fake, p.build_ws_bytes - 1, None) == -4
+    args[3] = ctypes.c_void_p((1 << 20) + 4)
+    assert lib.gracekv_build_trees(ctypes.byref(c), *args, fake, p.build_ws_bytes, None) == -1
+
+
 def test_null_pointers_are_refused_before_any_launch():
     c = _cfg(N_ctx=8192, x=8.0)
     lib = gk.lib()
     assert lib.gracekv_segment(ctypes.byref(c), None, None, None, None, None, None, None, 0, None) == -1
-    assert lib.gracekv_build_trees(ctypes.byref(c), *([None] * 10), None, 0, None) == -1
+    assert lib.gracekv_build_trees(ctypes.byref(c), *([None] * 11), None, 0, None) == -1
     assert lib.gracekv_score(ctypes.byref(c), None, None, None) == -1
     assert lib.gracekv_select(ctypes.byref(c), None, None, None, 0, None) == -1
     assert lib.gracekv_pack(ctypes.byref(c), *([None] * 12), 0, None) == -1

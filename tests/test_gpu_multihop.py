@@ -1,0 +1,111 @@
+"""Multi-hop relevance (App. A.4 eq:app_global_seed_score, eq:app_hop_propagation,
+eq:app_diffused_relevance, eq:app_bottom_up_value) on the GPU against the oracle.
+
+d-hat itself is read back through the interface: a run with lambda_graph = 0
+gives s-hat, a run with lambda_graph > 0 gives (1 - lambda) s-hat + lambda d-hat
+in the token values, so d-hat = (R_mixed - (1 - lambda) s-hat) / lambda for every
+(l, g).  It is compared with the oracle's d-hat (computed from the oracle's own
+s-hat), and the mixed token values, trees, selected set and packed cache with
+the oracle run at the same lambda."""
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import gracekv_oracle as O
+from synth.workloads import CONFIGS, make_case, make_graph_queries, small_shape
+
+import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+LAM = 0.3
+RTOL_R, RTOL_D, ATOL_D, TAU = 1e-4, 2e-3, 1e-7, 2e-4
+# fp32 logits, exponentials and sums against fp64: d-hat to 1e-4 of its largest value
+RTOL_DHAT = 1e-4
+
+
+def _oracle_dhat(case, N_c, p):
+    """d-hat from the oracle alone: s-hat of every (l, g), then the hops."""
+    sh = case["shape"]
+    hpg = sh.H // sh.G
+    K = H.np32(case["K"]).astype(np.float64)
+    Q = H.np32(case["Q"]).astype(np.float64)
+    qg = H.np32(case["Q_graph"]).astype(np.float64)
+    shat = {(l, g): O.relevance(K[l, g], Q[l, g * hpg:(g + 1) * hpg], sh.N_ctx, N_c, p)[0]
+            for l in range(sh.L) for g in range(sh.G)}
+    gl = O.graph_layer_indices(sh.L, p)
+    Kl = {(l, g): K[l, g] for l in gl for g in range(sh.G)}
+    Qd = {(l, h): qg[i, h] for i, l in enumerate(gl) for h in range(sh.H)}
+    return shat, O.multi_hop(shat, Kl, Qd, sh.G, hpg, N_c, p)
+
+
+def _runs(shape, seed):
+    case = make_case(shape, seed, with_hidden=True)
+    case["Q_graph"] = make_graph_queries(shape, seed, case["K"], case["rope_cos"], case["rope_sin"])
+    dev = H.to_dev(case)
+    g0 = H.gpu_run(dev)
+    g1 = H.gpu_run(dev, Q_graph=dev["Q_graph"], lambda_graph=LAM)
+    assert g1["slots"] == g0["slots"]
+    return case, g0, g1
+
+
+def _check_dhat(case, g0, g1, p):
+    sh = case["shape"]
+    N_c = g1["plan"].N_c
+    LG = sh.L * sh.G
+    s0 = g0["tok_R"].double().view(LG, N_c).numpy()
+    r1 = g1["tok_R"].double().view(LG, N_c).numpy()
+    shat_o, dhat_o = _oracle_dhat(case, N_c, p)
+    dh = (r1 - (1.0 - LAM) * s0) / LAM                 # one d-hat per (l, g) row, all equal
+    scale = dhat_o.max()
+    err = np.abs(dh - dhat_o[None, :]).max() / scale
+    seeds1, _ = O.select_seeds(np.mean(np.stack([shat_o[k] for k in sorted(shat_o)]), axis=0), p)
+    print(f"{sh.name}: N_c {N_c}, hop-1 seeds {len(seeds1)}, d-hat max {scale:.3e}, max err / max {err:.2e}")
+    assert abs(dhat_o.sum() - 1.0) < 1e-5
+    assert err <= RTOL_DHAT, err
+    # the mixed token values against the oracle's mix
+    for l in range(sh.L):
+        for g in range(sh.G):
+            ro = (1.0 - LAM) * shat_o[(l, g)] + LAM * dhat_o
+            e = np.abs(r1[l * sh.G + g] - ro).max() / ro.max()
+            assert e <= RTOL_DHAT, (l, g, e)
+
+
+SMALL = [
+    CONFIGS["tiny"],
+    small_shape("mh-bf16", L=4, G=2, H=8, d=128, N_ctx=2000, W=32, dtype="bf16", x=16.0, n_segments=12),
+    small_shape("mh-odd", L=3, G=3, H=3, d=64, N_ctx=700, W=8, x=7.0, n_segments=6),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=["tiny-f32", "bf16-d128", "f32-3heads"])
+def test_multi_hop_trees_and_selection(shape):
+    case, g0, g1 = _runs(shape, 4)
+    p = dataclasses.replace(O.Params(), lam_graph=LAM)
+    _check_dhat(case, g0, g1, p)
+    o = H.oracle_run(case, p=p, Qgraph=case["Q_graph"])
+    assert g1["slots"] == o.slot_starts
+    st = H.compare_trees(o, g1, RTOL_D, ATOL_D, RTOL_R, TAU)
+    assert not st.mismatches, st.mismatches[:10]
+    ga, gs = H.gpu_selected(g1)
+    oa, os_ = H.oracle_selected(o, shape.G)
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    print(f"{shape.name} multi-hop: nodes {st.nodes} near-ties {st.near_ties} maxrelD {st.max_rel_D:.2e}; "
+          f"adds {len(oa)} splits {len(os_)} spent {spent} b_used {g1['b_used']}")
+    assert g1["b_used"] == spent
+    if st.near_ties == 0:
+        assert ga == oa and gs == os_
+        offs = g1["offsets"].numpy()
+        pos = g1["pos_out"].numpy()
+        for (l, gg), pk in o.packed.items():
+            lg = l * shape.G + gg
+            assert np.array_equal(pos[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+
+
+def test_multi_hop_relevance_8b_heads_8k():
+    # Llama-3-8B head layout (8 KV heads x 4 query heads, d = 128) on four layers
+    # at 8K context: the row passes span eight 1024-token chunks and a ragged tail
+    shape = small_shape("mh-8k", L=4, G=8, H=32, d=128, N_ctx=8000, W=64, dtype="bf16", x=8.0, n_segments=60)
+    case, g0, g1 = _runs(shape, 5)
+    _check_dhat(case, g0, g1, dataclasses.replace(O.Params(), lam_graph=LAM))
