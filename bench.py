@@ -34,6 +34,9 @@ def parse():
     ap.add_argument("--ablation-uniform-slots", action="store_true",
                     help="the paper's w/o-curvature-segmentation ablation: uniform 64-token slots, midpoint-only "
                          "binary candidates, no curvature reward")
+    ap.add_argument("--lambda-graph", type=float, default=0.0,
+                    help="mix the multi-hop relevance into the token values with this weight (e.g. 0.3); the "
+                         "queries of every position at the propagation layers are synthesised")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention measurement")
     ap.add_argument("--no-overlap", action="store_true",
@@ -74,10 +77,13 @@ def recorded_traffic(workload):
     return blob.get("build_trees_bytes_per_call"), blob
 
 
-def algorithmic_bytes(sh, plan, b):
+def algorithmic_bytes(sh, plan, b, n_graph=0, hops=2, seeds=64):
     """Bytes the method must move once: K + V + window queries + RoPE tables
-    (build), hidden slabs + surprisal (segment), packed cache (pack)."""
+    (build), hidden slabs + surprisal (segment), packed cache (pack).  With the
+    multi-hop relevance the build also reads, per hop, the keys of C at the
+    ``n_graph`` propagation layers and the seeds' queries there."""
     kv = 2 * sh.L * sh.G * sh.T * sh.d * b
+    kv += hops * n_graph * (sh.G * plan.N_c + sh.H * seeds) * sh.d * b
     q = sh.L * sh.H * sh.W * sh.d * b
     rope = 2 * sh.T * (sh.d // 2) * 4
     hidden = sh.n_seg * sh.T * sh.D * b + sh.T * 4
@@ -191,7 +197,7 @@ def main():
         sys.exit(2)
     import torch
     from paper_2608_07001_amd import gracekv as gk
-    from synth.workloads import CONFIGS, make_case
+    from synth.workloads import CONFIGS, make_case, make_graph_queries
     sh = CONFIGS[args.config]
     if args.x is not None:
         sh = sh.with_(x=args.x)
@@ -202,8 +208,13 @@ def main():
                         flags=(0 if args.no_prune or args.ablation_pair_quotas else gk.FLAG_PRUNE) |
                               (gk.FLAG_UNIFORM_SLOTS if args.ablation_uniform_slots else 0) |
                               (gk.FLAG_PAIR_QUOTAS if args.ablation_pair_quotas else 0),
+                        lambda_graph=args.lambda_graph,
                         **(dict(k_curv=0, lam_kappa=0.0, n0=64) if args.ablation_uniform_slots else {}))
     buf = gk.allocate(cfg, dev)
+    q_graph = None
+    if args.lambda_graph > 0:
+        q_graph = make_graph_queries(sh, args.seed, case["K"], case["rope_cos"], case["rope_sin"], device=dev)
+        torch.cuda.synchronize()
     p = buf.plan
     stream = torch.cuda.current_stream()
     # the relevance row statistics need neither the hidden states nor the slots:
@@ -232,7 +243,8 @@ def main():
         if overlap:
             stream.wait_event(join)
         gk.build_trees(cfg_b, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
-                       buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"])
+                       buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"], Q_graph=q_graph,
+                       ws=buf.build_ws)
         mark(2)
         gk.score(cfg, case["omega_raw"], buf.trees, stream)
         mark(3)
@@ -264,10 +276,12 @@ def main():
         b2.copy_(a)
         torch.cuda.synchronize()
         del a, b2
-    traffic, _ = recorded_traffic(sh.name)
+    # the committed counters were taken on the default path (pruned build, direct relevance)
+    default_path = not (args.no_prune or args.ablation_pair_quotas or args.ablation_uniform_slots or q_graph is not None)
+    traffic = recorded_traffic(sh.name)[0] if default_path else None
     tokens = sh.L * sh.G * sh.N_ctx
     b = 2 if sh.dtype == "bf16" else 4
-    ab = algorithmic_bytes(sh, p, b)
+    ab = algorithmic_bytes(sh, p, b, n_graph=0 if q_graph is None else q_graph.shape[0])
     build_gbs = ab["build"] / (stage_ms["build"] * 1e-3) / 1e9
     res = {
         "metric": "compressed context tokens/sec (layers x KV-heads x tokens)",
@@ -281,6 +295,7 @@ def main():
                    "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),
                    "pruned_build": not (args.no_prune or args.ablation_pair_quotas),
                    "stats_on_second_stream": overlap,
+                   "lambda_graph": args.lambda_graph,
                    "ablation": ", ".join(x for x, on in (("uniform 64-token slots, midpoint-only trees",
                                                           args.ablation_uniform_slots),
                                                          ("fixed per-(l, g) capacities", args.ablation_pair_quotas))
@@ -296,7 +311,7 @@ def main():
     }
     if not args.no_decode:
         res["decode_attention"] = decode_measure(cfg, sh, case, buf, stream)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and q_graph is None:
         res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)
     print(json.dumps(res), flush=True)
 

@@ -142,8 +142,8 @@ gracekv_status gracekv_default_config(gracekv_config* cfg);
 /* Validates cfg and fills plan.  Returns GRACEKV_ERR_BUDGET when the budget
  * cannot hold a recent window of r_min entries per (layer, KV head)
  * (App. A.1), GRACEKV_ERR_INVALID_ARG for lambda_graph outside [0, 1],
- * GRACEKV_ERR_UNSUPPORTED for alpha_floor != 0 or shapes outside the
- * documented limits. */
+ * GRACEKV_ERR_UNSUPPORTED for alpha_floor != 0, lambda_graph > 0 with
+ * H / G > 8, or shapes outside the documented limits. */
 gracekv_status gracekv_plan_sizes(const gracekv_config* cfg, gracekv_plan* plan);
 
 /* Human-readable name of a status. */
@@ -213,8 +213,9 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  * probability of the query at u (range [0, u]) on each token of C; the scores
  * at the current and earlier seeds are then zeroed and the next hop seeds from
  * them; d = d^(1) + 0.5 d^(2), d-hat = d / (sum_C d + eps), and every token
- * value becomes (1 - lambda_graph) s-hat + lambda_graph d-hat.  The relevance
- * and roots are evaluated twice (once for s-hat, once with the mix).
+ * value becomes (1 - lambda_graph) s-hat + lambda_graph d-hat.  s-hat is
+ * computed first by a relevance-only pass (bf16 caches) or a root pass without
+ * the mix (fp32 caches).  Needs H / G <= 8. 
  * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
  * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops
  * known so far gives theta_lb, the (B_free-1)-th largest effective key among

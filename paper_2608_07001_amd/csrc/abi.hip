@@ -152,6 +152,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->dtype != GRACEKV_F32 && c->dtype != GRACEKV_BF16) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->lambda_graph >= 0.f && c->lambda_graph <= 1.f)) return GRACEKV_ERR_INVALID_ARG;
+  if (c->lambda_graph > 0.f && c->H / c->G > 8) return GRACEKV_ERR_UNSUPPORTED;   // one wave per query head
   if (c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
   if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
                    GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY))
@@ -294,16 +295,19 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
   };
   if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  // multi-hop relevance: s-hat of every (l, g) first (bf16: a relevance-only
+  // pass; fp32: a root pass without the mix), then seeds and hops, then the
+  // roots with R^tok = (1 - lambda) s-hat + lambda d-hat
+  const bool graph_first = graph && dm.dtype == GRACEKV_BF16;
+  if (graph && !graph_first &&
+      launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess)
+    return GRACEKV_ERR_HIP;
   if (graph) {
-    // the first root pass left s-hat in the token values: seeds and hops from
-    // it, then the roots again with R^tok = (1 - lambda) s-hat + lambda d-hat
-    if (launch_multihop(dm, K, Q_graph, tv, ws, st) != hipSuccess) return GRACEKV_ERR_HIP;
+    if (launch_multihop(dm, K, Q, Q_graph, tv, ws, st) != hipSuccess) return GRACEKV_ERR_HIP;
     tv.dhat = mh_view(ws, dm).dhat;
     if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-    if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess)
-      return GRACEKV_ERR_HIP;
   }
+  if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
   // pruned: bound from the roots -> root splits -> tighter bound -> the rest.  The
   // first bound is taken at rank B_free (one below the cut's rank B_free - 1): it

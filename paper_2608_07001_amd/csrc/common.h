@@ -88,6 +88,8 @@ struct MhView {
   float2* rstat;        // [groups][rows] (max, log2 partition sum) of each seed row
   float2* rpart;        // [chunks][groups][rows] their chunk partials
   float* dpart;         // [groups][row blocks][N_c] per-token partial sums
+  uint64_t* cand;       // [blocks][64] seed candidates (score, position keys) of each block
+  double* bsum;         // [blocks] score sum of each block
   size_t bytes;
 };
 
@@ -136,8 +138,8 @@ constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0,
 hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
 size_t mh_bytes(const Dims& dm);
 MhView mh_view(void* base, const Dims& dm);
-hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q_graph, const TreeView& tv, void* mh_base,
-                           hipStream_t st);
+hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q, const void* Q_graph, const TreeView& tv,
+                           void* mh_base, hipStream_t st);
 TreeView make_view(void* base, const gracekv_plan& p);
 
 // ---- device helpers -------------------------------------------------------

@@ -1,25 +1,33 @@
 // Multi-hop relevance (App. A.4 eq:app_global_seed_score,
 // eq:app_hop_propagation, eq:app_diffused_relevance, eq:app_bottom_up_value).
 //
-// Runs inside gracekv_build_trees when lambda_graph > 0, after a first pass of
-// the root kernel has written the direct relevance s-hat of every (l, g) into
-// the token-value array:
+// Runs inside gracekv_build_trees when lambda_graph > 0, once the relevance
+// row statistics (m_V, Z_V per window query) and the per-(l, g) sums S_{l,g}
+// are known:
+//   * s-hat of every (l, g) into the token-value array: bf16 caches by the
+//     direct pass below (the root kernel later overwrites those values); fp32
+//     caches by a first run of the root kernel;
 //   * k_mh_seed_score: S_t = mean over (l, g) of s-hat_{l,g,t};
-//   * k_mh_seeds (one workgroup): positions in descending score (ties to the
+//   * k_mh_top + k_mh_seeds: the positions in descending score (ties to the
 //     smaller position) while their cumulative share of the total stays below
 //     0.9 (the one reaching it included), at most 64, weights proportional to
-//     the score;
-//   * k_mh_rows, pass 0 and 1, grid (token chunk, propagation layer x KV head,
-//     row block): one thread per row (query head of the group x seed) holds
-//     the seed's query of that layer and head in registers; 64-token blocks of
-//     keys are staged in LDS.  Pass 0 gives each row's maximum and partition
-//     sum over its causal range [0, u]; pass 1 sums w_u pi_{u,t} over the rows
-//     for every token of C;
+//     the score.  k_mh_top keeps the 64 largest keys of each 4096-token block,
+//     k_mh_seeds (one workgroup) takes the seeds from those candidates;
+//   * two passes per hop over (propagation layer, KV head, token chunk):
+//     pass 0 gives each seed row's maximum and partition sum over its causal
+//     range [0, u]; pass 1 sums w_u pi_{u,t} over the rows for every token;
 //   * k_mh_hop_reduce: d^(k)_t over layers and heads, zero at the current and
 //     earlier seeds, accumulated with the decay 0.5^(k-1);
 //   * k_mh_finish: d-hat = d / (sum_C d + eps).
-// The root kernel then runs again and mixes R^tok = (1 - lambda) s-hat +
-// lambda d-hat.
+// The root kernel then mixes R^tok = (1 - lambda) s-hat + lambda d-hat.
+//
+// Row layout: a group is (propagation layer, KV head) for the hops and (layer,
+// KV head) for the direct pass; row j of query head slot hl is r = 64 hl + j,
+// j a seed (hops) or a window query (direct pass).  bf16 caches run the logits
+// on MFMA (16x16x32: 16 tokens x 16 rows per tile, the bf16 products exact in
+// fp32, summed in fp32 like the reference dot product), one wave per query
+// head slot, 64-token blocks of keys staged in LDS.  fp32 caches use one
+// thread per row on the vector ALUs.
 #include "common.h"
 
 namespace gkv {
@@ -28,8 +36,10 @@ constexpr int MH_SEEDS = 64;                 // at most this many seeds per hop
 constexpr int MH_HOPS = 2;
 constexpr int MH_CH = 1024;                  // tokens per workgroup of the row passes
 constexpr int MH_SUB = 64;                   // tokens staged at once
+constexpr int MH_TOPB = 4096;                // tokens per block of the candidate pass
 constexpr double MH_ETA = 0.9;               // cumulative seed share
 constexpr float MH_RHO = 0.5f;               // inter-hop decay
+constexpr float LOG2E = 1.44269504088896341f;
 
 static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -41,6 +51,7 @@ MhView mh_view(void* base, const Dims& dm) {
   const int ngrp = dm.n_gl * dm.G;
   const int nz = (rmax + 255) / 256;
   const int nch = (int)((N + MH_CH - 1) / MH_CH);
+  const size_t ntop = (N + MH_TOPB - 1) / MH_TOPB;
   v.dk = (float*)p; p += al(N * 4);
   v.dacc = (float*)p; p += al(N * 4);
   v.dhat = (float*)p; p += al(N * 4);
@@ -52,6 +63,8 @@ MhView mh_view(void* base, const Dims& dm) {
   v.rstat = (float2*)p; p += al((size_t)ngrp * rmax * 8);
   v.rpart = (float2*)p; p += al((size_t)nch * ngrp * rmax * 8);
   v.dpart = (float*)p; p += al((size_t)ngrp * nz * N * 4);
+  v.cand = (uint64_t*)p; p += al(ntop * MH_SEEDS * 8);
+  v.bsum = (double*)p; p += al(ntop * 8);
   v.bytes = (size_t)(p - (char*)base);
   return v;
 }
@@ -73,40 +86,80 @@ __device__ __forceinline__ uint64_t mh_key(float s, int64_t t) {
   return ((uint64_t)__float_as_uint(s > 0.f ? s : 0.f) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)t);
 }
 
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t b = __shfl_xor(v, o, 64);
+    v = b > v ? b : v;
+  }
+  return v;
+}
+
+// The 64 largest keys of one block of MH_TOPB scores (descending, 0 past the
+// block's size) and the block's score sum.
+__global__ __launch_bounds__(256) void k_mh_top(Dims dm, MhView mh) {
+  __shared__ float ss[MH_TOPB];
+  __shared__ unsigned long long skey[4];
+  __shared__ double sred[4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int64_t b0 = (int64_t)blockIdx.x * MH_TOPB;
+  const int n = (int)(dm.N_c - b0 < MH_TOPB ? dm.N_c - b0 : MH_TOPB);
+  double a = 0.0;
+  for (int i = tid; i < n; i += 256) {
+    const float v = mh.dk[b0 + i];
+    ss[i] = v;
+    a += v;
+  }
+  a = wave_sum(a);
+  if (lane == 0) sred[wave] = a;
+  __syncthreads();
+  if (tid == 0) mh.bsum[blockIdx.x] = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+  uint64_t prev = ~0ull;
+  for (int k = 0; k < MH_SEEDS; ++k) {
+    uint64_t best = 0;
+    for (int i = tid; i < n; i += 256) {
+      const uint64_t key = mh_key(ss[i], b0 + i);
+      if (key < prev && key > best) best = key;
+    }
+    best = wave_max_u64(best);
+    if (lane == 0) skey[wave] = best;
+    __syncthreads();
+    uint64_t b = skey[0];
+    for (int w = 1; w < 4; ++w) b = skey[w] > b ? skey[w] : b;
+    __syncthreads();
+    if (tid == 0) mh.cand[(int64_t)blockIdx.x * MH_SEEDS + k] = b;
+    prev = b;
+  }
+}
+
+// Seeds from the block candidates: every key among the 64 largest overall is
+// among its block's 64 largest.
 __global__ __launch_bounds__(1024) void k_mh_seeds(Dims dm, MhView mh) {
   __shared__ double sred[16];
   __shared__ unsigned long long skey[16];
-  __shared__ double tot;
+  __shared__ float swt[MH_SEEDS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const float* sc = mh.dk;
+  const int nb = (int)((dm.N_c + MH_TOPB - 1) / MH_TOPB);
+  const int nc = nb * MH_SEEDS;
   double a = 0.0;
-  for (int64_t t = tid; t < dm.N_c; t += 1024) a += sc[t];
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+  for (int b = tid; b < nb; b += 1024) a += mh.bsum[b];
+  a = wave_sum(a);
   if (lane == 0) sred[wave] = a;
   __syncthreads();
-  if (tid == 0) {
-    double s = 0.0;
-    for (int w = 0; w < 16; ++w) s += sred[w];
-    tot = s;
-  }
-  __syncthreads();
-  const double total = tot;
+  double total = 0.0;
+  for (int w = 0; w < 16; ++w) total += sred[w];
+  const int nused0 = *mh.nused;
   uint64_t prev = ~0ull;
   double cum = 0.0, wsum = 0.0;
   int ns = 0;
   for (int k = 0; k < MH_SEEDS; ++k) {
     if (!(total > 0.0) || cum >= MH_ETA) break;
     uint64_t best = 0;
-    for (int64_t t = tid; t < dm.N_c; t += 1024) {
-      const uint64_t key = mh_key(sc[t], t);
+    for (int i = tid; i < nc; i += 1024) {
+      const uint64_t key = mh.cand[i];
       if (key < prev && key > best) best = key;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint64_t b2 = __shfl_xor(best, o, 64);
-      best = b2 > best ? b2 : best;
-    }
+    best = wave_max_u64(best);
     if (lane == 0) skey[wave] = best;
     __syncthreads();
     uint64_t b = skey[0];
@@ -115,59 +168,208 @@ __global__ __launch_bounds__(1024) void k_mh_seeds(Dims dm, MhView mh) {
     const float s = __uint_as_float((uint32_t)(b >> 32));
     if (!(s > 0.f)) break;
     const int t = (int)(0xFFFFFFFFu - (uint32_t)(b & 0xFFFFFFFFu));
-    if (tid == 0) { mh.seeds[ns] = t; mh.wts[ns] = s; }
+    if (tid == 0) { mh.seeds[ns] = t; swt[ns] = s; mh.used[nused0 + ns] = t; }
     cum += (double)s / total;
     wsum += (double)s;
     ++ns;
     prev = b;
   }
   __syncthreads();
-  if (tid < ns) {
-    mh.wts[tid] = (float)((double)mh.wts[tid] / wsum);
-    mh.used[*mh.nused + tid] = mh.seeds[tid];
-  }
-  __syncthreads();
-  if (tid == 0) { *mh.ns = ns; *mh.nused += ns; }
+  if (tid < ns) mh.wts[tid] = (float)((double)swt[tid] / wsum);
+  if (tid == 0) { *mh.ns = ns; *mh.nused = nused0 + ns; }
 }
 
-// the seed query of row r (head slot r / ns, seed r % ns), scaled to base-2 logits
-template <typename T, int D>
-__device__ __forceinline__ bool mh_row(const Dims& dm, const T* __restrict__ Qg, const MhView& mh, int gi, int g,
-                                       int r, float* q, int& u, float& w) {
-  const int ns = *mh.ns;
-  if (ns == 0 || r >= dm.hpg * ns) return false;
-  const int hl = r / ns, s = r % ns;
-  u = mh.seeds[s];
-  w = mh.wts[s];
-  const int h = g * dm.hpg + hl;
-  const T* qr = Qg + (((int64_t)gi * dm.H + h) * dm.T + u) * D;
-  const float sc2 = 1.44269504088896341f / sqrtf((float)D);
+// ---------------------------------------------------------------------------
+// bf16: logits on MFMA.  MODE 0: hop row statistics; MODE 1: hop token sums;
+// MODE 2: direct relevance s-hat of (l, g) into the token values.  Block:
+// one wave per query head slot of the group (hpg waves).
+// ---------------------------------------------------------------------------
+template <int D, int MODE>
+__global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __restrict__ K,
+                                                 const uint16_t* __restrict__ Qs, TreeView tv, MhView mh) {
+  constexpr int KS = D / 32;
+  constexpr int LDK = D + 8;                  // staged key row stride (bf16): conflict-free fragment reads
+  constexpr int C8 = D / 8;                   // 16-byte chunks per key row
+  __shared__ __align__(16) uint16_t sk[MH_SUB * LDK];
+  __shared__ float red[8][MH_SUB];
+  const int ch = blockIdx.x, grp = blockIdx.y;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+  const int nw = blockDim.x >> 6;
+  const int gi = MODE == 2 ? 0 : grp / dm.G;
+  const int g = grp % dm.G;
+  const int l = MODE == 2 ? grp / dm.G : dm.gl[gi];
+  const int h = g * dm.hpg + w;               // the wave's query head
+  const int nrow = MODE == 2 ? dm.W : *mh.ns;
+  const int rmax = dm.hpg * MH_SEEDS;
+  const float sc2 = LOG2E / sqrtf((float)D);
+  // the wave's rows j = 16 rt + i16: query fragment, causal limit, weight, log2 normaliser
+  uint4 qf[4][KS];
+  int uj[4];
+  float wj[4], cj[4];
+  int umax = -1;
+  if (MODE != 2)
+    for (int s = 0; s < nrow; ++s) umax = max(umax, mh.seeds[s]);
 #pragma unroll
-  for (int k = 0; k < D; ++k) q[k] = ldf(qr, k) * sc2;
-  return true;
+  for (int rt = 0; rt < 4; ++rt) {
+    const int j = 16 * rt + i16;
+    const bool ok = j < nrow;
+    const uint16_t* qrow;
+    if (MODE == 2) {
+      qrow = Qs + (((int64_t)l * dm.H + h) * dm.W + (ok ? j : 0)) * D;
+      uj[rt] = ok ? 0x7fffffff : -1;
+      wj[rt] = 1.f;
+      cj[rt] = 0.f;
+      if (ok) {
+        const float4 st = tv.row_stats[((int64_t)l * dm.G + g) * dm.rows + w * dm.W + j];
+        cj[rt] = st.x * LOG2E + __log2f(st.y);
+      }
+    } else {
+      const int u = ok ? mh.seeds[j] : 0;
+      qrow = Qs + (((int64_t)gi * dm.H + h) * dm.T + u) * D;
+      uj[rt] = ok ? u : -1;
+      wj[rt] = ok ? mh.wts[j] : 0.f;
+      cj[rt] = 0.f;
+      if (MODE == 1 && ok) {
+        const float2 st = mh.rstat[(int64_t)grp * rmax + w * MH_SEEDS + j];
+        cj[rt] = st.x + st.y;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[rt][s] = ok ? *(const uint4*)(qrow + 32 * s + 8 * g4) : make_uint4(0, 0, 0, 0);
+  }
+  const int64_t c0 = (int64_t)ch * MH_CH;
+  int64_t c1 = c0 + MH_CH < dm.N_c ? c0 + MH_CH : dm.N_c;
+  if (MODE != 2 && (int64_t)umax + 1 < c1) c1 = (int64_t)umax + 1;
+  const uint16_t* Kp = K + ((int64_t)l * dm.G + g) * dm.T * D;
+  float m[4], z[4];
+#pragma unroll
+  for (int rt = 0; rt < 4; ++rt) { m[rt] = -INFINITY; z[rt] = 0.f; }
+  for (int64_t s0 = c0; s0 < c1; s0 += MH_SUB) {
+    const int nt = (int)(c1 - s0 < MH_SUB ? c1 - s0 : MH_SUB);
+    __syncthreads();
+    for (int e = tid; e < MH_SUB * C8; e += blockDim.x) {
+      const int tt = e / C8, c = e % C8;
+      const uint4 v = tt < nt ? *(const uint4*)(Kp + (s0 + tt) * D + 8 * c) : make_uint4(0, 0, 0, 0);
+      *(uint4*)(sk + tt * LDK + 8 * c) = v;
+    }
+    __syncthreads();
+    for (int tt = 0; tt < MH_SUB / 16; ++tt) {
+      if (16 * tt >= nt) break;
+      uint4 kf[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) kf[s] = *(const uint4*)(sk + (16 * tt + i16) * LDK + 32 * s + 8 * g4);
+      f32x4 acc[4];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < KS; ++s) acc[rt] = mfma_bf16_16x16x32(pk8(kf[s]), pk8(qf[rt][s]), acc[rt]);
+      }
+      // lane holds tokens tb + r of row 16 rt + i16
+      const int64_t tb = s0 + 16 * tt + 4 * g4;
+      if (MODE == 0) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+          float x[4], lm = -INFINITY;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool ok = tb + r < c1 && tb + r <= uj[rt];
+            x[r] = ok ? acc[rt][r] * sc2 : -INFINITY;
+            lm = fmaxf(lm, x[r]);
+          }
+          if (lm > m[rt]) { z[rt] *= __builtin_amdgcn_exp2f(m[rt] - lm); m[rt] = lm; }
+          if (lm != -INFINITY)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) z[rt] += __builtin_amdgcn_exp2f(x[r] - m[rt]);
+        }
+      } else {
+        float sv[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool ok = tb + r < c1 && tb + r <= uj[rt];
+            const float v = wj[rt] * __builtin_amdgcn_exp2f(acc[rt][r] * sc2 - cj[rt]);
+            sv[r] += ok ? v : 0.f;
+          }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sv[r] = row_sum16(sv[r]);
+        if (i16 < 4) red[w][16 * tt + 4 * g4 + i16] = i16 == 0 ? sv[0] : i16 == 1 ? sv[1] : i16 == 2 ? sv[2] : sv[3];
+      }
+    }
+    if (MODE != 0) {
+      __syncthreads();
+      if (tid < nt) {
+        float s = 0.f;
+        for (int w2 = 0; w2 < nw; ++w2) s += red[w2][tid];
+        if (MODE == 1) {
+          mh.dpart[(int64_t)grp * dm.N_c + s0 + tid] = s;
+        } else {
+          const int lg = l * dm.G + g;
+          tv.tok_R[(int64_t)lg * dm.N_c + s0 + tid] = s / (tv.lg_S[lg] + dm.eps);
+        }
+      }
+    }
+  }
+  if (MODE == 0) {
+    // merge the four lanes of each row (lanes i16 + 16 k)
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+      for (int o = 16; o < 64; o <<= 1) {
+        const float m2 = __shfl_xor(m[rt], o, 64), z2 = __shfl_xor(z[rt], o, 64);
+        const float mn = fmaxf(m[rt], m2);
+        if (mn != -INFINITY) {
+          z[rt] = z[rt] * __builtin_amdgcn_exp2f(m[rt] - mn) + z2 * __builtin_amdgcn_exp2f(m2 - mn);
+          m[rt] = mn;
+        }
+      }
+      if (g4 == 0) {
+        const int ngrp = dm.n_gl * dm.G;
+        mh.rpart[((int64_t)ch * ngrp + grp) * rmax + w * MH_SEEDS + 16 * rt + i16] = make_float2(m[rt], z[rt]);
+      }
+    }
+  }
 }
 
-template <typename T, int D, int PASS>
-__global__ __launch_bounds__(256) void k_mh_rows(Dims dm, const T* __restrict__ K, const T* __restrict__ Qg,
+// ---------------------------------------------------------------------------
+// fp32: one thread per row r = 64 hl + j on the vector ALUs (hop passes only).
+// ---------------------------------------------------------------------------
+template <int D, int PASS>
+__global__ __launch_bounds__(256) void k_mh_rows(Dims dm, const float* __restrict__ K, const float* __restrict__ Qg,
                                                  MhView mh) {
   __shared__ __align__(16) float sk[MH_SUB * D];
   __shared__ float red[4][MH_SUB];
-  const int ch = blockIdx.x, grp = blockIdx.y, z = blockIdx.z;
+  const int ch = blockIdx.x, grp = blockIdx.y, zb = blockIdx.z;
   const int gi = grp / dm.G, g = grp % dm.G;
   const int l = dm.gl[gi];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int rmax = dm.hpg * MH_SEEDS;
-  const int r = z * 256 + tid;
+  const int nz = (rmax + 255) / 256;
+  const int r = zb * 256 + tid;
+  const int hl = r / MH_SEEDS, j = r % MH_SEEDS;
+  const int ns = *mh.ns;
+  const bool on = hl < dm.hpg && j < ns;
   float q[D];
   int u = -1;
   float w = 0.f;
-  const bool on = mh_row<T, D>(dm, Qg, mh, gi, g, r, q, u, w);
-  // the furthest seed bounds the tokens any row sees
+  if (on) {
+    u = mh.seeds[j];
+    w = mh.wts[j];
+    const float* qr = Qg + (((int64_t)gi * dm.H + g * dm.hpg + hl) * dm.T + u) * D;
+    const float sc2 = LOG2E / sqrtf((float)D);
+#pragma unroll
+    for (int k = 0; k < D; ++k) q[k] = qr[k] * sc2;
+  } else {
+#pragma unroll
+    for (int k = 0; k < D; ++k) q[k] = 0.f;
+  }
   int umax = -1;
-  for (int s = 0; s < *mh.ns; ++s) umax = max(umax, mh.seeds[s]);
+  for (int s = 0; s < ns; ++s) umax = max(umax, mh.seeds[s]);
   const int64_t c0 = (int64_t)ch * MH_CH;
   const int64_t c1 = min((int64_t)umax + 1, min(c0 + MH_CH, dm.N_c));
-  const T* Kp = K + ((int64_t)l * dm.G + g) * dm.T * D;
+  const float* Kp = K + ((int64_t)l * dm.G + g) * dm.T * D;
   float2 st = make_float2(0.f, 0.f);
   if (PASS == 1 && on) st = mh.rstat[(int64_t)grp * rmax + r];
   float m = -INFINITY, zs = 0.f;
@@ -176,7 +378,7 @@ __global__ __launch_bounds__(256) void k_mh_rows(Dims dm, const T* __restrict__ 
     __syncthreads();
     for (int e = tid; e < MH_SUB * D; e += 256) {
       const int tt = e / D, k = e % D;
-      sk[e] = tt < nt ? ldf(Kp + (s0 + tt) * D, k) : 0.f;
+      sk[e] = tt < nt ? Kp[(s0 + tt) * D + k] : 0.f;
     }
     __syncthreads();
     for (int tt = 0; tt < nt; ++tt) {
@@ -202,11 +404,9 @@ __global__ __launch_bounds__(256) void k_mh_rows(Dims dm, const T* __restrict__ 
     }
     if (PASS == 1) {
       __syncthreads();
-      if (tid < nt) {
-        const int nz = (rmax + 255) / 256;
-        mh.dpart[((int64_t)grp * nz + z) * dm.N_c + s0 + tid] =
+      if (tid < nt)
+        mh.dpart[((int64_t)grp * nz + zb) * dm.N_c + s0 + tid] =
             (red[0][tid] + red[1][tid]) + (red[2][tid] + red[3][tid]);
-      }
     }
   }
   if (PASS == 0 && r < rmax) {
@@ -257,8 +457,7 @@ __global__ __launch_bounds__(1024) void k_mh_finish(Dims dm, MhView mh) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   double a = 0.0;
   for (int64_t t = tid; t < dm.N_c; t += 1024) a += mh.dacc[t];
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+  a = wave_sum(a);
   if (lane == 0) sred[wave] = a;
   __syncthreads();
   double s = 0.0;
@@ -267,36 +466,66 @@ __global__ __launch_bounds__(1024) void k_mh_finish(Dims dm, MhView mh) {
   for (int64_t t = tid; t < dm.N_c; t += 1024) mh.dhat[t] = mh.dacc[t] * inv;
 }
 
-template <typename T, int D>
-static hipError_t mh_hops(const Dims& dm, const T* K, const T* Qg, const TreeView& tv, const MhView& mh,
-                          hipStream_t st) {
+static void mh_seeds(const Dims& dm, const MhView& mh, hipStream_t st) {
+  const unsigned nb = (unsigned)((dm.N_c + MH_TOPB - 1) / MH_TOPB);
+  hipLaunchKernelGGL(k_mh_top, dim3(nb), dim3(256), 0, st, dm, mh);
+  hipLaunchKernelGGL(k_mh_seeds, dim3(1), dim3(1024), 0, st, dm, mh);
+}
+
+template <int D>
+static hipError_t mh_bf16(const Dims& dm, const uint16_t* K, const uint16_t* Q, const uint16_t* Qg,
+                          const TreeView& tv, const MhView& mh, hipStream_t st) {
+  const int rmax = dm.hpg * MH_SEEDS;
+  const int ngrp = dm.n_gl * dm.G;
+  const unsigned nch = (unsigned)((dm.N_c + MH_CH - 1) / MH_CH);
+  const unsigned tb = (unsigned)((dm.N_c + 255) / 256);
+  const dim3 blk(64 * dm.hpg);
+  hipLaunchKernelGGL((k_mh_mfma<D, 2>), dim3(nch, dm.L * dm.G), blk, 0, st, dm, K, Q, tv, mh);
+  hipLaunchKernelGGL(k_mh_seed_score, dim3(tb), dim3(256), 0, st, dm, tv, mh);
+  for (int hop = 0; hop < MH_HOPS; ++hop) {
+    mh_seeds(dm, mh, st);
+    hipLaunchKernelGGL((k_mh_mfma<D, 0>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
+    hipLaunchKernelGGL(k_mh_rowstat_combine, dim3((unsigned)((ngrp * rmax + 255) / 256)), dim3(256), 0, st, dm, mh,
+                       (int)nch);
+    hipLaunchKernelGGL((k_mh_mfma<D, 1>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
+    hipLaunchKernelGGL(k_mh_hop_reduce, dim3(tb), dim3(256), 0, st, dm, mh, hop, 1);
+  }
+  hipLaunchKernelGGL(k_mh_finish, dim3(1), dim3(1024), 0, st, dm, mh);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t mh_f32(const Dims& dm, const float* K, const float* Qg, const TreeView& tv, const MhView& mh,
+                         hipStream_t st) {
   const int rmax = dm.hpg * MH_SEEDS;
   const int ngrp = dm.n_gl * dm.G;
   const int nz = (rmax + 255) / 256;
-  const int nch = (int)((dm.N_c + MH_CH - 1) / MH_CH);
+  const unsigned nch = (unsigned)((dm.N_c + MH_CH - 1) / MH_CH);
   const unsigned tb = (unsigned)((dm.N_c + 255) / 256);
   hipLaunchKernelGGL(k_mh_seed_score, dim3(tb), dim3(256), 0, st, dm, tv, mh);
   for (int hop = 0; hop < MH_HOPS; ++hop) {
-    hipLaunchKernelGGL(k_mh_seeds, dim3(1), dim3(1024), 0, st, dm, mh);
-    hipLaunchKernelGGL((k_mh_rows<T, D, 0>), dim3(nch, ngrp, nz), dim3(256), 0, st, dm, K, Qg, mh);
+    mh_seeds(dm, mh, st);
+    hipLaunchKernelGGL((k_mh_rows<D, 0>), dim3(nch, ngrp, nz), dim3(256), 0, st, dm, K, Qg, mh);
     hipLaunchKernelGGL(k_mh_rowstat_combine, dim3((unsigned)((ngrp * rmax + 255) / 256)), dim3(256), 0, st, dm, mh,
-                       nch);
-    hipLaunchKernelGGL((k_mh_rows<T, D, 1>), dim3(nch, ngrp, nz), dim3(256), 0, st, dm, K, Qg, mh);
+                       (int)nch);
+    hipLaunchKernelGGL((k_mh_rows<D, 1>), dim3(nch, ngrp, nz), dim3(256), 0, st, dm, K, Qg, mh);
     hipLaunchKernelGGL(k_mh_hop_reduce, dim3(tb), dim3(256), 0, st, dm, mh, hop, nz);
   }
   hipLaunchKernelGGL(k_mh_finish, dim3(1), dim3(1024), 0, st, dm, mh);
   return hipGetLastError();
 }
 
-hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q_graph, const TreeView& tv, void* mh_base,
-                           hipStream_t st) {
+hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q, const void* Q_graph, const TreeView& tv,
+                           void* mh_base, hipStream_t st) {
   const MhView mh = mh_view(mh_base, dm);
   if (dm.N_c <= 0) return hipSuccess;
+  if (dm.hpg < 1 || dm.hpg > 8 || dm.W > MH_SEEDS) return hipErrorInvalidValue;
   if (dm.dtype == GRACEKV_BF16) {
-    if (dm.d == 128) return mh_hops<uint16_t, 128>(dm, (const uint16_t*)K, (const uint16_t*)Q_graph, tv, mh, st);
-    if (dm.d == 64) return mh_hops<uint16_t, 64>(dm, (const uint16_t*)K, (const uint16_t*)Q_graph, tv, mh, st);
+    const uint16_t *k = (const uint16_t*)K, *q = (const uint16_t*)Q, *qg = (const uint16_t*)Q_graph;
+    if (dm.d == 128) return mh_bf16<128>(dm, k, q, qg, tv, mh, st);
+    if (dm.d == 64) return mh_bf16<64>(dm, k, q, qg, tv, mh, st);
   } else if (dm.d == 64) {
-    return mh_hops<float, 64>(dm, (const float*)K, (const float*)Q_graph, tv, mh, st);
+    return mh_f32<64>(dm, (const float*)K, (const float*)Q_graph, tv, mh, st);
   }
   return hipErrorInvalidValue;
 }

@@ -96,6 +96,10 @@ def test_multi_hop_workspace_and_arguments():
     # the build workspace exists only with lambda_graph > 0, and then Q_graph
     # and the workspace are checked on the host before anything is enqueued
     assert gk.plan_sizes(_cfg(N_ctx=8192, x=8.0)).build_ws_bytes == 0
+    with pytest.raises(gk.GraceKVError) as e:                 # one wave per query head: at most 8
+        gk.plan_sizes(_cfg(N_ctx=8192, x=8.0, H=64, G=4, lambda_graph=0.3))
+    assert e.value.status == -2
+    gk.plan_sizes(_cfg(N_ctx=8192, x=8.0, H=64, G=4))          # fine without the multi-hop relevance
     c = _cfg(N_ctx=8192, x=8.0, lambda_graph=0.3)
     p = gk.plan_sizes(c)
     assert p.build_ws_bytes >= 3 * p.N_c * 4

@@ -70,20 +70,35 @@ def _check_dhat(case, g0, g1, p):
             ro = (1.0 - LAM) * shat_o[(l, g)] + LAM * dhat_o
             e = np.abs(r1[l * sh.G + g] - ro).max() / ro.max()
             assert e <= RTOL_DHAT, (l, g, e)
+    return len(seeds1)
 
 
 SMALL = [
     CONFIGS["tiny"],
     small_shape("mh-bf16", L=4, G=2, H=8, d=128, N_ctx=2000, W=32, dtype="bf16", x=16.0, n_segments=12),
     small_shape("mh-odd", L=3, G=3, H=3, d=64, N_ctx=700, W=8, x=7.0, n_segments=6),
+    # eight query heads per KV head (one wave each), 24 window queries (rows past W masked)
+    small_shape("mh-hpg8", L=2, G=1, H=8, d=64, N_ctx=1500, W=24, dtype="bf16", x=10.0, n_segments=10),
 ]
 
 
-@pytest.mark.parametrize("shape", SMALL, ids=["tiny-f32", "bf16-d128", "f32-3heads"])
+@pytest.mark.parametrize("shape", SMALL, ids=["tiny-f32", "bf16-d128", "f32-3heads", "bf16-d64-8heads"])
 def test_multi_hop_trees_and_selection(shape):
-    case, g0, g1 = _runs(shape, 4)
+    _trees_and_selection(shape, 4)
+
+
+def test_multi_hop_short_context_share_rule():
+    # a 48-token compressible context: the cumulative-share rule (0.9) stops
+    # before the 64-seed cap
+    n = _trees_and_selection(small_shape("mh-short", L=2, G=2, H=4, d=64, N_ctx=80, W=16, dtype="bf16", x=2.0,
+                                         n_segments=2), 6)
+    assert 0 < n < 64, n
+
+
+def _trees_and_selection(shape, seed):
+    case, g0, g1 = _runs(shape, seed)
     p = dataclasses.replace(O.Params(), lam_graph=LAM)
-    _check_dhat(case, g0, g1, p)
+    n_seeds = _check_dhat(case, g0, g1, p)
     o = H.oracle_run(case, p=p, Qgraph=case["Q_graph"])
     assert g1["slots"] == o.slot_starts
     st = H.compare_trees(o, g1, RTOL_D, ATOL_D, RTOL_R, TAU)
@@ -101,6 +116,7 @@ def test_multi_hop_trees_and_selection(shape):
         for (l, gg), pk in o.packed.items():
             lg = l * shape.G + gg
             assert np.array_equal(pos[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+    return n_seeds
 
 
 def test_multi_hop_relevance_8b_heads_8k():
