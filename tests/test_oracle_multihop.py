@@ -80,3 +80,23 @@ def test_token_values_mix_direct_and_multi_hop():
     z = O.run(*args, slot_starts=slots, kappa=kap, p=dataclasses.replace(O.Params(), lam_graph=0.0), Qgraph=qg)
     for k in base.ctx:
         assert np.array_equal(z.ctx[k].R, base.ctx[k].R)
+
+
+def test_two_hop_worked_example():
+    # tests/golden/multihop_worked_example.txt: seed rule on the mean score,
+    # hop-2 seeds and weights from the zeroed hop-1 scores, zeroing of both
+    # hops' seeds, the decay 0.5 on hop 2, and the final normalisation
+    import os
+    rows = {}
+    with open(os.path.join(os.path.dirname(__file__), "golden", "multihop_worked_example.txt")) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                k, *v = line.split()
+                rows[k] = [float(x) for x in v]
+    K = (np.array(rows["keys_over_ln3"]) * math.log(3.0))[:, None]
+    Qh = np.ones((6, 1))
+    shat = {(0, 0): np.array(rows["s_a"]), (0, 1): np.array(rows["s_b"])}
+    p = dataclasses.replace(O.Params(), m_seed=int(rows["m_seed"][0]))
+    dhat = O.multi_hop(shat, {(0, 0): K}, {(0, 0): Qh}, 1, 1, 6, p)
+    want = np.array(rows["dhat_times_6926"]) / 6926.0
+    assert np.allclose(dhat, want, rtol=2e-6, atol=0.0), (dhat, want)
