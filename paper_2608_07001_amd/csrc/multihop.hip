@@ -217,7 +217,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
     if (MODE == 2) {
       qrow = Qs + (((int64_t)l * dm.H + h) * dm.W + (ok ? j : 0)) * D;
       uj[rt] = ok ? 0x7fffffff : -1;
-      wj[rt] = 1.f;
+      wj[rt] = ok ? 1.f : 0.f;                // a masked row has a zero query: weight 0 times 2^(-0)
       cj[rt] = 0.f;
       if (ok) {
         const float4 st = tv.row_stats[((int64_t)l * dm.G + g) * dm.rows + w * dm.W + j];
@@ -285,14 +285,23 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
         }
       } else {
         float sv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (MODE == 2 && 16 * tt + 16 <= nt) {
+          // direct pass, no token past the chunk: every row sees every token
+          // and the masked rows weigh 0
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
+          for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const bool ok = tb + r < c1 && tb + r <= uj[rt];
-            const float v = wj[rt] * __builtin_amdgcn_exp2f(acc[rt][r] * sc2 - cj[rt]);
-            sv[r] += ok ? v : 0.f;
-          }
+            for (int r = 0; r < 4; ++r) sv[r] += wj[rt] * __builtin_amdgcn_exp2f(acc[rt][r] * sc2 - cj[rt]);
+        } else {
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const bool ok = tb + r < c1 && tb + r <= uj[rt];
+              const float v = wj[rt] * __builtin_amdgcn_exp2f(acc[rt][r] * sc2 - cj[rt]);
+              sv[r] += ok ? v : 0.f;
+            }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) sv[r] = row_sum16(sv[r]);
         if (i16 < 4) red[w][16 * tt + 4 * g4 + i16] = i16 == 0 ? sv[0] : i16 == 1 ? sv[1] : i16 == 2 ? sv[2] : sv[3];
