@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--lambda-graph", type=float, default=0.0,
                     help="mix the multi-hop relevance into the token values with this weight (e.g. 0.3); the "
                          "queries of every position at the propagation layers are synthesised")
+    ap.add_argument("--no-multi-hop", action="store_true",
+                    help="skip the second measurement with the multi-hop relevance (lambda_graph = 0.3)")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention measurement")
     ap.add_argument("--no-overlap", action="store_true",
@@ -225,50 +227,57 @@ def main():
     if overlap:
         cfg_b.flags |= gk.FLAG_STATS_READY
 
-    def step(ev=None):
-        def mark(i):
-            if ev is not None:
-                ev[i].record(stream)
-        mark(0)
-        if overlap:
-            fork = torch.cuda.Event()
-            fork.record(stream)
-            side.wait_event(fork)
-            gk.relevance_stats(cfg, case["K"], case["Q"], buf.trees, side)
-            join = torch.cuda.Event()
-            join.record(side)
-        gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
-                   buf.seg_ws, stream)
-        mark(1)
-        if overlap:
-            stream.wait_event(join)
-        gk.build_trees(cfg_b, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], buf.slot_starts,
-                       buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"], Q_graph=q_graph,
-                       ws=buf.build_ws)
-        mark(2)
-        gk.score(cfg, case["omega_raw"], buf.trees, stream)
-        mark(3)
-        gk.select(cfg, buf.trees, buf.b_used, buf.sel_ws, stream)
-        mark(4)
-        gk.pack(cfg, case["K"], case["V"], case["rope_cos"], case["rope_sin"], buf.trees, buf.offsets,
-                buf.counts, buf.K_out, buf.V_out, buf.pos_out, buf.logm_out, buf.pack_ws, stream)
-        mark(5)
+    def make_step(cfg, cfg_b, buf, q_graph):
+        def step(ev=None):
+            def mark(i):
+                if ev is not None:
+                    ev[i].record(stream)
+            mark(0)
+            if overlap:
+                fork = torch.cuda.Event()
+                fork.record(stream)
+                side.wait_event(fork)
+                gk.relevance_stats(cfg, case["K"], case["Q"], buf.trees, side)
+                join = torch.cuda.Event()
+                join.record(side)
+            gk.segment(cfg, case["hidden"], case["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots,
+                       buf.seg_ws, stream)
+            mark(1)
+            if overlap:
+                stream.wait_event(join)
+            gk.build_trees(cfg_b, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"],
+                           buf.slot_starts, buf.n_slots, buf.kappa, buf.trees, stream, omega_raw=case["omega_raw"],
+                           Q_graph=q_graph, ws=buf.build_ws)
+            mark(2)
+            gk.score(cfg, case["omega_raw"], buf.trees, stream)
+            mark(3)
+            gk.select(cfg, buf.trees, buf.b_used, buf.sel_ws, stream)
+            mark(4)
+            gk.pack(cfg, case["K"], case["V"], case["rope_cos"], case["rope_sin"], buf.trees, buf.offsets,
+                    buf.counts, buf.K_out, buf.V_out, buf.pos_out, buf.logm_out, buf.pack_ws, stream)
+            mark(5)
+        return step
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    gk.check(cfg, buf.trees, stream)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(evs[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     names = ["segment", "build", "score", "select", "pack"]
-    stage_ms = {n: sum(evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(args.steps)) / args.steps
-                for i, n in enumerate(names)}
-    ms = sum(evs[s][0].elapsed_time(evs[s][5]) for s in range(args.steps)) / args.steps
+
+    def timed(step, steps, warmup, cfg, buf):
+        """(ms per step, per-stage ms) from HIP events on the stream the calls run on."""
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        gk.check(cfg, buf.trees, stream)
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for s_ in range(steps):
+            step(evs[s_])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - w0
+        st = {n: sum(evs[k][i].elapsed_time(evs[k][i + 1]) for k in range(steps)) / steps for i, n in enumerate(names)}
+        return sum(evs[k][0].elapsed_time(evs[k][5]) for k in range(steps)) / steps, st, wall
+
+    step = make_step(cfg, cfg_b, buf, q_graph)
+    ms, stage_ms, wall = timed(step, args.steps, args.warmup, cfg, buf)
     if args.copy_probe_mib > 0:                    # untimed: a plain copy of known size for the counters
         a = torch.ones(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
         b2 = torch.empty_like(a)
@@ -311,6 +320,23 @@ def main():
     }
     if not args.no_decode:
         res["decode_attention"] = decode_measure(cfg, sh, case, buf, stream)
+    if not args.no_multi_hop and q_graph is None and not (args.ablation_pair_quotas or args.ablation_uniform_slots):
+        # the same step with the multi-hop relevance mixed into the token values
+        # (lambda_graph = 0.3, the paper's default weight); inputs already resident
+        lam = 0.3
+        cfg_m = gk.Config.from_buffer_copy(cfg)
+        cfg_m.lambda_graph = lam
+        buf_m = gk.allocate(cfg_m, dev)
+        qg = make_graph_queries(sh, args.seed, case["K"], case["rope_cos"], case["rope_sin"], device=dev)
+        cfg_mb = gk.Config.from_buffer_copy(cfg_m)
+        if overlap:
+            cfg_mb.flags |= gk.FLAG_STATS_READY
+        ms_m, st_m, _ = timed(make_step(cfg_m, cfg_mb, buf_m, qg), args.steps, args.warmup, cfg_m, buf_m)
+        res["multi_hop"] = {"lambda_graph": lam, "ms_per_step": ms_m, "value": tokens / (ms_m * 1e-3),
+                            "unit": "tokens/s", "stages_ms": st_m, "extra_ms_vs_direct": ms_m - ms,
+                            "b_used": int(buf_m.b_used.item())}
+        del buf_m, qg
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline and q_graph is None:
         res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)
     print(json.dumps(res), flush=True)

@@ -87,6 +87,10 @@ def test_pruned_equals_complete_build_at_full_size(runs):
 
 def test_budget_and_frontier_properties_at_full_size(runs):
     case, pr, fu = runs
+    _budget_and_frontier(pr)
+
+
+def _budget_and_frontier(pr):
     p = pr.plan
     LG = SH.L * SH.G
     b_used = int(pr.b_used.item())
@@ -200,3 +204,42 @@ def test_decode_attention_at_full_size(runs):
         assert err <= tol, (l, h, err, tol)
         worst = max(worst, err / float(np.abs(want).max()))
     print(f"full size decode: {len(pairs)} (l, h) pairs, max rel err {worst:.2e}")
+
+
+def test_multi_hop_properties_at_full_size(runs):
+    # the multi-hop relevance (lambda_graph = 0.3) on the full-size workload, run
+    # as bench.py --lambda-graph 0.3 runs it.  The oracle cannot produce d-hat at
+    # this size (it needs s-hat of every (l, g)); what holds at any size: d-hat,
+    # read back as (R_mixed - (1 - lambda) s-hat) / lambda, is one distribution
+    # shared by every (l, g) row; the mixed values of each row sum to 1; the
+    # budget and frontier properties hold
+    from synth.workloads import make_graph_queries
+    case, pr, fu = runs
+    lam = 0.3
+    qg = make_graph_queries(SH, 0, case["K"], case["rope_cos"], case["rope_sin"], device="cuda")
+    cfg = H.make_cfg(SH, flags=gk.FLAG_PRUNE, lambda_graph=lam)
+    buf = gk.allocate(cfg)
+    gk.compress(buf, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], case["hidden"],
+                case["surprisal"], case["omega_raw"], Q_graph=qg)
+    torch.cuda.synchronize()
+    gk.check(cfg, buf.trees)
+    p = buf.plan
+    LG = SH.L * SH.G
+    assert torch.equal(buf.slot_starts, pr.slot_starts)
+    view = lambda b: b.trees[p.off_tok_R:p.off_tok_R + LG * p.N_c * 4].view(torch.float32).view(LG, p.N_c).double()
+    s0, r1 = view(pr), view(buf)
+    lf = float(np.float32(lam))                    # the weights as the kernel forms them in fp32
+    dh = (r1 - float(np.float32(1.0) - np.float32(lam)) * s0) / lf
+    dmean = dh.mean(dim=0)
+    spread = float((dh - dmean).abs().max())
+    top = float(dmean.max())
+    print(f"full size multi-hop: d-hat max {top:.3e}, row spread / max {spread / top:.2e}, "
+          f"sum {float(dmean.sum()):.6f}, zeros {int((dmean.abs() < 1e-6 * top).sum())}")
+    assert spread <= 1e-5 * top
+    assert abs(float(dmean.sum()) - 1.0) < 1e-4
+    assert float(dmean.min()) >= -1e-6 * top
+    assert float((r1.sum(dim=1) - 1.0).abs().max()) < 1e-4
+    assert not torch.allclose(r1, s0)
+    _budget_and_frontier(buf)
+    del buf, qg
+    torch.cuda.empty_cache()
