@@ -217,8 +217,8 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
     if (MODE == 2) {
       qrow = Qs + (((int64_t)l * dm.H + h) * dm.W + (ok ? j : 0)) * D;
       uj[rt] = ok ? 0x7fffffff : -1;
-      wj[rt] = ok ? 1.f : 0.f;                // a masked row has a zero query: weight 0 times 2^(-0)
-      cj[rt] = 0.f;
+      wj[rt] = ok ? 1.f : 0.f;
+      cj[rt] = INFINITY;                      // a masked row (zero query) contributes 2^(-inf) = 0
       if (ok) {
         const float4 st = tv.row_stats[((int64_t)l * dm.G + g) * dm.rows + w * dm.W + j];
         cj[rt] = st.x * LOG2E + __log2f(st.y);
@@ -287,11 +287,11 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
         float sv[4] = {0.f, 0.f, 0.f, 0.f};
         if (MODE == 2 && 16 * tt + 16 <= nt) {
           // direct pass, no token past the chunk: every row sees every token
-          // and the masked rows weigh 0
+          // (weight 1) and the masked rows add 0
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sv[r] += wj[rt] * __builtin_amdgcn_exp2f(acc[rt][r] * sc2 - cj[rt]);
+            for (int r = 0; r < 4; ++r) sv[r] += __builtin_amdgcn_exp2f(fmaf(acc[rt][r], sc2, -cj[rt]));
         } else {
 #pragma unroll
           for (int rt = 0; rt < 4; ++rt)

@@ -263,10 +263,14 @@ __global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __
         // lane holds tokens s0 + 32 tp + 16 h + 4 g4 + r of its row
         float y[8];
         if (allC) {
+          // every token of the block is in C and visible to every window query;
+          // a lane of a row past the last one computes on row 0's query and its
+          // statistics are never written
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) y[4 * h + r] = rok[k] ? acc[h][r] * sc2 : -INFINITY;
+            for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[h][r] * sc2;
+          lse2_add8(mC[k], zC[k], y);
         } else {
           float xt[8];
 #pragma unroll
@@ -281,8 +285,8 @@ __global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __
             }
           lse_add4(mT[k], zT[k], xt[0], xt[1], xt[2], xt[3]);
           lse_add4(mT[k], zT[k], xt[4], xt[5], xt[6], xt[7]);
+          lse2_add8(mC[k], zC[k], y);
         }
-        lse2_add8(mC[k], zC[k], y);
       }
     }
   }
