@@ -125,3 +125,45 @@ def test_multi_hop_relevance_8b_heads_8k():
     shape = small_shape("mh-8k", L=4, G=8, H=32, d=128, N_ctx=8000, W=64, dtype="bf16", x=8.0, n_segments=60)
     case, g0, g1 = _runs(shape, 5)
     _check_dhat(case, g0, g1, dataclasses.replace(O.Params(), lam_graph=LAM))
+
+
+def test_multi_hop_pruned_build_equals_complete_build_and_second_stream():
+    # with the mix the budget-pruned build must still select and pack exactly
+    # what the complete build does, and the relevance statistics may come from
+    # gracekv_relevance_stats (GRACEKV_FLAG_STATS_READY) as bench.py runs them
+    from paper_2608_07001_amd import gracekv as gk
+    shape = small_shape("mh-prune", L=4, G=4, H=16, d=128, N_ctx=6000, W=64, dtype="bf16", x=32.0, n_segments=40)
+    case = make_case(shape, 8, with_hidden=True)
+    case["Q_graph"] = make_graph_queries(shape, 8, case["K"], case["rope_cos"], case["rope_sin"])
+    dev = H.to_dev(case)
+    full = H.gpu_run(dev, Q_graph=dev["Q_graph"], lambda_graph=LAM)
+    pruned = H.gpu_run(dev, Q_graph=dev["Q_graph"], prune=True, lambda_graph=LAM)
+    assert pruned["slots"] == full["slots"]
+    assert torch.equal(pruned["tok_R"], full["tok_R"])
+    assert pruned["b_used"] == full["b_used"]
+    assert torch.equal(pruned["offsets"], full["offsets"])
+    n = int(full["offsets"][-1])
+    for k in ("pos_out", "logm_out", "K_out", "V_out"):
+        assert torch.equal(pruned[k][:n], full[k][:n]), k
+    # the same build with the row statistics from the separate call
+    cfg = H.make_cfg(shape, flags=gk.FLAG_PRUNE, lambda_graph=LAM)
+    buf = gk.allocate(cfg)
+    gk.segment(cfg, dev["hidden"], dev["surprisal"], buf.kappa, buf.bscore, buf.slot_starts, buf.n_slots, buf.seg_ws)
+    gk.relevance_stats(cfg, dev["K"], dev["Q"], buf.trees)
+    cfg_b = gk.Config.from_buffer_copy(cfg)
+    cfg_b.flags |= gk.FLAG_STATS_READY
+    gk.build_trees(cfg_b, dev["K"], dev["V"], dev["Q"], dev["rope_cos"], dev["rope_sin"], buf.slot_starts,
+                   buf.n_slots, buf.kappa, buf.trees, omega_raw=dev["omega_raw"], Q_graph=dev["Q_graph"],
+                   ws=buf.build_ws)
+    gk.score(cfg, dev["omega_raw"], buf.trees)
+    gk.select(cfg, buf.trees, buf.b_used, buf.sel_ws)
+    gk.pack(cfg, dev["K"], dev["V"], dev["rope_cos"], dev["rope_sin"], buf.trees, buf.offsets, buf.counts,
+            buf.K_out, buf.V_out, buf.pos_out, buf.logm_out, buf.pack_ws)
+    torch.cuda.synchronize()
+    gk.check(cfg, buf.trees)
+    LG = shape.L * shape.G
+    p = buf.plan
+    tr = buf.trees[p.off_tok_R:p.off_tok_R + LG * p.N_c * 4].view(torch.float32).cpu()
+    assert torch.equal(tr, pruned["tok_R"])
+    assert torch.equal(buf.offsets.cpu(), pruned["offsets"])
+    assert torch.equal(buf.pos_out[:n].cpu(), pruned["pos_out"][:n])
