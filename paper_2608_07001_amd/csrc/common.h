@@ -136,6 +136,11 @@ hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, 
                          const float* logm_out, const void* K, const void* V, float* out, void* ws, hipStream_t st);
 constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0, TreeView at 512
 hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
+// bf16 caches with at most 8 query heads per KV head: the direct relevance s-hat
+// of every token comes from its own pass (launch_token_relevance, after the row
+// statistics) and the root kernel reads it from the token values.
+inline bool token_relevance_pass(const Dims& dm) { return dm.dtype == GRACEKV_BF16 && dm.hpg <= 8 && dm.W <= 64; }
+hipError_t launch_token_relevance(const Dims& dm, const void* K, const void* Q, const TreeView& tv, hipStream_t st);
 size_t mh_bytes(const Dims& dm);
 MhView mh_view(void* base, const Dims& dm);
 hipError_t launch_multihop(const Dims& dm, const void* K, const void* Q, const void* Q_graph, const TreeView& tv,

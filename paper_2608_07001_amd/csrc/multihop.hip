@@ -4,9 +4,10 @@
 // Runs inside gracekv_build_trees when lambda_graph > 0, once the relevance
 // row statistics (m_V, Z_V per window query) and the per-(l, g) sums S_{l,g}
 // are known:
-//   * s-hat of every (l, g) into the token-value array: bf16 caches by the
-//     direct pass below (the root kernel later overwrites those values); fp32
-//     caches by a first run of the root kernel;
+//   * s-hat of every (l, g) is in the token-value array: bf16 caches from the
+//     token relevance pass below (run for every build; the root kernel later
+//     overwrites the values with the mix); fp32 caches from a first run of the
+//     root kernel;
 //   * k_mh_seed_score: S_t = mean over (l, g) of s-hat_{l,g,t};
 //   * k_mh_top + k_mh_seeds: the positions in descending score (ties to the
 //     smaller position) while their cumulative share of the total stays below
@@ -489,7 +490,7 @@ static hipError_t mh_bf16(const Dims& dm, const uint16_t* K, const uint16_t* Q, 
   const unsigned nch = (unsigned)((dm.N_c + MH_CH - 1) / MH_CH);
   const unsigned tb = (unsigned)((dm.N_c + 255) / 256);
   const dim3 blk(64 * dm.hpg);
-  hipLaunchKernelGGL((k_mh_mfma<D, 2>), dim3(nch, dm.L * dm.G), blk, 0, st, dm, K, Q, tv, mh);
+  (void)Q;                                    // s-hat is in the token values (launch_token_relevance)
   hipLaunchKernelGGL(k_mh_seed_score, dim3(tb), dim3(256), 0, st, dm, tv, mh);
   for (int hop = 0; hop < MH_HOPS; ++hop) {
     mh_seeds(dm, mh, st);
@@ -521,6 +522,23 @@ static hipError_t mh_f32(const Dims& dm, const float* K, const float* Qg, const 
     hipLaunchKernelGGL(k_mh_hop_reduce, dim3(tb), dim3(256), 0, st, dm, mh, hop, nz);
   }
   hipLaunchKernelGGL(k_mh_finish, dim3(1), dim3(1024), 0, st, dm, mh);
+  return hipGetLastError();
+}
+
+// The direct relevance s-hat of every (l, g, t) into the token values (bf16
+// caches, hpg <= 8): the pass-2 sums of eq:app_direct_relevance over the hpg W
+// window-query rows, each normalised by its row statistics, divided by S_{l,g}.
+hipError_t launch_token_relevance(const Dims& dm, const void* K, const void* Q, const TreeView& tv, hipStream_t st) {
+  if (!token_relevance_pass(dm)) return hipErrorInvalidValue;
+  if (dm.N_c <= 0) return hipSuccess;
+  const MhView none{};
+  const dim3 grid((unsigned)((dm.N_c + MH_CH - 1) / MH_CH), (unsigned)(dm.L * dm.G)), blk(64 * dm.hpg);
+  if (dm.d == 128)
+    hipLaunchKernelGGL((k_mh_mfma<128, 2>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
+  else if (dm.d == 64)
+    hipLaunchKernelGGL((k_mh_mfma<64, 2>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

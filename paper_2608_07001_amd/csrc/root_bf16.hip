@@ -87,7 +87,9 @@ __device__ __forceinline__ float pick4f(const float* v, int i) {
   return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
-template <int D, bool MP>
+// RI: the direct relevance s-hat is already in the token values (the token
+// relevance pass ran before), so only the probe rows are evaluated here.
+template <int D, bool MP, bool RI>
 __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ V, const uint16_t* __restrict__ Q,
                                                      const float* __restrict__ cosT, const float* __restrict__ sinT,
@@ -101,7 +103,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
   constexpr int H2 = D / 2;
   constexpr int DT = D / 16;                 // 16-wide value tiles of M^T
   constexpr int KS = D / 32;                 // k steps of a logit tile
-  constexpr int HG = 4;                      // head slots whose Q rows are held at once
+  constexpr int HG = RI ? 1 : 4;             // head slots whose Q rows are held at once
   constexpr int CHP = H2 / 8;                // 8-dim pair chunks per token in the k° staging
   constexpr int CPR = D / 8;                 // 16-byte chunks per V row
   extern __shared__ __align__(16) char smem[];
@@ -137,7 +139,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
   const int hp = uq % dm.hpg;                 // query head of probe u
   const bool wave_on = 16 * w < dm.W;
   const bool wave_full = 16 * w + 16 <= dm.W;  // every query of the wave exists
-  const int npass = MP ? (dm.hpg + HG - 1) / HG : 1;
+  const int npass = (MP && !RI) ? (dm.hpg + HG - 1) / HG : 1;
   const int klast = HG * (npass - 1);         // first slot of the last pass (run first)
   // Q rows of head slots k0 .. k0 + HG - 1 (slot k = head (hp + k) mod |H(g)|): lane (i, g)
   // holds dims 32 s + 8 g .. + 7 of its query for k step s; row statistics (m_V, 1 / Z_V),
@@ -156,8 +158,10 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
       const uint16_t* qrow = Q + (((int64_t)l * dm.H + (int64_t)g * dm.hpg + hl) * dm.W + uq) * D;
 #pragma unroll
       for (int s = 0; s < KS; ++s) qr[h][s] = *(const uint4*)(qrow + 32 * s + g8);
-      const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
-      cR[h] = k < dm.hpg ? st.x * 1.44269504088896341f + __log2f(st.y) : INFINITY;
+      if constexpr (!RI) {
+        const float4 st = tv.row_stats[(int64_t)lg * dm.rows + hl * dm.W + uq];
+        cR[h] = k < dm.hpg ? st.x * 1.44269504088896341f + __log2f(st.y) : INFINITY;
+      }
     }
   };
 
@@ -212,7 +216,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
     const int nb = (n + 31) >> 5;             // 32-token blocks
     const uint16_t* Kp = K + ((int64_t)lg * dm.T + a0) * D;
     const uint16_t* Vp = V + ((int64_t)lg * dm.T + a0) * D;
-    if (lg != cur_lg || MP) {
+    if (lg != cur_lg || (MP && !RI)) {
       if (wave_on) load_pass(l, g, lg, klast);
       if (lg != cur_lg) {
         if (wave_on) {
@@ -317,7 +321,7 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
     float Zl = 0.f;
     if (wave_on) {
       for (int k0 = klast; k0 >= 0; k0 -= HG) {
-        if (MP && k0 != klast) load_pass(l, g, lg, k0);
+        if (MP && !RI && k0 != klast) load_pass(l, g, lg, k0);
         for (int b = 0; b < nb; ++b) {
           float ev[8];                        // probe exponentials of the block, (tile, row) order
           const bool full = wave_full && 32 * b + 32 <= n;   // no token or query to mask
@@ -340,12 +344,14 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
             // lane holds tokens t0 + r of its query in every slot:
             // pi = e^{l - m_V} / Z_V = 2^(acc sc2 - cR)
             float Rp[4];
+            if constexpr (!RI) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              float s = 0.f;
+              for (int r = 0; r < 4; ++r) {
+                float s = 0.f;
 #pragma unroll
-              for (int h = 0; h < HG; ++h) s += __builtin_amdgcn_exp2f(acc[h][r] * sc2 - cR[h]);
-              Rp[r] = (full || (uok && t0 + r < n)) ? s : 0.f;
+                for (int h = 0; h < HG; ++h) s += __builtin_amdgcn_exp2f(acc[h][r] * sc2 - cR[h]);
+                Rp[r] = (full || (uok && t0 + r < n)) ? s : 0.f;
+              }
             }
             if (k0 == 0) {
               float ap[4];
@@ -361,11 +367,13 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
               for (int r = 0; r < 4; ++r) ap[r] = row_sum16(ap[r]);
               if (i16 < 4) sAp[w * NMAX + t0 + i16] = pick4f(ap, i16);
             }
+            if constexpr (!RI) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) Rp[r] = row_sum16(Rp[r]);
-            if (i16 < 4) {
-              float* dst = sRp + w * NMAX + t0 + i16;
-              *dst = (k0 == klast ? 0.f : *dst) + pick4f(Rp, i16);
+              for (int r = 0; r < 4; ++r) Rp[r] = row_sum16(Rp[r]);
+              if (i16 < 4) {
+                float* dst = sRp + w * NMAX + t0 + i16;
+                *dst = (k0 == klast ? 0.f : *dst) + pick4f(Rp, i16);
+              }
             }
           }
           if (k0 == 0) {
@@ -393,8 +401,12 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
         float s = 0.f, am = 0.f;
 #pragma unroll
         for (int w2 = 0; w2 < RB_W; ++w2)
-          if (16 * w2 < dm.W) { s += sRp[w2 * NMAX + tid]; am += sAp[w2 * NMAX + tid]; }
-        R = s / Sg;
+          if (16 * w2 < dm.W) {
+            if constexpr (!RI) s += sRp[w2 * NMAX + tid];
+            am += sAp[w2 * NMAX + tid];
+          }
+        if constexpr (RI) R = tv.tok_R[(int64_t)lg * dm.N_c + a0 + tid];
+        else R = s / Sg;
         if (tv.dhat) R = (1.f - dm.lam_graph) * R + dm.lam_graph * tv.dhat[a0 + tid];   // eq:app_bottom_up_value
         A = am / (float)dm.W;
         kn = Kn[tid];
@@ -525,9 +537,10 @@ hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const 
   const int64_t cap = (int64_t)dm.L * dm.G * dm.J_cap;
   const dim3 grid((unsigned)(cap < RB_GRID ? cap : RB_GRID));
   const int lds = root_bf16_lds_bytes(dm.d);
+  const bool ri = token_relevance_pass(dm);   // s-hat already in the token values
 #define GKV_LAUNCH_ROOT_BF(DD)                                                                              \
   do {                                                                                                      \
-    auto fn = dm.hpg > 4 ? k_root_bf<DD, true> : k_root_bf<DD, false>;                                      \
+    auto fn = ri ? k_root_bf<DD, false, true> : (dm.hpg > 4 ? k_root_bf<DD, true, false> : k_root_bf<DD, false, false>); \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);  \
     if (e0 != hipSuccess) return e0;                                                                        \
     hipLaunchKernelGGL(fn, grid, dim3(RB_T), lds, st, (const Dims*)tv.kargs, (const uint16_t*)K,            \
