@@ -33,7 +33,8 @@ namespace gkv {
 
 constexpr int RB_T = 256;          // threads per workgroup
 constexpr int RB_W = RB_T / 64;    // waves
-constexpr int RB_GRID = 2048;      // persistent workgroups
+constexpr int RB_GRID = 2048;      // persistent workgroups (two per CU, four rounds)
+constexpr int RB_GRID_RI = 2304;   // ... without K rows in LDS (three per CU, three rounds)
 
 template <int D>
 struct RbLds {
@@ -90,7 +91,7 @@ __device__ __forceinline__ float pick4f(const float* v, int i) {
 // RI: the direct relevance s-hat is already in the token values (the token
 // relevance pass ran before), so only the probe rows are evaluated here.
 template <int D, bool MP, bool RI>
-__global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
+__global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ V, const uint16_t* __restrict__ Q,
                                                      const float* __restrict__ cosT, const float* __restrict__ sinT,
                                                      const int32_t* __restrict__ slot_starts,
@@ -260,8 +261,10 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
         if (e < nk) {
           uint4 ka = k1, kc = k2;
           if (t >= n) { ka = make_uint4(0, 0, 0, 0); kc = ka; }
-          *(uint4*)(sK + t * Lay::LDK + c) = ka;
-          *(uint4*)(sK + t * Lay::LDK + c + H2) = kc;
+          if constexpr (!RI) {                // RI: the logits read K from L2 (staged here once)
+            *(uint4*)(sK + t * Lay::LDK + c) = ka;
+            *(uint4*)(sK + t * Lay::LDK + c + H2) = kc;
+          }
           const uint32_t w1[4] = {ka.x, ka.y, ka.z, ka.w}, w2[4] = {kc.x, kc.y, kc.z, kc.w};
           const float cs8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
           const float sn8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
@@ -325,6 +328,18 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
         for (int b = 0; b < nb; ++b) {
           float ev[8];                        // probe exponentials of the block, (tile, row) order
           const bool full = wave_full && 32 * b + 32 <= n;   // no token or query to mask
+          // RI: the block's K fragments straight from L2 (the rows were just
+          // read by the staging), rows past n clamped (their logits are masked)
+          uint4 kg[RI ? 2 : 1][KS];
+          if constexpr (RI) {
+#pragma unroll
+            for (int tl = 0; tl < 2; ++tl) {
+              const int tr = 32 * b + 16 * tl + i16;
+              const uint16_t* kr = Kp + (int64_t)(tr < n ? tr : n - 1) * D + 8 * g4;
+#pragma unroll
+              for (int s = 0; s < KS; ++s) kg[tl][s] = *(const uint4*)(kr + 32 * s);
+            }
+          }
 #pragma unroll
           for (int tl = 0; tl < 2; ++tl) {
             const int t0 = 32 * b + 16 * tl + 4 * g4;   // the lane's first token of this tile
@@ -332,10 +347,15 @@ __global__ __launch_bounds__(RB_T, 2) void k_root_bf(const Dims* __restrict__ dm
 #pragma unroll
             for (int h = 0; h < HG; ++h) acc[h] = f32x4{0.f, 0.f, 0.f, 0.f};
             {
-              const uint16_t* kr = sK + (32 * b + 16 * tl + i16) * Lay::LDK + 8 * g4;
               uint4 kv[KS];
+              if constexpr (RI) {
 #pragma unroll
-              for (int s = 0; s < KS; ++s) kv[s] = *(const uint4*)(kr + 32 * s);
+                for (int s = 0; s < KS; ++s) kv[s] = kg[tl][s];
+              } else {
+                const uint16_t* kr = sK + (32 * b + 16 * tl + i16) * Lay::LDK + 8 * g4;
+#pragma unroll
+                for (int s = 0; s < KS; ++s) kv[s] = *(const uint4*)(kr + 32 * s);
+              }
 #pragma unroll
               for (int s = 0; s < KS; ++s)
 #pragma unroll
@@ -535,9 +555,11 @@ hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const 
                             const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const TreeView& tv,
                             hipStream_t st) {
   const int64_t cap = (int64_t)dm.L * dm.G * dm.J_cap;
-  const dim3 grid((unsigned)(cap < RB_GRID ? cap : RB_GRID));
-  const int lds = root_bf16_lds_bytes(dm.d);
   const bool ri = token_relevance_pass(dm);   // s-hat already in the token values
+  // RI: no K rows in LDS (they are the last region), three workgroups per CU
+  const int64_t gmax = ri ? RB_GRID_RI : RB_GRID;
+  const dim3 grid((unsigned)(cap < gmax ? cap : gmax));
+  const int lds = ri ? (dm.d == 128 ? RbLds<128>::oK : RbLds<64>::oK) : root_bf16_lds_bytes(dm.d);
 #define GKV_LAUNCH_ROOT_BF(DD)                                                                              \
   do {                                                                                                      \
     auto fn = ri ? k_root_bf<DD, false, true> : (dm.hpg > 4 ? k_root_bf<DD, true, false> : k_root_bf<DD, false, false>); \
