@@ -320,7 +320,7 @@ def main():
         "wall_s": wall,
         "roofline": {"kernel": "gracekv_build_trees call (" + ("k_root_bf, theta passes, k_work_mark, k_refine; the "
                                                                 "relevance passes run on the second stream)" if overlap else
-                                                                "k_rowstats_bf, k_mh_mfma token relevance, k_root_bf, "
+                                                                "k_rowstats_bf, k_rel_rows token relevance, k_root_bf, "
                                                                 "theta passes, k_work_mark, k_refine)"), "bound": "hbm",
                      "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": build_gbs / HBM_PEAK_GBS, "traffic": traffic},

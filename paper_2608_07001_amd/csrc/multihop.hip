@@ -181,12 +181,15 @@ __global__ __launch_bounds__(1024) void k_mh_seeds(Dims dm, MhView mh) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16: logits on MFMA.  MODE 0: hop row statistics; MODE 1: hop token sums;
-// MODE 2: direct relevance s-hat of (l, g) into the token values.  Block:
+// bf16: relevance rows on MFMA.  RR_HOP_STATS: hop row statistics;
+// RR_HOP_SUMS: hop token sums; RR_DIRECT: direct relevance s-hat of (l, g) into
+// the token values (the token relevance pass).  Block:
 // one wave per query head slot of the group (hpg waves).
 // ---------------------------------------------------------------------------
+enum { RR_HOP_STATS = 0, RR_HOP_SUMS = 1, RR_DIRECT = 2 };
+
 template <int D, int MODE>
-__global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __restrict__ K,
+__global__ __launch_bounds__(512) void k_rel_rows(Dims dm, const uint16_t* __restrict__ K,
                                                  const uint16_t* __restrict__ Qs, TreeView tv, MhView mh) {
   constexpr int KS = D / 32;
   constexpr int LDK = D + 8;                  // staged key row stride (bf16): conflict-free fragment reads
@@ -196,11 +199,11 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
   const int ch = blockIdx.x, grp = blockIdx.y;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
   const int nw = blockDim.x >> 6;
-  const int gi = MODE == 2 ? 0 : grp / dm.G;
+  const int gi = MODE == RR_DIRECT ? 0 : grp / dm.G;
   const int g = grp % dm.G;
-  const int l = MODE == 2 ? grp / dm.G : dm.gl[gi];
+  const int l = MODE == RR_DIRECT ? grp / dm.G : dm.gl[gi];
   const int h = g * dm.hpg + w;               // the wave's query head
-  const int nrow = MODE == 2 ? dm.W : *mh.ns;
+  const int nrow = MODE == RR_DIRECT ? dm.W : *mh.ns;
   const int rmax = dm.hpg * MH_SEEDS;
   const float sc2 = LOG2E / sqrtf((float)D);
   // the wave's rows j = 16 rt + i16: query fragment, causal limit, weight, log2 normaliser
@@ -208,14 +211,14 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
   int uj[4];
   float wj[4], cj[4];
   int umax = -1;
-  if (MODE != 2)
+  if (MODE != RR_DIRECT)
     for (int s = 0; s < nrow; ++s) umax = max(umax, mh.seeds[s]);
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) {
     const int j = 16 * rt + i16;
     const bool ok = j < nrow;
     const uint16_t* qrow;
-    if (MODE == 2) {
+    if (MODE == RR_DIRECT) {
       qrow = Qs + (((int64_t)l * dm.H + h) * dm.W + (ok ? j : 0)) * D;
       uj[rt] = ok ? 0x7fffffff : -1;
       wj[rt] = ok ? 1.f : 0.f;
@@ -230,7 +233,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
       uj[rt] = ok ? u : -1;
       wj[rt] = ok ? mh.wts[j] : 0.f;
       cj[rt] = 0.f;
-      if (MODE == 1 && ok) {
+      if (MODE == RR_HOP_SUMS && ok) {
         const float2 st = mh.rstat[(int64_t)grp * rmax + w * MH_SEEDS + j];
         cj[rt] = st.x + st.y;
       }
@@ -241,7 +244,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
   }
   const int64_t c0 = (int64_t)ch * MH_CH;
   int64_t c1 = c0 + MH_CH < dm.N_c ? c0 + MH_CH : dm.N_c;
-  if (MODE != 2 && (int64_t)umax + 1 < c1) c1 = (int64_t)umax + 1;
+  if (MODE != RR_DIRECT && (int64_t)umax + 1 < c1) c1 = (int64_t)umax + 1;
   const uint16_t* Kp = K + ((int64_t)l * dm.G + g) * dm.T * D;
   float m[4], z[4];
 #pragma unroll
@@ -269,7 +272,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
       }
       // lane holds tokens tb + r of row 16 rt + i16
       const int64_t tb = s0 + 16 * tt + 4 * g4;
-      if (MODE == 0) {
+      if (MODE == RR_HOP_STATS) {
 #pragma unroll
         for (int rt = 0; rt < 4; ++rt) {
           float x[4], lm = -INFINITY;
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
         }
       } else {
         float sv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (MODE == 2 && 16 * tt + 16 <= nt) {
+        if (MODE == RR_DIRECT && 16 * tt + 16 <= nt) {
           // direct pass, no token past the chunk: every row sees every token
           // (weight 1) and the masked rows add 0
 #pragma unroll
@@ -308,12 +311,12 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
         if (i16 < 4) red[w][16 * tt + 4 * g4 + i16] = i16 == 0 ? sv[0] : i16 == 1 ? sv[1] : i16 == 2 ? sv[2] : sv[3];
       }
     }
-    if (MODE != 0) {
+    if (MODE != RR_HOP_STATS) {
       __syncthreads();
       if (tid < nt) {
         float s = 0.f;
         for (int w2 = 0; w2 < nw; ++w2) s += red[w2][tid];
-        if (MODE == 1) {
+        if (MODE == RR_HOP_SUMS) {
           mh.dpart[(int64_t)grp * dm.N_c + s0 + tid] = s;
         } else {
           const int lg = l * dm.G + g;
@@ -322,7 +325,7 @@ __global__ __launch_bounds__(512) void k_mh_mfma(Dims dm, const uint16_t* __rest
       }
     }
   }
-  if (MODE == 0) {
+  if (MODE == RR_HOP_STATS) {
     // merge the four lanes of each row (lanes i16 + 16 k)
 #pragma unroll
     for (int rt = 0; rt < 4; ++rt) {
@@ -494,10 +497,10 @@ static hipError_t mh_bf16(const Dims& dm, const uint16_t* K, const uint16_t* Q, 
   hipLaunchKernelGGL(k_mh_seed_score, dim3(tb), dim3(256), 0, st, dm, tv, mh);
   for (int hop = 0; hop < MH_HOPS; ++hop) {
     mh_seeds(dm, mh, st);
-    hipLaunchKernelGGL((k_mh_mfma<D, 0>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
+    hipLaunchKernelGGL((k_rel_rows<D, RR_HOP_STATS>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
     hipLaunchKernelGGL(k_mh_rowstat_combine, dim3((unsigned)((ngrp * rmax + 255) / 256)), dim3(256), 0, st, dm, mh,
                        (int)nch);
-    hipLaunchKernelGGL((k_mh_mfma<D, 1>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
+    hipLaunchKernelGGL((k_rel_rows<D, RR_HOP_SUMS>), dim3(nch, ngrp), blk, 0, st, dm, K, Qg, tv, mh);
     hipLaunchKernelGGL(k_mh_hop_reduce, dim3(tb), dim3(256), 0, st, dm, mh, hop, 1);
   }
   hipLaunchKernelGGL(k_mh_finish, dim3(1), dim3(1024), 0, st, dm, mh);
@@ -534,9 +537,9 @@ hipError_t launch_token_relevance(const Dims& dm, const void* K, const void* Q, 
   const MhView none{};
   const dim3 grid((unsigned)((dm.N_c + MH_CH - 1) / MH_CH), (unsigned)(dm.L * dm.G)), blk(64 * dm.hpg);
   if (dm.d == 128)
-    hipLaunchKernelGGL((k_mh_mfma<128, 2>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
+    hipLaunchKernelGGL((k_rel_rows<128, RR_DIRECT>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
   else if (dm.d == 64)
-    hipLaunchKernelGGL((k_mh_mfma<64, 2>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
+    hipLaunchKernelGGL((k_rel_rows<64, RR_DIRECT>), grid, blk, 0, st, dm, (const uint16_t*)K, (const uint16_t*)Q, tv, none);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
