@@ -99,10 +99,13 @@ static SegWs seg_view(void* ws, const Dims& dm) {
   return s;
 }
 
-// Lane p owns position i0 + p; wave w owns the column quads w, w + 4, ... of
-// each 64-column chunk and keeps partial dot products, summed over the waves
-// at the end.  Rows are scaled by 1 / max(||h||, eps) while staged, the norm
-// taken from the diagonal of the banded Gram (computed first).
+// Thread (p, q) owns the four positions i0 + 4p .. i0 + 4p + 3 and column quad
+// q of each 64-column chunk (p = lane % 16, q = 4 wave + lane / 16).  The window
+// sums of the first position are built tap by tap, then slid one position at a
+// time (one row in, one out per window); the partial dot products are summed
+// over the four quads of a wave by row-swap permutations and over the waves in
+// LDS.  Rows are scaled by 1 / max(||h||, eps) while staged, the norm taken
+// from the diagonal of the banded Gram (computed first).
 template <typename T>
 __global__ __launch_bounds__(256) void k_curvature(Dims dm, const T* __restrict__ hidden, SegWs ws) {
   __shared__ float inv[CROWS];
@@ -120,12 +123,16 @@ __global__ __launch_bounds__(256) void k_curvature(Dims dm, const T* __restrict_
     if (i >= 0 && i < T_) v = 1.0f / fmaxf(sqrtf(ws.gram[((int64_t)slab * T_ + i) * BAND]), dm.eps_seg);
     inv[tid] = v;
   }
-  const int rr = lane + CHALO;
-  float acc[3][3], accD = 0.f;
+  const int pg = lane & 15, cq = wave * 4 + (lane >> 4);
+  const int r0 = 4 * pg + CHALO;                    // staged row of the first position
+  float acc[4][10];                                  // per position: 3 windows x (dot, |d-|^2, |d+|^2), then |h_{i+1} - h_i|^2
 #pragma unroll
-  for (int w = 0; w < 3; ++w) acc[w][0] = acc[w][1] = acc[w][2] = 0.f;
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int v = 0; v < 10; ++v) acc[k][v] = 0.f;
   constexpr int EPL = 16 / (int)sizeof(T);          // elements per 16-byte load
   constexpr int LPR = CCOL / EPL;                   // loads per staged row
+  static_assert(CCOL / 4 == 16, "sixteen column quads per chunk");
   for (int c0 = 0; c0 < Dh; c0 += CCOL) {
     __syncthreads();
     for (int e = tid; e < CROWS * LPR; e += 256) {
@@ -153,44 +160,69 @@ __global__ __launch_bounds__(256) void k_curvature(Dims dm, const T* __restrict_
       for (int k = 0; k < EPL; k += 4) *(float4*)(hb + r * CLD + c + k) = make_float4(x[k], x[k + 1], x[k + 2], x[k + 3]);
     }
     __syncthreads();
-#pragma unroll 1
-    for (int qd = wave; qd < CCOL / 4; qd += 4) {
-      const int c = 4 * qd;
-      const float4 x4 = *(const float4*)(hb + rr * CLD + c);
-      const float xv[4] = {x4.x, x4.y, x4.z, x4.w};
-      float sm[4] = {0.f, 0.f, 0.f, 0.f}, sp[4] = {0.f, 0.f, 0.f, 0.f};
+    const float* col = hb + 4 * cq;
+    auto ld = [&](int r) { return *(const float4*)(col + r * CLD); };
+    // window sums of the first position: left [r - w + 1, r], right [r + 1, r + w]
+    float4 sm[3], sp[3];
+    {
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
       int tau = 0;
 #pragma unroll
       for (int w = 0; w < 3; ++w) {
         const int ww = w == 0 ? 4 : (w == 1 ? 8 : 16);
 #pragma unroll
         for (; tau < ww; ++tau) {
-          const float4 a = *(const float4*)(hb + (rr - tau) * CLD + c);
-          const float4 b = *(const float4*)(hb + (rr + 1 + tau) * CLD + c);
-          sm[0] += a.x; sm[1] += a.y; sm[2] += a.z; sm[3] += a.w;
-          sp[0] += b.x; sp[1] += b.y; sp[2] += b.z; sp[3] += b.w;
+          const float4 x1 = ld(r0 - tau), x2 = ld(r0 + 1 + tau);
+          a.x += x1.x; a.y += x1.y; a.z += x1.z; a.w += x1.w;
+          b.x += x2.x; b.y += x2.y; b.z += x2.z; b.w += x2.w;
         }
-        const float iw = 1.0f / (float)ww;
+        sm[w] = a;
+        sp[w] = b;
+      }
+    }
+    float4 xc = ld(r0);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const float dmn = xv[k] - sm[k] * iw;
-          const float dpl = sp[k] * iw - xv[k];
-          acc[w][0] += dmn * dpl;
-          acc[w][1] += dmn * dmn;
-          acc[w][2] += dpl * dpl;
+    for (int k = 0; k < 4; ++k) {
+      const int r = r0 + k;
+      if (k > 0) {                                   // slide every window by one position
+        const float4 xn = ld(r);
+#pragma unroll
+        for (int w = 0; w < 3; ++w) {
+          const int ww = w == 0 ? 4 : (w == 1 ? 8 : 16);
+          const float4 o = ld(r - ww), in = ld(r + ww);
+          sm[w].x += xn.x - o.x; sm[w].y += xn.y - o.y; sm[w].z += xn.z - o.z; sm[w].w += xn.w - o.w;
+          sp[w].x += in.x - xn.x; sp[w].y += in.y - xn.y; sp[w].z += in.z - xn.z; sp[w].w += in.w - xn.w;
+        }
+        xc = xn;
+      }
+      const float xv[4] = {xc.x, xc.y, xc.z, xc.w};
+#pragma unroll
+      for (int w = 0; w < 3; ++w) {
+        const float iw = w == 0 ? 0.25f : (w == 1 ? 0.125f : 0.0625f);
+        const float smv[4] = {sm[w].x, sm[w].y, sm[w].z, sm[w].w}, spv[4] = {sp[w].x, sp[w].y, sp[w].z, sp[w].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float dmn = xv[q] - smv[q] * iw;
+          const float dpl = spv[q] * iw - xv[q];
+          acc[k][3 * w] += dmn * dpl;
+          acc[k][3 * w + 1] += dmn * dmn;
+          acc[k][3 * w + 2] += dpl * dpl;
         }
       }
-      const float4 n4 = *(const float4*)(hb + (rr + 1) * CLD + c);
+      const float4 n4 = ld(r + 1);
       const float nv[4] = {n4.x, n4.y, n4.z, n4.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) { const float dd = nv[k] - xv[k]; accD += dd * dd; }
+      for (int q = 0; q < 4; ++q) { const float dd = nv[q] - xv[q]; acc[k][9] += dd * dd; }
     }
   }
+  // the four quads of the wave (lanes p + 16 j), then the waves in LDS
 #pragma unroll
-  for (int w = 0; w < 3; ++w)
+  for (int k = 0; k < 4; ++k)
 #pragma unroll
-    for (int k = 0; k < 3; ++k) red[wave][3 * w + k][lane] = acc[w][k];
-  red[wave][9][lane] = accD;
+    for (int v = 0; v < 10; ++v) {
+      const float t = col_sum4(acc[k][v]);
+      if (lane < 16) red[wave][v][4 * pg + k] = t;
+    }
   __syncthreads();
   if (wave == 0) {
     float v[10];
