@@ -105,8 +105,7 @@ typedef struct {
  * the auction on its own ops; budget it leaves unused is not used elsewhere.
  * Not with GRACEKV_FLAG_PRUNE (whose bounds belong to the shared auction). */
 #define GRACEKV_FLAG_PAIR_QUOTAS 8
-/* gracekv_build_trees skips the relevance row statistics (and, for bf16
- * caches with H / G <= 8, the token relevance pass): the caller has run
+/* gracekv_build_trees skips the relevance row statistics: the caller has run
  * gracekv_relevance_stats on the same tree buffer, completed before this call
  * starts (same stream, or joined with an event). */
 #define GRACEKV_FLAG_STATS_READY 16
@@ -261,15 +260,15 @@ gracekv_status gracekv_pack(const gracekv_config* cfg, const void* K, const void
                             int64_t* offsets, int64_t* counts, void* K_out, void* V_out,
                             int32_t* pos_out, float* logm_out, void* ws, size_t ws_bytes, void* stream);
 
-/* The direct relevance (App. A.4 eq:app_attention_probability,
- * eq:app_direct_relevance) on its own: pass 1, per (l, g) and probe row the
- * maximum and partition sum of the logits over the visible range and over C,
- * the normaliser S_{l,g} and the probe shifts m_q, Z_q(C); for bf16 caches
- * with H / G <= 8 also pass 2, s-hat of every token of C into the token values
- * (the roots then read it instead of recomputing the relevance rows); all in
- * the tree buffer (plan.tree_bytes).  It needs neither the hidden states nor
- * the slot partition, so it can run on a second stream while gracekv_segment
- * runs; gracekv_build_trees then takes GRACEKV_FLAG_STATS_READY.
+/* Pass 1 of the direct relevance (App. A.4 eq:app_attention_probability,
+ * eq:app_direct_relevance) on its own: per (l, g) and probe row the maximum
+ * and partition sum of the logits over the visible range and over C, the
+ * normaliser S_{l,g} and the probe shifts m_q, Z_q(C), written into the tree
+ * buffer (plan.tree_bytes).  It needs neither the hidden states nor the slot
+ * partition, so it can run on a second stream while gracekv_segment runs;
+ * gracekv_build_trees then takes GRACEKV_FLAG_STATS_READY.  (Pass 2, s-hat of
+ * every token, runs inside gracekv_build_trees: for bf16 caches with
+ * H / G <= 8 as a pass of its own before the roots, else inside the roots.)
  *   K [L][G][T][d], Q [L][H][W][d] (cfg->dtype), 16-byte aligned; trees as in
  *   gracekv_build_trees.  Enqueued on stream, nothing allocated. */
 gracekv_status gracekv_relevance_stats(const gracekv_config* cfg, const void* K, const void* Q, void* trees,

@@ -288,11 +288,10 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
   if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (!(c->flags & GRACEKV_FLAG_STATS_READY)) {
-    if (launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess)
-      return GRACEKV_ERR_HIP;
-    if (token_relevance_pass(dm) && launch_token_relevance(dm, K, Q, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  }
+  if (!(c->flags & GRACEKV_FLAG_STATS_READY) &&
+      launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess)
+    return GRACEKV_ERR_HIP;
+  if (token_relevance_pass(dm) && launch_token_relevance(dm, K, Q, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   auto build = [&](int mode) {
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
   };
@@ -367,10 +366,7 @@ gracekv_status gracekv_relevance_stats(const gracekv_config* c, const void* K, c
   if (!K || !Q || !trees || !aligned16(K) || !aligned16(Q) || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
   const Dims dm = make_dims(*c, p);
   const TreeView tv = make_view(trees, p);
-  if (launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), (hipStream_t)stream) != hipSuccess)
-    return GRACEKV_ERR_HIP;
-  if (token_relevance_pass(dm)) return hip_status(launch_token_relevance(dm, K, Q, tv, (hipStream_t)stream));
-  return GRACEKV_OK;
+  return hip_status(launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), (hipStream_t)stream));
 }
 
 gracekv_status gracekv_decode_ws_bytes(const gracekv_config* c, size_t* ws_bytes) {
