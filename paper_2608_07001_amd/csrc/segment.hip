@@ -357,12 +357,13 @@ __global__ void k_rz_score(Dims dm, const float* __restrict__ kappa, const float
 // 16 x 16 tiles (i-tile w, j-tile w .. w + 8) that touch the band.  A lane
 // supplies 16 consecutive dims of a chunk per operand (4 k-steps), so each
 // operand is two 16-byte LDS reads.
-constexpr int GB_I = 64;                 // rows i per workgroup
+constexpr int GB_I = 128;                // rows i per workgroup (one 16-row tile per wave)
+constexpr int GB_T = 4 * GB_I;           // threads per workgroup
 constexpr int GB_J = GB_I + BAND;        // rows j staged
 constexpr int GB_C = 64;                 // dims per chunk
 constexpr int GB_LD = GB_C + 8;          // LDS row stride (bf16)
 
-__global__ __launch_bounds__(256) void k_gram_bf16(Dims dm, const uint16_t* __restrict__ hidden, SegWs ws) {
+__global__ __launch_bounds__(GB_T) void k_gram_bf16(Dims dm, const uint16_t* __restrict__ hidden, SegWs ws) {
   __shared__ __align__(16) uint16_t sh[2][GB_J * GB_LD];
   const int slab = blockIdx.y;
   const int64_t i0 = (int64_t)blockIdx.x * GB_I;
@@ -377,8 +378,8 @@ __global__ __launch_bounds__(256) void k_gram_bf16(Dims dm, const uint16_t* __re
   constexpr int CPR = GB_C / 8;          // 16-byte chunks per staged row
   auto stage = [&](int buf, int c0, uint4* reg) {
 #pragma unroll
-    for (int k = 0; k < (GB_J * CPR) / 256; ++k) {
-      const int e = tid + 256 * k;
+    for (int k = 0; k < (GB_J * CPR) / GB_T; ++k) {
+      const int e = tid + GB_T * k;
       const int r = e / CPR, c = (e % CPR) * 8;
       const int64_t row = j0 + r;
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -388,13 +389,14 @@ __global__ __launch_bounds__(256) void k_gram_bf16(Dims dm, const uint16_t* __re
   };
   auto store = [&](int buf, const uint4* reg) {
 #pragma unroll
-    for (int k = 0; k < (GB_J * CPR) / 256; ++k) {
-      const int e = tid + 256 * k;
+    for (int k = 0; k < (GB_J * CPR) / GB_T; ++k) {
+      const int e = tid + GB_T * k;
       const int r = e / CPR, c = (e % CPR) * 8;
       *(uint4*)(sh[buf] + r * GB_LD + c) = reg[k];
     }
   };
-  uint4 reg[(GB_J * CPR) / 256];
+  static_assert((GB_J * CPR) % GB_T == 0, "whole staging rounds");
+  uint4 reg[(GB_J * CPR) / GB_T];
   stage(0, 0, reg);
   store(0, reg);
   int buf = 0;
@@ -1017,7 +1019,7 @@ hipError_t launch_segment(const Dims& dm, const void* hidden, const float* surpr
   // the Gram first: its diagonal gives the row norms of the curvature pass
   if (dm.dtype == GRACEKV_BF16) {
     const dim3 g3((unsigned)((dm.T + GB_I - 1) / GB_I), dm.n_seg);
-    hipLaunchKernelGGL(k_gram_bf16, g3, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
+    hipLaunchKernelGGL(k_gram_bf16, g3, dim3(GB_T), 0, st, dm, (const uint16_t*)hidden, ws);
     hipLaunchKernelGGL(k_curvature<uint16_t>, g1, dim3(256), 0, st, dm, (const uint16_t*)hidden, ws);
   } else {
     const dim3 g3((unsigned)((dm.T + 15) / 16), dm.n_seg);
