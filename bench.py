@@ -194,7 +194,7 @@ def cpu_baseline(case, sh, budget_s):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; the multi-GPU layout is described in DESIGN.md",
+        print(json.dumps({"error": "the compression runs on one GPU: --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
@@ -302,7 +302,7 @@ def main():
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": sh.dtype, "data": "synthetic (seeded Llama-shaped cache, see DESIGN.md)",
+        "dtype": sh.dtype, "data": "synthetic (seeded Llama-shaped cache)",
         "config": {"workload": f"{sh.name}: L={sh.L} G={sh.G} H={sh.H} d={sh.d} N_ctx={sh.N_ctx} W={sh.W} "
                                f"x={sh.x:g} ({sh.dtype})",
                    "B_total": p.B_total, "J": int(buf.n_slots.item()), "b_used": int(buf.b_used.item()),

@@ -14,7 +14,7 @@ suffix positions.  All random draws come from ``torch.Generator`` objects
 seeded per ``(seed, config, tensor, layer, kv-head)`` so that any slab can be
 regenerated on its own, on the CPU or on a GPU.
 
-Recipe (values are stated again in the design doc):
+Recipe:
   * segments: the context is cut into ``n_segments`` true segments (uniform
     cut points with a minimum gap, or lognormal lengths); the suffix is one
     more segment;
