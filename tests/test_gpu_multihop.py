@@ -167,3 +167,31 @@ def test_multi_hop_pruned_build_equals_complete_build_and_second_stream():
     assert torch.equal(tr, pruned["tok_R"])
     assert torch.equal(buf.offsets.cpu(), pruned["offsets"])
     assert torch.equal(buf.pos_out[:n].cpu(), pruned["pos_out"][:n])
+
+
+def test_multi_hop_weight_one():
+    # lambda_graph = 1: the token values are d-hat alone (zero at every seed), so
+    # some units carry no value at all; trees, selection and pack still match
+    shape = CONFIGS["tiny"]
+    case = make_case(shape, 9, with_hidden=True)
+    case["Q_graph"] = make_graph_queries(shape, 9, case["K"], case["rope_cos"], case["rope_sin"])
+    dev = H.to_dev(case)
+    g1 = H.gpu_run(dev, Q_graph=dev["Q_graph"], lambda_graph=1.0)
+    p = dataclasses.replace(O.Params(), lam_graph=1.0)
+    o = H.oracle_run(case, p=p, Qgraph=case["Q_graph"])
+    N_c = g1["plan"].N_c
+    LG = shape.L * shape.G
+    r1 = g1["tok_R"].double().view(LG, N_c).numpy()
+    for l in range(shape.L):
+        for g in range(shape.G):
+            ro = o.ctx[(l, g)].R
+            assert np.abs(r1[l * shape.G + g] - ro).max() <= RTOL_DHAT * ro.max()
+    assert g1["slots"] == o.slot_starts
+    st = H.compare_trees(o, g1, RTOL_D, ATOL_D, RTOL_R, TAU)
+    assert not st.mismatches, st.mismatches[:10]
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
+    assert g1["b_used"] == spent
+    if st.near_ties == 0:
+        ga, gs = H.gpu_selected(g1)
+        oa, os_ = H.oracle_selected(o, shape.G)
+        assert ga == oa and gs == os_
