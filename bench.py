@@ -318,8 +318,9 @@ def main():
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": stage_ms,
         "wall_s": wall,
-        "roofline": {"kernel": "gracekv_build_trees call (" + ("k_root_bf, theta passes, k_work_mark, k_refine; the "
-                                                                "relevance passes run on the second stream)" if overlap else
+        "roofline": {"kernel": "gracekv_build_trees call (" + ("k_rel_rows token relevance, k_root_bf, theta passes, "
+                                                                "k_work_mark, k_refine; the row statistics run on the "
+                                                                "second stream)" if overlap else
                                                                 "k_rowstats_bf, k_rel_rows token relevance, k_root_bf, "
                                                                 "theta passes, k_work_mark, k_refine)"), "bound": "hbm",
                      "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
