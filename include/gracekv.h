@@ -213,9 +213,13 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  * probability of the query at u (range [0, u]) on each token of C; the scores
  * at the current and earlier seeds are then zeroed and the next hop seeds from
  * them; d = d^(1) + 0.5 d^(2), d-hat = d / (sum_C d + eps), and every token
- * value becomes (1 - lambda_graph) s-hat + lambda_graph d-hat.  s-hat is
- * computed first by a relevance-only pass (bf16 caches) or a root pass without
- * the mix (fp32 caches).  Needs H / G <= 8. 
+ * value becomes (1 - lambda_graph) s-hat + lambda_graph d-hat.  Needs
+ * H / G <= 8.
+ * The direct relevance s-hat of every token: for bf16 caches with H / G <= 8
+ * a pass of its own writes it into the token values before the roots are
+ * evaluated (the root pass then reads it and mixes in d-hat); otherwise the
+ * root pass computes it (and, with lambda_graph > 0, runs once without and once
+ * with the mix).
  * With GRACEKV_FLAG_PRUNE the trees are built only as deep as the auction can
  * reach: every unit's root is evaluated; a cost-weighted radix pass over the ops
  * known so far gives theta_lb, the (B_free-1)-th largest effective key among
