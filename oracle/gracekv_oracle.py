@@ -67,6 +67,13 @@ class Params:
     r_hop: int = 2                 # propagation steps
     rho_hop: float = 0.5           # inter-hop decay, eq:app_diffused_relevance
     graph_rhos: Tuple[float, ...] = (0.50, 0.75)   # relative depths of the propagation layers
+    # budget-aware singleton floor (App. A.5 Stage I): off on the hot path (the
+    # paper's "w/o SF" setting); the paper's default cap is 0.6
+    alpha_floor: float = 0.0       # eq:app_floor_cap
+    c_floor: float = 0.5           # cross-head consensus weight, eq:app_floor_score
+    gamma_floor: float = 1.2       # quality gate, eq:app_floor_gate
+    eta_floor: float = 0.95        # cumulative original value of the candidates
+    pool_floor: int = 3            # max-pool half width (width 7)
 
 
 def f32(x) -> float:
@@ -83,7 +90,8 @@ class Budget:
     B_total: int
     r: int
     N_c: int
-    B_free: int
+    B_free: int                # auction budget (after the singleton floor when it runs)
+    B_floor: int = 0           # entries the singleton floor reserved
 
 
 def budget(L: int, G: int, N_ctx: int, x: float, p: Params = Params()) -> Budget:
@@ -505,7 +513,7 @@ class Node:
     depth: int = 0
 
 
-def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache=None):
+def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache=None, floor=None):
     """Choose the preselected refinement of node [a, b) (n >= 2).
 
     Binary candidates: the top-16 curvature positions t in [a, b-2] (ties to
@@ -515,7 +523,10 @@ def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache
     p = argmax_t mean_q e_{q,t}/Z_q(C) (reading A12); children are the
     non-empty parts of [a,p), {p}, [p+1,b); rho_ext = G_ext / (#children - 1).
     The binary form wins ties, and n = 2 is always binary (reading A13).
-    Scores are compared in fp32."""
+    Scores are compared in fp32.  ``floor``: the singleton-floor candidates of
+    this (l, g); an interval of n >= 3 holding one is extracted at the
+    candidate of largest token value R (ties to the smaller t), with no choice
+    (App. A.3 split choice with the floor, reading F3)."""
     if dcache is None:
         dcache = {}
 
@@ -530,6 +541,12 @@ def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache
         kids = [(a, a + 1), (a + 1, b)]
         score = Dv - D(a, a + 1) - D(a + 1, b)
         return "bin", a + 1, kids, [("bin", a + 1, kids, f32(score))]
+    inside = [t for t in range(a, b) if floor and t in floor]
+    if inside:
+        pp = max(inside, key=lambda t: (np.float32(c.R[t]), -t))
+        kids = [iv for iv in [(a, pp), (pp, pp + 1), (pp + 1, b)] if iv[1] > iv[0]]
+        g_ext = f32(f32(Dv - sum(D(x, y) for (x, y) in kids)) / (len(kids) - 1))
+        return "ext", pp, kids, [("ext", pp, kids, g_ext)]
     kap = c.kappa[a:b]
     kmin, kmax = kap.min(), kap.max()
     khat = (kap - kmin) / (kmax - kmin) if kmax > kmin else np.zeros_like(kap)
@@ -554,9 +571,10 @@ def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache
     return "ext", pp, kids, cands
 
 
-def build_tree(c: LGContext, a: int, b: int, p: Params = Params()) -> List[Node]:
+def build_tree(c: LGContext, a: int, b: int, p: Params = Params(), floor=None) -> List[Node]:
     """Full prototype tree of slot [a, b), recursing to singletons (reading A14).
-    Nodes are returned in BFS order (level by level, left to right)."""
+    Nodes are returned in BFS order (level by level, left to right).  ``floor``:
+    singleton-floor candidates of this (l, g) (forced extraction, see refine)."""
     dcache: Dict[Tuple[int, int], Tuple[float, float]] = {}
 
     def dd(x, y):
@@ -570,7 +588,7 @@ def build_tree(c: LGContext, a: int, b: int, p: Params = Params()) -> List[Node]
     while head < len(nodes):
         v = nodes[head]
         if v.b - v.a >= 2:
-            kind, cut, kids, cands = refine(c, v.a, v.b, v.D, p, dcache)
+            kind, cut, kids, cands = refine(c, v.a, v.b, v.D, p, dcache, floor)
             v.kind, v.cut, v.cands = kind, cut, cands
             for (x, y) in kids:
                 Dk, Ddk = dd(x, y)
@@ -650,12 +668,29 @@ def make_ops(trees: Dict[Tuple[int, int, int], List[Node]], omega: np.ndarray, G
 # Global greedy allocation (App. A.5 "Stage II", eq:app_allocation_problem;
 # App. C.3 procedure; App. C.5 non-elastic)
 # ---------------------------------------------------------------------------
-def select_heap(ops: List[Op], B_free: int) -> List[bool]:
+def select_heap(ops: List[Op], B_free: int, pre: Optional[List[bool]] = None) -> List[bool]:
     """Literal max-priority queue: start from every Add; pop the highest key;
     execute it if its cost fits the remaining budget (then push the Splits it
     exposes), otherwise discard it for good (reading Q2); stop when the budget
-    is zero or the queue is empty (reading Q3)."""
-    executed = [False] * len(ops)
+    is zero or the queue is empty (reading Q3).  ``pre``: ops already executed
+    by the singleton floor; they are not queued again, and the queue starts
+    from the Adds and the Splits their execution exposed (App. C.3 queue
+    initialisation after the floor stage)."""
+    executed = list(pre) if pre is not None else [False] * len(ops)
+    if pre is not None:
+        start = [i for i, op in enumerate(ops) if op.kind == "add" and not executed[i]]
+        start += [k for i, op in enumerate(ops) if executed[i] for k in op.children if not executed[k]]
+        heap = [(-ops[i].key, i) for i in start]
+        heapq.heapify(heap)
+        B = B_free
+        while heap and B > 0:
+            _, i = heapq.heappop(heap)
+            if ops[i].cost <= B:
+                executed[i] = True
+                B -= ops[i].cost
+                for k in ops[i].children:
+                    heapq.heappush(heap, (-ops[k].key, k))
+        return executed
     heap = [(-op.key, i) for i, op in enumerate(ops) if op.kind == "add"]
     heapq.heapify(heap)
     B = B_free
@@ -699,6 +734,95 @@ def select_heap_pairs(ops: List[Op], quotas: List[int]) -> List[bool]:
 # ---------------------------------------------------------------------------
 # Packing (App. A.5 "Frontier updates and physical packing", eq:app_frontier_update)
 # ---------------------------------------------------------------------------
+# ---------------------------------------------------------------------------
+# Budget-aware singleton floor (App. A.5 Stage I, eq:app_floor_score,
+# eq:app_floor_gate, eq:app_floor_cap)
+# ---------------------------------------------------------------------------
+def floor_scores(Rtok: Dict[Tuple[int, int], np.ndarray], N_c: int, p: Params = Params()) -> Dict[Tuple[int, int], np.ndarray]:
+    """eq:app_floor_score: f_{l,g,t} = max over tau in C with |tau - t| <= 3 of
+    (1 - c) R_{l,g,tau} + c Rbar_tau, Rbar the mean of R over every (l, g)."""
+    Rbar = np.mean(np.stack([np.asarray(Rtok[k], dtype=F64) for k in sorted(Rtok)]), axis=0)
+    out = {}
+    for k, R in Rtok.items():
+        mix = (1.0 - p.c_floor) * np.asarray(R, dtype=F64) + p.c_floor * Rbar
+        f = np.empty(N_c)
+        for t in range(N_c):
+            f[t] = mix[max(0, t - p.pool_floor):min(N_c, t + p.pool_floor + 1)].max()
+        out[k] = f
+    return out
+
+
+def floor_candidates(f: np.ndarray, R: np.ndarray, N_c: int, p: Params = Params()) -> List[int]:
+    """Tokens of one (l, g) in descending f (ties to the smaller t) that pass the
+    gate f >= gamma / N_c (eq:app_floor_gate), taken while the cumulative
+    original value R of the taken tokens stays <= eta = 0.95 (the first token
+    that would exceed it stops the list; reading F2)."""
+    order = sorted(range(N_c), key=lambda t: (-f[t], t))
+    out, cum = [], 0.0
+    for t in order:
+        if f[t] < p.gamma_floor / N_c or cum + R[t] > p.eta_floor:
+            break
+        out.append(t)
+        cum += R[t]
+    return out
+
+
+def floor_path_ops(nodes: List[Node], t: int) -> List[int]:
+    """Node indices whose Split lies on the path from the root to the leaf {t}
+    (the root first); the Add of the unit precedes them."""
+    path, i = [], 0
+    while nodes[i].children:
+        path.append(i)
+        i = next(k for k in nodes[i].children if nodes[k].a <= t < nodes[k].b)
+    assert nodes[i].a == t and nodes[i].b == t + 1, "a floor candidate must end as a singleton leaf"
+    return path
+
+
+def floor_stage(cands: Dict[Tuple[int, int], List[int]], trees, ops: List[Op], slot_starts: List[int], N_c: int,
+                G: int, B_base: int, p: Params = Params()) -> Tuple[List[bool], int]:
+    """Realises the floor candidates (App. A.5 Stage I; readings F4-F7).  The
+    cost of a candidate is the cost of the not-yet-executed ops on its path
+    (the Add of its unit, then the Split of every ancestor of the leaf {t});
+    cap = floor(alpha B_base).  If the cost of every initial candidate of every
+    (l, g) (shared ops counted once per (l, g)) exceeds the cap, (l, g) keeps
+    its first max(1, floor(n cap / total)) candidates.  Then, (l, g) in order
+    and each list in order, a candidate is executed iff its incremental cost
+    still fits the cap.  Returns the executed flags and B_floor."""
+    cap = int(math.floor(p.alpha_floor * B_base))
+    J = len(slot_starts)
+    bounds = list(slot_starts) + [N_c]
+    op_of = {}
+    for i, op in enumerate(ops):
+        op_of[(op.unit, op.kind, op.node)] = i
+
+    def path_ops(l, g, t):
+        j = max(k for k in range(J) if bounds[k] <= t)
+        unit = (l * G + g) * J + j
+        nodes = trees[(l, g, j)]
+        return [op_of[(unit, "add", 0)]] + [op_of[(unit, "split", v)] for v in floor_path_ops(nodes, t)]
+
+    total = 0
+    for (l, g), ts in cands.items():
+        seen = set()
+        for t in ts:
+            seen.update(path_ops(l, g, t))
+        total += sum(ops[i].cost for i in seen)
+    lists = dict(cands)
+    if total > cap:
+        lists = {k: ts[:max(1, (len(ts) * cap) // total)] if ts else [] for k, ts in cands.items()}
+    executed = [False] * len(ops)
+    used = 0
+    for (l, g) in sorted(lists):
+        for t in lists[(l, g)]:
+            need = [i for i in path_ops(l, g, t) if not executed[i]]
+            c = sum(ops[i].cost for i in need)
+            if used + c <= cap:
+                for i in need:
+                    executed[i] = True
+                used += c
+    return executed, used
+
+
 def frontier(nodes: List[Node], add_exec: bool, split_exec: Dict[int, bool]) -> List[int]:
     """Frontier of one tree: empty unless Add executed; every executed Split
     replaces its node by its children."""
@@ -776,16 +900,27 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
         dhat = multi_hop({k: c.R for k, c in ctxs.items()}, Kl, Qd, G, hpg, bud.N_c, p)
         for c in ctxs.values():
             c.R = (1.0 - p.lam_graph) * c.R + p.lam_graph * dhat
+    fcands: Dict[Tuple[int, int], List[int]] = {}
+    if p.alpha_floor > 0:
+        assert lg_pairs is None and not pair_capacities, "the singleton floor needs every (l, g) and the shared auction"
+        fs = floor_scores({k: c.R for k, c in ctxs.items()}, bud.N_c, p)
+        fcands = {k: floor_candidates(fs[k], ctxs[k].R, bud.N_c, p) for k in ctxs}
     for (l, g) in pairs:
         c = ctxs[(l, g)]
+        fl = set(fcands.get((l, g), []))
         for j in range(J):
-            trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p)
+            trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p, fl if fl else None)
     if not do_select or lg_pairs is not None:
         return OracleResult(bud, seg, list(slot_starts), trees, ctxs, [], [], np.zeros(0), {})
     omega = normalize_omega(omega_raw, p)
     ops = make_ops(trees, omega, G, J)
-    ex = (select_heap_pairs(ops, pair_quotas(bud.B_free, L * G)) if pair_capacities
-          else select_heap(ops, bud.B_free))
+    if p.alpha_floor > 0:
+        pre, B_floor = floor_stage(fcands, trees, ops, list(slot_starts), bud.N_c, G, bud.B_free, p)
+        bud = dataclasses.replace(bud, B_floor=B_floor, B_free=bud.B_free - B_floor)
+        ex = select_heap(ops, bud.B_free, pre)
+    else:
+        ex = (select_heap_pairs(ops, pair_quotas(bud.B_free, L * G)) if pair_capacities
+              else select_heap(ops, bud.B_free))
     add_exec: Dict[Tuple[int, int, int], bool] = {}
     split_exec: Dict[Tuple[int, int, int], Dict[int, bool]] = {}
     for op, e in zip(ops, ex):
