@@ -12,7 +12,8 @@ interval sums are explicit sums over the interval's tokens, the budget auction
 is a literal max-priority queue.  Where the paper is silent or ambiguous the
 reading used is named in the docstring (the list of readings is in the design
 notes).  The hot-path settings are the paper's own ablation settings
-lambda_graph = 0 (no multi-hop relevance) and alpha = 0 (no singleton floor).
+lambda_graph = 0 (no multi-hop relevance) and alpha = 0 (no singleton floor);
+both features are here too (Params.lam_graph, Params.alpha_floor).
 
 Where a floating-point score decides a discrete outcome, the decision is taken
 on the score rounded to fp32 (the precision in which the GPU decides), except
@@ -20,7 +21,10 @@ for the segmentation DP, which both sides run in fp64.
 
 Parity unpinned: the absolute values of D, of the gains and of the selected set
 on general inputs have no printed value to check against; they are pinned
-through the invariants and special cases in tests/test_oracle_*.py.
+through the invariants and special cases in tests/test_oracle_*.py.  The same
+holds for the singleton floor's list reduction and realisation order (readings
+with no printed example), pinned by the cap, the budget accounting and the
+telescoping of its entries.
 """
 from __future__ import annotations
 
