@@ -45,28 +45,31 @@ constexpr float LOG2E = 1.44269504088896341f;
 static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
 
 MhView mh_view(void* base, const Dims& dm) {
-  char* p = (char*)base;
-  MhView v;
+  // offsets first (base may be null when only the size is wanted)
   const size_t N = (size_t)dm.N_c;
   const int rmax = dm.hpg * MH_SEEDS;
   const int ngrp = dm.n_gl * dm.G;
   const int nz = (rmax + 255) / 256;
   const int nch = (int)((N + MH_CH - 1) / MH_CH);
   const size_t ntop = (N + MH_TOPB - 1) / MH_TOPB;
-  v.dk = (float*)p; p += al(N * 4);
-  v.dacc = (float*)p; p += al(N * 4);
-  v.dhat = (float*)p; p += al(N * 4);
-  v.seeds = (int32_t*)p; p += al(MH_SEEDS * 4);
-  v.wts = (float*)p; p += al(MH_SEEDS * 4);
-  v.ns = (int32_t*)p; p += al(16);
-  v.used = (int32_t*)p; p += al(MH_HOPS * MH_SEEDS * 4);
-  v.nused = (int32_t*)p; p += al(16);
-  v.rstat = (float2*)p; p += al((size_t)ngrp * rmax * 8);
-  v.rpart = (float2*)p; p += al((size_t)nch * ngrp * rmax * 8);
-  v.dpart = (float*)p; p += al((size_t)ngrp * nz * N * 4);
-  v.cand = (uint64_t*)p; p += al(ntop * MH_SEEDS * 8);
-  v.bsum = (double*)p; p += al(ntop * 8);
-  v.bytes = (size_t)(p - (char*)base);
+  size_t o = 0;
+  auto take = [&](size_t bytes) { const size_t at = o; o += al(bytes); return at; };
+  const size_t o_dk = take(N * 4), o_dacc = take(N * 4), o_dhat = take(N * 4);
+  const size_t o_seeds = take(MH_SEEDS * 4), o_wts = take(MH_SEEDS * 4), o_ns = take(16);
+  const size_t o_used = take(MH_HOPS * MH_SEEDS * 4), o_nused = take(16);
+  const size_t o_rstat = take((size_t)ngrp * rmax * 8), o_rpart = take((size_t)nch * ngrp * rmax * 8);
+  const size_t o_dpart = take((size_t)ngrp * nz * N * 4);
+  const size_t o_cand = take(ntop * MH_SEEDS * 8), o_bsum = take(ntop * 8);
+  MhView v{};
+  v.bytes = o;
+  if (base) {
+    char* b = (char*)base;
+    v.dk = (float*)(b + o_dk); v.dacc = (float*)(b + o_dacc); v.dhat = (float*)(b + o_dhat);
+    v.seeds = (int32_t*)(b + o_seeds); v.wts = (float*)(b + o_wts); v.ns = (int32_t*)(b + o_ns);
+    v.used = (int32_t*)(b + o_used); v.nused = (int32_t*)(b + o_nused);
+    v.rstat = (float2*)(b + o_rstat); v.rpart = (float2*)(b + o_rpart); v.dpart = (float*)(b + o_dpart);
+    v.cand = (uint64_t*)(b + o_cand); v.bsum = (double*)(b + o_bsum);
+  }
   return v;
 }
 
