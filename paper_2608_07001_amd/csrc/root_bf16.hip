@@ -296,11 +296,17 @@ __global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __rest
           }
         }
       }
-      // lanes l, l + CHP, ... of a wave hold the same chunk
+      // lanes l, l + CHP, ... of a wave hold the same chunk: rotations by CHP ..
+      // 8 within each 16-lane row (DPP), then the four rows by row swaps
+      static_assert(CHP == 4 || CHP == 8, "chunk classes within a 16-lane row");
 #pragma unroll
-      for (int o = CHP; o < 64; o <<= 1)
-#pragma unroll
-        for (int h = 0; h < 16; ++h) kacc[h] += __shfl_xor(kacc[h], o, 64);
+      for (int h = 0; h < 16; ++h) {
+        float v = kacc[h];
+        if constexpr (CHP == 4)
+          v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+        kacc[h] = col_sum4(v);
+      }
       // empty Split slots of the unit's node range
       for (int i = tid; i < 2 * n; i += RB_T) {
         const int64_t sl = (int64_t)lg * 2 * dm.N_c + 2 * a0 + i;
