@@ -711,14 +711,8 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
           const float am = U.A[t];
           if (am > best || (am == best && t < bi)) { best = am; bi = t; }
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          kmn = fminf(kmn, __shfl_xor(kmn, o, 64));
-          kmx = fmaxf(kmx, __shfl_xor(kmx, o, 64));
-          const float b2 = __shfl_xor(best, o, 64);
-          const int i2 = __shfl_xor(bi, o, 64);
-          if (b2 > best || (b2 == best && i2 < bi)) { best = b2; bi = i2; }
-        }
+        wave_minmax(kmn, kmx);
+        wave_argmax(best, bi);
         if (lane == 0) {
           meta[3] = bi;
           meta[4] = __float_as_int(kmn);
@@ -800,12 +794,7 @@ __global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __res
           best = ((Dv - cD[posL[lane]]) - cD[CM + posR[lane]]) + dm.lam_kappa * kh;
           bk = lane;
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const float b2 = __shfl_xor(best, o, 64);
-          const int k2 = __shfl_xor(bk, o, 64);
-          if (b2 > best || (b2 == best && k2 < bk)) { best = b2; bk = k2; }
-        }
+        wave_argmax(best, bk);
         if (lane == 0) {
           const int iL = meta[6], iR = meta[7];
           float dsum = 0.f;

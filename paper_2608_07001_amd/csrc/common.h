@@ -204,6 +204,61 @@ __device__ __forceinline__ float col_sum4(float v) {
   return __uint_as_float(q[0]) + __uint_as_float(q[1]);
 }
 
+// Wave all-reduces without LDS traffic: rotations by 8, 4, 2, 1 inside each
+// 16-lane row (DPP), then the row swaps of col_sum4; every lane gets the result.
+__device__ __forceinline__ float dpp_ror_f(float v, int ctrl_sel) {
+  switch (ctrl_sel) {
+    case 8: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+    case 4: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
+    case 2: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x122, 0xf, 0xf, false));
+    default: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x121, 0xf, 0xf, false));
+  }
+}
+__device__ __forceinline__ int dpp_ror_i(int v, int ctrl_sel) {
+  switch (ctrl_sel) {
+    case 8: return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xf, 0xf, false);
+    case 4: return __builtin_amdgcn_update_dpp(0, v, 0x124, 0xf, 0xf, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, v, 0x122, 0xf, 0xf, false);
+    default: return __builtin_amdgcn_update_dpp(0, v, 0x121, 0xf, 0xf, false);
+  }
+}
+// (value, index) with the larger value, ties to the smaller index, over the wave
+__device__ __forceinline__ void wave_argmax(float& v, int& i) {
+#pragma unroll
+  for (int sh = 8; sh > 0; sh >>= 1) {
+    const float v2 = dpp_ror_f(v, sh);
+    const int i2 = dpp_ror_i(i, sh);
+    if (v2 > v || (v2 == v && i2 < i)) { v = v2; i = i2; }
+  }
+  const auto pv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const auto pi = __builtin_amdgcn_permlane16_swap((uint32_t)i, (uint32_t)i, false, false);
+  float a = __uint_as_float(pv[0]), b = __uint_as_float(pv[1]);
+  int ia = (int)pi[0], ib = (int)pi[1];
+  if (b > a || (b == a && ib < ia)) { a = b; ia = ib; }
+  const auto qv = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(a), false, false);
+  const auto qi = __builtin_amdgcn_permlane32_swap((uint32_t)ia, (uint32_t)ia, false, false);
+  v = __uint_as_float(qv[0]); i = (int)qi[0];
+  const float c = __uint_as_float(qv[1]);
+  const int ic = (int)qi[1];
+  if (c > v || (c == v && ic < i)) { v = c; i = ic; }
+}
+// minimum and maximum over the wave
+__device__ __forceinline__ void wave_minmax(float& mn, float& mx) {
+#pragma unroll
+  for (int sh = 8; sh > 0; sh >>= 1) {
+    mn = fminf(mn, dpp_ror_f(mn, sh));
+    mx = fmaxf(mx, dpp_ror_f(mx, sh));
+  }
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(mn), __float_as_uint(mn), false, false);
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+  mn = fminf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  mx = fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+  const auto p2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(mn), __float_as_uint(mn), false, false);
+  const auto q2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+  mn = fminf(__uint_as_float(p2[0]), __uint_as_float(p2[1]));
+  mx = fmaxf(__uint_as_float(q2[0]), __uint_as_float(q2[1]));
+}
+
 // Sum over the wave, returned to every lane: 16-lane row sums by DPP, then the
 // four row results read as scalars.
 __device__ __forceinline__ float wave_sum_dpp(float v) {
