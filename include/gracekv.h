@@ -31,9 +31,11 @@
  *     all of cfg->dtype.  Query head h belongs to KV head h / (H/G).
  *   - Errors: argument errors are detected on the host before anything is
  *     enqueued and return GRACEKV_ERR_INVALID_ARG / _UNSUPPORTED / _BUDGET /
- *     _WORKSPACE.  A failed launch returns GRACEKV_ERR_HIP.  Numeric faults
- *     found on the device (NaN gains, capacity overflow) are latched in the
- *     status word inside the tree buffer and returned by gracekv_check.
+ *     _WORKSPACE.  A failed launch returns GRACEKV_ERR_HIP.  Faults found on
+ *     the device (a non-finite gain, a malformed slot partition, a packed
+ *     cache over capacity) are latched in the status word inside the tree
+ *     buffer and returned by gracekv_check.  gracekv_build_trees clears the
+ *     word and marks the buffer as built before any kernel can latch a fault.
  */
 #ifndef GRACEKV_H
 #define GRACEKV_H
@@ -52,7 +54,10 @@ typedef enum {
   GRACEKV_ERR_BUDGET = -3,
   GRACEKV_ERR_WORKSPACE = -4,
   GRACEKV_ERR_HIP = -5,
-  GRACEKV_ERR_NUMERIC = -6
+  GRACEKV_ERR_NUMERIC = -6,    /* a non-finite gain or utility (device) */
+  GRACEKV_ERR_STATE = -7,      /* the tree buffer holds no build (gracekv_check) */
+  GRACEKV_ERR_PARTITION = -8,  /* slot partition malformed: J outside [1, J_cap] (device) */
+  GRACEKV_ERR_CAPACITY = -9    /* the packed cache would exceed B_total entries (device) */
 } gracekv_status;
 
 typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
@@ -60,7 +65,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 8
+#define GRACEKV_ABI_VERSION 9
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -149,8 +154,16 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* cfg, gracekv_plan* plan)
 /* Human-readable name of a status. */
 const char* gracekv_status_string(gracekv_status s);
 
-/* Synchronises `stream` and returns the device status word latched in the
- * tree buffer (GRACEKV_OK, GRACEKV_ERR_NUMERIC). */
+/* Synchronises `stream` and reads the status word of the tree buffer.
+ * Returns GRACEKV_ERR_STATE when no gracekv_build_trees call has been enqueued
+ * on the buffer (a buffer is recognised as built by a marker that call writes
+ * first; a caller that allocates the buffer should zero its first use, which
+ * the Python binding does), else the first latched fault in this order:
+ * GRACEKV_ERR_NUMERIC (a non-finite gain or utility in gracekv_score),
+ * GRACEKV_ERR_PARTITION (gracekv_build_trees found J outside [1, J_cap]),
+ * GRACEKV_ERR_CAPACITY (gracekv_pack found more frontier entries than
+ * B_total), else GRACEKV_OK.  The word covers the calls since the last
+ * gracekv_build_trees on the buffer. */
 gracekv_status gracekv_check(const gracekv_config* cfg, void* trees, void* stream);
 
 /* Curvature-guided slot segmentation (App. B.2 eq:app_hidden_normalization ..
@@ -311,9 +324,10 @@ gracekv_status gracekv_decode_attention(const gracekv_config* cfg, const void* q
  * a 16x16 product from fixed inputs with the fp32 16x16x4 (which = 0), the
  * bf16 16x16x16 (which = 1) or the bf16 16x16x32 (which = 2) matrix
  * instruction, or (which = 3) the sum of lane + 1 over the four lanes
- * l % 16 + 16 k of a wave (host_out[0..63], the rest 0), and copies it to
- * host_out[256] (synchronous). */
-gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out);
+ * l % 16 + 16 k of a wave (out[0..63], the rest 0), into the caller's device
+ * buffer out[256] (fp32, row-major 16x16).  Enqueued on stream; nothing is
+ * allocated or synchronised. */
+gracekv_status gracekv_selftest_mfma(int32_t which, float* out, void* stream);
 
 #ifdef __cplusplus
 }

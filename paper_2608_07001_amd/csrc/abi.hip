@@ -85,7 +85,9 @@ TreeView make_view(void* base, const gracekv_plan& p) {
 __global__ void k_copy_slots(const int32_t* __restrict__ slot_starts, const int32_t* __restrict__ n_slots, int J_cap,
                              TreeView tv) {
   for (int i = threadIdx.x; i <= J_cap; i += blockDim.x) tv.slots[i] = slot_starts[i];
-  if (threadIdx.x == 0) { *tv.nslots = *n_slots; *tv.status = 0; }
+  // the status word is cleared and the buffer marked as built before any
+  // later kernel of the build can latch a fault into it
+  if (threadIdx.x == 0) { *tv.nslots = *n_slots; tv.status[0] = 0; tv.status[1] = STATUS_BUILT; }
 }
 
 // Copies the kernel arguments into the tree buffer, in stream order, for the
@@ -139,6 +141,9 @@ const char* gracekv_status_string(gracekv_status s) {
     case GRACEKV_ERR_WORKSPACE: return "workspace too small";
     case GRACEKV_ERR_HIP: return "HIP error";
     case GRACEKV_ERR_NUMERIC: return "non-finite gain on the device";
+    case GRACEKV_ERR_STATE: return "the tree buffer holds no build";
+    case GRACEKV_ERR_PARTITION: return "malformed slot partition on the device";
+    case GRACEKV_ERR_CAPACITY: return "packed cache over its capacity on the device";
   }
   return "unknown status";
 }
@@ -249,9 +254,13 @@ gracekv_status gracekv_check(const gracekv_config* c, void* trees, void* stream)
   if (s != GRACEKV_OK) return s;
   if (!trees) return GRACEKV_ERR_INVALID_ARG;
   if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return GRACEKV_ERR_HIP;
-  int32_t st = 0;
-  if (hipMemcpy(&st, (char*)trees + p.off_status, 4, hipMemcpyDeviceToHost) != hipSuccess) return GRACEKV_ERR_HIP;
-  return st ? GRACEKV_ERR_NUMERIC : GRACEKV_OK;
+  int32_t st[2] = {0, 0};
+  if (hipMemcpy(st, (char*)trees + p.off_status, 8, hipMemcpyDeviceToHost) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (st[1] != STATUS_BUILT) return GRACEKV_ERR_STATE;
+  if (st[0] & STATUS_NUMERIC) return GRACEKV_ERR_NUMERIC;
+  if (st[0] & STATUS_PARTITION) return GRACEKV_ERR_PARTITION;
+  if (st[0] & STATUS_CAPACITY) return GRACEKV_ERR_CAPACITY;
+  return GRACEKV_OK;
 }
 
 gracekv_status gracekv_segment(const gracekv_config* c, const void* hidden, const float* surprisal, float* kappa,
@@ -393,9 +402,9 @@ gracekv_status gracekv_decode_attention(const gracekv_config* c, const void* q, 
   return hip_status(launch_decode(dm, q, offsets, K_out, V_out, logm_out, K, V, out, ws, (hipStream_t)stream));
 }
 
-gracekv_status gracekv_selftest_mfma(int32_t which, float* host_out) {
-  if (!host_out || which < 0 || which > 3) return GRACEKV_ERR_INVALID_ARG;
-  return hip_status(selftest_mfma(which, host_out));
+gracekv_status gracekv_selftest_mfma(int32_t which, float* out, void* stream) {
+  if (!out || !aligned16(out) || which < 0 || which > 3) return GRACEKV_ERR_INVALID_ARG;
+  return hip_status(selftest_mfma(which, out, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -134,6 +134,10 @@ size_t decode_ws_bytes(const Dims& dm, int P);
 int decode_parts(const Dims& dm);
 hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out, const void* V_out,
                          const float* logm_out, const void* K, const void* V, float* out, void* ws, hipStream_t st);
+// status word of the tree buffer: [0] latched fault bits, [1] the marker
+// gracekv_build_trees writes first
+constexpr int32_t STATUS_NUMERIC = 1, STATUS_PARTITION = 2, STATUS_CAPACITY = 4;
+constexpr int32_t STATUS_BUILT = 0x4b56424c;
 constexpr size_t KARGS_BYTES = 1024;      // tail of the tree buffer: Dims at 0, TreeView at 512
 hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st);
 // bf16 caches with at most 8 query heads per KV head: the direct relevance s-hat
@@ -360,6 +364,6 @@ size_t select_ws_bytes(const Dims& dm);
 size_t pack_ws_bytes(const Dims& dm);
 int rowstats_chunks(const Dims& dm);
 int build_lds_bytes(const Dims& dm);
-hipError_t selftest_mfma(int which, float* host_out);
+hipError_t selftest_mfma(int which, float* out, hipStream_t st);
 
 }  // namespace gkv

@@ -127,7 +127,7 @@ __global__ __launch_bounds__(64) void k_pack_emit(Dims dm, const T* __restrict__
     const int i = fid[r];
     const int a = tv.node_a[base + i], n = tv.node_n[base + i];
     const int64_t o = out0 + r;
-    if (o >= dm.B_total) { if (lane == 0) atomicOr(tv.status, 4); break; }
+    if (o >= dm.B_total) { if (lane == 0) atomicOr(tv.status, STATUS_CAPACITY); break; }
     if (n == 1) {
       for (int c = lane; c < D; c += 64) {
         Ko[o * D + c] = Kp[(int64_t)a * D + c];

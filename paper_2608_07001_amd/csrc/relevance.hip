@@ -398,15 +398,9 @@ __global__ void k_selftest_mfma(int which, float* out) {
   for (int r = 0; r < 4; ++r) out[(4 * (lane >> 4) + r) * 16 + (lane & 15)] = acc[r];
 }
 
-hipError_t selftest_mfma(int which, float* host_out) {
-  float* d = nullptr;
-  hipError_t e = hipMalloc(&d, 256 * sizeof(float));
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_selftest_mfma, dim3(1), dim3(64), 0, 0, which, d);
-  e = hipGetLastError();
-  if (e == hipSuccess) e = hipMemcpy(host_out, d, 256 * sizeof(float), hipMemcpyDeviceToHost);
-  hipFree(d);
-  return e;
+hipError_t selftest_mfma(int which, float* out, hipStream_t st) {
+  hipLaunchKernelGGL(k_selftest_mfma, dim3(1), dim3(64), 0, st, which, out);
+  return hipGetLastError();
 }
 
 }  // namespace gkv

@@ -122,7 +122,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
   const int tid0 = threadIdx.x, w = tid0 >> 6, g4o = (tid0 >> 4) & 3;
   const int J = *n_slots;
   if (J < 1 || J > dm.J_cap) {                // malformed partition: nothing to build
-    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(tv.status, 2);
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(tv.status, STATUS_PARTITION);
     return;
   }
   const int64_t total = (int64_t)dm.L * dm.G * J;
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
     const int64_t a0 = slot_starts[j];
     const int n = slot_starts[j + 1] - (int)a0;
     if (n < 1 || n > NMAX || a0 < 0 || a0 + n > dm.N_c) {   // malformed partition: refuse the unit
-      if (tid == 0) { atomicOr(tv.status, 2); tv.unit_nn[unit] = 0; }
+      if (tid == 0) { atomicOr(tv.status, STATUS_PARTITION); tv.unit_nn[unit] = 0; }
       continue;
     }
     const int rows16 = (n + 15) & ~15;

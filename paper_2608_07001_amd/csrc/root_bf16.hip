@@ -124,7 +124,7 @@ __global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __rest
   const int tid0 = threadIdx.x, w = tid0 >> 6;
   const int J = *n_slots;
   if (J < 1 || J > dm.J_cap) {                // malformed partition: nothing to build
-    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(tv.status, 2);
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(tv.status, STATUS_PARTITION);
     return;
   }
   const int64_t total = (int64_t)dm.L * dm.G * J;
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __rest
     const int64_t a0 = slot_starts[j];
     const int n = slot_starts[j + 1] - (int)a0;
     if (n < 1 || n > NMAX || a0 < 0 || a0 + n > dm.N_c) {   // malformed partition: refuse the unit
-      if (tid == 0) { atomicOr(tv.status, 2); tv.unit_nn[unit] = 0; }
+      if (tid == 0) { atomicOr(tv.status, STATUS_PARTITION); tv.unit_nn[unit] = 0; }
       continue;
     }
     const int nb = (n + 31) >> 5;             // 32-token blocks

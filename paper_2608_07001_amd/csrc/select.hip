@@ -131,7 +131,7 @@ __global__ void k_score(Dims dm, TreeView tv) {
     tv.sp_U[s] = Uv;
     tv.sp_cost[s] = (uint8_t)(nch - 1);
   }
-  if (bad) atomicOr(tv.status, 1);
+  if (bad) atomicOr(tv.status, STATUS_NUMERIC);
 }
 
 hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st) {

@@ -16,9 +16,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 8          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 9          # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
-           -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device"}
+           -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device",
+           -7: "the tree buffer holds no build", -8: "malformed slot partition on the device",
+           -9: "packed cache over its capacity on the device"}
 
 
 class GraceKVError(RuntimeError):
@@ -99,7 +101,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_score": [ctypes.POINTER(Config), P, P, P],
         "gracekv_select": [ctypes.POINTER(Config), P, P, P, S, P],
         "gracekv_pack": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, P, P, P, S, P],
-        "gracekv_selftest_mfma": [ctypes.c_int32, P],
+        "gracekv_selftest_mfma": [ctypes.c_int32, P, P],
         "gracekv_decode_ws_bytes": [ctypes.POINTER(Config), ctypes.POINTER(S)],
         "gracekv_relevance_stats": [ctypes.POINTER(Config), P, P, P, P],
         "gracekv_decode_attention": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, S, P],
@@ -202,10 +204,10 @@ def decode_attention(cfg, q, offsets, K_out, V_out, logm_out, K, V, out, ws, str
         "decode_attention")
 
 
-def selftest_mfma(which: int) -> torch.Tensor:
-    out = torch.zeros(256, dtype=torch.float32)
-    _ok(lib().gracekv_selftest_mfma(which, ctypes.c_void_p(out.data_ptr())), "selftest_mfma")
-    return out.view(16, 16)
+def selftest_mfma(which: int, stream=None) -> torch.Tensor:
+    out = torch.zeros(256, dtype=torch.float32, device="cuda")
+    _ok(lib().gracekv_selftest_mfma(which, _ptr(out), _stream(stream)), "selftest_mfma")
+    return out.view(16, 16).cpu()
 
 
 # ---------------------------------------------------------------------------
@@ -226,7 +228,7 @@ def tree_arrays(plan: Plan, trees: torch.Tensor) -> Dict[str, torch.Tensor]:
         sp_exec=v(plan.off_sp_exec, NC, torch.uint8), unit_nn=v(plan.off_unit_nn, UC, torch.int32),
         unit_Ddrop=v(plan.off_unit_Ddrop, UC, torch.float32), add_U=v(plan.off_add_U, UC, torch.float32),
         add_E=v(plan.off_add_E, UC, torch.int64), add_exec=v(plan.off_add_exec, UC, torch.uint8),
-        status=v(plan.off_status, 1, torch.int32), nslots=v(plan.off_nslots, 1, torch.int32),
+        status=v(plan.off_status, 2, torch.int32), nslots=v(plan.off_nslots, 1, torch.int32),
         slots=v(plan.off_slots, plan.J_cap + 1, torch.int32),
     )
 
@@ -263,6 +265,8 @@ def allocate(cfg: Config, device="cuda") -> Buffers:
     p = plan_sizes(cfg)
     kvdt = torch.bfloat16 if cfg.dtype == BF16 else torch.float32
     u8 = dict(dtype=torch.uint8, device=device)
+    trees = torch.empty(max(p.tree_bytes, 16), **u8)
+    trees[p.off_status:p.off_status + 16].zero_()     # no build yet: check() reports it
     return Buffers(
         cfg=cfg, plan=p,
         kappa=torch.empty(p.T, dtype=torch.float32, device=device),
@@ -270,7 +274,7 @@ def allocate(cfg: Config, device="cuda") -> Buffers:
         slot_starts=torch.zeros(p.J_cap + 1, dtype=torch.int32, device=device),
         n_slots=torch.zeros(1, dtype=torch.int32, device=device),
         seg_ws=torch.empty(max(p.seg_ws_bytes, 16), **u8),
-        trees=torch.empty(max(p.tree_bytes, 16), **u8),
+        trees=trees,
         sel_ws=torch.empty(max(p.sel_ws_bytes, 16), **u8),
         pack_ws=torch.empty(max(p.pack_ws_bytes, 16), **u8),
         b_used=torch.zeros(1, dtype=torch.int64, device=device),

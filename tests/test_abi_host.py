@@ -128,3 +128,7 @@ def test_null_pointers_are_refused_before_any_launch():
     assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), None) == -1
     assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), ctypes.byref(n)) == 0 and n.value > 0
     assert lib.gracekv_status_string(-3) == b"budget cannot hold the minimum recent window"
+    # every device-latched fault has its own code and message
+    msgs = {code: lib.gracekv_status_string(code) for code in range(-9, 1)}
+    assert len(set(msgs.values())) == len(msgs) and b"unknown status" not in msgs.values()
+    assert msgs[-7] == b"the tree buffer holds no build"

@@ -364,3 +364,26 @@ def test_relevance_stats_on_a_second_stream_give_the_same_result():
                      "logm": buf.logm_out[:n].cpu(), "offsets": buf.offsets.cpu(), "b_used": buf.b_used.cpu()})
     for k in outs[0]:
         assert torch.equal(outs[0][k], outs[1][k]), k
+
+
+def test_status_word_before_a_build_and_after_a_numeric_fault():
+    # a freshly allocated tree buffer holds no build: check says so instead of
+    # reading an unwritten word; a NaN sensitivity makes every gain non-finite,
+    # which gracekv_score latches (the kernels still run to their end)
+    from paper_2608_07001_amd import gracekv as gk
+    sh = small_shape("status", L=1, G=2, H=4, d=64, N_ctx=400, W=16, x=6.0, n_segments=4)
+    cfg = H.make_cfg(sh)
+    buf = gk.allocate(cfg)
+    with pytest.raises(gk.GraceKVError) as e:
+        gk.check(cfg, buf.trees)
+    assert e.value.status == -7
+    case = make_case(sh, 2, with_hidden=True)
+    case["omega_raw"] = case["omega_raw"].clone()
+    case["omega_raw"].view(-1)[0] = float("nan")
+    with pytest.raises(gk.GraceKVError) as e:
+        H.gpu_run(H.to_dev(case))
+    assert e.value.status == -6
+    # the same buffer shape with finite sensitivities is clean again
+    case["omega_raw"].view(-1)[0] = 1.0
+    g = H.gpu_run(H.to_dev(case))
+    assert g["b_used"] >= 0
