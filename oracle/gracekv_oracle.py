@@ -575,10 +575,15 @@ def refine(c: LGContext, a: int, b: int, Dv: float, p: Params = Params(), dcache
     return "ext", pp, kids, cands
 
 
-def build_tree(c: LGContext, a: int, b: int, p: Params = Params(), floor=None) -> List[Node]:
+def build_tree(c: LGContext, a: int, b: int, p: Params = Params(), floor=None, follow=None) -> List[Node]:
     """Full prototype tree of slot [a, b), recursing to singletons (reading A14).
     Nodes are returned in BFS order (level by level, left to right).  ``floor``:
-    singleton-floor candidates of this (l, g) (forced extraction, see refine)."""
+    singleton-floor candidates of this (l, g) (forced extraction, see refine).
+    ``follow``: {(a, b): (kind, cut)} decisions to adopt at those nodes instead
+    of the best candidate (the parity protocol's follow mode: a decision the
+    compared implementation took differently within the near-tie margin is
+    adopted, so the difference does not cascade); the adopted candidate must be
+    one of the node's candidates."""
     dcache: Dict[Tuple[int, int], Tuple[float, float]] = {}
 
     def dd(x, y):
@@ -593,6 +598,11 @@ def build_tree(c: LGContext, a: int, b: int, p: Params = Params(), floor=None) -
         v = nodes[head]
         if v.b - v.a >= 2:
             kind, cut, kids, cands = refine(c, v.a, v.b, v.D, p, dcache, floor)
+            if follow and (v.a, v.b) in follow:
+                fk, fc = follow[(v.a, v.b)]
+                pick = [cd for cd in cands if cd[0] == fk and cd[1] == fc]
+                assert pick, ("adopted decision is no candidate", v.a, v.b, fk, fc)
+                kind, cut, kids = fk, fc, pick[0][2]
             v.kind, v.cut, v.cands = kind, cut, cands
             for (x, y) in kids:
                 Dk, Ddk = dd(x, y)
@@ -872,7 +882,8 @@ class OracleResult:
 def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ctx, x,
         kv_dtype="f32", p: Params = Params(), slot_starts: Optional[List[int]] = None,
         kappa: Optional[np.ndarray] = None, lg_pairs=None, do_select=True,
-        pair_capacities: bool = False, Qgraph: Optional[np.ndarray] = None) -> OracleResult:
+        pair_capacities: bool = False, Qgraph: Optional[np.ndarray] = None,
+        follow: Optional[Dict[Tuple[int, int, int], dict]] = None) -> OracleResult:
     """Segment -> build -> score -> select -> pack for one case.  Arrays are
     numpy (any float dtype; converted to fp64).  ``slot_starts``/``kappa`` may be
     given to test the later stages on their own; ``lg_pairs`` restricts the tree
@@ -880,7 +891,8 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
     runs the auction with fixed per-(l, g) capacities (select_heap_pairs).
     With p.lam_graph > 0, ``Qgraph`` [len(graph layers)][H][T][d] holds the
     queries of every position at the propagation layers and the token values
-    mix in the multi-hop relevance (eq:app_bottom_up_value)."""
+    mix in the multi-hop relevance (eq:app_bottom_up_value).  ``follow``:
+    per unit (l, g, j), tree decisions to adopt (build_tree)."""
     bud = budget(L, G, N_ctx, x, p)
     seg = None
     if slot_starts is None or kappa is None:
@@ -913,7 +925,8 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
         c = ctxs[(l, g)]
         fl = set(fcands.get((l, g), []))
         for j in range(J):
-            trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p, fl if fl else None)
+            trees[(l, g, j)] = build_tree(c, bounds[j], bounds[j + 1], p, fl if fl else None,
+                                          (follow or {}).get((l, g, j)))
     if not do_select or lg_pairs is not None:
         return OracleResult(bud, seg, list(slot_starts), trees, ctxs, [], [], np.zeros(0), {})
     omega = normalize_omega(omega_raw, p)
@@ -938,23 +951,28 @@ def run(K, V, Q, rope_cos, rope_sin, surprisal, omega_raw, hidden, L, G, H, N_ct
     packed = {}
     for (l, g) in pairs:
         c = ctxs[(l, g)]
-        ks, vs, ps, lm = [], [], [], []
+        ks, vs, ps, lm, kraw, vraw = [], [], [], [], [], []
         for j in range(J):
             nodes = trees[(l, g, j)]
             for i in frontier(nodes, add_exec[(l, g, j)], split_exec.get((l, g, j), {})):
                 pr = prototype(c, nodes[i].a, nodes[i].b, p)
+                kraw.append(pr.k)
+                vraw.append(pr.v)
                 ks.append(round_kv(pr.k, kv_dtype))
                 vs.append(round_kv(pr.v, kv_dtype))
                 ps.append(pr.pos)
                 lm.append(math.log(pr.m_eff))
         for t in range(bud.N_c, N_ctx):            # recent window, kept exactly
+            kraw.append(c.K[t])
+            vraw.append(c.V[t])
             ks.append(round_kv(c.K[t], kv_dtype))
             vs.append(round_kv(c.V[t], kv_dtype))
             ps.append(t)
             lm.append(0.0)
         counts[l * G + g] = len(ps)
+        # k_raw, v_raw: the fp64 entries before the storage rounding
         packed[(l, g)] = dict(k=np.array(ks), v=np.array(vs), pos=np.array(ps, dtype=np.int64),
-                              logm=np.array(lm))
+                              logm=np.array(lm), k_raw=np.array(kraw), v_raw=np.array(vraw))
     return OracleResult(bud, seg, list(slot_starts), trees, ctxs, ops, ex, counts, packed)
 
 

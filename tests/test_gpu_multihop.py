@@ -20,7 +20,14 @@ import gpu_harness as H
 
 pytestmark = pytest.mark.gpu
 LAM = 0.3
-RTOL_R, RTOL_D, ATOL_D, TAU = 1e-4, 2e-3, 1e-7, 2e-4
+RTOL_R = 1e-4
+
+
+def _tol(dtype):
+    # token values mix in d-hat, whose fp32 error is bounded relative to its
+    # largest value (RTOL_DHAT), so node values take 1e-4; the rest as the
+    # direct-relevance cases
+    return dataclasses.replace(H.tol_for(dtype), R=RTOL_R)
 # fp32 logits, exponentials and sums against fp64: d-hat to 1e-4 of its largest value
 RTOL_DHAT = 1e-4
 
@@ -101,21 +108,7 @@ def _trees_and_selection(shape, seed):
     n_seeds = _check_dhat(case, g0, g1, p)
     o = H.oracle_run(case, p=p, Qgraph=case["Q_graph"])
     assert g1["slots"] == o.slot_starts
-    st = H.compare_trees(o, g1, RTOL_D, ATOL_D, RTOL_R, TAU)
-    assert not st.mismatches, st.mismatches[:10]
-    ga, gs = H.gpu_selected(g1)
-    oa, os_ = H.oracle_selected(o, shape.G)
-    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
-    print(f"{shape.name} multi-hop: nodes {st.nodes} near-ties {st.near_ties} maxrelD {st.max_rel_D:.2e}; "
-          f"adds {len(oa)} splits {len(os_)} spent {spent} b_used {g1['b_used']}")
-    assert g1["b_used"] == spent
-    if st.near_ties == 0:
-        assert ga == oa and gs == os_
-        offs = g1["offsets"].numpy()
-        pos = g1["pos_out"].numpy()
-        for (l, gg), pk in o.packed.items():
-            lg = l * shape.G + gg
-            assert np.array_equal(pos[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+    H.parity(case, g1, f"{shape.name} multi-hop", _tol(shape.dtype), orc=o, p=p, Qgraph=case["Q_graph"])
     return n_seeds
 
 
@@ -187,11 +180,4 @@ def test_multi_hop_weight_one():
             ro = o.ctx[(l, g)].R
             assert np.abs(r1[l * shape.G + g] - ro).max() <= RTOL_DHAT * ro.max()
     assert g1["slots"] == o.slot_starts
-    st = H.compare_trees(o, g1, RTOL_D, ATOL_D, RTOL_R, TAU)
-    assert not st.mismatches, st.mismatches[:10]
-    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
-    assert g1["b_used"] == spent
-    if st.near_ties == 0:
-        ga, gs = H.gpu_selected(g1)
-        oa, os_ = H.oracle_selected(o, shape.G)
-        assert ga == oa and gs == os_
+    H.parity(case, g1, "tiny multi-hop, lambda_graph 1", _tol(shape.dtype), orc=o, p=p, Qgraph=case["Q_graph"])

@@ -1,14 +1,23 @@
 """Parity of the HIP path (through the C ABI) with the CPU oracle on the same
 seeded inputs.  Marked gpu: needs an MI355X.
 
-Tolerances (fp32 arithmetic on both sides of a comparison, inputs exact):
-  * token values R^tok and node values R: rtol 1e-4 (sums of <= 10^4
-    exponentials in fp32 against fp64);
-  * distortions D: |dD| <= 2e-3 |D| + 1e-7 -- D is a mean of squared relative
-    errors, so an fp32 error e in Z~ or M~ moves D_q by about 2 e sqrt(D_q);
-  * topology, partition and selection: exact except near ties, where the
-    GPU's choice scores within tau = 2e-4 (relative) of the oracle's best; those
-    are counted and their subtrees are only checked for validity.
+Tolerances (gpu_harness.tol_for; fp32 arithmetic on the GPU against fp64,
+inputs exact):
+  * token values R^tok, probe masses and node values R: rtol 1e-5 (sums of up
+    to 10^4 exponentials in fp32 against fp64; measured 9e-7);
+  * distortions D: |dD| <= rtol |D| + 1e-7 with rtol 1e-4 for fp32 caches
+    (measured 4e-5) and 1e-3 for bf16 caches (measured 8e-5): D is a mean of
+    squared relative errors, so an fp32 error e in Z~ or M~ moves D_q by about
+    2 e sqrt(D_q);
+  * utilities U = Delta+ / c: the D tolerance plus that tolerance times the
+    largest utility of the (l, g) (gains are differences of D values);
+  * topology, partition and selection: exact.  Near ties (the GPU's choice
+    within tau = 2e-4 of the oracle's best by the oracle's candidate table)
+    would be counted; every seeded case asserts there are none.  Ops within
+    the gain tolerance of the auction's cut are counted and reported;
+  * pack: positions exact; fp32 k~, v~ within 1e-5 of the row's largest entry;
+    bf16 k~, v~ correctly rounded from the fp64 prototype up to that error;
+    log m_eff within 1e-5.
 """
 import math
 
@@ -23,9 +32,8 @@ pytestmark = pytest.mark.gpu
 
 import gpu_harness as H  # noqa: E402
 
-RTOL_R = 1e-4
-RTOL_D, ATOL_D = 2e-3, 1e-7
-TAU = 2e-4
+RTOL_R = 1e-5
+TOL32, TOL16 = H.tol_for("f32"), H.tol_for("bf16")
 
 
 def _partition(N, lens=(16, 40, 64, 100, 128, 23, 77)):
@@ -87,42 +95,12 @@ def test_tiny_token_values(tiny_staged):
     assert worstA < RTOL_R
 
 
-def test_tiny_trees(tiny_staged):
+def test_tiny_trees_gains_selection_and_pack(tiny_staged):
     sh, case, g, o = tiny_staged
-    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
-    print(f"tiny trees: nodes {st.nodes} near-ties {st.near_ties} maxrelD {st.max_rel_D:.3e} "
-          f"maxabsD {st.max_abs_D:.3e} maxrelR {st.max_rel_R:.3e} maxrelDdrop {st.max_rel_Ddrop:.3e}")
-    assert not st.mismatches, st.mismatches[:10]
-    assert st.max_rel_Ddrop < RTOL_R
-
-
-def test_tiny_selection_and_pack(tiny_staged):
-    sh, case, g, o = tiny_staged
-    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
-    ga, gs = H.gpu_selected(g)
-    oa, os_ = H.oracle_selected(o, sh.G)
-    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
-    print(f"tiny select: oracle adds {len(oa)} splits {len(os_)} spent {spent}; gpu adds {len(ga)} splits {len(gs)} "
-          f"b_used {g['b_used']}; diff adds {len(ga ^ oa)} splits {len(gs ^ os_)}")
-    assert g["b_used"] == spent
-    if st.near_ties == 0:
-        assert ga == oa and gs == os_
-    # packed cache
+    o, _ = H.parity(case, g, "tiny", orc=o, slots=g["slots"], kappa=make_kappa(sh, 0))
     offs = g["offsets"].numpy()
+    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
     assert offs[-1] == o.counts.sum() == g["plan"].B_total - (g["plan"].B_free - spent)
-    K_out, V_out = g["K_out"].float().numpy(), g["V_out"].float().numpy()
-    pos, logm = g["pos_out"].numpy(), g["logm_out"].numpy()
-    worst_k = worst_v = worst_l = 0.0
-    for (l, gg), pk in o.packed.items():
-        lg = l * sh.G + gg
-        s, e = offs[lg], offs[lg + 1]
-        assert np.array_equal(pos[s:e], pk["pos"]), (l, gg)
-        scale_k = np.abs(pk["k"]).max()
-        worst_k = max(worst_k, float(np.abs(K_out[s:e] - pk["k"]).max() / scale_k))
-        worst_v = max(worst_v, float(np.abs(V_out[s:e] - pk["v"]).max() / np.abs(pk["v"]).max()))
-        worst_l = max(worst_l, float(np.abs(logm[s:e] - pk["logm"]).max()))
-    print(f"tiny pack: max rel err k {worst_k:.3e} v {worst_v:.3e} logm abs {worst_l:.3e}")
-    assert worst_k < 1e-5 and worst_v < 1e-5 and worst_l < 1e-4
 
 
 def test_tiny_full_pipeline_with_segmentation():
@@ -136,8 +114,10 @@ def test_tiny_full_pipeline_with_segmentation():
           f"J gpu {len(g['slots'])} oracle {len(o.slot_starts)}")
     print("gpu slots", g["slots"])
     print("orc slots", o.slot_starts)
-    assert kap_err < 1e-4
+    assert kap_err < 1e-5
+    assert b_err < 1e-4
     assert g["slots"] == o.slot_starts
+    H.parity(case, g, "tiny, segmented on the GPU", orc=o)
 
 
 @pytest.mark.parametrize("serial", [False, True])
@@ -162,19 +142,20 @@ def test_segmentation_across_dp_chunks(serial):
     assert int(buf.slot_starts[J].item()) == N_c
 
 
-def test_fullkv_recovery_on_gpu():
+@pytest.mark.parametrize("dtype,d,hpg", [("f32", 64, 2), ("bf16", 128, 4)], ids=["f32", "bf16"])
+def test_fullkv_recovery_on_gpu(dtype, d, hpg):
     # x = 1: the packed cache is the original context cache, entry by entry
-    sh = small_shape(L=2, G=2, H=4, d=64, N_ctx=600, W=16, x=1.0, n_segments=5)
+    sh = small_shape(f"fullkv-{dtype}", L=2, G=2, H=2 * hpg, d=d, N_ctx=600, W=16, x=1.0, n_segments=5, dtype=dtype)
     case = make_case(sh, 3, with_hidden=True)
     g = H.gpu_run(H.to_dev(case))
     offs = g["offsets"].numpy()
     for lg in range(sh.L * sh.G):
         s, e = offs[lg], offs[lg + 1]
         assert np.array_equal(g["pos_out"].numpy()[s:e], np.arange(sh.N_ctx))
-        K = case["K"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx].numpy()
-        V = case["V"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx].numpy()
-        assert np.array_equal(g["K_out"].numpy()[s:e], K)
-        assert np.array_equal(g["V_out"].numpy()[s:e], V)
+        K = case["K"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx]
+        V = case["V"].reshape(sh.L * sh.G, sh.T, sh.d)[lg, :sh.N_ctx]
+        assert torch.equal(g["K_out"][s:e], K)
+        assert torch.equal(g["V_out"][s:e], V)
         assert np.all(g["logm_out"].numpy()[s:e] == 0.0)
 
 
@@ -197,21 +178,13 @@ def test_bf16_trees_and_selection(bf16_staged):
     tokR = g["tok_R"].numpy().reshape(sh.L * sh.G, N_c)
     worstR = max(float((np.abs(tokR[l * sh.G + gg] - c.R) / np.maximum(c.R, 1e-30)).max())
                  for (l, gg), c in o.ctx.items())
-    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
-    ga, gs = H.gpu_selected(g)
-    oa, os_ = H.oracle_selected(o, sh.G)
-    print(f"bf16 R^tok maxrel {worstR:.3e}; trees nodes {st.nodes} near-ties {st.near_ties} "
-          f"maxrelD {st.max_rel_D:.3e} maxabsD {st.max_abs_D:.3e}; select diff adds {len(ga ^ oa)} "
-          f"splits {len(gs ^ os_)}")
     tokA = g["tok_A"].numpy().reshape(sh.L * sh.G, N_c)
     worstA = max(float((np.abs(tokA[l * sh.G + gg] - _probe_mass(c)) / np.maximum(_probe_mass(c), 1e-30)).max())
                  for (l, gg), c in o.ctx.items())
-    print(f"bf16 A maxrel {worstA:.3e}")
+    print(f"bf16 R^tok maxrel {worstR:.3e} A maxrel {worstA:.3e}")
     assert worstR < RTOL_R
     assert worstA < RTOL_R
-    assert not st.mismatches, st.mismatches[:10]
-    if st.near_ties == 0:
-        assert ga == oa and gs == os_
+    H.parity(case, g, "bf16 d128", orc=o, slots=g["slots"], kappa=make_kappa(sh, 7))
 
 
 def _same_cache(g1, g2):
@@ -284,22 +257,9 @@ def test_edge_shapes_trees_and_selection(name, kw):
                  for (l, gg), c in o.ctx.items())
     worstA = max(float((np.abs(tokA[l * sh.G + gg] - _probe_mass(c)) / np.maximum(_probe_mass(c), 1e-30)).max())
                  for (l, gg), c in o.ctx.items())
-    st = H.compare_trees(o, g, RTOL_D, ATOL_D, RTOL_R, TAU)
-    ga, gs = H.gpu_selected(g)
-    oa, os_ = H.oracle_selected(o, sh.G)
-    spent = sum(op.cost for op, e in zip(o.ops, o.executed) if e)
-    print(f"{name}: R^tok maxrel {worstR:.3e} A maxrel {worstA:.3e}; nodes {st.nodes} near-ties {st.near_ties} "
-          f"maxrelD {st.max_rel_D:.3e}; b_used {g['b_used']} oracle {spent}")
+    print(f"{name}: R^tok maxrel {worstR:.3e} A maxrel {worstA:.3e}")
     assert worstR < RTOL_R and worstA < RTOL_R
-    assert not st.mismatches, st.mismatches[:10]
-    assert g["b_used"] == spent
-    if st.near_ties == 0:
-        assert ga == oa and gs == os_
-    offs = g["offsets"].numpy()
-    assert offs[-1] == o.counts.sum()
-    for (l, gg), pk in o.packed.items():
-        lg = l * sh.G + gg
-        assert np.array_equal(g["pos_out"].numpy()[offs[lg]:offs[lg + 1]], pk["pos"]), (l, gg)
+    H.parity(case, g, name, orc=o, slots=slots, kappa=kappa)
 
 
 def test_budget_with_nothing_free():

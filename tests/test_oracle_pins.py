@@ -21,7 +21,6 @@ becomes a no-op) and the copy is run against the same pins."""
 import dataclasses
 import inspect
 import os
-import types
 
 import numpy as np
 import pytest
@@ -248,3 +247,29 @@ REFINE_MISTAKES = [
 @pytest.mark.parametrize("name,old,new", REFINE_MISTAKES, ids=[m[0] for m in REFINE_MISTAKES])
 def test_planted_refine_mistake_fails_the_pin(name, old, new):
     assert _refine_failures(_planted(O.refine, old, new)) != []
+
+
+def test_follow_mode_adopts_the_given_decision():
+    # the parity protocol's follow mode: a decision given for a node replaces the
+    # oracle's choice there (and only there); a decision that is no candidate of
+    # the node is refused
+    from synth.workloads import make_case, make_kappa, small_shape
+    sh = small_shape("follow", L=1, G=1, H=2, d=16, N_ctx=80, W=4, x=4.0, n_segments=2)
+    case = make_case(sh, 1, with_hidden=False)
+    f = lambda t: t.float().numpy().astype(np.float64)
+    kappa = f(make_kappa(sh, 1))
+    c = O.lg_context(f(case["K"][0, 0]), f(case["V"][0, 0]), f(case["Q"][0, 0:2]), f(case["rope_cos"]),
+                     f(case["rope_sin"]), kappa, sh.N_ctx, 40)
+    base = O.build_tree(c, 0, 40)
+    root = base[0]
+    alt = [cd for cd in root.cands if (cd[0], cd[1]) != (root.kind, root.cut)][0]
+    tree = O.build_tree(c, 0, 40, follow={(0, 40): (alt[0], alt[1])})
+    assert (tree[0].kind, tree[0].cut) == (alt[0], alt[1])
+    assert [(tree[k].a, tree[k].b) for k in tree[0].children] == alt[2]
+    # every other node is the oracle's own choice
+    for v in tree[1:]:
+        if v.children:
+            best = max(cd[3] for cd in v.cands)
+            assert [cd for cd in v.cands if (cd[0], cd[1]) == (v.kind, v.cut)][0][3] == best
+    with pytest.raises(AssertionError):
+        O.build_tree(c, 0, 40, follow={(0, 40): ("ext", -5)})
