@@ -320,6 +320,29 @@ gracekv_status gracekv_decode_attention(const gracekv_config* cfg, const void* q
                                         const void* K, const void* V, float* out, void* ws, size_t ws_bytes,
                                         void* stream);
 
+/* Size of the fixed device scratch of gracekv_decode_attention_noalloc (bytes). */
+#define GRACEKV_DECODE_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * computation as gracekv_decode_attention, with the same arguments except the
+ * workspace, whose partial softmax states go to a fixed scratch array of
+ * GRACEKV_DECODE_SCRATCH_BYTES inside the library instead.  Each GPU holds
+ * its own copy of that array from the first call on it until the process
+ * ends; the library locates it once per device (the device current at the
+ * call) and never allocates, frees or synchronises.  Every partial state a
+ * call reads is written by the same call, so nothing needs clearing.  Calls
+ * that overlap on one GPU (on different streams, or from several host
+ * threads) share the array and race: serialise them.
+ * Returns GRACEKV_ERR_WORKSPACE, before anything is enqueued, when the partial
+ * states of cfg (gracekv_decode_ws_bytes) exceed GRACEKV_DECODE_SCRATCH_BYTES
+ * (the 8B-shaped caches fit at every ratio, the 70B-shaped 32K share from
+ * about 11x), and the errors of gracekv_decode_attention
+ * otherwise. */
+gracekv_status gracekv_decode_attention_noalloc(const gracekv_config* cfg, const void* q, const int64_t* offsets,
+                                                const void* K_out, const void* V_out, const float* logm_out,
+                                                const void* K, const void* V, float* out, void* stream);
+
 /* Layout check of the cross-lane instructions used by the kernels: computes
  * a 16x16 product from fixed inputs with the fp32 16x16x4 (which = 0), the
  * bf16 16x16x16 (which = 1) or the bf16 16x16x32 (which = 2) matrix

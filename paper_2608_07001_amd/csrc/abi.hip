@@ -402,6 +402,20 @@ gracekv_status gracekv_decode_attention(const gracekv_config* c, const void* q, 
   return hip_status(launch_decode(dm, q, offsets, K_out, V_out, logm_out, K, V, out, ws, (hipStream_t)stream));
 }
 
+gracekv_status gracekv_decode_attention_noalloc(const gracekv_config* c, const void* q, const int64_t* offsets,
+                                                const void* K_out, const void* V_out, const float* logm_out,
+                                                const void* K, const void* V, float* out, void* stream) {
+  gracekv_plan p;
+  gracekv_status s = prep(c, &p);
+  if (s != GRACEKV_OK) return s;
+  if (!q || !offsets || !K_out || !V_out || !logm_out || !K || !V || !out) return GRACEKV_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(K_out) || !aligned16(V_out) || !aligned16(K) || !aligned16(V))
+    return GRACEKV_ERR_INVALID_ARG;
+  const Dims dm = make_dims(*c, p);
+  if (decode_ws_bytes(dm, decode_parts(dm)) > (size_t)GRACEKV_DECODE_SCRATCH_BYTES) return GRACEKV_ERR_WORKSPACE;
+  return hip_status(launch_decode_noalloc(dm, q, offsets, K_out, V_out, logm_out, K, V, out, (hipStream_t)stream));
+}
+
 gracekv_status gracekv_selftest_mfma(int32_t which, float* out, void* stream) {
   if (!out || !aligned16(out) || which < 0 || which > 3) return GRACEKV_ERR_INVALID_ARG;
   return hip_status(selftest_mfma(which, out, (hipStream_t)stream));

@@ -134,6 +134,11 @@ size_t decode_ws_bytes(const Dims& dm, int P);
 int decode_parts(const Dims& dm);
 hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out, const void* V_out,
                          const float* logm_out, const void* K, const void* V, float* out, void* ws, hipStream_t st);
+// the same, with the partial states in the library's fixed device scratch
+// (hipErrorInvalidValue when they exceed GRACEKV_DECODE_SCRATCH_BYTES)
+hipError_t launch_decode_noalloc(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out,
+                                 const void* V_out, const float* logm_out, const void* K, const void* V, float* out,
+                                 hipStream_t st);
 // status word of the tree buffer: [0] latched fault bits, [1] the marker
 // gracekv_build_trees writes first
 constexpr int32_t STATUS_NUMERIC = 1, STATUS_PARTITION = 2, STATUS_CAPACITY = 4;

@@ -20,6 +20,8 @@
 //     last-arriving workgroup could merge them in the same launch, but the
 //     device-scope fences that needs write back and invalidate the L2 of the
 //     XCD on this chip, which costs far more than a second launch.)
+#include <mutex>
+
 #include "common.h"
 
 namespace gkv {
@@ -259,6 +261,43 @@ __global__ __launch_bounds__(512) void k_decode_combine(Dims dm, int P, const fl
     }
     out[((int64_t)l * dm.H + (int64_t)g * dm.hpg + h) * D + dd] = S > 0.f ? O / S : 0.f;
   }
+}
+
+// Fixed device scratch of the allocation-free entry point: the partial softmax
+// states of the split over entries.  Every GPU the library runs on holds its own
+// copy at its own address until the process ends; host code never uses the
+// array's name as an address, only the pointer hipGetSymbolAddress returns
+// for the current device (scratch_on_device).
+static __device__ __align__(256) char scratch[GRACEKV_DECODE_SCRATCH_BYTES];
+
+static hipError_t scratch_on_device(void** out) {
+  constexpr int NDEV = 64;
+  static void* ptr[NDEV] = {nullptr};
+  static std::mutex mu;
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= NDEV) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    ptr[dev] = p;
+  }
+  *out = ptr[dev];
+  return hipSuccess;
+}
+
+hipError_t launch_decode_noalloc(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out,
+                                 const void* V_out, const float* logm_out, const void* K, const void* V, float* out,
+                                 hipStream_t st) {
+  if (decode_ws_bytes(dm, decode_parts(dm)) > (size_t)GRACEKV_DECODE_SCRATCH_BYTES) return hipErrorInvalidValue;
+  void* ws = nullptr;
+  const hipError_t e = scratch_on_device(&ws);
+  if (e != hipSuccess) return e;
+  return launch_decode(dm, q, offsets, K_out, V_out, logm_out, K, V, out, ws, st);
 }
 
 hipError_t launch_decode(const Dims& dm, const void* q, const int64_t* offsets, const void* K_out, const void* V_out,

@@ -69,7 +69,8 @@ class Plan(ctypes.Structure):
 
 SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
            "gracekv_segment", "gracekv_build_trees", "gracekv_score", "gracekv_select", "gracekv_pack",
-           "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention", "gracekv_relevance_stats"]
+           "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention", "gracekv_relevance_stats",
+           "gracekv_decode_attention_noalloc"]
 
 _lib = None
 
@@ -105,6 +106,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_decode_ws_bytes": [ctypes.POINTER(Config), ctypes.POINTER(S)],
         "gracekv_relevance_stats": [ctypes.POINTER(Config), P, P, P, P],
         "gracekv_decode_attention": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, S, P],
+        "gracekv_decode_attention_noalloc": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -202,6 +204,18 @@ def decode_attention(cfg, q, offsets, K_out, V_out, logm_out, K, V, out, ws, str
                                        _ptr(logm_out), _ptr(K), _ptr(V), _ptr(out), _ptr(ws),
                                        ctypes.c_size_t(ws.numel() * ws.element_size()), _stream(stream)),
         "decode_attention")
+
+
+DECODE_SCRATCH_BYTES = 64 << 20     # GRACEKV_DECODE_SCRATCH_BYTES
+
+
+def decode_attention_noalloc(cfg, q, offsets, K_out, V_out, logm_out, K, V, out, stream=None):
+    """decode_attention without a workspace: the partial states go to the
+    library's fixed device scratch (for callers that cannot allocate); calls
+    that overlap on one GPU race."""
+    _ok(lib().gracekv_decode_attention_noalloc(ctypes.byref(cfg), _ptr(q), _ptr(offsets), _ptr(K_out), _ptr(V_out),
+                                               _ptr(logm_out), _ptr(K), _ptr(V), _ptr(out), _stream(stream)),
+        "decode_attention_noalloc")
 
 
 def selftest_mfma(which: int, stream=None) -> torch.Tensor:

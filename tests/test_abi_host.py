@@ -132,3 +132,17 @@ def test_null_pointers_are_refused_before_any_launch():
     msgs = {code: lib.gracekv_status_string(code) for code in range(-9, 1)}
     assert len(set(msgs.values())) == len(msgs) and b"unknown status" not in msgs.values()
     assert msgs[-7] == b"the tree buffer holds no build"
+
+
+def test_noalloc_decode_refuses_a_configuration_beyond_its_scratch():
+    # the partial states of the 70B-shaped share without compression need more
+    # than the fixed scratch: refused on the host before anything is enqueued
+    # (the pointers are aligned placeholders, never dereferenced on this path)
+    c = _cfg(L=80, G=8, H=64, N_ctx=32768, x=1.0)
+    n = ctypes.c_size_t(0)
+    lib = gk.lib()
+    assert lib.gracekv_decode_ws_bytes(ctypes.byref(c), ctypes.byref(n)) == 0
+    assert n.value > gk.DECODE_SCRATCH_BYTES
+    fake = ctypes.c_void_p(1 << 20)
+    assert lib.gracekv_decode_attention_noalloc(ctypes.byref(c), *([fake] * 8), None) == -4
+    assert lib.gracekv_decode_attention_noalloc(ctypes.byref(c), *([None] * 8), None) == -1
