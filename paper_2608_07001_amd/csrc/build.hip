@@ -475,11 +475,16 @@ __device__ void probe_sweeps(Ref<T, D>& U, const Dims& dm, const T* __restrict__
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(BT) void k_refine(Dims dm, int mode, const T* __restrict__ K, const T* __restrict__ V,
-                                                const T* __restrict__ Q, const float* __restrict__ cosT,
-                                                const float* __restrict__ sinT, const int32_t* __restrict__ slot_starts,
+__global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int mode, const T* __restrict__ K,
+                                                const T* __restrict__ V, const T* __restrict__ Q,
+                                                const float* __restrict__ cosT, const float* __restrict__ sinT,
+                                                const int32_t* __restrict__ slot_starts,
                                                 const int32_t* __restrict__ n_slots, const float* __restrict__ kappa,
-                                                TreeView tv) {
+                                                const TreeView* __restrict__ tvp) {
+  // the argument structures are read from device memory where used (held in
+  // scalar registers they would not fit)
+  const Dims& dm = *dmp;
+  const TreeView& tv = *tvp;
   using Lay = RefLds<T, D>;
   constexpr bool BF = Lay::BF;
   constexpr int H2 = D / 2;
@@ -929,8 +934,9 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
     auto fn = k_refine<TT, DD>;                                                                            \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes); \
     if (e0 != hipSuccess) return e0;                                                                       \
-    hipLaunchKernelGGL(fn, grid, dim3(BT), lds_bytes, st, dm, mode, (const TT*)K, (const TT*)V, (const TT*)Q, \
-                       cosT, sinT, slot_starts, n_slots, kappa, tv);                                       \
+    hipLaunchKernelGGL(fn, grid, dim3(BT), lds_bytes, st, (const Dims*)tv.kargs, mode, (const TT*)K,         \
+                       (const TT*)V, (const TT*)Q, cosT, sinT, slot_starts, n_slots, kappa,                \
+                       (const TreeView*)((const char*)tv.kargs + 512));                                    \
   } while (0)
   if (dm.dtype == GRACEKV_BF16) {
     if (dm.d == 128) GKV_LAUNCH_REFINE(uint16_t, 128); else GKV_LAUNCH_REFINE(uint16_t, 64);
