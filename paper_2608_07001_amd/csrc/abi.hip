@@ -193,7 +193,8 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   gracekv_plan tmp = *p;
   Dims dm = make_dims(*c, tmp);
   p->build_lds_bytes = build_lds_bytes(dm);
-  if (p->build_lds_bytes > 160 * 1024 || root_lds_bytes(dm) > 160 * 1024) return GRACEKV_ERR_UNSUPPORTED;
+  if (p->build_lds_bytes > 160 * 1024 || root_lds_bytes(dm) > 160 * 1024 || split_root_lds_bytes(c->d) > 80 * 1024)
+    return GRACEKV_ERR_UNSUPPORTED;
   const size_t NC = (size_t)p->node_cap, UC = (size_t)p->unit_cap;
   size_t o = 0;
   auto put = [&](size_t& off, size_t bytes) { off = o; o = al256(o + bytes); };
@@ -228,7 +229,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_partial, (size_t)LG * rowstats_chunks(dm) * dm.rows * 16);
   put(p->off_theta, 16);
   put(p->off_selstate, selstate_bytes(dm));
-  put(p->off_work, UC * 4);
+  put(p->off_work, UC * 32);                // work items: 8 int32 each
   put(p->off_wctr, 16);
   put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));
   put(p->off_proto_logm, UC * 4);
@@ -318,7 +319,11 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   }
   if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (!(c->flags & GRACEKV_FLAG_PRUNE)) return hip_status(build(BUILD_FULL));
+  if (!(c->flags & GRACEKV_FLAG_PRUNE)) {
+    // bf16: the roots first, by the kernel the pruned build refines them with
+    if (c->dtype == GRACEKV_BF16 && build(BUILD_ROOT_FULL) != hipSuccess) return GRACEKV_ERR_HIP;
+    return hip_status(build(BUILD_FULL));
+  }
   // pruned: bound from the roots -> root splits -> tighter bound -> the rest.  The
   // first bound is taken at rank B_free (one below the cut's rank B_free - 1): it
   // is still a lower bound of the cut, and at least one Add keyed at or above it

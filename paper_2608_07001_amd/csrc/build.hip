@@ -514,7 +514,7 @@ __global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int
     __syncthreads();
     const int wi = sw[0];
     if (wi >= nwork) break;
-    const int64_t unit = tv.work[wi];
+    const int64_t unit = tv.work[8 * (int64_t)wi];
     const int lg = (int)(unit / dm.J_cap), j = (int)(unit % dm.J_cap);
     if (j >= J) continue;
     const int l = lg / dm.G, g = lg % dm.G;
@@ -888,13 +888,13 @@ __global__ void k_work_mark(Dims dm, int mode, TreeView tv) {
   const int64_t a0 = tv.slots[j];
   const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
   const int nn = tv.unit_nn[unit];
-  const uint64_t theta = mode == BUILD_FULL ? 0ull : tv.theta[0];
+  const uint64_t theta = (mode == BUILD_FULL || mode == BUILD_ROOT_FULL) ? 0ull : tv.theta[0];
   bool need = false;
   for (int i = 0; i < nn && !need; ++i) {
-    if (mode == BUILD_ROOT_SPLIT && i > 0) break;
+    if ((mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL) && i > 0) break;
     const int64_t s = base + i;
     if (tv.node_nch[s] != 0 || tv.node_n[s] < 2) continue;
-    if (mode == BUILD_FULL) { need = true; break; }
+    if (mode == BUILD_FULL || mode == BUILD_ROOT_FULL) { need = true; break; }
     const int par = tv.node_parent[s];
     if (par < 0) {                          // the root: its Add reaches theta and its Split may
       const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
@@ -905,8 +905,14 @@ __global__ void k_work_mark(Dims dm, int mode, TreeView tv) {
     }
   }
   if (need) {
+    // the item carries what the refinement of the root reads first, so a
+    // workgroup needs one load instead of a chain of dependent ones
     const int pos = atomicAdd(&tv.wctr[0], 1);
-    tv.work[pos] = (int32_t)unit;
+    const uint64_t Ea = tv.add_E[unit];
+    int4* it = (int4*)(tv.work + 8 * (int64_t)pos);
+    it[0] = make_int4((int32_t)unit, (int32_t)a0, tv.node_n[base], __float_as_int(tv.node_D[base]));
+    it[1] = make_int4(__float_as_int(tv.node_R[base]), __float_as_int(tv.omega[lg]), (int32_t)(uint32_t)Ea,
+                      (int32_t)(uint32_t)(Ea >> 32));
   }
 }
 
@@ -928,6 +934,8 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
   const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
   hipLaunchKernelGGL(k_work_reset, dim3(1), dim3(64), 0, st, tv);
   hipLaunchKernelGGL(k_work_mark, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, st, dm, mode, tv);
+  if (dm.dtype == GRACEKV_BF16 && (mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL))
+    return launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, 2 * device_cus(), st);
   const dim3 grid((unsigned)device_cus());
 #define GKV_LAUNCH_REFINE(TT, DD)                                                                          \
   do {                                                                                                     \

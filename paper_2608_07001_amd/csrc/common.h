@@ -66,7 +66,8 @@ struct TreeView {
   int32_t* nslots;      // [1] J
   uint64_t* theta;      // [2] pruned build: [0] lower bound of the auction cut, [1] root-split skip bound
   void* selstate;       // radix-select state of that bound
-  int32_t* work;        // [L*G*J_cap] units to refine
+  int32_t* work;        // [L*G*J_cap][8] work items: unit, slot start, slot length, and the root's
+                        // D, R (float bits), the sensitivity w (float bits), the Add key (two words)
   int32_t* wctr;        // [4] list length, next item
   void* proto;          // [unit_cap][2][d] root prototype (k~, v~) of each unit, cache dtype
   float* proto_logm;    // [unit_cap] log m_eff of the root
@@ -96,7 +97,10 @@ struct MhView {
 // Refinement modes (the roots come from the root kernel): FULL refines every
 // node; ROOT_SPLIT refines the root of units whose Add key reaches theta;
 // CONTINUE refines every unrefined node whose creating op reaches theta.
-enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3 };
+// ROOT_FULL refines the root of every unit (the first level of the complete
+// build).  For bf16 caches the roots are refined by their own kernel
+// (launch_split_root) in ROOT_SPLIT and ROOT_FULL.
+enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3, BUILD_ROOT_FULL = 4 };
 
 // ---- gains, utilities and keys (shared by the build and score kernels so that
 // both produce bit-identical keys) -------------------------------------------
@@ -369,6 +373,10 @@ size_t select_ws_bytes(const Dims& dm);
 size_t pack_ws_bytes(const Dims& dm);
 int rowstats_chunks(const Dims& dm);
 int build_lds_bytes(const Dims& dm);
+int split_root_lds_bytes(int d);
+hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void* V, const void* Q, const float* cosT,
+                             const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
+                             const TreeView& tv, int grid, hipStream_t st);
 hipError_t selftest_mfma(int which, float* out, hipStream_t st);
 
 }  // namespace gkv
