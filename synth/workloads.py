@@ -405,3 +405,70 @@ def make_graph_queries(shape: Shape, seed: int, K: torch.Tensor, cos: torch.Tens
                 lgt = (q[:: max(1, T // 512)] @ samp.t().contiguous()) / math.sqrt(d)
                 out[i, g * hpg + hh] = (q * (2.0 / lgt.std().clamp_min(1e-12))).to(out.dtype)
     return out
+
+
+def make_question(case: dict, q_index: int) -> dict:
+    """Another question over the same document, for structure reuse.
+
+    The context rows ``[0, N_ctx)`` of K, V, the hidden slabs and the
+    surprisal are the document's and are copied from ``case``; the question
+    suffix ``[N_ctx, T)`` is drawn anew: suffix keys/values around one random
+    "topic" segment, window queries aimed at fresh random target segments (the
+    recipe of the first question, with the channel scale estimated from the
+    context keys), suffix hidden states on a new great circle per slab, suffix
+    surprisal Exp(1), and new raw sensitivities.  Returns a case dict of the
+    same layout (own K/V/Q/hidden/surprisal tensors)."""
+    sh, seed = case["shape"], case["seed"]
+    dev = case["K"].device
+    N, T, W, d = sh.N_ctx, sh.T, sh.W, sh.d
+    starts = case["true_starts"]
+    n_ctx_seg = len(starts)
+    seg = _seg_index(sh, starts, dev)[:N]
+    cos, sin = case["rope_cos"], case["rope_sin"]
+    dt = case["K"].dtype
+    K, V = case["K"].clone(), case["V"].clone()
+    Q = torch.empty_like(case["Q"])
+    hpg = sh.H // sh.G
+    cnt = torch.zeros(n_ctx_seg, device=dev).index_add_(0, seg, torch.ones(N, device=dev)).clamp_min(1)[:, None]
+    for l in range(sh.L):
+        for g in range(sh.G):
+            gen = _gen(dev, seed, sh.name, "question", q_index, l, g)
+            k = K[l, g, :N].float()
+            kr = _rotate(k, cos[:N], -sin[:N])                   # context keys before rotation
+            kmean = torch.zeros(n_ctx_seg, d, device=dev).index_add_(0, seg, kr) / cnt
+            vmean = torch.zeros(n_ctx_seg, d, device=dev).index_add_(0, seg, V[l, g, :N].float()) / cnt
+            scale = (kr - kmean[seg]).std(dim=0) / 0.5          # per-channel scale of the key noise
+            topic = torch.randint(0, n_ctx_seg, (1,), generator=gen, device=dev)
+            kr_s = kmean[topic] + 0.5 * scale * torch.randn(W, d, generator=gen, device=dev)
+            K[l, g, N:] = _rotate(kr_s, cos[N:], sin[N:]).to(dt)
+            V[l, g, N:] = (vmean[topic] + 0.5 * torch.randn(W, d, generator=gen, device=dev)).to(dt)
+            tgt = torch.randint(0, max(1, n_ctx_seg), (hpg, W), generator=gen, device=dev)
+            qr = 0.5 * torch.randn(hpg, W, d, generator=gen, device=dev) * scale.mean() + 0.5 * kmean[tgt]
+            q = _rotate(qr, cos[N:T][None], sin[N:T][None])
+            samp = k[:: max(1, N // 512)]
+            lgt = (q.reshape(-1, d) @ samp.t().contiguous()) / math.sqrt(d)
+            Q[l, g * hpg:(g + 1) * hpg] = (q * (2.0 / lgt.std().clamp_min(1e-12))).to(dt)
+    out = dict(case, K=K, V=V, Q=Q)
+    gq = _gen("cpu", seed, sh.name, "question_scalars", q_index)
+    s = case["surprisal"].cpu().clone()
+    s[N:] = (-torch.log1p(-torch.rand(W, generator=gq, dtype=torch.float64))).to(torch.float32)
+    out["surprisal"] = s.to(case["surprisal"].device)
+    out["omega_raw"] = torch.exp(0.3 * torch.randn(sh.L, sh.G, generator=gq, dtype=torch.float64)) \
+        .to(torch.float32).to(case["omega_raw"].device)
+    if "hidden" in case:
+        hid = case["hidden"].clone()
+        t = torch.arange(W, dtype=torch.float32)
+        for s_ in range(sh.n_seg):
+            gh = _gen("cpu", seed, sh.name, "question_hidden", q_index, s_)
+            a = torch.randn(sh.D, generator=gh)
+            a = a / a.norm()
+            b = torch.randn(sh.D, generator=gh)
+            b = b - (b @ a) * a
+            b = b / b.norm()
+            rad = 1.0 + 2.0 * torch.rand(1, generator=gh)
+            w = sh.hidden_alpha * (0.4 + 1.2 * torch.rand(1, generator=gh))
+            h = rad * (torch.cos(w * t)[:, None] * a + torch.sin(w * t)[:, None] * b)
+            h = h + (sh.hidden_sigma / math.sqrt(sh.D)) * torch.randn(W, sh.D, generator=gh)
+            hid[s_, N:] = h.to(hid.dtype).to(hid.device)
+        out["hidden"] = hid
+    return out
