@@ -3,8 +3,10 @@ select -> pack) on one MI355X, on a synthetic Llama-3-8B-shaped cache.
 
 One step = one pass of the whole path over one cache resident in HBM.  Prints
 one JSON line (metric: compressed context tokens/s = L * G * N_ctx / step
-time), with a roofline entry for the tree-build call and the CPU oracle timed
-on a bounded sample of the same workload as a baseline.
+time), with the roofline of the dominant kernel (HIP events of the library's
+stage clock, recorded over the timed steps), the other stages' kernels beside
+it, and the CPU oracle timed on a bounded sample of the same workload on the
+host cores as a baseline.
 """
 import argparse
 import json
@@ -40,6 +42,8 @@ def parse():
     ap.add_argument("--no-multi-hop", action="store_true",
                     help="skip the second measurement with the multi-hop relevance (lambda_graph = 0.3)")
     ap.add_argument("--cpu-budget-s", type=float, default=12.0)
+    ap.add_argument("--cpu-workers", type=int, default=min(16, os.cpu_count() or 1),
+                    help="host cores (one process each) the CPU baseline runs on")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-attention measurement")
     ap.add_argument("--no-overlap", action="store_true",
                     help="relevance statistics inside gracekv_build_trees instead of on a second stream during "
@@ -65,20 +69,20 @@ def source_digest():
     return h.hexdigest()
 
 
-def recorded_traffic(workload):
-    """HBM bytes per gracekv_build_trees call from the committed counter summary
-    of this workload, if it was taken on the current kernel sources."""
+def recorded_traffic(workload, kernel):
+    """HBM bytes per launch of ``kernel`` from the committed counter summary of
+    this workload, if it was taken on the current kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.md")
     if not os.path.exists(path):
-        return None, None
+        return None
     text = open(path).read()
     try:
         blob = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
     except (IndexError, ValueError):
-        return None, None
+        return None
     if blob.get("source_digest") != source_digest():
-        return None, blob
-    return blob.get("build_trees_bytes_per_call"), blob
+        return None
+    return blob.get("bytes_per_launch", {}).get(kernel)
 
 
 def algorithmic_bytes(sh, plan, b, n_graph=0, hops=2, seeds=64):
@@ -145,6 +149,89 @@ def decode_measure(cfg, sh, case, buf, stream, reps=20, fullkv=True):
     return res
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+def kernel_names(dtype):
+    """The kernels each timed stage launches (bf16 or fp32 caches)."""
+    if dtype == "bf16":
+        return {"segment": "gracekv_segment (k_gram_bf16, k_curvature, k_dist2, DP kernels)",
+                "rowstats": "k_rowstats_bf + k_rowstats_combine", "token_relevance": "k_rel_rows",
+                "root": "k_root_bf", "root_split": "k_split_root", "refine": "k_refine", "pack": "k_pack_emit"}
+    return {"segment": "gracekv_segment (k_curvature, k_gram_f32, k_dist2, DP kernels)",
+            "rowstats": "k_rowstats + k_rowstats_combine", "token_relevance": "-", "root": "k_root",
+            "root_split": "k_refine (roots)", "refine": "k_refine", "pack": "k_pack_emit"}
+
+
+def stage_work(sh, plan, buf, b):
+    """Algorithmic bytes (and matrix-core flops where the stage is a
+    contraction) of one launch of each timed stage.  Bytes count what the stage
+    must read and write once: K/V rows of the tokens it covers (the refinement
+    stages: the tokens of the units they refine), the window queries, the
+    per-token values it reads or writes; flops count the logits (and, for the
+    roots, the three-part M^T products) at 2 per multiply-add."""
+    import torch
+    from paper_2608_07001_amd import gracekv as gk
+    LG, d, N_c, T, W = sh.L * sh.G, sh.d, plan.N_c, sh.T, sh.W
+    rows = (sh.H // sh.G) * W
+    q = sh.L * sh.H * W * d * b
+    arr = gk.tree_arrays(plan, buf.trees)
+    J = int(buf.n_slots.item())
+    starts = buf.slot_starts[:J + 1].long()
+    n = (starts[1:] - starts[:-1])                                   # [J]
+    nn = arr["unit_nn"].view(LG, plan.J_cap)[:, :J].long()            # nodes per unit
+    base = (torch.arange(LG, device=n.device)[:, None] * 2 * N_c + 2 * starts[None, :J])
+    nch_root = arr["node_nch"].long()[base]
+    tok_roots = int((n[None, :] * (nn > 1)).sum())                     # units whose root was refined
+    tok_cont = int((n[None, :] * (nn > 1 + nch_root)).sum())           # ... and a node below it
+    row = 2 * d * b                                                    # one K row and one V row
+    return {
+        "segment": dict(bytes=sh.n_seg * T * sh.D * b + T * 4, flops=None),
+        "rowstats": dict(bytes=LG * T * d * b + q, flops=2 * LG * rows * d * T),
+        "token_relevance": dict(bytes=LG * N_c * d * b + q + LG * N_c * 4, flops=2 * LG * rows * d * N_c),
+        "root": dict(bytes=LG * N_c * (row + 8) + q, flops=2 * LG * W * d * N_c * 4),
+        "root_split": dict(bytes=tok_roots * row, flops=None, tokens=tok_roots),
+        "refine": dict(bytes=tok_cont * row, flops=None, tokens=tok_cont),
+        # one K/V row (or stored root prototype) read and one entry written per packed
+        # entry; entries of a multi-token node below a root read all its rows (not counted)
+        "pack": dict(bytes=plan.B_total * (2 * row + 8), flops=None),
+    }
+
+
+def copy_bandwidth(dev, mib=4096, reps=5):
+    """GB/s (read + write) of a plain device-to-device copy of ``mib`` MiB."""
+    import torch
+    a = torch.ones(mib << 20, dtype=torch.uint8, device=dev)
+    c = torch.empty_like(a)
+    c.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2 * (mib << 20) * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, c
+    torch.cuda.empty_cache()
+    return gbs
+
+
+def kernel_table(work, clk, names):
+    out = {}
+    for st, w in work.items():
+        ms = clk.get(st)
+        if not ms:
+            continue
+        e = {"kernel": names[st], "ms": ms, "bytes": w["bytes"], "gbs": w["bytes"] / (ms * 1e-3) / 1e9}
+        e["frac_hbm"] = e["gbs"] / HBM_PEAK_GBS
+        if w.get("flops"):
+            e["tflops"] = w["flops"] / (ms * 1e-3) / 1e12
+            e["frac_mfma_bf16"] = e["tflops"] / MFMA_BF16_PEAK_TFLOPS
+        if "tokens" in w:
+            e["tokens"] = w["tokens"]
+        out[st] = e
+    return out
+
+
 def reuse_measure(cfg, sh, case, buf, stream, seg_ms, full_ms, n_questions=3):
     """Structure reuse across questions over one document: the partition and
     curvature the timed steps left in ``buf`` (one segmentation of the
@@ -183,35 +270,36 @@ def reuse_measure(cfg, sh, case, buf, stream, seg_ms, full_ms, n_questions=3):
                     "statistics run on the main stream (nothing left to overlap them with)"}
 
 
-def cpu_baseline(case, sh, budget_s):
-    """The oracle as it stands, one thread, on bounded samples of this workload.
-    Per (layer, KV head, token) it costs: segmentation of a 4096-token window
-    (shared by all L*G heads), relevance of one (l, g) over the full sequence,
-    tree build + auction of the first slots of that (l, g) until the time
-    budget is spent.  value = 1 / (sum of the per-token costs)."""
+def _np_f32(z, key):
+    """An array saved by cpu_baseline: bf16 bit patterns (uint16) or fp32."""
+    import numpy as np
+    a = z[key]
+    return (a.astype(np.uint32) << 16).view(np.float32) if a.dtype == np.uint16 else a
+
+
+def _cpu_worker(path, budget_s, x, L, G, N_ctx, s0, nwin):
+    """One host core's share of the CPU baseline (runs in its own process, one
+    thread): segmentation of the window [s0, s0 + nwin) of the context, the
+    relevance of one (l, g) over the full sequence, then the trees of the
+    window's slots until the time budget is spent and the auction over them.
+    Returns the stage times and the tokens covered."""
     import numpy as np
     from threadpoolctl import threadpool_limits
     from oracle import gracekv_oracle as O
+    z = np.load(path)
     with threadpool_limits(limits=1):
-        np32 = lambda t: t.detach().float().cpu().numpy()
-        bud = O.budget(sh.L, sh.G, sh.N_ctx, sh.x)
-        nseg = min(4096, bud.N_c)
-        hid = np32(case["hidden"][:, :nseg + 32])
+        bud = O.budget(L, G, N_ctx, x)
         t0 = time.perf_counter()
-        seg = O.segment(hid, np32(case["surprisal"][:nseg + 32]), nseg)
+        seg = O.segment(_np_f32(z, "hidden"), z["surprisal"], nwin)
         t_seg = time.perf_counter() - t0
-        l, g = 0, 0
-        hpg = sh.H // sh.G
-        K = np32(case["K"][l, g])
-        V = np32(case["V"][l, g])
-        Qg = np32(case["Q"][l, g * hpg:(g + 1) * hpg])
-        cos, sin = np32(case["rope_cos"]), np32(case["rope_sin"])
-        kappa = np.zeros(sh.T)
-        kappa[:nseg + 32] = seg.kappa
+        T = z["cos"].shape[0]
+        kappa = np.zeros(T)
+        kappa[s0:s0 + nwin] = seg.kappa[:nwin]
         t0 = time.perf_counter()
-        ctx = O.lg_context(K, V, Qg, cos, sin, kappa, sh.N_ctx, bud.N_c)
+        ctx = O.lg_context(_np_f32(z, "K"), _np_f32(z, "V"), _np_f32(z, "Q"), z["cos"], z["sin"], kappa, N_ctx,
+                           bud.N_c)
         t_rel = time.perf_counter() - t0
-        bounds = seg.slot_starts + [nseg]
+        bounds = [s0 + a for a in seg.slot_starts] + [s0 + nwin]
         trees, toks = {}, 0
         t0 = time.perf_counter()
         for j in range(len(seg.slot_starts)):
@@ -219,16 +307,64 @@ def cpu_baseline(case, sh, budget_s):
             toks += bounds[j + 1] - bounds[j]
             if time.perf_counter() - t0 > budget_s:
                 break
-        t_tree = time.perf_counter() - t0
-        t0 = time.perf_counter()
         ops = O.make_ops(trees, np.ones((1, 1)), 1, len(seg.slot_starts))
-        O.select_heap(ops, max(1, toks // int(sh.x)))
-        t_sel = time.perf_counter() - t0
-    per_tok = t_seg / (nseg * sh.L * sh.G) + t_rel / sh.N_ctx + (t_tree + t_sel) / toks
-    return dict(value=1.0 / per_tok, unit="compressed context tokens/s", cores=1, kind="oracle",
-                sample=(f"1 thread; segmentation of a {nseg}-token window ({t_seg:.1f} s, shared by L*G heads); "
-                        f"relevance of (l,g)=(0,0) over {sh.T} positions ({t_rel:.1f} s); trees + auction of "
-                        f"{toks} tokens of that head ({t_tree + t_sel:.1f} s)"))
+        O.select_heap(ops, max(1, toks // int(x)))
+        t_tree = time.perf_counter() - t0
+    return dict(t_seg=t_seg, t_rel=t_rel, t_tree=t_tree, toks=toks)
+
+
+def cpu_baseline(case, sh, budget_s, workers):
+    """The oracle as it stands on ``workers`` host cores, one process and one
+    thread each, all running at once on bounded samples of this workload:
+    worker w segments its own window of up to 4096 context tokens, takes one
+    (l, g) pair (relevance over the full sequence), then builds the trees of
+    its window's slots until the time budget is spent and runs the auction
+    over them.  A worker's rate is 1 / (its segmentation per token, shared by
+    the L*G heads + relevance per token + trees per token); value = the sum of
+    the rates."""
+    import numpy as np
+    import tempfile
+    import multiprocessing as mp
+    from concurrent.futures import ProcessPoolExecutor
+    from oracle import gracekv_oracle as O
+    import torch
+
+    def host(t):                              # bf16 as its bit patterns, fp32 as is
+        t = t.detach().cpu()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.float().numpy()
+    bud = O.budget(sh.L, sh.G, sh.N_ctx, sh.x)
+    nwin = min(4096, bud.N_c // workers)
+    cos, sin = host(case["rope_cos"]), host(case["rope_sin"])
+    hpg = sh.H // sh.G
+    tmp = tempfile.mkdtemp(prefix="gracekv_cpu_")
+    paths, jobs = [], []
+    try:
+        for w in range(workers):
+            l, g = w % sh.L, (w // sh.L) % sh.G
+            s0 = w * nwin
+            pth = os.path.join(tmp, f"w{w}.npz")
+            np.savez(pth, K=host(case["K"][l, g]), V=host(case["V"][l, g]),
+                     Q=host(case["Q"][l, g * hpg:(g + 1) * hpg]), cos=cos, sin=sin,
+                     hidden=host(case["hidden"][:, s0:s0 + nwin + 32]),
+                     surprisal=host(case["surprisal"][s0:s0 + nwin + 32]))
+            paths.append(pth)
+            jobs.append((pth, budget_s, sh.x, sh.L, sh.G, sh.N_ctx, s0, nwin))
+        t0 = time.perf_counter()
+        with ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
+            res = [f.result() for f in [ex.submit(_cpu_worker, *j) for j in jobs]]
+        wall = time.perf_counter() - t0
+    finally:
+        for pth in paths:
+            os.remove(pth)
+        os.rmdir(tmp)
+    rates = [1.0 / (r["t_seg"] / (nwin * sh.L * sh.G) + r["t_rel"] / sh.N_ctx + r["t_tree"] / r["toks"]) for r in res]
+    mean = lambda k: float(np.mean([r[k] for r in res]))
+    return dict(value=sum(rates), unit="compressed context tokens/s", cores=workers, kind="oracle",
+                sample=(f"{workers} processes x 1 thread, run at once ({wall:.1f} s wall): each segments its own "
+                        f"{nwin}-token window (mean {mean('t_seg'):.1f} s, shared by the L*G heads), takes one (l, g) "
+                        f"pair - relevance over {sh.T} positions (mean {mean('t_rel'):.1f} s) - and builds the trees "
+                        f"of its window's slots plus the auction (mean {mean('t_tree'):.1f} s, {mean('toks'):.0f} "
+                        f"tokens, budget {budget_s:g} s); value = sum of the per-worker rates"))
 
 
 def main():
@@ -263,6 +399,7 @@ def main():
     # they run on a second stream (default priority) while segmentation runs
     overlap = not args.no_overlap
     side = torch.cuda.Stream(device=dev)
+    cfg.flags |= gk.FLAG_STAGE_TIMES               # HIP events around each stage's kernels
     cfg_b = gk.Config.from_buffer_copy(cfg)
     if overlap:
         cfg_b.flags |= gk.FLAG_STATS_READY
@@ -306,6 +443,7 @@ def main():
         for _ in range(warmup):
             step()
         torch.cuda.synchronize()
+        gk.stage_times()                      # forget the warm-up's stage clock
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(steps)]
         torch.cuda.synchronize()
         w0 = time.perf_counter()
@@ -318,6 +456,8 @@ def main():
         # the build stage = waiting for the second stream + the gracekv_build_trees call
         st["build_wait"] = sum(evs[k][1].elapsed_time(evs[k][6]) for k in range(steps)) / steps
         st["build_call"] = sum(evs[k][6].elapsed_time(evs[k][2]) for k in range(steps)) / steps
+        clk = {k: (ms / n if n else None) for k, (ms, n) in gk.stage_times().items()}
+        st["kernels"] = clk
         return sum(evs[k][0].elapsed_time(evs[k][5]) for k in range(steps)) / steps, st, wall
 
     step = make_step(cfg, cfg_b, buf, q_graph)
@@ -331,7 +471,11 @@ def main():
         del a, b2
     # the committed counters were taken on the default path (pruned build, direct relevance)
     default_path = not (args.no_prune or args.ablation_pair_quotas or args.ablation_uniform_slots or q_graph is not None)
-    traffic = recorded_traffic(sh.name)[0] if default_path else None
+    work = stage_work(sh, p, buf, 2 if sh.dtype == "bf16" else 4)
+    ktab = kernel_table(work, stage_ms["kernels"], kernel_names(sh.dtype))
+    dom = max((k for k in ktab if k != "segment"), key=lambda k: ktab[k]["ms"])
+    copy_gbs = copy_bandwidth(dev)
+    traffic = recorded_traffic(sh.name, ktab[dom]["kernel"]) if default_path else None
     tokens = sh.L * sh.G * sh.N_ctx
     b = 2 if sh.dtype == "bf16" else 4
     ab = algorithmic_bytes(sh, p, b, n_graph=0 if q_graph is None else q_graph.shape[0])
@@ -358,13 +502,13 @@ def main():
         "hbm_fraction_pipeline": ab["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "stages_ms": stage_ms,
         "wall_s": wall,
-        "roofline": {"kernel": "gracekv_build_trees call (" + ("k_rel_rows token relevance, k_root_bf, theta passes, "
-                                                                "k_work_mark, k_refine; the row statistics run on the "
-                                                                "second stream)" if overlap else
-                                                                "k_rowstats_bf, k_rel_rows token relevance, k_root_bf, "
-                                                                "theta passes, k_work_mark, k_refine)"), "bound": "hbm",
-                     "achieved": build_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": build_gbs / HBM_PEAK_GBS, "traffic": traffic},
+        "roofline": {"kernel": ktab[dom]["kernel"], "bound": "hbm", "achieved": ktab[dom]["gbs"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ktab[dom]["frac_hbm"], "traffic": traffic,
+                     "ms_per_launch": ktab[dom]["ms"], "algorithmic_bytes_per_launch": ktab[dom]["bytes"],
+                     "copy_gbs": copy_gbs, "frac_of_copy": ktab[dom]["gbs"] / copy_gbs},
+        "kernels": ktab,
+        "build_call": {"ms": stage_ms["build_call"], "algorithmic_bytes": ab["build"], "gbs": build_gbs,
+                       "frac_hbm": build_gbs / HBM_PEAK_GBS},
     }
     if not args.no_reuse and default_path:
         res["structure_reuse"] = reuse_measure(cfg, sh, case, buf, stream, stage_ms["segment"], ms)
@@ -388,7 +532,7 @@ def main():
         del buf_m, qg
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline and q_graph is None:
-        res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s)
+        res["cpu_baseline"] = cpu_baseline(case, sh, args.cpu_budget_s, args.cpu_workers)
     print(json.dumps(res), flush=True)
 
 

@@ -65,7 +65,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 9
+#define GRACEKV_ABI_VERSION 10
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -114,6 +114,21 @@ typedef struct {
  * gracekv_relevance_stats on the same tree buffer, completed before this call
  * starts (same stream, or joined with an event). */
 #define GRACEKV_FLAG_STATS_READY 16
+/* Stage clock: the calls record a pair of HIP events on their stream around
+ * the main kernels of each stage (GRACEKV_STAGE_* below); gracekv_stage_times
+ * reads them.  Output unchanged. */
+#define GRACEKV_FLAG_STAGE_TIMES 32
+
+/* Stages timed with GRACEKV_FLAG_STAGE_TIMES: the kernels between the two events. */
+#define GRACEKV_STAGE_SEGMENT 0          /* every kernel of gracekv_segment */
+#define GRACEKV_STAGE_ROWSTATS 1         /* relevance row statistics (pass 1), both kernels */
+#define GRACEKV_STAGE_TOKEN_RELEVANCE 2  /* token relevance (pass 2, bf16 caches) */
+#define GRACEKV_STAGE_ROOT 3             /* root evaluation of every unit */
+#define GRACEKV_STAGE_ROOT_SPLIT 4       /* refinement of the roots (bf16: its own kernel) */
+#define GRACEKV_STAGE_REFINE 5           /* refinement below the roots (pruned build) or of every
+                                            node (complete fp32 build) */
+#define GRACEKV_STAGE_PACK 6             /* gracekv_pack's emitting kernel */
+#define GRACEKV_N_STAGES 7
 
 /* Sizes derived from a config (host only). */
 typedef struct {
@@ -165,6 +180,16 @@ const char* gracekv_status_string(gracekv_status s);
  * B_total), else GRACEKV_OK.  The word covers the calls since the last
  * gracekv_build_trees on the buffer. */
 gracekv_status gracekv_check(const gracekv_config* cfg, void* trees, void* stream);
+
+/* Stage clock (measurement, no part of the method).  Waits for every event
+ * pair the calls with GRACEKV_FLAG_STAGE_TIMES recorded since the previous
+ * gracekv_stage_times call (on any device and stream of this process), adds
+ * the elapsed times per stage and forgets the pairs.
+ *   total_ms   [GRACEKV_N_STAGES] fp32 host out: summed milliseconds per stage
+ *   launches   [GRACEKV_N_STAGES] int32 host out: event pairs per stage
+ * The events are created on first use and reused (they are not device
+ * memory).  Returns GRACEKV_ERR_HIP if an event cannot be read. */
+gracekv_status gracekv_stage_times(float* total_ms, int32_t* launches);
 
 /* Curvature-guided slot segmentation (App. B.2 eq:app_hidden_normalization ..
  * eq:app_boundary_score; App. B.3 eq:app_adjacent_difference ..

@@ -4,6 +4,9 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+#include <vector>
+
 #include "common.h"
 
 using namespace gkv;
@@ -29,6 +32,7 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.uniform_slots = (c.flags & GRACEKV_FLAG_UNIFORM_SLOTS) ? 1 : 0;
   d.pair_quotas = (c.flags & GRACEKV_FLAG_PAIR_QUOTAS) ? 1 : 0;
   d.lam_graph = c.lambda_graph;
+  d.stage_times = (c.flags & GRACEKV_FLAG_STAGE_TIMES) ? 1 : 0;
   // propagation layers at relative depths 0.50 and 0.75, rounded like the
   // segmentation layers (eq:app_seg_layers)
   d.n_gl = 0;
@@ -106,6 +110,53 @@ hipError_t launch_store_args(const Dims& dm, const TreeView& tv, hipStream_t st)
   return hipGetLastError();
 }
 
+
+// ---- stage clock ----
+// Event pairs recorded by calls with GRACEKV_FLAG_STAGE_TIMES wait in `pending`
+// until gracekv_stage_times reads them; read events go back to a per-device pool.
+namespace {
+struct ClockPair { int stage, device; hipEvent_t a, b; };
+std::mutex clock_mu;
+std::vector<ClockPair> clock_pending;
+std::vector<std::pair<int, hipEvent_t>> clock_pool;
+
+hipEvent_t clock_event(int dev) {
+  for (size_t i = 0; i < clock_pool.size(); ++i)
+    if (clock_pool[i].first == dev) {
+      hipEvent_t e = clock_pool[i].second;
+      clock_pool[i] = clock_pool.back();
+      clock_pool.pop_back();
+      return e;
+    }
+  hipEvent_t e = nullptr;
+  return hipEventCreate(&e) == hipSuccess ? e : nullptr;
+}
+}  // namespace
+
+int clock_begin(const Dims& dm, int stage, hipStream_t st) {
+  if (!dm.stage_times) return -1;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return -1;
+  std::lock_guard<std::mutex> g(clock_mu);
+  hipEvent_t a = clock_event(dev), b = clock_event(dev);
+  if (!a || !b || hipEventRecord(a, st) != hipSuccess) {
+    if (a) clock_pool.push_back({dev, a});
+    if (b) clock_pool.push_back({dev, b});
+    return -1;
+  }
+  clock_pending.push_back({stage, dev, a, b});
+  return (int)clock_pending.size() - 1;
+}
+
+void clock_end(int handle, hipStream_t st) {
+  if (handle < 0) return;
+  std::lock_guard<std::mutex> g(clock_mu);
+  if (handle < (int)clock_pending.size() && hipEventRecord(clock_pending[handle].b, st) != hipSuccess) {
+    clock_pool.push_back({clock_pending[handle].device, clock_pending[handle].b});
+    clock_pending[handle].b = nullptr;
+  }
+}
+
 }  // namespace gkv
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -160,7 +211,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (c->lambda_graph > 0.f && c->H / c->G > 8) return GRACEKV_ERR_UNSUPPORTED;   // one wave per query head
   if (c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
   if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
-                   GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY))
+                   GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY | GRACEKV_FLAG_STAGE_TIMES))
     return GRACEKV_ERR_INVALID_ARG;
   // the pruning bounds are those of the shared auction
   if ((c->flags & GRACEKV_FLAG_PAIR_QUOTAS) && (c->flags & GRACEKV_FLAG_PRUNE)) return GRACEKV_ERR_UNSUPPORTED;
@@ -274,7 +325,36 @@ gracekv_status gracekv_segment(const gracekv_config* c, const void* hidden, cons
   if (!aligned16(hidden) || !aligned16(ws)) return GRACEKV_ERR_INVALID_ARG;
   if (ws_bytes < p.seg_ws_bytes) return GRACEKV_ERR_WORKSPACE;
   Dims dm = make_dims(*c, p);
-  return hip_status(launch_segment(dm, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, (hipStream_t)stream));
+  const int clk = clock_begin(dm, GRACEKV_STAGE_SEGMENT, (hipStream_t)stream);
+  const hipError_t e = launch_segment(dm, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, (hipStream_t)stream);
+  clock_end(clk, (hipStream_t)stream);
+  return hip_status(e);
+}
+
+gracekv_status gracekv_stage_times(float* total_ms, int32_t* launches) {
+  if (!total_ms || !launches) return GRACEKV_ERR_INVALID_ARG;
+  for (int i = 0; i < GRACEKV_N_STAGES; ++i) { total_ms[i] = 0.f; launches[i] = 0; }
+  std::lock_guard<std::mutex> g(clock_mu);
+  gracekv_status s = GRACEKV_OK;
+  int cur = -1;
+  hipGetDevice(&cur);
+  for (const ClockPair& p : clock_pending) {
+    if (p.b && p.stage >= 0 && p.stage < GRACEKV_N_STAGES && s == GRACEKV_OK) {
+      float ms = 0.f;
+      hipSetDevice(p.device);
+      if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess) {
+        s = GRACEKV_ERR_HIP;
+      } else {
+        total_ms[p.stage] += ms;
+        launches[p.stage] += 1;
+      }
+    }
+    clock_pool.push_back({p.device, p.a});
+    if (p.b) clock_pool.push_back({p.device, p.b});
+  }
+  clock_pending.clear();
+  if (cur >= 0) hipSetDevice(cur);
+  return s;
 }
 
 gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const void* V, const void* Q,
@@ -298,10 +378,18 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
   if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
   if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
-  if (!(c->flags & GRACEKV_FLAG_STATS_READY) &&
-      launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st) != hipSuccess)
-    return GRACEKV_ERR_HIP;
-  if (token_relevance_pass(dm) && launch_token_relevance(dm, K, Q, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  if (!(c->flags & GRACEKV_FLAG_STATS_READY)) {
+    const int clk = clock_begin(dm, GRACEKV_STAGE_ROWSTATS, st);
+    const hipError_t e = launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), st);
+    clock_end(clk, st);
+    if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  }
+  if (token_relevance_pass(dm)) {
+    const int clk = clock_begin(dm, GRACEKV_STAGE_TOKEN_RELEVANCE, st);
+    const hipError_t e = launch_token_relevance(dm, K, Q, tv, st);
+    clock_end(clk, st);
+    if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  }
   auto build = [&](int mode) {
     return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
   };
@@ -318,7 +406,12 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     tv.dhat = mh_view(ws, dm).dhat;
     if (launch_store_args(dm, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   }
-  if (launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
+  {
+    const int clk = clock_begin(dm, GRACEKV_STAGE_ROOT, st);
+    const hipError_t e = launch_root(dm, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, tv, st);
+    clock_end(clk, st);
+    if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  }
   if (!(c->flags & GRACEKV_FLAG_PRUNE)) {
     // bf16: the roots first, by the kernel the pruned build refines them with
     if (c->dtype == GRACEKV_BF16 && build(BUILD_ROOT_FULL) != hipSuccess) return GRACEKV_ERR_HIP;
@@ -380,7 +473,10 @@ gracekv_status gracekv_relevance_stats(const gracekv_config* c, const void* K, c
   if (!K || !Q || !trees || !aligned16(K) || !aligned16(Q) || !aligned16(trees)) return GRACEKV_ERR_INVALID_ARG;
   const Dims dm = make_dims(*c, p);
   const TreeView tv = make_view(trees, p);
-  return hip_status(launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), (hipStream_t)stream));
+  const int clk = clock_begin(dm, GRACEKV_STAGE_ROWSTATS, (hipStream_t)stream);
+  const hipError_t e = launch_rowstats(dm, K, Q, tv, (float4*)((char*)trees + p.off_partial), (hipStream_t)stream);
+  clock_end(clk, (hipStream_t)stream);
+  return hip_status(e);
 }
 
 gracekv_status gracekv_decode_ws_bytes(const gracekv_config* c, size_t* ws_bytes) {

@@ -934,8 +934,14 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
   const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
   hipLaunchKernelGGL(k_work_reset, dim3(1), dim3(64), 0, st, tv);
   hipLaunchKernelGGL(k_work_mark, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, st, dm, mode, tv);
-  if (dm.dtype == GRACEKV_BF16 && (mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL))
-    return launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, 2 * device_cus(), st);
+  const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
+  const int clk = clock_begin(dm, roots ? GRACEKV_STAGE_ROOT_SPLIT : GRACEKV_STAGE_REFINE, st);
+  if (dm.dtype == GRACEKV_BF16 && roots) {
+    const hipError_t e = launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv,
+                                           2 * device_cus(), st);
+    clock_end(clk, st);
+    return e;
+  }
   const dim3 grid((unsigned)device_cus());
 #define GKV_LAUNCH_REFINE(TT, DD)                                                                          \
   do {                                                                                                     \
@@ -952,6 +958,7 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
     if (dm.d == 128) GKV_LAUNCH_REFINE(float, 128); else GKV_LAUNCH_REFINE(float, 64);
   }
 #undef GKV_LAUNCH_REFINE
+  clock_end(clk, st);
   return hipGetLastError();
 }
 

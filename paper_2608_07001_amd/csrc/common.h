@@ -32,6 +32,7 @@ struct Dims {
   int pair_quotas;               // the auction with fixed per-(l, g) capacities (ablation)
   float lam_graph;               // weight of the multi-hop relevance in the token values
   int n_gl, gl[2];               // propagation layers of the multi-hop relevance
+  int stage_times;               // record the stage clock's events (GRACEKV_FLAG_STAGE_TIMES)
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).
@@ -378,5 +379,11 @@ hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void
                              const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
                              const TreeView& tv, int grid, hipStream_t st);
 hipError_t selftest_mfma(int which, float* out, hipStream_t st);
+
+// Stage clock (GRACEKV_FLAG_STAGE_TIMES; stage ids GRACEKV_STAGE_*): clock_begin
+// records the first event of a pair on the stream and returns its handle (-1
+// when the clock is off or no event could be had); clock_end records the second.
+int clock_begin(const Dims& dm, int stage, hipStream_t st);
+void clock_end(int handle, hipStream_t st);
 
 }  // namespace gkv

@@ -228,6 +228,7 @@ hipError_t launch_pack(const Dims& dm, const void* K, const void* V, const float
   hipLaunchKernelGGL(k_pack_count, dim3((unsigned)((units + 127) / 128)), dim3(128), 0, st, dm, tv, pw);
   hipLaunchKernelGGL(k_pack_scan_units, dim3(LG), dim3(256), 0, st, dm, tv, pw, counts);
   hipLaunchKernelGGL(k_pack_scan_lg, dim3(1), dim3(64), 0, st, dm, (const int64_t*)counts, offsets);
+  const int clk = clock_begin(dm, GRACEKV_STAGE_PACK, st);
 #define GKV_EMIT(TT, DD)                                                                                     \
   hipLaunchKernelGGL((k_pack_emit<TT, DD>), dim3((unsigned)units), dim3(64), 0, st, dm, (const TT*)K,       \
                      (const TT*)V, cosT, sinT, tv, pw, (const int64_t*)offsets, (TT*)K_out, (TT*)V_out, pos_out, \
@@ -238,6 +239,7 @@ hipError_t launch_pack(const Dims& dm, const void* K, const void* V, const float
     if (dm.d == 128) GKV_EMIT(float, 128); else GKV_EMIT(float, 64);
   }
 #undef GKV_EMIT
+  clock_end(clk, st);
   if (dm.r > 0) {
     if (dm.dtype == GRACEKV_BF16)
       hipLaunchKernelGGL(k_pack_window<uint16_t>, dim3(dm.r, LG), dim3(64), 0, st, dm, (const uint16_t*)K,

@@ -8,7 +8,7 @@ from __future__ import annotations
 import ctypes
 import dataclasses
 import os
-from typing import Dict, Optional
+from typing import Dict, Optional, Tuple
 
 import torch
 
@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 9          # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 10         # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device",
            -7: "the tree buffer holds no build", -8: "malformed slot partition on the device",
@@ -47,6 +47,9 @@ FLAG_DP_SERIAL = 2
 FLAG_UNIFORM_SLOTS = 4
 FLAG_PAIR_QUOTAS = 8
 FLAG_STATS_READY = 16
+FLAG_STAGE_TIMES = 32
+# stage ids of the stage clock (GRACEKV_STAGE_*), in order
+STAGES = ["segment", "rowstats", "token_relevance", "root", "root_split", "refine", "pack"]
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",
@@ -70,7 +73,7 @@ class Plan(ctypes.Structure):
 SYMBOLS = ["gracekv_abi_version", "gracekv_default_config", "gracekv_plan_sizes", "gracekv_status_string", "gracekv_check",
            "gracekv_segment", "gracekv_build_trees", "gracekv_score", "gracekv_select", "gracekv_pack",
            "gracekv_selftest_mfma", "gracekv_decode_ws_bytes", "gracekv_decode_attention", "gracekv_relevance_stats",
-           "gracekv_decode_attention_noalloc"]
+           "gracekv_decode_attention_noalloc", "gracekv_stage_times"]
 
 _lib = None
 
@@ -107,6 +110,7 @@ def lib() -> ctypes.CDLL:
         "gracekv_relevance_stats": [ctypes.POINTER(Config), P, P, P, P],
         "gracekv_decode_attention": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P, S, P],
         "gracekv_decode_attention_noalloc": [ctypes.POINTER(Config), P, P, P, P, P, P, P, P, P],
+        "gracekv_stage_times": [P, P],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -153,6 +157,16 @@ def plan_sizes(cfg: Config) -> Plan:
 
 def check(cfg: Config, trees: torch.Tensor, stream=None):
     _ok(lib().gracekv_check(ctypes.byref(cfg), _ptr(trees), _stream(stream)), "check")
+
+
+def stage_times() -> Dict[str, Tuple[float, int]]:
+    """{stage: (summed ms, event pairs)} of the calls made with FLAG_STAGE_TIMES
+    since the previous read (waits for their events)."""
+    n = len(STAGES)
+    ms = (ctypes.c_float * n)()
+    cnt = (ctypes.c_int32 * n)()
+    _ok(lib().gracekv_stage_times(ms, cnt), "stage_times")
+    return {s: (float(ms[i]), int(cnt[i])) for i, s in enumerate(STAGES)}
 
 
 def segment(cfg, hidden, surprisal, kappa, bscore, slot_starts, n_slots, ws, stream=None):

@@ -86,7 +86,7 @@ def test_plan_rejections():
     assert e.value.status == -3
     for bad, code in [(dict(lambda_graph=1.5), -1), (dict(lambda_graph=-0.1), -1), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
                       (dict(W=65), -2), (dict(H=30), -1), (dict(x=0.5), -1), (dict(n_min=8), -2),
-                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=32), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
+                      (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=64), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
         with pytest.raises(gk.GraceKVError) as e:
             gk.plan_sizes(_cfg(**bad))
         assert e.value.status == code, bad
@@ -146,3 +146,13 @@ def test_noalloc_decode_refuses_a_configuration_beyond_its_scratch():
     fake = ctypes.c_void_p(1 << 20)
     assert lib.gracekv_decode_attention_noalloc(ctypes.byref(c), *([fake] * 8), None) == -4
     assert lib.gracekv_decode_attention_noalloc(ctypes.byref(c), *([None] * 8), None) == -1
+
+
+def test_stage_clock_reads_empty_without_calls():
+    # nothing recorded: every stage reads zero; null outputs are refused
+    t = gk.stage_times()
+    assert list(t) == gk.STAGES and all(v == (0.0, 0) for v in t.values())
+    assert gk.lib().gracekv_stage_times(None, None) == -1
+    cfg = gk.config_for(L=2, G=2, H=4, d=64, W=16, N_ctx=512, x=8.0, dtype=gk.F32, n_seg=2, D_hidden=64,
+                        flags=gk.FLAG_STAGE_TIMES | gk.FLAG_PRUNE)
+    assert gk.plan_sizes(cfg).B_total == 256
