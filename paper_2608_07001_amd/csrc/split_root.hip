@@ -8,18 +8,17 @@
 //
 // Every unit has exactly one node to refine here, so nothing of the unit has
 // to stay resident between nodes, and the workgroup is sized for two per CU
-// (256 threads, about 75 KB of LDS): while one workgroup waits at a barrier or
+// (256 threads, under 80 KB of LDS): while one workgroup waits at a barrier or
 // on memory, the other one computes.  Per unit:
 //   * candidates: curvature ranks of the positions t in [0, n-2] (cut t + 1),
 //     the midpoint, the extraction token (largest probe mass), all in local
 //     positions; prefix children [0, x) and suffix children [x, n);
-//   * key sums: k° = RoPE^{-1}(k) is staged in fp32 one half of the dimensions
-//     at a time (the pair (i, i + d/2) is rotated together, so each half
-//     re-reads the same rows); each direction's sums run in two token halves,
-//     the second half adding the first half's total at the end (fixed order);
-//   * value sums: V^T (bf16) replaces k° in the same LDS region; per direction
-//     and dimension, sum R v and sum v read off at the cuts; sum R and sum
-//     ||k°|| alongside;
+//   * child sums on the matrix cores: row c of the A operand masks the
+//     tokens of child c (prefix [0, x) or suffix [x, n)), alone or times R_t;
+//     the B operand is k° = RoPE^{-1}(k) (staged in fp32 one half of the
+//     dimensions at a time, the pair (i, i + d/2) rotated together), V^T (bf16)
+//     or (R_t, ||k°_t||); fp32 operands go in three bf16 parts, so every
+//     product is exact and only the fp32 accumulation rounds;
 //   * child keys k~ = RoPE(mean k°, p), coherence, multiplicity, then
 //     z = m_eff exp(k~ . q / sqrt(d) - m_q) for every child and probe on the
 //     matrix cores (k~ split in three bf16 parts: exact products), held in
@@ -49,15 +48,15 @@ struct SrLds {
   static constexpr int H2 = D / 2;
   static constexpr int LDV = NMAX + 8;                    // V^T row stride (bf16)
   static constexpr int KTS = D + 4;                       // child key row stride (fp32)
-  static constexpr int KOB = NMAX * H2 * 4;               // one half of k° [NMAX][H2] fp32
+  static constexpr int KOB = NMAX * (H2 + 4) * 4;         // one half of k° [NMAX][H2 + 4] fp32
   static constexpr int VTB = D * LDV * 2;                 // V^T [D][LDV] bf16
   static constexpr int oX = 0;                            // k° half, then V^T
   static constexpr int oKt = (KOB > VTB ? KOB : VTB);     // [SR_CC][KTS] child k° sums -> k~
   static constexpr int oVv = oKt + SR_CC * KTS * 4;       // [SR_CC][D] v~
   static constexpr int oCs = oVv + SR_CC * D * 4;         // [6][SR_CC] n, sum R, mean ||k°||, m_eff, D, ||v~||^2
   static constexpr int oCon = oCs + 6 * SR_CC * 4;        // [SR_CC][4] per-wave D partials
-  static constexpr int oTot = oCon + SR_CC * 4 * 4;       // [2][D] first-half totals of the key sums
-  static constexpr int oR = oTot + 2 * D * 4;             // [NMAX] R_t
+  static constexpr int oPart = oCon + SR_CC * 4 * 4;      // [2][SR_CC][D/16] partial norms, [SR_CC][8] sums
+  static constexpr int oR = oPart + (2 * (D / 16) + 8) * SR_CC * 4;   // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                // [NMAX] probe mass A_t
   static constexpr int oKap = oA + NMAX * 4;              // [NMAX] kappa_t
   static constexpr int oKn = oKap + NMAX * 4;             // [NMAX] ||k°_t||^2, then ||k°_t||
@@ -114,7 +113,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   float* sVv = (float*)(smem + Lay::oVv);
   float* sCs = (float*)(smem + Lay::oCs);
   float* sCon = (float*)(smem + Lay::oCon);
-  float* sTot = (float*)(smem + Lay::oTot);
+  float* sPart = (float*)(smem + Lay::oPart);
   float* sR = (float*)(smem + Lay::oR);
   float* sA = (float*)(smem + Lay::oA);
   float* sKap = (float*)(smem + Lay::oKap);
@@ -128,17 +127,22 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   int* meta = XL + 160;                    // nl, nr, nb, p, kmin, kmax, index of p in XL, of p+1 in XR, work item
   auto crow = [&](int r) { return sCs + r * SR_CC; };
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+  const int tid0 = threadIdx.x;
   const int J = *n_slots;
   const int nwork = tv.wctr[0];
   const float scale = 1.0f / sqrtf((float)D);
   const float LOG2E = 1.44269504088896341f;
-  const int pt = wave;                     // probe tile of this wave
-  const int q = 16 * pt + i16;             // the lane's probe (scoring layout)
-  const bool pok = q < dm.W;
 
-  if (tid == 0) meta[9] = atomicAdd(&tv.wctr[1], 1);
+  if (tid0 == 0) meta[9] = atomicAdd(&tv.wctr[1], 1);
   for (;;) {
+    // per-lane indices are formed inside the loop (values derived from them are
+    // not held across items, which would not fit the register budget)
+    int tid = tid0;
+    asm volatile("" : "+v"(tid));
+    const int wave = uni(tid >> 6), lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
+    const int pt = wave;                     // probe tile of this wave
+    const int q = 16 * pt + i16;             // the lane's probe (scoring layout)
+    const bool pok = q < dm.W;
     __syncthreads();
     const int wi = uni(meta[9]);
     __syncthreads();
@@ -223,22 +227,12 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       av = tv.tok_A[(int64_t)lg * dm.N_c + a0 + tid];
       kv = kappa[a0 + tid];
     }
-    // probe quarter rows of the wave's tile (probe q: window query q of head q mod |H(g)|)
-    uint32_t qreg[QW];
+    // probe shift and normaliser of the lane's probe (probe q: window query q of
+    // head q mod |H(g)|); its row is loaded with the child keys
     float mq2 = 0.f, izc = 1.f;
-    {
-      const int uq = pok ? q : 0;
-      const uint16_t* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
-      const uint4* q4 = (const uint4*)(Qp + ((int64_t)(uq % dm.hpg) * dm.W + uq) * D + QE * g4);
-#pragma unroll
-      for (int h = 0; h < QW / 4; ++h) {
-        const uint4 v = q4[h];
-        qreg[4 * h] = v.x; qreg[4 * h + 1] = v.y; qreg[4 * h + 2] = v.z; qreg[4 * h + 3] = v.w;
-      }
-      if (pok) {
-        mq2 = tv.probe_m[(int64_t)lg * dm.W + q] * LOG2E;
-        izc = 1.0f / tv.probe_ZC[(int64_t)lg * dm.W + q];
-      }
+    if (pok) {
+      mq2 = tv.probe_m[(int64_t)lg * dm.W + q] * LOG2E;
+      izc = 1.0f / tv.probe_ZC[(int64_t)lg * dm.W + q];
     }
     if (tid < n) {
       sR[tid] = rv;
@@ -325,7 +319,50 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     __syncthreads();
     const int nl = uni(meta[0]), nr = uni(meta[1]), nb = uni(meta[2]), p = uni(meta[3]);
 
+    // ---- children's sums on the matrix cores ----
+    // A operand rows = children (row gc: prefix child gc < SR_CM covers [0, XL[gc]),
+    // suffix child gc - SR_CM covers [XR[gc - SR_CM], n)), as a 0/1 mask or the
+    // masked token values; B operand = the tokens' k° or v (k° and R split in
+    // three bf16 parts: exact products, fp32 accumulation).  Lane (i16, g4)
+    // feeds row 16 ct + i16 and tokens 16 s + 4 g4 + r.
+    // bf16 1.0 (as 0xffff masks) per token t0 .. t0 + 3 inside child row 16 ct + i16
+    auto row_bounds = [&](int ct, int& lo, int& hi) {
+      const int gc = 16 * ct + i16;
+      lo = 0;
+      hi = 0;
+      if (gc < SR_CM) {
+        if (gc < nl) hi = XL[gc];
+      } else if (gc < SR_CC && gc - SR_CM < nr) {
+        lo = XR[gc - SR_CM];
+        hi = n;
+      }
+    };
+    auto mask16 = [&](int lo, int hi, int t0) {
+      uint32_t m[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m[r] = (t0 + r >= lo && t0 + r < hi) ? 0xffffu : 0u;
+      u32x2 v;
+      v.x = m[0] | (m[1] << 16);
+      v.y = m[2] | (m[3] << 16);
+      return v;
+    };
+    const u32x2 one2 = {0x3F803F80u, 0x3F803F80u};   // bf16 1.0 in every half
+    const int nks = (n + 15) >> 4;           // 16-token k steps
+    constexpr int NP = D / 16;               // 16-dim partials per child
+    float* sPss = sPart;                     // [SR_CC][NP] ||mean k°||^2 partials
+    float* sPvs = sPart + SR_CC * NP;        // [SR_CC][NP] ||v~||^2 partials
+    float* sTmp = sPart + 2 * SR_CC * NP;    // [SR_CC][8] sum R and sum ||k°|| in three parts each
+    // lengths of the children (0: no such child)
+    if (tid < SR_CC) {
+      int nch = 0;
+      if (tid < SR_CM) { if (tid < nl) nch = XL[tid]; }
+      else if (tid - SR_CM < nr) nch = n - XR[tid - SR_CM];
+      crow(0)[tid] = (float)nch;
+    }
+
     // ---- key sums: k° staged one half of the dims at a time ----
+    constexpr int KSTR = H2 + 4;             // k° row stride (fp32): conflict-free column reads
+    constexpr int HT = H2 / 16;              // 16-dim tiles per half
     for (int hf = 0; hf < 2; ++hf) {
       // k° of the half (item (token, 8-dim chunk): the pair (i, i + H2) is
       // rotated together); every load of the half in flight first
@@ -362,7 +399,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
           o[h] = hf == 0 ? k1 * cs[it][h] + k2 * sn[it][h] : k2 * cs[it][h] - k1 * sn[it][h];
           ss += o[h] * o[h];
         }
-        float4* d1 = (float4*)(sKo + t * H2 + c);
+        float4* d1 = (float4*)(sKo + t * KSTR + c);
         d1[0] = make_float4(o[0], o[1], o[2], o[3]);
         d1[1] = make_float4(o[4], o[5], o[6], o[7]);
         // ||k°_t||^2: the CH items of token t sit in CH consecutive lanes
@@ -371,86 +408,46 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         if (e % CH == 0) sKn[t] = hf == 0 ? ss : sKn[t] + ss;
       }
       __syncthreads();
-      // sums: thread (direction, token half, dim); the second half adds the first
-      // half's total afterwards (prefix: [0, x) = [0, h) + [h, x); suffix mirrored)
-      {
-        const int dir = tid >> 7;            // 0 prefix, 1 suffix
-        const int part = (tid >> 6) & 1;     // 0: the half the sweep starts in
-        const bool act = lane < H2;
-        const int i = act ? lane : 0;        // dim of the half (H2 <= 64)
-        const int h = n >> 1;
-        const int* xs = dir == 0 ? XL : XR;
-        const int nx = dir == 0 ? nl : nr;
-        // token range of this thread: prefix part 0 [0, h), part 1 [h, n);
-        // suffix part 0 [h, n) walked down, part 1 [0, h) walked down
-        const int lo = (dir == 0) == (part == 0) ? 0 : h;
-        const int hi = (dir == 0) == (part == 0) ? h : n;
-        float s = 0.f;
-        if (dir == 0) {
-          int t = lo;
-          for (int c = 0; c < nx; ++c) {
-            const int x = uni(xs[c]);
-            if (x <= lo || x > hi) continue;
-            for (; t + 4 <= x; t += 4) {
-              const float f0 = sKo[t * H2 + i], f1 = sKo[(t + 1) * H2 + i];
-              const float f2 = sKo[(t + 2) * H2 + i], f3 = sKo[(t + 3) * H2 + i];
-              s += f0; s += f1; s += f2; s += f3;
-            }
-            for (; t < x; ++t) s += sKo[t * H2 + i];
-            if (act) sKt[c * Lay::KTS + hf * H2 + i] = s;
-          }
-          if (part == 0) {                   // the first half's total for part 1
-            for (; t + 4 <= hi; t += 4) {
-              const float f0 = sKo[t * H2 + i], f1 = sKo[(t + 1) * H2 + i];
-              const float f2 = sKo[(t + 2) * H2 + i], f3 = sKo[(t + 3) * H2 + i];
-              s += f0; s += f1; s += f2; s += f3;
-            }
-            for (; t < hi; ++t) s += sKo[t * H2 + i];
-            if (act) sTot[i] = s;
-          }
-        } else {
-          int t = hi;                        // next token to add is t - 1
-          for (int c = nx - 1; c >= 0; --c) {
-            const int x = uni(xs[c]);
-            if (x < lo || x >= hi) continue;
-            for (; t - 4 >= x; t -= 4) {
-              const float f0 = sKo[(t - 1) * H2 + i], f1 = sKo[(t - 2) * H2 + i];
-              const float f2 = sKo[(t - 3) * H2 + i], f3 = sKo[(t - 4) * H2 + i];
-              s += f0; s += f1; s += f2; s += f3;
-            }
-            for (; t > x; --t) s += sKo[(t - 1) * H2 + i];
-            if (act) sKt[(SR_CM + c) * Lay::KTS + hf * H2 + i] = s;
-          }
-          if (part == 0) {
-            for (; t - 4 >= lo; t -= 4) {
-              const float f0 = sKo[(t - 1) * H2 + i], f1 = sKo[(t - 2) * H2 + i];
-              const float f2 = sKo[(t - 3) * H2 + i], f3 = sKo[(t - 4) * H2 + i];
-              s += f0; s += f1; s += f2; s += f3;
-            }
-            for (; t > lo; --t) s += sKo[(t - 1) * H2 + i];
-            if (act) sTot[D + i] = s;
+      // wave = 16-dim tile of the half: every child's sum, and the partial of
+      // ||mean k°||^2 over the tile's dims
+      for (int tile = wave; tile < HT; tile += SR_T / 64) {
+        int clo[CT], chi[CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) row_bounds(ct, clo[ct], chi[ct]);
+        f32x4 acc[CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < nks; ++s) {
+          const int t0 = 16 * s + 4 * g4;
+          float x[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] = t0 + r < n ? sKo[(t0 + r) * KSTR + 16 * tile + i16] : 0.f;
+          u32x2 kh, km, kl;
+          sr_split3(x, kh, km, kl);
+#pragma unroll
+          for (int ct = 0; ct < CT; ++ct) {
+            const s16x4 mk = sr_op(one2 & mask16(clo[ct], chi[ct], t0));
+            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(kl), acc[ct]);
+            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(km), acc[ct]);
+            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(kh), acc[ct]);
           }
         }
-      }
-      __syncthreads();
-      // part 1's children take the first half's total
-      {
-        const int dir = tid >> 7, part = (tid >> 6) & 1, i = lane;
-        if (part == 1 && i < H2) {
-          const int h = n >> 1;
-          const float tot = sTot[dir * D + i];
-          if (dir == 0) {
-            for (int c = 0; c < nl; ++c) {
-              const int x = uni(XL[c]);
-              if (x > h) sKt[c * Lay::KTS + hf * H2 + i] += tot;
-            }
-          } else {
-            for (int c = 0; c < nr; ++c) {
-              const int x = uni(XR[c]);
-              if (x < h) sKt[(SR_CM + c) * Lay::KTS + hf * H2 + i] += tot;
+        // lane (dim 16 tile + i16, g4) holds children 16 ct + 4 g4 + r
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int gr = 16 * ct + 4 * g4 + r;
+            const int grr = gr < SR_CC ? gr : 0;
+            const float nch = crow(0)[grr];
+            const float inv = nch > 0.f ? 1.0f / nch : 0.f;
+            const float m = acc[ct][r] * inv;
+            const float ps = row_sum16(m * m);
+            if (gr < SR_CC) {
+              sKt[gr * Lay::KTS + hf * H2 + 16 * tile + i16] = acc[ct][r];
+              if (i16 == 0) sPss[gr * NP + hf * HT + tile] = ps;
             }
           }
-        }
       }
       __syncthreads();
     }
@@ -482,125 +479,145 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       if (tid < n) sKn[tid] = sqrtf(sKn[tid]);
     }
     __syncthreads();
-    {
-      // thread (direction, dim): sum R v and sum v read off at the cuts; lanes
-      // 0 of each direction also sum R and ||k°||; then v~ and the child rows
-      const int dir = tid >> 7, i = tid & 127;
-      const bool act = i < D;
-      const int ii = act ? i : 0;
-      const int* xs = dir == 0 ? XL : XR;
-      const int nx = dir == 0 ? nl : nr;
-      float srv = 0.f, sv = 0.f, sr = 0.f, skn = 0.f;
-      const uint16_t* vrow = sVt + ii * Lay::LDV;
-      auto add2 = [&](int t) {               // tokens t, t + 1 (t even)
-        const uint32_t u = *(const uint32_t*)(vrow + t);
-        const float v0 = __uint_as_float(u << 16), v1 = __uint_as_float(u & 0xffff0000u);
-        const float2 r2 = *(const float2*)(sR + t);
-        const float2 k2 = *(const float2*)(sKn + t);
-        srv += r2.x * v0; sv += v0; sr += r2.x; skn += k2.x;
-        srv += r2.y * v1; sv += v1; sr += r2.y; skn += k2.y;
-      };
-      auto add1 = [&](int t) {
-        const float v0 = __uint_as_float((uint32_t)vrow[t] << 16);
-        const float r0 = sR[t];
-        srv += r0 * v0; sv += v0; sr += r0; skn += sKn[t];
-      };
-      auto emit = [&](int gc, int nch) {
-        if (nch >= 2) {
-          const float inv = 1.0f / (float)nch;
-          const float beta = dm.beta_frac * sr * inv;
-          if (act) sVv[gc * D + i] = (srv + beta * sv) / (sr + (float)nch * beta + dm.eps);
-        }
-        if (i == 0) {
-          crow(0)[gc] = (float)nch;
-          crow(1)[gc] = sr;
-          crow(2)[gc] = skn / (float)nch;
-        }
-      };
-      if (dir == 0) {
-        int t = 0;
-        for (int c = 0; c < nx; ++c) {
-          const int x = uni(xs[c]);
-          if (t & 1) { add1(t); ++t; }
-          for (; t + 2 <= x; t += 2) add2(t);
-          if (t < x) { add1(t); ++t; }
-          emit(c, x);
-        }
-      } else {
-        int t = n;                           // next token to add is t - 1
-        for (int c = nx - 1; c >= 0; --c) {
-          const int x = uni(xs[c]);
-          if (t & 1) { add1(t - 1); --t; }
-          for (; t - 2 >= x; t -= 2) {
-            // the same order as one token at a time, right to left
-            const uint32_t u = *(const uint32_t*)(vrow + t - 2);
-            const float v0 = __uint_as_float(u << 16), v1 = __uint_as_float(u & 0xffff0000u);
-            const float2 r2 = *(const float2*)(sR + t - 2);
-            const float2 k2 = *(const float2*)(sKn + t - 2);
-            srv += r2.y * v1; sv += v1; sr += r2.y; skn += k2.y;
-            srv += r2.x * v0; sv += v0; sr += r2.x; skn += k2.x;
-          }
-          if (t > x) { add1(t - 1); --t; }
-          emit(SR_CM + c, n - x);
-        }
+    // sum R and sum ||k°|| of every child: wave = child tile; B columns 0-2 hold
+    // R in three parts, columns 3-5 ||k°|| in three parts
+    if (wave < CT) {
+      const int ct = wave;
+      int clo, chi;
+      row_bounds(ct, clo, chi);
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int part = i16 % 3;
+      const float* src = i16 < 3 ? sR : sKn;
+      for (int s = 0; s < nks; ++s) {
+        const int t0 = 16 * s + 4 * g4;
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) x[r] = (i16 < 6 && t0 + r < n) ? src[t0 + r] : 0.f;
+        u32x2 xh, xm, xl;
+        sr_split3(x, xh, xm, xl);
+        const u32x2 b = part == 0 ? xh : (part == 1 ? xm : xl);
+        acc = mfma_bf16_16x16x16(sr_op(one2 & mask16(clo, chi, t0)), sr_op(b), acc);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int gr = 16 * ct + 4 * g4 + r;
+        if (gr < SR_CC && i16 < 6) sTmp[gr * 8 + i16] = acc[r];
       }
     }
     __syncthreads();
-
-    // ---- child keys: coherence, multiplicity, k~ = RoPE(mean k°, p) (one wave per child) ----
-    {
-      constexpr int KPW = (SR_CC + SR_T / 64 - 1) / (SR_T / 64);   // children per wave
-      const int i = lane < H2 ? lane : 0;
-      // the rotation rows of the wave's children, every load in flight together
-      float ccv[KPW], snv[KPW];
+    if (tid < SR_CC) {
+      const float* x = sTmp + tid * 8;
+      const float nch = crow(0)[tid];
+      crow(1)[tid] = x[2] + x[1] + x[0];
+      crow(2)[tid] = nch > 0.f ? (x[5] + x[4] + x[3]) / nch : 0.f;
+    }
+    __syncthreads();
+    // wave = 16-dim value tiles: sum v and sum R v of every child, then v~
+    // (eq:app_value_prototype) and the partial of ||v~||^2 over the tile
+    for (int dt = wave; dt < DT; dt += SR_T / 64) {
+      int clo[CT], chi[CT];
 #pragma unroll
-      for (int m = 0; m < KPW; ++m) {
-        const int k = wave + (SR_T / 64) * m;
+      for (int ct = 0; ct < CT; ++ct) row_bounds(ct, clo[ct], chi[ct]);
+      f32x4 av[CT], arv[CT];
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct) { av[ct] = f32x4{0.f, 0.f, 0.f, 0.f}; arv[ct] = av[ct]; }
+      for (int s = 0; s < nks; ++s) {
+        const int t0 = 16 * s + 4 * g4;
+        const uint2 vv = *(const uint2*)(sVt + (16 * dt + i16) * Lay::LDV + t0);
+        u32x2 vb;
+        vb.x = vv.x;
+        vb.y = vv.y;
+        const float4 r4 = *(const float4*)(sR + t0);
+        const float rx[4] = {t0 < n ? r4.x : 0.f, t0 + 1 < n ? r4.y : 0.f, t0 + 2 < n ? r4.z : 0.f,
+                             t0 + 3 < n ? r4.w : 0.f};
+        u32x2 rh, rm, rl;
+        sr_split3(rx, rh, rm, rl);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+          const u32x2 mk = mask16(clo[ct], chi[ct], t0);
+          av[ct] = mfma_bf16_16x16x16(sr_op(one2 & mk), sr_op(vb), av[ct]);
+          arv[ct] = mfma_bf16_16x16x16(sr_op(rl & mk), sr_op(vb), arv[ct]);
+          arv[ct] = mfma_bf16_16x16x16(sr_op(rm & mk), sr_op(vb), arv[ct]);
+          arv[ct] = mfma_bf16_16x16x16(sr_op(rh & mk), sr_op(vb), arv[ct]);
+        }
+      }
+#pragma unroll
+      for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int gr = 16 * ct + 4 * g4 + r;
+          const int grr = gr < SR_CC ? gr : 0;
+          const float nch = crow(0)[grr];
+          float vt = 0.f;
+          if (nch >= 2.f) {
+            const float sr = crow(1)[grr];
+            const float beta = dm.beta_frac * sr * (1.0f / nch);
+            vt = (arv[ct][r] + beta * av[ct][r]) / (sr + nch * beta + dm.eps);
+          }
+          const float ps = row_sum16(vt * vt);
+          if (gr < SR_CC && nch >= 2.f) {
+            sVv[gr * D + 16 * dt + i16] = vt;
+            if (i16 == 0) sPvs[gr * NP + dt] = ps;
+          }
+        }
+    }
+    __syncthreads();
+
+    // ---- child keys: coherence, multiplicity (eq:app_effective_multiplicity),
+    // k~ = RoPE(mean k°, p) (eq:app_rope_prototype) ----
+    // the probe quarter rows of the wave's tile, in flight meanwhile
+    uint32_t qreg[QW];
+    {
+      const int uq = pok ? q : 0;
+      const uint16_t* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
+      const uint4* q4 = (const uint4*)(Qp + ((int64_t)(uq % dm.hpg) * dm.W + uq) * D + QE * g4);
+#pragma unroll
+      for (int h = 0; h < QW / 4; ++h) {
+        const uint4 v = q4[h];
+        qreg[4 * h] = v.x; qreg[4 * h + 1] = v.y; qreg[4 * h + 2] = v.z; qreg[4 * h + 3] = v.w;
+      }
+    }
+    if (tid < SR_CC) {
+      const float nch = crow(0)[tid];
+      if (nch >= 2.f) {
+        float ss = 0.f, vs = 0.f;
+#pragma unroll
+        for (int k = 0; k < NP; ++k) { ss += sPss[tid * NP + k]; vs += sPvs[tid * NP + k]; }
+        const float coh = sqrtf(ss) / (crow(2)[tid] + dm.eps);
+        crow(3)[tid] = fminf(fmaxf(nch * coh * coh, 1.0f), nch);
+        crow(5)[tid] = vs;
+      }
+    }
+    {
+      constexpr int RPT = (SR_CC * H2 + SR_T - 1) / SR_T;   // (child, pair) items per thread
+      float ccv[RPT], snv[RPT];
+#pragma unroll
+      for (int m = 0; m < RPT; ++m) {         // the rotation rows, every load in flight together
+        const int e = tid + SR_T * m;
+        const int gc = e / H2, i = e % H2;
         int64_t pp = a0;
-        if (k < nl + nr) {
-          const bool pre = k < nl;
-          const int c = pre ? k : k - nl;
-          const int x0 = pre ? 0 : XR[c];
-          const int x1 = pre ? XL[c] : n;
-          pp = round_half_even_mid(a0 + x0, a0 + x1);
+        if (e < SR_CC * H2) {
+          const int nch = (int)crow(0)[gc];
+          if (nch >= 2) {
+            const int x0 = gc < SR_CM ? 0 : XR[gc - SR_CM];
+            pp = round_half_even_mid(a0 + x0, a0 + x0 + nch);
+          }
         }
         ccv[m] = cosT[pp * H2 + i];
         snv[m] = sinT[pp * H2 + i];
       }
 #pragma unroll
-      for (int m = 0; m < KPW; ++m) {
-        const int k = wave + (SR_T / 64) * m;
-        if (k >= nl + nr) break;
-        const bool pre = k < nl;
-        const int c = pre ? k : k - nl;
-        const int gc = pre ? c : SR_CM + c;
-        const int x0 = pre ? 0 : uni(XR[c]);
-        const int x1 = pre ? uni(XL[c]) : n;
-        const int nch = x1 - x0;
-        if (nch < 2) continue;
-        const float cc = ccv[m], sn = snv[m];
+      for (int m = 0; m < RPT; ++m) {
+        const int e = tid + SR_T * m;
+        if (e >= SR_CC * H2) break;
+        const int gc = e / H2, i = e % H2;
+        const float nch = crow(0)[gc];
+        if (nch < 2.f) continue;
+        const float inv = 1.0f / nch;
         float* kt = sKt + gc * Lay::KTS;
-        const float inv = 1.0f / (float)nch;
-        float ss = 0.f;
-        for (int d = lane; d < D; d += 64) {
-          const float m = kt[d] * inv;
-          ss += m * m;
-        }
-        float vs = 0.f;
-        for (int d = lane; d < D; d += 64) {
-          const float v = sVv[gc * D + d];
-          vs += v * v;
-        }
-        ss = wave_sum_dpp(ss);
-        vs = wave_sum_dpp(vs);
-        const float coh = sqrtf(ss) / (crow(2)[gc] + dm.eps);
-        const float me = fminf(fmaxf((float)nch * coh * coh, 1.0f), (float)nch);
-        if (lane == 0) { crow(3)[gc] = me; crow(5)[gc] = vs; }
-        if (lane < H2) {
-          const float m1 = kt[i] * inv, m2 = kt[i + H2] * inv;
-          kt[i] = m1 * cc - m2 * sn;
-          kt[i + H2] = m2 * cc + m1 * sn;
-        }
+        const float m1 = kt[i] * inv, m2 = kt[i + H2] * inv;
+        kt[i] = m1 * ccv[m] - m2 * snv[m];
+        kt[i + H2] = m2 * ccv[m] + m1 * snv[m];
       }
     }
     __syncthreads();
