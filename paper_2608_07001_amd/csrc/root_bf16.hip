@@ -34,29 +34,34 @@ namespace gkv {
 constexpr int RB_T = 256;          // threads per workgroup
 constexpr int RB_W = RB_T / 64;    // waves
 constexpr int RB_GRID = 2048;      // persistent workgroups (two per CU, four rounds)
-constexpr int RB_GRID_RI = 2304;   // ... without K rows in LDS (three per CU, three rounds)
+constexpr int RB_GRID_RI = 4096;   // ... without K rows in LDS (four per CU, four rounds)
 
-template <int D>
+// RI: the token relevance pass ran before (no relevance partials, no K rows).
+// The prototype k~, v~ share the probe-mass partials' space: those are last
+// read before barrier B, the prototype is first written after it and last read
+// before the next unit's barrier S.
+template <int D, bool RI>
 struct RbLds {
   static constexpr int LDK = D + 8;          // K rows [NMAX][LDK] bf16
   static constexpr int LDV = NMAX + 8;       // V^T rows [D][LDV] bf16, token columns permuted per 32-block
   static constexpr int oVt = 0;
-  static constexpr int oRp = oVt + D * LDV * 2;             // [RB_W][NMAX] relevance partials
-  static constexpr int oAp = oRp + RB_W * NMAX * 4;         // [RB_W][NMAX] probe-mass partials
+  static constexpr int oRp = oVt + D * LDV * 2;             // [RB_W][NMAX] relevance partials (not RI)
+  static constexpr int oAp = oRp + (RI ? 0 : RB_W * NMAX * 4);   // [RB_W][NMAX] probe-mass partials
+  static constexpr int oKt = oAp;                           // [D] prototype key k~
+  static constexpr int oVv = oKt + D * 4;                   // [D] prototype value v~
+  static_assert(2 * D <= RB_W * NMAX, "prototype inside the probe-mass partials");
   static constexpr int oR = oAp + RB_W * NMAX * 4;          // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                  // [NMAX] A_t
-  static constexpr int oKn = oA + NMAX * 4;                 // [2][NMAX] ||k°_t|| (unit parity)
-  static constexpr int oPk = oKn + 2 * NMAX * 4;            // [RB_W][D] partial sums of k°
-  static constexpr int oKt = oPk + RB_W * D * 4;            // [D] prototype key k~
-  static constexpr int oVv = oKt + D * 4;                   // [D] prototype value v~
-  static constexpr int oSum = oVv + D * 4;                  // [RB_W][4] per-wave sums of R, A, ||k°||
+  static constexpr int oKn = oA + NMAX * 4;                 // [NMAX] ||k°_t||
+  static constexpr int oPk = oKn + NMAX * 4;                // [RB_W][D] partial sums of k°
+  static constexpr int oSum = oPk + RB_W * D * 4;           // [RB_W][4] per-wave sums of R, A, ||k°||
   static constexpr int oRed = oSum + RB_W * 4 * 4;          // [2][RB_W] distortion sums (unit parity)
   static constexpr int oPend = oRed + 2 * RB_W * 4;         // deferred outputs of the previous unit
-  static constexpr int oK = oPend + 64;                     // K rows [NMAX][LDK]
-  static constexpr int bytes = oK + NMAX * LDK * 2;
+  static constexpr int oK = oPend + 64;                     // K rows [NMAX][LDK] (not RI)
+  static constexpr int bytes = RI ? oK : oK + NMAX * LDK * 2;
 };
 
-int root_bf16_lds_bytes(int d) { return d == 128 ? RbLds<128>::bytes : RbLds<64>::bytes; }
+int root_bf16_lds_bytes(int d) { return d == 128 ? RbLds<128, false>::bytes : RbLds<64, false>::bytes; }
 
 // LDS column of token t of a unit: within each 32-token block, the token
 // 16 h + 4 g + r (tile h, lane group g, row r) sits at 8 g + 4 h + r
@@ -91,7 +96,7 @@ __device__ __forceinline__ float pick4f(const float* v, int i) {
 // RI: the direct relevance s-hat is already in the token values (the token
 // relevance pass ran before), so only the probe rows are evaluated here.
 template <int D, bool MP, bool RI>
-__global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
+__global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __restrict__ dmp, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ V, const uint16_t* __restrict__ Q,
                                                      const float* __restrict__ cosT, const float* __restrict__ sinT,
                                                      const int32_t* __restrict__ slot_starts,
@@ -100,7 +105,7 @@ __global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __rest
   // scalar registers they would not fit)
   const Dims& dm = *dmp;
   const TreeView& tv = *tvp;
-  using Lay = RbLds<D>;
+  using Lay = RbLds<D, RI>;
   constexpr int H2 = D / 2;
   constexpr int DT = D / 16;                 // 16-wide value tiles of M^T
   constexpr int KS = D / 32;                 // k steps of a logit tile
@@ -230,7 +235,7 @@ __global__ __launch_bounds__(RB_T, RI ? 3 : 2) void k_root_bf(const Dims* __rest
       }
     }
     const int64_t pmid = round_half_even_mid((int)a0, (int)a0 + n);
-    float* Kn = sKn + buf * NMAX;
+    float* Kn = sKn;
 
     // ---- staging: K rows (zero past n) with RoPE undone on the way for the k°
     // sums and ||k°_t||; V^T with permuted token columns (zero past n) ----
@@ -562,10 +567,10 @@ hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const 
                             hipStream_t st) {
   const int64_t cap = (int64_t)dm.L * dm.G * dm.J_cap;
   const bool ri = token_relevance_pass(dm);   // s-hat already in the token values
-  // RI: no K rows in LDS (they are the last region), three workgroups per CU
+  // RI: no relevance partials and no K rows in LDS, four workgroups per CU
   const int64_t gmax = ri ? RB_GRID_RI : RB_GRID;
   const dim3 grid((unsigned)(cap < gmax ? cap : gmax));
-  const int lds = ri ? (dm.d == 128 ? RbLds<128>::oK : RbLds<64>::oK) : root_bf16_lds_bytes(dm.d);
+  const int lds = ri ? (dm.d == 128 ? RbLds<128, true>::bytes : RbLds<64, true>::bytes) : root_bf16_lds_bytes(dm.d);
 #define GKV_LAUNCH_ROOT_BF(DD)                                                                              \
   do {                                                                                                      \
     auto fn = ri ? k_root_bf<DD, false, true> : (dm.hpg > 4 ? k_root_bf<DD, true, false> : k_root_bf<DD, false, false>); \
