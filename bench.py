@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-overlap", action="store_true",
                     help="relevance statistics inside gracekv_build_trees instead of on a second stream during "
                          "segmentation")
+    ap.add_argument("--no-floor", action="store_true",
+                    help="skip the singleton-floor measurement (alpha = 0.6 on the 8B-8K workload)")
     ap.add_argument("--no-reuse", action="store_true",
                     help="skip the structure-reuse measurement (one segmentation serving further questions)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -230,6 +232,51 @@ def kernel_table(work, clk, names):
             e["tokens"] = w["tokens"]
         out[st] = e
     return out
+
+
+def floor_measure(seed, steps=3, warmup=1, config="8b-8k", alpha=0.6):
+    """The whole path with the singleton floor (alpha = 0.6, the paper's default
+    share) on a smaller workload: the floor needs every tree complete (no
+    budget-aware pruning), which at 128K takes seconds per step.  Steps timed
+    with HIP events on the stream the calls run on; the floor's stages from the
+    stage clock."""
+    import torch
+    from paper_2608_07001_amd import gracekv as gk
+    from synth.workloads import CONFIGS, make_case
+    sh = CONFIGS[config]
+    case = make_case(sh, seed, device="cuda")
+    cfg = gk.config_for(L=sh.L, G=sh.G, H=sh.H, d=sh.d, W=sh.W, N_ctx=sh.N_ctx, x=sh.x,
+                        dtype=gk.BF16 if sh.dtype == "bf16" else gk.F32, n_seg=sh.n_seg, D_hidden=sh.D,
+                        flags=gk.FLAG_STAGE_TIMES, alpha_floor=alpha)
+    buf = gk.allocate(cfg, "cuda")
+    stream = torch.cuda.current_stream()
+    args = (buf, case["K"], case["V"], case["Q"], case["rope_cos"], case["rope_sin"], case["hidden"],
+            case["surprisal"], case["omega_raw"])
+    for _ in range(warmup):
+        gk.compress(*args, stream=stream)
+    torch.cuda.synchronize()
+    gk.stage_times()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        gk.compress(*args, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gk.check(cfg, buf.trees, stream)
+    ms = e0.elapsed_time(e1) / steps
+    clk = {k: (v / n if n else None) for k, (v, n) in gk.stage_times().items()}
+    fl = gk.floor_arrays(buf.plan, buf.trees)
+    st = fl["state"].cpu().tolist()
+    res = {"workload": f"{sh.name}: L={sh.L} G={sh.G} H={sh.H} d={sh.d} N_ctx={sh.N_ctx} W={sh.W} x={sh.x:g} "
+                       f"({sh.dtype}), complete build", "alpha_floor": alpha, "ms_per_step": ms,
+           "value": sh.L * sh.G * sh.N_ctx / (ms * 1e-3), "unit": "tokens/s", "steps": steps,
+           "B_floor": st[0], "cap": st[1], "path_cost_of_the_initial_lists": st[2], "lists_reduced": bool(st[3]),
+           "candidates": int(fl["cnt"].sum().item()), "b_used": int(buf.b_used.item()),
+           "floor_candidates_ms": clk["floor_candidates"], "floor_realise_ms": clk["floor_realise"],
+           "stages_ms": clk}
+    del buf, case
+    torch.cuda.empty_cache()
+    return res
 
 
 def reuse_measure(cfg, sh, case, buf, stream, seg_ms, full_ms, n_questions=3):
@@ -512,6 +559,8 @@ def main():
     }
     if not args.no_reuse and default_path:
         res["structure_reuse"] = reuse_measure(cfg, sh, case, buf, stream, stage_ms["segment"], ms)
+    if not args.no_floor and default_path:
+        res["alpha_floor"] = floor_measure(args.seed)
     if not args.no_decode:
         res["decode_attention"] = decode_measure(cfg, sh, case, buf, stream)
     if not args.no_multi_hop and q_graph is None and not (args.ablation_pair_quotas or args.ablation_uniform_slots):

@@ -65,7 +65,7 @@ typedef enum { GRACEKV_F32 = 0, GRACEKV_BF16 = 1 } gracekv_dtype;
 /* Version of this interface (structures and signatures).  A binding must
  * refuse a library whose gracekv_abi_version() differs from the value it was
  * written for: argument lists shift silently across versions. */
-#define GRACEKV_ABI_VERSION 10
+#define GRACEKV_ABI_VERSION 11
 
 /* Shapes and hyperparameters.  gracekv_default_config fills the paper's
  * defaults (App. A and B); the caller then sets the shape fields. */
@@ -87,7 +87,10 @@ typedef struct {
   float lam_kappa, beta_frac, eps;           /* 0.05, 0.1, 1e-6 */
   float lambda_graph;                        /* multi-hop weight in [0, 1]: 0 (direct relevance
                                                 only) or e.g. 0.3 (App. A.4 eq:app_bottom_up_value) */
-  float alpha_floor;                         /* must be 0 (no singleton floor) */
+  double alpha_floor;                        /* singleton floor share in [0, 1]: 0 (no floor) or
+                                                e.g. 0.6 (App. A.5 Stage I, eq:app_floor_cap); with a
+                                                floor the build is complete (no GRACEKV_FLAG_PRUNE,
+                                                no GRACEKV_FLAG_PAIR_QUOTAS) */
   int32_t flags;                             /* GRACEKV_FLAG_* below */
 } gracekv_config;
 
@@ -128,7 +131,9 @@ typedef struct {
 #define GRACEKV_STAGE_REFINE 5           /* refinement below the roots (pruned build) or of every
                                             node (complete fp32 build) */
 #define GRACEKV_STAGE_PACK 6             /* gracekv_pack's emitting kernel */
-#define GRACEKV_N_STAGES 7
+#define GRACEKV_STAGE_FLOOR_CANDIDATES 7 /* singleton floor: scores, sorted candidate lists */
+#define GRACEKV_STAGE_FLOOR_REALISE 8    /* singleton floor: path costs, reduction, realisation */
+#define GRACEKV_N_STAGES 9
 
 /* Sizes derived from a config (host only). */
 typedef struct {
@@ -148,7 +153,8 @@ typedef struct {
          off_unit_nn, off_unit_Ddrop, off_add_U, off_add_E, off_add_exec,
          off_tok_R, off_tok_A, off_row_stats, off_probe_m, off_probe_ZC, off_lg_S,
          off_omega, off_status, off_slots, off_nslots, off_partial, off_theta, off_selstate,
-         off_work, off_wctr, off_proto, off_proto_logm;
+         off_work, off_wctr, off_proto, off_proto_logm,
+         off_floor;        /* the singleton floor's region (alpha_floor > 0; see gracekv_select) */
   int32_t build_lds_bytes; /* dynamic LDS of the tree-build kernel */
   size_t build_ws_bytes;   /* workspace of gracekv_build_trees: 0 unless lambda_graph > 0 */
 } gracekv_plan;
@@ -162,7 +168,8 @@ gracekv_status gracekv_default_config(gracekv_config* cfg);
 /* Validates cfg and fills plan.  Returns GRACEKV_ERR_BUDGET when the budget
  * cannot hold a recent window of r_min entries per (layer, KV head)
  * (App. A.1), GRACEKV_ERR_INVALID_ARG for lambda_graph outside [0, 1],
- * GRACEKV_ERR_UNSUPPORTED for alpha_floor != 0, lambda_graph > 0 with
+ * or alpha_floor outside [0, 1], GRACEKV_ERR_UNSUPPORTED for alpha_floor > 0
+ * with GRACEKV_FLAG_PRUNE or GRACEKV_FLAG_PAIR_QUOTAS, lambda_graph > 0 with
  * H / G > 8, or shapes outside the documented limits. */
 gracekv_status gracekv_plan_sizes(const gracekv_config* cfg, gracekv_plan* plan);
 

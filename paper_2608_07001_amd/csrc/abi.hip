@@ -33,6 +33,8 @@ Dims make_dims(const gracekv_config& c, const gracekv_plan& p) {
   d.pair_quotas = (c.flags & GRACEKV_FLAG_PAIR_QUOTAS) ? 1 : 0;
   d.lam_graph = c.lambda_graph;
   d.stage_times = (c.flags & GRACEKV_FLAG_STAGE_TIMES) ? 1 : 0;
+  d.alpha_floor = (float)c.alpha_floor;
+  d.floor_cap = c.alpha_floor > 0.0 ? (int64_t)floor(c.alpha_floor * (double)p.B_free) : 0;
   // propagation layers at relative depths 0.50 and 0.75, rounded like the
   // segmentation layers (eq:app_seg_layers)
   d.n_gl = 0;
@@ -83,7 +85,23 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.work = (int32_t*)(b + p.off_work);
   v.wctr = (int32_t*)(b + p.off_wctr);
   v.dhat = nullptr;
+  v.fl_flag = nullptr;
+  v.fl_pre_add = nullptr;
+  v.fl_pre_sp = nullptr;
+  v.fl_state = nullptr;
   return v;
+}
+
+// the floor's region (alpha_floor > 0) and the view's pointers into it
+static FloorView floor_of(void* trees, const Dims& dm, const gracekv_plan& p, TreeView* tv) {
+  FloorView f = floor_view((char*)trees + p.off_floor, dm, p.unit_cap, p.node_cap);
+  if (tv) {
+    tv->fl_flag = f.flag;
+    tv->fl_pre_add = f.pre_add;
+    tv->fl_pre_sp = f.pre_sp;
+    tv->fl_state = f.state;
+  }
+  return f;
 }
 
 __global__ void k_copy_slots(const int32_t* __restrict__ slot_starts, const int32_t* __restrict__ n_slots, int J_cap,
@@ -179,7 +197,7 @@ gracekv_status gracekv_default_config(gracekv_config* c) {
   c->lam_Z = 0.25f; c->lam_M = 0.75f;
   c->k_curv = 16;
   c->lam_kappa = 0.05f; c->beta_frac = 0.1f; c->eps = 1e-6f;
-  c->lambda_graph = 0.f; c->alpha_floor = 0.f;
+  c->lambda_graph = 0.f; c->alpha_floor = 0.0;
   return GRACEKV_OK;
 }
 
@@ -209,7 +227,9 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   if (!(c->x >= 1.0) || !isfinite(c->x)) return GRACEKV_ERR_INVALID_ARG;
   if (!(c->lambda_graph >= 0.f && c->lambda_graph <= 1.f)) return GRACEKV_ERR_INVALID_ARG;
   if (c->lambda_graph > 0.f && c->H / c->G > 8) return GRACEKV_ERR_UNSUPPORTED;   // one wave per query head
-  if (c->alpha_floor != 0.f) return GRACEKV_ERR_UNSUPPORTED;
+  if (!(c->alpha_floor >= 0.0 && c->alpha_floor <= 1.0)) return GRACEKV_ERR_INVALID_ARG;
+  if (c->alpha_floor > 0.0 && (c->flags & (GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_PAIR_QUOTAS)))
+    return GRACEKV_ERR_UNSUPPORTED;   // the floor needs every tree complete and the shared auction
   if (c->flags & ~(GRACEKV_FLAG_PRUNE | GRACEKV_FLAG_DP_SERIAL | GRACEKV_FLAG_UNIFORM_SLOTS |
                    GRACEKV_FLAG_PAIR_QUOTAS | GRACEKV_FLAG_STATS_READY | GRACEKV_FLAG_STAGE_TIMES))
     return GRACEKV_ERR_INVALID_ARG;
@@ -284,6 +304,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_wctr, 16);
   put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));
   put(p->off_proto_logm, UC * 4);
+  put(p->off_floor, c->alpha_floor > 0.0 ? floor_view(nullptr, dm, p->unit_cap, p->node_cap).bytes : 0);
   o += KARGS_BYTES;                          // device copy of the kernel arguments
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
@@ -337,11 +358,11 @@ gracekv_status gracekv_stage_times(float* total_ms, int32_t* launches) {
   std::lock_guard<std::mutex> g(clock_mu);
   gracekv_status s = GRACEKV_OK;
   int cur = -1;
-  hipGetDevice(&cur);
+  (void)hipGetDevice(&cur);
   for (const ClockPair& p : clock_pending) {
     if (p.b && p.stage >= 0 && p.stage < GRACEKV_N_STAGES && s == GRACEKV_OK) {
       float ms = 0.f;
-      hipSetDevice(p.device);
+      (void)hipSetDevice(p.device);
       if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess) {
         s = GRACEKV_ERR_HIP;
       } else {
@@ -353,7 +374,7 @@ gracekv_status gracekv_stage_times(float* total_ms, int32_t* launches) {
     if (p.b) clock_pool.push_back({p.device, p.b});
   }
   clock_pending.clear();
-  if (cur >= 0) hipSetDevice(cur);
+  if (cur >= 0) (void)hipSetDevice(cur);
   return s;
 }
 
@@ -374,6 +395,8 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
   }
   Dims dm = make_dims(*c, p);
   TreeView tv = make_view(trees, p);
+  FloorView fv{};
+  if (c->alpha_floor > 0.0) fv = floor_of(trees, dm, p, &tv);
   hipStream_t st = (hipStream_t)stream;
   hipLaunchKernelGGL(k_copy_slots, dim3(1), dim3(256), 0, st, slot_starts, n_slots, p.J_cap, tv);
   if (hipGetLastError() != hipSuccess) return GRACEKV_ERR_HIP;
@@ -412,6 +435,13 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     clock_end(clk, st);
     if (e != hipSuccess) return GRACEKV_ERR_HIP;
   }
+  // singleton floor: the candidates, from the final token values, before any split
+  if (c->alpha_floor > 0.0) {
+    const int clk = clock_begin(dm, GRACEKV_STAGE_FLOOR_CANDIDATES, st);
+    const hipError_t e = launch_floor_candidates(dm, tv, fv, st);
+    clock_end(clk, st);
+    if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  }
   if (!(c->flags & GRACEKV_FLAG_PRUNE)) {
     // bf16: the roots first, by the kernel the pruned build refines them with
     if (c->dtype == GRACEKV_BF16 && build(BUILD_ROOT_FULL) != hipSuccess) return GRACEKV_ERR_HIP;
@@ -445,7 +475,15 @@ gracekv_status gracekv_select(const gracekv_config* c, void* trees, int64_t* b_u
   if (!trees || !b_used || !ws || !aligned16(trees) || !aligned16(ws)) return GRACEKV_ERR_INVALID_ARG;
   if (ws_bytes < p.sel_ws_bytes) return GRACEKV_ERR_WORKSPACE;
   Dims dm = make_dims(*c, p);
-  return hip_status(launch_select(dm, make_view(trees, p), b_used, ws, (hipStream_t)stream));
+  TreeView tv = make_view(trees, p);
+  if (c->alpha_floor > 0.0) {                 // the floor's realisation, then the auction from it
+    const FloorView fv = floor_of(trees, dm, p, &tv);
+    const int clk = clock_begin(dm, GRACEKV_STAGE_FLOOR_REALISE, (hipStream_t)stream);
+    const hipError_t e = launch_floor_realise(dm, tv, fv, (hipStream_t)stream);
+    clock_end(clk, (hipStream_t)stream);
+    if (e != hipSuccess) return GRACEKV_ERR_HIP;
+  }
+  return hip_status(launch_select(dm, tv, b_used, ws, (hipStream_t)stream));
 }
 
 gracekv_status gracekv_pack(const gracekv_config* c, const void* K, const void* V, const float* rope_cos,

@@ -71,7 +71,8 @@ struct RefLds {
   static constexpr int oCs = oZt + CC * WMAX * 4;         // [5][CC] n, sum R, mean ||k||, m_eff, D
   static constexpr int oX = oCs + 5 * CC * 4;             // cut lists and metadata
   static constexpr int oFlag = oX + 256 * 4;
-  static constexpr int bytes = oFlag + NMAX * 4;
+  static constexpr int oFl = oFlag + NMAX * 4;            // [NMAX] singleton-floor candidate flags
+  static constexpr int bytes = oFl + NMAX;
 };
 
 int build_lds_bytes(const Dims& dm) {
@@ -86,7 +87,7 @@ struct Ref {
   float* Ko; T* Vt; float* R; float* A; float* Kap; float* Kn; float* Mq; float* Zc;
   int* na; int* nn; int* nc; int* np; int* ncut; float* nD; float* nR; float* nU; uint64_t* nE;
   uint8_t* nch; uint8_t* nk;
-  float* Kt; float* Con; float* Vv; float* Zt; float* cs; int* xi; int* flag;
+  float* Kt; float* Con; float* Vv; float* Zt; float* cs; int* xi; int* flag; uint8_t* fl;
   __device__ Ref(char* base) : s(base) {
     Ko = (float*)(s + Lay::oKo); Vt = (T*)(s + Lay::oVt); R = (float*)(s + Lay::oR); A = (float*)(s + Lay::oA);
     Kap = (float*)(s + Lay::oKap); Kn = (float*)(s + Lay::oKn); Mq = (float*)(s + Lay::oMq);
@@ -97,6 +98,7 @@ struct Ref {
     nch = (uint8_t*)(s + Lay::oNch); nk = (uint8_t*)(s + Lay::oNk);
     Kt = (float*)(s + Lay::oKt); Con = Kt; Vv = (float*)(s + Lay::oVv); Zt = (float*)(s + Lay::oZt);
     cs = (float*)(s + Lay::oCs); xi = (int*)(s + Lay::oX); flag = (int*)(s + Lay::oFlag);
+    fl = (uint8_t*)(s + Lay::oFl);
   }
   __device__ float* crow(int row) { return cs + row * CC; }
 };
@@ -502,7 +504,8 @@ __global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int
   int* XL = U.xi;              // [0..31]  prefix cut list
   int* XR = U.xi + 32;         // [32..63] suffix cut list
   int* XB = U.xi + 64;         // [64..95] binary cuts
-  int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits, index of p in XL, of p+1 in XR
+  int* meta = U.xi + 96;       // nXL, nXR, nXB, p, kmin bits, kmax bits, index of p in XL, of p+1 in XR,
+                               // forced extraction (singleton floor)
   int* posL = U.xi + 128;      // index of XB[k] in XL
   int* posR = U.xi + 160;      // index of XB[k] in XR
   int* cnt = U.xi + 192;       // node count
@@ -643,6 +646,7 @@ __global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int
         U.R[tid] = tv.tok_R[(int64_t)lg * dm.N_c + a0 + tid];
         U.A[tid] = tv.tok_A[(int64_t)lg * dm.N_c + a0 + tid];
         U.Kap[tid] = kappa[a0 + tid];
+        U.fl[tid] = tv.fl_flag ? tv.fl_flag[(int64_t)lg * dm.N_c + a0 + tid] : 0;
       }
       if (tid < dm.W) {
         U.Mq[tid] = tv.probe_m[(int64_t)lg * dm.W + tid];
@@ -707,29 +711,37 @@ __global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int
       if (tid == BT - 1) U.flag[nv / 2] = 1;      // midpoint a + floor(n/2)
       // curvature range and extraction token (wave 0)
       if (wave == 0) {
-        float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY;
-        int bi = 0x7fffffff;
+        float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY, bestf = -INFINITY;
+        int bi = 0x7fffffff, bf = 0x7fffffff;
         for (int t = a + lane; t < b; t += 64) {
           const float k = U.Kap[t];
           kmn = fminf(kmn, k);
           kmx = fmaxf(kmx, k);
           const float am = U.A[t];
           if (am > best || (am == best && t < bi)) { best = am; bi = t; }
+          // singleton floor: the candidate of largest token value (App. A.3 split choice)
+          if (U.fl[t] && (U.R[t] > bestf || (U.R[t] == bestf && t < bf))) { bestf = U.R[t]; bf = t; }
         }
         wave_minmax(kmn, kmx);
         wave_argmax(best, bi);
+        wave_argmax(bestf, bf);
         if (lane == 0) {
-          meta[3] = bi;
+          // a node of three or more tokens holding a floor candidate is extracted
+          // there, with no choice
+          const bool forced = bf != 0x7fffffff;
+          meta[3] = forced ? bf : bi;
           meta[4] = __float_as_int(kmn);
           meta[5] = __float_as_int(kmx);
+          meta[8] = forced ? 1 : 0;
         }
       }
       __syncthreads();
       // binary cuts XB (ascending) by ballot over the flags, then the prefix list
       // XL = XB + {p} (if p > a) and suffix list XR = XB + {p+1} (if p+1 < b)
       if (wave == 0) {
-        const bool f0 = lane >= 1 && lane < nv && U.flag[lane];
-        const bool f1 = 64 + lane < nv && U.flag[64 + lane];
+        const bool forced = meta[8] != 0;      // extraction only: no binary cut
+        const bool f0 = !forced && lane >= 1 && lane < nv && U.flag[lane];
+        const bool f1 = !forced && 64 + lane < nv && U.flag[64 + lane];
         const uint64_t m0 = __ballot(f0), m1 = __ballot(f1);
         const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
         const int n0 = __popcll(m0);

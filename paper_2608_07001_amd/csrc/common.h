@@ -33,6 +33,8 @@ struct Dims {
   float lam_graph;               // weight of the multi-hop relevance in the token values
   int n_gl, gl[2];               // propagation layers of the multi-hop relevance
   int stage_times;               // record the stage clock's events (GRACEKV_FLAG_STAGE_TIMES)
+  float alpha_floor;             // singleton floor share alpha (0: no floor)
+  int64_t floor_cap;             // floor(alpha B_free): entries the floor may spend
 };
 
 // Typed views into the tree buffer (offsets come from gracekv_plan).
@@ -75,7 +77,41 @@ struct TreeView {
   void* kargs;          // device copy of the kernel arguments (Dims, then this view) for the
                         // kernels that read them through pointers
   const float* dhat;    // [N_c] multi-hop relevance to mix into the token values, or null
+  // singleton floor (null without one)
+  const uint8_t* fl_flag;   // [LG][N_c] 1: the token is an initial floor candidate of its (l, g)
+  const uint8_t* fl_pre_add;  // [unit_cap] 1: the floor executed the unit's Add
+  const uint8_t* fl_pre_sp;   // [node_cap] 1: the floor executed the node's Split
+  const int64_t* fl_state;  // [8] B_floor first
 };
+
+// The singleton floor's region of the tree buffer (alpha_floor > 0).  Public
+// part, each array 256-byte aligned in this order: int64 state[8] (B_floor,
+// cap, total cost of the initial lists' paths, lists reduced, failure (l, g),
+// failure index, cost realised before it), int32 cnt[LG] (initial list
+// lengths), int32 keep[LG] (lengths after the proportional reduction), int32
+// list[LG][N_c] (candidates in the floor's order), uint8 flag[LG][N_c], uint8
+// pre_add[unit_cap], uint8 pre_sp[node_cap]; then scratch.
+struct FloorView {
+  int64_t* state;
+  int32_t* cnt;
+  int32_t* keep;
+  int32_t* list;        // also the sort's first key/value buffer's values
+  uint8_t* flag;
+  uint8_t* pre_add;
+  uint8_t* pre_sp;
+  float* rbar;          // [N_c] mean token value over (l, g)
+  uint32_t* keyA;       // [LG][N_c] sort keys (ping)
+  uint32_t* keyB;       // [LG][N_c] sort keys (pong); then the tail's path costs
+  int32_t* valB;        // [LG][N_c] sort values (pong); then the tail's unit ids
+  int32_t* first_add;   // [unit_cap] first list index whose path holds the Add
+  int32_t* first_sp;    // [node_cap] ... the Split
+  int32_t* inc;         // [LG][N_c] incremental path cost of each candidate
+  int64_t* lgsum;       // [LG] path cost of each (l, g)
+  size_t bytes;
+};
+FloorView floor_view(void* base, const Dims& dm, int64_t unit_cap, int64_t node_cap);
+hipError_t launch_floor_candidates(const Dims& dm, const TreeView& tv, const FloorView& fv, hipStream_t st);
+hipError_t launch_floor_realise(const Dims& dm, const TreeView& tv, const FloorView& fv, hipStream_t st);
 
 // Multi-hop relevance scratch (the build workspace when lambda_graph > 0).
 struct MhView {

@@ -41,6 +41,8 @@ struct SelState {
   int32_t mode;
   uint32_t done;        // workgroups finished with the current pass (the last one scans)
   uint64_t ncand;       // ops in the candidate list (> cap: the list is not used)
+  int64_t B;            // the auction's budget: B_free less the singleton floor's spending
+  int64_t floor;        // the floor's spending B_floor
   unsigned long long hist[256];
 };
 
@@ -147,11 +149,13 @@ hipError_t launch_score(const Dims& dm, const float* omega_raw, const TreeView& 
 }
 
 // ---------------------------------------------------------------------------
-__global__ void k_sel_init(Dims dm, SelState* S, int rank_extra) {
+__global__ void k_sel_init(Dims dm, SelState* S, int rank_extra, const int64_t* fstate) {
   const int t = threadIdx.x;
   S->hist[t] = 0;
   if (t == 0) {
-    S->prefix = 0; S->target = dm.B_free - 1 + rank_extra; S->above = 0; S->total = 0; S->R = 0;
+    S->floor = fstate ? fstate[0] : 0;
+    S->B = dm.B_free - S->floor;
+    S->prefix = 0; S->target = S->B - 1 + rank_extra; S->above = 0; S->total = 0; S->R = 0;
     S->resid_key = 0; S->mode = SEL_SELECT; S->done = 0; S->ncand = 0;
   }
 }
@@ -165,9 +169,9 @@ __device__ void sel_scan(const Dims& dm, SelState* S, int pass, const unsigned l
       int64_t tot = 0;
       for (int k = 0; k < 256; ++k) tot += (int64_t)hist[k];
       S->total = tot;
-      if (dm.B_free <= 0) { S->mode = SEL_NONE; break; }
-      if (tot <= dm.B_free) { S->mode = SEL_ALL; break; }
-      if (dm.B_free == 1) { S->mode = SEL_RESID; S->R = 1; break; }
+      if (S->B <= 0) { S->mode = SEL_NONE; break; }
+      if (tot <= S->B) { S->mode = SEL_ALL; break; }
+      if (S->B == 1) { S->mode = SEL_RESID; S->R = 1; break; }
     }
     const int shift = 56 - 8 * pass;
     const int64_t need = S->target - S->above;
@@ -240,19 +244,21 @@ __global__ __launch_bounds__(256) void k_sel_hist(Dims dm, TreeView tv, SelState
 #pragma unroll
         for (int bt = 0; bt < 4; ++bt) {
           const int c = (wds[q] >> (8 * bt)) & 255u;
-          if (c) take(tv.sp_E[16 * v + 4 * q + bt], c);
+          const int64_t i = 16 * v + 4 * q + bt;
+          if (c && !(tv.fl_pre_sp && tv.fl_pre_sp[i])) take(tv.sp_E[i], c);
         }
       }
     }
     for (int64_t i = 16 * n16 + (int64_t)blockIdx.x * 256 + tid; i < node_cap; i += stride) {
       const int c = tv.sp_cost[i];
-      if (c) take(tv.sp_E[i], c);
+      if (c && !(tv.fl_pre_sp && tv.fl_pre_sp[i])) take(tv.sp_E[i], c);
     }
     // Adds: cost 1 for every unit (l, g, j < J) of the partition
     const int64_t nadd = (int64_t)dm.L * dm.G * J;
     for (int64_t x = (int64_t)blockIdx.x * 256 + tid; x < nadd; x += stride) {
       const int lg = (int)(x / J), j = (int)(x - (int64_t)lg * J);
-      take(tv.add_E[(int64_t)lg * dm.J_cap + j], 1);
+      const int64_t u = (int64_t)lg * dm.J_cap + j;
+      if (!(tv.fl_pre_add && tv.fl_pre_add[u])) take(tv.add_E[u], 1);
     }
     if (pass == 0) {                          // append the workgroup's share to the list
       __syncthreads();
@@ -298,11 +304,13 @@ __global__ __launch_bounds__(256) void k_sel_flag(Dims dm, TreeView tv, const Se
       const int c = tv.sp_cost[i];
       uint8_t x = 0;
       if (c > 0) x = (mode == SEL_ALL) || (mode == SEL_SELECT && tv.sp_E[i] > theta);
+      if (tv.fl_pre_sp && tv.fl_pre_sp[i]) x = 1;     // executed by the singleton floor
       tv.sp_exec[i] = x;
     } else {
       const int64_t u = i - node_cap;
       if ((int)(u % dm.J_cap) >= J) continue;
-      tv.add_exec[u] = (mode == SEL_ALL) || (mode == SEL_SELECT && tv.add_E[u] > theta);
+      tv.add_exec[u] = (mode == SEL_ALL) || (mode == SEL_SELECT && tv.add_E[u] > theta) ||
+                       (tv.fl_pre_add && tv.fl_pre_add[u]);
     }
   }
 }
@@ -313,7 +321,7 @@ __global__ void k_sel_group(Dims dm, TreeView tv, SelState* S) {
   const int32_t* slot_starts = tv.slots;
   if (threadIdx.x != 0 || S->mode != SEL_SELECT) return;
   const uint64_t theta = S->prefix;
-  int64_t R = dm.B_free - S->above;
+  int64_t R = S->B - S->above;
   const int J = *n_slots;
   const uint32_t id = 0xFFFFFFFFu - (uint32_t)(theta & 0xFFFFFFFFu);
   const uint32_t ord = id >> 8;
@@ -401,8 +409,8 @@ __global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used)
   if (threadIdx.x != 0) return;
   const int mode = S->mode;
   int64_t R = S->R;
-  if (mode == SEL_ALL) { *b_used = S->total; return; }
-  if (mode == SEL_NONE) { *b_used = 0; return; }
+  if (mode == SEL_ALL) { *b_used = S->floor + S->total; return; }
+  if (mode == SEL_NONE) { *b_used = S->floor; return; }
   if (R == 1 && S->resid_key) {
     const int J = *n_slots;
     const uint32_t id = 0xFFFFFFFFu - (uint32_t)(S->resid_key & 0xFFFFFFFFu);
@@ -412,7 +420,7 @@ __global__ void k_sel_finish(Dims dm, TreeView tv, SelState* S, int64_t* b_used)
     else tv.sp_exec[(int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[j] + loc - 1] = 1;
     R = 0;
   }
-  *b_used = dm.B_free - R;
+  *b_used = S->floor + S->B - R;
 }
 
 // ---- the auction with fixed per-(l, g) capacities ---------------------------
@@ -621,7 +629,7 @@ hipError_t launch_select(const Dims& dm, const TreeView& tv, int64_t* b_used, vo
     return hipGetLastError();
   }
   SelState* S = (SelState*)ws;
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, 0);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, 0, tv.fl_state);
   const int64_t tot = (int64_t)dm.L * dm.G * 2 * dm.N_c + (int64_t)dm.L * dm.G * dm.J_cap;
   const unsigned blocks = (unsigned)std::min<int64_t>((tot + 255) / 256, 4096);
   sel_passes(dm, tv, S, st);
@@ -645,7 +653,7 @@ __global__ void k_theta_store(Dims dm, const SelState* S, uint64_t* theta, bool 
 
 hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound) {
   SelState* S = (SelState*)tv.selstate;
-  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, skip_bound ? 1 : 0);
+  hipLaunchKernelGGL(k_sel_init, dim3(1), dim3(256), 0, st, dm, S, skip_bound ? 1 : 0, (const int64_t*)nullptr);
   sel_passes(dm, tv, S, st);
   hipLaunchKernelGGL(k_theta_store, dim3(1), dim3(64), 0, st, dm, (const SelState*)S, tv.theta, skip_bound);
   return hipGetLastError();

@@ -62,7 +62,8 @@ struct SrLds {
   static constexpr int oKn = oKap + NMAX * 4;             // [NMAX] ||k°_t||^2, then ||k°_t||
   static constexpr int oFlag = oKn + NMAX * 4;            // [NMAX] candidate cut flags
   static constexpr int oL = oFlag + NMAX * 4;             // lists and metadata (int)
-  static constexpr int bytes = oL + 192 * 4;
+  static constexpr int oFl = oL + 192 * 4;                // [NMAX] singleton-floor candidate flags
+  static constexpr int bytes = oFl + NMAX;
 };
 
 int split_root_lds_bytes(int d) { return d == 128 ? SrLds<128>::bytes : SrLds<64>::bytes; }
@@ -119,12 +120,14 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   float* sKap = (float*)(smem + Lay::oKap);
   float* sKn = (float*)(smem + Lay::oKn);
   int* sFlag = (int*)(smem + Lay::oFlag);
+  uint8_t* sFl = (uint8_t*)(smem + Lay::oFl);
   int* XL = (int*)(smem + Lay::oL);        // [0, 32)   prefix cuts (child [0, x))
   int* XR = XL + 32;                       // [32, 64)  suffix cuts (child [x, n))
   int* XB = XL + 64;                       // [64, 96)  binary cuts
   int* posL = XL + 96;                     // index of XB[k] in XL
   int* posR = XL + 128;                    // index of XB[k] in XR
-  int* meta = XL + 160;                    // nl, nr, nb, p, kmin, kmax, index of p in XL, of p+1 in XR, work item
+  int* meta = XL + 160;                    // nl, nr, nb, p, kmin, kmax, index of p in XL, of p+1 in XR,
+                                           // forced extraction (singleton floor), work item
   auto crow = [&](int r) { return sCs + r * SR_CC; };
 
   const int tid0 = threadIdx.x;
@@ -222,10 +225,12 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     constexpr int CPR = D / 8;
     constexpr int VPT = (NMAX / 2) * CPR / SR_T;         // value items (token pair, 8-dim chunk) per thread
     float rv = 0.f, av = 0.f, kv = 0.f;
+    uint8_t fl = 0;
     if (tid < n) {
       rv = tokR[tid];
       av = tv.tok_A[(int64_t)lg * dm.N_c + a0 + tid];
       kv = kappa[a0 + tid];
+      if (tv.fl_flag) fl = tv.fl_flag[(int64_t)lg * dm.N_c + a0 + tid];
     }
     // probe shift and normaliser of the lane's probe (probe q: window query q of
     // head q mod |H(g)|); its row is loaded with the child keys
@@ -238,6 +243,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       sR[tid] = rv;
       sA[tid] = av;
       sKap[tid] = kv;
+      sFl[tid] = fl;
     }
     for (int t = tid; t < NMAX; t += SR_T) sFlag[t] = 0;
     __syncthreads();
@@ -261,29 +267,37 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     }
     if (tid == SR_T - 1) sFlag[n / 2] = 1;
     if (wave == 3) {                         // curvature range and extraction token
-      float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY;
-      int bi = 0x7fffffff;
+      float kmn = INFINITY, kmx = -INFINITY, best = -INFINITY, bestf = -INFINITY;
+      int bi = 0x7fffffff, bf = 0x7fffffff;
       for (int t = lane; t < n; t += 64) {
         const float k = sKap[t];
         kmn = fminf(kmn, k);
         kmx = fmaxf(kmx, k);
         const float am = sA[t];
         if (am > best || (am == best && t < bi)) { best = am; bi = t; }
+        // singleton floor: the candidate of largest token value (App. A.3 split choice)
+        if (sFl[t] && (sR[t] > bestf || (sR[t] == bestf && t < bf))) { bestf = sR[t]; bf = t; }
       }
       wave_minmax(kmn, kmx);
       wave_argmax(best, bi);
+      wave_argmax(bestf, bf);
       if (lane == 0) {
-        meta[3] = bi;
+        // a node of three or more tokens holding a floor candidate is extracted
+        // there, with no choice
+        const bool forced = bf != 0x7fffffff;
+        meta[3] = forced ? bf : bi;
         meta[4] = __float_as_int(kmn);
         meta[5] = __float_as_int(kmx);
+        meta[8] = forced ? 1 : 0;
       }
     }
     __syncthreads();
     // binary cuts XB ascending (by ballot over the flags), then XL = XB + {p}
     // (p > 0) and XR = XB + {p+1} (p+1 < n)
     if (wave == 0) {
-      const bool f0 = lane >= 1 && lane < n && sFlag[lane];
-      const bool f1 = 64 + lane < n && sFlag[64 + lane];
+      const bool forced = meta[8] != 0;        // extraction only: no binary cut
+      const bool f0 = !forced && lane >= 1 && lane < n && sFlag[lane];
+      const bool f1 = !forced && 64 + lane < n && sFlag[64 + lane];
       const uint64_t m0 = __ballot(f0), m1 = __ballot(f1);
       const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
       const int c0 = __popcll(m0);
@@ -622,10 +636,12 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     }
     __syncthreads();
 
-    // the prefix sweep's first key block, in flight during the z products
+    // the first sweep's first key block (the prefix sweep's, or the suffix
+    // sweep's when there is no prefix child), in flight during the z products
     uint32_t kcur[QW];
     {
-      const int tr = i16 < n ? i16 : n - 1;
+      int tr = (nl > 0 ? 0 : 16 * ((n - 1) >> 4)) + i16;
+      tr = tr < n ? tr : n - 1;
       const uint4* k4 = (const uint4*)(Kp + (int64_t)tr * D + QE * g4);
 #pragma unroll
       for (int h = 0; h < QW / 4; ++h) {

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libgracekv.so")
 
 F32, BF16 = 0, 1
-ABI_VERSION = 10         # GRACEKV_ABI_VERSION this binding is written for
+ABI_VERSION = 11         # GRACEKV_ABI_VERSION this binding is written for
 _STATUS = {0: "ok", -1: "invalid argument", -2: "unsupported configuration", -3: "budget",
            -4: "workspace too small", -5: "HIP error", -6: "numeric fault on the device",
            -7: "the tree buffer holds no build", -8: "malformed slot partition on the device",
@@ -40,7 +40,7 @@ class Config(ctypes.Structure):
                 ("lam_d", ctypes.c_float), ("lam_n", ctypes.c_float), ("c_cut", ctypes.c_float),
                 ("lam_Z", ctypes.c_float), ("lam_M", ctypes.c_float), ("k_curv", ctypes.c_int32),
                 ("lam_kappa", ctypes.c_float), ("beta_frac", ctypes.c_float), ("eps", ctypes.c_float),
-                ("lambda_graph", ctypes.c_float), ("alpha_floor", ctypes.c_float), ("flags", ctypes.c_int32)]
+                ("lambda_graph", ctypes.c_float), ("alpha_floor", ctypes.c_double), ("flags", ctypes.c_int32)]
 
 FLAG_PRUNE = 1
 FLAG_DP_SERIAL = 2
@@ -49,7 +49,8 @@ FLAG_PAIR_QUOTAS = 8
 FLAG_STATS_READY = 16
 FLAG_STAGE_TIMES = 32
 # stage ids of the stage clock (GRACEKV_STAGE_*), in order
-STAGES = ["segment", "rowstats", "token_relevance", "root", "root_split", "refine", "pack"]
+STAGES = ["segment", "rowstats", "token_relevance", "root", "root_split", "refine", "pack", "floor_candidates",
+          "floor_realise"]
 
 
 _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_node_nch", "off_node_kind",
@@ -57,7 +58,7 @@ _OFFS = ["off_node_a", "off_node_n", "off_node_child", "off_node_parent", "off_n
          "off_unit_nn", "off_unit_Ddrop", "off_add_U", "off_add_E", "off_add_exec", "off_tok_R",
          "off_tok_A", "off_row_stats", "off_probe_m", "off_probe_ZC", "off_lg_S", "off_omega", "off_status", "off_slots",
          "off_nslots", "off_partial", "off_theta", "off_selstate", "off_work", "off_wctr", "off_proto",
-         "off_proto_logm"]
+         "off_proto_logm", "off_floor"]
 
 
 class Plan(ctypes.Structure):
@@ -259,6 +260,24 @@ def tree_arrays(plan: Plan, trees: torch.Tensor) -> Dict[str, torch.Tensor]:
         status=v(plan.off_status, 2, torch.int32), nslots=v(plan.off_nslots, 1, torch.int32),
         slots=v(plan.off_slots, plan.J_cap + 1, torch.int32),
     )
+
+
+def floor_arrays(plan: Plan, trees: torch.Tensor) -> Dict[str, torch.Tensor]:
+    """Typed views of the singleton floor's region (alpha_floor > 0): state (B_floor,
+    cap, total cost of the initial lists, lists reduced, ...), initial and kept list
+    lengths, the lists, the candidate flags and the ops the floor executed."""
+    LG = plan.unit_cap // plan.J_cap
+    N = plan.N_c
+    al = lambda x: (x + 255) & ~255
+    o = plan.off_floor
+    out = {}
+    for name, n, dt in (("state", 8, torch.int64), ("cnt", LG, torch.int32), ("keep", LG, torch.int32),
+                        ("list", LG * N, torch.int32), ("flag", LG * N, torch.uint8),
+                        ("pre_add", plan.unit_cap, torch.uint8), ("pre_sp", plan.node_cap, torch.uint8)):
+        nbytes = n * torch.tensor([], dtype=dt).element_size()
+        out[name] = trees[o:o + nbytes].view(dt)
+        o += al(nbytes)
+    return out
 
 
 @dataclasses.dataclass

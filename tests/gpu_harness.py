@@ -66,6 +66,8 @@ def gpu_run(case_dev: dict, x=None, slots: Optional[List[int]] = None, kappa: Op
                tok_A=buf.trees[buf.plan.off_tok_A:buf.plan.off_tok_A + LG * buf.plan.N_c * 4].view(torch.float32).cpu(),
                b_used=int(buf.b_used.item()), offsets=buf.offsets.cpu(), counts=buf.counts.cpu(),
                K_out=buf.K_out.cpu(), V_out=buf.V_out.cpu(), pos_out=buf.pos_out.cpu(), logm_out=buf.logm_out.cpu())
+    if cfg.alpha_floor > 0:
+        out["floor"] = {k: v.cpu() for k, v in gk.floor_arrays(buf.plan, buf.trees).items()}
     if slots is None:
         J = int(buf.n_slots.item())
         out.update(kappa=buf.kappa.cpu(), bscore=buf.bscore.cpu(), slots=buf.slot_starts[:J].cpu().tolist())

@@ -84,7 +84,8 @@ def test_plan_rejections():
     with pytest.raises(gk.GraceKVError) as e:
         gk.plan_sizes(_cfg(N_ctx=8192, x=4000.0))        # < 4 entries per (l, g)
     assert e.value.status == -3
-    for bad, code in [(dict(lambda_graph=1.5), -1), (dict(lambda_graph=-0.1), -1), (dict(alpha_floor=0.6), -2), (dict(d=96), -2),
+    for bad, code in [(dict(lambda_graph=1.5), -1), (dict(lambda_graph=-0.1), -1), (dict(alpha_floor=0.6, flags=1), -2), (dict(alpha_floor=0.6, flags=8), -2),
+                      (dict(alpha_floor=1.5), -1), (dict(alpha_floor=-0.1), -1), (dict(d=96), -2),
                       (dict(W=65), -2), (dict(H=30), -1), (dict(x=0.5), -1), (dict(n_min=8), -2),
                       (dict(dtype=gk.F32), -2), (dict(N_ctx=0), -1), (dict(flags=64), -1), (dict(flags=9), -2), (dict(flags=4, n0=200), -2), (dict(flags=4, n0=8), -2)]:
         with pytest.raises(gk.GraceKVError) as e:

@@ -41,6 +41,8 @@ def test_bench_json_line_on_the_small_workload():
     st = r["stages_ms"]
     assert abs(sum(st[k] for k in ("segment", "build", "score", "select", "pack")) - r["ms_per_step"]) < 0.05 * r["ms_per_step"]
     assert r["multi_hop"]["ms_per_step"] > 0
+    fl = r["alpha_floor"]
+    assert fl["ms_per_step"] > 0 and 0 < fl["B_floor"] <= fl["cap"] and fl["floor_candidates_ms"] > 0
 
 
 def test_stage_clock_leaves_the_output_unchanged():
