@@ -891,13 +891,18 @@ __global__ void k_work_reset(TreeView tv) {
   if (threadIdx.x < 4) tv.wctr[threadIdx.x] = 0;
 }
 
-__global__ void k_work_mark(Dims dm, int mode, TreeView tv) {
+// Lists the units to refine whose slot length lies in [n_lo, n_hi): the
+// launches go from long slots to short ones, so the persistent workgroups take
+// the long (slow) items first and finish together.
+__global__ void k_work_mark(Dims dm, int mode, TreeView tv, int n_lo, int n_hi) {
   const int64_t unit = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (unit >= (int64_t)dm.L * dm.G * dm.J_cap) return;
   const int lg = (int)(unit / dm.J_cap), j = (int)(unit % dm.J_cap);
   const int J = *tv.nslots;
   if (j >= J || J > dm.J_cap) return;
   const int64_t a0 = tv.slots[j];
+  const int ns = tv.slots[j + 1] - (int)a0;
+  if (ns < n_lo || ns >= n_hi) return;
   const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * a0;
   const int nn = tv.unit_nn[unit];
   const uint64_t theta = (mode == BUILD_FULL || mode == BUILD_ROOT_FULL) ? 0ull : tv.theta[0];
@@ -945,7 +950,10 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
                         const float* kappa, const TreeView& tv, hipStream_t st) {
   const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
   hipLaunchKernelGGL(k_work_reset, dim3(1), dim3(64), 0, st, tv);
-  hipLaunchKernelGGL(k_work_mark, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, st, dm, mode, tv);
+  const unsigned mb = (unsigned)((units + 255) / 256);
+  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 96, NMAX + 1);
+  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 48, 96);
+  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 0, 48);
   const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
   const int clk = clock_begin(dm, roots ? GRACEKV_STAGE_ROOT_SPLIT : GRACEKV_STAGE_REFINE, st);
   if (dm.dtype == GRACEKV_BF16 && roots) {
