@@ -181,6 +181,20 @@ __device__ __forceinline__ void lse2_add8(float& m, float& z, const float* y) {
   m = mn;
 }
 
+// The same update from eight raw logits x (y = x * sc2, sc2 > 0, all present):
+// the maximum is taken on x (scaling by a positive number keeps the order, and
+// rounding is monotonic, so max(x) * sc2 is the largest y), and each term is
+// 2^(x * sc2 - max) with the product fused into the subtraction.
+__device__ __forceinline__ void lse2_add8_raw(float& m, float& z, const float* x, float sc2) {
+  const float mxr = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+  const float mn = fmaxf(m, mxr * sc2);
+  float acc = z * __builtin_amdgcn_exp2f(m - mn);   // m = -inf at first: 2^-inf = 0
+#pragma unroll
+  for (int r = 0; r < 8; ++r) acc += __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], sc2, -mn));
+  z = acc;
+  m = mn;
+}
+
 template <int D>
 __global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ Q, float4* __restrict__ partial,
@@ -269,8 +283,8 @@ __global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[h][r] * sc2;
-          lse2_add8(mC[k], zC[k], y);
+            for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[h][r];
+          lse2_add8_raw(mC[k], zC[k], y, sc2);
         } else {
           float xt[8];
 #pragma unroll
