@@ -521,7 +521,8 @@ def main():
     work = stage_work(sh, p, buf, 2 if sh.dtype == "bf16" else 4)
     ktab = kernel_table(work, stage_ms["kernels"], kernel_names(sh.dtype))
     dom = max((k for k in ktab if k != "segment"), key=lambda k: ktab[k]["ms"])
-    copy_gbs = copy_bandwidth(dev)
+    # (a counter calibration run has its own copy probe; the bandwidth copy would be mistaken for it)
+    copy_gbs = copy_bandwidth(dev) if args.copy_probe_mib == 0 else None
     traffic = recorded_traffic(sh.name, ktab[dom]["kernel"]) if default_path else None
     tokens = sh.L * sh.G * sh.N_ctx
     b = 2 if sh.dtype == "bf16" else 4
@@ -552,7 +553,7 @@ def main():
         "roofline": {"kernel": ktab[dom]["kernel"], "bound": "hbm", "achieved": ktab[dom]["gbs"],
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ktab[dom]["frac_hbm"], "traffic": traffic,
                      "ms_per_launch": ktab[dom]["ms"], "algorithmic_bytes_per_launch": ktab[dom]["bytes"],
-                     "copy_gbs": copy_gbs, "frac_of_copy": ktab[dom]["gbs"] / copy_gbs},
+                     "copy_gbs": copy_gbs, "frac_of_copy": ktab[dom]["gbs"] / copy_gbs if copy_gbs else None},
         "kernels": ktab,
         "build_call": {"ms": stage_ms["build_call"], "algorithmic_bytes": ab["build"], "gbs": build_gbs,
                        "frac_hbm": build_gbs / HBM_PEAK_GBS},
