@@ -658,7 +658,7 @@ __global__ __launch_bounds__(BT) void k_refine(const Dims* __restrict__ dmp, int
     if (16 * pt + i16 < dm.W) { mq = U.Mq[16 * pt + i16]; zc = U.Zc[16 * pt + i16]; }
     // ---- top-down refinement in BFS order ----
     for (int head = 0;; ++head) {
-      __syncthreads();
+      sync_after_lds_stores();               // the node table and cnt were stored at the end of the last pass
       const int count = cnt[0];
       if (head >= count || (mode == BUILD_ROOT_SPLIT && head > 0)) break;
       const int a = U.na[head], nv = U.nn[head], b = a + nv;

@@ -214,6 +214,17 @@ __device__ __forceinline__ float ldf(const uint16_t* p, int64_t i) { return bf16
 __device__ __forceinline__ void stf(float* p, int64_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void stf(uint16_t* p, int64_t i, float v) { p[i] = f32_to_bf16_rne(v); }
 
+// Workgroup barrier at the top of a loop whose previous iteration ended with
+// LDS stores that the other waves read after it (a work-item index, a node
+// table): the wave waits for its own LDS operations explicitly first.  The
+// wait that the barrier's fence implies is not kept on such a loop back edge
+// by the compiler, and without it a store may still be in flight, and be read
+// stale by a wave on another SIMD, when the barrier opens.
+__device__ __forceinline__ void sync_after_lds_stores() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // s_waitcnt lgkmcnt(0)
+  __syncthreads();
+}
+
 // Workgroup barrier that orders LDS accesses only: unlike __syncthreads() it
 // does not wait for the wave's global loads in flight.
 __device__ __forceinline__ void lds_barrier() {

@@ -14,25 +14,27 @@
 //     the midpoint, the extraction token (largest probe mass), all in local
 //     positions; prefix children [0, x) and suffix children [x, n);
 //   * child sums on the matrix cores: row c of the A operand masks the
-//     tokens of child c (prefix [0, x) or suffix [x, n)), alone or times R_t;
-//     the B operand is k° = RoPE^{-1}(k) (staged in fp32 one half of the
-//     dimensions at a time, the pair (i, i + d/2) rotated together), V^T (bf16)
-//     or (R_t, ||k°_t||); fp32 operands go in three bf16 parts, so every
-//     product is exact and only the fp32 accumulation rounds;
+//     tokens of child c (prefix [0, x) or suffix [x, n)); the B operand is
+//     k° = RoPE^{-1}(k) (staged in fp32 one half of the dimensions at a time,
+//     the pair (i, i + d/2) rotated together) or (R_t, ||k°_t||); fp32
+//     operands go in three bf16 parts, so every product is exact and only the
+//     fp32 accumulation rounds;
 //   * child keys k~ = RoPE(mean k°, p), coherence, multiplicity, then
 //     z = m_eff exp(k~ . q / sqrt(d) - m_q) for every child and probe on the
 //     matrix cores (k~ split in three bf16 parts: exact products), held in
 //     registers in the layout the scoring reads;
-//   * distortion sweeps: wave = probe tile; it recomputes the probe
-//     exponentials of each 16-token block (transposed logits on the matrix
-//     cores), accumulates M^T = V^T E^T piece by piece between cuts with the
-//     exact three-part split of e, and scores each child when the sweep
-//     reaches its cut; prefix children left to right, then suffix children
-//     right to left.  Cut positions are read into scalar registers, so the
-//     sweep's control flow is uniform.  The value term of D_q is formed as
-//     ||M||^2 - 2 z <M, v~> + z^2 ||v~||^2 (clamped at 0): its rounding error
-//     is a few fp32 ulps of ||M||^2, i.e. about 1e-6 of the node's attention
-//     mass in D, far below the distortions compared;
+//   * distortions from the Gram matrix G = V V^T of the node (bf16 products,
+//     exact; stored as 16 x 16 tiles in three bf16 parts).  For a child C and
+//     probe q, ||M_q||^2, <M_q, v~_C> and ||v~_C||^2 are quadratic forms in G
+//     over C's token pairs; for the nested prefix children [0, x) (suffix
+//     children [x, n)) each is a sum over the child of per-token increments
+//     built from Y_t = sum_{t' < t} G_tt' e_t' (t' > t), so one product
+//     Y = G E^T per direction (strictly lower or upper tiles) and one masked
+//     sum per child on the matrix cores replace the per-cut value sums M^T.
+//     The value term ||M - z v~||^2 = ||M||^2 - 2 z <M, v~> + z^2 ||v~||^2
+//     (clamped at 0) carries a rounding error of a few fp32 ulps of ||M||^2,
+//     about 1e-6 of the node's attention mass in D, far below the distortions
+//     compared;
 //   * the fp32 scores decide (binary form wins ties, smaller cut wins ties)
 //     and the root and its children are written to the node table.
 #include "common.h"
@@ -46,17 +48,22 @@ constexpr int SR_CC = 2 * SR_CM;        // prefix side [0, SR_CM), suffix side [
 template <int D>
 struct SrLds {
   static constexpr int H2 = D / 2;
-  static constexpr int LDV = NMAX + 8;                    // V^T row stride (bf16)
+  static constexpr int NTM = NMAX / 16;                   // 16-token tiles
   static constexpr int KTS = D + 4;                       // child key row stride (fp32)
   static constexpr int KOB = NMAX * (H2 + 4) * 4;         // one half of k° [NMAX][H2 + 4] fp32
-  static constexpr int VTB = D * LDV * 2;                 // V^T [D][LDV] bf16
-  static constexpr int oX = 0;                            // k° half, then V^T
-  static constexpr int oKt = (KOB > VTB ? KOB : VTB);     // [SR_CC][KTS] child k° sums -> k~
-  static constexpr int oVv = oKt + SR_CC * KTS * 4;       // [SR_CC][D] v~
-  static constexpr int oCs = oVv + SR_CC * D * 4;         // [6][SR_CC] n, sum R, mean ||k°||, m_eff, D, ||v~||^2
-  static constexpr int oCon = oCs + 6 * SR_CC * 4;        // [SR_CC][4] per-wave D partials
-  static constexpr int oPart = oCon + SR_CC * 4 * 4;      // [2][SR_CC][D/16] partial norms, [SR_CC][8] sums
-  static constexpr int oR = oPart + (2 * (D / 16) + 8) * SR_CC * 4;   // [NMAX] R_t
+  static constexpr int KTB = SR_CC * KTS * 4;             // child k° sums -> k~
+  static constexpr int GTB = 3 * 256 * 2;                 // one Gram tile: three bf16 planes of 16 x 16
+  static constexpr int GB = NTM * (NTM + 1) / 2 * GTB;    // the Gram tiles (a >= b)
+  // k° halves, then the Gram tiles over them and over the child keys (read
+  // for the last time by the z products)
+  static constexpr int oX = 0;
+  static constexpr int oKt = (KOB > GB - KTB ? KOB : GB - KTB);   // [SR_CC][KTS]
+  static constexpr int oCs = (oKt + KTB > GB ? oKt + KTB : GB);   // [8][SR_CC] per-child scalars
+  static constexpr int oCon = oCs + 8 * SR_CC * 4;        // [SR_CC][4] per-wave D partials
+  static constexpr int oPart = oCon + SR_CC * 4 * 4;      // [SR_CC][D/16] partial norms, [SR_CC][12] sums
+  static constexpr int oAG = oPart + ((D / 16) + 12) * SR_CC * 4;   // [4][NMAX] rows of G against R and 1
+  static constexpr int oGd = oAG + 4 * NMAX * 4;          // [NMAX] G_tt
+  static constexpr int oR = oGd + NMAX * 4;               // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                // [NMAX] probe mass A_t
   static constexpr int oKap = oA + NMAX * 4;              // [NMAX] kappa_t
   static constexpr int oKn = oKap + NMAX * 4;             // [NMAX] ||k°_t||^2, then ||k°_t||
@@ -105,13 +112,12 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   constexpr int H2 = D / 2;
   constexpr int QE = D / 4;                // dims of a probe quarter row
   constexpr int QW = QE / 2;               // 32-bit words of it
-  constexpr int DT = D / 16;               // 16-wide value tiles of M^T
   constexpr int CT = (SR_CC + 15) / 16;    // 16-wide child tiles
+  constexpr int NTM = Lay::NTM;            // 16-token tiles
   extern __shared__ __align__(16) char smem[];
   float* sKo = (float*)(smem + Lay::oX);
-  uint16_t* sVt = (uint16_t*)(smem + Lay::oX);
+  uint16_t* sG = (uint16_t*)(smem + Lay::oX);
   float* sKt = (float*)(smem + Lay::oKt);
-  float* sVv = (float*)(smem + Lay::oVv);
   float* sCs = (float*)(smem + Lay::oCs);
   float* sCon = (float*)(smem + Lay::oCon);
   float* sPart = (float*)(smem + Lay::oPart);
@@ -119,6 +125,8 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   float* sA = (float*)(smem + Lay::oA);
   float* sKap = (float*)(smem + Lay::oKap);
   float* sKn = (float*)(smem + Lay::oKn);
+  float* sAG = (float*)(smem + Lay::oAG);
+  float* sGd = (float*)(smem + Lay::oGd);
   int* sFlag = (int*)(smem + Lay::oFlag);
   uint8_t* sFl = (uint8_t*)(smem + Lay::oFl);
   int* XL = (int*)(smem + Lay::oL);        // [0, 32)   prefix cuts (child [0, x))
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     const int pt = wave;                     // probe tile of this wave
     const int q = 16 * pt + i16;             // the lane's probe (scoring layout)
     const bool pok = q < dm.W;
-    __syncthreads();
+    sync_after_lds_stores();                 // meta[9] was stored at the end of the last pass
     const int wi = uni(meta[9]);
     __syncthreads();
     if (wi >= nwork) break;
@@ -222,8 +230,6 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     // ---- staging: token values, probe masses, curvature, probe rows ----
     constexpr int CH = H2 / 8;
     constexpr int IPT = (NMAX * CH + SR_T - 1) / SR_T;   // k° items (token, 8-dim chunk) per thread
-    constexpr int CPR = D / 8;
-    constexpr int VPT = (NMAX / 2) * CPR / SR_T;         // value items (token pair, 8-dim chunk) per thread
     float rv = 0.f, av = 0.f, kv = 0.f;
     uint8_t fl = 0;
     if (tid < n) {
@@ -364,8 +370,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     const int nks = (n + 15) >> 4;           // 16-token k steps
     constexpr int NP = D / 16;               // 16-dim partials per child
     float* sPss = sPart;                     // [SR_CC][NP] ||mean k°||^2 partials
-    float* sPvs = sPart + SR_CC * NP;        // [SR_CC][NP] ||v~||^2 partials
-    float* sTmp = sPart + 2 * SR_CC * NP;    // [SR_CC][8] sum R and sum ||k°|| in three parts each
+    float* sTmp = sPart + SR_CC * NP;        // [SR_CC][12] sums in three parts each
     // lengths of the children (0: no such child)
     if (tid < SR_CC) {
       int nch = 0;
@@ -466,32 +471,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       __syncthreads();
     }
 
-    // ---- value sums: V^T replaces k° ----
-    {
-      uint4 vraw[VPT][2];
-#pragma unroll
-      for (int it = 0; it < VPT; ++it) {             // every load in flight before the first store
-        const int e = tid + SR_T * it;
-        const int grp = e / (8 * CPR), rem = e % (8 * CPR);
-        const int c = rem / 8, t = 2 * (8 * grp + rem % 8);
-        vraw[it][0] = t < n ? *(const uint4*)(Vp + (int64_t)t * D + 8 * c) : make_uint4(0, 0, 0, 0);
-        vraw[it][1] = t + 1 < n ? *(const uint4*)(Vp + (int64_t)(t + 1) * D + 8 * c) : make_uint4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int it = 0; it < VPT; ++it) {
-        const int e = tid + SR_T * it;
-        const int grp = e / (8 * CPR), rem = e % (8 * CPR);
-        const int c = rem / 8, t = 2 * (8 * grp + rem % 8);
-        const uint4 v0 = vraw[it][0], v1 = vraw[it][1];
-        const uint32_t pa[4] = {v0.x, v0.y, v0.z, v0.w}, pb[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          *(uint32_t*)(sVt + (8 * c + 2 * h) * Lay::LDV + t) = (pa[h] & 0xffffu) | (pb[h] << 16);
-          *(uint32_t*)(sVt + (8 * c + 2 * h + 1) * Lay::LDV + t) = (pa[h] >> 16) | (pb[h] & 0xffff0000u);
-        }
-      }
-      if (tid < n) sKn[tid] = sqrtf(sKn[tid]);
-    }
+    if (tid < n) sKn[tid] = sqrtf(sKn[tid]);
     __syncthreads();
     // sum R and sum ||k°|| of every child: wave = child tile; B columns 0-2 hold
     // R in three parts, columns 3-5 ||k°|| in three parts
@@ -515,68 +495,17 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int gr = 16 * ct + 4 * g4 + r;
-        if (gr < SR_CC && i16 < 6) sTmp[gr * 8 + i16] = acc[r];
+        if (gr < SR_CC && i16 < 6) sTmp[gr * 12 + i16] = acc[r];
       }
     }
     __syncthreads();
     if (tid < SR_CC) {
-      const float* x = sTmp + tid * 8;
+      const float* x = sTmp + tid * 12;
       const float nch = crow(0)[tid];
       crow(1)[tid] = x[2] + x[1] + x[0];
       crow(2)[tid] = nch > 0.f ? (x[5] + x[4] + x[3]) / nch : 0.f;
     }
     __syncthreads();
-    // wave = 16-dim value tiles: sum v and sum R v of every child, then v~
-    // (eq:app_value_prototype) and the partial of ||v~||^2 over the tile
-    for (int dt = wave; dt < DT; dt += SR_T / 64) {
-      int clo[CT], chi[CT];
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) row_bounds(ct, clo[ct], chi[ct]);
-      f32x4 av[CT], arv[CT];
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct) { av[ct] = f32x4{0.f, 0.f, 0.f, 0.f}; arv[ct] = av[ct]; }
-      for (int s = 0; s < nks; ++s) {
-        const int t0 = 16 * s + 4 * g4;
-        const uint2 vv = *(const uint2*)(sVt + (16 * dt + i16) * Lay::LDV + t0);
-        u32x2 vb;
-        vb.x = vv.x;
-        vb.y = vv.y;
-        const float4 r4 = *(const float4*)(sR + t0);
-        const float rx[4] = {t0 < n ? r4.x : 0.f, t0 + 1 < n ? r4.y : 0.f, t0 + 2 < n ? r4.z : 0.f,
-                             t0 + 3 < n ? r4.w : 0.f};
-        u32x2 rh, rm, rl;
-        sr_split3(rx, rh, rm, rl);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-          const u32x2 mk = mask16(clo[ct], chi[ct], t0);
-          av[ct] = mfma_bf16_16x16x16(sr_op(one2 & mk), sr_op(vb), av[ct]);
-          arv[ct] = mfma_bf16_16x16x16(sr_op(rl & mk), sr_op(vb), arv[ct]);
-          arv[ct] = mfma_bf16_16x16x16(sr_op(rm & mk), sr_op(vb), arv[ct]);
-          arv[ct] = mfma_bf16_16x16x16(sr_op(rh & mk), sr_op(vb), arv[ct]);
-        }
-      }
-#pragma unroll
-      for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int gr = 16 * ct + 4 * g4 + r;
-          const int grr = gr < SR_CC ? gr : 0;
-          const float nch = crow(0)[grr];
-          float vt = 0.f;
-          if (nch >= 2.f) {
-            const float sr = crow(1)[grr];
-            const float beta = dm.beta_frac * sr * (1.0f / nch);
-            vt = (arv[ct][r] + beta * av[ct][r]) / (sr + nch * beta + dm.eps);
-          }
-          const float ps = row_sum16(vt * vt);
-          if (gr < SR_CC && nch >= 2.f) {
-            sVv[gr * D + 16 * dt + i16] = vt;
-            if (i16 == 0) sPvs[gr * NP + dt] = ps;
-          }
-        }
-    }
-    __syncthreads();
-
     // ---- child keys: coherence, multiplicity (eq:app_effective_multiplicity),
     // k~ = RoPE(mean k°, p) (eq:app_rope_prototype) ----
     // the probe quarter rows of the wave's tile, in flight meanwhile
@@ -594,12 +523,11 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     if (tid < SR_CC) {
       const float nch = crow(0)[tid];
       if (nch >= 2.f) {
-        float ss = 0.f, vs = 0.f;
+        float ss = 0.f;
 #pragma unroll
-        for (int k = 0; k < NP; ++k) { ss += sPss[tid * NP + k]; vs += sPvs[tid * NP + k]; }
+        for (int k = 0; k < NP; ++k) ss += sPss[tid * NP + k];
         const float coh = sqrtf(ss) / (crow(2)[tid] + dm.eps);
         crow(3)[tid] = fminf(fmaxf(nch * coh * coh, 1.0f), nch);
-        crow(5)[tid] = vs;
       }
     }
     {
@@ -636,19 +564,20 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     }
     __syncthreads();
 
-    // the first sweep's first key block (the prefix sweep's, or the suffix
-    // sweep's when there is no prefix child), in flight during the z products
-    uint32_t kcur[QW];
-    {
-      int tr = (nl > 0 ? 0 : 16 * ((n - 1) >> 4)) + i16;
+    // the keys of the first 16-token tile, in flight during the z products
+    const int nt = (n + 15) >> 4;            // 16-token tiles
+    auto kload = [&](int j, uint32_t* dst) {
+      int tr = 16 * j + i16;
       tr = tr < n ? tr : n - 1;
       const uint4* k4 = (const uint4*)(Kp + (int64_t)tr * D + QE * g4);
 #pragma unroll
       for (int h = 0; h < QW / 4; ++h) {
         const uint4 v = k4[h];
-        kcur[4 * h] = v.x; kcur[4 * h + 1] = v.y; kcur[4 * h + 2] = v.z; kcur[4 * h + 3] = v.w;
+        dst[4 * h] = v.x; dst[4 * h + 1] = v.y; dst[4 * h + 2] = v.z; dst[4 * h + 3] = v.w;
       }
-    }
+    };
+    uint32_t kcur[QW];
+    kload(0, kcur);
     // ---- z_{q,c} = m_eff exp(k~_c . q / sqrt(d) - m_q): child rows x probe columns
     // on the matrix cores; lane (i16 = probe, g4) holds children 16 ct + 4 g4 + r ----
     float zreg[CT][4];
@@ -682,139 +611,335 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         }
       }
     }
-
-    // z moves to LDS in the scoring layout [child][probe], over the child key
-    // rows (no longer read once every wave has its z)
-    __syncthreads();
-    float* sZt = sKt;
+    // ---- probe exponentials e_{q,t} = exp(q . k_t / sqrt(d) - m_q) of every token
+    // (transposed logits on the matrix cores): lane (i16 = probe, g4) holds tokens
+    // 16 j + 4 g4 + r of tile j, in fp32 and in three bf16 parts ----
+    const bool probes = 16 * pt < dm.W;
+    u32x2 eh[NTM], em[NTM], el[NTM];
+    if (probes) {
+      const float sc2 = scale * LOG2E;
 #pragma unroll
-    for (int ct = 0; ct < CT; ++ct)
+      for (int j = 0; j < NTM; ++j) {
+        if (j < nt) {
+          uint32_t knext[QW];
+          if (j + 1 < nt) kload(j + 1, knext);
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < QE / 8; ++s)
+            acc = mfma_bf16_16x16x32(pk8(make_uint4(kcur[4 * s], kcur[4 * s + 1], kcur[4 * s + 2], kcur[4 * s + 3])),
+                                     pk8(make_uint4(qreg[4 * s], qreg[4 * s + 1], qreg[4 * s + 2], qreg[4 * s + 3])),
+                                     acc);
+          float ev[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = 16 * j + 4 * g4 + r;
+            ev[r] = (pok && t < n) ? __builtin_amdgcn_exp2f(acc[r] * sc2 - mq2) : 0.f;
+          }
+          sr_split3(ev, eh[j], em[j], el[j]);
+          if (j + 1 < nt) {
+#pragma unroll
+            for (int h = 0; h < QW; ++h) kcur[h] = knext[h];
+          }
+        }
+      }
+    }
+    __syncthreads();                         // the child keys are read: the Gram tiles go over them
+
+    // ---- Gram matrix of the node's values, G = V V^T (the value terms of D_q,
+    // eq:app_node_and_drop_distortion, are quadratic forms in it), in 16 x 16
+    // tiles a >= b: tile a (a + 1) / 2 + b holds G[16 a + i][16 b + j] at lane
+    // i + 16 (j / 4), element j % 4 (the A-operand layout of G[a, b], and read
+    // across, of G[b, a]), as three bf16 planes with G = hi + mid + lo exactly.
+    // bf16 products are exact, so G carries only the fp32 accumulation. ----
+    {
+      const int np = nt * (nt + 1) / 2;
+      for (int k = wave; k < np; k += SR_T / 64) {
+        int a = 0;
+        while ((a + 1) * (a + 2) / 2 <= k) ++a;
+        const int b = k - a * (a + 1) / 2;
+        int ta = 16 * a + i16, tb = 16 * b + i16;
+        ta = ta < n ? ta : n - 1;
+        tb = tb < n ? tb : n - 1;
+        uint4 xa[D / 32], xb[D / 32];
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) {
+          xb[s] = *(const uint4*)(Vp + (int64_t)tb * D + 32 * s + 8 * g4);
+          xa[s] = *(const uint4*)(Vp + (int64_t)ta * D + 32 * s + 8 * g4);
+        }
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) acc = mfma_bf16_16x16x32(pk8(xb[s]), pk8(xa[s]), acc);
+        // C[i][j] = v_{16b+i} . v_{16a+j}: lane (i16, g4) holds G[16a + i16][16b + 4 g4 + r]
+        const float x[4] = {acc[0], acc[1], acc[2], acc[3]};
+        if (a == b && g4 == (i16 >> 2)) {
+          const int rr = i16 & 3;
+          sGd[16 * a + i16] = rr == 0 ? x[0] : (rr == 1 ? x[1] : (rr == 2 ? x[2] : x[3]));
+        }
+        u32x2 h, m, lo;
+        sr_split3(x, h, m, lo);
+        u32x2* dst = (u32x2*)(sG + (size_t)k * 768);
+        dst[lane] = h;
+        dst[64 + lane] = m;
+        dst[128 + lane] = lo;
+      }
+    }
+    // A operand of G[i, j] (rows: tokens of tile i, k: tokens of tile j)
+    auto gread = [&](int i, int j, u32x2& h, u32x2& m, u32x2& lo) {
+      if (j <= i) {
+        const u32x2* src = (const u32x2*)(sG + (size_t)(i * (i + 1) / 2 + j) * 768);
+        h = src[lane];
+        m = src[64 + lane];
+        lo = src[128 + lane];
+      } else {
+        // G[i, j] = G[j, i]^T: element (i16, 4 g4 + r) is element (4 g4 + r, i16) of tile (j, i)
+        const uint16_t* src = sG + (size_t)(j * (j + 1) / 2 + i) * 768 + 16 * g4 + 64 * (i16 >> 2) + (i16 & 3);
+        u32x2 v[3];
+#pragma unroll
+        for (int p3 = 0; p3 < 3; ++p3) {
+          const uint16_t* pp = src + 256 * p3;
+          v[p3].x = (uint32_t)pp[0] | ((uint32_t)pp[4] << 16);
+          v[p3].y = (uint32_t)pp[8] | ((uint32_t)pp[12] << 16);
+        }
+        h = v[0];
+        m = v[1];
+        lo = v[2];
+      }
+    };
+    // strictly lower (k < row) and strictly upper (k > row) parts of a diagonal tile
+    u32x2 mlo, mup;
+    {
+      uint32_t a4[4], b4[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int gr = 16 * ct + 4 * g4 + r;
-        if (gr < SR_CC) sZt[gr * WMAX + q] = zreg[ct][r];
+        a4[r] = 4 * g4 + r < i16 ? 0xffffu : 0u;
+        b4[r] = 4 * g4 + r > i16 ? 0xffffu : 0u;
       }
-    // ---- distortion sweeps: prefix children left to right, suffix children right to left ----
-    // The sweep walks 16-token blocks; a block's probe exponentials and value
-    // operands are formed once, then the pieces between the cuts inside it
-    // are accumulated and each child is scored at its cut.
-    if (16 * pt < dm.W) {
-      const float sc2 = scale * LOG2E;
-      for (int dir = 0; dir < 2; ++dir) {
-        const bool prefix = dir == 0;
-        const int nx = prefix ? nl : nr;
-        if (nx == 0) continue;
-        f32x4 M[DT];
+      mlo.x = a4[0] | (a4[1] << 16); mlo.y = a4[2] | (a4[3] << 16);
+      mup.x = b4[0] | (b4[1] << 16); mup.y = b4[2] | (b4[3] << 16);
+    }
+    __syncthreads();
+    // ---- rows of G against R and 1: a_t = sum G_{t t'} R_t', g_t = sum G_{t t'} over
+    // t' < t (lower) and t' > t (upper); wave = token tiles i = wave mod 4.  B
+    // columns: R in three bf16 parts, 1 (zero past the node) ----
+    for (int i = wave; i < nt; i += SR_T / 64) {
+      f32x4 clo = {0.f, 0.f, 0.f, 0.f}, cup = {0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < nt; ++j) {
+        const int t0 = 16 * j + 4 * g4;
+        float rx[4];
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) M[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        float Z = 0.f;
-        int ci = prefix ? 0 : nx - 1;            // next cut (scalar)
-        int cur = prefix ? 0 : n;                // tokens between 0 and cur (prefix) or cur and n (suffix) are in M
-        for (int blk = prefix ? 0 : ((n - 1) >> 4); ; blk += prefix ? 1 : -1) {
-          const int B0 = 16 * blk, B1 = min(B0 + 16, n);
-          // the next key block in flight: the next block of this direction, or,
-          // when every remaining cut lies in this block, the suffix sweep's first
-          uint32_t knext[QW];
-          {
-            const bool last = prefix ? uni(XL[nx - 1]) <= B1 : uni(XR[0]) >= B0;
-            const int nb2 = last ? (prefix ? ((n - 1) >> 4) : 0) : blk + (prefix ? 1 : -1);
-            int tr = 16 * nb2 + i16;
-            tr = tr < n ? tr : n - 1;
-            const uint4* k4 = (const uint4*)(Kp + (int64_t)tr * D + QE * g4);
+        for (int r = 0; r < 4; ++r) rx[r] = t0 + r < n ? sR[t0 + r] : 0.f;
+        u32x2 rh, rm, rl;
+        sr_split3(rx, rh, rm, rl);
+        const u32x2 z2 = {0u, 0u};
+        const u32x2 bop = i16 == 0 ? rh : (i16 == 1 ? rm : (i16 == 2 ? rl : (i16 == 3 ? (one2 & mask16(0, n, t0)) : z2)));
+        u32x2 gh, gm, gl;
+        gread(i, j, gh, gm, gl);
+        if (j <= i) {
+          const u32x2 mk = j == i ? mlo : u32x2{0xffffffffu, 0xffffffffu};
+          clo = mfma_bf16_16x16x16(sr_op(gl & mk), sr_op(bop), clo);
+          clo = mfma_bf16_16x16x16(sr_op(gm & mk), sr_op(bop), clo);
+          clo = mfma_bf16_16x16x16(sr_op(gh & mk), sr_op(bop), clo);
+        }
+        if (j >= i) {
+          const u32x2 mk = j == i ? mup : u32x2{0xffffffffu, 0xffffffffu};
+          cup = mfma_bf16_16x16x16(sr_op(gl & mk), sr_op(bop), cup);
+          cup = mfma_bf16_16x16x16(sr_op(gm & mk), sr_op(bop), cup);
+          cup = mfma_bf16_16x16x16(sr_op(gh & mk), sr_op(bop), cup);
+        }
+      }
+      // lane (column i16, g4) holds token 16 i + 4 g4 + r; a = columns 0 + 1 + 2, g = column 3
 #pragma unroll
-            for (int h = 0; h < QW / 4; ++h) {
-              const uint4 v = k4[h];
-              knext[4 * h] = v.x; knext[4 * h + 1] = v.y; knext[4 * h + 2] = v.z; knext[4 * h + 3] = v.w;
-            }
+      for (int r = 0; r < 4; ++r) {
+        const float l1 = __shfl_down(clo[r], 1, 16), l2 = __shfl_down(clo[r], 2, 16);
+        const float u1 = __shfl_down(cup[r], 1, 16), u2 = __shfl_down(cup[r], 2, 16);
+        const int t = 16 * i + 4 * g4 + r;
+        if (i16 == 0) {
+          sAG[t] = (clo[r] + l1) + l2;
+          sAG[2 * NMAX + t] = (cup[r] + u1) + u2;
+        }
+        if (i16 == 3) {
+          sAG[NMAX + t] = clo[r];
+          sAG[3 * NMAX + t] = cup[r];
+        }
+      }
+    }
+    __syncthreads();
+    // ---- ||v~||^2 of every child (eq:app_value_prototype): with w_t = R_t + beta,
+    // ||sum w_t v_t||^2 = RR + 2 beta RG + beta^2 GG, RR = sum R_t R_t' G_tt',
+    // RG = sum R_t G_tt', GG = sum G_tt' over the child's tokens; each is the sum
+    // of per-token increments over the child (prefix children: lower rows,
+    // suffix children: upper rows), summed on the matrix cores with the child
+    // masks.  Wave 0 takes the prefix children, wave 1 the suffix children. ----
+    if (wave < 2) {
+      const int dir = wave;
+      const float* av = sAG + 2 * dir * NMAX;
+      const float* gv = av + NMAX;
+      int cl0, ch0, cl1, ch1;
+      row_bounds(dir, cl0, ch0);
+      row_bounds(dir + 1, cl1, ch1);
+      f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+      const int qi = i16 / 3, part = i16 - 3 * qi;   // B column i16: quantity qi, part
+      for (int j = 0; j < nt; ++j) {
+        const int t0 = 16 * j + 4 * g4;
+        float x[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = t0 + r;
+          float v = 0.f;
+          if (t < n) {
+            const float R = sR[t], a = av[t], gg = gv[t], gd = sGd[t];
+            v = qi == 0 ? R * (2.f * a + gd * R) : (qi == 1 ? (R * gg + a) + R * gd : 2.f * gg + gd);
           }
-          // e_{q,t} of the block: transposed logits, lane holds tokens B0 + 4 g4 + r
-          float ev[4];
-          {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+          x[r] = v;
+        }
+        u32x2 h, m, lo;
+        sr_split3(x, h, m, lo);
+        u32x2 bop = part == 0 ? h : (part == 1 ? m : lo);
+        if (i16 >= 9) bop = u32x2{0u, 0u};
+        c0 = mfma_bf16_16x16x16(sr_op(one2 & mask16(cl0, ch0, t0)), sr_op(bop), c0);
+        c1 = mfma_bf16_16x16x16(sr_op(one2 & mask16(cl1, ch1, t0)), sr_op(bop), c1);
+      }
+      // lane (column i16, g4) holds child rows 16 (dir + c) + 4 g4 + r
 #pragma unroll
-            for (int s = 0; s < QE / 8; ++s)
-              acc = mfma_bf16_16x16x32(pk8(make_uint4(kcur[4 * s], kcur[4 * s + 1], kcur[4 * s + 2], kcur[4 * s + 3])),
-                                       pk8(make_uint4(qreg[4 * s], qreg[4 * s + 1], qreg[4 * s + 2], qreg[4 * s + 3])),
-                                       acc);
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int gr = 16 * (dir + c) + 4 * g4 + r;
+          const bool mine = dir == 0 ? gr < SR_CM : (gr >= SR_CM && gr < SR_CC);
+          if (mine && i16 < 9) sTmp[gr * 12 + i16] = c ? c1[r] : c0[r];
+        }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      if (lane < SR_CM) {
+        const int gc = dir * SR_CM + lane;
+        const float nch = crow(0)[gc];
+        if (nch >= 2.f) {
+          const float* v = sTmp + gc * 12;
+          const float RR = (v[2] + v[1]) + v[0], RG = (v[5] + v[4]) + v[3], GG = (v[8] + v[7]) + v[6];
+          const float sr = crow(1)[gc];
+          const float beta = dm.beta_frac * sr * (1.0f / nch);
+          const float iden = 1.0f / (sr + nch * beta + dm.eps);
+          crow(5)[gc] = (RR + beta * (2.f * RG + beta * GG)) * (iden * iden);
+          crow(6)[gc] = beta;
+          crow(7)[gc] = iden;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- distortions of every child and probe (eq:app_node_and_drop_distortion).
+    // With Y_t = sum G_tt' e_t' over t' < t (prefix children) or t' > t (suffix
+    // children), the sums over a child of the increments
+    //   e_t (Z), e_t (Y_t + u_t) (||M||^2), R_t u_t + e_t a_t and u_t + e_t g_t
+    //   (<M, sum R v> and <M, sum v>), u_t = Y_t + e_t G_tt,
+    // give Z_q, ||M_q||^2 and <M_q, v~> exactly as the sums over the child's token
+    // pairs; the sums over each child are taken on the matrix cores with the
+    // child masks (fp32 increments in three bf16 parts: exact products).  Y
+    // comes from the Gram tiles and e (both in three parts; the three part
+    // products below 2^-24 of |G e| are left out). ----
+    if (probes) {
+#pragma unroll 1
+      for (int dir = 0; dir < 2; ++dir) {
+        const float* av = sAG + 2 * dir * NMAX;
+        const float* gv = av + NMAX;
+        const u32x2 dmk = dir == 0 ? mlo : mup;
+        int cl[2], ch[2];
+        row_bounds(dir, cl[0], ch[0]);
+        row_bounds(dir + 1, cl[1], ch[1]);
+        f32x4 aZ[2], aS[2], aP[2], aQ[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          aZ[c] = f32x4{0.f, 0.f, 0.f, 0.f}; aS[c] = aZ[c]; aP[c] = aZ[c]; aQ[c] = aZ[c];
+        }
+#pragma unroll
+        for (int i = 0; i < NTM; ++i) {
+          if (i < nt) {
+            f32x4 Y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int j = 0; j < NTM; ++j) {
+              const bool use = j < nt && (j == i || (j < i ? dir == 0 : dir == 1));
+              if (use) {
+                // one tile pair at a time (hoisted operand reads would not fit the register budget)
+                __builtin_amdgcn_sched_barrier(0);
+                u32x2 gh, gm, gl;
+                gread(i, j, gh, gm, gl);
+                if (j == i) { gh = gh & dmk; gm = gm & dmk; gl = gl & dmk; }
+                Y = mfma_bf16_16x16x16(sr_op(gl), sr_op(eh[j]), Y);
+                Y = mfma_bf16_16x16x16(sr_op(gm), sr_op(em[j]), Y);
+                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(el[j]), Y);
+                Y = mfma_bf16_16x16x16(sr_op(gm), sr_op(eh[j]), Y);
+                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(em[j]), Y);
+                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(eh[j]), Y);
+              }
+            }
+            const int t0 = 16 * i + 4 * g4;
+            const float4 R4 = *(const float4*)(sR + t0), A4 = *(const float4*)(av + t0);
+            const float4 G4 = *(const float4*)(gv + t0), D4 = *(const float4*)(sGd + t0);
+            const float Rv[4] = {R4.x, R4.y, R4.z, R4.w}, Av[4] = {A4.x, A4.y, A4.z, A4.w};
+            const float Gv[4] = {G4.x, G4.y, G4.z, G4.w}, Dg[4] = {D4.x, D4.y, D4.z, D4.w};
+            // e_t = hi + mid + lo exactly
+            float ev[4];
+            {
+              const uint32_t hv[4] = {eh[i].x << 16, eh[i].x & 0xffff0000u, eh[i].y << 16, eh[i].y & 0xffff0000u};
+              const uint32_t mv[4] = {em[i].x << 16, em[i].x & 0xffff0000u, em[i].y << 16, em[i].y & 0xffff0000u};
+              const uint32_t lv[4] = {el[i].x << 16, el[i].x & 0xffff0000u, el[i].y << 16, el[i].y & 0xffff0000u};
+#pragma unroll
+              for (int r = 0; r < 4; ++r) ev[r] = (__uint_as_float(hv[r]) + __uint_as_float(mv[r])) + __uint_as_float(lv[r]);
+            }
+            float xS[4], xP[4], xQ[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int t = B0 + 4 * g4 + r;
-              ev[r] = (pok && t < n) ? __builtin_amdgcn_exp2f(acc[r] * sc2 - mq2) : 0.f;
+              const bool ok = t0 + r < n;
+              const float e = ev[r];
+              const float u = Y[r] + e * Dg[r];
+              xS[r] = ok ? e * (Y[r] + u) : 0.f;
+              xP[r] = ok ? Rv[r] * u + e * Av[r] : 0.f;
+              xQ[r] = ok ? u + e * Gv[r] : 0.f;
+            }
+            u32x2 sh, sm, sl, ph, pm, pl, qh, qm, ql;
+            sr_split3(xS, sh, sm, sl);
+            sr_split3(xP, ph, pm, pl);
+            sr_split3(xQ, qh, qm, ql);
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+              const s16x4 mk = sr_op(one2 & mask16(cl[c], ch[c], t0));
+              aZ[c] = mfma_bf16_16x16x16(mk, sr_op(el[i]), aZ[c]);
+              aZ[c] = mfma_bf16_16x16x16(mk, sr_op(em[i]), aZ[c]);
+              aZ[c] = mfma_bf16_16x16x16(mk, sr_op(eh[i]), aZ[c]);
+              aS[c] = mfma_bf16_16x16x16(mk, sr_op(sl), aS[c]);
+              aS[c] = mfma_bf16_16x16x16(mk, sr_op(sm), aS[c]);
+              aS[c] = mfma_bf16_16x16x16(mk, sr_op(sh), aS[c]);
+              aP[c] = mfma_bf16_16x16x16(mk, sr_op(pl), aP[c]);
+              aP[c] = mfma_bf16_16x16x16(mk, sr_op(pm), aP[c]);
+              aP[c] = mfma_bf16_16x16x16(mk, sr_op(ph), aP[c]);
+              aQ[c] = mfma_bf16_16x16x16(mk, sr_op(ql), aQ[c]);
+              aQ[c] = mfma_bf16_16x16x16(mk, sr_op(qm), aQ[c]);
+              aQ[c] = mfma_bf16_16x16x16(mk, sr_op(qh), aQ[c]);
             }
           }
-#pragma unroll
-          for (int h = 0; h < QW; ++h) kcur[h] = knext[h];
-          u32x2 eh, em, el;
-          sr_split3(ev, eh, em, el);
-          u32x2 vop[DT];
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-            const uint2 vv = *(const uint2*)(sVt + (16 * dt + i16) * Lay::LDV + B0 + 4 * g4);
-            vop[dt].x = vv.x;
-            vop[dt].y = vv.y;
-          }
-          const int t0 = B0 + 4 * g4;
-          bool more = true;
-          for (;;) {
-            const int x = uni(prefix ? XL[ci] : XR[ci]);
-            const bool inblk = prefix ? (x <= B1) : (x >= B0);
-            const int pend = inblk ? x : (prefix ? B1 : B0);
-            const int lo = prefix ? cur : pend, hi = prefix ? pend : cur;
-            if (hi > lo) {                       // the piece [lo, hi) of this block
-              bool in[4];
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                in[r] = (unsigned)(t0 + r - lo) < (unsigned)(hi - lo);
-                Z += in[r] ? ev[r] : 0.f;
-              }
-              u32x2 mk;
-              mk.x = (in[0] ? 0xffffu : 0u) | (in[1] ? 0xffff0000u : 0u);
-              mk.y = (in[2] ? 0xffffu : 0u) | (in[3] ? 0xffff0000u : 0u);
-              const s16x4 ph = sr_op(eh & mk), pm = sr_op(em & mk), pl = sr_op(el & mk);
-#pragma unroll
-              for (int dt = 0; dt < DT; ++dt) {
-                const s16x4 va = sr_op(vop[dt]);
-                M[dt] = mfma_bf16_16x16x16(va, pl, M[dt]);
-                M[dt] = mfma_bf16_16x16x16(va, pm, M[dt]);
-                M[dt] = mfma_bf16_16x16x16(va, ph, M[dt]);
-              }
-            }
-            cur = pend;
-            if (!inblk) break;
-            // child gc at cut x: z of the lane's probe from the lane holding row gc % 16
-            const int gc = prefix ? ci : SR_CM + ci;
-            const int nch = prefix ? x : n - x;
-            if (nch >= 2) {
-              const float z = sZt[gc * WMAX + q];
-              // ||M - z v~||^2 = ||M||^2 - 2 z <M, v~> + z^2 ||v~||^2
-              float s2a = 0.f, s2b = 0.f, xva = 0.f, xvb = 0.f;
-              const float* vv = sVv + gc * D + 4 * g4;
-#pragma unroll
-              for (int dt = 0; dt < DT; ++dt) {
-                const float4 v4 = *(const float4*)(vv + 16 * dt);
-                const float vt[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                  const float Mv = M[dt][r];
-                  if (dt & 1) { s2b += Mv * Mv; xvb += Mv * vt[r]; }
-                  else { s2a += Mv * Mv; xva += Mv * vt[r]; }
-                }
-              }
-              const float s2 = col_sum4(s2a + s2b);
-              const float xv = col_sum4(xva + xvb);
-              const float Zs = col_sum4(Z);
-              const float s1 = fmaxf(s2 - 2.f * z * xv + z * z * crow(5)[gc], 0.f);
-              const float dz = Zs - z;
-              const float Dq = dm.lam_Z * dz * dz * __builtin_amdgcn_rcpf(Zs * Zs + dm.eps) +
-                               dm.lam_M * s1 * __builtin_amdgcn_rcpf(s2 + dm.eps);
-              const float con = row_sum16((g4 == 0 && pok) ? (Zs * izc) * Dq : 0.f);
-              if (lane == 0) sCon[gc * 4 + pt] = con;
-            }
-            ci += prefix ? 1 : -1;
-            if (prefix ? ci >= nx : ci < 0) { more = false; break; }
-          }
-          if (!more) break;
         }
+        // lane (probe i16, g4) holds children 16 (dir + c) + 4 g4 + r:
+        // ||M - z v~||^2 = ||M||^2 - 2 z <M, v~> + z^2 ||v~||^2 (clamped at 0)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int ct = dir + c;
+            const int gr = 16 * ct + 4 * g4 + r;
+            const bool live = dir == 0 ? gr < nl : (gr >= SR_CM && gr - SR_CM < nr);
+            const int grr = live ? gr : 0;
+            const bool sc = live && crow(0)[grr] >= 2.f;
+            const float z = ct == 0 ? zreg[0][r] : (ct == 1 ? zreg[1][r] : zreg[CT - 1][r]);
+            const float Zs = aZ[c][r], s2 = aS[c][r];
+            const float xv = (aP[c][r] + crow(6)[grr] * aQ[c][r]) * crow(7)[grr];
+            const float s1 = fmaxf(s2 - 2.f * z * xv + z * z * crow(5)[grr], 0.f);
+            const float dz = Zs - z;
+            const float Dq = dm.lam_Z * dz * dz * __builtin_amdgcn_rcpf(Zs * Zs + dm.eps) +
+                             dm.lam_M * s1 * __builtin_amdgcn_rcpf(s2 + dm.eps);
+            const float con = row_sum16((sc && pok) ? (Zs * izc) * Dq : 0.f);
+            if (sc && i16 == 0) sCon[gr * 4 + pt] = con;
+          }
       }
     }
     __syncthreads();
