@@ -63,7 +63,9 @@ struct SrLds {
   static constexpr int oPart = oCon + SR_CC * 4 * 4;      // [SR_CC][D/16] partial norms, [SR_CC][12] sums
   static constexpr int oAG = oPart + ((D / 16) + 12) * SR_CC * 4;   // [4][NMAX] rows of G against R and 1
   static constexpr int oGd = oAG + 4 * NMAX * 4;          // [NMAX] G_tt
-  static constexpr int oR = oGd + NMAX * 4;               // [NMAX] R_t
+  static constexpr int oLo = oGd + NMAX * 4;              // [Gram tiles][16] lower partial rows (R, 1)
+  static constexpr int oUp = oLo + NTM * (NTM + 1) / 2 * 16 * 8;   // [Gram tiles][16] upper partials
+  static constexpr int oR = oUp + NTM * (NTM + 1) / 2 * 16 * 8;    // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                // [NMAX] probe mass A_t
   static constexpr int oKap = oA + NMAX * 4;              // [NMAX] kappa_t
   static constexpr int oKn = oKap + NMAX * 4;             // [NMAX] ||k°_t||^2, then ||k°_t||
@@ -127,6 +129,8 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   float* sKn = (float*)(smem + Lay::oKn);
   float* sAG = (float*)(smem + Lay::oAG);
   float* sGd = (float*)(smem + Lay::oGd);
+  float2* sLo = (float2*)(smem + Lay::oLo);
+  float2* sUp = (float2*)(smem + Lay::oUp);
   int* sFlag = (int*)(smem + Lay::oFlag);
   uint8_t* sFl = (uint8_t*)(smem + Lay::oFl);
   int* XL = (int*)(smem + Lay::oL);        // [0, 32)   prefix cuts (child [0, x))
@@ -578,6 +582,25 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     };
     uint32_t kcur[QW];
     kload(0, kcur);
+    const int np = nt * (nt + 1) / 2;        // Gram tiles
+    auto tile_ab = [&](int k, int& a, int& b) {
+      a = 0;
+      while ((a + 1) * (a + 2) / 2 <= k) ++a;
+      b = k - a * (a + 1) / 2;
+    };
+    auto vload = [&](int k, uint4* xa, uint4* xb) {
+      int a, b;
+      tile_ab(k, a, b);
+      int ta = 16 * a + i16, tb = 16 * b + i16;
+      ta = ta < n ? ta : n - 1;
+      tb = tb < n ? tb : n - 1;
+#pragma unroll
+      for (int s = 0; s < D / 32; ++s) {
+        xb[s] = *(const uint4*)(Vp + (int64_t)tb * D + 32 * s + 8 * g4);
+        xa[s] = *(const uint4*)(Vp + (int64_t)ta * D + 32 * s + 8 * g4);
+      }
+    };
+
     // ---- z_{q,c} = m_eff exp(k~_c . q / sqrt(d) - m_q): child rows x probe columns
     // on the matrix cores; lane (i16 = probe, g4) holds children 16 ct + 4 g4 + r ----
     float zreg[CT][4];
@@ -640,9 +663,25 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
             for (int h = 0; h < QW; ++h) kcur[h] = knext[h];
           }
+        } else {
+          // defined on every path: an undefined value would be carried from
+          // item to item, and kept in registers across the whole loop
+          eh[j] = u32x2{0u, 0u};
+          em[j] = eh[j];
+          el[j] = eh[j];
         }
       }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NTM; ++j) {
+        eh[j] = u32x2{0u, 0u};
+        em[j] = eh[j];
+        el[j] = eh[j];
+      }
     }
+    // the values of the wave's first Gram tile pair, in flight during the barrier
+    uint4 va[D / 32], vb[D / 32];
+    vload(wave < np ? wave : 0, va, vb);
     __syncthreads();                         // the child keys are read: the Gram tiles go over them
 
     // ---- Gram matrix of the node's values, G = V V^T (the value terms of D_q,
@@ -650,30 +689,52 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     // tiles a >= b: tile a (a + 1) / 2 + b holds G[16 a + i][16 b + j] at lane
     // i + 16 (j / 4), element j % 4 (the A-operand layout of G[a, b], and read
     // across, of G[b, a]), as three bf16 planes with G = hi + mid + lo exactly.
-    // bf16 products are exact, so G carries only the fp32 accumulation. ----
+    // bf16 products are exact, so G carries only the fp32 accumulation.  With
+    // each tile, the partial rows of G against R and 1 over t' < t: for the
+    // rows t of tile a, sum over the columns t' of tile b (lower), and for the
+    // columns t' of tile b, sum over the rows t of tile a (upper); tokens past
+    // the node count as zero. ----
     {
-      const int np = nt * (nt + 1) / 2;
       for (int k = wave; k < np; k += SR_T / 64) {
-        int a = 0;
-        while ((a + 1) * (a + 2) / 2 <= k) ++a;
-        const int b = k - a * (a + 1) / 2;
-        int ta = 16 * a + i16, tb = 16 * b + i16;
-        ta = ta < n ? ta : n - 1;
-        tb = tb < n ? tb : n - 1;
-        uint4 xa[D / 32], xb[D / 32];
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-          xb[s] = *(const uint4*)(Vp + (int64_t)tb * D + 32 * s + 8 * g4);
-          xa[s] = *(const uint4*)(Vp + (int64_t)ta * D + 32 * s + 8 * g4);
-        }
+        int a, b;
+        tile_ab(k, a, b);
+        // the next tile's values in flight (the last pass reloads its own: no
+        // value is left undefined on any path)
+        uint4 na[D / 32], nb[D / 32];
+        vload(k + SR_T / 64 < np ? k + SR_T / 64 : k, na, nb);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) acc = mfma_bf16_16x16x32(pk8(xb[s]), pk8(xa[s]), acc);
+        for (int s = 0; s < D / 32; ++s) acc = mfma_bf16_16x16x32(pk8(vb[s]), pk8(va[s]), acc);
         // C[i][j] = v_{16b+i} . v_{16a+j}: lane (i16, g4) holds G[16a + i16][16b + 4 g4 + r]
         const float x[4] = {acc[0], acc[1], acc[2], acc[3]};
         if (a == b && g4 == (i16 >> 2)) {
           const int rr = i16 & 3;
           sGd[16 * a + i16] = rr == 0 ? x[0] : (rr == 1 ? x[1] : (rr == 2 ? x[2] : x[3]));
+        }
+        const int tr = 16 * a + i16, tc0 = 16 * b + 4 * g4;
+        const float Rrow = tr < n ? sR[tr] : 0.f;
+        float la = 0.f, lg = 0.f, ua[4], ug[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool keep = tc0 + r < tr && tr < n;       // t' < t < n
+          const float gv = keep ? x[r] : 0.f;
+          const float Rc = keep ? sR[tc0 + r] : 0.f;
+          la = fmaf(gv, Rc, la);
+          lg += gv;
+          ua[r] = gv * Rrow;
+          ug[r] = gv;
+        }
+        la = col_sum4(la);
+        lg = col_sum4(lg);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          ua[r] = row_sum16(ua[r]);
+          ug[r] = row_sum16(ug[r]);
+        }
+        if (g4 == 0) sLo[16 * k + i16] = make_float2(la, lg);
+        if (i16 == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sUp[16 * k + 4 * g4 + r] = make_float2(ua[r], ug[r]);
         }
         u32x2 h, m, lo;
         sr_split3(x, h, m, lo);
@@ -681,6 +742,8 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         dst[lane] = h;
         dst[64 + lane] = m;
         dst[128 + lane] = lo;
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) { va[s] = na[s]; vb[s] = nb[s]; }
       }
     }
     // A operand of G[i, j] (rows: tokens of tile i, k: tokens of tile j)
@@ -718,112 +781,86 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       mup.x = b4[0] | (b4[1] << 16); mup.y = b4[2] | (b4[3] << 16);
     }
     __syncthreads();
-    // ---- rows of G against R and 1: a_t = sum G_{t t'} R_t', g_t = sum G_{t t'} over
-    // t' < t (lower) and t' > t (upper); wave = token tiles i = wave mod 4.  B
-    // columns: R in three bf16 parts, 1 (zero past the node) ----
-    for (int i = wave; i < nt; i += SR_T / 64) {
-      f32x4 clo = {0.f, 0.f, 0.f, 0.f}, cup = {0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < nt; ++j) {
-        const int t0 = 16 * j + 4 * g4;
-        float rx[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) rx[r] = t0 + r < n ? sR[t0 + r] : 0.f;
-        u32x2 rh, rm, rl;
-        sr_split3(rx, rh, rm, rl);
-        const u32x2 z2 = {0u, 0u};
-        const u32x2 bop = i16 == 0 ? rh : (i16 == 1 ? rm : (i16 == 2 ? rl : (i16 == 3 ? (one2 & mask16(0, n, t0)) : z2)));
-        u32x2 gh, gm, gl;
-        gread(i, j, gh, gm, gl);
-        if (j <= i) {
-          const u32x2 mk = j == i ? mlo : u32x2{0xffffffffu, 0xffffffffu};
-          clo = mfma_bf16_16x16x16(sr_op(gl & mk), sr_op(bop), clo);
-          clo = mfma_bf16_16x16x16(sr_op(gm & mk), sr_op(bop), clo);
-          clo = mfma_bf16_16x16x16(sr_op(gh & mk), sr_op(bop), clo);
-        }
-        if (j >= i) {
-          const u32x2 mk = j == i ? mup : u32x2{0xffffffffu, 0xffffffffu};
-          cup = mfma_bf16_16x16x16(sr_op(gl & mk), sr_op(bop), cup);
-          cup = mfma_bf16_16x16x16(sr_op(gm & mk), sr_op(bop), cup);
-          cup = mfma_bf16_16x16x16(sr_op(gh & mk), sr_op(bop), cup);
-        }
-      }
-      // lane (column i16, g4) holds token 16 i + 4 g4 + r; a = columns 0 + 1 + 2, g = column 3
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float l1 = __shfl_down(clo[r], 1, 16), l2 = __shfl_down(clo[r], 2, 16);
-        const float u1 = __shfl_down(cup[r], 1, 16), u2 = __shfl_down(cup[r], 2, 16);
-        const int t = 16 * i + 4 * g4 + r;
-        if (i16 == 0) {
-          sAG[t] = (clo[r] + l1) + l2;
-          sAG[2 * NMAX + t] = (cup[r] + u1) + u2;
-        }
-        if (i16 == 3) {
-          sAG[NMAX + t] = clo[r];
-          sAG[3 * NMAX + t] = cup[r];
-        }
-      }
-    }
-    __syncthreads();
-    // ---- ||v~||^2 of every child (eq:app_value_prototype): with w_t = R_t + beta,
-    // ||sum w_t v_t||^2 = RR + 2 beta RG + beta^2 GG, RR = sum R_t R_t' G_tt',
-    // RG = sum R_t G_tt', GG = sum G_tt' over the child's tokens; each is the sum
-    // of per-token increments over the child (prefix children: lower rows,
-    // suffix children: upper rows), summed on the matrix cores with the child
-    // masks.  Wave 0 takes the prefix children, wave 1 the suffix children. ----
+    // ---- per token, a_t = sum G_tt' R_t' and g_t = sum G_tt' over t' < t (wave 0)
+    // or t' > t (wave 1), summed from the partials in a fixed order; then
+    // ||v~||^2 of every child (eq:app_value_prototype): with w_t = R_t + beta,
+    // ||sum w_t v_t||^2 = RR + 2 beta RG + beta^2 GG with RR = sum R_t R_t' G_tt',
+    // RG = sum R_t G_tt', GG = sum G_tt' over the child's token pairs, each the
+    // sum over the child of a per-token increment (prefix children: lower rows
+    // and a prefix scan, wave 0; suffix children: upper rows and a suffix scan,
+    // wave 1); two tokens per lane. ----
     if (wave < 2) {
       const int dir = wave;
-      const float* av = sAG + 2 * dir * NMAX;
-      const float* gv = av + NMAX;
-      int cl0, ch0, cl1, ch1;
-      row_bounds(dir, cl0, ch0);
-      row_bounds(dir + 1, cl1, ch1);
-      f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
-      const int qi = i16 / 3, part = i16 - 3 * qi;   // B column i16: quantity qi, part
-      for (int j = 0; j < nt; ++j) {
-        const int t0 = 16 * j + 4 * g4;
-        float x[4];
+      float x0[3], x1[3];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = t0 + r;
-          float v = 0.f;
-          if (t < n) {
-            const float R = sR[t], a = av[t], gg = gv[t], gd = sGd[t];
-            v = qi == 0 ? R * (2.f * a + gd * R) : (qi == 1 ? (R * gg + a) + R * gd : 2.f * gg + gd);
+      for (int e2 = 0; e2 < 2; ++e2) {
+        const int t = 2 * lane + e2;
+        const int a = t >> 4, i = t & 15;
+        float av = 0.f, gv = 0.f;
+        if (a < nt) {
+          if (dir == 0) {
+            for (int b = 0; b <= a; ++b) {
+              const float2 p2 = sLo[16 * (a * (a + 1) / 2 + b) + i];
+              av += p2.x;
+              gv += p2.y;
+            }
+          } else {
+            for (int a2 = a; a2 < nt; ++a2) {
+              const float2 p2 = sUp[16 * (a2 * (a2 + 1) / 2 + a) + i];
+              av += p2.x;
+              gv += p2.y;
+            }
           }
-          x[r] = v;
+          sAG[2 * dir * NMAX + t] = av;
+          sAG[(2 * dir + 1) * NMAX + t] = gv;
         }
-        u32x2 h, m, lo;
-        sr_split3(x, h, m, lo);
-        u32x2 bop = part == 0 ? h : (part == 1 ? m : lo);
-        if (i16 >= 9) bop = u32x2{0u, 0u};
-        c0 = mfma_bf16_16x16x16(sr_op(one2 & mask16(cl0, ch0, t0)), sr_op(bop), c0);
-        c1 = mfma_bf16_16x16x16(sr_op(one2 & mask16(cl1, ch1, t0)), sr_op(bop), c1);
+        float q0 = 0.f, q1 = 0.f, q2 = 0.f;
+        if (t < n) {
+          const float R = sR[t], gd = sGd[t];
+          q0 = R * (2.f * av + gd * R);
+          q1 = (R * gv + av) + R * gd;
+          q2 = 2.f * gv + gd;
+        }
+        float* xs = e2 ? x1 : x0;
+        xs[0] = q0; xs[1] = q1; xs[2] = q2;
       }
-      // lane (column i16, g4) holds child rows 16 (dir + c) + 4 g4 + r
+      // inclusive prefix sums over t (wave 0) or suffix sums (wave 1) at both tokens of the lane
+      float s0[3], s1[3];
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int qq = 0; qq < 3; ++qq) {
+        const float tot = x0[qq] + x1[qq];
+        float sc = tot;                      // scan of the lane totals, lanes before (after) this one
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int gr = 16 * (dir + c) + 4 * g4 + r;
-          const bool mine = dir == 0 ? gr < SR_CM : (gr >= SR_CM && gr < SR_CC);
-          if (mine && i16 < 9) sTmp[gr * 12 + i16] = c ? c1[r] : c0[r];
+        for (int off = 1; off < 64; off <<= 1) {
+          const float y = dir == 0 ? __shfl_up(sc, off, 64) : __shfl_down(sc, off, 64);
+          if (dir == 0 ? lane >= off : lane + off < 64) sc += y;
         }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-      if (lane < SR_CM) {
-        const int gc = dir * SR_CM + lane;
-        const float nch = crow(0)[gc];
-        if (nch >= 2.f) {
-          const float* v = sTmp + gc * 12;
-          const float RR = (v[2] + v[1]) + v[0], RG = (v[5] + v[4]) + v[3], GG = (v[8] + v[7]) + v[6];
-          const float sr = crow(1)[gc];
-          const float beta = dm.beta_frac * sr * (1.0f / nch);
-          const float iden = 1.0f / (sr + nch * beta + dm.eps);
-          crow(5)[gc] = (RR + beta * (2.f * RG + beta * GG)) * (iden * iden);
-          crow(6)[gc] = beta;
-          crow(7)[gc] = iden;
-        }
+        const float ex0 = dir == 0 ? __shfl_up(sc, 1, 64) : __shfl_down(sc, 1, 64);
+        const float ex = dir == 0 ? (lane > 0 ? ex0 : 0.f) : (lane < 63 ? ex0 : 0.f);
+        s0[qq] = dir == 0 ? ex + x0[qq] : ex + tot;
+        s1[qq] = dir == 0 ? ex + tot : ex + x1[qq];
+      }
+      // the child of this lane: prefix [0, x) reads the sums at x - 1, suffix [x, n) at x
+      int tq = 0;
+      bool cv = false;
+      const int gc = dir * SR_CM + (lane < SR_CM ? lane : 0);
+      if (lane < SR_CM && crow(0)[gc] >= 2.f) {
+        tq = dir == 0 ? XL[lane] - 1 : XR[lane];
+        cv = true;
+      }
+      float v3[3];
+#pragma unroll
+      for (int qq = 0; qq < 3; ++qq) {
+        const float a0v = __shfl(s0[qq], tq >> 1, 64), a1v = __shfl(s1[qq], tq >> 1, 64);
+        v3[qq] = (tq & 1) ? a1v : a0v;
+      }
+      if (cv) {
+        const float nch = crow(0)[gc], sr = crow(1)[gc];
+        const float beta = dm.beta_frac * sr * (1.0f / nch);
+        const float iden = 1.0f / (sr + nch * beta + dm.eps);
+        crow(5)[gc] = (v3[0] + beta * (2.f * v3[1] + beta * v3[2])) * (iden * iden);
+        crow(6)[gc] = beta;
+        crow(7)[gc] = iden;
       }
     }
     __syncthreads();
@@ -855,13 +892,13 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
         for (int i = 0; i < NTM; ++i) {
           if (i < nt) {
+            // one token tile at a time (work of later tiles moved up would not fit the register budget)
+            __builtin_amdgcn_sched_barrier(0);
             f32x4 Y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int j = 0; j < NTM; ++j) {
               const bool use = j < nt && (j == i || (j < i ? dir == 0 : dir == 1));
               if (use) {
-                // one tile pair at a time (hoisted operand reads would not fit the register budget)
-                __builtin_amdgcn_sched_barrier(0);
                 u32x2 gh, gm, gl;
                 gread(i, j, gh, gm, gl);
                 if (j == i) { gh = gh & dmk; gm = gm & dmk; gl = gl & dmk; }
