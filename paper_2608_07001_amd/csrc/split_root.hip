@@ -51,6 +51,8 @@ struct SrLds {
   static constexpr int NTM = NMAX / 16;                   // 16-token tiles
   static constexpr int KTS = D + 4;                       // child key row stride (fp32)
   static constexpr int KOB = NMAX * (H2 + 4) * 4;         // one half of k° [NMAX][H2 + 4] fp32
+  static constexpr int LDVR = D + 8;                      // staged value rows (bf16), over the k° half
+  static_assert(NMAX * LDVR * 2 <= KOB, "value rows fit the k° half");
   static constexpr int KTB = SR_CC * KTS * 4;             // child k° sums -> k~
   static constexpr int GTB = 3 * 256 * 2;                 // one Gram tile: three bf16 planes of 16 x 16
   static constexpr int GB = NTM * (NTM + 1) / 2 * GTB;    // the Gram tiles (a >= b)
@@ -476,6 +478,20 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     }
 
     if (tid < n) sKn[tid] = sqrtf(sKn[tid]);
+    // the node's values, row-major bf16 into the k° half (free from here on):
+    // every load in flight now, stored after the child keys; rows past the
+    // node up to the last 16-token tile are zero
+    const int nt = (n + 15) >> 4;            // 16-token tiles
+    constexpr int VCH = D / 8;               // 16-byte chunks of a row
+    constexpr int VIT = NMAX * VCH / SR_T;   // (row, chunk) items per thread
+    uint4 vst[VIT];
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int e = tid + SR_T * it;
+      const int t = e / VCH, c = e % VCH;
+      vst[it] = make_uint4(0u, 0u, 0u, 0u);
+      if (t < n) vst[it] = *(const uint4*)(Vp + (int64_t)t * D + 8 * c);
+    }
     __syncthreads();
     // sum R and sum ||k°|| of every child: wave = child tile; B columns 0-2 hold
     // R in three parts, columns 3-5 ||k°|| in three parts
@@ -566,10 +582,16 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         kt[i + H2] = m2 * ccv[m] + m1 * snv[m];
       }
     }
+    uint16_t* sVr = (uint16_t*)(smem + Lay::oX);
+#pragma unroll
+    for (int it = 0; it < VIT; ++it) {
+      const int e = tid + SR_T * it;
+      const int t = e / VCH, c = e % VCH;
+      if (t < 16 * nt) *(uint4*)(sVr + t * Lay::LDVR + 8 * c) = vst[it];
+    }
     __syncthreads();
 
     // the keys of the first 16-token tile, in flight during the z products
-    const int nt = (n + 15) >> 4;            // 16-token tiles
     auto kload = [&](int j, uint32_t* dst) {
       int tr = 16 * j + i16;
       tr = tr < n ? tr : n - 1;
@@ -580,26 +602,14 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         dst[4 * h] = v.x; dst[4 * h + 1] = v.y; dst[4 * h + 2] = v.z; dst[4 * h + 3] = v.w;
       }
     };
-    uint32_t kcur[QW];
-    kload(0, kcur);
     const int np = nt * (nt + 1) / 2;        // Gram tiles
     auto tile_ab = [&](int k, int& a, int& b) {
       a = 0;
       while ((a + 1) * (a + 2) / 2 <= k) ++a;
       b = k - a * (a + 1) / 2;
     };
-    auto vload = [&](int k, uint4* xa, uint4* xb) {
-      int a, b;
-      tile_ab(k, a, b);
-      int ta = 16 * a + i16, tb = 16 * b + i16;
-      ta = ta < n ? ta : n - 1;
-      tb = tb < n ? tb : n - 1;
-#pragma unroll
-      for (int s = 0; s < D / 32; ++s) {
-        xb[s] = *(const uint4*)(Vp + (int64_t)tb * D + 32 * s + 8 * g4);
-        xa[s] = *(const uint4*)(Vp + (int64_t)ta * D + 32 * s + 8 * g4);
-      }
-    };
+    uint32_t kcur[QW];
+    kload(0, kcur);
 
     // ---- z_{q,c} = m_eff exp(k~_c . q / sqrt(d) - m_q): child rows x probe columns
     // on the matrix cores; lane (i16 = probe, g4) holds children 16 ct + 4 g4 + r ----
@@ -679,32 +689,33 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         el[j] = eh[j];
       }
     }
-    // the values of the wave's first Gram tile pair, in flight during the barrier
-    uint4 va[D / 32], vb[D / 32];
-    vload(wave < np ? wave : 0, va, vb);
-    __syncthreads();                         // the child keys are read: the Gram tiles go over them
-
     // ---- Gram matrix of the node's values, G = V V^T (the value terms of D_q,
     // eq:app_node_and_drop_distortion, are quadratic forms in it), in 16 x 16
-    // tiles a >= b: tile a (a + 1) / 2 + b holds G[16 a + i][16 b + j] at lane
+    // tiles a >= b, from the staged value rows; wave w takes the tiles
+    // w, w + 4, ... and holds them in registers until the planes can be
+    // stored.  Tile a (a + 1) / 2 + b holds G[16 a + i][16 b + j] at lane
     // i + 16 (j / 4), element j % 4 (the A-operand layout of G[a, b], and read
-    // across, of G[b, a]), as three bf16 planes with G = hi + mid + lo exactly.
+    // across, of G[b, a]), as three bf16 planes with G = hi + mid + lo exactly;
     // bf16 products are exact, so G carries only the fp32 accumulation.  With
     // each tile, the partial rows of G against R and 1 over t' < t: for the
     // rows t of tile a, sum over the columns t' of tile b (lower), and for the
     // columns t' of tile b, sum over the rows t of tile a (upper); tokens past
     // the node count as zero. ----
-    {
-      for (int k = wave; k < np; k += SR_T / 64) {
+    constexpr int GTM = (NTM * (NTM + 1) / 2 + SR_T / 64 - 1) / (SR_T / 64);   // tiles per wave
+    float gt[GTM][4];
+#pragma unroll
+    for (int m = 0; m < GTM; ++m) {
+      const int k = wave + (SR_T / 64) * m;
+      if (k < np) {
         int a, b;
         tile_ab(k, a, b);
-        // the next tile's values in flight (the last pass reloads its own: no
-        // value is left undefined on any path)
-        uint4 na[D / 32], nb[D / 32];
-        vload(k + SR_T / 64 < np ? k + SR_T / 64 : k, na, nb);
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) acc = mfma_bf16_16x16x32(pk8(vb[s]), pk8(va[s]), acc);
+        for (int s2 = 0; s2 < D / 32; ++s2) {
+          const uint4 xb = *(const uint4*)(sVr + (16 * b + i16) * Lay::LDVR + 32 * s2 + 8 * g4);
+          const uint4 xa = *(const uint4*)(sVr + (16 * a + i16) * Lay::LDVR + 32 * s2 + 8 * g4);
+          acc = mfma_bf16_16x16x32(pk8(xb), pk8(xa), acc);
+        }
         // C[i][j] = v_{16b+i} . v_{16a+j}: lane (i16, g4) holds G[16a + i16][16b + 4 g4 + r]
         const float x[4] = {acc[0], acc[1], acc[2], acc[3]};
         if (a == b && g4 == (i16 >> 2)) {
@@ -736,14 +747,24 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
           for (int r = 0; r < 4; ++r) sUp[16 * k + 4 * g4 + r] = make_float2(ua[r], ug[r]);
         }
-        u32x2 h, m, lo;
-        sr_split3(x, h, m, lo);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gt[m][r] = x[r];
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) gt[m][r] = 0.f;   // defined on every path
+      }
+    }
+    __syncthreads();                         // child keys and value rows are read: the Gram planes go over them
+#pragma unroll
+    for (int m = 0; m < GTM; ++m) {
+      const int k = wave + (SR_T / 64) * m;
+      if (k < np) {
+        u32x2 h, mi, lo;
+        sr_split3(gt[m], h, mi, lo);
         u32x2* dst = (u32x2*)(sG + (size_t)k * 768);
         dst[lane] = h;
-        dst[64 + lane] = m;
+        dst[64 + lane] = mi;
         dst[128 + lane] = lo;
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s) { va[s] = na[s]; vb[s] = nb[s]; }
       }
     }
     // A operand of G[i, j] (rows: tokens of tile i, k: tokens of tile j)
@@ -892,8 +913,6 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
         for (int i = 0; i < NTM; ++i) {
           if (i < nt) {
-            // one token tile at a time (work of later tiles moved up would not fit the register budget)
-            __builtin_amdgcn_sched_barrier(0);
             f32x4 Y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int j = 0; j < NTM; ++j) {
