@@ -340,7 +340,7 @@ __device__ __forceinline__ void block_e(const uint32_t* kreg, int n, int blk, co
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int t = 16 * blk + 4 * g4 + r;
-    ev[r] = (pok && t < n) ? __builtin_amdgcn_exp2f(acc[r] * sc2 - mq2) : 0.f;
+    ev[r] = __builtin_amdgcn_exp2f((pok && t < n) ? acc[r] * sc2 - mq2 : -INFINITY);   // exp2(-inf) = 0: no branch
   }
 }
 

@@ -369,7 +369,7 @@ __global__ __launch_bounds__(RT, 2) void k_root(Dims dm, const T* __restrict__ K
             float ev[4], ap[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              ev[r] = (uok && t0 + 4 * g4 + r < n) ? fexp(acc[0][r] * scale - mq) : 0.f;
+              ev[r] = fexp((uok && t0 + 4 * g4 + r < n) ? acc[0][r] * scale - mq : -INFINITY);   // e^-inf = 0: no branch
               ap[r] = ev[r] * zcq;
               Zl += ev[r];
             }

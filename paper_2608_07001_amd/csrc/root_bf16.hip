@@ -388,8 +388,8 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
               float ap[4];
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
-                float e = __builtin_amdgcn_exp2f(acc[0][r] * sc2 - mq2);
-                e = (full || (uok && t0 + r < n)) ? e : 0.f;
+                // exp2(-inf) = 0 for the masked ones: no branch around the exponential
+                const float e = __builtin_amdgcn_exp2f((full || (uok && t0 + r < n)) ? acc[0][r] * sc2 - mq2 : -INFINITY);
                 ev[4 * tl + r] = e;
                 ap[r] = e * zcq;
                 Zl += e;

@@ -666,7 +666,8 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = 16 * j + 4 * g4 + r;
-            ev[r] = (pok && t < n) ? __builtin_amdgcn_exp2f(acc[r] * sc2 - mq2) : 0.f;
+            // exp2(-inf) = 0 for the masked ones: no branch around the exponential
+            ev[r] = __builtin_amdgcn_exp2f((pok && t < n) ? acc[r] * sc2 - mq2 : -INFINITY);
           }
           sr_split3(ev, eh[j], em[j], el[j]);
           if (j + 1 < nt) {
