@@ -49,7 +49,8 @@ struct RbLds {
   static constexpr int oAp = oRp + (RI ? 0 : RB_W * NMAX * 4);   // [RB_W][NMAX] probe-mass partials
   static constexpr int oKt = oAp;                           // [D] prototype key k~
   static constexpr int oVv = oKt + D * 4;                   // [D] prototype value v~
-  static_assert(2 * D <= RB_W * NMAX, "prototype inside the probe-mass partials");
+  static constexpr int oKp = oVv + D * 4;                   // [3][D] k~ in three bf16 parts
+  static_assert(2 * D * 4 + 3 * D * 2 <= RB_W * NMAX * 4, "prototype inside the probe-mass partials");
   static constexpr int oR = oAp + RB_W * NMAX * 4;          // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                  // [NMAX] A_t
   static constexpr int oKn = oA + NMAX * 4;                 // [NMAX] ||k°_t||
@@ -123,6 +124,7 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
   float* sPk = (float*)(smem + Lay::oPk);
   float* sKt = (float*)(smem + Lay::oKt);
   float* sVv = (float*)(smem + Lay::oVv);
+  uint16_t* sKp = (uint16_t*)(smem + Lay::oKp);
   float* sSum = (float*)(smem + Lay::oSum);
   float* sRed = (float*)(smem + Lay::oRed);
 
@@ -478,7 +480,16 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
       for (int q = 0; q < RB_W; ++q) { m1 += sPk[q * D + i]; m2 += sPk[q * D + i + H2]; }
       m1 *= inv;
       m2 *= inv;
-      sKt[d] = d < H2 ? m1 * pcos - m2 * psin : m2 * pcos + m1 * psin;
+      const float kt = d < H2 ? m1 * pcos - m2 * psin : m2 * pcos + m1 * psin;
+      sKt[d] = kt;
+      // k~ = hi + mid + lo exactly (each a bf16) for the q . k~ products
+      const uint32_t hb = __float_as_uint(kt) & 0xffff0000u;
+      const float r1 = kt - __uint_as_float(hb);
+      const uint32_t mb = __float_as_uint(r1) & 0xffff0000u;
+      const uint32_t lb = __float_as_uint(r1 - __uint_as_float(mb));
+      sKp[d] = (uint16_t)(hb >> 16);
+      sKp[D + d] = (uint16_t)(mb >> 16);
+      sKp[2 * D + d] = (uint16_t)(lb >> 16);
     }
     __syncthreads();                          // C: prototype in LDS
     if (tid < 2 * D) {                        // the unit's root prototype, as pack writes it
@@ -505,19 +516,18 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
       if (tid == 0) tv.proto_logm[unit] = logf(me);
       float con = 0.f;
       if (wave_on) {
-        // q . k~ of the lane's probe (head slot 0): dims 32 s + 8 g4 .. + 7
-        float qk = 0.f;
+        // q . k~ for the wave's probes (head slot 0) on the matrix cores: A rows
+        // 0-2 hold k~ in three bf16 parts (exact products), B the probes' query
+        // rows; lane (probe, g4 = 0) gets the three parts and passes the sum on
+        f32x4 qa = {0.f, 0.f, 0.f, 0.f};
+        const uint16_t* kp = sKp + (i16 < 3 ? i16 : 0) * D + 8 * g4;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-          const uint32_t qw[4] = {qr[0][s].x, qr[0][s].y, qr[0][s].z, qr[0][s].w};
-          const float4 ka = *(const float4*)(sKt + 32 * s + 8 * g4);
-          const float4 kc = *(const float4*)(sKt + 32 * s + 8 * g4 + 4);
-          const float kx[8] = {ka.x, ka.y, ka.z, ka.w, kc.x, kc.y, kc.z, kc.w};
-#pragma unroll
-          for (int x = 0; x < 8; ++x)
-            qk += __uint_as_float((x & 1) ? (qw[x >> 1] & 0xffff0000u) : (qw[x >> 1] << 16)) * kx[x];
+          uint4 a8 = *(const uint4*)(kp + 32 * s);
+          if (i16 >= 3) a8 = make_uint4(0u, 0u, 0u, 0u);
+          qa = mfma_bf16_16x16x32(pk8(a8), pk8(qr[0][s]), qa);
         }
-        qk = col_sum4(qk);
+        const float qk = __shfl((qa[0] + qa[1]) + qa[2], i16, 64);
         const float z = me * __builtin_amdgcn_exp2f(qk * sc2 - mq2);
         const float Z = col_sum4(Zl);
         float s1 = 0.f, s2 = 0.f;
