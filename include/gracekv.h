@@ -27,8 +27,10 @@
  *   - `stream` is a hipStream_t passed as void*; kernels are only enqueued.
  *   - Layouts are row-major:  K, V [L][G][T][d];  Q [L][H][W][d];
  *     hidden [n_seg][T][D_hidden];  rope_cos/rope_sin [T][d/2] fp32 (rotate-half
- *     RoPE: the pair (i, i + d/2) turns by the table's angle);  K/V/Q/hidden are
- *     all of cfg->dtype.  Query head h belongs to KV head h / (H/G).
+ *     RoPE: the pair (i, i + d/2) turns by the angle p theta_i of row p, so the
+ *     turn from position p to position p' is that of row |p' - p| with the sine
+ *     negated when p' < p; the library uses both forms);  K/V/Q/hidden are all
+ *     of cfg->dtype.  Query head h belongs to KV head h / (H/G).
  *   - Errors: argument errors are detected on the host before anything is
  *     enqueued and return GRACEKV_ERR_INVALID_ARG / _UNSUPPORTED / _BUDGET /
  *     _WORKSPACE.  A failed launch returns GRACEKV_ERR_HIP.  Faults found on

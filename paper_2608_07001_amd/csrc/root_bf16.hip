@@ -54,7 +54,7 @@ struct RbLds {
   static constexpr int oR = oAp + RB_W * NMAX * 4;          // [NMAX] R_t
   static constexpr int oA = oR + NMAX * 4;                  // [NMAX] A_t
   static constexpr int oKn = oA + NMAX * 4;                 // [NMAX] ||k°_t||
-  static constexpr int oPk = oKn + NMAX * 4;                // [RB_W][D] partial sums of k°
+  static constexpr int oPk = oKn + NMAX * 4;                // [RB_W][D] partial sums of the turned keys
   static constexpr int oSum = oPk + RB_W * D * 4;           // [RB_W][4] per-wave sums of R, A, ||k°||
   static constexpr int oRed = oSum + RB_W * 4 * 4;          // [2][RB_W] distortion sums (unit parity)
   static constexpr int oPend = oRed + 2 * RB_W * 4;         // deferred outputs of the previous unit
@@ -239,9 +239,10 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
     const int64_t pmid = round_half_even_mid((int)a0, (int)a0 + n);
     float* Kn = sKn;
 
-    // ---- staging: K rows (zero past n) with RoPE undone on the way for the k°
-    // sums and ||k°_t||; V^T with permuted token columns (zero past n) ----
-    float kacc[16];                           // partial sums of k° (written after barrier S)
+    // ---- staging: K rows (zero past n) turned to the representative position
+    // on the way (R_{p~} R_{p_t}^{-1} is the turn by p~ - p_t) for the k~ sums
+    // and ||k°_t||; V^T with permuted token columns (zero past n) ----
+    float kacc[16];                           // partial sums of the turned keys (written after barrier S)
     const int c = 8 * (tid % CHP);
     {
 #pragma unroll
@@ -258,7 +259,11 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
         const int tk = t < n ? t : n - 1;
         const uint4 k1 = *(const uint4*)(Kp + (int64_t)tk * D + c);
         const uint4 k2 = *(const uint4*)(Kp + (int64_t)tk * D + c + H2);
-        const int64_t ta = a0 + tk;
+        // the turn from position a0 + tk to the representative position is
+        // the table row of their distance, its sine negated for a token past it
+        const int dl = (int)(a0 + tk - pmid);
+        const int64_t ta = dl < 0 ? -dl : dl;
+        const uint32_t sgn = dl < 0 ? 0x80000000u : 0u;
         const float4 c0 = *(const float4*)(cosT + ta * H2 + c), c1 = *(const float4*)(cosT + ta * H2 + c + 4);
         const float4 s0 = *(const float4*)(sinT + ta * H2 + c), s1 = *(const float4*)(sinT + ta * H2 + c + 4);
         const int cv = (e / 16) % CPR, t0 = 2 * (16 * (e / (16 * CPR)) + e % 16);
@@ -274,7 +279,10 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
           }
           const uint32_t w1[4] = {ka.x, ka.y, ka.z, ka.w}, w2[4] = {kc.x, kc.y, kc.z, kc.w};
           const float cs8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-          const float sn8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+          const float sn8[8] = {__uint_as_float(__float_as_uint(s0.x) ^ sgn), __uint_as_float(__float_as_uint(s0.y) ^ sgn),
+                                __uint_as_float(__float_as_uint(s0.z) ^ sgn), __uint_as_float(__float_as_uint(s0.w) ^ sgn),
+                                __uint_as_float(__float_as_uint(s1.x) ^ sgn), __uint_as_float(__float_as_uint(s1.y) ^ sgn),
+                                __uint_as_float(__float_as_uint(s1.z) ^ sgn), __uint_as_float(__float_as_uint(s1.w) ^ sgn)};
           float ss = 0.f;
 #pragma unroll
           for (int h = 0; h < 8; ++h) {
@@ -314,14 +322,11 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
         v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
         kacc[h] = col_sum4(v);
       }
-      // empty Split slots of the unit's node range
-      for (int i = tid; i < 2 * n; i += RB_T) {
-        const int64_t sl = (int64_t)lg * 2 * dm.N_c + 2 * a0 + i;
-        tv.sp_U[sl] = 0.f;
-        tv.sp_E[sl] = 0;
-        tv.sp_cost[sl] = 0;
-        tv.sp_exec[sl] = 0;
-      }
+      // empty Split slots of the unit's node range: cost 0 (the flat scans
+      // over the ops read a slot's key only where its cost is not 0; the
+      // refinement writes every field of a node it creates, the scoring pass
+      // every field of a live node, the selection every execution flag)
+      for (int i = tid; i < n; i += RB_T) *(uint16_t*)(tv.sp_cost + (int64_t)lg * 2 * dm.N_c + 2 * a0 + 2 * i) = 0;
     }
     __syncthreads();                          // S: staging done; every wave is past the previous unit
     if (tid == 0 && pend) flush(buf ^ 1);
@@ -423,8 +428,6 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
         }
       }
     }
-    // rotation of the representative position (used by the k~ threads after barrier B)
-    const float pcos = cosT[pmid * H2 + (tid % H2)], psin = sinT[pmid * H2 + (tid % H2)];
     __syncthreads();                          // A: token loop done
 
     // ---- token values R_t, A_t (LDS and out, zero up to 32 nb) and their sums ----
@@ -473,14 +476,13 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
       const float beta = dm.beta_frac * sr * inv;
       sVv[d] = (vr + beta * vs) / (sr + (float)n * beta + dm.eps);
     } else if (tid < 2 * D) {
-      // k~ of dim tid - D: the mean k° rotated to the representative position
-      const int d = tid - D, i = d % H2;
-      float m1 = 0.f, m2 = 0.f;
+      // k~ of dim tid - D: the mean of the keys turned to the representative
+      // position (the staging summed them turned there)
+      const int d = tid - D;
+      float m = 0.f;
 #pragma unroll
-      for (int q = 0; q < RB_W; ++q) { m1 += sPk[q * D + i]; m2 += sPk[q * D + i + H2]; }
-      m1 *= inv;
-      m2 *= inv;
-      const float kt = d < H2 ? m1 * pcos - m2 * psin : m2 * pcos + m1 * psin;
+      for (int q = 0; q < RB_W; ++q) m += sPk[q * D + d];
+      const float kt = m * inv;
       sKt[d] = kt;
       // k~ = hi + mid + lo exactly (each a bf16) for the q . k~ products
       const uint32_t hb = __float_as_uint(kt) & 0xffff0000u;
@@ -501,7 +503,7 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
     {
       const float sa = sSum[1] + sSum[5] + sSum[9] + sSum[13];
       const float skn = sSum[2] + sSum[6] + sSum[10] + sSum[14];
-      // coherence of the mean k° (eq:app_effective_multiplicity)
+      // coherence of the mean k° (eq:app_effective_multiplicity); a turn keeps its norm
       float ss = 0.f;
       for (int d = lane; d < D; d += 64) {
         float m = 0.f;
