@@ -7,7 +7,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 SRC = ["abi.hip", "relevance.hip", "root.hip", "root_bf16.hip", "build.hip", "select.hip", "pack.hip", "segment.hip", "decode.hip",
-       "multihop.hip", "split_root.hip", "floor.hip"]
+       "multihop.hip", "split_root.hip", "levels.hip", "floor.hip"]
 LIB = os.path.join(HERE, "libgracekv.so")
 
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

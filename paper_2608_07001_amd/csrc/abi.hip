@@ -89,6 +89,18 @@ TreeView make_view(void* base, const gracekv_plan& p) {
   v.fl_pre_add = nullptr;
   v.fl_pre_sp = nullptr;
   v.fl_state = nullptr;
+  // the level region sits just before the kernel-argument copy
+  const int64_t LG = p.unit_cap / p.J_cap;
+  char* lv = b + p.tree_bytes - KARGS_BYTES - level_region_bytes(LG, p.N_c, p.unit_cap);
+  const int64_t cap = level_capacity(LG, p.N_c);
+  size_t o = 0;
+  auto take = [&](size_t bytes) { char* q = lv + o; o = (o + bytes + 255) & ~(size_t)255; return q; };
+  v.lv_items = (int32_t*)take((size_t)cap * 32);
+  v.lv_res = (int32_t*)take((size_t)cap * 48);
+  v.lv_units = (int32_t*)take((size_t)p.unit_cap * 8);
+  v.lv_state = (int4*)take((size_t)p.unit_cap * 16);
+  v.lv_ctr = (int32_t*)take(64);
+  v.lv_cap = cap;
   return v;
 }
 
@@ -305,6 +317,7 @@ gracekv_status gracekv_plan_sizes(const gracekv_config* c, gracekv_plan* p) {
   put(p->off_proto, UC * 2 * (size_t)c->d * (c->dtype == GRACEKV_BF16 ? 2 : 4));
   put(p->off_proto_logm, UC * 4);
   put(p->off_floor, c->alpha_floor > 0.0 ? floor_view(nullptr, dm, p->unit_cap, p->node_cap).bytes : 0);
+  o += level_region_bytes(LG, p->N_c, p->unit_cap);   // level-by-level refinement lists
   o += KARGS_BYTES;                          // device copy of the kernel arguments
   p->tree_bytes = o;
   p->seg_ws_bytes = segment_ws_bytes(dm);
@@ -413,8 +426,18 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     clock_end(clk, st);
     if (e != hipSuccess) return GRACEKV_ERR_HIP;
   }
+  // one clock pair per stage: the root splits, then everything below them (the
+  // depths refined level by level and the per-unit kernel after them)
   auto build = [&](int mode) {
-    return launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
+    const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
+    const int clk = clock_begin(dm, roots ? GRACEKV_STAGE_ROOT_SPLIT : GRACEKV_STAGE_REFINE, st);
+    hipError_t e = hipSuccess;
+    if (!roots && dm.dtype == GRACEKV_BF16)
+      e = launch_levels_bf16(dm, mode == BUILD_FULL, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
+    if (e == hipSuccess)
+      e = launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
+    clock_end(clk, st);
+    return e;
   };
   if (launch_omega(dm, omega_raw, tv, st) != hipSuccess) return GRACEKV_ERR_HIP;
   // multi-hop relevance: s-hat of every (l, g) first (bf16: the token relevance

@@ -955,13 +955,8 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
   hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 48, 96);
   hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 0, 48);
   const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
-  const int clk = clock_begin(dm, roots ? GRACEKV_STAGE_ROOT_SPLIT : GRACEKV_STAGE_REFINE, st);
-  if (dm.dtype == GRACEKV_BF16 && roots) {
-    const hipError_t e = launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv,
-                                           2 * device_cus(), st);
-    clock_end(clk, st);
-    return e;
-  }
+  if (dm.dtype == GRACEKV_BF16 && roots)
+    return launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, 2 * device_cus(), st);
   const dim3 grid((unsigned)device_cus());
 #define GKV_LAUNCH_REFINE(TT, DD)                                                                          \
   do {                                                                                                     \
@@ -978,8 +973,13 @@ hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, 
     if (dm.d == 128) GKV_LAUNCH_REFINE(float, 128); else GKV_LAUNCH_REFINE(float, 64);
   }
 #undef GKV_LAUNCH_REFINE
-  clock_end(clk, st);
   return hipGetLastError();
+}
+
+hipError_t launch_levels_bf16(const Dims& dm, bool full, const void* K, const void* V, const void* Q,
+                              const float* cosT, const float* sinT, const int32_t* slot_starts,
+                              const int32_t* n_slots, const float* kappa, const TreeView& tv, hipStream_t st) {
+  return launch_levels(dm, full, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, 2 * device_cus(), st);
 }
 
 }  // namespace gkv

@@ -82,7 +82,22 @@ struct TreeView {
   const uint8_t* fl_pre_add;  // [unit_cap] 1: the floor executed the unit's Add
   const uint8_t* fl_pre_sp;   // [node_cap] 1: the floor executed the node's Split
   const int64_t* fl_state;  // [8] B_floor first
+  // level-by-level refinement (bf16): items [lv_cap][8] as in work (the slot
+  // length word also holds the node's BFS index << 16, the Add key word the key
+  // of the op that creates the node), results [lv_cap][12], two lists of the
+  // units with nodes at the current depth, per unit (first, end, item base,
+  // items) of that depth, and counters
+  int32_t* lv_items;
+  int32_t* lv_res;
+  int32_t* lv_units;    // [2][unit_cap]
+  int4* lv_state;       // [unit_cap]
+  int32_t* lv_ctr;      // [16]
+  int64_t lv_cap;
 };
+// bytes of the level region at the end of the tree buffer, and its item capacity
+// (the nodes of one depth are disjoint, at least two tokens each: N_c / 2 per (l, g))
+size_t level_region_bytes(int64_t LG, int64_t N_c, int64_t unit_cap);
+int64_t level_capacity(int64_t LG, int64_t N_c);
 
 // The singleton floor's region of the tree buffer (alpha_floor > 0).  Public
 // part, each array 256-byte aligned in this order: int64 state[8] (B_floor,
@@ -136,8 +151,13 @@ struct MhView {
 // CONTINUE refines every unrefined node whose creating op reaches theta.
 // ROOT_FULL refines the root of every unit (the first level of the complete
 // build).  For bf16 caches the roots are refined by their own kernel
-// (launch_split_root) in ROOT_SPLIT and ROOT_FULL.
-enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3, BUILD_ROOT_FULL = 4 };
+// (launch_split_root) in ROOT_SPLIT and ROOT_FULL, and the next levels by the
+// same kernel one depth at a time: LEVEL (pruned) and LEVEL_FULL (complete)
+// take the nodes of one depth from a list and write one result per node, which
+// the level pass then numbers in BFS order.
+enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3, BUILD_ROOT_FULL = 4, BUILD_LEVEL = 5,
+       BUILD_LEVEL_FULL = 6 };
+constexpr int LEVELS_MAX = 48;   // depths refined level by level; deeper nodes go to the per-unit kernel
 
 // ---- gains, utilities and keys (shared by the build and score kernels so that
 // both produce bit-identical keys) -------------------------------------------
@@ -425,6 +445,14 @@ int split_root_lds_bytes(int d);
 hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void* V, const void* Q, const float* cosT,
                              const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
                              const TreeView& tv, int grid, hipStream_t st);
+// the levels below the roots (bf16): LEVELS_MAX rounds of the split kernel over
+// one depth's list and the level pass; full: the complete build
+hipError_t launch_levels(const Dims& dm, bool full, const void* K, const void* V, const void* Q, const float* cosT,
+                         const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
+                         const TreeView& tv, int grid, hipStream_t st);
+hipError_t launch_levels_bf16(const Dims& dm, bool full, const void* K, const void* V, const void* Q,
+                              const float* cosT, const float* sinT, const int32_t* slot_starts,
+                              const int32_t* n_slots, const float* kappa, const TreeView& tv, hipStream_t st);
 hipError_t selftest_mfma(int which, float* out, hipStream_t st);
 
 // Stage clock (GRACEKV_FLAG_STAGE_TIMES; stage ids GRACEKV_STAGE_*): clock_begin

@@ -99,7 +99,7 @@ __device__ __forceinline__ s16x4 sr_op(u32x2 v) { return __builtin_bit_cast(s16x
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 template <int D>
-__global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__ dmp, int mode,
+__global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__ dmp, int mode, int lvl,
                                                          const uint16_t* __restrict__ K,
                                                          const uint16_t* __restrict__ V,
                                                          const uint16_t* __restrict__ Q,
@@ -146,11 +146,22 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
 
   const int tid0 = threadIdx.x;
   const int J = *n_slots;
-  const int nwork = tv.wctr[0];
+  // roots: the build's work list; a level (depth lvl >= 1): that depth's list,
+  // its length in lv_ctr[lvl & 1], the next item in lv_ctr[2]
+  const bool level = mode == BUILD_LEVEL || mode == BUILD_LEVEL_FULL;
+  const int32_t* items = level ? tv.lv_items : tv.work;
+  int32_t* next_ctr = level ? tv.lv_ctr + 2 : tv.wctr + 1;
+  const int nwork = level ? (int)min((int64_t)tv.lv_ctr[lvl & 1], tv.lv_cap) : tv.wctr[0];
+  if (level && blockIdx.x == 0 && tid0 == 0) {
+    // the counters the level pass after this kernel accumulates into: the next
+    // depth's items and units
+    tv.lv_ctr[(lvl + 1) & 1] = 0;
+    tv.lv_ctr[4 + ((lvl + 1) & 1)] = 0;
+  }
   const float scale = 1.0f / sqrtf((float)D);
   const float LOG2E = 1.44269504088896341f;
 
-  if (tid0 == 0) meta[9] = atomicAdd(&tv.wctr[1], 1);
+  if (tid0 == 0) meta[9] = atomicAdd(next_ctr, 1);
   for (;;) {
     // per-lane indices are formed inside the loop (values derived from them are
     // not held across items, which would not fit the register budget)
@@ -167,17 +178,18 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     // the next item, in flight while this one is processed (stored before the
     // barrier at the top of the next pass)
     int wnext = 0;
-    if (tid == 0) wnext = atomicAdd(&tv.wctr[1], 1);
+    if (tid == 0) wnext = atomicAdd(next_ctr, 1);
     auto publish_next = [&]() { if (tid == 0) meta[9] = wnext; };
     do {
-    // the work item: unit, slot, the root's D and R, w and the Add key (one load)
-    const int4 d0 = *(const int4*)(tv.work + 8 * (int64_t)wi);
-    const int4 d1 = *(const int4*)(tv.work + 8 * (int64_t)wi + 4);
+    // the work item: unit, the node's start, length (and BFS index), D and R, w
+    // and the key of the op that creates it (one load)
+    const int4 d0 = *(const int4*)(items + 8 * (int64_t)wi);
+    const int4 d1 = *(const int4*)(items + 8 * (int64_t)wi + 4);
     const int64_t unit = uni(d0.x);
     const int lg = (int)(unit / dm.J_cap), j = (int)(unit % dm.J_cap);
     const int l = lg / dm.G, g = lg % dm.G;
     const int a0 = uni(d0.y);
-    const int n = uni(d0.z);
+    const int n = uni(d0.z) & 0xffff;
     const float Dv = __int_as_float(uni(d0.w));
     const float Rroot = __int_as_float(uni(d1.x));
     const float w = __int_as_float(uni(d1.y));
@@ -189,9 +201,22 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     const uint16_t* Kp = K + ((int64_t)lg * dm.T + a0) * D;
     const uint16_t* Vp = V + ((int64_t)lg * dm.T + a0) * D;
     const float* tokR = tv.tok_R + (int64_t)lg * dm.N_c + a0;
-    // ---- writes the root and its children (local positions) ----
+    // ---- writes the root and its children (local positions), or a level's
+    // result: kind | nkid << 8 | cut << 16, U, then per child (start | length << 16),
+    // D, R (node-local positions; the level pass numbers and places them) ----
     auto write_tree = [&](int kind, int cut, int nkid, const int* ka, const int* kn, const float* kD,
                           const float* kR) {
+      if (level) {
+        float sd = 0.f;
+        for (int k = 0; k < nkid; ++k) sd += kD[k];
+        const float Us = utility(split_gain(w, Rroot, Dv, sd), nkid - 1);
+        int4* r = (int4*)(tv.lv_res + 12 * (int64_t)wi);
+        const int k2 = nkid > 2 ? ka[2] | (kn[2] << 16) : 0;
+        r[0] = make_int4(kind | (nkid << 8) | (cut << 16), __float_as_int(Us), ka[0] | (kn[0] << 16), ka[1] | (kn[1] << 16));
+        r[1] = make_int4(k2, __float_as_int(kD[0]), __float_as_int(kD[1]), nkid > 2 ? __float_as_int(kD[2]) : 0);
+        r[2] = make_int4(__float_as_int(kR[0]), __float_as_int(kR[1]), nkid > 2 ? __float_as_int(kR[2]) : 0, 0);
+        return;
+      }
       tv.node_child[base] = 1;
       tv.node_nch[base] = (uint8_t)nkid;
       tv.node_kind[base] = (uint8_t)kind;
@@ -1054,9 +1079,10 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   }
 }
 
-hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void* V, const void* Q, const float* cosT,
-                             const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
-                             const TreeView& tv, int grid, hipStream_t st) {
+static hipError_t launch_split(const Dims& dm, int mode, int lvl, const void* K, const void* V, const void* Q,
+                               const float* cosT, const float* sinT, const int32_t* slot_starts,
+                               const int32_t* n_slots, const float* kappa, const TreeView& tv, int grid,
+                               hipStream_t st) {
   const int lds = split_root_lds_bytes(dm.d);
   const Dims* dmp = (const Dims*)tv.kargs;
   const TreeView* tvp = (const TreeView*)((const char*)tv.kargs + 512);
@@ -1065,12 +1091,26 @@ hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void
     auto fn = k_split_root<DD>;                                                                           \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds); \
     if (e0 != hipSuccess) return e0;                                                                      \
-    hipLaunchKernelGGL(fn, dim3(grid), dim3(SR_T), lds, st, dmp, mode, (const uint16_t*)K,                \
+    hipLaunchKernelGGL(fn, dim3(grid), dim3(SR_T), lds, st, dmp, mode, lvl, (const uint16_t*)K,           \
                        (const uint16_t*)V, (const uint16_t*)Q, cosT, sinT, slot_starts, n_slots, kappa, tvp); \
   } while (0)
   if (dm.d == 128) GKV_SR(128); else if (dm.d == 64) GKV_SR(64); else return hipErrorInvalidValue;
 #undef GKV_SR
   return hipGetLastError();
+}
+
+hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void* V, const void* Q, const float* cosT,
+                             const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
+                             const TreeView& tv, int grid, hipStream_t st) {
+  return launch_split(dm, mode, 0, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, grid, st);
+}
+
+hipError_t launch_split_level(const Dims& dm, bool full, int lvl, const void* K, const void* V, const void* Q,
+                              const float* cosT, const float* sinT, const int32_t* slot_starts,
+                              const int32_t* n_slots, const float* kappa, const TreeView& tv, int grid,
+                              hipStream_t st) {
+  return launch_split(dm, full ? BUILD_LEVEL_FULL : BUILD_LEVEL, lvl, K, V, Q, cosT, sinT, slot_starts, n_slots,
+                      kappa, tv, grid, st);
 }
 
 }  // namespace gkv

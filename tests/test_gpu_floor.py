@@ -120,6 +120,17 @@ def test_singleton_floor_matches_the_oracle(shape, seed, capped):
     assert over == capped
 
 
+def _level_region_bytes(p) -> int:
+    # after the floor's region: the level-by-level refinement lists (items of 32
+    # bytes and results of 48 for up to N_c / 2 nodes per (l, g), two unit lists,
+    # per-unit state of 16 bytes, 64 bytes of counters), each 256-byte aligned;
+    # then the 1024-byte copy of the kernel arguments
+    al = lambda x: (x + 255) // 256 * 256
+    LG = p.unit_cap // p.J_cap
+    cap = LG * (p.N_c // 2) + 1
+    return al(cap * 32) + al(cap * 48) + al(p.unit_cap * 8) + al(p.unit_cap * 16) + al(64)
+
+
 def test_floor_off_is_the_hot_path():
     # alpha = 0 leaves no floor region and the same output as the default
     sh = CONFIGS["tiny"]
@@ -128,4 +139,5 @@ def test_floor_off_is_the_hot_path():
     b = H.gpu_run(case, alpha_floor=0.0)
     for k in ("offsets", "K_out", "V_out", "pos_out", "logm_out"):
         assert torch.equal(a[k], b[k]), k
-    assert "floor" not in b and b["plan"].off_floor == b["plan"].tree_bytes - 1024
+    p = b["plan"]
+    assert "floor" not in b and p.off_floor == p.tree_bytes - _level_region_bytes(p) - 1024
