@@ -432,10 +432,12 @@ gracekv_status gracekv_build_trees(const gracekv_config* c, const void* K, const
     const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
     const int clk = clock_begin(dm, roots ? GRACEKV_STAGE_ROOT_SPLIT : GRACEKV_STAGE_REFINE, st);
     hipError_t e = hipSuccess;
-    if (!roots && dm.dtype == GRACEKV_BF16)
+    const bool levels = !roots && dm.dtype == GRACEKV_BF16;
+    if (levels)
       e = launch_levels_bf16(dm, mode == BUILD_FULL, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
     if (e == hipSuccess)
-      e = launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st);
+      e = launch_build(dm, p.build_lds_bytes, mode, K, V, Q, rope_cos, rope_sin, slot_starts, n_slots, kappa, tv, st,
+                       levels);
     clock_end(clk, st);
     return e;
   };

@@ -947,13 +947,15 @@ static int device_cus() {
 
 hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
-                        const float* kappa, const TreeView& tv, hipStream_t st) {
-  const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
-  hipLaunchKernelGGL(k_work_reset, dim3(1), dim3(64), 0, st, tv);
-  const unsigned mb = (unsigned)((units + 255) / 256);
-  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 96, NMAX + 1);
-  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 48, 96);
-  hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 0, 48);
+                        const float* kappa, const TreeView& tv, hipStream_t st, bool listed) {
+  if (!listed) {                            // else the level passes left the work list
+    const int64_t units = (int64_t)dm.L * dm.G * dm.J_cap;
+    hipLaunchKernelGGL(k_work_reset, dim3(1), dim3(64), 0, st, tv);
+    const unsigned mb = (unsigned)((units + 255) / 256);
+    hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 96, NMAX + 1);
+    hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 48, 96);
+    hipLaunchKernelGGL(k_work_mark, dim3(mb), dim3(256), 0, st, dm, mode, tv, 0, 48);
+  }
   const bool roots = mode == BUILD_ROOT_SPLIT || mode == BUILD_ROOT_FULL;
   if (dm.dtype == GRACEKV_BF16 && roots)
     return launch_split_root(dm, mode, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv, 2 * device_cus(), st);

@@ -422,9 +422,11 @@ hipError_t launch_root_bf16(const Dims& dm, const void* K, const void* V, const 
                             const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const TreeView& tv,
                             hipStream_t st);
 int root_bf16_lds_bytes(int d);
+// listed: the work list is already made (by the level passes); otherwise the
+// units with nodes to refine are listed first
 hipError_t launch_build(const Dims& dm, int lds_bytes, int mode, const void* K, const void* V, const void* Q,
                         const float* cosT, const float* sinT, const int32_t* slot_starts, const int32_t* n_slots,
-                        const float* kappa, const TreeView& tv, hipStream_t st);
+                        const float* kappa, const TreeView& tv, hipStream_t st, bool listed = false);
 hipError_t launch_omega(const Dims& dm, const float* omega_raw, const TreeView& tv, hipStream_t st);
 // rank: B_free - 1 (the cut) or B_free (the skip bound, also stored in theta[1])
 hipError_t launch_theta(const Dims& dm, const TreeView& tv, hipStream_t st, bool skip_bound);

@@ -17,9 +17,9 @@
 // depth done here and continues from the same node table.
 //
 // Counters (lv_ctr): [d & 1] items of depth d; [2] next item of the split
-// kernel; [4 + (d & 1)] units with items at depth d.  The split kernel of depth
-// d clears the counters of depth d + 1; the level pass of depth d clears the
-// split kernel's cursor.
+// kernel; [4 + (d & 1)] units with items at depth d; [8] the unit capacity.
+// The split kernel of depth d clears the counters of depth d + 1; the level
+// pass of depth d clears the split kernel's cursor.
 #include "common.h"
 
 namespace gkv {
@@ -33,9 +33,9 @@ size_t level_region_bytes(int64_t LG, int64_t N_c, int64_t unit_cap) {
   return al256(cap * 32) + al256(cap * 48) + al256((size_t)unit_cap * 8) + al256((size_t)unit_cap * 16) + al256(64);
 }
 
-__global__ void k_level_reset(const TreeView* __restrict__ tvp) {
+__global__ void k_level_reset(const TreeView* __restrict__ tvp, int ucap) {
   const TreeView& tv = *tvp;
-  if (threadIdx.x < 16) tv.lv_ctr[threadIdx.x] = 0;
+  if (threadIdx.x < 16) tv.lv_ctr[threadIdx.x] = threadIdx.x == 8 ? ucap : 0;
 }
 
 // exclusive prefix over the wave (lane order) and the wave total
@@ -50,16 +50,16 @@ __device__ __forceinline__ int wave_excl(int v, int& total) {
   return x - v;
 }
 
-// first: depth 0 was refined by the root pass (units from the build's work
-// list), only the depth-1 items are listed.  Otherwise the units of depth lvl.
+// The units with nodes at depth lvl (>= 1): children numbered and placed, depth
+// lvl + 1 listed.
 __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, const TreeView* __restrict__ tvp, int lvl,
-                                               int full, int first) {
+                                               int full) {
   const Dims& dm = *dmp;
   const TreeView& tv = *tvp;
   const int lane = threadIdx.x & 63;
   const int P = lvl & 1, Pn = (lvl + 1) & 1;
   if (blockIdx.x == 0 && threadIdx.x == 0) tv.lv_ctr[2] = 0;   // the next split kernel's cursor
-  const int nunits = __builtin_amdgcn_readfirstlane(first ? tv.wctr[0] : tv.lv_ctr[4 + P]);
+  const int nunits = __builtin_amdgcn_readfirstlane(tv.lv_ctr[4 + P]);
   const int J = *tv.nslots;
   const uint64_t theta = full ? 0ull : tv.theta[0];
   const int64_t ucap = (int64_t)dm.L * dm.G * dm.J_cap;
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
   for (int k = __builtin_amdgcn_readfirstlane((int)blockIdx.x * (int)(blockDim.x >> 6) + (int)(threadIdx.x >> 6));
        k < nunits; k += nw) {
     do {
-    const int64_t unit = first ? (int64_t)tv.work[8 * (int64_t)k] : (int64_t)tv.lv_units[(int64_t)P * ucap + k];
+    const int64_t unit = tv.lv_units[(int64_t)P * ucap + k];
     const int lg = (int)(unit / dm.J_cap), j = (int)(unit % dm.J_cap);
     if (j >= J) break;
     const int a0 = tv.slots[j];
@@ -81,15 +81,9 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
     const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
     const int32_t w_bits = __float_as_int(tv.omega[lg]);
     const int cnt = tv.unit_nn[unit];
-    // this depth's nodes [lo, hi) with their items from ib (first: none; the
-    // children of the root are the next depth)
-    int lo = 1, hi = 1, ib = 0;
-    if (!first) {
-      const int4 st = tv.lv_state[unit];
-      lo = st.x; hi = st.y; ib = st.z;
-    } else if (cnt < 2) {
-      break;                                 // the root was not refined
-    }
+    // this depth's nodes [lo, hi) with their items from ib
+    const int4 st = tv.lv_state[unit];
+    const int lo = st.x, hi = st.y, ib = st.z;
     // per lane: two nodes i = lo + lane + 64 h; refined ones read their result
     int nk[2] = {0, 0}, nx[2] = {0, 0};
     int4 r0[2], r1[2], r2[2];
@@ -130,18 +124,9 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
         nx[h] = pass ? (int)(kn0 >= 2) + (int)(kn1 >= 2) + (int)(nk[h] > 2 && kn2 >= 2) : 0;
       }
     }
-    // first: the root's children are this pass's new nodes, listed directly
-    int fn = 0, fnx = 0;
-    uint64_t Ef = 0ull;
-    if (first) {
-      if (!full) Ef = tv.sp_E[base];         // the root's Split (written by the root pass)
-      const int c = 1 + lane;
-      if (c < cnt && tv.node_n[base + c] >= 2 && (full || Ef >= theta)) fnx = 1;
-      fn = fnx;
-    }
     int tk0, tk1, tx0, tx1;
     const int ck0 = wave_excl(nk[0], tk0), ck1 = wave_excl(nk[1], tk1);
-    const int cx0 = wave_excl(first ? fn : nx[0], tx0), cx1 = wave_excl(nx[1], tx1);
+    const int cx0 = wave_excl(nx[0], tx0), cx1 = wave_excl(nx[1], tx1);
     const int newcnt = cnt + tk0 + tk1;
     const int ktot = tx0 + tx1;
     int nbl = 0;
@@ -158,13 +143,7 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
       it[0] = make_int4((int32_t)unit, a_abs, n | (c << 16), __float_as_int(Dc));
       it[1] = make_int4(__float_as_int(Rc), w_bits, (int32_t)(uint32_t)E, (int32_t)(uint32_t)(E >> 32));
     };
-    if (first) {
-      if (fnx) {
-        const int c = 1 + lane;
-        const int64_t s = base + c;
-        put_item(nb + cx0, c, tv.node_a[s], tv.node_n[s], tv.node_D[s], tv.node_R[s], Ef);
-      }
-    } else {
+    {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         if (nk[h] == 0) continue;
@@ -211,8 +190,7 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
     }
     if (lane == 0) {
       tv.unit_nn[unit] = newcnt;
-      const int nlo = first ? 1 : cnt;
-      tv.lv_state[unit] = make_int4(nlo, first ? cnt : newcnt, nb, ktot);
+      tv.lv_state[unit] = make_int4(cnt, newcnt, nb, ktot);
       if (ktot > 0) {
         const int pos = atomicAdd(&tv.lv_ctr[4 + Pn], 1);
         tv.lv_units[(int64_t)Pn * ucap + pos] = (int32_t)unit;
@@ -220,6 +198,80 @@ __global__ __launch_bounds__(256) void k_level(const Dims* __restrict__ dmp, con
     }
     } while (0);
   }
+}
+
+// Depth 1: the children of every root the root pass refined, one unit per
+// lane; the wave takes one block of items and one block of list entries.
+__global__ __launch_bounds__(256) void k_level_first(const Dims* __restrict__ dmp, const TreeView* __restrict__ tvp,
+                                                     int full) {
+  const Dims& dm = *dmp;
+  const TreeView& tv = *tvp;
+  const int lane = threadIdx.x & 63;
+  if (blockIdx.x == 0 && threadIdx.x == 0) tv.lv_ctr[2] = 0;   // the next split kernel's cursor
+  const int nunits = __builtin_amdgcn_readfirstlane(tv.wctr[0]);
+  const int J = *tv.nslots;
+  const uint64_t theta = full ? 0ull : tv.theta[0];
+  const int64_t ucap = (int64_t)dm.L * dm.G * dm.J_cap;
+  const int stride = (int)gridDim.x * (int)blockDim.x;
+  for (int k0 = __builtin_amdgcn_readfirstlane((int)blockIdx.x * (int)blockDim.x + (int)(threadIdx.x & ~63u));
+       k0 < nunits; k0 += stride) {
+    const int k = k0 + lane;
+    int64_t unit = 0, base = 0;
+    int cnt = 0, m = 0;
+    uint64_t Ef = 0ull;
+    bool ok[3] = {false, false, false};
+    if (k < nunits) {
+      unit = tv.work[8 * (int64_t)k];
+      const int lg = (int)(unit / dm.J_cap), j = (int)(unit % dm.J_cap);
+      if (j < J) {
+        base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)tv.slots[j];
+        cnt = tv.unit_nn[unit];
+        if (!full && cnt > 1) Ef = tv.sp_E[base];   // the root's Split (written by the root pass)
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+          ok[c] = 1 + c < cnt && tv.node_n[base + 1 + c] >= 2 && (full || Ef >= theta);
+          m += ok[c] ? 1 : 0;
+        }
+      }
+    }
+    int tot;
+    const int ex = wave_excl(m, tot);
+    int nbl = 0;
+    if (lane == 0 && tot > 0) nbl = atomicAdd(&tv.lv_ctr[1], tot);
+    const int nb = __builtin_amdgcn_readfirstlane(__shfl(nbl, 0, 64));
+    const uint64_t has = __ballot(m > 0);
+    int ubl = 0;
+    if (lane == 0 && has) ubl = atomicAdd(&tv.lv_ctr[5], __popcll(has));
+    const int ub = __builtin_amdgcn_readfirstlane(__shfl(ubl, 0, 64));
+    const bool fits = (int64_t)nb + tot <= tv.lv_cap;   // always (the roots' children are disjoint)
+    if (!fits && lane == 0) atomicOr(tv.status, STATUS_CAPACITY);
+    if (fits && m > 0) {
+      int xi = nb + ex;
+      const int32_t w_bits = __float_as_int(tv.omega[unit / dm.J_cap]);
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        if (!ok[c]) continue;
+        const int64_t s = base + 1 + c;
+        int4* it = (int4*)(tv.lv_items + 8 * (int64_t)xi);
+        it[0] = make_int4((int32_t)unit, tv.node_a[s], tv.node_n[s] | ((1 + c) << 16), __float_as_int(tv.node_D[s]));
+        it[1] = make_int4(__float_as_int(tv.node_R[s]), w_bits, (int32_t)(uint32_t)Ef, (int32_t)(uint32_t)(Ef >> 32));
+        ++xi;
+      }
+      tv.lv_state[unit] = make_int4(1, cnt, nb + ex, m);
+      tv.lv_units[ucap + ub + __popcll(has & ((1ull << lane) - 1ull))] = (int32_t)unit;
+    }
+  }
+}
+
+// Below the last depth done here: the units still holding nodes to refine
+// become the per-unit kernel's work list.
+__global__ void k_level_handoff(const TreeView* __restrict__ tvp) {
+  const TreeView& tv = *tvp;
+  const int64_t ucap = (int64_t)tv.lv_ctr[8];
+  constexpr int P = (LEVELS_MAX + 1) & 1;
+  const int n = tv.lv_ctr[4 + P];
+  for (int i = threadIdx.x; i < n; i += blockDim.x) tv.work[8 * (int64_t)i] = tv.lv_units[P * ucap + i];
+  if (threadIdx.x == 0) { tv.wctr[0] = n; tv.wctr[1] = 0; }
 }
 
 hipError_t launch_split_level(const Dims& dm, bool full, int lvl, const void* K, const void* V, const void* Q,
@@ -233,14 +285,15 @@ hipError_t launch_levels(const Dims& dm, bool full, const void* K, const void* V
   const Dims* dmp = (const Dims*)tv.kargs;
   const TreeView* tvp = (const TreeView*)((const char*)tv.kargs + 512);
   const dim3 lgrid((unsigned)grid);
-  hipLaunchKernelGGL(k_level_reset, dim3(1), dim3(64), 0, st, tvp);
-  hipLaunchKernelGGL(k_level, lgrid, dim3(256), 0, st, dmp, tvp, 0, full ? 1 : 0, 1);
+  hipLaunchKernelGGL(k_level_reset, dim3(1), dim3(64), 0, st, tvp, (int)((int64_t)dm.L * dm.G * dm.J_cap));
+  hipLaunchKernelGGL(k_level_first, lgrid, dim3(256), 0, st, dmp, tvp, full ? 1 : 0);
   for (int lvl = 1; lvl <= LEVELS_MAX; ++lvl) {
     const hipError_t e = launch_split_level(dm, full, lvl, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv,
                                             grid, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_level, lgrid, dim3(256), 0, st, dmp, tvp, lvl, full ? 1 : 0, 0);
+    hipLaunchKernelGGL(k_level, lgrid, dim3(256), 0, st, dmp, tvp, lvl, full ? 1 : 0);
   }
+  hipLaunchKernelGGL(k_level_handoff, dim3(1), dim3(256), 0, st, tvp);
   return hipGetLastError();
 }
 
