@@ -207,13 +207,19 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
   };
 
   int buf = 0;
-  for (int64_t uu = ub; uu < ue; ++uu) {
+  // (layer, KV head, slot) of the unit, stepped along the range (no division per unit)
+  int lg = (int)(ub / J), j = (int)(ub % J);
+  int l = lg / dm.G, g = lg % dm.G;
+  for (int64_t uu = ub; uu < ue; ++uu, ++j) {
+    if (j == J) {
+      j = 0;
+      ++lg;
+      if (++g == dm.G) { g = 0; ++l; }
+    }
     // per-thread addresses are formed inside the loop (not held across it)
     int tid = tid0;
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, i16 = lane & 15, g4 = lane >> 4;
-    const int lg = (int)(uu / J), j = (int)(uu % J);
-    const int l = lg / dm.G, g = lg % dm.G;
     const int64_t unit = (int64_t)lg * dm.J_cap + j;
     const int64_t a0 = slot_starts[j];
     const int n = slot_starts[j + 1] - (int)a0;
@@ -247,12 +253,12 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
     {
 #pragma unroll
       for (int h = 0; h < 16; ++h) kacc[h] = 0.f;
-      // K item e: token e / CHP, pair chunk c (rows up to 32 nb, zero past n);
+      // K item e: token e / CHP, pair chunk c (rows up to n; not RI: up to 32 nb, zero past n);
       // V item e: token pair 16 (e / (16 CPR)) + e % 16 (pairs fastest within a
       // 32-token block), 8-dim chunk (e / 16) % CPR.  One item of each kind per
       // thread and round, all its loads issued before any is used (a second
       // round in flight would not fit the register budget).
-      const int nk = 32 * nb * CHP, nv = 16 * nb * CPR;
+      const int nk = (RI ? n : 32 * nb) * CHP, nv = 16 * nb * CPR;
       const int nmax = nk > nv ? nk : nv;
       for (int e = tid; e < nmax; e += RB_T) {
         const int t = e / CHP;
@@ -283,16 +289,16 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
                                 __uint_as_float(__float_as_uint(s0.z) ^ sgn), __uint_as_float(__float_as_uint(s0.w) ^ sgn),
                                 __uint_as_float(__float_as_uint(s1.x) ^ sgn), __uint_as_float(__float_as_uint(s1.y) ^ sgn),
                                 __uint_as_float(__float_as_uint(s1.z) ^ sgn), __uint_as_float(__float_as_uint(s1.w) ^ sgn)};
+          // the pair (a1, a2) turned, added in place; ||k°_t||^2 from the key
+          // itself (a turn keeps the norm)
           float ss = 0.f;
 #pragma unroll
           for (int h = 0; h < 8; ++h) {
             const float a1 = __uint_as_float((h & 1) ? (w1[h >> 1] & 0xffff0000u) : (w1[h >> 1] << 16));
             const float a2 = __uint_as_float((h & 1) ? (w2[h >> 1] & 0xffff0000u) : (w2[h >> 1] << 16));
-            const float o1 = a1 * cs8[h] + a2 * sn8[h];
-            const float o2 = a2 * cs8[h] - a1 * sn8[h];
-            kacc[h] += o1;
-            kacc[8 + h] += o2;
-            ss += o1 * o1 + o2 * o2;
+            kacc[h] = fmaf(a1, cs8[h], fmaf(a2, sn8[h], kacc[h]));
+            kacc[8 + h] = fmaf(a2, cs8[h], fmaf(-a1, sn8[h], kacc[8 + h]));
+            ss = fmaf(a1, a1, fmaf(a2, a2, ss));
           }
 #pragma unroll
           for (int o = 1; o < CHP; o <<= 1) ss += __shfl_xor(ss, o, 64);
@@ -311,26 +317,58 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
           }
         }
       }
-      // lanes l, l + CHP, ... of a wave hold the same chunk: rotations by CHP ..
-      // 8 within each 16-lane row (DPP), then the four rows by row swaps
+      // lanes l, l + CHP, ... of a wave hold the same chunk
       static_assert(CHP == 4 || CHP == 8, "chunk classes within a 16-lane row");
+      if constexpr (CHP == 8) {
+        // eight lanes per chunk (lane bits 3, 4, 5): each exchange halves the
+        // values a lane holds and doubles the lanes summed (lane ^ 8 by a DPP
+        // rotation inside the row, then the row swaps of permlane16/32, which
+        // leave the first operand's sum in the even rows (the lower half) and
+        // the second's in the odd rows (upper half)); lane (chunk, b3 b4 b5)
+        // ends with the chunk's values 8 b3 + 4 b4 + 2 b5 and one more
+        const bool b3 = (lane >> 3) & 1;
+        float r1[8];
 #pragma unroll
-      for (int h = 0; h < 16; ++h) {
-        float v = kacc[h];
-        if constexpr (CHP == 4)
+        for (int i = 0; i < 8; ++i) {
+          const float snd = b3 ? kacc[i] : kacc[8 + i], kp = b3 ? kacc[8 + i] : kacc[i];
+          r1[i] = kp + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(snd), 0x128, 0xf, 0xf, false));
+        }
+        float r2[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const auto pq = __builtin_amdgcn_permlane16_swap(__float_as_uint(r1[i]), __float_as_uint(r1[i + 4]), false, false);
+          r2[i] = __uint_as_float(pq[0]) + __uint_as_float(pq[1]);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const auto pq = __builtin_amdgcn_permlane32_swap(__float_as_uint(r2[i]), __float_as_uint(r2[i + 2]), false, false);
+          kacc[i] = __uint_as_float(pq[0]) + __uint_as_float(pq[1]);
+        }
+      } else {
+        // rotations by 4 and 8 within each 16-lane row (DPP), then the row swaps
+#pragma unroll
+        for (int h = 0; h < 16; ++h) {
+          float v = kacc[h];
           v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x124, 0xf, 0xf, false));
-        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
-        kacc[h] = col_sum4(v);
+          v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x128, 0xf, 0xf, false));
+          kacc[h] = col_sum4(v);
+        }
       }
       // empty Split slots of the unit's node range: cost 0 (the flat scans
       // over the ops read a slot's key only where its cost is not 0; the
       // refinement writes every field of a node it creates, the scoring pass
       // every field of a live node, the selection every execution flag)
-      for (int i = tid; i < n; i += RB_T) *(uint16_t*)(tv.sp_cost + (int64_t)lg * 2 * dm.N_c + 2 * a0 + 2 * i) = 0;
+      static_assert(NMAX <= RB_T, "one thread per slot pair");
+      uint16_t* spc = (uint16_t*)(tv.sp_cost + ((int64_t)lg * dm.N_c + a0) * 2);
+      if (tid < n) spc[tid] = 0;
     }
     __syncthreads();                          // S: staging done; every wave is past the previous unit
     if (tid == 0 && pend) flush(buf ^ 1);
-    if (lane < CHP) {
+    if constexpr (CHP == 8) {
+      const int h0 = 8 * ((lane >> 3) & 1) + 4 * ((lane >> 4) & 1) + 2 * ((lane >> 5) & 1);
+      const int dd = h0 < 8 ? c + h0 : c + H2 + (h0 - 8);
+      *(float2*)(sPk + w * D + dd) = make_float2(kacc[0], kacc[1]);
+    } else if (lane < CHP) {
 #pragma unroll
       for (int h = 0; h < 8; ++h) { sPk[w * D + c + h] = kacc[h]; sPk[w * D + c + H2 + h] = kacc[8 + h]; }
     }
