@@ -157,7 +157,9 @@ def kernel_names(dtype):
     if dtype == "bf16":
         return {"segment": "gracekv_segment (k_gram_bf16, k_curvature, k_dist2, DP kernels)",
                 "rowstats": "k_rowstats_bf + k_rowstats_combine", "token_relevance": "k_rel_rows",
-                "root": "k_root_bf", "root_split": "k_split_root", "refine": "k_refine", "pack": "k_pack_emit"}
+                "root": "k_root_bf", "root_split": "k_split_root<d, false> (the roots)",
+                "refine": "k_split_root<d, true> (one launch per depth) + k_level + k_refine (below 48 depths)",
+                "pack": "k_pack_emit"}
     return {"segment": "gracekv_segment (k_curvature, k_gram_f32, k_dist2, DP kernels)",
             "rowstats": "k_rowstats + k_rowstats_combine", "token_relevance": "-", "root": "k_root",
             "root_split": "k_refine (roots)", "refine": "k_refine", "pack": "k_pack_emit"}

@@ -98,7 +98,9 @@ __device__ __forceinline__ void sr_split3(const float* x, u32x2& hi, u32x2& mid,
 __device__ __forceinline__ s16x4 sr_op(u32x2 v) { return __builtin_bit_cast(s16x4, v); }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-template <int D>
+// LV: a depth below the roots (the level list and results; mode BUILD_LEVEL or
+// BUILD_LEVEL_FULL), else the roots (mode BUILD_ROOT_SPLIT or BUILD_ROOT_FULL)
+template <int D, bool LV>
 __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__ dmp, int mode, int lvl,
                                                          const uint16_t* __restrict__ K,
                                                          const uint16_t* __restrict__ V,
@@ -148,7 +150,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
   const int J = *n_slots;
   // roots: the build's work list; a level (depth lvl >= 1): that depth's list,
   // its length in lv_ctr[lvl & 1], the next item in lv_ctr[2]
-  const bool level = mode == BUILD_LEVEL || mode == BUILD_LEVEL_FULL;
+  constexpr bool level = LV;
   const int32_t* items = level ? tv.lv_items : tv.work;
   int32_t* next_ctr = level ? tv.lv_ctr + 2 : tv.wctr + 1;
   const int nwork = level ? (int)min((int64_t)tv.lv_ctr[lvl & 1], tv.lv_cap) : tv.wctr[0];
@@ -206,7 +208,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     // D, R (node-local positions; the level pass numbers and places them) ----
     auto write_tree = [&](int kind, int cut, int nkid, const int* ka, const int* kn, const float* kD,
                           const float* kR) {
-      if (level) {
+      if constexpr (level) {
         float sd = 0.f;
         for (int k = 0; k < nkid; ++k) sd += kD[k];
         const float Us = utility(split_gain(w, Rroot, Dv, sd), nkid - 1);
@@ -1088,7 +1090,7 @@ static hipError_t launch_split(const Dims& dm, int mode, int lvl, const void* K,
   const TreeView* tvp = (const TreeView*)((const char*)tv.kargs + 512);
 #define GKV_SR(DD)                                                                                        \
   do {                                                                                                    \
-    auto fn = k_split_root<DD>;                                                                           \
+    auto fn = (mode == BUILD_LEVEL || mode == BUILD_LEVEL_FULL) ? k_split_root<DD, true> : k_split_root<DD, false>; \
     hipError_t e0 = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds); \
     if (e0 != hipSuccess) return e0;                                                                      \
     hipLaunchKernelGGL(fn, dim3(grid), dim3(SR_T), lds, st, dmp, mode, lvl, (const uint16_t*)K,           \
