@@ -938,23 +938,40 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         for (int c = 0; c < 2; ++c) {
           aZ[c] = f32x4{0.f, 0.f, 0.f, 0.f}; aS[c] = aZ[c]; aP[c] = aZ[c]; aQ[c] = aZ[c];
         }
+        // Y of a token tile from the Gram tiles in pairs (j2, j2 + 1) on the
+        // 16x16x32 instruction: its operands take tile j2's four values of the
+        // lane, then tile j2 + 1's (the A and B sides pair the tokens alike); a
+        // half that must not contribute gets a zero Gram part, and e is zero
+        // past the last tile
+        static_assert(NTM % 2 == 0, "token tiles in pairs");
+        auto cat = [](u32x2 a, u32x2 b) { return pk8(make_uint4(a.x, a.y, b.x, b.y)); };
 #pragma unroll
         for (int i = 0; i < NTM; ++i) {
           if (i < nt) {
             f32x4 Y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int j = 0; j < NTM; ++j) {
-              const bool use = j < nt && (j == i || (j < i ? dir == 0 : dir == 1));
-              if (use) {
-                u32x2 gh, gm, gl;
-                gread(i, j, gh, gm, gl);
-                if (j == i) { gh = gh & dmk; gm = gm & dmk; gl = gl & dmk; }
-                Y = mfma_bf16_16x16x16(sr_op(gl), sr_op(eh[j]), Y);
-                Y = mfma_bf16_16x16x16(sr_op(gm), sr_op(em[j]), Y);
-                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(el[j]), Y);
-                Y = mfma_bf16_16x16x16(sr_op(gm), sr_op(eh[j]), Y);
-                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(em[j]), Y);
-                Y = mfma_bf16_16x16x16(sr_op(gh), sr_op(eh[j]), Y);
+            for (int j2 = 0; j2 < NTM; j2 += 2) {
+              const bool use0 = j2 < nt && (j2 == i || (j2 < i ? dir == 0 : dir == 1));
+              const bool use1 = j2 + 1 < nt && (j2 + 1 == i || (j2 + 1 < i ? dir == 0 : dir == 1));
+              if (use0 || use1) {
+                const u32x2 z2 = {0u, 0u};
+                u32x2 gh0 = z2, gm0 = z2, gl0 = z2, gh1 = z2, gm1 = z2, gl1 = z2;
+                if (use0) {
+                  gread(i, j2, gh0, gm0, gl0);
+                  if (j2 == i) { gh0 = gh0 & dmk; gm0 = gm0 & dmk; gl0 = gl0 & dmk; }
+                }
+                if (use1) {
+                  gread(i, j2 + 1, gh1, gm1, gl1);
+                  if (j2 + 1 == i) { gh1 = gh1 & dmk; gm1 = gm1 & dmk; gl1 = gl1 & dmk; }
+                }
+                const s16x8 ah = cat(gh0, gh1), am = cat(gm0, gm1), al = cat(gl0, gl1);
+                const s16x8 bh = cat(eh[j2], eh[j2 + 1]), bm = cat(em[j2], em[j2 + 1]), bl = cat(el[j2], el[j2 + 1]);
+                Y = mfma_bf16_16x16x32(al, bh, Y);
+                Y = mfma_bf16_16x16x32(am, bm, Y);
+                Y = mfma_bf16_16x16x32(ah, bl, Y);
+                Y = mfma_bf16_16x16x32(am, bh, Y);
+                Y = mfma_bf16_16x16x32(ah, bm, Y);
+                Y = mfma_bf16_16x16x32(ah, bh, Y);
               }
             }
             const int t0 = 16 * i + 4 * g4;
