@@ -556,6 +556,9 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
       if (tid == 0) tv.proto_logm[unit] = logf(me);
       float con = 0.f;
       if (wave_on) {
+        float vv = 0.f;                        // ||v~||^2
+        for (int d = lane; d < D; d += 64) vv = fmaf(sVv[d], sVv[d], vv);
+        vv = wave_sum_dpp(vv);
         // q . k~ for the wave's probes (head slot 0) on the matrix cores: A rows
         // 0-2 hold k~ in three bf16 parts (exact products), B the probes' query
         // rows; lane (probe, g4 = 0) gets the three parts and passes the sum on
@@ -570,7 +573,9 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
         const float qk = __shfl((qa[0] + qa[1]) + qa[2], i16, 64);
         const float z = me * __builtin_amdgcn_exp2f(qk * sc2 - mq2);
         const float Z = col_sum4(Zl);
-        float s1 = 0.f, s2 = 0.f;
+        // ||M - z v~||^2 = ||M||^2 - 2 z <M, v~> + z^2 ||v~||^2 (clamped at 0), as
+        // the refinement forms it: a rounding error of a few fp32 ulps of ||M||^2
+        float mv = 0.f, s2 = 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
           const float4 v4 = *(const float4*)(sVv + 16 * dt + 4 * g4);
@@ -578,15 +583,16 @@ __global__ __launch_bounds__(RB_T, RI ? 4 : 2) void k_root_bf(const Dims* __rest
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const float M = Macc[dt][r];
-            const float df = M - z * vt[r];
-            s1 += df * df;
-            s2 += M * M;
+            mv = fmaf(M, vt[r], mv);
+            s2 = fmaf(M, M, s2);
           }
         }
-        s1 = col_sum4(s1);
+        mv = col_sum4(mv);
         s2 = col_sum4(s2);
+        const float s1 = fmaxf(s2 - 2.f * z * mv + z * z * vv, 0.f);
         const float dz = Z - z;
-        const float Dq = dm.lam_Z * dz * dz / (Z * Z + dm.eps) + dm.lam_M * s1 / (s2 + dm.eps);
+        const float Dq = dm.lam_Z * dz * dz * __builtin_amdgcn_rcpf(Z * Z + dm.eps) +
+                         dm.lam_M * s1 * __builtin_amdgcn_rcpf(s2 + dm.eps);
         con = (uok && g4 == 0) ? (Z * zcq) * Dq : 0.f;
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) con += __shfl_xor(con, o, 64);
