@@ -417,7 +417,9 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
     constexpr int HT = H2 / 16;              // 16-dim tiles per half
     for (int hf = 0; hf < 2; ++hf) {
       // k° of the half (item (token, 8-dim chunk): the pair (i, i + H2) is
-      // rotated together); every load of the half in flight first
+      // rotated together), turned back to the node's start a0: the table row of
+      // the offset t (R_{p~} R_{a0 + t}^{-1} = R_{p~ - a0} R_t^{-1}; rows below
+      // NMAX stay cached); every load of the half in flight first
       uint32_t kw1[IPT][4], kw2[IPT][4];
       float cs[IPT][8], sn[IPT][8];
 #pragma unroll
@@ -425,7 +427,7 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         const int e = tid + SR_T * it;
         const int ee = e < n * CH ? e : 0;
         const int t = ee / CH, c = 8 * (ee % CH);
-        const int64_t ta = a0 + t;
+        const int64_t ta = t;
         const uint4 u1 = *(const uint4*)(Kp + (int64_t)t * D + c);
         const uint4 u2 = *(const uint4*)(Kp + (int64_t)t * D + c + H2);
         const float4 c0 = *(const float4*)(cosT + ta * H2 + c), c1 = *(const float4*)(cosT + ta * H2 + c + 4);
@@ -584,12 +586,12 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
       for (int m = 0; m < RPT; ++m) {         // the rotation rows, every load in flight together
         const int e = tid + SR_T * m;
         const int gc = e / H2, i = e % H2;
-        int64_t pp = a0;
+        int64_t pp = 0;                      // the child's representative position less a0
         if (e < SR_CC * H2) {
           const int nch = (int)crow(0)[gc];
           if (nch >= 2) {
             const int x0 = gc < SR_CM ? 0 : XR[gc - SR_CM];
-            pp = round_half_even_mid(a0 + x0, a0 + x0 + nch);
+            pp = round_half_even_mid(a0 + x0, a0 + x0 + nch) - a0;
           }
         }
         ccv[m] = cosT[pp * H2 + i];
