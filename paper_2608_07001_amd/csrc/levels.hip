@@ -20,6 +20,8 @@
 // kernel; [4 + (d & 1)] units with items at depth d; [8] the unit capacity.
 // The split kernel of depth d clears the counters of depth d + 1; the level
 // pass of depth d clears the split kernel's cursor.
+#include <cstdlib>
+
 #include "common.h"
 
 namespace gkv {
@@ -265,10 +267,10 @@ __global__ __launch_bounds__(256) void k_level_first(const Dims* __restrict__ dm
 
 // Below the last depth done here: the units still holding nodes to refine
 // become the per-unit kernel's work list.
-__global__ void k_level_handoff(const TreeView* __restrict__ tvp) {
+__global__ void k_level_handoff(const TreeView* __restrict__ tvp, int levels) {
   const TreeView& tv = *tvp;
   const int64_t ucap = (int64_t)tv.lv_ctr[8];
-  constexpr int P = (LEVELS_MAX + 1) & 1;
+  const int P = (levels + 1) & 1;
   const int n = tv.lv_ctr[4 + P];
   for (int i = threadIdx.x; i < n; i += blockDim.x) tv.work[8 * (int64_t)i] = tv.lv_units[P * ucap + i];
   if (threadIdx.x == 0) { tv.wctr[0] = n; tv.wctr[1] = 0; }
@@ -287,13 +289,20 @@ hipError_t launch_levels(const Dims& dm, bool full, const void* K, const void* V
   const dim3 lgrid((unsigned)grid);
   hipLaunchKernelGGL(k_level_reset, dim3(1), dim3(64), 0, st, tvp, (int)((int64_t)dm.L * dm.G * dm.J_cap));
   hipLaunchKernelGGL(k_level_first, lgrid, dim3(256), 0, st, dmp, tvp, full ? 1 : 0);
-  for (int lvl = 1; lvl <= LEVELS_MAX; ++lvl) {
+  // depths refined here: LEVELS_MAX, or fewer where GRACEKV_LEVELS says so (a
+  // knob for tests of the per-unit kernel continuing below the last depth)
+  int levels = LEVELS_MAX;
+  if (const char* env = std::getenv("GRACEKV_LEVELS")) {
+    const int v = std::atoi(env);
+    levels = v < 0 ? 0 : (v < LEVELS_MAX ? v : LEVELS_MAX);
+  }
+  for (int lvl = 1; lvl <= levels; ++lvl) {
     const hipError_t e = launch_split_level(dm, full, lvl, K, V, Q, cosT, sinT, slot_starts, n_slots, kappa, tv,
                                             grid, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_level, lgrid, dim3(256), 0, st, dmp, tvp, lvl, full ? 1 : 0);
   }
-  hipLaunchKernelGGL(k_level_handoff, dim3(1), dim3(256), 0, st, tvp);
+  hipLaunchKernelGGL(k_level_handoff, dim3(1), dim3(256), 0, st, tvp, levels);
   return hipGetLastError();
 }
 
