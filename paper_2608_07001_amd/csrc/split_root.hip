@@ -471,19 +471,27 @@ __global__ __launch_bounds__(SR_T, 2) void k_split_root(const Dims* __restrict__
         f32x4 acc[CT];
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < nks; ++s) {
-          const int t0 = 16 * s + 4 * g4;
-          float x[4];
+        // 16-token steps in pairs on the 16x16x32 instruction (the lane's four
+        // tokens of step s, then of step s + 1, on both sides)
+        auto cat2 = [](u32x2 a, u32x2 b) { return pk8(make_uint4(a.x, a.y, b.x, b.y)); };
+        for (int s = 0; s < nks; s += 2) {
+          u32x2 kh[2], km[2], kl[2];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) x[r] = t0 + r < n ? sKo[(t0 + r) * KSTR + 16 * tile + i16] : 0.f;
-          u32x2 kh, km, kl;
-          sr_split3(x, kh, km, kl);
+          for (int h = 0; h < 2; ++h) {
+            const int t0 = 16 * (s + h) + 4 * g4;
+            float x[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) x[r] = t0 + r < n ? sKo[(t0 + r) * KSTR + 16 * tile + i16] : 0.f;
+            sr_split3(x, kh[h], km[h], kl[h]);
+          }
+          const int ta = 16 * s + 4 * g4, tb = ta + 16;
+          const s16x8 bl = cat2(kl[0], kl[1]), bm = cat2(km[0], km[1]), bh = cat2(kh[0], kh[1]);
 #pragma unroll
           for (int ct = 0; ct < CT; ++ct) {
-            const s16x4 mk = sr_op(one2 & mask16(clo[ct], chi[ct], t0));
-            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(kl), acc[ct]);
-            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(km), acc[ct]);
-            acc[ct] = mfma_bf16_16x16x16(mk, sr_op(kh), acc[ct]);
+            const s16x8 mk = cat2(one2 & mask16(clo[ct], chi[ct], ta), one2 & mask16(clo[ct], chi[ct], tb));
+            acc[ct] = mfma_bf16_16x16x32(mk, bl, acc[ct]);
+            acc[ct] = mfma_bf16_16x16x32(mk, bm, acc[ct]);
+            acc[ct] = mfma_bf16_16x16x32(mk, bh, acc[ct]);
           }
         }
         // lane (dim 16 tile + i16, g4) holds children 16 ct + 4 g4 + r
