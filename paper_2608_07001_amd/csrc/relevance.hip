@@ -188,15 +188,17 @@ __device__ __forceinline__ void lse2_add8(float& m, float& z, const float* y) {
 __device__ __forceinline__ void lse2_add8_raw(float& m, float& z, const float* x, float sc2) {
   const float mxr = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
   const float mn = fmaxf(m, mxr * sc2);
-  float acc = z * __builtin_amdgcn_exp2f(m - mn);   // m = -inf at first: 2^-inf = 0
+  float e[8];
 #pragma unroll
-  for (int r = 0; r < 8; ++r) acc += __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], sc2, -mn));
-  z = acc;
+  for (int r = 0; r < 8; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], sc2, -mn));
+  // pairwise: a short dependency chain instead of eight additions in a row
+  const float s8 = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+  z = __builtin_fmaf(z, __builtin_amdgcn_exp2f(m - mn), s8);   // m = -inf at first: 2^-inf = 0
   m = mn;
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __restrict__ K,
+__global__ __launch_bounds__(256, 2) void k_rowstats_bf(Dims dm, const uint16_t* __restrict__ K,
                                                      const uint16_t* __restrict__ Q, float4* __restrict__ partial,
                                                      int nchunk) {
   constexpr int QE = D / 4;                       // elements of a lane's quarter row
@@ -257,6 +259,43 @@ __global__ __launch_bounds__(256) void k_rowstats_bf(Dims dm, const uint16_t* __
     if (s0 + RS_SUB < t_end) load_sub(s0 + RS_SUB);
     __syncthreads();
     const bool allC = s0 + RS_SUB <= dm.N_c && s0 + RS_SUB <= t_end;
+    if (allC && tile_ok[3]) {
+      // the common case, wave-uniform: every token of the block is in C and
+      // visible to every window query, and the wave's four row tiles all
+      // exist; one straight-line block per 32 tokens, so the products of one
+      // tile overlap the exponentials of another (a lane of a row past the
+      // last one computes on row 0's query; its statistics are never written)
+#pragma unroll
+      for (int tp = 0; tp < RS_SUB / 32; ++tp) {
+        uint4 kv[2][KS];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint4* k4 = (const uint4*)(sK + (32 * tp + 16 * h + i16) * LDK + QE * g4);
+#pragma unroll
+          for (int s = 0; s < KS; ++s) kv[h][s] = k4[s];
+        }
+        f32x4 acc[4][2];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          acc[k][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+          acc[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) acc[k][h] = mfma_bf16_16x16x32(pk8(kv[h][s]), pk8(qv[k][s]), acc[k][h]);
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          float y[8];
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[k][h][r];
+          lse2_add8_raw(mC[k], zC[k], y, sc2);
+        }
+      }
+      continue;
+    }
 #pragma unroll
     for (int tp = 0; tp < RS_SUB / 32; ++tp) {
       uint4 kv[2][KS];
