@@ -37,6 +37,7 @@ constexpr int MH_SEEDS = 64;                 // at most this many seeds per hop
 constexpr int MH_HOPS = 2;
 constexpr int MH_CH = 1024;                  // tokens per workgroup of the row passes
 constexpr int MH_SUB = 64;                   // tokens staged at once
+constexpr int MH_PF = 4;                     // staging rounds prefetched into registers
 constexpr int MH_TOPB = 4096;                // tokens per block of the candidate pass
 constexpr double MH_ETA = 0.9;               // cumulative seed share
 constexpr float MH_RHO = 0.5f;               // inter-hop decay
@@ -245,6 +246,23 @@ __global__ __launch_bounds__(512) void k_rel_rows(Dims dm, const uint16_t* __res
     for (int s = 0; s < KS; ++s)
       qf[rt][s] = ok ? *(const uint4*)(qrow + 32 * s + 8 * g4) : make_uint4(0, 0, 0, 0);
   }
+  // direct pass: the normaliser of row 16 rt + 4 g4 + r, the lane's rows once
+  // the products are taken with the rows as M and the tokens as N (+inf for a
+  // row past the last: 2^(-inf) = 0)
+  float cT[4][4];
+  if (MODE == RR_DIRECT) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int j = 16 * rt + 4 * g4 + r;
+        cT[rt][r] = INFINITY;
+        if (j < nrow) {
+          const float4 st = tv.row_stats[((int64_t)l * dm.G + g) * dm.rows + w * dm.W + j];
+          cT[rt][r] = st.x * LOG2E + __log2f(st.y);
+        }
+      }
+  }
   const int64_t c0 = (int64_t)ch * MH_CH;
   int64_t c1 = c0 + MH_CH < dm.N_c ? c0 + MH_CH : dm.N_c;
   if (MODE != RR_DIRECT && (int64_t)umax + 1 < c1) c1 = (int64_t)umax + 1;
@@ -252,20 +270,65 @@ __global__ __launch_bounds__(512) void k_rel_rows(Dims dm, const uint16_t* __res
   float m[4], z[4];
 #pragma unroll
   for (int rt = 0; rt < 4; ++rt) { m[rt] = -INFINITY; z[rt] = 0.f; }
+  // the first MH_PF staging rounds of the next sub-chunk are loaded into
+  // registers while the current one is computed (all of them for blocks of
+  // 256 threads or more at d = 128); further rounds load at store time
+  const int bd = blockDim.x;
+  uint4 pre[MH_PF];
+  auto prefetch = [&](int64_t s0n) {
+    const int ntn = (int)(c1 - s0n < MH_SUB ? c1 - s0n : MH_SUB);
+#pragma unroll
+    for (int q = 0; q < MH_PF; ++q) {
+      const int e = tid + bd * q, tt = e / C8, c = e % C8;
+      pre[q] = e < MH_SUB * C8 && tt < ntn ? *(const uint4*)(Kp + (s0n + tt) * D + 8 * c) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  if (c0 < c1) prefetch(c0);
   for (int64_t s0 = c0; s0 < c1; s0 += MH_SUB) {
     const int nt = (int)(c1 - s0 < MH_SUB ? c1 - s0 : MH_SUB);
     __syncthreads();
-    for (int e = tid; e < MH_SUB * C8; e += blockDim.x) {
+#pragma unroll
+    for (int q = 0; q < MH_PF; ++q) {
+      const int e = tid + bd * q;
+      if (e < MH_SUB * C8) *(uint4*)(sk + (e / C8) * LDK + 8 * (e % C8)) = pre[q];
+    }
+    for (int e = tid + bd * MH_PF; e < MH_SUB * C8; e += bd) {
       const int tt = e / C8, c = e % C8;
       const uint4 v = tt < nt ? *(const uint4*)(Kp + (s0 + tt) * D + 8 * c) : make_uint4(0, 0, 0, 0);
       *(uint4*)(sk + tt * LDK + 8 * c) = v;
     }
+    if (s0 + MH_SUB < c1) prefetch(s0 + MH_SUB);
     __syncthreads();
     for (int tt = 0; tt < MH_SUB / 16; ++tt) {
       if (16 * tt >= nt) break;
       uint4 kf[KS];
 #pragma unroll
       for (int s = 0; s < KS; ++s) kf[s] = *(const uint4*)(sk + (16 * tt + i16) * LDK + 32 * s + 8 * g4);
+      if (MODE == RR_DIRECT) {
+        // rows as M, tokens as N: the lane holds rows 16 rt + 4 g4 + r of token
+        // s0 + 16 tt + i16, summed in registers and over the four lanes of its
+        // column; a token past the chunk (zero key rows) is computed and never
+        // read back
+        f32x4 acc[4];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt) {
+          acc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int s = 0; s < KS; ++s) acc[rt] = mfma_bf16_16x16x32(pk8(qf[rt][s]), pk8(kf[s]), acc[rt]);
+        }
+        float e[16];
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) e[4 * rt + r] = __builtin_amdgcn_exp2f(fmaf(acc[rt][r], sc2, -cT[rt][r]));
+#pragma unroll
+        for (int w2 = 8; w2 > 0; w2 >>= 1)
+#pragma unroll
+          for (int i = 0; i < w2; ++i) e[i] += e[i + w2];
+        const float sv = col_sum4(e[0]);
+        if (g4 == 0) red[w][16 * tt + i16] = sv;
+        continue;
+      }
       f32x4 acc[4];
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) {
