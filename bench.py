@@ -158,7 +158,7 @@ def kernel_names(dtype):
         return {"segment": "gracekv_segment (k_gram_bf16, k_curvature, k_dist2, DP kernels)",
                 "rowstats": "k_rowstats_bf + k_rowstats_combine", "token_relevance": "k_rel_rows",
                 "root": "k_root_bf", "root_split": "k_split_root<d, false> (the roots)",
-                "refine": "k_split_root<d, true> (one launch per depth) + k_level + k_refine (below 48 depths)",
+                "refine": "k_split_root<d, true> (one launch per depth) + k_level + k_refine (below 48 depths, 12 at 64x or more)",
                 "pack": "k_pack_emit"}
     return {"segment": "gracekv_segment (k_curvature, k_gram_f32, k_dist2, DP kernels)",
             "rowstats": "k_rowstats + k_rowstats_combine", "token_relevance": "-", "root": "k_root",

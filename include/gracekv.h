@@ -276,10 +276,12 @@ gracekv_status gracekv_segment(const gracekv_config* cfg, const void* hidden, co
  * split nor on the final frontier, so score, select and pack give the same
  * result as the full build.
  * For bf16 caches the nodes below the roots are refined one depth at a time
- * (all units at once) for up to 48 depths, the rest unit by unit; the
- * environment variable GRACEKV_LEVELS (0 .. 48, read at each call) lowers that
- * number, for tests of the unit-by-unit continuation; the result does not
- * depend on it beyond fp32 rounding of the distortions. */
+ * (all units at once) for up to 48 depths, or 12 where 64 B_total <= L G
+ * N_ctx (a compression of 64x or more), the rest unit by unit, in the pruned
+ * and the complete build alike; the environment variable GRACEKV_LEVELS
+ * (0 .. 48, read at each call) sets that number instead, for tests of the
+ * unit-by-unit continuation; the result does not depend on it beyond fp32
+ * rounding of the distortions. */
 gracekv_status gracekv_build_trees(const gracekv_config* cfg, const void* K, const void* V, const void* Q,
                                    const void* Q_graph, const float* rope_cos, const float* rope_sin,
                                    const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,

@@ -158,6 +158,7 @@ struct MhView {
 enum { BUILD_FULL = 0, BUILD_ROOT_SPLIT = 2, BUILD_CONTINUE = 3, BUILD_ROOT_FULL = 4, BUILD_LEVEL = 5,
        BUILD_LEVEL_FULL = 6 };
 constexpr int LEVELS_MAX = 48;   // depths refined level by level; deeper nodes go to the per-unit kernel
+constexpr int LEVELS_SPARSE = 12; // the same at a compression of 64x or more
 
 // ---- gains, utilities and keys (shared by the build and score kernels so that
 // both produce bit-identical keys) -------------------------------------------
@@ -447,7 +448,7 @@ int split_root_lds_bytes(int d);
 hipError_t launch_split_root(const Dims& dm, int mode, const void* K, const void* V, const void* Q, const float* cosT,
                              const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,
                              const TreeView& tv, int grid, hipStream_t st);
-// the levels below the roots (bf16): LEVELS_MAX rounds of the split kernel over
+// the levels below the roots (bf16): LEVELS_MAX (or LEVELS_SPARSE) rounds of the split kernel over
 // one depth's list and the level pass; full: the complete build
 hipError_t launch_levels(const Dims& dm, bool full, const void* K, const void* V, const void* Q, const float* cosT,
                          const float* sinT, const int32_t* slot_starts, const int32_t* n_slots, const float* kappa,

@@ -289,9 +289,16 @@ hipError_t launch_levels(const Dims& dm, bool full, const void* K, const void* V
   const dim3 lgrid((unsigned)grid);
   hipLaunchKernelGGL(k_level_reset, dim3(1), dim3(64), 0, st, tvp, (int)((int64_t)dm.L * dm.G * dm.J_cap));
   hipLaunchKernelGGL(k_level_first, lgrid, dim3(256), 0, st, dmp, tvp, full ? 1 : 0);
-  // depths refined here: LEVELS_MAX, or fewer where GRACEKV_LEVELS says so (a
-  // knob for tests of the per-unit kernel continuing below the last depth)
+  // depths refined here: LEVELS_MAX; LEVELS_SPARSE at a compression of 64x or
+  // more, where the budget-pruned build refines few nodes below that depth and
+  // the per-unit kernel ends their chains sooner than a pair of launches per
+  // depth would (with less compression the depths stay dense and the rounds
+  // are faster).  The complete build takes the same depth, so that both
+  // compute every node with the same kernel and round it alike.  Fewer where
+  // GRACEKV_LEVELS says so (a knob for tests of the per-unit kernel
+  // continuing below the last depth).
   int levels = LEVELS_MAX;
+  if (64 * dm.B_total <= (int64_t)dm.L * dm.G * dm.N_ctx) levels = LEVELS_SPARSE;
   if (const char* env = std::getenv("GRACEKV_LEVELS")) {
     const int v = std::atoi(env);
     levels = v < 0 ? 0 : (v < LEVELS_MAX ? v : LEVELS_MAX);
