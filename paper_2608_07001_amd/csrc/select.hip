@@ -369,34 +369,30 @@ __global__ __launch_bounds__(256) void k_sel_resid_find(Dims dm, TreeView tv, Se
   const int32_t* slot_starts = tv.slots;
   if (!((S->mode == SEL_SELECT || S->mode == SEL_RESID) && S->R == 1)) return;
   const int J = *n_slots;
-  const int64_t node_cap = (int64_t)dm.L * dm.G * 2 * dm.N_c;
-  const int64_t unit_cap = (int64_t)dm.L * dm.G * dm.J_cap;
   uint64_t best = 0;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < node_cap + unit_cap; i += (int64_t)gridDim.x * 256) {
-    if (i < node_cap) {
-      if (tv.sp_cost[i] != 1 || tv.sp_exec[i]) continue;
-      const int lg = (int)(i / (2 * dm.N_c));
-      const int o = (int)(i % (2 * dm.N_c));
-      // unit j with 2 a_j <= o < 2 a_{j+1}
-      int lo = 0, hi = J - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (2 * slot_starts[mid] <= o) lo = mid; else hi = mid - 1;
-      }
-      const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[lo];
-      const int loc = (int)(i - base);
-      const int par = tv.node_parent[i];
-      const bool pe = par < 0 ? tv.add_exec[(int64_t)lg * dm.J_cap + lo] : tv.sp_exec[base + par];
-      if (!pe) continue;
-      const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)lo;
-      const uint64_t k = make_key(tv.sp_U[i], ord * 256u + 1u + (uint32_t)loc);
-      best = k > best ? k : best;
-    } else {
-      const int64_t u = i - node_cap;
-      const int j = (int)(u % dm.J_cap);
-      if (j >= J || tv.add_exec[u]) continue;
-      const uint32_t ord = (uint32_t)(u / dm.J_cap) * (uint32_t)J + (uint32_t)j;
+  // unit by unit: its Add, then the Split slots of its live nodes (the slots
+  // of a unit's node range past its live nodes have cost 0); a Split counts
+  // if it costs 1, is not executed and its parent's Split (the unit's Add,
+  // for the root) is
+  const int64_t nu = (int64_t)dm.L * dm.G * J;
+  for (int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x; x < nu; x += (int64_t)gridDim.x * 256) {
+    const int lg = (int)(x / J), j = (int)(x - (int64_t)lg * J);
+    const int64_t u = (int64_t)lg * dm.J_cap + j;
+    const uint32_t ord = (uint32_t)lg * (uint32_t)J + (uint32_t)j;
+    const bool added = tv.add_exec[u] != 0;
+    if (!added) {
       const uint64_t k = make_key(tv.add_U[u], ord * 256u);
+      best = k > best ? k : best;
+      continue;                               // nothing of the unit's tree is open
+    }
+    const int64_t base = (int64_t)lg * 2 * dm.N_c + 2 * (int64_t)slot_starts[j];
+    const int nn = tv.unit_nn[u];
+    for (int loc = 0; loc < nn; ++loc) {
+      const int64_t i = base + loc;
+      if (tv.sp_cost[i] != 1 || tv.sp_exec[i]) continue;
+      const int par = tv.node_parent[i];
+      if (par >= 0 && !tv.sp_exec[base + par]) continue;
+      const uint64_t k = make_key(tv.sp_U[i], ord * 256u + 1u + (uint32_t)loc);
       best = k > best ? k : best;
     }
   }
