@@ -185,9 +185,19 @@ __device__ __forceinline__ void lse2_add8(float& m, float& z, const float* y) {
 // the maximum is taken on x (scaling by a positive number keeps the order, and
 // rounding is monotonic, so max(x) * sc2 is the largest y), and each term is
 // 2^(x * sc2 - max) with the product fused into the subtraction.
-__device__ __forceinline__ void lse2_add8_raw(float& m, float& z, const float* x, float sc2) {
-  const float mxr = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-  const float mn = fmaxf(m, mxr * sc2);
+// The maximum is taken as med3(a, b, +inf), which equals max(a, b) for any
+// a, b that are not NaN and, unlike fmaxf, needs no quieting of its operands;
+// pinf holds +inf in a register the optimiser cannot see through (an empty asm
+// statement, no instruction), so the median is not folded back into a maximum.
+__device__ __forceinline__ float opaque_inf() {
+  float v = INFINITY;
+  asm volatile("" : "+v"(v));
+  return v;
+}
+__device__ __forceinline__ void lse2_add8_raw(float& m, float& z, const float* x, float sc2, float pinf) {
+  auto mx = [pinf](float a, float b) { return __builtin_amdgcn_fmed3f(a, b, pinf); };
+  const float mxr = mx(mx(mx(x[0], x[1]), mx(x[2], x[3])), mx(mx(x[4], x[5]), mx(x[6], x[7])));
+  const float mn = mx(m, mxr * sc2);
   float e[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) e[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[r], sc2, -mn));
@@ -216,6 +226,7 @@ __global__ __launch_bounds__(256, 2) void k_rowstats_bf(Dims dm, const uint16_t*
   const uint16_t* Qp = Q + ((int64_t)l * dm.H + (int64_t)g * dm.hpg) * dm.W * D;
   const float scale = 1.0f / sqrtf((float)D);
   const float sc2 = scale * 1.44269504088896341f;
+  const float pinf = opaque_inf();
 
   // the wave's 4 row tiles: lane (row i16, group g4) holds dims QE g4 .. QE g4 + QE - 1
   uint4 qv[4][KS];
@@ -291,7 +302,7 @@ __global__ __launch_bounds__(256, 2) void k_rowstats_bf(Dims dm, const uint16_t*
           for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[k][h][r];
-          lse2_add8_raw(mC[k], zC[k], y, sc2);
+          lse2_add8_raw(mC[k], zC[k], y, sc2, pinf);
         }
       }
       continue;
@@ -323,7 +334,7 @@ __global__ __launch_bounds__(256, 2) void k_rowstats_bf(Dims dm, const uint16_t*
           for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int r = 0; r < 4; ++r) y[4 * h + r] = acc[h][r];
-          lse2_add8_raw(mC[k], zC[k], y, sc2);
+          lse2_add8_raw(mC[k], zC[k], y, sc2, pinf);
         } else {
           float xt[8];
 #pragma unroll
